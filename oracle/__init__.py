@@ -1,0 +1,155 @@
+"""ctypes wrapper of the CPU oracle (oracle/avo.c).
+
+TEST INFRASTRUCTURE, NOT PART OF THE PRODUCT: only the test-suite, the smoke check and
+the benchmark's CPU-baseline leg import this package.  It never loads the GPU library.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "avo.c")
+LIB = os.path.join(HERE, "libavo.so")
+
+AVO_OK, AVO_EINVAL, AVO_ENOMEM, AVO_ESTATE = 0, 1, 2, 4
+
+
+def build(out: str = LIB, src: str = SRC, extra=()) -> str:
+    """Compile the oracle with gcc (-O2, OpenMP); returns the library path."""
+    cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-Wall", "-Wextra", "-shared", "-fPIC",
+           *extra, src, "-o", out]
+    subprocess.run(cmd, check=True, cwd=HERE)
+    return out
+
+
+_libs = {}
+
+
+def load(path: str = LIB) -> ctypes.CDLL:
+    if path in _libs:
+        return _libs[path]
+    if not os.path.exists(path):
+        if path != LIB:
+            raise FileNotFoundError(path)
+        build()
+    lib = ctypes.CDLL(path)
+    P, I = ctypes.c_void_p, ctypes.c_int
+    lib.avo_create.argtypes = [I, I, I, I, I, I, I, I, I, ctypes.POINTER(P)]
+    lib.avo_load_rules.argtypes = [P, I, P, P, P, P]
+    lib.avo_reset.argtypes = [P, P]
+    lib.avo_step.argtypes = [P, P, P, P, I, ctypes.POINTER(I)]
+    lib.avo_get_maps.argtypes = [P, P]
+    lib.avo_get_counters.argtypes = [P, P]
+    lib.avo_destroy.argtypes = [P]
+    lib.avo_destroy.restype = None
+    for f in ("avo_create", "avo_load_rules", "avo_reset", "avo_step", "avo_get_maps",
+              "avo_get_counters"):
+        getattr(lib, f).restype = I
+    _libs[path] = lib
+    return lib
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+class OracleError(RuntimeError):
+    def __init__(self, fn, code):
+        super().__init__(f"{fn} returned {code}")
+        self.code = code
+
+
+class Oracle:
+    """One batch of environments stepped on the CPU by the oracle."""
+
+    def __init__(self, B, H, W, C, max_rules, max_h, max_w, per_env=False, episode_len=0,
+                 lib_path: str = LIB):
+        self.lib = load(lib_path)
+        self.B, self.H, self.W, self.C = B, H, W, C
+        self.max_h, self.max_w, self.per_env = max_h, max_w, bool(per_env)
+        h = ctypes.c_void_p()
+        rc = self.lib.avo_create(B, H, W, C, max_rules, max_h, max_w, int(bool(per_env)),
+                                 episode_len, ctypes.byref(h))
+        if rc != AVO_OK:
+            raise OracleError("avo_create", rc)
+        self.h = h
+        self._keep = []
+
+    @classmethod
+    def for_workload(cls, wl, B=None, lib_path: str = LIB):
+        return cls(wl.B if B is None else B, wl.H, wl.W, wl.C, wl.R, wl.max_h, wl.max_w,
+                   wl.per_env, wl.L, lib_path=lib_path)
+
+    def close(self):
+        if getattr(self, "h", None):
+            self.lib.avo_destroy(self.h)
+            self.h = None
+
+    __del__ = close
+
+    def load_rules(self, shape, in_pat, out_pat, reward):
+        shape = np.ascontiguousarray(shape, dtype=np.int32)
+        in_pat = np.ascontiguousarray(in_pat, dtype=np.int8)
+        out_pat = np.ascontiguousarray(out_pat, dtype=np.int8)
+        reward = np.ascontiguousarray(reward, dtype=np.int32)
+        R = shape.shape[1] if shape.ndim == 3 else 0
+        rc = self.lib.avo_load_rules(self.h, R, _ptr(shape), _ptr(in_pat), _ptr(out_pat),
+                                     _ptr(reward))
+        if rc != AVO_OK:
+            raise OracleError("avo_load_rules", rc)
+
+    def reset(self, init_maps):
+        m = np.ascontiguousarray(init_maps, dtype=np.uint8)
+        assert m.shape == (self.B, self.C, self.H, self.W), m.shape
+        rc = self.lib.avo_reset(self.h, _ptr(m))
+        if rc != AVO_OK:
+            raise OracleError("avo_reset", rc)
+
+    def step(self, actions, nthreads: int = 1):
+        a = np.ascontiguousarray(actions, dtype=np.uint8)
+        assert a.shape == (self.B,), a.shape
+        rewards = np.zeros(self.B, dtype=np.float32)
+        done = np.zeros(self.B, dtype=np.uint8)
+        used = ctypes.c_int(0)
+        rc = self.lib.avo_step(self.h, _ptr(a), _ptr(rewards), _ptr(done), nthreads,
+                               ctypes.byref(used))
+        if rc != AVO_OK:
+            raise OracleError("avo_step", rc)
+        self.threads_used = used.value
+        return rewards, done
+
+    def maps(self):
+        out = np.zeros((self.B, self.C, self.H, self.W), dtype=np.uint8)
+        rc = self.lib.avo_get_maps(self.h, _ptr(out))
+        if rc != AVO_OK:
+            raise OracleError("avo_get_maps", rc)
+        return out
+
+    def counters(self):
+        out = np.zeros(self.B, dtype=np.int32)
+        rc = self.lib.avo_get_counters(self.h, _ptr(out))
+        if rc != AVO_OK:
+            raise OracleError("avo_get_counters", rc)
+        return out
+
+
+def run(wl, maps, rules, actions, nthreads: int = 1, B=None, lib_path: str = LIB):
+    """Step a workload's arrays for len(actions) steps; returns the per-step trajectory
+    (maps [T][B][C][H][W], rewards [T][B], done [T][B])."""
+    B = maps.shape[0] if B is None else B
+    o = Oracle.for_workload(wl, B=B, lib_path=lib_path)
+    o.load_rules(*rules)
+    o.reset(maps)
+    T = actions.shape[0]
+    out_maps = np.zeros((T,) + maps.shape, dtype=np.uint8)
+    out_r = np.zeros((T, B), dtype=np.float32)
+    out_d = np.zeros((T, B), dtype=np.uint8)
+    for t in range(T):
+        out_r[t], out_d[t] = o.step(actions[t], nthreads)
+        out_maps[t] = o.maps()
+    o.close()
+    return out_maps, out_r, out_d

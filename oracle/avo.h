@@ -1,0 +1,56 @@
+/* avo.h — CPU oracle for the Autoverse batched rule step (arXiv 2407.04221).
+ *
+ * TEST INFRASTRUCTURE, NOT PART OF THE PRODUCT.  Only the test-suite, the smoke check and
+ * the benchmark's CPU-baseline leg call this code.  It shares no source with the GPU
+ * library; both are fed the same seeded arrays.
+ *
+ * The oracle is the plain definition of one environment step written out with int8 loops
+ * over maps, rules, anchors and pattern entries (paper Sec. 2.1, the patch-replacement
+ * equation generalised to many matches by the convolution / transposed-convolution pair,
+ * Sec. 2.1.1 for parallel rule application, Sec. 2.2.1 for force-tile moves, rewards and
+ * kill rules).  All arrays are host memory.
+ *
+ * Layouts (all C-contiguous):
+ *   maps, init_maps  uint8 [B][C][H][W], values 0/1
+ *   shape            int32 [S][R][2]  (rows n, cols m) of each rule
+ *   in_pat, out_pat  int8  [S][R][C+1][max_h][max_w]; 1, 0, or -1 = don't care.
+ *                    Channel C is the force plane.  Entries outside n x m are ignored.
+ *   reward           int32 [S][R]
+ *   actions          uint8 [B]  0 none, 1 up, 2 right, 3 down, 4 left; >= 5 acts as 0
+ *   rewards          float [B], done uint8 [B]
+ *   S = B when per_env is set, else 1.
+ */
+#ifndef AVO_H
+#define AVO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { AVO_OK = 0, AVO_EINVAL = 1, AVO_ENOMEM = 2, AVO_ESTATE = 4 };
+
+/* Largest |sum of rewards| one step may produce, so that the float output is exact. */
+#define AVO_REWARD_LIMIT (1 << 24)
+
+typedef struct avo_batch avo_batch;
+
+int  avo_create(int B, int H, int W, int C, int max_rules, int max_h, int max_w,
+                int per_env, int episode_len, avo_batch **out);
+int  avo_load_rules(avo_batch *ab, int R, const int32_t *shape, const int8_t *in_pat,
+                    const int8_t *out_pat, const int32_t *reward);
+int  avo_reset(avo_batch *ab, const uint8_t *init_maps);
+/* One step of every environment.  nthreads > 1 splits the environments over OpenMP
+ * threads (they are independent); returns the thread count used through *used. */
+int  avo_step(avo_batch *ab, const uint8_t *actions, float *rewards, uint8_t *done,
+              int nthreads, int *used);
+int  avo_get_maps(const avo_batch *ab, uint8_t *dst);
+int  avo_get_counters(const avo_batch *ab, int32_t *dst);
+void avo_destroy(avo_batch *ab);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,124 @@
+"""The step written as the paper's convolution pair (Sec. 2.1), with torch CPU library
+convolutions in float64.  Used only as an independent pin of the oracle: the oracle
+loops over anchors and entries; this module never does.
+
+    B_t     = ReLU(conv_{K_I}(D_t) - I + 1)          (match activation)
+    D_{t+1} = conv^T_{K_O}(B_t) + D_t                 (write), then clamped to {0, 1}
+
+K_I holds +1 for a must-be-1 entry, -1 for must-be-0 and 0 for don't care; I is the
+number of +1 entries.  K_O = O - I, with don't-cares resolved so that an unspecified
+output leaves the cell alone and an unspecified input points the vote at the output.
+No padding: patterns lie wholly on the map.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+import torch.nn.functional as Fn
+
+PLAYER, WALL = 2, 1
+
+
+def move_rules(C: int):
+    """Built-in moves as (n, m, I, O, reward); force plane is channel C.
+    Moving right: player at (0,0), force on a wall-free cell at (0,1)."""
+    out = []
+    # (n, m, source cell, target cell)
+    for n, m, src, tgt in ((1, 2, (0, 0), (0, 1)), (1, 2, (0, 1), (0, 0)),
+                           (2, 1, (0, 0), (1, 0)), (2, 1, (1, 0), (0, 0))):
+        I = np.full((C + 1, n, m), -1, np.int8)
+        O = np.full((C + 1, n, m), -1, np.int8)
+        I[(PLAYER,) + src] = 1
+        O[(PLAYER,) + src] = 0
+        I[(C,) + tgt] = 1
+        I[(WALL,) + tgt] = 0
+        O[(PLAYER,) + tgt] = 1
+        O[(C,) + tgt] = 0
+        out.append((n, m, I, O, 0))
+    return out
+
+
+def kernels(I: np.ndarray, O: np.ndarray):
+    I = I.astype(np.int64)
+    O = O.astype(np.int64)
+    k_in = np.where(I == 1, 1.0, np.where(I == 0, -1.0, 0.0))
+    thr = float((I == 1).sum())
+    i_eff = np.where(I == -1, 1 - O, I)         # unspecified input: opposite of the output
+    o_eff = np.where(O == -1, i_eff, O)         # unspecified output: equal to the input
+    k_out = (o_eff - i_eff).astype(np.float64)
+    return (torch.from_numpy(k_in)[None].double(), thr,
+            torch.from_numpy(k_out)[None].double())
+
+
+def force_plane(P: torch.Tensor, actions: np.ndarray) -> torch.Tensor:
+    """P: [B][H][W]; force on the on-map neighbour of every player cell in the action's
+    direction (1 up, 2 right, 3 down, 4 left)."""
+    F = torch.zeros_like(P)
+    a = torch.from_numpy(np.asarray(actions, dtype=np.int64))
+    up, right, down, left = (a == 1), (a == 2), (a == 3), (a == 4)
+    F[up, :-1, :] = P[up, 1:, :]
+    F[down, 1:, :] = P[down, :-1, :]
+    F[right, :, 1:] = P[right, :, :-1]
+    F[left, :, :-1] = P[left, :, 1:]
+    return F
+
+
+def step(maps: np.ndarray, rules, actions: np.ndarray):
+    """One step with one rule list shared by all envs; no episode logic.
+    maps uint8 [B][C][H][W]; rules: list of (n, m, I [C+1][n][m], O, reward).
+    Returns (maps after, before any reset) uint8, rewards float64 [B]."""
+    B, C, H, W = maps.shape
+    X = torch.zeros((B, C + 1, H, W), dtype=torch.float64)
+    X[:, :C] = torch.from_numpy(maps.astype(np.float64))
+    X[:, C] = force_plane(X[:, PLAYER], actions)
+    delta = torch.zeros_like(X)
+    rho = torch.zeros(B, dtype=torch.float64)
+    for n, m, I, O, rew in move_rules(C) + list(rules):
+        if n > H or m > W:      # no anchor where the pattern lies on the map
+            continue
+        k_in, thr, k_out = kernels(I[:, :n, :m], O[:, :n, :m])
+        act = torch.relu(Fn.conv2d(X, k_in) - thr + 1.0)          # [B][1][H-n+1][W-m+1]
+        rho += rew * act.sum(dim=(1, 2, 3))
+        delta += Fn.conv_transpose2d(act, k_out)                  # [B][C+1][H][W]
+    Xn = (X + delta >= 1.0)
+    return Xn[:, :C].numpy().astype(np.uint8), rho.numpy()
+
+
+def rules_from_abi(shape, in_pat, out_pat, reward, s: int = 0):
+    out = []
+    for r in range(shape.shape[1]):
+        n, m = int(shape[s, r, 0]), int(shape[s, r, 1])
+        out.append((n, m, in_pat[s, r, :, :n, :m], out_pat[s, r, :, :n, :m],
+                    int(reward[s, r])))
+    return out
+
+
+def run(maps, rules_abi, actions, L: int = 0, per_env: bool = False):
+    """Episode-level stepping on top of `step`: done when no player is left or the counter
+    reaches L; done envs return to their initial maps.  Returns per-step maps, rewards,
+    done like oracle.run."""
+    shape, in_pat, out_pat, reward = rules_abi
+    B = maps.shape[0]
+    cur = maps.copy()
+    t = np.zeros(B, np.int64)
+    T = actions.shape[0]
+    out_m = np.zeros((T,) + maps.shape, np.uint8)
+    out_r = np.zeros((T, B), np.float32)
+    out_d = np.zeros((T, B), np.uint8)
+    for k in range(T):
+        if per_env:
+            nxt = np.zeros_like(cur)
+            rho = np.zeros(B)
+            for b in range(B):
+                nb, rb = step(cur[b:b + 1], rules_from_abi(shape, in_pat, out_pat, reward, b),
+                              actions[k, b:b + 1])
+                nxt[b], rho[b] = nb[0], rb[0]
+        else:
+            nxt, rho = step(cur, rules_from_abi(shape, in_pat, out_pat, reward), actions[k])
+        t += 1
+        done = (nxt[:, PLAYER].reshape(B, -1).sum(1) == 0) | ((L > 0) & (t == L))
+        nxt[done] = maps[done]
+        t[done] = 0
+        cur = nxt
+        out_m[k], out_r[k], out_d[k] = cur, rho.astype(np.float32), done
+    return out_m, out_r, out_d
