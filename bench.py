@@ -1,0 +1,214 @@
+"""Benchmark of the batched rule step on one MI355X.
+
+Default workload: 16384 environments, 16x16 maps, 6 channels, 8 shared 3x3 rules (30 %
+don't-care entries), random actions, episodes of 100 steps, 5000 steps: the throughput
+workload.  Prints one JSON line with env-steps/s (whole batch), cell-rule-updates/s, the
+fraction of the HBM roofline for the step kernel, and the CPU oracle's rate on a bounded
+sample of the same workload on this host.
+
+Roofline: algorithmic bytes per env-step A = 2*C*H*W/8 (packed maps in and out) + 6
+(action u8, reward f32, done u8); a launch of k steps over B envs moves k*B*A algorithmic
+bytes; achieved = that / the launch's average duration (HIP events on the launch stream);
+peak = 8 TB/s.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "env-steps/sec and cell-rule-updates/sec at 1 MI355X; % of HBM roofline"
+KERNEL_SOURCES = ("paper_2407_04221_amd/csrc/k_generic.hip", "paper_2407_04221_amd/csrc/lane16.h",
+                  "paper_2407_04221_amd/csrc/k_lane16.hip")
+
+
+def kernel_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        p = os.path.join(ROOT, rel)
+        if os.path.exists(p):
+            h.update(open(p, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes(wl) -> int:
+    return 2 * wl.C * wl.H * wl.W // 8 + 6
+
+
+def measured_traffic(workload: str, engine: int):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it was taken
+    on the current kernel sources; otherwise None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path)).get(f"{workload}/{engine}")
+    except Exception:
+        return None
+    if not rec or rec.get("kernel_hash") != kernel_hash():
+        return None
+    return rec
+
+
+def cpu_baseline(wl, maps, rules, actions, budget_s: float, threads: int):
+    import oracle
+    from paper_2407_04221_amd import inputs
+    nb = min(wl.B, 1024)
+    envs = np.arange(nb)
+    m, r, a = inputs.subset_envs(wl, maps, rules, actions, envs)
+    o = oracle.Oracle.for_workload(wl, B=nb)
+    o.load_rules(*r)
+    o.reset(m)
+    steps = 0
+    t0 = time.perf_counter()
+    while steps < a.shape[0] and time.perf_counter() - t0 < budget_s:
+        o.step(a[steps], nthreads=threads)
+        steps += 1
+    dt = time.perf_counter() - t0
+    used = o.threads_used
+    o.close()
+    return {"value": nb * steps / dt, "unit": "env-steps/s", "cores": used, "kind": "oracle",
+            "sample": f"first {nb} of {wl.B} envs x {steps} steps ({dt:.1f} s, {used} threads)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default: workload T)")
+    ap.add_argument("--warmup", type=int, default=200)
+    ap.add_argument("--workload", default="c4")
+    ap.add_argument("--variant", default="literal", choices=["literal", "planted", "dense"])
+    ap.add_argument("--engine", default="auto", choices=["auto", "generic", "lane16"])
+    ap.add_argument("--chunk", type=int, default=1000, help="steps per av_step_n launch")
+    ap.add_argument("--launch-steps", type=int, default=500,
+                    help="steps timed one launch per step (av_step); 0 = skip")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--seed", type=int, default=0)
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU: this build has no multi-GPU path (asked for "
+              f"--gpus {args.gpus}); environments are independent, so N GPUs would each run "
+              f"this same kernel on B/N environments.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2407_04221_amd as av
+    from paper_2407_04221_amd import inputs
+
+    wl = inputs.WORKLOADS[args.workload]
+    T = wl.T if args.steps is None else args.steps
+    torch.cuda.set_device(0)
+    maps, rules, actions = inputs.make_all(wl, args.seed, args.variant, T=max(T, args.warmup, 1))
+    acts = torch.from_numpy(actions).cuda()
+    b = av.Batch.for_workload(wl, engine=args.engine)
+    b.load_rules(*rules)
+    b.reset(maps)
+    engine = b.info["engine"]
+    engine_name = {1: "generic", 2: "lane16"}[engine]
+    chunk = max(1, min(args.chunk, T))
+    rew = torch.empty((chunk, wl.B), dtype=torch.float32, device="cuda")
+    don = torch.empty((chunk, wl.B), dtype=torch.uint8, device="cuda")
+
+    def run(n_steps, base=0):
+        launches = 0
+        t = 0
+        while t < n_steps:
+            k = min(chunk, n_steps - t)
+            lo = (base + t) % actions.shape[0]
+            k = min(k, actions.shape[0] - lo)
+            av.av_step_n(b.h, k, acts[lo:lo + k], rew[:k], don[:k])
+            t += k
+            launches += 1
+        return launches
+
+    if args.warmup:
+        run(args.warmup)
+    b.reset(maps)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    launches = run(T)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+
+    env_steps = wl.B * T
+    value = env_steps / (ms / 1e3)
+    A = algorithmic_bytes(wl)
+    launch_ms = ms / launches
+    achieved = A * wl.B * (T / launches) / (launch_ms / 1e3) / 1e9
+    roof_env_steps = HBM_PEAK_GBS * 1e9 / A
+
+    per_launch = None
+    if args.launch_steps:
+        n = args.launch_steps
+        b.reset(maps)
+        torch.cuda.synchronize()
+        f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        f0.record(stream)
+        for t in range(n):
+            av.av_step(b.h, acts[t % actions.shape[0]], b.rewards, b.done)
+        f1.record(stream)
+        torch.cuda.synchronize()
+        ms1 = f0.elapsed_time(f1)
+        per_launch = {"api": "av_step", "steps": n, "ms_per_step": ms1 / n,
+                      "env_steps_per_sec": wl.B * n / (ms1 / 1e3),
+                      "frac_hbm_roofline": wl.B * n / (ms1 / 1e3) / roof_env_steps}
+
+    cpu = None
+    if not args.no_cpu:
+        cpu = cpu_baseline(wl, maps, rules, actions, args.cpu_seconds,
+                           threads=min(16, os.cpu_count() or 1))
+
+    traffic = measured_traffic(args.workload, engine)
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "env-steps/s",
+        "n_gpus": 1,
+        "steps": T,
+        "warmup": args.warmup,
+        "ms_per_step": ms / T,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{wl.name}: {wl.B} envs, {wl.H}x{wl.W} maps, C={wl.C}, R={wl.R} "
+                        f"{'per-env' if wl.per_env else 'shared'} rules "
+                        f"{'/'.join(f'{n}x{m}' for n, m in wl.shapes)}, p_dc={wl.p_dc:.2f}, "
+                        f"{args.variant}, episode {wl.L} steps",
+            "B": wl.B, "H": wl.H, "W": wl.W, "C": wl.C, "R": wl.R, "variant": args.variant,
+            "engine": engine_name, "api": "av_step_n", "steps_per_launch": chunk,
+        },
+        "cell_rule_updates_per_sec": value * wl.H * wl.W * wl.R,
+        "pct_hbm_roofline": 100.0 * value / roof_env_steps,
+        "roofline": {
+            "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": None if traffic is None else traffic["bytes_per_launch"],
+            "kernel": f"{engine_name}_step", "launch_ms": launch_ms,
+            "algorithmic_bytes_per_env_step": A,
+        },
+        "per_launch_path": per_launch,
+        "cpu_baseline": cpu,
+    }
+    b.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

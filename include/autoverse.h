@@ -1,0 +1,156 @@
+/* autoverse.h — C ABI of libautoverse.so: the batched environment step of Autoverse
+ * (Earle & Togelius, "Autoverse: an Evolvable Game Language for Learning Robust Embodied
+ * Agents", arXiv 2407.04221) on one AMD Instinct MI355X (gfx950).
+ *
+ * What one step computes, for every environment independently (paper Sec. 2.1, Sec. 2.1.1,
+ * Sec. 2.2.1):
+ *   - the map is C binary channels ("tiles"), multi-hot per cell; channel 0 empty, 1 wall,
+ *     2 player, 3 goal/food, 4.. extra tile types;
+ *   - the action (0 none, 1 up, 2 right, 3 down, 4 left; larger values act as 0) places a
+ *     transient force tile on the on-map neighbour of every player cell in that direction;
+ *     the force plane is channel C while the step runs and is never stored;
+ *   - four built-in move rules (player next to force on a wall-free cell moves there and
+ *     consumes the force) and the loaded rules are matched, all against the same map
+ *     (rules apply in parallel, Sec. 2.1.1), at every anchor where the pattern lies wholly
+ *     on the map; a match needs every specified input entry to hold (the thresholded
+ *     convolution of Sec. 2.1);
+ *   - the reward is the sum over rules of the rule's reward times its number of matches;
+ *   - every match votes K_O = O - I onto its patch (the transposed convolution of
+ *     Sec. 2.1; an unspecified output entry votes nothing, an unspecified input entry
+ *     votes toward the output); a cell-channel becomes 1 iff old value + votes >= 1;
+ *   - the episode is done when no player tile is left (a kill rule, Sec. 2.2.1) or the step
+ *     counter reaches max_episode_steps; a done environment is reset to its initial map
+ *     within the same step, and that step's reward and done flag are still reported.
+ *
+ * Status codes only: no exception crosses this boundary.  Errors in arguments are found on
+ * the host before any launch; device failures return AV_EDEVICE.  av_last_error() gives a
+ * thread-local message for the last failing call on the calling thread.
+ *
+ * Memory: the library allocates and owns all persistent device state (packed maps,
+ * initial maps, step counters, compiled rules).  The caller owns actions, rewards, done
+ * and dst buffers: device pointers on the batch's device (for example torch tensors'
+ * data_ptr()).  Host pointers appear only in av_load_rules, av_get_state, av_set_state.
+ *
+ * Ordering: all device work is issued on the batch's stream.  av_step and av_step_n never
+ * synchronise; av_load_rules, av_reset, av_get_state, av_set_state and av_destroy_batch
+ * may.  Calls on one batch must not overlap (one batch is not thread-safe); different
+ * batches are independent.
+ */
+#ifndef AUTOVERSE_H
+#define AUTOVERSE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct av_batch_s *av_batch_t;
+
+typedef enum {
+    AV_OK = 0,
+    AV_EINVAL = 1,   /* bad argument: NULL pointer, size out of range, bad pattern value */
+    AV_ENOMEM = 2,   /* host or device allocation failed */
+    AV_EDEVICE = 3,  /* a HIP call failed; av_last_error() names it */
+    AV_ESTATE = 4    /* call out of order, e.g. av_step before av_load_rules and av_reset */
+} av_status;
+
+/* Kernel family used by av_step / av_step_n.  AUTO picks the fastest eligible one. */
+typedef enum {
+    AV_ENGINE_AUTO = 0,
+    AV_ENGINE_GENERIC = 1,  /* any size within the limits below; maps staged in LDS */
+    AV_ENGINE_LANE16 = 2    /* maps of at most 16 x 16: one map row per lane, two maps per
+                               32-bit lane word, rows shifted across lanes with DPP */
+} av_engine;
+
+typedef struct {
+    int32_t num_envs;           /* B >= 1 */
+    int32_t height, width;      /* H, W in [1, 64] */
+    int32_t channels;           /* C in [4, 31]; patterns span C + 1 channels */
+    int32_t max_rules;          /* most rules one av_load_rules may load, in [0, 252] */
+    int32_t max_pat_h, max_pat_w; /* pattern array extent, each in [1, 16] */
+    int32_t per_env_rules;      /* 0: one rule set shared by all B; 1: one set per env */
+    int32_t max_episode_steps;  /* L >= 0; 0 = episodes end only when the player is gone */
+    int32_t device;             /* HIP device ordinal */
+    int32_t engine;             /* av_engine */
+    void *stream;               /* hipStream_t for all device work; NULL = null stream */
+} av_config;
+
+/* Read-only facts about a batch, for callers that use the packed state directly. */
+typedef struct {
+    int32_t num_envs, height, width, channels;
+    int32_t row_bytes;          /* bytes per packed map row: 2 (W <= 16), 4 (W <= 32), 8 */
+    int32_t engine;             /* av_engine chosen for av_step / av_step_n */
+    size_t state_bytes;         /* size of the packed state behind av_state_ptr */
+    size_t blob_bytes;          /* size av_get_state needs */
+} av_info;
+
+/* Create a batch on cfg->device.  Maps start empty; av_load_rules and av_reset must both
+ * be called before the first step.  Fails with AV_EINVAL for sizes outside the limits in
+ * av_config, or when one environment's working set (its C + 1 planes and one match plane
+ * per rule, 64-bit rows for W > 32) exceeds 64 KiB of LDS. */
+av_status av_create_batch(const av_config *cfg, av_batch_t *out);
+
+/* Load the rules (paper Sec. 2.1: a rule is an n x m input pattern I, an n x m output
+ * pattern O, and a reward paid per application, Sec. 2.2.1).  All pointers are host memory
+ * and are copied; S = B if per_env_rules else 1; R = num_rules in [0, max_rules].
+ *   shape   int32 [S][R][2]: (n rows, m cols), 1 <= n <= min(H, max_pat_h), likewise m
+ *   in_pat  int8  [S][R][C+1][max_pat_h][max_pat_w]: 1 must be 1, 0 must be 0, -1 don't care
+ *   out_pat int8  same layout: 1 becomes 1, 0 becomes 0, -1 left alone
+ *   reward  int32 [S][R]
+ * Entries outside a rule's n x m are ignored but must still be in {-1, 0, 1}.  Channel C
+ * of a pattern is the force plane.  AV_EINVAL if any set could produce a step reward of
+ * magnitude >= 2^24 (sum over rules of |reward| x anchors), which keeps the float reward
+ * exact.  Synchronises the stream; replaces any earlier rules for later steps. */
+av_status av_load_rules(av_batch_t b, int32_t num_rules, const int32_t *shape,
+                        const int8_t *in_pat, const int8_t *out_pat, const int32_t *reward);
+
+/* Set every environment's initial map and current map to init_maps (device, uint8
+ * [B][C][H][W], nonzero = tile present) and its step counter to 0.  Environments that end
+ * an episode return to these maps.  May synchronise. */
+av_status av_reset(av_batch_t b, const uint8_t *init_maps);
+
+/* One step of all B environments.  actions: device uint8 [B]; rewards: device float
+ * [B] (exact small integers); done: device uint8 [B] (0/1).  Asynchronous. */
+av_status av_step(av_batch_t b, const uint8_t *actions, float *rewards, uint8_t *done);
+
+/* k consecutive steps in one launch, identical in result to k calls of av_step.
+ * actions uint8 [k][B], rewards float [k][B], done uint8 [k][B], all device; k >= 1.
+ * Maps stay on chip between the k steps.  Asynchronous. */
+av_status av_step_n(av_batch_t b, int32_t k, const uint8_t *actions, float *rewards,
+                    uint8_t *done);
+
+/* Current maps as device uint8 [B][C][H][W] (0/1) written to dst.  Asynchronous. */
+av_status av_get_maps(av_batch_t b, uint8_t *dst);
+
+/* Device pointer to the packed current maps, owned by the batch and valid until the
+ * next av_reset / av_set_state / av_destroy_batch.  Layout: rows of row_bytes bytes,
+ * index [c][env][y] (channel-major over the whole batch); cell (env, c, y, x) is bit x
+ * (least significant first) of that row.  NULL on error. */
+const void *av_state_ptr(av_batch_t b);
+
+av_status av_get_info(av_batch_t b, av_info *info);
+
+/* Checkpoint and resume.  av_get_state copies the packed current maps, initial maps and
+ * step counters into host_blob; *bytes holds its capacity on entry and the size written
+ * on return (call with host_blob = NULL to query).  av_set_state restores them; stepping
+ * on from a restored blob is bit-identical to stepping on from where it was taken.  The
+ * blob records B, H, W, C and is refused (AV_EINVAL) by a batch of another shape.
+ * Both synchronise. */
+av_status av_get_state(av_batch_t b, void *host_blob, size_t *bytes);
+av_status av_set_state(av_batch_t b, const void *host_blob, size_t bytes);
+
+/* Change the stream later calls use (hipStream_t; NULL = null stream). */
+av_status av_set_stream(av_batch_t b, void *stream);
+
+/* Free all device and host state of the batch; synchronises its stream.  NULL is a no-op. */
+av_status av_destroy_batch(av_batch_t b);
+
+/* Message for the last failing call on this thread; "" if none.  Never NULL. */
+const char *av_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* AUTOVERSE_H */

@@ -1,0 +1,301 @@
+"""MI355X-native batched Autoverse environment step (arXiv 2407.04221, Sec. 2.1).
+
+Python binding of libautoverse.so (C ABI: include/autoverse.h).  The functions below carry
+the C names and only marshal arguments: host numpy arrays for rules and checkpoints, torch
+device tensors (device memory and streams) for maps, actions, rewards and done flags.
+Every step runs in the library's HIP kernels; there is no CPU path.
+
+`Batch` bundles one batch handle with its own output tensors for convenience.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libautoverse.so")
+
+AV_OK, AV_EINVAL, AV_ENOMEM, AV_EDEVICE, AV_ESTATE = 0, 1, 2, 3, 4
+AV_ENGINE_AUTO, AV_ENGINE_GENERIC, AV_ENGINE_LANE16 = 0, 1, 2
+ENGINES = {"auto": AV_ENGINE_AUTO, "generic": AV_ENGINE_GENERIC, "lane16": AV_ENGINE_LANE16}
+
+# Every symbol include/autoverse.h declares.
+ABI_SYMBOLS = ("av_create_batch", "av_load_rules", "av_reset", "av_step", "av_step_n",
+               "av_get_maps", "av_state_ptr", "av_get_info", "av_get_state", "av_set_state",
+               "av_set_stream", "av_destroy_batch", "av_last_error")
+
+
+class av_config(ctypes.Structure):
+    _fields_ = [("num_envs", ctypes.c_int32), ("height", ctypes.c_int32),
+                ("width", ctypes.c_int32), ("channels", ctypes.c_int32),
+                ("max_rules", ctypes.c_int32), ("max_pat_h", ctypes.c_int32),
+                ("max_pat_w", ctypes.c_int32), ("per_env_rules", ctypes.c_int32),
+                ("max_episode_steps", ctypes.c_int32), ("device", ctypes.c_int32),
+                ("engine", ctypes.c_int32), ("stream", ctypes.c_void_p)]
+
+
+class av_info(ctypes.Structure):
+    _fields_ = [("num_envs", ctypes.c_int32), ("height", ctypes.c_int32),
+                ("width", ctypes.c_int32), ("channels", ctypes.c_int32),
+                ("row_bytes", ctypes.c_int32), ("engine", ctypes.c_int32),
+                ("state_bytes", ctypes.c_size_t), ("blob_bytes", ctypes.c_size_t)]
+
+
+class AvError(RuntimeError):
+    def __init__(self, fn: str, status: int, message: str):
+        super().__init__(f"{fn}: status {status}: {message}")
+        self.status = status
+        self.message = message
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libautoverse.so; raise if it has not been built (there is no fallback)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with __graft_entry__.build() or "
+                           f"python paper_2407_04221_amd/build.py")
+    lib = ctypes.CDLL(path)
+    P, I32, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    sig = {
+        "av_create_batch": ([ctypes.POINTER(av_config), ctypes.POINTER(P)], ctypes.c_int),
+        "av_load_rules": ([P, I32, P, P, P, P], ctypes.c_int),
+        "av_reset": ([P, P], ctypes.c_int),
+        "av_step": ([P, P, P, P], ctypes.c_int),
+        "av_step_n": ([P, I32, P, P, P], ctypes.c_int),
+        "av_get_maps": ([P, P], ctypes.c_int),
+        "av_state_ptr": ([P], P),
+        "av_get_info": ([P, ctypes.POINTER(av_info)], ctypes.c_int),
+        "av_get_state": ([P, P, ctypes.POINTER(SZ)], ctypes.c_int),
+        "av_set_state": ([P, P, SZ], ctypes.c_int),
+        "av_set_stream": ([P, P], ctypes.c_int),
+        "av_destroy_batch": ([P], ctypes.c_int),
+        "av_last_error": ([], ctypes.c_char_p),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = res
+    _lib = lib
+    return lib
+
+
+def av_last_error() -> str:
+    return load_library().av_last_error().decode()
+
+
+def _check(fn: str, rc: int):
+    if rc != AV_OK:
+        raise AvError(fn, rc, av_last_error())
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dev_ptr(t, dtype, shape, name):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a device tensor")
+    if t.dtype != dtype or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous {dtype} tensor of shape {tuple(shape)}, "
+                         f"got {t.dtype} {tuple(t.shape)}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _host(a, dtype, name):
+    a = np.ascontiguousarray(a, dtype=dtype)
+    return a, a.ctypes.data_as(ctypes.c_void_p)
+
+
+def current_stream_handle():
+    torch = _torch()
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def av_create_batch(num_envs, height, width, channels, max_rules, max_pat_h, max_pat_w,
+                    per_env_rules=False, max_episode_steps=0, device=None, engine="auto",
+                    stream=None):
+    """Returns an opaque handle (ctypes.c_void_p).  stream: a torch.cuda.Stream, a raw
+    handle, or None for torch's current stream on `device`."""
+    torch = _torch()
+    if device is None:
+        device = torch.cuda.current_device()
+    if stream is None:
+        with torch.cuda.device(device):
+            stream = current_stream_handle()
+    elif hasattr(stream, "cuda_stream"):
+        stream = ctypes.c_void_p(stream.cuda_stream)
+    cfg = av_config(num_envs, height, width, channels, max_rules, max_pat_h, max_pat_w,
+                    int(bool(per_env_rules)), max_episode_steps, int(device),
+                    ENGINES[engine] if isinstance(engine, str) else int(engine), stream)
+    h = ctypes.c_void_p()
+    _check("av_create_batch", load_library().av_create_batch(ctypes.byref(cfg), ctypes.byref(h)))
+    return h
+
+
+def av_load_rules(batch, shape, in_pat, out_pat, reward):
+    """Host arrays: shape int32 [S][R][2], in_pat / out_pat int8 [S][R][C+1][mh][mw],
+    reward int32 [S][R]."""
+    shape, ps = _host(shape, np.int32, "shape")
+    in_pat, pi = _host(in_pat, np.int8, "in_pat")
+    out_pat, po = _host(out_pat, np.int8, "out_pat")
+    reward, pr = _host(reward, np.int32, "reward")
+    R = shape.shape[1] if shape.ndim == 3 else 0
+    _check("av_load_rules", load_library().av_load_rules(batch, R, ps, pi, po, pr))
+
+
+def av_reset(batch, init_maps):
+    info = av_get_info(batch)
+    shp = (info["num_envs"], info["channels"], info["height"], info["width"])
+    torch = _torch()
+    _check("av_reset", load_library().av_reset(batch, _dev_ptr(init_maps, torch.uint8, shp,
+                                                                 "init_maps")))
+
+
+def av_step(batch, actions, rewards, done):
+    torch = _torch()
+    B = actions.shape[0] if hasattr(actions, "shape") else 0
+    _check("av_step", load_library().av_step(
+        batch, _dev_ptr(actions, torch.uint8, (B,), "actions"),
+        _dev_ptr(rewards, torch.float32, (B,), "rewards"),
+        _dev_ptr(done, torch.uint8, (B,), "done")))
+
+
+def av_step_n(batch, k, actions, rewards, done):
+    torch = _torch()
+    B = actions.shape[1] if hasattr(actions, "shape") and actions.dim() == 2 else 0
+    _check("av_step_n", load_library().av_step_n(
+        batch, int(k), _dev_ptr(actions, torch.uint8, (k, B), "actions"),
+        _dev_ptr(rewards, torch.float32, (k, B), "rewards"),
+        _dev_ptr(done, torch.uint8, (k, B), "done")))
+
+
+def av_get_maps(batch, dst):
+    info = av_get_info(batch)
+    shp = (info["num_envs"], info["channels"], info["height"], info["width"])
+    torch = _torch()
+    _check("av_get_maps", load_library().av_get_maps(batch, _dev_ptr(dst, torch.uint8, shp, "dst")))
+
+
+def av_state_ptr(batch) -> int:
+    p = load_library().av_state_ptr(batch)
+    if not p:
+        raise AvError("av_state_ptr", AV_EINVAL, av_last_error())
+    return int(p)
+
+
+def av_get_info(batch) -> dict:
+    info = av_info()
+    _check("av_get_info", load_library().av_get_info(batch, ctypes.byref(info)))
+    return {f: getattr(info, f) for f, _ in av_info._fields_}
+
+
+def av_get_state(batch) -> bytes:
+    lib = load_library()
+    n = ctypes.c_size_t(0)
+    _check("av_get_state", lib.av_get_state(batch, None, ctypes.byref(n)))
+    buf = ctypes.create_string_buffer(n.value)
+    _check("av_get_state", lib.av_get_state(batch, buf, ctypes.byref(n)))
+    return buf.raw[:n.value]
+
+
+def av_set_state(batch, blob: bytes):
+    buf = ctypes.create_string_buffer(blob, len(blob))
+    _check("av_set_state", load_library().av_set_state(batch, buf, len(blob)))
+
+
+def av_set_stream(batch, stream):
+    if hasattr(stream, "cuda_stream"):
+        stream = ctypes.c_void_p(stream.cuda_stream)
+    _check("av_set_stream", load_library().av_set_stream(batch, stream))
+
+
+def av_destroy_batch(batch):
+    _check("av_destroy_batch", load_library().av_destroy_batch(batch))
+
+
+class Batch:
+    """A batch of B environments on one GPU, with reusable device buffers for actions,
+    rewards and done flags."""
+
+    def __init__(self, num_envs, height, width, channels, max_rules, max_pat_h, max_pat_w,
+                 per_env_rules=False, max_episode_steps=0, device=None, engine="auto"):
+        torch = _torch()
+        self.device = torch.device("cuda", torch.cuda.current_device() if device is None
+                                   else device)
+        self.B, self.H, self.W, self.C = num_envs, height, width, channels
+        self.h = av_create_batch(num_envs, height, width, channels, max_rules, max_pat_h,
+                                 max_pat_w, per_env_rules, max_episode_steps,
+                                 self.device.index, engine)
+        self.rewards = torch.zeros(num_envs, dtype=torch.float32, device=self.device)
+        self.done = torch.zeros(num_envs, dtype=torch.uint8, device=self.device)
+
+    @classmethod
+    def for_workload(cls, wl, B=None, device=None, engine="auto"):
+        return cls(wl.B if B is None else B, wl.H, wl.W, wl.C, wl.R, wl.max_h, wl.max_w,
+                   wl.per_env, wl.L, device=device, engine=engine)
+
+    @property
+    def info(self):
+        return av_get_info(self.h)
+
+    def load_rules(self, shape, in_pat, out_pat, reward):
+        av_load_rules(self.h, shape, in_pat, out_pat, reward)
+
+    def reset(self, init_maps):
+        torch = _torch()
+        if not isinstance(init_maps, torch.Tensor):
+            init_maps = torch.from_numpy(np.ascontiguousarray(init_maps, dtype=np.uint8))
+        av_reset(self.h, init_maps.to(self.device).contiguous())
+
+    def step(self, actions):
+        """actions: uint8 device tensor [B]; returns this batch's (rewards, done) tensors."""
+        av_step(self.h, actions, self.rewards, self.done)
+        return self.rewards, self.done
+
+    def step_n(self, actions, rewards=None, done=None):
+        """actions [k][B] uint8 on the device; returns rewards [k][B], done [k][B]."""
+        torch = _torch()
+        k = actions.shape[0]
+        if rewards is None:
+            rewards = torch.empty((k, self.B), dtype=torch.float32, device=self.device)
+        if done is None:
+            done = torch.empty((k, self.B), dtype=torch.uint8, device=self.device)
+        av_step_n(self.h, k, actions, rewards, done)
+        return rewards, done
+
+    def maps(self, out=None):
+        torch = _torch()
+        if out is None:
+            out = torch.empty((self.B, self.C, self.H, self.W), dtype=torch.uint8,
+                              device=self.device)
+        av_get_maps(self.h, out)
+        return out
+
+    def state_ptr(self) -> int:
+        return av_state_ptr(self.h)
+
+    def get_state(self) -> bytes:
+        return av_get_state(self.h)
+
+    def set_state(self, blob: bytes):
+        av_set_state(self.h, blob)
+
+    def close(self):
+        if getattr(self, "h", None) is not None:
+            av_destroy_batch(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,500 @@
+// libautoverse host library: the C ABI of include/autoverse.h.
+//
+// Responsibilities: argument checks (all before any device work), rule compilation into
+// the kernels' programs, ownership of the packed device state, kernel-family choice and
+// launches on the batch's stream.  Device failures are reported as AV_EDEVICE with the
+// HIP error string.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "av_internal.h"
+#include "lane16.h"
+
+using namespace av;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+av_status fail(av_status st, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return st;
+}
+
+#define AV_HIP(call)                                                                  \
+    do {                                                                              \
+        hipError_t e_ = (call);                                                       \
+        if (e_ != hipSuccess)                                                         \
+            return fail(AV_EDEVICE, "%s failed: %s", #call, hipGetErrorString(e_));  \
+    } while (0)
+
+constexpr char kBlobMagic[8] = {'A', 'V', 'S', 'T', 'A', 'T', 'E', '1'};
+
+struct BlobHeader {
+    char magic[8];
+    int32_t B, H, W, C, row_bytes, reserved;
+    uint64_t state_bytes;
+};
+
+}  // namespace
+
+struct av_batch_s {
+    av_config cfg{};
+    hipStream_t stream = nullptr;
+    int row_bytes = 0;
+    size_t state_bytes = 0;
+    void *d_state = nullptr;
+    void *d_init = nullptr;
+    int32_t *d_t = nullptr;
+    int envs_per_block = 1;
+    int engine = AV_ENGINE_GENERIC;
+    bool have_rules = false, have_maps = false;
+    int32_t R = 0;
+    GenericProgram prog;
+    DeviceProgram dprog;
+    Lane16Program lprog;           // compiled form for the lane16 engine (when chosen)
+    Lane16Device dlprog;
+};
+
+namespace {
+
+void dev_free(void *p) {
+    if (p) (void)hipFree(p);
+}
+
+void free_device_program(av_batch_t b) {
+    dev_free(b->dprog.hdr);
+    dev_free(b->dprog.votes);
+    dev_free(b->dprog.match);
+    dev_free(b->dprog.vote);
+    b->dprog = DeviceProgram{};
+    lane16_free(b->dlprog);
+}
+
+// Output-kernel entry K_O = O - I; unspecified output: no vote; unspecified input: the
+// vote points at the output value (paper Sec. 2.1, transposed-convolution write).
+int kout(int in, int out) {
+    if (out < 0) return 0;
+    if (out == 1) return in == 1 ? 0 : 1;
+    return in == 0 ? 0 : -1;
+}
+
+// One rule in tri-valued form over C + 1 channels, n x m.
+struct HostRule {
+    int n = 1, m = 1, reward = 0;
+    std::vector<int8_t> in, out;   // [C+1][n][m]
+    int8_t at(const std::vector<int8_t> &p, int c, int i, int j) const {
+        return p[(size_t(c) * n + i) * m + j];
+    }
+};
+
+// The four built-in moves (paper Sec. 2.1: the player moves onto an adjacent cell that
+// holds force and no obstacle, consuming the force; Sec. 2.2.1: walls block): rules 0..3
+// are right, left, down, up.  Source cell: player 1 -> 0.  Target cell: force 1 and
+// wall 0 -> player 1, force 0.
+std::vector<HostRule> move_rules(int C) {
+    struct Mv { int n, m, sy, sx, ty, tx; };
+    const Mv mv[4] = {{1, 2, 0, 0, 0, 1}, {1, 2, 0, 1, 0, 0}, {2, 1, 0, 0, 1, 0}, {2, 1, 1, 0, 0, 0}};
+    std::vector<HostRule> out;
+    for (const Mv &q : mv) {
+        HostRule r;
+        r.n = q.n; r.m = q.m; r.reward = 0;
+        r.in.assign(size_t(C + 1) * q.n * q.m, -1);
+        r.out.assign(size_t(C + 1) * q.n * q.m, -1);
+        auto idx = [&](int c, int i, int j) { return (size_t(c) * q.n + i) * q.m + j; };
+        r.in[idx(kChPlayer, q.sy, q.sx)] = 1;
+        r.out[idx(kChPlayer, q.sy, q.sx)] = 0;
+        r.in[idx(C, q.ty, q.tx)] = 1;
+        r.in[idx(kChWall, q.ty, q.tx)] = 0;
+        r.out[idx(kChPlayer, q.ty, q.tx)] = 1;
+        r.out[idx(C, q.ty, q.tx)] = 0;
+        out.push_back(std::move(r));
+    }
+    return out;
+}
+
+// Order in which a rule's input entries are tested: rarest evidence first, so a thread
+// can stop as soon as its whole row has failed.  Force and player bits are rare; walls
+// and empty tiles are common; a must-be-1 entry rejects more than a must-be-0 one.
+int entry_rank(int c, int want, int C) {
+    int ch;
+    if (c == C) ch = 0;
+    else if (c == kChPlayer) ch = 1;
+    else if (c == kChGoal || c >= 4) ch = 2;
+    else if (c == kChWall) ch = 3;
+    else ch = 4;
+    return (want ? 0 : 8) + ch;
+}
+
+void compile_generic(const std::vector<std::vector<HostRule>> &sets, int C, GenericProgram &p) {
+    const int C1 = C + 1;
+    p.sets = int(sets.size());
+    p.rules_per_set = int(sets[0].size());
+    std::vector<std::vector<uint32_t>> match(sets.size()), vote(sets.size());
+    p.hdr.assign(size_t(p.sets) * p.rules_per_set, RuleHdr{});
+    p.votes.assign(size_t(p.sets) * C1, VoteList{});
+    for (size_t s = 0; s < sets.size(); ++s) {
+        std::vector<std::vector<uint32_t>> per_ch(C1);
+        for (int r = 0; r < p.rules_per_set; ++r) {
+            const HostRule &hr = sets[s][r];
+            RuleHdr &h = p.hdr[s * p.rules_per_set + r];
+            h.n = hr.n; h.m = hr.m; h.reward = hr.reward;
+            h.match_off = int(match[s].size());
+            std::vector<std::pair<int, uint32_t>> ents;
+            for (int c = 0; c < C1; ++c)
+                for (int i = 0; i < hr.n; ++i)
+                    for (int j = 0; j < hr.m; ++j) {
+                        const int w = hr.at(hr.in, c, i, j);
+                        if (w >= 0) ents.push_back({entry_rank(c, w, C), pack_match(c, i, j, w)});
+                        const int k = kout(w, hr.at(hr.out, c, i, j));
+                        if (k) per_ch[c].push_back(pack_vote(r, i, j, k > 0));
+                    }
+            std::stable_sort(ents.begin(), ents.end(),
+                             [](auto &a, auto &b) { return a.first < b.first; });
+            for (auto &e : ents) match[s].push_back(e.second);
+            h.match_cnt = int(match[s].size()) - h.match_off;
+        }
+        for (int c = 0; c < C1; ++c) {
+            p.votes[s * C1 + c] = VoteList{int(vote[s].size()), int(per_ch[c].size())};
+            vote[s].insert(vote[s].end(), per_ch[c].begin(), per_ch[c].end());
+        }
+    }
+    p.match_stride = 1;
+    p.vote_stride = 1;
+    for (size_t s = 0; s < sets.size(); ++s) {
+        p.match_stride = std::max(p.match_stride, int(match[s].size()));
+        p.vote_stride = std::max(p.vote_stride, int(vote[s].size()));
+    }
+    p.match.assign(size_t(p.sets) * p.match_stride, 0);
+    p.vote.assign(size_t(p.sets) * p.vote_stride, 0);
+    for (size_t s = 0; s < sets.size(); ++s) {
+        std::copy(match[s].begin(), match[s].end(), p.match.begin() + s * p.match_stride);
+        std::copy(vote[s].begin(), vote[s].end(), p.vote.begin() + s * p.vote_stride);
+    }
+}
+
+template <typename T>
+av_status upload(T **dst, const std::vector<T> &src) {
+    const size_t n = std::max<size_t>(src.size(), 1) * sizeof(T);
+    AV_HIP(hipMalloc(reinterpret_cast<void **>(dst), n));
+    if (!src.empty()) AV_HIP(hipMemcpy(*dst, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice));
+    return AV_OK;
+}
+
+av_status check_batch(av_batch_t b) {
+    if (!b) return fail(AV_EINVAL, "batch handle is NULL");
+    return AV_OK;
+}
+
+av_status set_device(av_batch_t b) {
+    AV_HIP(hipSetDevice(b->cfg.device));
+    return AV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *av_last_error(void) { return g_last_error.c_str(); }
+
+av_status av_create_batch(const av_config *cfg, av_batch_t *out) {
+    g_last_error.clear();
+    if (!out) return fail(AV_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (!cfg) return fail(AV_EINVAL, "cfg is NULL");
+    const av_config &c = *cfg;
+    if (c.num_envs < 1) return fail(AV_EINVAL, "num_envs must be >= 1 (got %d)", c.num_envs);
+    if (c.height < 1 || c.height > kMaxDim || c.width < 1 || c.width > kMaxDim)
+        return fail(AV_EINVAL, "height and width must be in [1, %d] (got %d x %d)", kMaxDim,
+                    c.height, c.width);
+    if (c.channels < 4 || c.channels > 31)
+        return fail(AV_EINVAL, "channels must be in [4, 31] (got %d)", c.channels);
+    if (c.max_rules < 0 || c.max_rules > kMaxRules)
+        return fail(AV_EINVAL, "max_rules must be in [0, %d] (got %d)", kMaxRules, c.max_rules);
+    if (c.max_pat_h < 1 || c.max_pat_h > kMaxPat || c.max_pat_w < 1 || c.max_pat_w > kMaxPat)
+        return fail(AV_EINVAL, "max_pat_h and max_pat_w must be in [1, %d]", kMaxPat);
+    if (c.per_env_rules != 0 && c.per_env_rules != 1)
+        return fail(AV_EINVAL, "per_env_rules must be 0 or 1");
+    if (c.max_episode_steps < 0) return fail(AV_EINVAL, "max_episode_steps must be >= 0");
+    if (c.engine < AV_ENGINE_AUTO || c.engine > AV_ENGINE_LANE16)
+        return fail(AV_EINVAL, "unknown engine %d", c.engine);
+    const size_t env_lds = generic_env_lds_bytes(c.height, c.width, c.channels,
+                                                 c.max_rules + kMoveRules);
+    if (env_lds > size_t(kLdsBudget))
+        return fail(AV_EINVAL, "one environment needs %zu bytes of LDS (limit %d): fewer rules, "
+                    "channels or a smaller map", env_lds, kLdsBudget);
+    const bool lane16_ok = lane16_eligible(c);
+    if (c.engine == AV_ENGINE_LANE16 && !lane16_ok)
+        return fail(AV_EINVAL, "the lane16 engine needs H, W <= 16 and patterns of at most "
+                    "%d x %d", kLane16MaxPat, kLane16MaxPat);
+
+    int dev_count = 0;
+    AV_HIP(hipGetDeviceCount(&dev_count));
+    if (c.device < 0 || c.device >= dev_count)
+        return fail(AV_EINVAL, "device %d out of range (%d devices)", c.device, dev_count);
+    AV_HIP(hipSetDevice(c.device));
+
+    av_batch_s *b = new (std::nothrow) av_batch_s;
+    if (!b) return fail(AV_ENOMEM, "host allocation failed");
+    b->cfg = c;
+    b->stream = static_cast<hipStream_t>(c.stream);
+    b->row_bytes = c.width <= 16 ? 2 : (c.width <= 32 ? 4 : 8);
+    b->state_bytes = size_t(c.channels) * c.num_envs * c.height * b->row_bytes;
+    b->envs_per_block = std::max(1, std::min(256 / c.height, int(kLdsBudget / env_lds)));
+    b->engine = (c.engine == AV_ENGINE_GENERIC || !lane16_ok) ? AV_ENGINE_GENERIC : AV_ENGINE_LANE16;
+    hipError_t e = hipMalloc(&b->d_state, b->state_bytes);
+    if (e == hipSuccess) e = hipMalloc(&b->d_init, b->state_bytes);
+    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&b->d_t), sizeof(int32_t) * c.num_envs);
+    if (e == hipSuccess) e = hipMemset(b->d_state, 0, b->state_bytes);
+    if (e == hipSuccess) e = hipMemset(b->d_init, 0, b->state_bytes);
+    if (e == hipSuccess) e = hipMemset(b->d_t, 0, sizeof(int32_t) * c.num_envs);
+    if (e != hipSuccess) {
+        dev_free(b->d_state); dev_free(b->d_init); dev_free(b->d_t);
+        delete b;
+        return fail(e == hipErrorOutOfMemory ? AV_ENOMEM : AV_EDEVICE, "device allocation: %s",
+                    hipGetErrorString(e));
+    }
+    *out = b;
+    return AV_OK;
+}
+
+av_status av_load_rules(av_batch_t b, int32_t R, const int32_t *shape, const int8_t *in_pat,
+                        const int8_t *out_pat, const int32_t *reward) {
+    g_last_error.clear();
+    if (av_status st = check_batch(b)) return st;
+    const av_config &c = b->cfg;
+    if (R < 0 || R > c.max_rules)
+        return fail(AV_EINVAL, "num_rules %d outside [0, max_rules = %d]", R, c.max_rules);
+    if (R > 0 && (!shape || !in_pat || !out_pat || !reward))
+        return fail(AV_EINVAL, "rule arrays must not be NULL");
+    const int S = c.per_env_rules ? c.num_envs : 1;
+    const int C1 = c.channels + 1, ph = c.max_pat_h, pw = c.max_pat_w;
+    const size_t pat = size_t(C1) * ph * pw;
+    std::vector<std::vector<HostRule>> sets(S);
+    const std::vector<HostRule> moves = move_rules(c.channels);
+    for (int s = 0; s < S; ++s) {
+        sets[s] = moves;
+        long long worst = 0;
+        for (int r = 0; r < R; ++r) {
+            const size_t k = size_t(s) * R + r;
+            HostRule hr;
+            hr.n = shape[2 * k];
+            hr.m = shape[2 * k + 1];
+            hr.reward = reward[k];
+            if (hr.n < 1 || hr.n > ph || hr.n > c.height || hr.m < 1 || hr.m > pw || hr.m > c.width)
+                return fail(AV_EINVAL, "set %d rule %d: shape %d x %d outside [1, min(max_pat, map)]",
+                            s, r, hr.n, hr.m);
+            for (size_t e = 0; e < pat; ++e) {
+                const int vi = in_pat[k * pat + e], vo = out_pat[k * pat + e];
+                if (vi < -1 || vi > 1 || vo < -1 || vo > 1)
+                    return fail(AV_EINVAL, "set %d rule %d: pattern value outside {-1, 0, 1}", s, r);
+            }
+            hr.in.assign(size_t(C1) * hr.n * hr.m, -1);
+            hr.out.assign(size_t(C1) * hr.n * hr.m, -1);
+            for (int ch = 0; ch < C1; ++ch)
+                for (int i = 0; i < hr.n; ++i)
+                    for (int j = 0; j < hr.m; ++j) {
+                        const size_t src = k * pat + (size_t(ch) * ph + i) * pw + j;
+                        hr.in[(size_t(ch) * hr.n + i) * hr.m + j] = in_pat[src];
+                        hr.out[(size_t(ch) * hr.n + i) * hr.m + j] = out_pat[src];
+                    }
+            const long long rw = hr.reward < 0 ? -(long long)hr.reward : hr.reward;
+            worst += rw * (long long)(c.height - hr.n + 1) * (c.width - hr.m + 1);
+            sets[s].push_back(std::move(hr));
+        }
+        if (worst >= (1LL << 24))
+            return fail(AV_EINVAL, "set %d: |reward| x anchors sums to %lld >= 2^24; the float "
+                        "reward would not be exact", s, worst);
+    }
+    if (av_status st = set_device(b)) return st;
+    AV_HIP(hipStreamSynchronize(b->stream));   // no step may still read the old program
+    free_device_program(b);
+    b->have_rules = false;
+    compile_generic(sets, c.channels, b->prog);
+    if (av_status st = upload(&b->dprog.hdr, b->prog.hdr)) return st;
+    if (av_status st = upload(&b->dprog.votes, b->prog.votes)) return st;
+    if (av_status st = upload(&b->dprog.match, b->prog.match)) return st;
+    if (av_status st = upload(&b->dprog.vote, b->prog.vote)) return st;
+    b->dprog.rules_per_set = b->prog.rules_per_set;
+    b->dprog.match_stride = b->prog.match_stride;
+    b->dprog.vote_stride = b->prog.vote_stride;
+    if (b->engine == AV_ENGINE_LANE16) {
+        std::vector<std::vector<Lane16Rule>> lsets(S);
+        for (int s = 0; s < S; ++s)
+            for (const HostRule &hr : sets[s]) {
+                Lane16Rule lr;
+                lr.n = hr.n; lr.m = hr.m; lr.reward = hr.reward;
+                lr.in = hr.in; lr.out = hr.out;
+                lsets[s].push_back(std::move(lr));
+            }
+        lane16_compile(lsets, c.channels, b->lprog);
+        hipError_t e = lane16_upload(b->lprog, b->dlprog);
+        if (e != hipSuccess) return fail(AV_EDEVICE, "lane16 upload: %s", hipGetErrorString(e));
+    }
+    b->R = R;
+    b->have_rules = true;
+    return AV_OK;
+}
+
+av_status av_reset(av_batch_t b, const uint8_t *init_maps) {
+    g_last_error.clear();
+    if (av_status st = check_batch(b)) return st;
+    if (!init_maps) return fail(AV_EINVAL, "init_maps is NULL");
+    if (av_status st = set_device(b)) return st;
+    const av_config &c = b->cfg;
+    AV_HIP(launch_pack(init_maps, b->d_init, b->d_state, c.num_envs, c.channels, c.height, c.width,
+                       b->row_bytes, b->stream));
+    AV_HIP(hipMemsetAsync(b->d_t, 0, sizeof(int32_t) * c.num_envs, b->stream));
+    b->have_maps = true;
+    return AV_OK;
+}
+
+static av_status step_k(av_batch_t b, int32_t k, const uint8_t *actions, float *rewards,
+                        uint8_t *done) {
+    if (av_status st = check_batch(b)) return st;
+    if (k < 1) return fail(AV_EINVAL, "k must be >= 1 (got %d)", k);
+    if (!actions || !rewards || !done) return fail(AV_EINVAL, "actions, rewards and done must not be NULL");
+    if (!b->have_rules || !b->have_maps)
+        return fail(AV_ESTATE, "call av_load_rules and av_reset before stepping");
+    if (av_status st = set_device(b)) return st;
+    const av_config &c = b->cfg;
+    StepArgs a{};
+    a.B = c.num_envs; a.H = c.height; a.W = c.width; a.C = c.channels;
+    a.L = c.max_episode_steps; a.per_env = c.per_env_rules; a.k = k;
+    a.row_bytes = b->row_bytes;
+    a.state = b->d_state; a.init = b->d_init; a.t = b->d_t;
+    a.actions = actions; a.rewards = rewards; a.done = done;
+    a.prog = b->dprog;
+    if (b->engine == AV_ENGINE_LANE16)
+        AV_HIP(launch_lane16_step(a, b->dlprog, b->stream));
+    else
+        AV_HIP(launch_generic_step(a, b->envs_per_block, b->stream));
+    return AV_OK;
+}
+
+av_status av_step(av_batch_t b, const uint8_t *actions, float *rewards, uint8_t *done) {
+    g_last_error.clear();
+    return step_k(b, 1, actions, rewards, done);
+}
+
+av_status av_step_n(av_batch_t b, int32_t k, const uint8_t *actions, float *rewards,
+                    uint8_t *done) {
+    g_last_error.clear();
+    return step_k(b, k, actions, rewards, done);
+}
+
+av_status av_get_maps(av_batch_t b, uint8_t *dst) {
+    g_last_error.clear();
+    if (av_status st = check_batch(b)) return st;
+    if (!dst) return fail(AV_EINVAL, "dst is NULL");
+    if (av_status st = set_device(b)) return st;
+    const av_config &c = b->cfg;
+    AV_HIP(launch_unpack(b->d_state, dst, c.num_envs, c.channels, c.height, c.width, b->row_bytes,
+                         b->stream));
+    return AV_OK;
+}
+
+const void *av_state_ptr(av_batch_t b) {
+    g_last_error.clear();
+    if (!b) { fail(AV_EINVAL, "batch handle is NULL"); return nullptr; }
+    return b->d_state;
+}
+
+av_status av_get_info(av_batch_t b, av_info *info) {
+    g_last_error.clear();
+    if (av_status st = check_batch(b)) return st;
+    if (!info) return fail(AV_EINVAL, "info is NULL");
+    info->num_envs = b->cfg.num_envs;
+    info->height = b->cfg.height;
+    info->width = b->cfg.width;
+    info->channels = b->cfg.channels;
+    info->row_bytes = b->row_bytes;
+    info->engine = b->engine;
+    info->state_bytes = b->state_bytes;
+    info->blob_bytes = sizeof(BlobHeader) + 2 * b->state_bytes + sizeof(int32_t) * b->cfg.num_envs;
+    return AV_OK;
+}
+
+av_status av_get_state(av_batch_t b, void *host_blob, size_t *bytes) {
+    g_last_error.clear();
+    if (av_status st = check_batch(b)) return st;
+    if (!bytes) return fail(AV_EINVAL, "bytes is NULL");
+    const size_t need = sizeof(BlobHeader) + 2 * b->state_bytes + sizeof(int32_t) * b->cfg.num_envs;
+    if (!host_blob) { *bytes = need; return AV_OK; }
+    if (*bytes < need) return fail(AV_EINVAL, "blob needs %zu bytes, got %zu", need, *bytes);
+    if (av_status st = set_device(b)) return st;
+    BlobHeader h{};
+    std::memcpy(h.magic, kBlobMagic, 8);
+    h.B = b->cfg.num_envs; h.H = b->cfg.height; h.W = b->cfg.width; h.C = b->cfg.channels;
+    h.row_bytes = b->row_bytes; h.state_bytes = b->state_bytes;
+    char *p = static_cast<char *>(host_blob);
+    std::memcpy(p, &h, sizeof h);
+    AV_HIP(hipStreamSynchronize(b->stream));
+    AV_HIP(hipMemcpy(p + sizeof h, b->d_state, b->state_bytes, hipMemcpyDeviceToHost));
+    AV_HIP(hipMemcpy(p + sizeof h + b->state_bytes, b->d_init, b->state_bytes, hipMemcpyDeviceToHost));
+    AV_HIP(hipMemcpy(p + sizeof h + 2 * b->state_bytes, b->d_t, sizeof(int32_t) * b->cfg.num_envs,
+                     hipMemcpyDeviceToHost));
+    *bytes = need;
+    return AV_OK;
+}
+
+av_status av_set_state(av_batch_t b, const void *host_blob, size_t bytes) {
+    g_last_error.clear();
+    if (av_status st = check_batch(b)) return st;
+    if (!host_blob) return fail(AV_EINVAL, "host_blob is NULL");
+    const size_t need = sizeof(BlobHeader) + 2 * b->state_bytes + sizeof(int32_t) * b->cfg.num_envs;
+    if (bytes < need) return fail(AV_EINVAL, "blob has %zu bytes, need %zu", bytes, need);
+    BlobHeader h;
+    std::memcpy(&h, host_blob, sizeof h);
+    if (std::memcmp(h.magic, kBlobMagic, 8) != 0) return fail(AV_EINVAL, "not a state blob");
+    if (h.B != b->cfg.num_envs || h.H != b->cfg.height || h.W != b->cfg.width ||
+        h.C != b->cfg.channels || h.row_bytes != b->row_bytes || h.state_bytes != b->state_bytes)
+        return fail(AV_EINVAL, "blob is for a %d x %dx%d x %d batch", h.B, h.H, h.W, h.C);
+    if (av_status st = set_device(b)) return st;
+    const char *p = static_cast<const char *>(host_blob);
+    AV_HIP(hipStreamSynchronize(b->stream));
+    AV_HIP(hipMemcpy(b->d_state, p + sizeof h, b->state_bytes, hipMemcpyHostToDevice));
+    AV_HIP(hipMemcpy(b->d_init, p + sizeof h + b->state_bytes, b->state_bytes, hipMemcpyHostToDevice));
+    AV_HIP(hipMemcpy(b->d_t, p + sizeof h + 2 * b->state_bytes, sizeof(int32_t) * b->cfg.num_envs,
+                     hipMemcpyHostToDevice));
+    b->have_maps = true;
+    return AV_OK;
+}
+
+av_status av_set_stream(av_batch_t b, void *stream) {
+    g_last_error.clear();
+    if (av_status st = check_batch(b)) return st;
+    b->stream = static_cast<hipStream_t>(stream);
+    b->cfg.stream = stream;
+    return AV_OK;
+}
+
+av_status av_destroy_batch(av_batch_t b) {
+    g_last_error.clear();
+    if (!b) return AV_OK;
+    av_status st = AV_OK;
+    if (hipSetDevice(b->cfg.device) == hipSuccess) {
+        hipError_t e = hipStreamSynchronize(b->stream);
+        if (e != hipSuccess) st = fail(AV_EDEVICE, "hipStreamSynchronize: %s", hipGetErrorString(e));
+        free_device_program(b);
+        dev_free(b->d_state);
+        dev_free(b->d_init);
+        dev_free(b->d_t);
+    }
+    delete b;
+    return st;
+}
+
+}  // extern "C"

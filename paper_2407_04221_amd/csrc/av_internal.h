@@ -1,0 +1,93 @@
+// Internal declarations of libautoverse: the compiled rule program, the batch object and
+// the kernel launchers.  Not part of the public ABI (include/autoverse.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/autoverse.h"
+
+namespace av {
+
+// Tile roles (paper Sec. 2.2.1, base maze game).
+constexpr int kChEmpty = 0, kChWall = 1, kChPlayer = 2, kChGoal = 3;
+constexpr int kMoveRules = 4;     // built-in moves, rule indices 0..3 of every set
+constexpr int kMaxRules = 252;    // loaded rules; with the moves a rule index fits a byte
+constexpr int kMaxDim = 64;       // largest H and W
+constexpr int kMaxPat = 16;       // largest pattern rows / cols
+constexpr int kLdsBudget = 64 * 1024;
+
+// ---------------------------------------------------------------------------------
+// Compiled rules, generic form.  Built on the host from the tri-valued patterns; one
+// "set" per environment or one shared set.  Every set starts with the four moves.
+//
+// Match entry (one specified input entry): bits 0-7 channel, 8-15 row i, 16-23 col j,
+// bit 24 wanted value.  Vote entry (one nonzero K_O entry), grouped by channel:
+// bits 0-7 rule, 8-15 row i, 16-23 col j, bit 24 set when the vote is +1.
+// ---------------------------------------------------------------------------------
+struct RuleHdr {
+    int32_t n, m;         // pattern rows, cols
+    int32_t reward;
+    int32_t match_off;    // into the set's match entries
+    int32_t match_cnt;
+};
+
+struct VoteList {
+    int32_t off, cnt;     // into the set's vote entries
+};
+
+struct GenericProgram {
+    int32_t rules_per_set = 0;        // R + 4
+    int32_t sets = 0;                 // S
+    int32_t match_stride = 0;         // match entries per set (max over sets)
+    int32_t vote_stride = 0;          // vote entries per set (max over sets)
+    std::vector<RuleHdr> hdr;         // [S][R+4]
+    std::vector<VoteList> votes;      // [S][C+1]
+    std::vector<uint32_t> match;      // [S][match_stride]
+    std::vector<uint32_t> vote;       // [S][vote_stride]
+};
+
+inline uint32_t pack_match(int c, int i, int j, int want) {
+    return uint32_t(c) | (uint32_t(i) << 8) | (uint32_t(j) << 16) | (uint32_t(want) << 24);
+}
+inline uint32_t pack_vote(int r, int i, int j, bool plus) {
+    return uint32_t(r) | (uint32_t(i) << 8) | (uint32_t(j) << 16) | (uint32_t(plus) << 24);
+}
+
+// Device-side copy of a generic program.
+struct DeviceProgram {
+    RuleHdr *hdr = nullptr;
+    VoteList *votes = nullptr;
+    uint32_t *match = nullptr;
+    uint32_t *vote = nullptr;
+    int32_t rules_per_set = 0, match_stride = 0, vote_stride = 0;
+};
+
+// Everything a step kernel needs, passed by value.
+struct StepArgs {
+    int32_t B, H, W, C, L;
+    int32_t per_env;
+    int32_t k;                       // steps in this launch
+    int32_t row_bytes;
+    void *state;                     // [C][B][H] rows
+    const void *init;                // [C][B][H] rows
+    int32_t *t;                      // [B] step counters
+    const uint8_t *actions;          // [k][B]
+    float *rewards;                  // [k][B]
+    uint8_t *done;                   // [k][B]
+    DeviceProgram prog;
+};
+
+// Launchers (k_generic.hip).  All return hipSuccess or the launch error.
+hipError_t launch_pack(const uint8_t *src, void *dst, void *dst2, int B, int C, int H, int W,
+                       int row_bytes, hipStream_t s);
+hipError_t launch_unpack(const void *src, uint8_t *dst, int B, int C, int H, int W,
+                         int row_bytes, hipStream_t s);
+hipError_t launch_generic_step(const StepArgs &a, int envs_per_block, hipStream_t s);
+size_t generic_env_lds_bytes(int H, int W, int C, int rules_per_set);
+
+}  // namespace av

@@ -1,0 +1,64 @@
+"""Helpers for the GPU tests: run the HIP path through the C ABI on the same seeded
+arrays the oracle gets."""
+import sys
+
+import numpy as np
+import pytest
+
+import paper_2407_04221_amd as av
+
+
+def require_gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    av.load_library()          # missing library = failure, not a skip
+
+
+def say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def gpu_run(wl, maps, rules, actions, engine="auto", mode="step", chunk=7, B=None,
+            per_step_maps=True):
+    """Returns (maps per step or None, final maps, rewards [T][B], done [T][B]) as numpy,
+    and the engine the batch used."""
+    import torch
+    B = maps.shape[0] if B is None else B
+    b = av.Batch.for_workload(wl, B=B, engine=engine)
+    try:
+        b.load_rules(*rules)
+        b.reset(maps)
+        T = actions.shape[0]
+        acts = torch.from_numpy(np.ascontiguousarray(actions)).cuda()
+        seq = [] if (mode == "step" and per_step_maps) else None
+        if mode == "step":
+            rs, ds = [], []
+            for t in range(T):
+                r, d = b.step(acts[t])
+                rs.append(r.clone())
+                ds.append(d.clone())
+                if seq is not None:
+                    seq.append(b.maps().cpu().numpy())
+            rewards = torch.stack(rs).cpu().numpy()
+            done = torch.stack(ds).cpu().numpy()
+        else:
+            rewards = torch.empty((T, B), dtype=torch.float32, device="cuda")
+            done = torch.empty((T, B), dtype=torch.uint8, device="cuda")
+            for t0 in range(0, T, chunk):
+                k = min(chunk, T - t0)
+                b.step_n(acts[t0:t0 + k], rewards[t0:t0 + k], done[t0:t0 + k])
+            rewards = rewards.cpu().numpy()
+            done = done.cpu().numpy()
+        final = b.maps().cpu().numpy()
+        torch.cuda.synchronize()
+        eng = b.info["engine"]
+    finally:
+        b.close()
+    return (None if seq is None else np.stack(seq)), final, rewards, done, eng
+
+
+def first_mismatch(a, b):
+    idx = np.argwhere(a != b)
+    return tuple(idx[0]) if len(idx) else None

@@ -1,0 +1,106 @@
+"""The C ABI boundary without a GPU: the library loads, exports every function that
+include/autoverse.h declares, and rejects bad arguments on the host before any device
+work, with a message."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2407_04221_amd as av
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADERS = [os.path.join(ROOT, "include", f) for f in os.listdir(os.path.join(ROOT, "include"))
+           if f.endswith(".h")]
+
+
+def declared_functions():
+    names = set()
+    for h in HEADERS:
+        text = open(h).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names |= set(re.findall(r"\b(av_[a-z_0-9]+)\s*\(", text))
+    return sorted(names)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(av.LIB_PATH):
+        from paper_2407_04221_amd import build
+        build.build()
+    return av.load_library()
+
+
+def test_every_declared_function_is_exported(lib):
+    names = declared_functions()
+    assert len(names) >= 13
+    assert set(names) == set(av.ABI_SYMBOLS)
+    out = subprocess.run(["nm", "-D", "--defined-only", av.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (av_[a-z_0-9]+)$", out, flags=re.M))
+    missing = set(names) - exported
+    assert not missing, f"not exported: {missing}"
+    for n in names:
+        assert hasattr(lib, n)
+
+
+def test_no_torch_types_in_the_abi():
+    for h in HEADERS:
+        text = open(h).read()
+        assert "torch" not in text.lower().replace("torch tensors", "")
+        assert "#include <hip" not in text      # plain C types only
+
+
+def _cfg(**kw):
+    base = dict(num_envs=4, height=16, width=16, channels=6, max_rules=8, max_pat_h=3,
+                max_pat_w=3, per_env_rules=0, max_episode_steps=0, device=0, engine=0,
+                stream=None)
+    base.update(kw)
+    return av.av_config(*[base[f] for f, _ in av.av_config._fields_])
+
+
+@pytest.mark.parametrize("bad", [
+    dict(num_envs=0), dict(height=0), dict(width=65), dict(height=65), dict(channels=3),
+    dict(channels=32), dict(max_rules=-1), dict(max_rules=253), dict(max_pat_h=0),
+    dict(max_pat_w=17), dict(per_env_rules=2), dict(max_episode_steps=-1), dict(engine=9),
+    # lane16 needs maps of at most 16 x 16
+    dict(engine=2, height=32, width=32),
+    # one environment's LDS working set over 64 KiB
+    dict(height=64, width=64, channels=31, max_rules=252),
+])
+def test_create_rejects_bad_config(lib, bad):
+    cfg = _cfg(**bad)
+    h = ctypes.c_void_p(1234)
+    rc = lib.av_create_batch(ctypes.byref(cfg), ctypes.byref(h))
+    assert rc == av.AV_EINVAL
+    assert h.value is None
+    assert av.av_last_error()
+
+
+def test_null_arguments_are_rejected(lib):
+    h = ctypes.c_void_p()
+    assert lib.av_create_batch(None, ctypes.byref(h)) == av.AV_EINVAL
+    cfg = _cfg()
+    assert lib.av_create_batch(ctypes.byref(cfg), None) == av.AV_EINVAL
+    assert lib.av_step(None, None, None, None) == av.AV_EINVAL
+    assert "NULL" in av.av_last_error()
+    assert lib.av_step_n(None, 1, None, None, None) == av.AV_EINVAL
+    assert lib.av_load_rules(None, 0, None, None, None, None) == av.AV_EINVAL
+    assert lib.av_reset(None, None) == av.AV_EINVAL
+    assert lib.av_get_maps(None, None) == av.AV_EINVAL
+    assert lib.av_state_ptr(None) is None
+    info = av.av_info()
+    assert lib.av_get_info(None, ctypes.byref(info)) == av.AV_EINVAL
+    n = ctypes.c_size_t(0)
+    assert lib.av_get_state(None, None, ctypes.byref(n)) == av.AV_EINVAL
+    assert lib.av_set_state(None, None, 0) == av.AV_EINVAL
+    assert lib.av_set_stream(None, None) == av.AV_EINVAL
+    assert lib.av_destroy_batch(None) == av.AV_OK
+
+
+def test_last_error_is_cleared_by_a_successful_call(lib):
+    lib.av_step(None, None, None, None)
+    assert av.av_last_error()
+    assert lib.av_destroy_batch(None) == av.AV_OK
+    assert av.av_last_error() == ""

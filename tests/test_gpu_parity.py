@@ -1,0 +1,56 @@
+"""GPU path vs the CPU oracle, bit for bit, on the same seeded inputs.
+
+Sizes here are ones the oracle finishes in seconds, with a ragged tail (B not a multiple
+of the environments a workgroup or wave holds).  Maps, rewards and done flags are compared
+after every step (av_step) or per step from av_step_n launches of ragged length."""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import first_mismatch, gpu_run, require_gpu, say
+from paper_2407_04221_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+# (workload, B, T): every benchmark workload, cut down in B and T
+CASES = [("c1", 1, 100), ("c2", 203, 40), ("c3", 37, 30), ("c4", 333, 60), ("c5", 5, 20)]
+
+
+def _case_ids():
+    return [f"{n}-B{b}-T{t}" for n, b, t in CASES]
+
+
+@pytest.mark.parametrize("variant", inputs.VARIANTS)
+@pytest.mark.parametrize("seed", [0, 1])
+@pytest.mark.parametrize("engine", ["generic", "auto"])
+@pytest.mark.parametrize("case", CASES, ids=_case_ids())
+def test_step_matches_oracle(case, engine, seed, variant):
+    require_gpu()
+    name, B, T = case
+    wl = inputs.WORKLOADS[name].with_(B=B, T=T, L=25)
+    say(f"[parity] {name} B={B} T={T} engine={engine} seed={seed} variant={variant}")
+    maps, rules, actions = inputs.make_all(wl, seed, variant)
+    want_m, want_r, want_d = oracle.run(wl, maps, rules, actions, nthreads=8)
+    seq, final, r, d, eng = gpu_run(wl, maps, rules, actions, engine=engine, mode="step")
+    for t in range(T):
+        assert first_mismatch(seq[t], want_m[t]) is None, \
+            f"maps differ at step {t}, index {first_mismatch(seq[t], want_m[t])}"
+        assert first_mismatch(r[t], want_r[t]) is None, f"rewards differ at step {t}"
+        assert first_mismatch(d[t], want_d[t]) is None, f"done differs at step {t}"
+    assert (want_r != 0).any() or variant == "literal" or name == "c5"
+
+
+@pytest.mark.parametrize("variant", ["literal", "dense"])
+@pytest.mark.parametrize("engine", ["generic", "auto"])
+@pytest.mark.parametrize("case", CASES, ids=_case_ids())
+def test_step_n_matches_oracle(case, engine, variant):
+    require_gpu()
+    name, B, T = case
+    wl = inputs.WORKLOADS[name].with_(B=B, T=T, L=25)
+    say(f"[parity step_n] {name} B={B} T={T} engine={engine} variant={variant}")
+    maps, rules, actions = inputs.make_all(wl, 2, variant)
+    want_m, want_r, want_d = oracle.run(wl, maps, rules, actions, nthreads=8)
+    _, final, r, d, _ = gpu_run(wl, maps, rules, actions, engine=engine, mode="step_n", chunk=7)
+    np.testing.assert_array_equal(r, want_r)
+    np.testing.assert_array_equal(d, want_d)
+    np.testing.assert_array_equal(final, want_m[-1])
