@@ -237,8 +237,8 @@ av_status av_create_batch(const av_config *cfg, av_batch_t *out) {
                     "channels or a smaller map", env_lds, kLdsBudget);
     const bool lane16_ok = lane16_eligible(c);
     if (c.engine == AV_ENGINE_LANE16 && !lane16_ok)
-        return fail(AV_EINVAL, "the lane16 engine needs H, W <= 16 and patterns of at most "
-                    "%d x %d", kLane16MaxPat, kLane16MaxPat);
+        return fail(AV_EINVAL, "the lane16 engine needs H, W <= 16 and one rule set shared "
+                    "by all environments");
 
     int dev_count = 0;
     AV_HIP(hipGetDeviceCount(&dev_count));
@@ -339,9 +339,11 @@ av_status av_load_rules(av_batch_t b, int32_t R, const int32_t *shape, const int
                 lr.in = hr.in; lr.out = hr.out;
                 lsets[s].push_back(std::move(lr));
             }
-        lane16_compile(lsets, c.channels, b->lprog);
-        hipError_t e = lane16_upload(b->lprog, b->dlprog);
-        if (e != hipSuccess) return fail(AV_EDEVICE, "lane16 upload: %s", hipGetErrorString(e));
+        lane16_compile(lsets, c.channels, c.height, c.width, c.max_episode_steps, b->lprog);
+        std::string log;
+        hipError_t e = lane16_upload(b->lprog, b->dlprog, &log);
+        if (e != hipSuccess)
+            return fail(AV_EDEVICE, "lane16 kernel build: %s %s", hipGetErrorString(e), log.c_str());
     }
     b->R = R;
     b->have_rules = true;

@@ -1,0 +1,350 @@
+// lane16 engine, host side: turns a shared rule set into the straight-line body of the
+// step kernel, compiles the kernel with hipRTC for gfx950 and launches it.
+//
+// Generated code, per rule r (n x m), all on 32-bit lane words that hold one map row of
+// two environments (see lane16_kernel.hip):
+//   M_r  = valid-anchor mask V_n_m (rows y <= H-n, columns x <= W-m of both halves),
+//          AND-ed with every specified input entry (c, i, j, want): plane c moved up i rows
+//          (DPP row shift) and right-aligned by j columns, complemented for want = 0.  This
+//          is the paper's thresholded convolution (Sec. 2.1) evaluated 32 anchors at a time.
+//          The two rarest entries are tested first; if no anchor of the wave survives them
+//          the rest of the rule is skipped (a wave-uniform branch).
+//   reward += reward_r * popcount(M_r) per half.
+//   votes: every nonzero K_O = O - I entry (c, i, j) moves M_r down i rows and left by j
+//          columns onto the cells it writes; +1 votes are OR-ed into PL_c, -1 votes into
+//          MI_c.  A cell with votes of one sign only takes that sign's value; if some cell
+//          of the wave has votes of both signs, the channel's votes are counted exactly with
+//          carry-save adders and the cell becomes 1 iff old + #plus > #minus, i.e. iff
+//          old + sum >= 1 (Sec. 2.1 transposed-convolution write, clamped to {0, 1}).
+//   The force plane's own votes are not evaluated: the plane is dropped after the step.
+#include <hip/hip_runtime.h>
+#include <hip/hiprtc.h>
+
+#include <algorithm>
+#include <deque>
+#include <map>
+#include <mutex>
+#include <set>
+#include <sstream>
+#include <string>
+#include <vector>
+
+#include "lane16.h"
+
+namespace av {
+namespace {
+
+#include "_lane16_template.inc"   // kLane16Template: lane16_kernel.hip as a string
+
+std::string plane(int c, int C) { return c == C ? std::string("F") : "p[" + std::to_string(c) + "]"; }
+
+struct Entry {
+    int c, i, j, want, rank;
+};
+
+// Rarest evidence first: force and player bits are rare, walls and empty tiles common;
+// a must-be-1 entry rejects more anchors than a must-be-0 entry.
+int rank_of(int c, int want, int C) {
+    int ch;
+    if (c == C) ch = 0;
+    else if (c == kChPlayer) ch = 1;
+    else if (c == kChGoal || c >= 4) ch = 2;
+    else if (c == kChWall) ch = 3;
+    else ch = 4;
+    return (want ? 0 : 8) + ch;
+}
+
+int kout(int in, int out) {
+    if (out < 0) return 0;
+    if (out == 1) return in == 1 ? 0 : 1;
+    return in == 0 ? 0 : -1;
+}
+
+struct Vote {
+    int r, i, j;
+};
+
+class Gen {
+  public:
+    std::ostringstream o;
+    int tmp = 0;
+    std::string fresh() { return "t" + std::to_string(tmp++); }
+
+    // Bit-sliced population count of `terms` (each a 32-bit plane): returns the count's
+    // bits, least significant first, built from full and half adders.
+    std::vector<std::string> count(const std::vector<std::string> &terms) {
+        std::vector<std::deque<std::string>> lv(1, std::deque<std::string>(terms.begin(), terms.end()));
+        std::vector<std::string> bits;
+        for (size_t k = 0; k < lv.size(); ++k) {
+            std::deque<std::string> q = lv[k];
+            std::vector<std::string> carries;
+            while (q.size() >= 3) {
+                const std::string a = q[0], b = q[1], c = q[2];
+                q.pop_front(); q.pop_front(); q.pop_front();
+                const std::string s = fresh(), cy = fresh();
+                o << "const u32 " << s << " = " << a << " ^ " << b << " ^ " << c << ";\n";
+                o << "const u32 " << cy << " = (" << a << " & " << b << ") | (" << c << " & (" << a
+                  << " ^ " << b << "));\n";
+                q.push_back(s);
+                carries.push_back(cy);
+            }
+            if (q.size() == 2) {
+                const std::string a = q[0], b = q[1];
+                const std::string s = fresh(), cy = fresh();
+                o << "const u32 " << s << " = " << a << " ^ " << b << ";\n";
+                o << "const u32 " << cy << " = " << a << " & " << b << ";\n";
+                q.clear();
+                q.push_back(s);
+                carries.push_back(cy);
+            }
+            bits.push_back(q.empty() ? std::string("0u") : q.front());
+            if (!carries.empty()) {
+                if (lv.size() == k + 1) lv.emplace_back();
+                lv[k + 1].insert(lv[k + 1].end(), carries.begin(), carries.end());
+            }
+        }
+        return bits;
+    }
+};
+
+}  // namespace
+
+bool lane16_eligible(const av_config &c) {
+    return c.height <= 16 && c.width <= 16 && c.per_env_rules == 0 && c.max_pat_h <= 16 &&
+           c.max_pat_w <= 16;
+}
+
+std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule> &rules) {
+    Gen g;
+    std::ostringstream &o = g.o;
+    const int C1 = C + 1, R = int(rules.size());
+    auto in_at = [&](const Lane16Rule &r, int c, int i, int j) {
+        return int(r.in[(size_t(c) * r.n + i) * r.m + j]);
+    };
+    auto out_at = [&](const Lane16Rule &r, int c, int i, int j) {
+        return int(r.out[(size_t(c) * r.n + i) * r.m + j]);
+    };
+
+    std::vector<std::vector<Entry>> ents(R);
+    std::set<std::pair<int, int>> xs, shapes;
+    std::vector<std::vector<Vote>> plus(C), minus(C);
+    std::vector<std::vector<std::pair<Vote, int>>> rule_votes(R);   // (vote, channel * 2 + sign)
+    for (int r = 0; r < R; ++r) {
+        const Lane16Rule &ru = rules[r];
+        shapes.insert({ru.n, ru.m});
+        for (int c = 0; c < C1; ++c)
+            for (int i = 0; i < ru.n; ++i)
+                for (int j = 0; j < ru.m; ++j) {
+                    const int w = in_at(ru, c, i, j);
+                    if (w >= 0) {
+                        ents[r].push_back({c, i, j, w, rank_of(c, w, C)});
+                        if (j > 0) xs.insert({c, j});
+                    }
+                    const int k = c < C ? kout(w, out_at(ru, c, i, j)) : 0;
+                    if (k > 0) plus[c].push_back({r, i, j});
+                    if (k < 0) minus[c].push_back({r, i, j});
+                    if (k) rule_votes[r].push_back({Vote{r, i, j}, c * 2 + (k > 0)});
+                }
+        std::stable_sort(ents[r].begin(), ents[r].end(),
+                         [](const Entry &a, const Entry &b) { return a.rank < b.rank; });
+    }
+
+    o << "// ---- generated: " << R << " rules over " << C1 << " planes ----\n";
+    for (auto &x : xs)
+        o << "const u32 X" << x.first << "_" << x.second << " = " << plane(x.first, C) << " >> "
+          << x.second << ";\n";
+    for (auto &s : shapes)
+        o << "const u32 V" << s.first << "_" << s.second << " = (y <= " << (H - s.first)
+          << ") ? BOTH(COLMASK(" << std::max(0, W - s.second + 1) << ")) : 0u;\n";
+
+    auto base = [&](const Entry &e) {
+        return e.j ? "X" + std::to_string(e.c) + "_" + std::to_string(e.j) : plane(e.c, C);
+    };
+
+    // match
+    for (int r = 0; r < R; ++r) {
+        const Lane16Rule &ru = rules[r];
+        const std::string M = "M" + std::to_string(r), f = "f" + std::to_string(r);
+        o << "u32 " << M << " = V" << ru.n << "_" << ru.m << ";\n";
+        const size_t probe = std::min<size_t>(2, ents[r].size());
+        for (size_t e = 0; e < probe; ++e) {
+            const Entry &en = ents[r][e];
+            const std::string t = en.i ? "DPP_SHL(" + base(en) + ", " + std::to_string(en.i) + ")" : base(en);
+            o << M << " &= " << (en.want ? "" : "~") << t << ";\n";
+        }
+        o << "bool " << f << " = ANY(" << M << ");\n";
+        if (ents[r].size() > probe) {
+            o << "if (" << f << ") {\n";
+            std::map<int, std::vector<Entry>> by_row;
+            for (size_t e = probe; e < ents[r].size(); ++e) by_row[ents[r][e].i].push_back(ents[r][e]);
+            for (auto &row : by_row) {
+                std::string q;
+                for (const Entry &en : row.second) {
+                    if (!q.empty()) q += " & ";
+                    q += (en.want ? "" : "~") + base(en);
+                }
+                if (row.first == 0) o << M << " &= " << q << ";\n";
+                else o << M << " &= DPP_SHL(" << q << ", " << row.first << ");\n";
+            }
+            o << f << " = ANY(" << M << ");\n";
+            o << "}\n";
+        }
+        if (ru.reward != 0)
+            o << "if (" << f << ") { rA += " << ru.reward << " * (int)__popc(" << M
+              << " & 0xFFFFu); rB += " << ru.reward << " * (int)__popc(" << M << " >> 16); }\n";
+    }
+
+    // votes, fast path: OR per channel and sign
+    for (int c = 0; c < C; ++c)
+        if (!plus[c].empty() || !minus[c].empty())
+            o << "u32 PL" << c << " = 0u, MI" << c << " = 0u;\n";
+    for (int r = 0; r < R; ++r) {
+        if (rule_votes[r].empty()) continue;
+        const std::string M = "M" + std::to_string(r);
+        o << "if (f" << r << ") {\n";
+        std::set<int> js;
+        for (auto &v : rule_votes[r])
+            if (v.first.j) js.insert(v.first.j);
+        for (int j : js) o << "const u32 L" << r << "_" << j << " = " << M << " << " << j << ";\n";
+        for (auto &v : rule_votes[r]) {
+            const int c = v.second / 2;
+            const bool pl = v.second & 1;
+            const std::string src = v.first.j ? "L" + std::to_string(r) + "_" + std::to_string(v.first.j) : M;
+            const std::string t = v.first.i ? "DPP_SHR(" + src + ", " + std::to_string(v.first.i) + ")" : src;
+            o << (pl ? "PL" : "MI") << c << " |= " << t << ";\n";
+        }
+        o << "}\n";
+    }
+    std::vector<int> both;
+    for (int c = 0; c < C; ++c)
+        if (!plus[c].empty() && !minus[c].empty()) both.push_back(c);
+    for (int c = 0; c < C; ++c)
+        if (!plus[c].empty() || !minus[c].empty())
+            o << "u32 N" << c << " = (p[" << c << "] | PL" << c << ") & ~MI" << c << ";\n";
+
+    // votes, exact path: some cell of the wave got votes of both signs
+    if (!both.empty()) {
+        o << "u32 CF = 0u;\n";
+        for (int c : both) o << "CF |= PL" << c << " & MI" << c << ";\n";
+        o << "if (ANY(CF)) {\n";
+        std::set<std::pair<int, int>> shifts;
+        std::set<std::tuple<int, int, int>> terms;
+        for (int c : both)
+            for (auto *lst : {&plus[c], &minus[c]})
+                for (const Vote &v : *lst) {
+                    if (v.j) shifts.insert({v.r, v.j});
+                    terms.insert({v.r, v.i, v.j});
+                }
+        for (auto &s : shifts)
+            o << "const u32 E" << s.first << "_" << s.second << " = M" << s.first << " << " << s.second << ";\n";
+        auto tname = [](int r, int i, int j) {
+            return "T" + std::to_string(r) + "_" + std::to_string(i) + "_" + std::to_string(j);
+        };
+        for (auto &t : terms) {
+            const int r = std::get<0>(t), i = std::get<1>(t), j = std::get<2>(t);
+            const std::string src = j ? "E" + std::to_string(r) + "_" + std::to_string(j) : "M" + std::to_string(r);
+            o << "const u32 " << tname(r, i, j) << " = "
+              << (i ? "DPP_SHR(" + src + ", " + std::to_string(i) + ")" : src) << ";\n";
+        }
+        for (int c : both) {
+            std::vector<std::string> pt{"p[" + std::to_string(c) + "]"}, mt;
+            for (const Vote &v : plus[c]) pt.push_back(tname(v.r, v.i, v.j));
+            for (const Vote &v : minus[c]) mt.push_back(tname(v.r, v.i, v.j));
+            o << "{ // channel " << c << ": " << pt.size() - 1 << " + votes, " << mt.size() << " - votes\n";
+            const std::vector<std::string> P = g.count(pt), Nn = g.count(mt);
+            const size_t K = std::max(P.size(), Nn.size());
+            o << "u32 GT = 0u, EQ = 0xFFFFFFFFu;\n";
+            for (size_t k = K; k-- > 0;) {
+                const std::string pk = k < P.size() ? P[k] : "0u", nk = k < Nn.size() ? Nn[k] : "0u";
+                o << "GT |= EQ & " << pk << " & ~" << nk << ";\n";
+                o << "EQ &= ~(" << pk << " ^ " << nk << ");\n";
+            }
+            o << "N" << c << " = GT;\n}\n";
+        }
+        o << "}\n";
+    }
+    for (int c = 0; c < C; ++c)
+        if (!plus[c].empty() || !minus[c].empty()) o << "p[" << c << "] = N" << c << ";\n";
+    o << "(void)F;\n";
+    return o.str();
+}
+
+void lane16_compile(const std::vector<std::vector<Lane16Rule>> &sets, int C, int H, int W, int L,
+                    Lane16Program &p) {
+    std::string src = kLane16Template;
+    std::ostringstream d;
+    d << "#define AV_C " << C << "\n#define AV_H " << H << "\n#define AV_W " << W << "\n#define AV_L "
+      << L << "\n";
+    auto put = [&](const std::string &marker, const std::string &text) {
+        const size_t at = src.find(marker);
+        if (at != std::string::npos) src.replace(at, marker.size(), text);
+    };
+    put("/*@DEFINES@*/", d.str());
+    put("/*@RULES@*/", lane16_rules_body(C, H, W, sets.at(0)));
+    p.source = std::move(src);
+}
+
+namespace {
+std::mutex g_mu;
+std::map<std::string, hipFunction_t> g_cache;   // (device, source) -> kernel; kept for the process
+}  // namespace
+
+hipError_t lane16_upload(const Lane16Program &p, Lane16Device &d, std::string *log) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    const std::string key = std::to_string(dev) + '\n' + p.source;
+    std::lock_guard<std::mutex> lock(g_mu);
+    auto it = g_cache.find(key);
+    if (it != g_cache.end()) {
+        d.fn = it->second;
+        return hipSuccess;
+    }
+    hiprtcProgram prog;
+    if (hiprtcCreateProgram(&prog, p.source.c_str(), "av_lane16.hip", 0, nullptr, nullptr) !=
+        HIPRTC_SUCCESS)
+        return hipErrorInvalidValue;
+    const char *opts[] = {"--offload-arch=gfx950", "-O3", "-std=c++17", "-Xclang", "-target-feature",
+                          "-Xclang", "-packed-fp32-ops"};
+    const hiprtcResult rc = hiprtcCompileProgram(prog, int(sizeof opts / sizeof opts[0]), opts);
+    if (rc != HIPRTC_SUCCESS) {
+        size_t n = 0;
+        hiprtcGetProgramLogSize(prog, &n);
+        std::string text(n, '\0');
+        if (n) hiprtcGetProgramLog(prog, &text[0]);
+        if (log) *log = std::string(hiprtcGetErrorString(rc)) + ": " + text;
+        hiprtcDestroyProgram(&prog);
+        return hipErrorInvalidKernelFile;
+    }
+    size_t n = 0;
+    hiprtcGetCodeSize(prog, &n);
+    std::vector<char> code(n);
+    hiprtcGetCode(prog, code.data());
+    hiprtcDestroyProgram(&prog);
+    hipModule_t mod;
+    e = hipModuleLoadData(&mod, code.data());
+    if (e != hipSuccess) return e;
+    hipFunction_t fn;
+    e = hipModuleGetFunction(&fn, mod, "av_lane16_step");
+    if (e != hipSuccess) return e;
+    g_cache[key] = fn;
+    d.fn = fn;
+    return hipSuccess;
+}
+
+hipError_t launch_lane16_step(const StepArgs &a, const Lane16Device &d, hipStream_t s) {
+    if (!d.fn) return hipErrorInvalidDeviceFunction;
+    const int waves = (a.B + 7) / 8;               // eight environments per wave
+    const unsigned blocks = unsigned((waves + 3) / 4);
+    void *state = a.state;
+    const void *init = a.init;
+    int *t = a.t;
+    const uint8_t *actions = a.actions;
+    float *rewards = a.rewards;
+    uint8_t *done = a.done;
+    int B = a.B, K = a.k;
+    void *args[] = {&state, &init, &t, &actions, &rewards, &done, &B, &K};
+    return hipModuleLaunchKernel(d.fn, blocks, 1, 1, 256, 1, 1, 0, s, args, nullptr);
+}
+
+}  // namespace av

@@ -1,0 +1,158 @@
+// lane16 step kernel: maps of at most 16 x 16 with one rule set shared by the batch.
+//
+// This file is the kernel's fixed part.  av_load_rules turns the rule set into straight-line
+// bit-sliced code (the body inserted at the RULES marker) and compiles the whole kernel for
+// gfx950 with hipRTC; the file also builds on its own, with no rules, as a syntax check.
+//
+// Layout on chip: a wave's four 16-lane DPP rows each hold one pair of environments; lane y
+// of a row holds map row y of both, environment 2p in bits 0-15 and 2p+1 in bits 16-31
+// (bit x = column x).  Every plane is one 32-bit register per lane.  Moving a plane up or
+// down by i rows is a DPP row shift, fused by the compiler into the consuming VALU op;
+// moving it by j columns is a shift of the register.  Rows H..15 and columns W..15 of each
+// half are kept zero.
+//
+// One step, per the paper (Sec. 2.1, Sec. 2.1.1, Sec. 2.2.1):
+//   force    F = the player plane moved one cell in each environment's action direction;
+//   rules    (generated) every rule is matched on the same map: the AND of its specified
+//            input entries, each a plane moved by the entry's offset, within the valid-anchor
+//            mask; votes of the matches are OR-ed per channel and sign; a wave whose cells
+//            got votes of both signs on some channel counts them exactly with carry-save
+//            adders; rewards are popcounts of the match masks times the rule rewards;
+//   done     no player bit left in the environment's half, or the counter reached L;
+//   reset    done environments reload their initial rows.
+#ifndef __HIPCC_RTC__
+#include <hip/hip_runtime.h>
+#endif
+
+/*@DEFINES@*/
+#ifndef AV_C
+#define AV_C 4
+#define AV_H 16
+#define AV_W 16
+#define AV_L 0
+#endif
+
+typedef unsigned int u32;
+
+#define AV_PLAYER 2
+// lane y <- lane y + i (row shift left), lane y <- lane y - i (row shift right), rotate
+#define DPP_SHL(x, i) ((u32)__builtin_amdgcn_update_dpp(0, (int)(x), 0x100 + (i), 0xF, 0xF, true))
+#define DPP_SHR(x, i) ((u32)__builtin_amdgcn_update_dpp(0, (int)(x), 0x110 + (i), 0xF, 0xF, true))
+#define DPP_ROR(x, i) (__builtin_amdgcn_update_dpp(0, (x), 0x120 + (i), 0xF, 0xF, true))
+#define ANY(x) (__builtin_amdgcn_ballot_w64((x) != 0u) != 0ull)
+#define COLMASK(k) ((k) >= 16 ? 0xFFFFu : ((1u << (k)) - 1u))
+#define BOTH(m) ((m) * 0x10001u)
+#define HALF(a, b) (((a) ? 0xFFFFu : 0u) | ((b) ? 0xFFFF0000u : 0u))
+
+extern "C" __global__ void __launch_bounds__(256)
+av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restrict__ init,
+               int *__restrict__ tctr, const unsigned char *__restrict__ actions,
+               float *__restrict__ rewards, unsigned char *__restrict__ done, int B, int K) {
+    const int lane = threadIdx.x & 63;
+    const int wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    const int y = lane & 15;
+    const int eA = 2 * (wave * 4 + (lane >> 4));
+    const int eB = eA + 1;
+    const bool hasA = eA < B, hasB = eB < B;
+    const bool rowok = y < AV_H;
+    const u32 CELL = rowok ? BOTH(COLMASK(AV_W)) : 0u;
+    const u32 RT_MASK = CELL & ~BOTH(1u);                      // column 0 receives nothing
+    const u32 LF_MASK = CELL & ~BOTH(1u << (AV_W - 1));        // column W-1 receives nothing
+
+    u32 p[AV_C];
+#pragma unroll
+    for (int c = 0; c < AV_C; ++c) {
+        const u32 lo = (hasA && rowok) ? u32(state[(size_t(c) * B + eA) * AV_H + y]) : 0u;
+        const u32 hi = (hasB && rowok) ? u32(state[(size_t(c) * B + eB) * AV_H + y]) : 0u;
+        p[c] = lo | (hi << 16);
+    }
+    int tA = hasA ? tctr[eA] : 0;
+    int tB = hasB ? tctr[eB] : 0;
+    u32 aA = (hasA && K > 0) ? u32(actions[eA]) : 0u;
+    u32 aB = (hasB && K > 0) ? u32(actions[eB]) : 0u;
+
+    for (int k = 0; k < K; ++k) {
+        // next step's actions, loaded early
+        u32 nA = 0u, nB = 0u;
+        if (k + 1 < K) {
+            nA = hasA ? u32(actions[size_t(k + 1) * B + eA]) : 0u;
+            nB = hasB ? u32(actions[size_t(k + 1) * B + eB]) : 0u;
+        }
+
+        // force tiles next to every player cell, toward each environment's action
+        u32 F;
+        {
+            const u32 P = p[AV_PLAYER];
+            u32 f = DPP_SHL(P, 1) & HALF(aA == 1u, aB == 1u);
+            f |= (P << 1) & RT_MASK & HALF(aA == 2u, aB == 2u);
+            f |= DPP_SHR(P, 1) & HALF(aA == 3u, aB == 3u);
+            f |= (P >> 1) & LF_MASK & HALF(aA == 4u, aB == 4u);
+            F = f & CELL;
+        }
+
+        int rA = 0, rB = 0;
+        /*@RULES@*/
+
+        // episode end: any player bit left in each half of this 16-lane row
+        u32 o = p[AV_PLAYER];
+        o |= (u32)DPP_ROR((int)o, 1);
+        o |= (u32)DPP_ROR((int)o, 2);
+        o |= (u32)DPP_ROR((int)o, 4);
+        o |= (u32)DPP_ROR((int)o, 8);
+        tA += 1;
+        tB += 1;
+        const bool dA = ((o & 0xFFFFu) == 0u) || (AV_L > 0 && tA == AV_L);
+        const bool dB = ((o >> 16) == 0u) || (AV_L > 0 && tB == AV_L);
+        if (dA) tA = 0;
+        if (dB) tB = 0;
+
+        // reward: sum of the row's 16 lanes
+        if (ANY(u32(rA | rB))) {
+            rA += DPP_ROR(rA, 1);
+            rA += DPP_ROR(rA, 2);
+            rA += DPP_ROR(rA, 4);
+            rA += DPP_ROR(rA, 8);
+            rB += DPP_ROR(rB, 1);
+            rB += DPP_ROR(rB, 2);
+            rB += DPP_ROR(rB, 4);
+            rB += DPP_ROR(rB, 8);
+        }
+        if (y == 0) {
+            if (hasA) {
+                rewards[size_t(k) * B + eA] = float(rA);
+                done[size_t(k) * B + eA] = (unsigned char)dA;
+            }
+            if (hasB) {
+                rewards[size_t(k) * B + eB] = float(rB);
+                done[size_t(k) * B + eB] = (unsigned char)dB;
+            }
+        }
+
+        // automatic reset to the initial map
+        if (ANY(u32(dA || dB))) {
+#pragma unroll
+            for (int c = 0; c < AV_C; ++c) {
+                u32 v = p[c];
+                if (dA)
+                    v = (v & 0xFFFF0000u) |
+                        ((hasA && rowok) ? u32(init[(size_t(c) * B + eA) * AV_H + y]) : 0u);
+                if (dB)
+                    v = (v & 0xFFFFu) |
+                        ((hasB && rowok) ? (u32(init[(size_t(c) * B + eB) * AV_H + y]) << 16) : 0u);
+                p[c] = v;
+            }
+        }
+        aA = nA;
+        aB = nB;
+    }
+
+#pragma unroll
+    for (int c = 0; c < AV_C; ++c) {
+        if (hasA && rowok) state[(size_t(c) * B + eA) * AV_H + y] = (unsigned short)(p[c] & 0xFFFFu);
+        if (hasB && rowok) state[(size_t(c) * B + eB) * AV_H + y] = (unsigned short)(p[c] >> 16);
+    }
+    if (y == 0) {
+        if (hasA) tctr[eA] = tA;
+        if (hasB) tctr[eB] = tB;
+    }
+}

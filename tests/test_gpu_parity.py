@@ -54,3 +54,35 @@ def test_step_n_matches_oracle(case, engine, variant):
     np.testing.assert_array_equal(r, want_r)
     np.testing.assert_array_equal(d, want_d)
     np.testing.assert_array_equal(final, want_m[-1])
+
+
+# Shapes that stress the row-per-lane engine's edges: odd B (a half-empty lane word),
+# maps narrower and shorter than 16, 1x1 up to 5x5 and 1x7 patterns, 2x2 maps.
+EDGE = {
+    "odd": inputs.Workload("odd", 31, B=77, H=5, W=11, C=5, R=6,
+                           shapes=((1, 1), (2, 3), (4, 4), (3, 2)), p_dc=0.5, per_env=False,
+                           T=30, L=7),
+    "wide": inputs.Workload("wide", 32, B=40, H=16, W=16, C=9, R=10, shapes=((5, 5), (1, 7)),
+                            p_dc=0.6, per_env=False, T=25, L=11),
+    "tiny": inputs.Workload("tiny", 33, B=3, H=2, W=2, C=4, R=2, shapes=((1, 1), (2, 2)),
+                            p_dc=0.4, per_env=False, T=20, L=0),
+    "tall": inputs.Workload("tall", 34, B=9, H=16, W=3, C=6, R=4, shapes=((3, 1), (16, 1)),
+                            p_dc=0.5, per_env=False, T=20, L=6),
+}
+
+
+@pytest.mark.parametrize("variant", inputs.VARIANTS)
+@pytest.mark.parametrize("engine", ["generic", "lane16"])
+@pytest.mark.parametrize("name", sorted(EDGE))
+def test_edge_shapes_match_oracle(name, engine, variant):
+    require_gpu()
+    wl = EDGE[name]
+    say(f"[parity edge] {name} engine={engine} variant={variant}")
+    maps, rules, actions = inputs.make_all(wl, 0, variant)
+    want_m, want_r, want_d = oracle.run(wl, maps, rules, actions, nthreads=8)
+    seq, final, r, d, eng = gpu_run(wl, maps, rules, actions, engine=engine, mode="step")
+    for t in range(wl.T):
+        assert first_mismatch(seq[t], want_m[t]) is None, \
+            f"maps differ at step {t}, index {first_mismatch(seq[t], want_m[t])}"
+        np.testing.assert_array_equal(r[t], want_r[t], err_msg=f"rewards, step {t}")
+        np.testing.assert_array_equal(d[t], want_d[t], err_msg=f"done, step {t}")
