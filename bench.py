@@ -27,8 +27,10 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 METRIC = "env-steps/sec and cell-rule-updates/sec at 1 MI355X; % of HBM roofline"
-KERNEL_SOURCES = ("paper_2407_04221_amd/csrc/k_generic.hip", "paper_2407_04221_amd/csrc/lane16.h",
-                  "paper_2407_04221_amd/csrc/k_lane16.hip")
+# the sources that determine the step kernels' code (the lane16 body is generated)
+KERNEL_SOURCES = ("paper_2407_04221_amd/csrc/k_generic.hip",
+                  "paper_2407_04221_amd/csrc/lane16_kernel.hip",
+                  "paper_2407_04221_amd/csrc/lane16_jit.cpp")
 
 
 def kernel_hash() -> str:
@@ -62,7 +64,7 @@ def measured_traffic(workload: str, engine: int):
 def cpu_baseline(wl, maps, rules, actions, budget_s: float, threads: int):
     import oracle
     from paper_2407_04221_amd import inputs
-    nb = min(wl.B, 1024)
+    nb = min(wl.B, 4096)
     envs = np.arange(nb)
     m, r, a = inputs.subset_envs(wl, maps, rules, actions, envs)
     o = oracle.Oracle.for_workload(wl, B=nb)
@@ -84,13 +86,17 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None, help="timed steps (default: workload T)")
-    ap.add_argument("--warmup", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=None,
+                    help="untimed steps before timing (default: one launch of --chunk steps)")
     ap.add_argument("--workload", default="c4")
     ap.add_argument("--variant", default="literal", choices=["literal", "planted", "dense"])
     ap.add_argument("--engine", default="auto", choices=["auto", "generic", "lane16"])
     ap.add_argument("--chunk", type=int, default=1000, help="steps per av_step_n launch")
-    ap.add_argument("--launch-steps", type=int, default=500,
-                    help="steps timed one launch per step (av_step); 0 = skip")
+    ap.add_argument("--launch-steps", type=int, default=0,
+                    help="also time this many steps with one launch per step (av_step)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="before timing, copy MIB MiB with a plain device copy (a known-size "
+                         "reference for the HBM byte counters)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
@@ -108,7 +114,16 @@ def main():
 
     wl = inputs.WORKLOADS[args.workload]
     T = wl.T if args.steps is None else args.steps
+    if args.warmup is None:
+        args.warmup = min(args.chunk, T)
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        n = args.copy_calibration << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     maps, rules, actions = inputs.make_all(wl, args.seed, args.variant, T=max(T, args.warmup, 1))
     acts = torch.from_numpy(actions).cuda()
     b = av.Batch.for_workload(wl, engine=args.engine)
