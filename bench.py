@@ -215,9 +215,16 @@ def main():
             "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
             "traffic": None if traffic is None else traffic["bytes_per_launch"],
-            "kernel": f"{engine_name}_step", "launch_ms": launch_ms,
+            "kernel": f"av_{engine_name}_step", "launch_ms": launch_ms,
             "algorithmic_bytes_per_env_step": A,
+            "note": "achieved = A x B x (steps per launch) / launch time, A = maps in and out "
+                    "once per step + action + reward + done; av_step_n keeps the maps on chip "
+                    "across the launch, so the HBM traffic actually moved is `traffic` and frac "
+                    "may exceed 1",
         },
+        "valu": None if traffic is None or "valu_busy" not in traffic else {
+            "busy": traffic["valu_busy"], "insts_per_wave_step": traffic["valu_insts_per_wave_step"],
+            "peak_lane_ops": 256 * 4 * 16 * 2.4e9, "source": traffic["source"]},
         "per_launch_path": per_launch,
         "cpu_baseline": cpu,
     }

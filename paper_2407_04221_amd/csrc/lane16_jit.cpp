@@ -161,47 +161,24 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
         return e.j ? "X" + std::to_string(e.c) + "_" + std::to_string(e.j) : plane(e.c, C);
     };
 
-    // match
-    for (int r = 0; r < R; ++r) {
-        const Lane16Rule &ru = rules[r];
-        const std::string M = "M" + std::to_string(r), f = "f" + std::to_string(r);
-        o << "u32 " << M << " = V" << ru.n << "_" << ru.m << ";\n";
-        const size_t probe = std::min<size_t>(2, ents[r].size());
-        for (size_t e = 0; e < probe; ++e) {
-            const Entry &en = ents[r][e];
-            const std::string t = en.i ? "DPP_SHL(" + base(en) + ", " + std::to_string(en.i) + ")" : base(en);
-            o << M << " &= " << (en.want ? "" : "~") << t << ";\n";
+    auto row_and = [&](const std::vector<Entry> &es) {
+        std::string q;
+        for (const Entry &en : es) {
+            if (!q.empty()) q += " & ";
+            q += (en.want ? "" : "~") + base(en);
         }
-        o << "bool " << f << " = ANY(" << M << ");\n";
-        if (ents[r].size() > probe) {
-            o << "if (" << f << ") {\n";
-            std::map<int, std::vector<Entry>> by_row;
-            for (size_t e = probe; e < ents[r].size(); ++e) by_row[ents[r][e].i].push_back(ents[r][e]);
-            for (auto &row : by_row) {
-                std::string q;
-                for (const Entry &en : row.second) {
-                    if (!q.empty()) q += " & ";
-                    q += (en.want ? "" : "~") + base(en);
-                }
-                if (row.first == 0) o << M << " &= " << q << ";\n";
-                else o << M << " &= DPP_SHL(" << q << ", " << row.first << ");\n";
-            }
-            o << f << " = ANY(" << M << ");\n";
-            o << "}\n";
+        return q;
+    };
+    auto emit_rows = [&](const std::string &M, const std::vector<Entry> &es) {
+        std::map<int, std::vector<Entry>> by_row;
+        for (const Entry &en : es) by_row[en.i].push_back(en);
+        for (auto &row : by_row) {
+            if (row.first == 0) o << M << " &= " << row_and(row.second) << ";\n";
+            else o << M << " &= DPP_SHL(" << row_and(row.second) << ", " << row.first << ");\n";
         }
-        if (ru.reward != 0)
-            o << "if (" << f << ") { rA += " << ru.reward << " * (int)__popc(" << M
-              << " & 0xFFFFu); rB += " << ru.reward << " * (int)__popc(" << M << " >> 16); }\n";
-    }
-
-    // votes, fast path: OR per channel and sign
-    for (int c = 0; c < C; ++c)
-        if (!plus[c].empty() || !minus[c].empty())
-            o << "u32 PL" << c << " = 0u, MI" << c << " = 0u;\n";
-    for (int r = 0; r < R; ++r) {
-        if (rule_votes[r].empty()) continue;
+    };
+    auto emit_votes = [&](int r) {
         const std::string M = "M" + std::to_string(r);
-        o << "if (f" << r << ") {\n";
         std::set<int> js;
         for (auto &v : rule_votes[r])
             if (v.first.j) js.insert(v.first.j);
@@ -212,6 +189,57 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
             const std::string src = v.first.j ? "L" + std::to_string(r) + "_" + std::to_string(v.first.j) : M;
             const std::string t = v.first.i ? "DPP_SHR(" + src + ", " + std::to_string(v.first.i) + ")" : src;
             o << (pl ? "PL" : "MI") << c << " |= " << t << ";\n";
+        }
+    };
+    auto emit_reward = [&](int r) {
+        const std::string M = "M" + std::to_string(r);
+        if (rules[r].reward != 0)
+            o << "rA += " << rules[r].reward << " * (int)__popc(" << M << " & 0xFFFFu); rB += "
+              << rules[r].reward << " * (int)__popc(" << M << " >> 16);\n";
+    };
+
+    // The built-in moves (rules 0..3) are cheap and fire in most waves: evaluated in full,
+    // without branches.  Loaded rules are probed with their two rarest entries; one
+    // wave-uniform test over all probes skips the rest when no anchor survives anywhere.
+    const int n_fixed = std::min(R, kMoveRules);
+    for (int r = 0; r < R; ++r) {
+        const Lane16Rule &ru = rules[r];
+        const std::string M = "M" + std::to_string(r);
+        o << "u32 " << M << " = V" << ru.n << "_" << ru.m << ";\n";
+        if (r < n_fixed) {
+            emit_rows(M, ents[r]);
+            continue;
+        }
+        const size_t probe = std::min<size_t>(2, ents[r].size());
+        for (size_t e = 0; e < probe; ++e) {
+            const Entry &en = ents[r][e];
+            const std::string t = en.i ? "DPP_SHL(" + base(en) + ", " + std::to_string(en.i) + ")" : base(en);
+            o << M << " &= " << (en.want ? "" : "~") << t << ";\n";
+        }
+    }
+    for (int c = 0; c < C; ++c)
+        if (!plus[c].empty() || !minus[c].empty())
+            o << "u32 PL" << c << " = 0u, MI" << c << " = 0u;\n";
+    for (int r = 0; r < n_fixed; ++r) {
+        emit_reward(r);
+        emit_votes(r);
+    }
+    if (R > n_fixed) {
+        o << "if (ANY(";
+        for (int r = n_fixed; r < R; ++r) o << (r > n_fixed ? " | " : "") << "M" << r;
+        o << ")) {\n";
+        for (int r = n_fixed; r < R; ++r) {
+            const std::string M = "M" + std::to_string(r);
+            const size_t probe = std::min<size_t>(2, ents[r].size());
+            o << "if (ANY(" << M << ")) {\n";
+            if (ents[r].size() > probe) {
+                emit_rows(M, std::vector<Entry>(ents[r].begin() + probe, ents[r].end()));
+                o << "if (ANY(" << M << ")) {\n";
+            }
+            emit_reward(r);
+            emit_votes(r);
+            if (ents[r].size() > probe) o << "}\n";
+            o << "}\n";
         }
         o << "}\n";
     }
@@ -275,6 +303,9 @@ void lane16_compile(const std::vector<std::vector<Lane16Rule>> &sets, int C, int
     std::ostringstream d;
     d << "#define AV_C " << C << "\n#define AV_H " << H << "\n#define AV_W " << W << "\n#define AV_L "
       << L << "\n";
+    bool pays = false;
+    for (const Lane16Rule &r : sets.at(0)) pays |= r.reward != 0;
+    if (!pays) d << "#define AV_NO_REWARD 1\n";
     auto put = [&](const std::string &marker, const std::string &text) {
         const size_t at = src.find(marker);
         if (at != std::string::npos) src.replace(at, marker.size(), text);

@@ -11,6 +11,10 @@
 // moving it by j columns is a shift of the register.  Rows H..15 and columns W..15 of each
 // half are kept zero.
 //
+// Environments of a wave that do not exist (B not a multiple of 8) compute on zero rows and
+// are never stored.  The initial rows stay in registers for resets; actions are fetched 16
+// steps at a time and broadcast per step across each row with ds_bpermute.
+//
 // One step, per the paper (Sec. 2.1, Sec. 2.1.1, Sec. 2.2.1):
 //   force    F = the player plane moved one cell in each environment's action direction;
 //   rules    (generated) every rule is matched on the same map: the AND of its specified
@@ -58,26 +62,44 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
     const u32 CELL = rowok ? BOTH(COLMASK(AV_W)) : 0u;
     const u32 RT_MASK = CELL & ~BOTH(1u);                      // column 0 receives nothing
     const u32 LF_MASK = CELL & ~BOTH(1u << (AV_W - 1));        // column W-1 receives nothing
+    // safe (clamped) environment indices for loads; values of absent envs are masked off
+    const int iA = hasA ? eA : 0, iB = hasB ? eB : 0;
 
-    u32 p[AV_C];
+    u32 p[AV_C], q[AV_C];   // current rows, initial rows (kept for automatic resets)
 #pragma unroll
     for (int c = 0; c < AV_C; ++c) {
-        const u32 lo = (hasA && rowok) ? u32(state[(size_t(c) * B + eA) * AV_H + y]) : 0u;
-        const u32 hi = (hasB && rowok) ? u32(state[(size_t(c) * B + eB) * AV_H + y]) : 0u;
-        p[c] = lo | (hi << 16);
+        const size_t row = size_t(c) * B;
+        const int yy = rowok ? y : 0;
+        const u32 lo = u32(state[(row + iA) * AV_H + yy]);
+        const u32 hi = u32(state[(row + iB) * AV_H + yy]);
+        const u32 ilo = u32(init[(row + iA) * AV_H + yy]);
+        const u32 ihi = u32(init[(row + iB) * AV_H + yy]);
+        const u32 keep = HALF(hasA && rowok, hasB && rowok);
+        p[c] = (lo | (hi << 16)) & keep;
+        q[c] = (ilo | (ihi << 16)) & keep;
     }
-    int tA = hasA ? tctr[eA] : 0;
-    int tB = hasB ? tctr[eB] : 0;
-    u32 aA = (hasA && K > 0) ? u32(actions[eA]) : 0u;
-    u32 aB = (hasB && K > 0) ? u32(actions[eB]) : 0u;
+    int tA = tctr[iA], tB = tctr[iB];
+
+    // Actions arrive 16 steps at a time: lane y of a row holds step k0 + y of its pair
+    // (env A in byte 0, env B in byte 1); each step reads its entry across the row.
+    auto load_block = [&](int k0) -> u32 {
+        const int k = k0 + y;
+        if (k >= K) return 0u;
+        const unsigned char *row = actions + size_t(k) * B;
+        return (hasA ? u32(row[iA]) : 0u) | (hasB ? (u32(row[iB]) << 8) : 0u);
+    };
+    u32 ablk = load_block(0);
+    u32 anext = load_block(16);
+    const int src_base = (lane & 48) << 2;
 
     for (int k = 0; k < K; ++k) {
-        // next step's actions, loaded early
-        u32 nA = 0u, nB = 0u;
-        if (k + 1 < K) {
-            nA = hasA ? u32(actions[size_t(k + 1) * B + eA]) : 0u;
-            nB = hasB ? u32(actions[size_t(k + 1) * B + eB]) : 0u;
+        const int s = k & 15;
+        if (s == 0 && k > 0) {
+            ablk = anext;
+            anext = load_block(k + 16);
         }
+        const u32 act = u32(__builtin_amdgcn_ds_bpermute(src_base + (s << 2), int(ablk)));
+        const u32 aA = act & 0xFFu, aB = act >> 8;
 
         // force tiles next to every player cell, toward each environment's action
         u32 F;
@@ -106,6 +128,7 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
         if (dA) tA = 0;
         if (dB) tB = 0;
 
+#ifndef AV_NO_REWARD
         // reward: sum of the row's 16 lanes
         if (ANY(u32(rA | rB))) {
             rA += DPP_ROR(rA, 1);
@@ -117,33 +140,20 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
             rB += DPP_ROR(rB, 4);
             rB += DPP_ROR(rB, 8);
         }
-        if (y == 0) {
-            if (hasA) {
-                rewards[size_t(k) * B + eA] = float(rA);
-                done[size_t(k) * B + eA] = (unsigned char)dA;
-            }
-            if (hasB) {
-                rewards[size_t(k) * B + eB] = float(rB);
-                done[size_t(k) * B + eB] = (unsigned char)dB;
-            }
+#endif
+        // lane 0 of the row reports env A, lane 1 env B
+        if (y < 2 && (y ? hasB : hasA)) {
+            const int e = y ? eB : eA;
+            rewards[size_t(k) * B + e] = float(y ? rB : rA);
+            done[size_t(k) * B + e] = (unsigned char)(y ? dB : dA);
         }
 
         // automatic reset to the initial map
         if (ANY(u32(dA || dB))) {
+            const u32 dm = HALF(dA, dB);
 #pragma unroll
-            for (int c = 0; c < AV_C; ++c) {
-                u32 v = p[c];
-                if (dA)
-                    v = (v & 0xFFFF0000u) |
-                        ((hasA && rowok) ? u32(init[(size_t(c) * B + eA) * AV_H + y]) : 0u);
-                if (dB)
-                    v = (v & 0xFFFFu) |
-                        ((hasB && rowok) ? (u32(init[(size_t(c) * B + eB) * AV_H + y]) << 16) : 0u);
-                p[c] = v;
-            }
+            for (int c = 0; c < AV_C; ++c) p[c] = (q[c] & dm) | (p[c] & ~dm);
         }
-        aA = nA;
-        aB = nB;
     }
 
 #pragma unroll
