@@ -1,0 +1,95 @@
+"""GPU vs oracle on the limits and degenerate cases: the most channels, a pattern as large
+as the map, one-row and one-column maps, rules with no specified input entry, many rules,
+no loaded rules, a single environment, 33- and 64-wide maps, out-of-range action values.
+Maps, rewards and done flags are compared after every step."""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import first_mismatch, gpu_run, require_gpu, say
+from paper_2407_04221_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def W_(name, cid, **kw):
+    base = dict(per_env=False, T=12, L=5, p_dc=0.5)
+    base.update(kw)
+    return inputs.Workload(name, cid, **base)
+
+
+CASES = {
+    "channels31": W_("channels31", 41, B=37, H=16, W=16, C=31, R=10, shapes=((4, 4), (1, 1))),
+    "pattern_is_map": W_("pattern_is_map", 42, B=21, H=16, W=16, C=8, R=2, shapes=((16, 16),)),
+    "pattern_is_map8": W_("pattern_is_map8", 43, B=9, H=8, W=8, C=4, R=3, shapes=((8, 8), (8, 1))),
+    "one_row": W_("one_row", 44, B=19, H=1, W=16, C=5, R=4, shapes=((1, 1), (1, 3))),
+    "one_col": W_("one_col", 45, B=19, H=16, W=1, C=5, R=4, shapes=((1, 1), (3, 1))),
+    "many_rules": W_("many_rules", 46, B=30, H=16, W=16, C=6, R=60, shapes=((3, 3), (2, 5)),
+                     T=6),
+    "one_env": W_("one_env", 47, B=1, H=11, W=7, C=4, R=5, shapes=((2, 2), (1, 3))),
+    "wide33": W_("wide33", 48, B=6, H=33, W=33, C=6, R=6, shapes=((3, 3), (1, 4)), T=8),
+    "big64": W_("big64", 49, B=3, H=64, W=64, C=20, R=40, shapes=((5, 5), (2, 3)), T=4),
+    "per_env_small": W_("per_env_small", 50, B=13, H=10, W=12, C=5, R=5,
+                        shapes=((3, 3), (1, 2)), per_env=True),
+}
+LANE16 = {n for n, w in CASES.items() if w.H <= 16 and w.W <= 16 and not w.per_env}
+
+
+def engines(name):
+    return ["generic", "lane16"] if name in LANE16 else ["generic"]
+
+
+def check(wl, maps, rules, actions, engine):
+    want_m, want_r, want_d = oracle.run(wl, maps, rules, actions, nthreads=8)
+    seq, final, r, d, eng = gpu_run(wl, maps, rules, actions, engine=engine, mode="step")
+    for t in range(actions.shape[0]):
+        assert first_mismatch(seq[t], want_m[t]) is None, \
+            f"maps differ at step {t}, index {first_mismatch(seq[t], want_m[t])}"
+        np.testing.assert_array_equal(r[t], want_r[t], err_msg=f"rewards, step {t}")
+        np.testing.assert_array_equal(d[t], want_d[t], err_msg=f"done, step {t}")
+    return want_r
+
+
+@pytest.mark.parametrize("variant", ["literal", "planted", "dense"])
+@pytest.mark.parametrize("name,engine", [(n, e) for n in sorted(CASES) for e in engines(n)])
+def test_edge_case(name, engine, variant):
+    require_gpu()
+    wl = CASES[name]
+    say(f"[edge] {name} engine={engine} variant={variant}")
+    maps, rules, actions = inputs.make_all(wl, 0, variant)
+    check(wl, maps, rules, actions, engine)
+
+
+@pytest.mark.parametrize("engine", ["generic", "lane16"])
+def test_rules_with_no_specified_input(engine):
+    """An all-don't-care input matches at every anchor (the paper's empty "no-op" rules,
+    Sec. 2.2.1); with outputs it writes everywhere, with heavily overlapping votes."""
+    require_gpu()
+    wl = W_("dc", 51, B=17, H=9, W=14, C=5, R=3, shapes=((2, 3), (1, 1), (3, 2)), T=6)
+    maps, (shape, ip, op, rw), actions = inputs.make_all(wl, 0, "dense")
+    ip[:] = -1
+    op[:, 1] = -1                 # rule 1 matches everywhere and changes nothing
+    rw[:] = (1, 1, -1)
+    r = check(wl, maps, (shape, ip, op, rw), actions, engine)
+    assert (r != 0).all()
+
+
+@pytest.mark.parametrize("engine", ["generic", "lane16"])
+def test_no_loaded_rules(engine):
+    require_gpu()
+    wl = W_("moves", 52, B=41, H=13, W=16, C=4, R=0, shapes=((1, 1),), T=30, L=0)
+    maps = inputs.make_maps(wl, 0)
+    actions = inputs.make_actions(wl, 0)
+    empty = (np.zeros((1, 0, 2), np.int32), np.zeros((1, 0, 5, 1, 1), np.int8),
+             np.zeros((1, 0, 5, 1, 1), np.int8), np.zeros((1, 0), np.int32))
+    check(wl, maps, empty, actions, engine)
+
+
+@pytest.mark.parametrize("engine", ["generic", "lane16"])
+def test_out_of_range_actions_are_no_ops(engine):
+    require_gpu()
+    wl = W_("acts", 53, B=24, H=8, W=8, C=4, R=2, shapes=((1, 2),), T=10)
+    maps, rules, _ = inputs.make_all(wl, 0, "planted")
+    actions = np.random.default_rng(5).integers(0, 256, size=(wl.T, wl.B)).astype(np.uint8)
+    actions[:, ::3] = 0
+    check(wl, maps, rules, actions, engine)
