@@ -29,6 +29,7 @@ HBM_PEAK_GBS = 8000.0
 METRIC = "env-steps/sec and cell-rule-updates/sec at 1 MI355X; % of HBM roofline"
 # the sources that determine the step kernels' code (the lane16 body is generated)
 KERNEL_SOURCES = ("paper_2407_04221_amd/csrc/k_generic.hip",
+                  "paper_2407_04221_amd/csrc/k_wave.hip",
                   "paper_2407_04221_amd/csrc/lane16_kernel.hip",
                   "paper_2407_04221_amd/csrc/lane16_jit.cpp")
 
@@ -90,7 +91,7 @@ def main():
                     help="untimed steps before timing (default: one launch of --chunk steps)")
     ap.add_argument("--workload", default="c4")
     ap.add_argument("--variant", default="literal", choices=["literal", "planted", "dense"])
-    ap.add_argument("--engine", default="auto", choices=["auto", "generic", "lane16"])
+    ap.add_argument("--engine", default="auto", choices=["auto", "generic", "lane16", "wave"])
     ap.add_argument("--chunk", type=int, default=1000, help="steps per av_step_n launch")
     ap.add_argument("--launch-steps", type=int, default=0,
                     help="also time this many steps with one launch per step (av_step)")
@@ -130,7 +131,7 @@ def main():
     b.load_rules(*rules)
     b.reset(maps)
     engine = b.info["engine"]
-    engine_name = {1: "generic", 2: "lane16"}[engine]
+    engine_name = av.ENGINE_NAMES[engine]
     chunk = max(1, min(args.chunk, T))
     rew = torch.empty((chunk, wl.B), dtype=torch.float32, device="cuda")
     don = torch.empty((chunk, wl.B), dtype=torch.uint8, device="cuda")

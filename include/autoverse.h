@@ -56,12 +56,17 @@ typedef enum {
     AV_ESTATE = 4    /* call out of order, e.g. av_step before av_load_rules and av_reset */
 } av_status;
 
-/* Kernel family used by av_step / av_step_n.  AUTO picks the fastest eligible one. */
+/* Kernel family used by av_step / av_step_n.  AUTO picks lane16 when eligible, else wave
+ * when its LDS working set (C + 1 padded planes, one match plane per rule, two vote
+ * accumulators per stored channel) fits in 64 KiB, else generic. */
 typedef enum {
     AV_ENGINE_AUTO = 0,
     AV_ENGINE_GENERIC = 1,  /* any size within the limits below; maps staged in LDS */
-    AV_ENGINE_LANE16 = 2    /* maps of at most 16 x 16: one map row per lane, two maps per
-                               32-bit lane word, rows shifted across lanes with DPP */
+    AV_ENGINE_LANE16 = 2,   /* maps of at most 16 x 16 and one shared rule set: one map
+                               row per lane, two maps per 32-bit lane word, rows shifted
+                               across lanes with DPP, the rule set compiled into the kernel */
+    AV_ENGINE_WAVE = 3      /* one environment per 64-lane wave, map rows in LDS; rule
+                               programs read with scalar loads (per-environment rules) */
 } av_engine;
 
 typedef struct {

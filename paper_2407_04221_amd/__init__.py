@@ -18,8 +18,10 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libautoverse.so")
 
 AV_OK, AV_EINVAL, AV_ENOMEM, AV_EDEVICE, AV_ESTATE = 0, 1, 2, 3, 4
-AV_ENGINE_AUTO, AV_ENGINE_GENERIC, AV_ENGINE_LANE16 = 0, 1, 2
-ENGINES = {"auto": AV_ENGINE_AUTO, "generic": AV_ENGINE_GENERIC, "lane16": AV_ENGINE_LANE16}
+AV_ENGINE_AUTO, AV_ENGINE_GENERIC, AV_ENGINE_LANE16, AV_ENGINE_WAVE = 0, 1, 2, 3
+ENGINES = {"auto": AV_ENGINE_AUTO, "generic": AV_ENGINE_GENERIC, "lane16": AV_ENGINE_LANE16,
+           "wave": AV_ENGINE_WAVE}
+ENGINE_NAMES = {v: k for k, v in ENGINES.items()}
 
 # Every symbol include/autoverse.h declares.
 ABI_SYMBOLS = ("av_create_batch", "av_load_rules", "av_reset", "av_step", "av_step_n",

@@ -79,6 +79,7 @@ void free_device_program(av_batch_t b) {
     dev_free(b->dprog.votes);
     dev_free(b->dprog.match);
     dev_free(b->dprog.vote);
+    dev_free(b->dprog.rvote);
     b->dprog = DeviceProgram{};
     lane16_free(b->dlprog);
 }
@@ -140,9 +141,10 @@ int entry_rank(int c, int want, int C) {
 
 void compile_generic(const std::vector<std::vector<HostRule>> &sets, int C, GenericProgram &p) {
     const int C1 = C + 1;
+    p.any_reward = 0;
     p.sets = int(sets.size());
     p.rules_per_set = int(sets[0].size());
-    std::vector<std::vector<uint32_t>> match(sets.size()), vote(sets.size());
+    std::vector<std::vector<uint32_t>> match(sets.size()), vote(sets.size()), rvote(sets.size());
     p.hdr.assign(size_t(p.sets) * p.rules_per_set, RuleHdr{});
     p.votes.assign(size_t(p.sets) * C1, VoteList{});
     for (size_t s = 0; s < sets.size(); ++s) {
@@ -161,6 +163,15 @@ void compile_generic(const std::vector<std::vector<HostRule>> &sets, int C, Gene
                         const int k = kout(w, hr.at(hr.out, c, i, j));
                         if (k) per_ch[c].push_back(pack_vote(r, i, j, k > 0));
                     }
+            h.vote_off = int(rvote[s].size());
+            for (int c = 0; c < C; ++c)           // the force plane's votes are never used
+                for (int i = 0; i < hr.n; ++i)
+                    for (int j = 0; j < hr.m; ++j) {
+                        const int k = kout(hr.at(hr.in, c, i, j), hr.at(hr.out, c, i, j));
+                        if (k) rvote[s].push_back(pack_vote(c, i, j, k > 0));
+                    }
+            h.vote_cnt = int(rvote[s].size()) - h.vote_off;
+            if (hr.reward != 0) p.any_reward = 1;
             std::stable_sort(ents.begin(), ents.end(),
                              [](auto &a, auto &b) { return a.first < b.first; });
             for (auto &e : ents) match[s].push_back(e.second);
@@ -173,10 +184,15 @@ void compile_generic(const std::vector<std::vector<HostRule>> &sets, int C, Gene
     }
     p.match_stride = 1;
     p.vote_stride = 1;
+    p.rvote_stride = 1;
     for (size_t s = 0; s < sets.size(); ++s) {
         p.match_stride = std::max(p.match_stride, int(match[s].size()));
         p.vote_stride = std::max(p.vote_stride, int(vote[s].size()));
+        p.rvote_stride = std::max(p.rvote_stride, int(rvote[s].size()));
     }
+    p.rvote.assign(size_t(p.sets) * p.rvote_stride, 0);
+    for (size_t s = 0; s < sets.size(); ++s)
+        std::copy(rvote[s].begin(), rvote[s].end(), p.rvote.begin() + s * p.rvote_stride);
     p.match.assign(size_t(p.sets) * p.match_stride, 0);
     p.vote.assign(size_t(p.sets) * p.vote_stride, 0);
     for (size_t s = 0; s < sets.size(); ++s) {
@@ -228,7 +244,7 @@ av_status av_create_batch(const av_config *cfg, av_batch_t *out) {
     if (c.per_env_rules != 0 && c.per_env_rules != 1)
         return fail(AV_EINVAL, "per_env_rules must be 0 or 1");
     if (c.max_episode_steps < 0) return fail(AV_EINVAL, "max_episode_steps must be >= 0");
-    if (c.engine < AV_ENGINE_AUTO || c.engine > AV_ENGINE_LANE16)
+    if (c.engine < AV_ENGINE_AUTO || c.engine > AV_ENGINE_WAVE)
         return fail(AV_EINVAL, "unknown engine %d", c.engine);
     const size_t env_lds = generic_env_lds_bytes(c.height, c.width, c.channels,
                                                  c.max_rules + kMoveRules);
@@ -239,6 +255,11 @@ av_status av_create_batch(const av_config *cfg, av_batch_t *out) {
     if (c.engine == AV_ENGINE_LANE16 && !lane16_ok)
         return fail(AV_EINVAL, "the lane16 engine needs H, W <= 16 and one rule set shared "
                     "by all environments");
+    const size_t wave_lds = wave_lds_bytes(c.height, c.width, c.channels, c.max_rules + kMoveRules);
+    const bool wave_ok = wave_lds <= size_t(kLdsBudget);
+    if (c.engine == AV_ENGINE_WAVE && !wave_ok)
+        return fail(AV_EINVAL, "the wave engine needs %zu bytes of LDS (limit %d)", wave_lds,
+                    kLdsBudget);
 
     int dev_count = 0;
     AV_HIP(hipGetDeviceCount(&dev_count));
@@ -253,7 +274,8 @@ av_status av_create_batch(const av_config *cfg, av_batch_t *out) {
     b->row_bytes = c.width <= 16 ? 2 : (c.width <= 32 ? 4 : 8);
     b->state_bytes = size_t(c.channels) * c.num_envs * c.height * b->row_bytes;
     b->envs_per_block = std::max(1, std::min(256 / c.height, int(kLdsBudget / env_lds)));
-    b->engine = (c.engine == AV_ENGINE_GENERIC || !lane16_ok) ? AV_ENGINE_GENERIC : AV_ENGINE_LANE16;
+    if (c.engine != AV_ENGINE_AUTO) b->engine = c.engine;
+    else b->engine = lane16_ok ? AV_ENGINE_LANE16 : (wave_ok ? AV_ENGINE_WAVE : AV_ENGINE_GENERIC);
     hipError_t e = hipMalloc(&b->d_state, b->state_bytes);
     if (e == hipSuccess) e = hipMalloc(&b->d_init, b->state_bytes);
     if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&b->d_t), sizeof(int32_t) * c.num_envs);
@@ -327,9 +349,12 @@ av_status av_load_rules(av_batch_t b, int32_t R, const int32_t *shape, const int
     if (av_status st = upload(&b->dprog.votes, b->prog.votes)) return st;
     if (av_status st = upload(&b->dprog.match, b->prog.match)) return st;
     if (av_status st = upload(&b->dprog.vote, b->prog.vote)) return st;
+    if (av_status st = upload(&b->dprog.rvote, b->prog.rvote)) return st;
     b->dprog.rules_per_set = b->prog.rules_per_set;
     b->dprog.match_stride = b->prog.match_stride;
     b->dprog.vote_stride = b->prog.vote_stride;
+    b->dprog.rvote_stride = b->prog.rvote_stride;
+    b->dprog.any_reward = b->prog.any_reward;
     if (b->engine == AV_ENGINE_LANE16) {
         std::vector<std::vector<Lane16Rule>> lsets(S);
         for (int s = 0; s < S; ++s)
@@ -381,6 +406,8 @@ static av_status step_k(av_batch_t b, int32_t k, const uint8_t *actions, float *
     a.prog = b->dprog;
     if (b->engine == AV_ENGINE_LANE16)
         AV_HIP(launch_lane16_step(a, b->dlprog, b->stream));
+    else if (b->engine == AV_ENGINE_WAVE)
+        AV_HIP(launch_wave_step(a, b->stream));
     else
         AV_HIP(launch_generic_step(a, b->envs_per_block, b->stream));
     return AV_OK;

@@ -27,13 +27,18 @@ constexpr int kLdsBudget = 64 * 1024;
 //
 // Match entry (one specified input entry): bits 0-7 channel, 8-15 row i, 16-23 col j,
 // bit 24 wanted value.  Vote entry (one nonzero K_O entry), grouped by channel:
-// bits 0-7 rule, 8-15 row i, 16-23 col j, bit 24 set when the vote is +1.
+// bits 0-7 rule, 8-15 row i, 16-23 col j, bit 24 set when the vote is +1.  Rule-major
+// vote entry (the same votes grouped by rule, force plane left out because it is dropped
+// after the step): bits 0-7 channel, 8-15 row i, 16-23 col j, bit 24 set for +1.
 // ---------------------------------------------------------------------------------
 struct RuleHdr {
     int32_t n, m;         // pattern rows, cols
     int32_t reward;
     int32_t match_off;    // into the set's match entries
     int32_t match_cnt;
+    int32_t vote_off;     // into the set's rule-major vote entries (stored channels only)
+    int32_t vote_cnt;
+    int32_t pad;
 };
 
 struct VoteList {
@@ -45,10 +50,13 @@ struct GenericProgram {
     int32_t sets = 0;                 // S
     int32_t match_stride = 0;         // match entries per set (max over sets)
     int32_t vote_stride = 0;          // vote entries per set (max over sets)
+    int32_t any_reward = 0;
     std::vector<RuleHdr> hdr;         // [S][R+4]
     std::vector<VoteList> votes;      // [S][C+1]
     std::vector<uint32_t> match;      // [S][match_stride]
     std::vector<uint32_t> vote;       // [S][vote_stride]
+    int32_t rvote_stride = 0;         // rule-major vote entries per set (max over sets)
+    std::vector<uint32_t> rvote;      // [S][rvote_stride]
 };
 
 inline uint32_t pack_match(int c, int i, int j, int want) {
@@ -64,7 +72,9 @@ struct DeviceProgram {
     VoteList *votes = nullptr;
     uint32_t *match = nullptr;
     uint32_t *vote = nullptr;
-    int32_t rules_per_set = 0, match_stride = 0, vote_stride = 0;
+    uint32_t *rvote = nullptr;
+    int32_t rules_per_set = 0, match_stride = 0, vote_stride = 0, rvote_stride = 0;
+    int32_t any_reward = 0;           // some rule of some set pays a nonzero reward
 };
 
 // Everything a step kernel needs, passed by value.
@@ -89,5 +99,9 @@ hipError_t launch_unpack(const void *src, uint8_t *dst, int B, int C, int H, int
                          int row_bytes, hipStream_t s);
 hipError_t launch_generic_step(const StepArgs &a, int envs_per_block, hipStream_t s);
 size_t generic_env_lds_bytes(int H, int W, int C, int rules_per_set);
+
+// The wave engine (k_wave.hip): one environment per 64-lane workgroup.
+size_t wave_lds_bytes(int H, int W, int C, int rules_per_set);
+hipError_t launch_wave_step(const StepArgs &a, hipStream_t s);
 
 }  // namespace av

@@ -64,8 +64,10 @@ def _cfg(**kw):
     dict(num_envs=0), dict(height=0), dict(width=65), dict(height=65), dict(channels=3),
     dict(channels=32), dict(max_rules=-1), dict(max_rules=253), dict(max_pat_h=0),
     dict(max_pat_w=17), dict(per_env_rules=2), dict(max_episode_steps=-1), dict(engine=9),
-    # lane16 needs maps of at most 16 x 16
-    dict(engine=2, height=32, width=32),
+    # lane16 needs maps of at most 16 x 16 and one shared rule set
+    dict(engine=2, height=32, width=32), dict(engine=2, per_env_rules=1),
+    # the wave engine's LDS working set over 64 KiB (the generic engine's fits)
+    dict(engine=3, channels=31, max_rules=140),
     # one environment's LDS working set over 64 KiB
     dict(height=64, width=64, channels=31, max_rules=252),
 ])

@@ -36,7 +36,7 @@ LANE16 = {n for n, w in CASES.items() if w.H <= 16 and w.W <= 16 and not w.per_e
 
 
 def engines(name):
-    return ["generic", "lane16"] if name in LANE16 else ["generic"]
+    return ["generic", "wave", "lane16"] if name in LANE16 else ["generic", "wave"]
 
 
 def check(wl, maps, rules, actions, engine):
@@ -60,7 +60,7 @@ def test_edge_case(name, engine, variant):
     check(wl, maps, rules, actions, engine)
 
 
-@pytest.mark.parametrize("engine", ["generic", "lane16"])
+@pytest.mark.parametrize("engine", ["generic", "lane16", "wave"])
 def test_rules_with_no_specified_input(engine):
     """An all-don't-care input matches at every anchor (the paper's empty "no-op" rules,
     Sec. 2.2.1); with outputs it writes everywhere, with heavily overlapping votes."""
@@ -74,7 +74,7 @@ def test_rules_with_no_specified_input(engine):
     assert (r != 0).all()
 
 
-@pytest.mark.parametrize("engine", ["generic", "lane16"])
+@pytest.mark.parametrize("engine", ["generic", "lane16", "wave"])
 def test_no_loaded_rules(engine):
     require_gpu()
     wl = W_("moves", 52, B=41, H=13, W=16, C=4, R=0, shapes=((1, 1),), T=30, L=0)
@@ -85,7 +85,7 @@ def test_no_loaded_rules(engine):
     check(wl, maps, empty, actions, engine)
 
 
-@pytest.mark.parametrize("engine", ["generic", "lane16"])
+@pytest.mark.parametrize("engine", ["generic", "lane16", "wave"])
 def test_out_of_range_actions_are_no_ops(engine):
     require_gpu()
     wl = W_("acts", 53, B=24, H=8, W=8, C=4, R=2, shapes=((1, 2),), T=10)
