@@ -27,16 +27,18 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 METRIC = "env-steps/sec and cell-rule-updates/sec at 1 MI355X; % of HBM roofline"
-# the sources that determine the step kernels' code (the lane16 body is generated)
-KERNEL_SOURCES = ("paper_2407_04221_amd/csrc/k_generic.hip",
-                  "paper_2407_04221_amd/csrc/k_wave.hip",
-                  "paper_2407_04221_amd/csrc/lane16_kernel.hip",
-                  "paper_2407_04221_amd/csrc/lane16_jit.cpp")
+# the sources that determine each engine's step kernel (the lane16 body is generated)
+KERNEL_SOURCES = {
+    "generic": ("paper_2407_04221_amd/csrc/k_generic.hip",),
+    "wave": ("paper_2407_04221_amd/csrc/k_wave.hip",),
+    "lane16": ("paper_2407_04221_amd/csrc/lane16_kernel.hip",
+               "paper_2407_04221_amd/csrc/lane16_jit.cpp"),
+}
 
 
-def kernel_hash() -> str:
+def kernel_hash(engine: str) -> str:
     h = hashlib.sha256()
-    for rel in KERNEL_SOURCES:
+    for rel in KERNEL_SOURCES[engine]:
         p = os.path.join(ROOT, rel)
         if os.path.exists(p):
             h.update(open(p, "rb").read())
@@ -47,9 +49,9 @@ def algorithmic_bytes(wl) -> int:
     return 2 * wl.C * wl.H * wl.W // 8 + 6
 
 
-def measured_traffic(workload: str, engine: int):
+def measured_traffic(workload: str, engine: int, engine_name: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary, if it was taken
-    on the current kernel sources; otherwise None."""
+    on the current sources of that engine's kernel; otherwise None."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
@@ -57,7 +59,7 @@ def measured_traffic(workload: str, engine: int):
         rec = json.load(open(path)).get(f"{workload}/{engine}")
     except Exception:
         return None
-    if not rec or rec.get("kernel_hash") != kernel_hash():
+    if not rec or rec.get("kernel_hash") != kernel_hash(engine_name):
         return None
     return rec
 
@@ -188,7 +190,7 @@ def main():
         cpu = cpu_baseline(wl, maps, rules, actions, args.cpu_seconds,
                            threads=min(16, os.cpu_count() or 1))
 
-    traffic = measured_traffic(args.workload, engine)
+    traffic = measured_traffic(args.workload, engine, engine_name)
     out = {
         "metric": METRIC,
         "value": value,

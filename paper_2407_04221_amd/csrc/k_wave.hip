@@ -1,27 +1,31 @@
-// wave engine: one environment per 64-lane workgroup; lane y owns map row y (H <= 64).
+// wave engine: one environment per workgroup, its rules split over four row groups.
 //
-// With one environment per wave, the environment's rule program is wave-uniform even
-// when every environment has its own rules: rule headers and entries come in through
-// scalar loads, and a rule that matches nowhere in the map costs one ballot.
+// A workgroup holds one environment.  Its threads form four groups of Hq lanes (Hq = 16,
+// 32 or 64 rows, the map height rounded up); lane y of every group owns map row y.  Group
+// g evaluates rules g, g+4, g+8, ... so four rules are matched at once, and with one
+// environment per workgroup the environment's own rules need no per-lane selection:
+// every lane of a group reads the same rule entry.  The rule program (headers, input
+// entries rarest first, rule-major votes) is copied into LDS once per launch when it fits.
 //
-// LDS (one environment):
+// LDS:
 //   planes  [C+1][H+16] rows: the map and the force plane; 16 zero rows below the map let
 //           a lane read row y+i of any pattern without a bounds test
-//   match   [R+4][16+64] rows: match planes of the rules that fired, 16 zero rows on top
-//           so that row y-i of a vote is always a valid read
+//   match   [R+4][16+64] rows: match planes of the rules that fired (for exact counts)
 //   plus, minus [C][64] rows: per channel, OR of the +1 and of the -1 votes
-//   fired   [R+4] indices of the rules that fired this step
+//   fired   [R+4] flags, reward accumulator, program copy
 // Rows are 32-bit words for W <= 32, 64-bit for W <= 64; bit x = column x.
 //
 // Per step (paper Sec. 2.1, Sec. 2.1.1, Sec. 2.2.1):
 //   force   F[y] = the player row moved one cell toward the action;
-//   match   for every rule, AND over its specified entries (rarest first) of plane row
-//           y+i shifted right by j (complemented for must-be-0), within the valid-anchor
-//           mask; the wave leaves the rule as soon as no anchor survives;
-//   votes   for the rules that fired, each nonzero K_O = O - I entry ORs the match plane
-//           moved by (i, j) into the plus or minus accumulator of its channel (LDS atomic OR);
-//   write   new = (old | plus) & ~minus where no cell got both signs; a row with mixed
-//           cells counts their votes exactly: new = (old + sum >= 1);
+//   match   per rule, AND over its specified entries of plane row y+i shifted right by j
+//           (complemented for must-be-0), within the valid-anchor mask; a group leaves the
+//           rule as soon as none of its lanes has a surviving anchor;
+//   votes   right after a rule fired, each nonzero K_O = O - I entry takes the match row
+//           y-i from the group's lane y-i (ds_bpermute), shifts it by j and ORs it into the
+//           plus or minus row of its channel (LDS atomic OR);
+//   write   new = (old | plus) & ~minus where no cell got both signs; a channel whose rows
+//           have mixed cells is recounted exactly with bit-sliced counters of its plus and
+//           minus votes: new = (old + #plus > #minus) = (old + sum >= 1);
 //   end     done when no player bit is left or the counter reaches L; reward = sum over
 //           fired rules of reward * popcount; done environments reload their initial rows.
 #include "av_internal.h"
@@ -31,6 +35,7 @@ namespace {
 
 constexpr int kPad = 16;       // zero rows below the planes and above the match planes
 constexpr int kMRows = kPad + 64;
+constexpr int kGroups = 4;
 
 template <typename RowT>
 __device__ inline RowT load_row(const void *base, size_t idx, int row_bytes) {
@@ -54,26 +59,90 @@ __device__ inline void lds_or(uint32_t *p, uint32_t v) { atomicOr(p, v); }
 __device__ inline void lds_or(uint64_t *p, uint64_t v) {
     atomicOr(reinterpret_cast<unsigned long long *>(p), static_cast<unsigned long long>(v));
 }
+// value of lane `src` of this wave (byte address src * 4)
+__device__ inline uint32_t from_lane(uint32_t v, int src) {
+    return uint32_t(__builtin_amdgcn_ds_bpermute(src << 2, int(v)));
+}
+__device__ inline uint64_t from_lane(uint64_t v, int src) {
+    return uint64_t(from_lane(uint32_t(v), src)) | (uint64_t(from_lane(uint32_t(v >> 32), src)) << 32);
+}
 
 template <typename RowT>
 __device__ inline RowT low_mask(int bits) {
     return bits >= int(8 * sizeof(RowT)) ? ~RowT(0) : ((RowT(1) << bits) - 1);
 }
 
-__device__ inline bool wave_any(bool p) { return __builtin_amdgcn_ballot_w64(p) != 0ull; }
-
-__device__ inline int wave_sum(int v) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-    return v;
+// Does any lane of this thread's group (Hq consecutive lanes of the wave) hold a nonzero?
+__device__ inline bool group_any(bool p, int Hq, int lane) {
+    const unsigned long long bal = __builtin_amdgcn_ballot_w64(p);
+    if (Hq >= 64) return bal != 0ull;
+    const int base = lane & ~(Hq - 1);
+    return ((bal >> base) & ((1ull << Hq) - 1ull)) != 0ull;
 }
 
+constexpr int kCountBits = 17;   // a cell-channel gets at most 256 rules x 16 x 16 votes
+
+// Add the one-bit plane t to the bit-sliced counter cnt (bit k of every cell's count in
+// cnt[k]); the carry ripples only as far as some lane of the group still carries.
 template <typename RowT>
-__global__ void __launch_bounds__(64) wave_step(StepArgs a) {
+__device__ inline void count_add(RowT (&cnt)[kCountBits], RowT t, int Hq, int lane) {
+#pragma unroll
+    for (int k = 0; k < kCountBits; ++k) {
+        if (!group_any(t != 0, Hq, lane)) break;
+        const RowT carry = cnt[k] & t;
+        cnt[k] ^= t;
+        t = carry;
+    }
+}
+
+// The exact write of channel c for this lane's row: counts every vote of every rule that
+// fired (plus and minus separately, old value counted as a plus vote) and returns the
+// cells where old + #plus > #minus, i.e. old + sum of votes >= 1.
+template <typename RowT>
+__device__ RowT exact_channel(int c, RowT old, int Rt, const int *fired, const uint32_t *hdrw,
+                              const uint32_t *vent, const RowT *M, int y, int Hq, int lane) {
+    RowT pc[kCountBits], nc[kCountBits];
+#pragma unroll
+    for (int k = 0; k < kCountBits; ++k) pc[k] = nc[k] = 0;
+    count_add<RowT>(pc, old, Hq, lane);
+    constexpr int kHdrWords = sizeof(RuleHdr) / 4;
+    for (int r = 0; r < Rt; ++r) {
+        if (!fired[r]) continue;
+        const uint32_t *hw = hdrw + r * kHdrWords;
+        const RowT *Mr = M + size_t(r) * kMRows + kPad;
+        const int voff = int(hw[5]), vcnt = int(hw[6]);
+        for (int ev = 0; ev < vcnt; ++ev) {
+            const uint32_t v = vent[voff + ev];
+            if (int(v & 255) != c) continue;
+            const int i = (v >> 8) & 255, j = (v >> 16) & 255;
+            const RowT t = Mr[y - i] << j;
+            if ((v >> 24) & 1) count_add<RowT>(pc, t, Hq, lane);
+            else count_add<RowT>(nc, t, Hq, lane);
+        }
+    }
+    RowT gt = 0, eq = ~RowT(0);
+#pragma unroll
+    for (int k = kCountBits - 1; k >= 0; --k) {
+        gt |= eq & pc[k] & ~nc[k];
+        eq &= ~(pc[k] ^ nc[k]);
+    }
+    return gt;
+}
+
+struct WaveLayout {
+    int Hq;          // lanes per group (16, 32 or 64)
+    int prog_lds;    // 1 if the rule program is copied into LDS
+    int hdr_words, match_words, vote_words;
+};
+
+template <typename RowT>
+__global__ void __launch_bounds__(256) wave_step(StepArgs a, WaveLayout L) {
     extern __shared__ __align__(16) unsigned char lds[];
-    const int H = a.H, W = a.W, C = a.C, C1 = C + 1, Hp = a.H + kPad;
+    const int H = a.H, W = a.W, C = a.C, C1 = C + 1, Hp = a.H + kPad, Hq = L.Hq;
     const int Rt = a.prog.rules_per_set;
-    const int y = threadIdx.x;
+    const int tid = threadIdx.x, nthreads = blockDim.x;
+    const int g = tid / Hq, y = tid - g * Hq;
+    const int lane = tid & 63;
     const int b = blockIdx.x;
     const int s = a.per_env ? b : 0;
     const bool row = y < H;
@@ -83,25 +152,40 @@ __global__ void __launch_bounds__(64) wave_step(StepArgs a) {
     RowT *M = P + size_t(C1) * Hp;                // [Rt][kMRows]
     RowT *PL = M + size_t(Rt) * kMRows;           // [C][64]
     RowT *MI = PL + size_t(C) * 64;               // [C][64]
-    int *fired = reinterpret_cast<int *>(MI + size_t(C) * 64);
+    int *fired = reinterpret_cast<int *>(MI + size_t(C) * 64);   // [Rt]
+    int *red = fired + Rt;                        // [1] reward sum
+    uint32_t *pcopy = reinterpret_cast<uint32_t *>(red + 2);   // program copy (8-byte aligned)
 
     const size_t words = size_t(C1) * Hp + size_t(Rt) * kMRows + size_t(2) * C * 64;
-    for (size_t w = y; w < words; w += 64) P[w] = 0;
+    for (size_t w = tid; w < words; w += nthreads) P[w] = 0;
+
+    const uint32_t *ghdr = reinterpret_cast<const uint32_t *>(a.prog.hdr + size_t(s) * Rt);
+    const uint32_t *gment = a.prog.match + size_t(s) * a.prog.match_stride;
+    const uint32_t *gvent = a.prog.rvote + size_t(s) * a.prog.rvote_stride;
+    const uint32_t *hdrw = ghdr, *ment = gment, *vent = gvent;
+    if (L.prog_lds) {
+        uint32_t *ph = pcopy, *pm = ph + L.hdr_words, *pv = pm + L.match_words;
+        for (int w = tid; w < L.hdr_words; w += nthreads) ph[w] = ghdr[w];
+        for (int w = tid; w < L.match_words; w += nthreads) pm[w] = gment[w];
+        for (int w = tid; w < L.vote_words; w += nthreads) pv[w] = gvent[w];
+        hdrw = ph;
+        ment = pm;
+        vent = pv;
+    }
     __syncthreads();
     if (row)
-        for (int c = 0; c < C; ++c)
+        for (int c = g; c < C; c += kGroups)
             P[c * Hp + y] = load_row<RowT>(a.state, (size_t(c) * a.B + b) * H + y, a.row_bytes);
     int t_env = a.t[b];
-
-    const RuleHdr *hdr = a.prog.hdr + size_t(s) * Rt;
-    const uint32_t *ment = a.prog.match + size_t(s) * a.prog.match_stride;
-    const uint32_t *vent = a.prog.rvote + size_t(s) * a.prog.rvote_stride;
     const RowT rowmask = low_mask<RowT>(W);
+    constexpr int kHdrWords = sizeof(RuleHdr) / 4;
 
     for (int k = 0; k < a.k; ++k) {
+        for (int r = tid; r < Rt; r += nthreads) fired[r] = 0;
+        if (tid == 0) *red = 0;
         __syncthreads();                          // previous step's rows are all written
-        const int act = a.actions[size_t(k) * a.B + b];
-        {
+        if (g == 0) {
+            const int act = a.actions[size_t(k) * a.B + b];
             const RowT *Pp = P + kChPlayer * Hp;
             RowT f = 0;
             if (act == 1) f = Pp[ry + 1];         // row H is a zero pad row
@@ -112,117 +196,111 @@ __global__ void __launch_bounds__(64) wave_step(StepArgs a) {
         }
         __syncthreads();
 
-        // match every rule on the same map; remember the ones that fired
-        int rsum = 0, nf = 0;
-        for (int r = 0; r < Rt; ++r) {
-            const RuleHdr h = hdr[r];
-            RowT acc = (row && y + h.n <= H) ? low_mask<RowT>(W - h.m + 1) : RowT(0);
-            const uint32_t *en = ment + h.match_off;
+        // match: group g takes rules g, g+4, ...; a rule that fired casts its votes at once
+        int rsum = 0;
+        for (int r = g; r < Rt; r += kGroups) {
+            const uint32_t *hw = hdrw + r * kHdrWords;
+            const int hn = int(hw[0]), hm = int(hw[1]), hreward = int(hw[2]);
+            const int moff = int(hw[3]), mcnt = int(hw[4]), voff = int(hw[5]), vcnt = int(hw[6]);
+            RowT acc = (row && y + hn <= H) ? low_mask<RowT>(W - hm + 1) : RowT(0);
+            const uint32_t *en = ment + moff;
             int e = 0;
-            for (; e + 4 <= h.match_cnt && wave_any(acc != 0); e += 4) {
+            for (; e + 4 <= mcnt && group_any(acc != 0, Hq, lane); e += 4) {
                 RowT v[4];
+                uint32_t q[4];
 #pragma unroll
                 for (int u = 0; u < 4; ++u) {
-                    const uint32_t q = en[e + u];
-                    v[u] = P[(q & 255) * Hp + ry + ((q >> 8) & 255)] >> ((q >> 16) & 255);
+                    q[u] = en[e + u];
+                    v[u] = P[(q[u] & 255) * Hp + ry + ((q[u] >> 8) & 255)] >> ((q[u] >> 16) & 255);
                 }
 #pragma unroll
-                for (int u = 0; u < 4; ++u) acc &= ((en[e + u] >> 24) & 1) ? v[u] : RowT(~v[u]);
+                for (int u = 0; u < 4; ++u) acc &= ((q[u] >> 24) & 1) ? v[u] : RowT(~v[u]);
             }
-            for (; e < h.match_cnt && wave_any(acc != 0); ++e) {
+            for (; e < mcnt && group_any(acc != 0, Hq, lane); ++e) {
                 const uint32_t q = en[e];
                 const RowT v = P[(q & 255) * Hp + ry + ((q >> 8) & 255)] >> ((q >> 16) & 255);
                 acc &= ((q >> 24) & 1) ? v : RowT(~v);
             }
-            if (wave_any(acc != 0)) {
+            if (group_any(acc != 0, Hq, lane)) {
                 M[size_t(r) * kMRows + kPad + y] = acc;
-                if (y == 0) fired[nf] = r;
-                ++nf;
-                rsum += h.reward * popc(acc);
+                if (y == 0) fired[r] = 1;
+                rsum += hreward * popc(acc);
+                for (int ev = 0; ev < vcnt; ++ev) {
+                    const uint32_t v = vent[voff + ev];
+                    const int c = v & 255, i = (v >> 8) & 255, j = (v >> 16) & 255;
+                    const RowT src = from_lane(acc, lane - (y >= i ? i : 0));
+                    const RowT t = (y >= i) ? RowT(src << j) : RowT(0);
+                    if (row && t) lds_or(((v >> 24) & 1 ? PL : MI) + c * 64 + y, t);
+                }
             }
         }
+        if (rsum) atomicAdd(red, rsum);
         __syncthreads();
 
-        // votes of the rules that fired
-        for (int q = 0; q < nf; ++q) {
-            const int r = __builtin_amdgcn_readfirstlane(fired[q]);
-            const RuleHdr h = hdr[r];
-            const RowT *Mr = M + size_t(r) * kMRows + kPad;
-            for (int e = 0; e < h.vote_cnt; ++e) {
-                const uint32_t v = vent[h.vote_off + e];
-                const int c = v & 255, i = (v >> 8) & 255, j = (v >> 16) & 255;
-                const RowT t = Mr[y - i] << j;
-                if (row && t) lds_or(((v >> 24) & 1 ? PL : MI) + c * 64 + y, t);
-            }
-        }
-        __syncthreads();
-
-        // new rows, one channel at a time (each lane rewrites only its own row)
-        for (int c = 0; c < C; ++c) {
+        // new rows: group g rewrites channels g, g+4, ... (each lane its own row)
+        for (int c = g; c < C; c += kGroups) {
             const RowT old = P[c * Hp + ry];
             const RowT pl = PL[c * 64 + y], mi = MI[c * 64 + y];
             RowT nw = (old | pl) & ~mi;
             RowT mixed = pl & mi;
-            if (wave_any(mixed != 0)) {
-                while (mixed) {              // cells with votes of both signs: count exactly
-                    const int x = lowbit(mixed);
-                    mixed &= mixed - 1;
-                    int sum = int((old >> x) & 1);
-                    for (int q = 0; q < nf; ++q) {
-                        const int r = fired[q];
-                        const RuleHdr h = hdr[r];
-                        const RowT *Mr = M + size_t(r) * kMRows + kPad;
-                        for (int e = 0; e < h.vote_cnt; ++e) {
-                            const uint32_t v = vent[h.vote_off + e];
-                            const int i = (v >> 8) & 255, j = (v >> 16) & 255;
-                            if (int(v & 255) != c || x < j) continue;
-                            if ((Mr[y - i] >> (x - j)) & 1) sum += ((v >> 24) & 1) ? 1 : -1;
-                        }
-                    }
-                    nw = (nw & ~(RowT(1) << x)) | (RowT(sum >= 1 ? 1 : 0) << x);
-                }
-            }
+            if (group_any(mixed != 0, Hq, lane))
+                nw = exact_channel<RowT>(c, old, Rt, fired, hdrw, vent, M, y, Hq, lane);
             if (row) P[c * Hp + y] = nw;
             PL[c * 64 + y] = 0;
             MI[c * 64 + y] = 0;
         }
 
         // episode end, reward, outputs, reset
-        const bool anyp = wave_any(row && P[kChPlayer * Hp + y] != 0);
+        const bool anyp = __syncthreads_or(g == kChPlayer % kGroups && row &&
+                                           P[kChPlayer * Hp + y] != 0) != 0;
         t_env += 1;
         const bool d = !anyp || (a.L > 0 && t_env == a.L);
         if (d) t_env = 0;
-        int reward = 0;
-        if (a.prog.any_reward && nf > 0) reward = wave_sum(rsum);
-        if (y == 0) {
-            a.rewards[size_t(k) * a.B + b] = float(reward);
+        if (tid == 0) {
+            a.rewards[size_t(k) * a.B + b] = float(*red);
             a.done[size_t(k) * a.B + b] = uint8_t(d);
         }
         if (d && row)
-            for (int c = 0; c < C; ++c)
+            for (int c = g; c < C; c += kGroups)
                 P[c * Hp + y] = load_row<RowT>(a.init, (size_t(c) * a.B + b) * H + y, a.row_bytes);
     }
 
+    __syncthreads();
     if (row)
-        for (int c = 0; c < C; ++c)
+        for (int c = g; c < C; c += kGroups)
             store_row<RowT>(a.state, (size_t(c) * a.B + b) * H + y, a.row_bytes, P[c * Hp + y]);
-    if (y == 0) a.t[b] = t_env;
+    if (tid == 0) a.t[b] = t_env;
+}
+
+int rows_per_group(int H) { return H <= 16 ? 16 : (H <= 32 ? 32 : 64); }
+
+size_t wave_base_bytes(int H, int W, int C, int rules_per_set) {
+    const size_t rowb = W <= 32 ? 4 : 8;
+    return (size_t(C + 1) * (H + kPad) + size_t(rules_per_set) * kMRows + size_t(2) * C * 64) * rowb +
+           sizeof(int) * (size_t(rules_per_set) + 2);
 }
 
 }  // namespace
 
 size_t wave_lds_bytes(int H, int W, int C, int rules_per_set) {
-    const size_t rowb = W <= 32 ? 4 : 8;
-    return (size_t(C + 1) * (H + kPad) + size_t(rules_per_set) * kMRows + size_t(2) * C * 64) * rowb +
-           sizeof(int) * size_t(rules_per_set);
+    return wave_base_bytes(H, W, C, rules_per_set);
 }
 
 hipError_t launch_wave_step(const StepArgs &a, hipStream_t s) {
-    const size_t lds = wave_lds_bytes(a.H, a.W, a.C, a.prog.rules_per_set);
+    WaveLayout L;
+    L.Hq = rows_per_group(a.H);
+    L.hdr_words = int(a.prog.rules_per_set * (sizeof(RuleHdr) / 4));
+    L.match_words = a.prog.match_stride;
+    L.vote_words = a.prog.rvote_stride;
+    const size_t base = wave_base_bytes(a.H, a.W, a.C, a.prog.rules_per_set);
+    const size_t prog = size_t(L.hdr_words + L.match_words + L.vote_words) * 4;
+    L.prog_lds = base + prog <= size_t(kLdsBudget) ? 1 : 0;
+    const size_t lds = base + (L.prog_lds ? prog : 0);
+    const int threads = kGroups * L.Hq;
     if (a.W <= 32)
-        hipLaunchKernelGGL(wave_step<uint32_t>, dim3(a.B), dim3(64), lds, s, a);
+        hipLaunchKernelGGL(wave_step<uint32_t>, dim3(a.B), dim3(threads), lds, s, a, L);
     else
-        hipLaunchKernelGGL(wave_step<uint64_t>, dim3(a.B), dim3(64), lds, s, a);
+        hipLaunchKernelGGL(wave_step<uint64_t>, dim3(a.B), dim3(threads), lds, s, a, L);
     return hipGetLastError();
 }
 
