@@ -42,12 +42,13 @@ def load(path: str = LIB) -> ctypes.CDLL:
     lib.avo_load_rules.argtypes = [P, I, P, P, P, P]
     lib.avo_reset.argtypes = [P, P]
     lib.avo_step.argtypes = [P, P, P, P, I, ctypes.POINTER(I)]
+    lib.avo_set_rule_mode.argtypes = [P, I]
     lib.avo_get_maps.argtypes = [P, P]
     lib.avo_get_counters.argtypes = [P, P]
     lib.avo_destroy.argtypes = [P]
     lib.avo_destroy.restype = None
     for f in ("avo_create", "avo_load_rules", "avo_reset", "avo_step", "avo_get_maps",
-              "avo_get_counters"):
+              "avo_get_counters", "avo_set_rule_mode"):
         getattr(lib, f).restype = I
     _libs[path] = lib
     return lib
@@ -67,7 +68,7 @@ class Oracle:
     """One batch of environments stepped on the CPU by the oracle."""
 
     def __init__(self, B, H, W, C, max_rules, max_h, max_w, per_env=False, episode_len=0,
-                 lib_path: str = LIB):
+                 lib_path: str = LIB, rule_mode: int = 0):
         self.lib = load(lib_path)
         self.B, self.H, self.W, self.C = B, H, W, C
         self.max_h, self.max_w, self.per_env = max_h, max_w, bool(per_env)
@@ -77,12 +78,14 @@ class Oracle:
         if rc != AVO_OK:
             raise OracleError("avo_create", rc)
         self.h = h
-        self._keep = []
+        rc = self.lib.avo_set_rule_mode(self.h, int(rule_mode))
+        if rc != AVO_OK:
+            raise OracleError("avo_set_rule_mode", rc)
 
     @classmethod
-    def for_workload(cls, wl, B=None, lib_path: str = LIB):
+    def for_workload(cls, wl, B=None, lib_path: str = LIB, rule_mode: int = 0):
         return cls(wl.B if B is None else B, wl.H, wl.W, wl.C, wl.R, wl.max_h, wl.max_w,
-                   wl.per_env, wl.L, lib_path=lib_path)
+                   wl.per_env, wl.L, lib_path=lib_path, rule_mode=rule_mode)
 
     def close(self):
         if getattr(self, "h", None):
@@ -137,11 +140,12 @@ class Oracle:
         return out
 
 
-def run(wl, maps, rules, actions, nthreads: int = 1, B=None, lib_path: str = LIB):
+def run(wl, maps, rules, actions, nthreads: int = 1, B=None, lib_path: str = LIB,
+        rule_mode: int = 0):
     """Step a workload's arrays for len(actions) steps; returns the per-step trajectory
     (maps [T][B][C][H][W], rewards [T][B], done [T][B])."""
     B = maps.shape[0] if B is None else B
-    o = Oracle.for_workload(wl, B=B, lib_path=lib_path)
+    o = Oracle.for_workload(wl, B=B, lib_path=lib_path, rule_mode=rule_mode)
     o.load_rules(*rules)
     o.reset(maps)
     T = actions.shape[0]

@@ -24,6 +24,9 @@
  *     don't care, and the target value where only I is don't care.
  *  7. Every cell of every plane (F included) becomes 1 iff old value + votes >= 1, which
  *     keeps the multi-hot map binary (Sec. 2.2.1).
+ *     In sequential mode (the paper's alternative "sequence of convolutions" reading),
+ *     steps 4-7 run once per rule in list order instead: each rule is matched on the map
+ *     the rules before it left, and its own votes are applied before the next rule.
  *  8. F is dropped.  The step counter advances; the episode is done when no player tile
  *     is left (a kill rule, Sec. 2.2.1) or the counter reaches the episode length.
  *     A done environment is reset to its initial map within the same step.
@@ -41,6 +44,7 @@ enum { CH_EMPTY = 0, CH_WALL = 1, CH_PLAYER = 2, CH_GOAL = 3 };
 struct avo_batch {
     int B, H, W, C, max_rules, max_h, max_w, per_env, episode_len;
     int R;               /* loaded rules per set */
+    int rule_mode;       /* 0 parallel, 1 sequential */
     int have_rules, have_maps;
     int32_t *shape;      /* [S][R][2] */
     int8_t *in_pat;      /* [S][R][C+1][max_h][max_w] */
@@ -255,6 +259,12 @@ static void step_env(avo_batch *ab, int b, uint8_t action, float *reward_out,
                             delta[(size_t)c * plane + (size_t)(ay + i) * W + ax + j] += k;
                         }
             }
+        if (ab->rule_mode == 1) {   /* sequential: this rule's votes take effect now */
+            for (size_t k = 0; k < (size_t)C1 * plane; k++) {
+                X[k] = (X[k] + delta[k] >= 1) ? 1 : 0;
+                delta[k] = 0;
+            }
+        }
     }
 
     /* 7. clamp old + votes to {0, 1} on every plane */
@@ -306,6 +316,13 @@ int avo_step(avo_batch *ab, const uint8_t *actions, float *rewards, uint8_t *don
     free(X);
     free(delta);
     if (used) *used = got;
+    return AVO_OK;
+}
+
+int avo_set_rule_mode(avo_batch *ab, int mode)
+{
+    if (!ab || (mode != 0 && mode != 1)) return AVO_EINVAL;
+    ab->rule_mode = mode;
     return AVO_OK;
 }
 

@@ -46,6 +46,11 @@ int  avo_reset(avo_batch *ab, const uint8_t *init_maps);
  * threads (they are independent); returns the thread count used through *used. */
 int  avo_step(avo_batch *ab, const uint8_t *actions, float *rewards, uint8_t *done,
               int nthreads, int *used);
+/* Rule order within a step: 0 = parallel (every rule matches the same map and all votes
+ * are summed once, Sec. 2.1.1; the default), 1 = sequential (rules apply one after another
+ * in list order, each matching the map the previous ones left; a rule's own matches are
+ * applied together). */
+int  avo_set_rule_mode(avo_batch *ab, int mode);
 int  avo_get_maps(const avo_batch *ab, uint8_t *dst);
 int  avo_get_counters(const avo_batch *ab, int32_t *dst);
 void avo_destroy(avo_batch *ab);

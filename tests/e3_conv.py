@@ -63,9 +63,11 @@ def force_plane(P: torch.Tensor, actions: np.ndarray) -> torch.Tensor:
     return F
 
 
-def step(maps: np.ndarray, rules, actions: np.ndarray):
+def step(maps: np.ndarray, rules, actions: np.ndarray, sequential: bool = False):
     """One step with one rule list shared by all envs; no episode logic.
     maps uint8 [B][C][H][W]; rules: list of (n, m, I [C+1][n][m], O, reward).
+    sequential: each rule's convolution pair is applied (and clamped) before the next rule
+    is matched, instead of summing all rules' writes onto the same map.
     Returns (maps after, before any reset) uint8, rewards float64 [B]."""
     B, C, H, W = maps.shape
     X = torch.zeros((B, C + 1, H, W), dtype=torch.float64)
@@ -80,6 +82,9 @@ def step(maps: np.ndarray, rules, actions: np.ndarray):
         act = torch.relu(Fn.conv2d(X, k_in) - thr + 1.0)          # [B][1][H-n+1][W-m+1]
         rho += rew * act.sum(dim=(1, 2, 3))
         delta += Fn.conv_transpose2d(act, k_out)                  # [B][C+1][H][W]
+        if sequential:
+            X = (X + delta >= 1.0).double()
+            delta = torch.zeros_like(X)
     Xn = (X + delta >= 1.0)
     return Xn[:, :C].numpy().astype(np.uint8), rho.numpy()
 
@@ -93,7 +98,7 @@ def rules_from_abi(shape, in_pat, out_pat, reward, s: int = 0):
     return out
 
 
-def run(maps, rules_abi, actions, L: int = 0, per_env: bool = False):
+def run(maps, rules_abi, actions, L: int = 0, per_env: bool = False, sequential: bool = False):
     """Episode-level stepping on top of `step`: done when no player is left or the counter
     reaches L; done envs return to their initial maps.  Returns per-step maps, rewards,
     done like oracle.run."""
@@ -111,10 +116,11 @@ def run(maps, rules_abi, actions, L: int = 0, per_env: bool = False):
             rho = np.zeros(B)
             for b in range(B):
                 nb, rb = step(cur[b:b + 1], rules_from_abi(shape, in_pat, out_pat, reward, b),
-                              actions[k, b:b + 1])
+                              actions[k, b:b + 1], sequential)
                 nxt[b], rho[b] = nb[0], rb[0]
         else:
-            nxt, rho = step(cur, rules_from_abi(shape, in_pat, out_pat, reward), actions[k])
+            nxt, rho = step(cur, rules_from_abi(shape, in_pat, out_pat, reward), actions[k],
+                            sequential)
         t += 1
         done = (nxt[:, PLAYER].reshape(B, -1).sum(1) == 0) | ((L > 0) & (t == L))
         nxt[done] = maps[done]

@@ -2,6 +2,7 @@
 
 Format (line based, '#' starts a comment):
 
+    mode sequential              optional: rules applied one after another (default parallel)
     channels <C>                 stored channels; tiles E W P G a b c ... (0, 1, 2, 3, 4 ...)
     episode <L>                  optional episode length (default 0 = none)
     rule <n>x<m> reward <r>      one block per loaded rule, in index order
@@ -49,6 +50,7 @@ class Fixture:
     name: str
     C: int
     L: int
+    mode: int = 0                                # 0 parallel, 1 sequential
     rules: list = field(default_factory=list)   # (n, m, in [C+1][n][m], out, reward)
     init: np.ndarray = None                      # [C][H][W]
     steps: List[Step] = field(default_factory=list)
@@ -113,7 +115,8 @@ def parse(path: str) -> Fixture:
                 lines.append(s.strip())
     fx = Fixture(name=name, C=0, L=0)
     k = 0
-    keywords = ("channels", "episode", "rule", "in", "out", "map", "step", "reward", "done")
+    keywords = ("mode", "channels", "episode", "rule", "in", "out", "map", "step", "reward",
+                "done")
 
     def grab_rows(k):
         rows = []
@@ -126,7 +129,9 @@ def parse(path: str) -> Fixture:
         head, *rest = lines[k].split(None, 1)
         rest = rest[0] if rest else ""
         k += 1
-        if head == "channels":
+        if head == "mode":
+            fx.mode = {"parallel": 0, "sequential": 1}[rest.strip()]
+        elif head == "channels":
             fx.C = int(rest)
         elif head == "episode":
             fx.L = int(rest)

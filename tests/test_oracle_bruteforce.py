@@ -133,3 +133,23 @@ def test_b4_per_env_rule_sets_against_conv_form(oracle_lib):
     got = oracle.run(wl, maps, rules, actions)
     for a, b in zip(got, want):
         np.testing.assert_array_equal(a, b)
+
+
+@pytest.mark.parametrize("seed", range(4))
+@pytest.mark.parametrize("variant", ["literal", "planted", "dense"])
+def test_b4_sequential_mode_against_conv_form(oracle_lib, seed, variant):
+    """Rules applied in sequence: each rule's conv / conv^T pair is applied and clamped
+    before the next rule is matched."""
+    shapes = (((2, 2), (1, 2)), ((3, 3), (2, 1), (1, 1)))[seed % 2]
+    wl = inputs.Workload("t", 110 + seed, B=20, H=5 + seed % 3, W=6 + seed % 4, C=4 + seed % 3,
+                         R=5, shapes=shapes, p_dc=0.5, per_env=bool(seed % 2), T=5, L=4)
+    maps, rules, actions = inputs.make_all(wl, seed, variant)
+    maps = maps | (np.random.default_rng(seed).random(maps.shape) < 0.25).astype(np.uint8)
+    want = e3_conv.run(maps, rules, actions, L=wl.L, per_env=wl.per_env, sequential=True)
+    got = oracle.run(wl, maps, rules, actions, rule_mode=1)
+    for a, b in zip(got, want):
+        np.testing.assert_array_equal(a, b)
+    par = oracle.run(wl, maps, rules, actions, rule_mode=0)
+    if variant != "literal":
+        assert not all(np.array_equal(a, b) for a, b in zip(got, par)), \
+            "sequential and parallel application should differ on firing rules"

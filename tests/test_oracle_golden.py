@@ -17,7 +17,8 @@ def _ids(paths):
 
 def run_oracle(fx):
     shape, ip, op, rw, mh, mw = fx.abi_rules()
-    o = oracle.Oracle(1, fx.H, fx.W, fx.C, max(len(fx.rules), 1), mh, mw, False, fx.L)
+    o = oracle.Oracle(1, fx.H, fx.W, fx.C, max(len(fx.rules), 1), mh, mw, False, fx.L,
+                      rule_mode=fx.mode)
     o.load_rules(shape, ip, op, rw)
     o.reset(fx.init[None])
     got = []
@@ -43,7 +44,8 @@ def test_conv_form_matches_worked_case(path):
     fx = fixtures.parse(path)
     shape, ip, op, rw, _, _ = fx.abi_rules()
     acts = np.array([[st.action] for st in fx.steps], np.uint8)
-    maps, rewards, done = e3_conv.run(fx.init[None], (shape, ip, op, rw), acts, L=fx.L)
+    maps, rewards, done = e3_conv.run(fx.init[None], (shape, ip, op, rw), acts, L=fx.L,
+                                      sequential=bool(fx.mode))
     for k, st in enumerate(fx.steps):
         np.testing.assert_array_equal(maps[k, 0], st.after, err_msg=f"{fx.name} step {k}")
         assert rewards[k, 0] == st.reward
@@ -54,5 +56,6 @@ def test_fixture_set_is_complete():
     names = set(_ids(FIXTURES))
     # a single rule firing, a don't-care cell, overlapping matches, a move into a wall
     for need in ("w01_single_rule", "w02_dont_care", "w03_overlap", "w04_move_into_wall",
-                 "w06_food", "w07_kill", "w08_edge", "w10_vote_count"):
+                 "w06_food", "w07_kill", "w08_edge", "w10_vote_count", "ws01_food_sequential",
+                 "ws02_chain_sequential"):
         assert need in names

@@ -24,7 +24,8 @@ MUTANTS = {
     "set_vote_ignores_input": ("if (out == 1) return in == 1 ? 0 : 1;", "if (out == 1) return 1;"),
     "anchor_rows_short": ("ay + rv.n <= H", "ay + rv.n < H"),
     "anchor_cols_short": ("ax + rv.m <= W", "ax + rv.m < W"),
-    "clamp_threshold": ("(X[k] + delta[k] >= 1)", "(X[k] + delta[k] > 1)"),
+    "clamp_threshold": ("(X[k] + delta[k] >= 1) ? 1 : 0;\n\n", "(X[k] + delta[k] > 1) ? 1 : 0;\n\n"),
+    "sequential_votes_carried_over": ("                delta[k] = 0;\n", ""),
     "dont_care_read_as_zero": ("if (want == -1) continue;", "if (want == -1) want = 0;"),
     "wall_does_not_block": ("in[k][CH_WALL][ty][tx] = 0;", "(void)0;"),
     "reward_not_accumulated": ("rho += rv.reward;", "rho = rv.reward;"),
@@ -62,7 +63,7 @@ def pin_worked_cases(lib):
         fx = fixtures.parse(path)
         shape, ip, op, rw, mh, mw = fx.abi_rules()
         o = oracle.Oracle(1, fx.H, fx.W, fx.C, max(len(fx.rules), 1), mh, mw, False, fx.L,
-                          lib_path=lib)
+                          lib_path=lib, rule_mode=fx.mode)
         o.load_rules(shape, ip, op, rw)
         o.reset(fx.init[None])
         for st in fx.steps:
