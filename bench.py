@@ -64,13 +64,14 @@ def measured_traffic(workload: str, engine: int, engine_name: str):
     return rec
 
 
-def cpu_baseline(wl, maps, rules, actions, budget_s: float, threads: int):
+def cpu_baseline(wl, maps, rules, actions, budget_s: float, threads: int,
+                 rule_mode: str = "parallel"):
     import oracle
     from paper_2407_04221_amd import inputs
     nb = min(wl.B, 4096)
     envs = np.arange(nb)
     m, r, a = inputs.subset_envs(wl, maps, rules, actions, envs)
-    o = oracle.Oracle.for_workload(wl, B=nb)
+    o = oracle.Oracle.for_workload(wl, B=nb, rule_mode=int(rule_mode == "sequential"))
     o.load_rules(*r)
     o.reset(m)
     steps = 0
@@ -94,6 +95,7 @@ def main():
     ap.add_argument("--workload", default="c4")
     ap.add_argument("--variant", default="literal", choices=["literal", "planted", "dense"])
     ap.add_argument("--engine", default="auto", choices=["auto", "generic", "lane16", "wave"])
+    ap.add_argument("--rule-mode", default="parallel", choices=["parallel", "sequential"])
     ap.add_argument("--chunk", type=int, default=1000, help="steps per av_step_n launch")
     ap.add_argument("--launch-steps", type=int, default=0,
                     help="also time this many steps with one launch per step (av_step)")
@@ -129,7 +131,7 @@ def main():
         del src, dst
     maps, rules, actions = inputs.make_all(wl, args.seed, args.variant, T=max(T, args.warmup, 1))
     acts = torch.from_numpy(actions).cuda()
-    b = av.Batch.for_workload(wl, engine=args.engine)
+    b = av.Batch.for_workload(wl, engine=args.engine, rule_mode=args.rule_mode)
     b.load_rules(*rules)
     b.reset(maps)
     engine = b.info["engine"]
@@ -188,7 +190,7 @@ def main():
     cpu = None
     if not args.no_cpu:
         cpu = cpu_baseline(wl, maps, rules, actions, args.cpu_seconds,
-                           threads=min(16, os.cpu_count() or 1))
+                           threads=min(16, os.cpu_count() or 1), rule_mode=args.rule_mode)
 
     traffic = measured_traffic(args.workload, engine, engine_name)
     out = {
@@ -211,6 +213,7 @@ def main():
                         f"{args.variant}, episode {wl.L} steps",
             "B": wl.B, "H": wl.H, "W": wl.W, "C": wl.C, "R": wl.R, "variant": args.variant,
             "engine": engine_name, "api": "av_step_n", "steps_per_launch": chunk,
+            "rule_mode": args.rule_mode,
         },
         "cell_rule_updates_per_sec": value * wl.H * wl.W * wl.R,
         "pct_hbm_roofline": 100.0 * value / roof_env_steps,

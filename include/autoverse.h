@@ -62,12 +62,24 @@ typedef enum {
 typedef enum {
     AV_ENGINE_AUTO = 0,
     AV_ENGINE_GENERIC = 1,  /* any size within the limits below; maps staged in LDS */
-    AV_ENGINE_LANE16 = 2,   /* maps of at most 16 x 16 and one shared rule set: one map
-                               row per lane, two maps per 32-bit lane word, rows shifted
-                               across lanes with DPP, the rule set compiled into the kernel */
+    AV_ENGINE_LANE16 = 2,   /* maps of at most 16 x 16, one shared rule set, parallel rule
+                               mode: one map row per lane, two maps per 32-bit lane word,
+                               rows shifted across lanes with DPP, the rule set compiled
+                               into the kernel */
     AV_ENGINE_WAVE = 3      /* one environment per 64-lane wave, map rows in LDS; rule
                                programs read with scalar loads (per-environment rules) */
 } av_engine;
+
+/* Order in which the rules of one step are applied. */
+typedef enum {
+    AV_RULES_PARALLEL = 0,    /* every rule matches the same map; all votes summed once
+                                 (paper Sec. 2.1.1; the default) */
+    AV_RULES_SEQUENTIAL = 1   /* rules apply one after another in list order (the four moves,
+                                 then the loaded rules by index); each matches the map the
+                                 rules before it left, force plane included; all matches of
+                                 one rule apply together (the "sequence of convolutions"
+                                 reading of the Fig. 2a caption) */
+} av_rule_mode;
 
 typedef struct {
     int32_t num_envs;           /* B >= 1 */
@@ -79,6 +91,7 @@ typedef struct {
     int32_t max_episode_steps;  /* L >= 0; 0 = episodes end only when the player is gone */
     int32_t device;             /* HIP device ordinal */
     int32_t engine;             /* av_engine */
+    int32_t rule_mode;          /* av_rule_mode */
     void *stream;               /* hipStream_t for all device work; NULL = null stream */
 } av_config;
 

@@ -22,6 +22,8 @@ AV_ENGINE_AUTO, AV_ENGINE_GENERIC, AV_ENGINE_LANE16, AV_ENGINE_WAVE = 0, 1, 2, 3
 ENGINES = {"auto": AV_ENGINE_AUTO, "generic": AV_ENGINE_GENERIC, "lane16": AV_ENGINE_LANE16,
            "wave": AV_ENGINE_WAVE}
 ENGINE_NAMES = {v: k for k, v in ENGINES.items()}
+AV_RULES_PARALLEL, AV_RULES_SEQUENTIAL = 0, 1
+RULE_MODES = {"parallel": AV_RULES_PARALLEL, "sequential": AV_RULES_SEQUENTIAL}
 
 # Every symbol include/autoverse.h declares.
 ABI_SYMBOLS = ("av_create_batch", "av_load_rules", "av_reset", "av_step", "av_step_n",
@@ -35,7 +37,8 @@ class av_config(ctypes.Structure):
                 ("max_rules", ctypes.c_int32), ("max_pat_h", ctypes.c_int32),
                 ("max_pat_w", ctypes.c_int32), ("per_env_rules", ctypes.c_int32),
                 ("max_episode_steps", ctypes.c_int32), ("device", ctypes.c_int32),
-                ("engine", ctypes.c_int32), ("stream", ctypes.c_void_p)]
+                ("engine", ctypes.c_int32), ("rule_mode", ctypes.c_int32),
+                ("stream", ctypes.c_void_p)]
 
 
 class av_info(ctypes.Structure):
@@ -124,7 +127,7 @@ def current_stream_handle():
 
 def av_create_batch(num_envs, height, width, channels, max_rules, max_pat_h, max_pat_w,
                     per_env_rules=False, max_episode_steps=0, device=None, engine="auto",
-                    stream=None):
+                    stream=None, rule_mode="parallel"):
     """Returns an opaque handle (ctypes.c_void_p).  stream: a torch.cuda.Stream, a raw
     handle, or None for torch's current stream on `device`."""
     torch = _torch()
@@ -137,7 +140,9 @@ def av_create_batch(num_envs, height, width, channels, max_rules, max_pat_h, max
         stream = ctypes.c_void_p(stream.cuda_stream)
     cfg = av_config(num_envs, height, width, channels, max_rules, max_pat_h, max_pat_w,
                     int(bool(per_env_rules)), max_episode_steps, int(device),
-                    ENGINES[engine] if isinstance(engine, str) else int(engine), stream)
+                    ENGINES[engine] if isinstance(engine, str) else int(engine),
+                    RULE_MODES[rule_mode] if isinstance(rule_mode, str) else int(rule_mode),
+                    stream)
     h = ctypes.c_void_p()
     _check("av_create_batch", load_library().av_create_batch(ctypes.byref(cfg), ctypes.byref(h)))
     return h
@@ -229,21 +234,22 @@ class Batch:
     rewards and done flags."""
 
     def __init__(self, num_envs, height, width, channels, max_rules, max_pat_h, max_pat_w,
-                 per_env_rules=False, max_episode_steps=0, device=None, engine="auto"):
+                 per_env_rules=False, max_episode_steps=0, device=None, engine="auto",
+                 rule_mode="parallel"):
         torch = _torch()
         self.device = torch.device("cuda", torch.cuda.current_device() if device is None
                                    else device)
         self.B, self.H, self.W, self.C = num_envs, height, width, channels
         self.h = av_create_batch(num_envs, height, width, channels, max_rules, max_pat_h,
                                  max_pat_w, per_env_rules, max_episode_steps,
-                                 self.device.index, engine)
+                                 self.device.index, engine, rule_mode=rule_mode)
         self.rewards = torch.zeros(num_envs, dtype=torch.float32, device=self.device)
         self.done = torch.zeros(num_envs, dtype=torch.uint8, device=self.device)
 
     @classmethod
-    def for_workload(cls, wl, B=None, device=None, engine="auto"):
+    def for_workload(cls, wl, B=None, device=None, engine="auto", rule_mode="parallel"):
         return cls(wl.B if B is None else B, wl.H, wl.W, wl.C, wl.R, wl.max_h, wl.max_w,
-                   wl.per_env, wl.L, device=device, engine=engine)
+                   wl.per_env, wl.L, device=device, engine=engine, rule_mode=rule_mode)
 
     @property
     def info(self):

@@ -139,7 +139,8 @@ int entry_rank(int c, int want, int C) {
     return (want ? 0 : 8) + ch;
 }
 
-void compile_generic(const std::vector<std::vector<HostRule>> &sets, int C, GenericProgram &p) {
+void compile_generic(const std::vector<std::vector<HostRule>> &sets, int C, bool force_votes,
+                     GenericProgram &p) {
     const int C1 = C + 1;
     p.any_reward = 0;
     p.sets = int(sets.size());
@@ -164,7 +165,7 @@ void compile_generic(const std::vector<std::vector<HostRule>> &sets, int C, Gene
                         if (k) per_ch[c].push_back(pack_vote(r, i, j, k > 0));
                     }
             h.vote_off = int(rvote[s].size());
-            for (int c = 0; c < C; ++c)           // the force plane's votes are never used
+            for (int c = 0; c < (force_votes ? C1 : C); ++c)
                 for (int i = 0; i < hr.n; ++i)
                     for (int j = 0; j < hr.m; ++j) {
                         const int k = kout(hr.at(hr.in, c, i, j), hr.at(hr.out, c, i, j));
@@ -244,6 +245,8 @@ av_status av_create_batch(const av_config *cfg, av_batch_t *out) {
     if (c.per_env_rules != 0 && c.per_env_rules != 1)
         return fail(AV_EINVAL, "per_env_rules must be 0 or 1");
     if (c.max_episode_steps < 0) return fail(AV_EINVAL, "max_episode_steps must be >= 0");
+    if (c.rule_mode != AV_RULES_PARALLEL && c.rule_mode != AV_RULES_SEQUENTIAL)
+        return fail(AV_EINVAL, "unknown rule_mode %d", c.rule_mode);
     if (c.engine < AV_ENGINE_AUTO || c.engine > AV_ENGINE_WAVE)
         return fail(AV_EINVAL, "unknown engine %d", c.engine);
     const size_t env_lds = generic_env_lds_bytes(c.height, c.width, c.channels,
@@ -253,8 +256,8 @@ av_status av_create_batch(const av_config *cfg, av_batch_t *out) {
                     "channels or a smaller map", env_lds, kLdsBudget);
     const bool lane16_ok = lane16_eligible(c);
     if (c.engine == AV_ENGINE_LANE16 && !lane16_ok)
-        return fail(AV_EINVAL, "the lane16 engine needs H, W <= 16 and one rule set shared "
-                    "by all environments");
+        return fail(AV_EINVAL, "the lane16 engine needs H, W <= 16, one rule set shared by "
+                    "all environments and parallel rule mode");
     const size_t wave_lds = wave_lds_bytes(c.height, c.width, c.channels, c.max_rules + kMoveRules);
     const bool wave_ok = wave_lds <= size_t(kLdsBudget);
     if (c.engine == AV_ENGINE_WAVE && !wave_ok)
@@ -344,7 +347,7 @@ av_status av_load_rules(av_batch_t b, int32_t R, const int32_t *shape, const int
     AV_HIP(hipStreamSynchronize(b->stream));   // no step may still read the old program
     free_device_program(b);
     b->have_rules = false;
-    compile_generic(sets, c.channels, b->prog);
+    compile_generic(sets, c.channels, c.rule_mode == AV_RULES_SEQUENTIAL, b->prog);
     if (av_status st = upload(&b->dprog.hdr, b->prog.hdr)) return st;
     if (av_status st = upload(&b->dprog.votes, b->prog.votes)) return st;
     if (av_status st = upload(&b->dprog.match, b->prog.match)) return st;
@@ -400,6 +403,7 @@ static av_status step_k(av_batch_t b, int32_t k, const uint8_t *actions, float *
     StepArgs a{};
     a.B = c.num_envs; a.H = c.height; a.W = c.width; a.C = c.channels;
     a.L = c.max_episode_steps; a.per_env = c.per_env_rules; a.k = k;
+    a.sequential = c.rule_mode == AV_RULES_SEQUENTIAL;
     a.row_bytes = b->row_bytes;
     a.state = b->d_state; a.init = b->d_init; a.t = b->d_t;
     a.actions = actions; a.rewards = rewards; a.done = done;

@@ -28,15 +28,16 @@ constexpr int kLdsBudget = 64 * 1024;
 // Match entry (one specified input entry): bits 0-7 channel, 8-15 row i, 16-23 col j,
 // bit 24 wanted value.  Vote entry (one nonzero K_O entry), grouped by channel:
 // bits 0-7 rule, 8-15 row i, 16-23 col j, bit 24 set when the vote is +1.  Rule-major
-// vote entry (the same votes grouped by rule, force plane left out because it is dropped
-// after the step): bits 0-7 channel, 8-15 row i, 16-23 col j, bit 24 set for +1.
+// vote entry (the same votes grouped by rule; the force plane's are left out in parallel
+// mode, where the plane is dropped before anything reads it again): bits 0-7 channel,
+// 8-15 row i, 16-23 col j, bit 24 set for +1.
 // ---------------------------------------------------------------------------------
 struct RuleHdr {
     int32_t n, m;         // pattern rows, cols
     int32_t reward;
     int32_t match_off;    // into the set's match entries
     int32_t match_cnt;
-    int32_t vote_off;     // into the set's rule-major vote entries (stored channels only)
+    int32_t vote_off;     // into the set's rule-major vote entries
     int32_t vote_cnt;
     int32_t pad;
 };
@@ -81,6 +82,7 @@ struct DeviceProgram {
 struct StepArgs {
     int32_t B, H, W, C, L;
     int32_t per_env;
+    int32_t sequential;              // rules applied one after another (else in parallel)
     int32_t k;                       // steps in this launch
     int32_t row_bytes;
     void *state;                     // [C][B][H] rows

@@ -11,6 +11,8 @@
 //             y + i shifted right by j (bit x then holds cell x + j), complemented for
 //             must-be-0 entries, masked to anchors where the pattern lies on the map;
 //   reward    sum over rules of reward_r * popcount(M_r), reduced per environment;
+//   (order)   all rules match the same map (parallel mode), or in sequential mode each rule
+//             is matched, and its votes applied, before the next one;
 //   write     per channel, the OR of +1 votes and of -1 votes (match planes shifted back
 //             by (i, j)); cells that got votes of one sign take that sign's value, cells
 //             with both signs count the votes exactly: new = (old + sum >= 1);
@@ -93,53 +95,61 @@ __global__ void __launch_bounds__(256) generic_step(StepArgs a, int G) {
         }
         __syncthreads();
 
-        // match every rule on the same map
+        // Rules in batches: all of them at once (parallel mode) or one at a time
+        // (sequential mode, each rule matched on the map the previous ones left).
         int rsum = 0;
-        if (live) {
-            for (int r = 0; r < Rt; ++r) {
-                const RuleHdr h = hdr[r];
-                RowT acc = (y + h.n <= H) ? low_mask<RowT>(W - h.m + 1) : RowT(0);
-                for (int e = 0; e < h.match_cnt && acc; ++e) {
-                    const uint32_t en = ment[h.match_off + e];
-                    const int c = en & 255, i = (en >> 8) & 255, j = (en >> 16) & 255;
-                    const RowT v = my[c * H + y + i] >> j;
-                    acc &= ((en >> 24) & 1) ? v : RowT(~v);
+        for (int r0 = 0, r1 = 0; r0 < Rt; r0 = r1) {
+            r1 = a.sequential ? r0 + 1 : Rt;
+            if (r0 > 0) __syncthreads();      // the previous batch's rows are all written
+            if (live) {
+                for (int r = r0; r < r1; ++r) {
+                    const RuleHdr h = hdr[r];
+                    RowT acc = (y + h.n <= H) ? low_mask<RowT>(W - h.m + 1) : RowT(0);
+                    for (int e = 0; e < h.match_cnt && acc; ++e) {
+                        const uint32_t en = ment[h.match_off + e];
+                        const int c = en & 255, i = (en >> 8) & 255, j = (en >> 16) & 255;
+                        const RowT v = my[c * H + y + i] >> j;
+                        acc &= ((en >> 24) & 1) ? v : RowT(~v);
+                    }
+                    myM[r * H + y] = acc;
+                    rsum += h.reward * popc(acc);
                 }
-                myM[r * H + y] = acc;
-                rsum += h.reward * popc(acc);
             }
-        }
-        __syncthreads();
+            __syncthreads();
 
-        // votes and clamp, one channel at a time; each thread rewrites only its own row
-        if (live) {
-            for (int c = 0; c < C1; ++c) {
-                const VoteList L = vl[c];
-                RowT plus = 0, minus = 0;
-                for (int e = 0; e < L.cnt; ++e) {
-                    const uint32_t v = vent[L.off + e];
-                    const int r = v & 255, i = (v >> 8) & 255, j = (v >> 16) & 255;
-                    if (y < i) continue;
-                    const RowT mv = myM[r * H + y - i] << j;
-                    if ((v >> 24) & 1) plus |= mv; else minus |= mv;
-                }
-                const RowT old = my[c * H + y];
-                RowT nw = (old | plus) & ~minus;
-                RowT mixed = plus & minus;
-                while (mixed) {           // cells with votes of both signs: count exactly
-                    const int x = lowbit(mixed);
-                    mixed &= mixed - 1;
-                    int sum = int((old >> x) & 1);
+            // votes of this batch and clamp, one channel at a time; each thread rewrites
+            // only its own row
+            if (live) {
+                for (int c = 0; c < C1; ++c) {
+                    const VoteList L = vl[c];
+                    RowT plus = 0, minus = 0;
                     for (int e = 0; e < L.cnt; ++e) {
                         const uint32_t v = vent[L.off + e];
                         const int r = v & 255, i = (v >> 8) & 255, j = (v >> 16) & 255;
-                        if (y < i || x < j) continue;
-                        if ((myM[r * H + y - i] >> (x - j)) & 1) sum += ((v >> 24) & 1) ? 1 : -1;
+                        if (r < r0 || r >= r1 || y < i) continue;
+                        const RowT mv = myM[r * H + y - i] << j;
+                        if ((v >> 24) & 1) plus |= mv; else minus |= mv;
                     }
-                    nw = (nw & ~(RowT(1) << x)) | (RowT(sum >= 1 ? 1 : 0) << x);
+                    const RowT old = my[c * H + y];
+                    RowT nw = (old | plus) & ~minus;
+                    RowT mixed = plus & minus;
+                    while (mixed) {       // cells with votes of both signs: count exactly
+                        const int x = lowbit(mixed);
+                        mixed &= mixed - 1;
+                        int sum = int((old >> x) & 1);
+                        for (int e = 0; e < L.cnt; ++e) {
+                            const uint32_t v = vent[L.off + e];
+                            const int r = v & 255, i = (v >> 8) & 255, j = (v >> 16) & 255;
+                            if (r < r0 || r >= r1 || y < i || x < j) continue;
+                            if ((myM[r * H + y - i] >> (x - j)) & 1) sum += ((v >> 24) & 1) ? 1 : -1;
+                        }
+                        nw = (nw & ~(RowT(1) << x)) | (RowT(sum >= 1 ? 1 : 0) << x);
+                    }
+                    my[c * H + y] = nw;
                 }
-                my[c * H + y] = nw;
             }
+        }
+        if (live) {
             if (my[kChPlayer * H + y]) atomicOr(&anyp[g], 1);
             atomicAdd(&red[g], rsum);
         }

@@ -11,11 +11,12 @@
 //   planes  [C+1][H+16] rows: the map and the force plane; 16 zero rows below the map let
 //           a lane read row y+i of any pattern without a bounds test
 //   match   [R+4][16+64] rows: match planes of the rules that fired (for exact counts)
-//   plus, minus [C][64] rows: per channel, OR of the +1 and of the -1 votes
+//   plus, minus [C+1][64] rows: per plane, OR of the +1 and of the -1 votes
 //   fired   [R+4] flags, reward accumulator, program copy
 // Rows are 32-bit words for W <= 32, 64-bit for W <= 64; bit x = column x.
 //
-// Per step (paper Sec. 2.1, Sec. 2.1.1, Sec. 2.2.1):
+// Per step (paper Sec. 2.1, Sec. 2.1.1, Sec. 2.2.1), for one batch of all rules (parallel
+// mode) or for one rule after another (sequential mode):
 //   force   F[y] = the player row moved one cell toward the action;
 //   match   per rule, AND over its specified entries of plane row y+i shifted right by j
 //           (complemented for must-be-0), within the valid-anchor mask; a group leaves the
@@ -95,18 +96,19 @@ __device__ inline void count_add(RowT (&cnt)[kCountBits], RowT t, int Hq, int la
     }
 }
 
-// The exact write of channel c for this lane's row: counts every vote of every rule that
-// fired (plus and minus separately, old value counted as a plus vote) and returns the
-// cells where old + #plus > #minus, i.e. old + sum of votes >= 1.
+// The exact write of channel c for this lane's row: counts every vote of every rule of the
+// batch [rb, re) that fired (plus and minus separately, old value counted as a plus vote)
+// and returns the cells where old + #plus > #minus, i.e. old + sum of votes >= 1.
 template <typename RowT>
-__device__ RowT exact_channel(int c, RowT old, int Rt, const int *fired, const uint32_t *hdrw,
-                              const uint32_t *vent, const RowT *M, int y, int Hq, int lane) {
+__device__ RowT exact_channel(int c, RowT old, int rb, int re, const int *fired,
+                              const uint32_t *hdrw, const uint32_t *vent, const RowT *M, int y,
+                              int Hq, int lane) {
     RowT pc[kCountBits], nc[kCountBits];
 #pragma unroll
     for (int k = 0; k < kCountBits; ++k) pc[k] = nc[k] = 0;
     count_add<RowT>(pc, old, Hq, lane);
     constexpr int kHdrWords = sizeof(RuleHdr) / 4;
-    for (int r = 0; r < Rt; ++r) {
+    for (int r = rb; r < re; ++r) {
         if (!fired[r]) continue;
         const uint32_t *hw = hdrw + r * kHdrWords;
         const RowT *Mr = M + size_t(r) * kMRows + kPad;
@@ -150,13 +152,13 @@ __global__ void __launch_bounds__(256) wave_step(StepArgs a, WaveLayout L) {
 
     RowT *P = reinterpret_cast<RowT *>(lds);      // [C1][Hp]
     RowT *M = P + size_t(C1) * Hp;                // [Rt][kMRows]
-    RowT *PL = M + size_t(Rt) * kMRows;           // [C][64]
-    RowT *MI = PL + size_t(C) * 64;               // [C][64]
-    int *fired = reinterpret_cast<int *>(MI + size_t(C) * 64);   // [Rt]
+    RowT *PL = M + size_t(Rt) * kMRows;           // [C1][64]
+    RowT *MI = PL + size_t(C1) * 64;              // [C1][64]
+    int *fired = reinterpret_cast<int *>(MI + size_t(C1) * 64);  // [Rt]
     int *red = fired + Rt;                        // [1] reward sum
     uint32_t *pcopy = reinterpret_cast<uint32_t *>(red + 2);   // program copy (8-byte aligned)
 
-    const size_t words = size_t(C1) * Hp + size_t(Rt) * kMRows + size_t(2) * C * 64;
+    const size_t words = size_t(C1) * Hp + size_t(Rt) * kMRows + size_t(2) * C1 * 64;
     for (size_t w = tid; w < words; w += nthreads) P[w] = 0;
 
     const uint32_t *ghdr = reinterpret_cast<const uint32_t *>(a.prog.hdr + size_t(s) * Rt);
@@ -196,59 +198,66 @@ __global__ void __launch_bounds__(256) wave_step(StepArgs a, WaveLayout L) {
         }
         __syncthreads();
 
-        // match: group g takes rules g, g+4, ...; a rule that fired casts its votes at once
+        // Rules in batches: all at once (parallel mode) or one at a time (sequential mode,
+        // each rule matched on the map the previous ones left, force plane included).
+        const int Cw = a.sequential ? C1 : C;     // planes the rules write
         int rsum = 0;
-        for (int r = g; r < Rt; r += kGroups) {
-            const uint32_t *hw = hdrw + r * kHdrWords;
-            const int hn = int(hw[0]), hm = int(hw[1]), hreward = int(hw[2]);
-            const int moff = int(hw[3]), mcnt = int(hw[4]), voff = int(hw[5]), vcnt = int(hw[6]);
-            RowT acc = (row && y + hn <= H) ? low_mask<RowT>(W - hm + 1) : RowT(0);
-            const uint32_t *en = ment + moff;
-            int e = 0;
-            for (; e + 4 <= mcnt && group_any(acc != 0, Hq, lane); e += 4) {
-                RowT v[4];
-                uint32_t q[4];
+        for (int rb = 0, re = 0; rb < Rt; rb = re) {
+            re = a.sequential ? rb + 1 : Rt;
+            if (rb > 0) __syncthreads();          // the previous batch's rows are all written
+            // group g takes rules rb+g, rb+g+4, ...; a rule that fired casts its votes at once
+            for (int r = rb + g; r < re; r += kGroups) {
+                const uint32_t *hw = hdrw + r * kHdrWords;
+                const int hn = int(hw[0]), hm = int(hw[1]), hreward = int(hw[2]);
+                const int moff = int(hw[3]), mcnt = int(hw[4]), voff = int(hw[5]), vcnt = int(hw[6]);
+                RowT acc = (row && y + hn <= H) ? low_mask<RowT>(W - hm + 1) : RowT(0);
+                const uint32_t *en = ment + moff;
+                int e = 0;
+                for (; e + 4 <= mcnt && group_any(acc != 0, Hq, lane); e += 4) {
+                    RowT v[4];
+                    uint32_t q[4];
 #pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    q[u] = en[e + u];
-                    v[u] = P[(q[u] & 255) * Hp + ry + ((q[u] >> 8) & 255)] >> ((q[u] >> 16) & 255);
-                }
+                    for (int u = 0; u < 4; ++u) {
+                        q[u] = en[e + u];
+                        v[u] = P[(q[u] & 255) * Hp + ry + ((q[u] >> 8) & 255)] >> ((q[u] >> 16) & 255);
+                    }
 #pragma unroll
-                for (int u = 0; u < 4; ++u) acc &= ((q[u] >> 24) & 1) ? v[u] : RowT(~v[u]);
-            }
-            for (; e < mcnt && group_any(acc != 0, Hq, lane); ++e) {
-                const uint32_t q = en[e];
-                const RowT v = P[(q & 255) * Hp + ry + ((q >> 8) & 255)] >> ((q >> 16) & 255);
-                acc &= ((q >> 24) & 1) ? v : RowT(~v);
-            }
-            if (group_any(acc != 0, Hq, lane)) {
-                M[size_t(r) * kMRows + kPad + y] = acc;
-                if (y == 0) fired[r] = 1;
-                rsum += hreward * popc(acc);
-                for (int ev = 0; ev < vcnt; ++ev) {
-                    const uint32_t v = vent[voff + ev];
-                    const int c = v & 255, i = (v >> 8) & 255, j = (v >> 16) & 255;
-                    const RowT src = from_lane(acc, lane - (y >= i ? i : 0));
-                    const RowT t = (y >= i) ? RowT(src << j) : RowT(0);
-                    if (row && t) lds_or(((v >> 24) & 1 ? PL : MI) + c * 64 + y, t);
+                    for (int u = 0; u < 4; ++u) acc &= ((q[u] >> 24) & 1) ? v[u] : RowT(~v[u]);
                 }
+                for (; e < mcnt && group_any(acc != 0, Hq, lane); ++e) {
+                    const uint32_t q = en[e];
+                    const RowT v = P[(q & 255) * Hp + ry + ((q >> 8) & 255)] >> ((q >> 16) & 255);
+                    acc &= ((q >> 24) & 1) ? v : RowT(~v);
+                }
+                if (group_any(acc != 0, Hq, lane)) {
+                    M[size_t(r) * kMRows + kPad + y] = acc;
+                    if (y == 0) fired[r] = 1;
+                    rsum += hreward * popc(acc);
+                    for (int ev = 0; ev < vcnt; ++ev) {
+                        const uint32_t v = vent[voff + ev];
+                        const int c = v & 255, i = (v >> 8) & 255, j = (v >> 16) & 255;
+                        const RowT src = from_lane(acc, lane - (y >= i ? i : 0));
+                        const RowT t = (y >= i) ? RowT(src << j) : RowT(0);
+                        if (row && t) lds_or(((v >> 24) & 1 ? PL : MI) + c * 64 + y, t);
+                    }
+                }
+            }
+            __syncthreads();
+
+            // new rows: group g rewrites planes g, g+4, ... (each lane its own row)
+            for (int c = g; c < Cw; c += kGroups) {
+                const RowT old = P[c * Hp + ry];
+                const RowT pl = PL[c * 64 + y], mi = MI[c * 64 + y];
+                RowT nw = (old | pl) & ~mi;
+                const RowT mixed = pl & mi;
+                if (group_any(mixed != 0, Hq, lane))
+                    nw = exact_channel<RowT>(c, old, rb, re, fired, hdrw, vent, M, y, Hq, lane);
+                if (row) P[c * Hp + y] = nw;
+                PL[c * 64 + y] = 0;
+                MI[c * 64 + y] = 0;
             }
         }
         if (rsum) atomicAdd(red, rsum);
-        __syncthreads();
-
-        // new rows: group g rewrites channels g, g+4, ... (each lane its own row)
-        for (int c = g; c < C; c += kGroups) {
-            const RowT old = P[c * Hp + ry];
-            const RowT pl = PL[c * 64 + y], mi = MI[c * 64 + y];
-            RowT nw = (old | pl) & ~mi;
-            RowT mixed = pl & mi;
-            if (group_any(mixed != 0, Hq, lane))
-                nw = exact_channel<RowT>(c, old, Rt, fired, hdrw, vent, M, y, Hq, lane);
-            if (row) P[c * Hp + y] = nw;
-            PL[c * 64 + y] = 0;
-            MI[c * 64 + y] = 0;
-        }
 
         // episode end, reward, outputs, reset
         const bool anyp = __syncthreads_or(g == kChPlayer % kGroups && row &&
@@ -276,7 +285,8 @@ int rows_per_group(int H) { return H <= 16 ? 16 : (H <= 32 ? 32 : 64); }
 
 size_t wave_base_bytes(int H, int W, int C, int rules_per_set) {
     const size_t rowb = W <= 32 ? 4 : 8;
-    return (size_t(C + 1) * (H + kPad) + size_t(rules_per_set) * kMRows + size_t(2) * C * 64) * rowb +
+    return (size_t(C + 1) * (H + kPad) + size_t(rules_per_set) * kMRows + size_t(2) * (C + 1) * 64) *
+               rowb +
            sizeof(int) * (size_t(rules_per_set) + 2);
 }
 

@@ -111,7 +111,7 @@ class Gen {
 
 bool lane16_eligible(const av_config &c) {
     return c.height <= 16 && c.width <= 16 && c.per_env_rules == 0 && c.max_pat_h <= 16 &&
-           c.max_pat_w <= 16;
+           c.max_pat_w <= 16 && c.rule_mode == AV_RULES_PARALLEL;
 }
 
 std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule> &rules) {

@@ -21,12 +21,12 @@ def say(msg):
 
 
 def gpu_run(wl, maps, rules, actions, engine="auto", mode="step", chunk=7, B=None,
-            per_step_maps=True):
+            per_step_maps=True, rule_mode="parallel"):
     """Returns (maps per step or None, final maps, rewards [T][B], done [T][B]) as numpy,
     and the engine the batch used."""
     import torch
     B = maps.shape[0] if B is None else B
-    b = av.Batch.for_workload(wl, B=B, engine=engine)
+    b = av.Batch.for_workload(wl, B=B, engine=engine, rule_mode=rule_mode)
     try:
         b.load_rules(*rules)
         b.reset(maps)

@@ -55,7 +55,7 @@ def test_no_torch_types_in_the_abi():
 def _cfg(**kw):
     base = dict(num_envs=4, height=16, width=16, channels=6, max_rules=8, max_pat_h=3,
                 max_pat_w=3, per_env_rules=0, max_episode_steps=0, device=0, engine=0,
-                stream=None)
+                rule_mode=0, stream=None)
     base.update(kw)
     return av.av_config(*[base[f] for f, _ in av.av_config._fields_])
 
@@ -66,6 +66,7 @@ def _cfg(**kw):
     dict(max_pat_w=17), dict(per_env_rules=2), dict(max_episode_steps=-1), dict(engine=9),
     # lane16 needs maps of at most 16 x 16 and one shared rule set
     dict(engine=2, height=32, width=32), dict(engine=2, per_env_rules=1),
+    dict(rule_mode=2), dict(rule_mode=-1),
     # the wave engine's LDS working set over 64 KiB (the generic engine's fits)
     dict(engine=3, channels=31, max_rules=140),
     # one environment's LDS working set over 64 KiB

@@ -1,0 +1,54 @@
+"""Sequential rule order on the GPU vs the oracle in sequential mode: every rule matched on
+the map the rules before it left (force plane included), each rule's matches applied
+together.  Maps, rewards and done flags compared after every step, and per step from
+av_step_n launches."""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import first_mismatch, gpu_run, require_gpu, say
+from paper_2407_04221_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+CASES = [("c1", 1, 60), ("c2", 75, 25), ("c3", 21, 20), ("c4", 133, 40), ("c5", 3, 10)]
+EXTRA = {
+    "odd": inputs.Workload("odd", 61, B=29, H=5, W=11, C=5, R=6,
+                           shapes=((1, 1), (2, 3), (3, 2)), p_dc=0.5, per_env=False, T=20, L=6),
+    "wide": inputs.Workload("wide", 62, B=7, H=33, W=40, C=6, R=5, shapes=((3, 3), (1, 4)),
+                            p_dc=0.5, per_env=True, T=10, L=5),
+}
+
+
+@pytest.mark.parametrize("variant", inputs.VARIANTS)
+@pytest.mark.parametrize("engine", ["generic", "wave", "auto"])
+@pytest.mark.parametrize("case", CASES, ids=[f"{n}-B{b}-T{t}" for n, b, t in CASES])
+def test_sequential_step_matches_oracle(case, engine, variant):
+    require_gpu()
+    name, B, T = case
+    wl = inputs.WORKLOADS[name].with_(B=B, T=T, L=15)
+    say(f"[sequential] {name} engine={engine} variant={variant}")
+    maps, rules, actions = inputs.make_all(wl, 3, variant)
+    want_m, want_r, want_d = oracle.run(wl, maps, rules, actions, nthreads=8, rule_mode=1)
+    seq, final, r, d, eng = gpu_run(wl, maps, rules, actions, engine=engine, mode="step",
+                                    rule_mode="sequential")
+    for t in range(T):
+        assert first_mismatch(seq[t], want_m[t]) is None, \
+            f"maps differ at step {t}, index {first_mismatch(seq[t], want_m[t])}"
+        np.testing.assert_array_equal(r[t], want_r[t], err_msg=f"rewards, step {t}")
+        np.testing.assert_array_equal(d[t], want_d[t], err_msg=f"done, step {t}")
+
+
+@pytest.mark.parametrize("engine", ["generic", "wave"])
+@pytest.mark.parametrize("name", sorted(EXTRA))
+def test_sequential_step_n_matches_oracle(name, engine):
+    require_gpu()
+    wl = EXTRA[name]
+    say(f"[sequential step_n] {name} engine={engine}")
+    maps, rules, actions = inputs.make_all(wl, 0, "dense")
+    want_m, want_r, want_d = oracle.run(wl, maps, rules, actions, nthreads=8, rule_mode=1)
+    _, final, r, d, _ = gpu_run(wl, maps, rules, actions, engine=engine, mode="step_n", chunk=6,
+                                rule_mode="sequential")
+    np.testing.assert_array_equal(r, want_r)
+    np.testing.assert_array_equal(d, want_d)
+    np.testing.assert_array_equal(final, want_m[-1])
