@@ -62,10 +62,9 @@ typedef enum {
 typedef enum {
     AV_ENGINE_AUTO = 0,
     AV_ENGINE_GENERIC = 1,  /* any size within the limits below; maps staged in LDS */
-    AV_ENGINE_LANE16 = 2,   /* maps of at most 16 x 16, one shared rule set, parallel rule
-                               mode: one map row per lane, two maps per 32-bit lane word,
-                               rows shifted across lanes with DPP, the rule set compiled
-                               into the kernel */
+    AV_ENGINE_LANE16 = 2,   /* maps of at most 16 x 16 and one shared rule set: one map
+                               row per lane, two maps per 32-bit lane word, rows shifted
+                               across lanes with DPP, the rule set compiled into the kernel */
     AV_ENGINE_WAVE = 3      /* one environment per 64-lane wave, map rows in LDS; rule
                                programs read with scalar loads (per-environment rules) */
 } av_engine;

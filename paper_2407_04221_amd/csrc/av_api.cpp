@@ -256,8 +256,8 @@ av_status av_create_batch(const av_config *cfg, av_batch_t *out) {
                     "channels or a smaller map", env_lds, kLdsBudget);
     const bool lane16_ok = lane16_eligible(c);
     if (c.engine == AV_ENGINE_LANE16 && !lane16_ok)
-        return fail(AV_EINVAL, "the lane16 engine needs H, W <= 16, one rule set shared by "
-                    "all environments and parallel rule mode");
+        return fail(AV_EINVAL, "the lane16 engine needs H, W <= 16 and one rule set shared by "
+                    "all environments");
     const size_t wave_lds = wave_lds_bytes(c.height, c.width, c.channels, c.max_rules + kMoveRules);
     const bool wave_ok = wave_lds <= size_t(kLdsBudget);
     if (c.engine == AV_ENGINE_WAVE && !wave_ok)
@@ -367,7 +367,8 @@ av_status av_load_rules(av_batch_t b, int32_t R, const int32_t *shape, const int
                 lr.in = hr.in; lr.out = hr.out;
                 lsets[s].push_back(std::move(lr));
             }
-        lane16_compile(lsets, c.channels, c.height, c.width, c.max_episode_steps, b->lprog);
+        lane16_compile(lsets, c.channels, c.height, c.width, c.max_episode_steps,
+                       c.rule_mode == AV_RULES_SEQUENTIAL, b->lprog);
         std::string log;
         hipError_t e = lane16_upload(b->lprog, b->dlprog, &log);
         if (e != hipSuccess)

@@ -32,10 +32,11 @@ struct Lane16Device {
 // shared rule set (the rules become code).  Pattern extents up to 16 fit DPP row shifts.
 bool lane16_eligible(const av_config &c);
 
-// Generate the kernel source for C stored channels, an H x W map, episode length L and a
-// rule list (the four moves first, then the loaded rules).
+// Generate the kernel source for C stored channels, an H x W map, episode length L, the
+// rule order (parallel or sequential) and a rule list (the four moves first, then the
+// loaded rules).
 void lane16_compile(const std::vector<std::vector<Lane16Rule>> &sets, int C, int H, int W,
-                    int L, Lane16Program &p);
+                    int L, bool sequential, Lane16Program &p);
 
 // Compile (hipRTC, gfx950) and load the program on the current device, reusing an
 // identical earlier build.  On failure returns an error and the compiler log in *log.

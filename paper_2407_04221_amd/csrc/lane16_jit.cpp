@@ -111,7 +111,7 @@ class Gen {
 
 bool lane16_eligible(const av_config &c) {
     return c.height <= 16 && c.width <= 16 && c.per_env_rules == 0 && c.max_pat_h <= 16 &&
-           c.max_pat_w <= 16 && c.rule_mode == AV_RULES_PARALLEL;
+           c.max_pat_w <= 16;
 }
 
 std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule> &rules) {
@@ -297,8 +297,156 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
     return o.str();
 }
 
+// Sequential rule order: one block per rule, in list order.  Each block derives its shifted
+// planes from the map as the rules before it left it (force plane included), matches the
+// rule, and applies its votes (exactly counted where its own matches overlap with both
+// signs) before the next block.
+std::string lane16_rules_body_sequential(int C, int H, int W, const std::vector<Lane16Rule> &rules) {
+    Gen g;
+    std::ostringstream &o = g.o;
+    const int C1 = C + 1, R = int(rules.size());
+    auto in_at = [&](const Lane16Rule &r, int c, int i, int j) {
+        return int(r.in[(size_t(c) * r.n + i) * r.m + j]);
+    };
+    auto out_at = [&](const Lane16Rule &r, int c, int i, int j) {
+        return int(r.out[(size_t(c) * r.n + i) * r.m + j]);
+    };
+    std::set<std::pair<int, int>> shapes;
+    for (const Lane16Rule &ru : rules) shapes.insert({ru.n, ru.m});
+    o << "// ---- generated: " << R << " rules in sequence over " << C1 << " planes ----\n";
+    for (auto &s : shapes)
+        o << "const u32 V" << s.first << "_" << s.second << " = (y <= " << (H - s.first)
+          << ") ? BOTH(COLMASK(" << std::max(0, W - s.second + 1) << ")) : 0u;\n";
+
+    for (int r = 0; r < R; ++r) {
+        const Lane16Rule &ru = rules[r];
+        std::vector<Entry> ents;
+        std::set<std::pair<int, int>> xs;
+        std::vector<std::vector<Vote>> plus(C1), minus(C1);
+        for (int c = 0; c < C1; ++c)
+            for (int i = 0; i < ru.n; ++i)
+                for (int j = 0; j < ru.m; ++j) {
+                    const int w = in_at(ru, c, i, j);
+                    if (w >= 0) {
+                        ents.push_back({c, i, j, w, rank_of(c, w, C)});
+                        if (j > 0) xs.insert({c, j});
+                    }
+                    const int k = kout(w, out_at(ru, c, i, j));
+                    if (k > 0) plus[c].push_back({r, i, j});
+                    if (k < 0) minus[c].push_back({r, i, j});
+                }
+        std::stable_sort(ents.begin(), ents.end(),
+                         [](const Entry &a, const Entry &b) { return a.rank < b.rank; });
+        auto base = [&](const Entry &e) {
+            return e.j ? "X" + std::to_string(e.c) + "_" + std::to_string(e.j) : plane(e.c, C);
+        };
+        auto row_and = [&](const std::vector<Entry> &es) {
+            std::string q;
+            for (const Entry &en : es) {
+                if (!q.empty()) q += " & ";
+                q += (en.want ? "" : "~") + base(en);
+            }
+            return q;
+        };
+        auto emit_rows = [&](const std::vector<Entry> &es) {
+            std::map<int, std::vector<Entry>> by_row;
+            for (const Entry &en : es) by_row[en.i].push_back(en);
+            for (auto &row : by_row) {
+                if (row.first == 0) o << "M &= " << row_and(row.second) << ";\n";
+                else o << "M &= DPP_SHL(" << row_and(row.second) << ", " << row.first << ");\n";
+            }
+        };
+        bool writes = false;
+        for (int c = 0; c < C1; ++c) writes |= !plus[c].empty() || !minus[c].empty();
+        if (!writes && ru.reward == 0) continue;   // a rule that neither writes nor pays
+
+        o << "{ // rule " << r << "\n";
+        for (auto &x : xs)
+            o << "const u32 X" << x.first << "_" << x.second << " = " << plane(x.first, C) << " >> "
+              << x.second << ";\n";
+        o << "u32 M = V" << ru.n << "_" << ru.m << ";\n";
+        const bool fixed = r < kMoveRules;
+        const size_t probe = fixed ? ents.size() : std::min<size_t>(2, ents.size());
+        int open = 0;
+        if (fixed) {
+            emit_rows(ents);
+        } else {
+            for (size_t e = 0; e < probe; ++e) {
+                const Entry &en = ents[e];
+                const std::string t = en.i ? "DPP_SHL(" + base(en) + ", " + std::to_string(en.i) + ")" : base(en);
+                o << "M &= " << (en.want ? "" : "~") << t << ";\n";
+            }
+            o << "if (ANY(M)) {\n";
+            ++open;
+            if (ents.size() > probe) {
+                emit_rows(std::vector<Entry>(ents.begin() + probe, ents.end()));
+                o << "if (ANY(M)) {\n";
+                ++open;
+            }
+        }
+        if (ru.reward != 0)
+            o << "rA += " << ru.reward << " * (int)__popc(M & 0xFFFFu); rB += " << ru.reward
+              << " * (int)__popc(M >> 16);\n";
+        // votes of this rule
+        std::set<int> js;
+        std::vector<int> touched, both;
+        for (int c = 0; c < C1; ++c) {
+            if (plus[c].empty() && minus[c].empty()) continue;
+            touched.push_back(c);
+            if (!plus[c].empty() && !minus[c].empty()) both.push_back(c);
+            for (auto *lst : {&plus[c], &minus[c]})
+                for (const Vote &v : *lst)
+                    if (v.j) js.insert(v.j);
+        }
+        for (int j : js) o << "const u32 L" << j << " = M << " << j << ";\n";
+        auto term = [&](const Vote &v) {
+            const std::string src = v.j ? "L" + std::to_string(v.j) : std::string("M");
+            return v.i ? "DPP_SHR(" + src + ", " + std::to_string(v.i) + ")" : src;
+        };
+        for (int c : touched) {
+            o << "u32 PL" << c << " = 0u, MI" << c << " = 0u;\n";
+            for (const Vote &v : plus[c]) o << "PL" << c << " |= " << term(v) << ";\n";
+            for (const Vote &v : minus[c]) o << "MI" << c << " |= " << term(v) << ";\n";
+            o << "u32 N" << c << " = (" << plane(c, C) << " | PL" << c << ") & ~MI" << c << ";\n";
+        }
+        if (!both.empty()) {
+            o << "u32 CF = 0u;\n";
+            for (int c : both) o << "CF |= PL" << c << " & MI" << c << ";\n";
+            o << "if (ANY(CF)) {\n";
+            std::set<std::pair<int, int>> tset;
+            for (int c : both)
+                for (auto *lst : {&plus[c], &minus[c]})
+                    for (const Vote &v : *lst) tset.insert({v.i, v.j});
+            auto tname = [](int i, int j) { return "T" + std::to_string(i) + "_" + std::to_string(j); };
+            for (auto &t : tset)
+                o << "const u32 " << tname(t.first, t.second) << " = " << term(Vote{r, t.first, t.second})
+                  << ";\n";
+            for (int c : both) {
+                std::vector<std::string> pt{plane(c, C)}, mt;
+                for (const Vote &v : plus[c]) pt.push_back(tname(v.i, v.j));
+                for (const Vote &v : minus[c]) mt.push_back(tname(v.i, v.j));
+                o << "{ // plane " << c << "\n";
+                const std::vector<std::string> Pb = g.count(pt), Nb = g.count(mt);
+                const size_t K = std::max(Pb.size(), Nb.size());
+                o << "u32 GT = 0u, EQ = 0xFFFFFFFFu;\n";
+                for (size_t k = K; k-- > 0;) {
+                    const std::string pk = k < Pb.size() ? Pb[k] : "0u", nk = k < Nb.size() ? Nb[k] : "0u";
+                    o << "GT |= EQ & " << pk << " & ~" << nk << ";\n";
+                    o << "EQ &= ~(" << pk << " ^ " << nk << ");\n";
+                }
+                o << "N" << c << " = GT;\n}\n";
+            }
+            o << "}\n";
+        }
+        for (int c : touched) o << plane(c, C) << " = N" << c << ";\n";
+        for (; open > 0; --open) o << "}\n";
+        o << "}\n";
+    }
+    return o.str();
+}
+
 void lane16_compile(const std::vector<std::vector<Lane16Rule>> &sets, int C, int H, int W, int L,
-                    Lane16Program &p) {
+                    bool sequential, Lane16Program &p) {
     std::string src = kLane16Template;
     std::ostringstream d;
     d << "#define AV_C " << C << "\n#define AV_H " << H << "\n#define AV_W " << W << "\n#define AV_L "
@@ -311,7 +459,8 @@ void lane16_compile(const std::vector<std::vector<Lane16Rule>> &sets, int C, int
         if (at != std::string::npos) src.replace(at, marker.size(), text);
     };
     put("/*@DEFINES@*/", d.str());
-    put("/*@RULES@*/", lane16_rules_body(C, H, W, sets.at(0)));
+    put("/*@RULES@*/", sequential ? lane16_rules_body_sequential(C, H, W, sets.at(0))
+                                  : lane16_rules_body(C, H, W, sets.at(0)));
     p.source = std::move(src);
 }
 

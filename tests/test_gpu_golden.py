@@ -19,7 +19,7 @@ def _cases():
         fx = fixtures.parse(path)
         name = path.rsplit("/", 1)[-1][:-3]
         engines = ["generic", "wave"]
-        if fx.mode == 0 and fx.H <= 16 and fx.W <= 16:
+        if fx.H <= 16 and fx.W <= 16:
             engines.append("lane16")
         out += [(name, path, e) for e in engines]
     return out

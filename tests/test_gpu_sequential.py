@@ -17,7 +17,11 @@ EXTRA = {
                            shapes=((1, 1), (2, 3), (3, 2)), p_dc=0.5, per_env=False, T=20, L=6),
     "wide": inputs.Workload("wide", 62, B=7, H=33, W=40, C=6, R=5, shapes=((3, 3), (1, 4)),
                             p_dc=0.5, per_env=True, T=10, L=5),
+    "square16": inputs.Workload("square16", 63, B=45, H=16, W=16, C=7, R=9,
+                                shapes=((3, 3), (1, 2), (4, 1)), p_dc=0.5, per_env=False, T=15,
+                                L=7),
 }
+LANE16 = {n for n, w in EXTRA.items() if w.H <= 16 and w.W <= 16 and not w.per_env}
 
 
 @pytest.mark.parametrize("variant", inputs.VARIANTS)
@@ -39,11 +43,13 @@ def test_sequential_step_matches_oracle(case, engine, variant):
         np.testing.assert_array_equal(d[t], want_d[t], err_msg=f"done, step {t}")
 
 
-@pytest.mark.parametrize("engine", ["generic", "wave"])
+@pytest.mark.parametrize("engine", ["generic", "wave", "lane16"])
 @pytest.mark.parametrize("name", sorted(EXTRA))
 def test_sequential_step_n_matches_oracle(name, engine):
     require_gpu()
     wl = EXTRA[name]
+    if engine == "lane16" and name not in LANE16:
+        pytest.skip("lane16 takes maps of at most 16 x 16 with one shared rule set")
     say(f"[sequential step_n] {name} engine={engine}")
     maps, rules, actions = inputs.make_all(wl, 0, "dense")
     want_m, want_r, want_d = oracle.run(wl, maps, rules, actions, nthreads=8, rule_mode=1)
