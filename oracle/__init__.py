@@ -43,12 +43,14 @@ def load(path: str = LIB) -> ctypes.CDLL:
     lib.avo_reset.argtypes = [P, P]
     lib.avo_step.argtypes = [P, P, P, P, I, ctypes.POINTER(I)]
     lib.avo_set_rule_mode.argtypes = [P, I]
+    lib.avo_observe.argtypes = [P, I, P]
+    lib.avo_rule_features.argtypes = [P, P]
     lib.avo_get_maps.argtypes = [P, P]
     lib.avo_get_counters.argtypes = [P, P]
     lib.avo_destroy.argtypes = [P]
     lib.avo_destroy.restype = None
     for f in ("avo_create", "avo_load_rules", "avo_reset", "avo_step", "avo_get_maps",
-              "avo_get_counters", "avo_set_rule_mode"):
+              "avo_get_counters", "avo_set_rule_mode", "avo_observe", "avo_rule_features"):
         getattr(lib, f).restype = I
     _libs[path] = lib
     return lib
@@ -130,6 +132,20 @@ class Oracle:
         rc = self.lib.avo_get_maps(self.h, _ptr(out))
         if rc != AVO_OK:
             raise OracleError("avo_get_maps", rc)
+        return out
+
+    def observe(self, w: int):
+        out = np.zeros((self.B, self.C, w, w), dtype=np.uint8)
+        rc = self.lib.avo_observe(self.h, int(w), _ptr(out))
+        if rc != AVO_OK:
+            raise OracleError("avo_observe", rc)
+        return out
+
+    def rule_features(self, S: int, R: int):
+        out = np.zeros((S, R, 2, 2, self.C + 1, self.max_h, self.max_w), dtype=np.uint8)
+        rc = self.lib.avo_rule_features(self.h, _ptr(out))
+        if rc != AVO_OK:
+            raise OracleError("avo_rule_features", rc)
         return out
 
     def counters(self):

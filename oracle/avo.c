@@ -333,6 +333,50 @@ int avo_get_maps(const avo_batch *ab, uint8_t *dst)
     return AVO_OK;
 }
 
+int avo_observe(const avo_batch *ab, int w, uint8_t *dst)
+{
+    if (!ab || !dst || w < 1) return AVO_EINVAL;
+    const int H = ab->H, W = ab->W, C = ab->C;
+    const size_t plane = (size_t)H * W;
+    for (int b = 0; b < ab->B; b++) {
+        const uint8_t *D = ab->maps + (size_t)b * C * plane;
+        uint8_t *out = dst + (size_t)b * C * w * w;
+        memset(out, 0, (size_t)C * w * w);
+        int py = -1, px = -1;
+        for (int y = 0; y < H && py < 0; y++)
+            for (int x = 0; x < W; x++)
+                if (D[(size_t)CH_PLAYER * plane + (size_t)y * W + x]) { py = y; px = x; break; }
+        if (py < 0) continue;
+        for (int c = 0; c < C; c++)
+            for (int wy = 0; wy < w; wy++)
+                for (int wx = 0; wx < w; wx++) {
+                    int y = py - w / 2 + wy, x = px - w / 2 + wx;
+                    if (y < 0 || y >= H || x < 0 || x >= W) continue;
+                    out[((size_t)c * w + wy) * w + wx] = D[(size_t)c * plane + (size_t)y * W + x];
+                }
+    }
+    return AVO_OK;
+}
+
+int avo_rule_features(const avo_batch *ab, uint8_t *dst)
+{
+    if (!ab || !dst) return AVO_EINVAL;
+    if (!ab->have_rules) return AVO_ESTATE;
+    const int S = ab->per_env ? ab->B : 1;
+    const size_t pat = (size_t)(ab->C + 1) * ab->max_h * ab->max_w;
+    for (size_t k = 0; k < (size_t)S * ab->R; k++)
+        for (int io = 0; io < 2; io++) {
+            const int8_t *src = (io ? ab->out_pat : ab->in_pat) + k * pat;
+            uint8_t *spec = dst + ((k * 2 + io) * 2 + 0) * pat;
+            uint8_t *val = dst + ((k * 2 + io) * 2 + 1) * pat;
+            for (size_t e = 0; e < pat; e++) {
+                spec[e] = src[e] != -1;
+                val[e] = src[e] == 1;
+            }
+        }
+    return AVO_OK;
+}
+
 int avo_get_counters(const avo_batch *ab, int32_t *dst)
 {
     if (!ab || !dst) return AVO_EINVAL;

@@ -52,6 +52,16 @@ int  avo_step(avo_batch *ab, const uint8_t *actions, float *rewards, uint8_t *do
  * applied together). */
 int  avo_set_rule_mode(avo_batch *ab, int mode);
 int  avo_get_maps(const avo_batch *ab, uint8_t *dst);
+/* Player-centred observation of the current maps (paper Sec. 2.2.2: a local patch of tiles
+ * around the player's position; Table 1 uses windows of 5, 10, 20 and 31 cells).
+ * dst uint8 [B][C][w][w]: window cell (wy, wx) shows map cell (py - w/2 + wy, px - w/2 + wx),
+ * with (py, px) the environment's first player cell in row-major order and w/2 rounded
+ * down; cells off the map, and every cell when there is no player, are 0. */
+int  avo_observe(const avo_batch *ab, int w, uint8_t *dst);
+/* The loaded rules as binary features (paper Sec. 2.2.2: the observation also holds a binary
+ * representation of the environment's rules).  dst uint8 [S][R][2][2][C+1][max_h][max_w]:
+ * [.][.][0 = input, 1 = output][0 = entry specified, 1 = entry value (0 when unspecified)]. */
+int  avo_rule_features(const avo_batch *ab, uint8_t *dst);
 int  avo_get_counters(const avo_batch *ab, int32_t *dst);
 void avo_destroy(avo_batch *ab);
 
