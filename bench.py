@@ -102,6 +102,8 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="before timing, copy MIB MiB with a plain device copy (a known-size "
                          "reference for the HBM byte counters)")
+    ap.add_argument("--observe", type=int, default=0, metavar="W",
+                    help="also time av_observe with a W x W window (HBM-bound gather)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
@@ -187,6 +189,28 @@ def main():
                       "env_steps_per_sec": wl.B * n / (ms1 / 1e3),
                       "frac_hbm_roofline": wl.B * n / (ms1 / 1e3) / roof_env_steps}
 
+    observe = None
+    if args.observe:
+        w = args.observe
+        obs = torch.empty((wl.B, wl.C, w, w), dtype=torch.uint8, device="cuda")
+        av.av_observe(b.h, w, obs)
+        torch.cuda.synchronize()
+        reps = 200
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        g0.record(stream)
+        for _ in range(reps):
+            av.av_observe(b.h, w, obs)
+        g1.record(stream)
+        torch.cuda.synchronize()
+        us = g0.elapsed_time(g1) * 1e3 / reps
+        moved = wl.B * (wl.C * w * w + wl.C * wl.H * wl.W // 8)   # window out, packed maps in
+        observe = {"api": "av_observe", "w": w, "us_per_call": us,
+                   "obs_per_sec": wl.B / (us * 1e-6),
+                   "roofline": {"bound": "hbm", "achieved": moved / (us * 1e-6) / 1e9,
+                                "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                "frac": moved / (us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+                                "bytes_per_call": moved}}
+
     cpu = None
     if not args.no_cpu:
         cpu = cpu_baseline(wl, maps, rules, actions, args.cpu_seconds,
@@ -232,6 +256,7 @@ def main():
             "busy": traffic["valu_busy"], "insts_per_wave_step": traffic["valu_insts_per_wave_step"],
             "peak_lane_ops": 256 * 4 * 16 * 2.4e9, "source": traffic["source"]},
         "per_launch_path": per_launch,
+        "observe": observe,
         "cpu_baseline": cpu,
     }
     b.close()

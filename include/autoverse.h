@@ -141,6 +141,21 @@ av_status av_step_n(av_batch_t b, int32_t k, const uint8_t *actions, float *rewa
 /* Current maps as device uint8 [B][C][H][W] (0/1) written to dst.  Asynchronous. */
 av_status av_get_maps(av_batch_t b, uint8_t *dst);
 
+/* The player-centred observation of the current maps (paper Sec. 2.2.2: a local patch of
+ * tiles centred on the player's position; Table 1 uses windows of 5, 10, 20 and 31 cells).
+ * dst: device uint8 [B][C][w][w], w in [1, 255].  Window cell (wy, wx) shows map cell
+ * (py - w/2 + wy, px - w/2 + wx), where (py, px) is the environment's first player cell in
+ * row-major order and w/2 is rounded down; cells off the map, and the whole window of an
+ * environment without a player, are 0.  Asynchronous. */
+av_status av_observe(av_batch_t b, int32_t w, uint8_t *dst);
+
+/* The loaded rules as binary features (paper Sec. 2.2.2: the agent also observes a binary
+ * representation of its environment's rules).  dst: device uint8
+ * [S][R][2][2][C+1][max_pat_h][max_pat_w] with S = B if per_env_rules else 1: index 2 is
+ * 0 input / 1 output pattern, index 3 is 0 "entry specified" / 1 "entry value" (0 when not
+ * specified).  AV_ESTATE before av_load_rules.  May synchronise. */
+av_status av_rule_features(av_batch_t b, uint8_t *dst);
+
 /* Device pointer to the packed current maps, owned by the batch and valid until the
  * next av_reset / av_set_state / av_destroy_batch.  Layout: rows of row_bytes bytes,
  * index [c][env][y] (channel-major over the whole batch); cell (env, c, y, x) is bit x

@@ -27,8 +27,9 @@ RULE_MODES = {"parallel": AV_RULES_PARALLEL, "sequential": AV_RULES_SEQUENTIAL}
 
 # Every symbol include/autoverse.h declares.
 ABI_SYMBOLS = ("av_create_batch", "av_load_rules", "av_reset", "av_step", "av_step_n",
-               "av_get_maps", "av_state_ptr", "av_get_info", "av_get_state", "av_set_state",
-               "av_set_stream", "av_destroy_batch", "av_last_error")
+               "av_get_maps", "av_observe", "av_rule_features", "av_state_ptr", "av_get_info",
+               "av_get_state", "av_set_state", "av_set_stream", "av_destroy_batch",
+               "av_last_error")
 
 
 class av_config(ctypes.Structure):
@@ -75,6 +76,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "av_step": ([P, P, P, P], ctypes.c_int),
         "av_step_n": ([P, I32, P, P, P], ctypes.c_int),
         "av_get_maps": ([P, P], ctypes.c_int),
+        "av_observe": ([P, I32, P], ctypes.c_int),
+        "av_rule_features": ([P, P], ctypes.c_int),
         "av_state_ptr": ([P], P),
         "av_get_info": ([P, ctypes.POINTER(av_info)], ctypes.c_int),
         "av_get_state": ([P, P, ctypes.POINTER(SZ)], ctypes.c_int),
@@ -192,6 +195,24 @@ def av_get_maps(batch, dst):
     _check("av_get_maps", load_library().av_get_maps(batch, _dev_ptr(dst, torch.uint8, shp, "dst")))
 
 
+def av_observe(batch, w, dst):
+    """dst: device uint8 tensor [B][C][w][w]."""
+    info = av_get_info(batch)
+    shp = (info["num_envs"], info["channels"], w, w)
+    torch = _torch()
+    _check("av_observe", load_library().av_observe(batch, int(w),
+                                                   _dev_ptr(dst, torch.uint8, shp, "dst")))
+
+
+def av_rule_features(batch, dst):
+    """dst: device uint8 tensor [S][R][2][2][C+1][max_pat_h][max_pat_w] (contiguous)."""
+    torch = _torch()
+    if not isinstance(dst, torch.Tensor) or not dst.is_cuda or dst.dtype != torch.uint8 \
+            or not dst.is_contiguous():
+        raise TypeError("dst must be a contiguous uint8 device tensor")
+    _check("av_rule_features", load_library().av_rule_features(batch, ctypes.c_void_p(dst.data_ptr())))
+
+
 def av_state_ptr(batch) -> int:
     p = load_library().av_state_ptr(batch)
     if not p:
@@ -286,6 +307,13 @@ class Batch:
             out = torch.empty((self.B, self.C, self.H, self.W), dtype=torch.uint8,
                               device=self.device)
         av_get_maps(self.h, out)
+        return out
+
+    def observe(self, w, out=None):
+        torch = _torch()
+        if out is None:
+            out = torch.empty((self.B, self.C, w, w), dtype=torch.uint8, device=self.device)
+        av_observe(self.h, w, out)
         return out
 
     def state_ptr(self) -> int:

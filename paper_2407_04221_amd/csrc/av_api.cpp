@@ -62,6 +62,7 @@ struct av_batch_s {
     int engine = AV_ENGINE_GENERIC;
     bool have_rules = false, have_maps = false;
     int32_t R = 0;
+    std::vector<uint8_t> features;   // binary rule features, [S][R][2][2][C+1][mh][mw]
     GenericProgram prog;
     DeviceProgram dprog;
     Lane16Program lprog;           // compiled form for the lane16 engine (when chosen)
@@ -343,6 +344,17 @@ av_status av_load_rules(av_batch_t b, int32_t R, const int32_t *shape, const int
             return fail(AV_EINVAL, "set %d: |reward| x anchors sums to %lld >= 2^24; the float "
                         "reward would not be exact", s, worst);
     }
+    std::vector<uint8_t> feats(size_t(S) * R * 4 * pat);
+    for (size_t k = 0; k < size_t(S) * R; ++k)
+        for (int io = 0; io < 2; ++io) {
+            const int8_t *src = (io ? out_pat : in_pat) + k * pat;
+            uint8_t *spec = &feats[((k * 2 + io) * 2 + 0) * pat];
+            uint8_t *val = &feats[((k * 2 + io) * 2 + 1) * pat];
+            for (size_t e = 0; e < pat; ++e) {
+                spec[e] = src[e] != -1;
+                val[e] = src[e] == 1;
+            }
+        }
     if (av_status st = set_device(b)) return st;
     AV_HIP(hipStreamSynchronize(b->stream));   // no step may still read the old program
     free_device_program(b);
@@ -375,6 +387,7 @@ av_status av_load_rules(av_batch_t b, int32_t R, const int32_t *shape, const int
             return fail(AV_EDEVICE, "lane16 kernel build: %s %s", hipGetErrorString(e), log.c_str());
     }
     b->R = R;
+    b->features.swap(feats);
     b->have_rules = true;
     return AV_OK;
 }
@@ -437,6 +450,32 @@ av_status av_get_maps(av_batch_t b, uint8_t *dst) {
     const av_config &c = b->cfg;
     AV_HIP(launch_unpack(b->d_state, dst, c.num_envs, c.channels, c.height, c.width, b->row_bytes,
                          b->stream));
+    return AV_OK;
+}
+
+av_status av_observe(av_batch_t b, int32_t w, uint8_t *dst) {
+    g_last_error.clear();
+    if (av_status st = check_batch(b)) return st;
+    if (!dst) return fail(AV_EINVAL, "dst is NULL");
+    if (w < 1 || w > 255) return fail(AV_EINVAL, "window size %d outside [1, 255]", w);
+    if (!b->have_maps) return fail(AV_ESTATE, "call av_reset first");
+    if (av_status st = set_device(b)) return st;
+    const av_config &c = b->cfg;
+    AV_HIP(launch_observe(b->d_state, c.num_envs, c.channels, c.height, c.width, b->row_bytes, w,
+                          dst, b->stream));
+    return AV_OK;
+}
+
+av_status av_rule_features(av_batch_t b, uint8_t *dst) {
+    g_last_error.clear();
+    if (av_status st = check_batch(b)) return st;
+    if (!dst) return fail(AV_EINVAL, "dst is NULL");
+    if (!b->have_rules) return fail(AV_ESTATE, "call av_load_rules first");
+    if (av_status st = set_device(b)) return st;
+    if (!b->features.empty())
+        AV_HIP(hipMemcpyAsync(dst, b->features.data(), b->features.size(), hipMemcpyHostToDevice,
+                              b->stream));
+    AV_HIP(hipStreamSynchronize(b->stream));
     return AV_OK;
 }
 

@@ -102,7 +102,11 @@ hipError_t launch_unpack(const void *src, uint8_t *dst, int B, int C, int H, int
 hipError_t launch_generic_step(const StepArgs &a, int envs_per_block, hipStream_t s);
 size_t generic_env_lds_bytes(int H, int W, int C, int rules_per_set);
 
-// The wave engine (k_wave.hip): one environment per 64-lane workgroup.
+// Player-centred observation window (k_observe.hip).
+hipError_t launch_observe(const void *state, int B, int C, int H, int W, int row_bytes, int w,
+                          uint8_t *dst, hipStream_t s);
+
+// The wave engine (k_wave.hip): one environment per workgroup.
 size_t wave_lds_bytes(int H, int W, int C, int rules_per_set);
 hipError_t launch_wave_step(const StepArgs &a, hipStream_t s);
 

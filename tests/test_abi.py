@@ -34,7 +34,7 @@ def lib():
 
 def test_every_declared_function_is_exported(lib):
     names = declared_functions()
-    assert len(names) >= 13
+    assert len(names) >= 15
     assert set(names) == set(av.ABI_SYMBOLS)
     out = subprocess.run(["nm", "-D", "--defined-only", av.LIB_PATH], capture_output=True,
                          text=True, check=True).stdout
@@ -92,6 +92,8 @@ def test_null_arguments_are_rejected(lib):
     assert lib.av_load_rules(None, 0, None, None, None, None) == av.AV_EINVAL
     assert lib.av_reset(None, None) == av.AV_EINVAL
     assert lib.av_get_maps(None, None) == av.AV_EINVAL
+    assert lib.av_observe(None, 5, None) == av.AV_EINVAL
+    assert lib.av_rule_features(None, None) == av.AV_EINVAL
     assert lib.av_state_ptr(None) is None
     info = av.av_info()
     assert lib.av_get_info(None, ctypes.byref(info)) == av.AV_EINVAL
