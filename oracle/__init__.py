@@ -43,6 +43,11 @@ def load(path: str = LIB) -> ctypes.CDLL:
     lib.avo_reset.argtypes = [P, P]
     lib.avo_step.argtypes = [P, P, P, P, I, ctypes.POINTER(I)]
     lib.avo_set_rule_mode.argtypes = [P, I]
+    lib.avo_set_rule_control.argtypes = [P, P, P, I, ctypes.c_uint64]
+    lib.avo_site_key.argtypes = [I, ctypes.c_uint64, ctypes.c_uint64, I, I]
+    lib.avo_site_key.restype = ctypes.c_uint32
+    lib.avo_philox4x64.argtypes = [P, P, P]
+    lib.avo_philox4x64.restype = None
     lib.avo_observe.argtypes = [P, I, P]
     lib.avo_rule_features.argtypes = [P, P]
     lib.avo_get_maps.argtypes = [P, P]
@@ -50,7 +55,8 @@ def load(path: str = LIB) -> ctypes.CDLL:
     lib.avo_destroy.argtypes = [P]
     lib.avo_destroy.restype = None
     for f in ("avo_create", "avo_load_rules", "avo_reset", "avo_step", "avo_get_maps",
-              "avo_get_counters", "avo_set_rule_mode", "avo_observe", "avo_rule_features"):
+              "avo_get_counters", "avo_set_rule_mode", "avo_observe", "avo_rule_features",
+              "avo_set_rule_control"):
         getattr(lib, f).restype = I
     _libs[path] = lib
     return lib
@@ -107,6 +113,21 @@ class Oracle:
         if rc != AVO_OK:
             raise OracleError("avo_load_rules", rc)
 
+    def set_rule_control(self, limit=None, inhibit=None, order: int = 0, seed: int = 0):
+        """Rule application control: limit int32 [S][R] (0 = all), inhibit uint8 [S][R][R]
+        ([q][r]: q inhibits r, q < r), order 0 row-major / 1 random, seed of the random
+        index channel.  Cleared by load_rules."""
+        lp = ip = None
+        if limit is not None:
+            limit = np.ascontiguousarray(limit, dtype=np.int32)
+            lp = _ptr(limit)
+        if inhibit is not None:
+            inhibit = np.ascontiguousarray(inhibit, dtype=np.uint8)
+            ip = _ptr(inhibit)
+        rc = self.lib.avo_set_rule_control(self.h, lp, ip, int(order), int(seed))
+        if rc != AVO_OK:
+            raise OracleError("avo_set_rule_control", rc)
+
     def reset(self, init_maps):
         m = np.ascontiguousarray(init_maps, dtype=np.uint8)
         assert m.shape == (self.B, self.C, self.H, self.W), m.shape
@@ -156,13 +177,29 @@ class Oracle:
         return out
 
 
+def site_key(order: int, seed: int, n: int, b: int, pos: int, lib_path: str = LIB) -> int:
+    """The oracle's index-channel value of anchor pos of env b at batch step n."""
+    return int(load(lib_path).avo_site_key(order, seed, n, b, pos))
+
+
+def philox4x64(ctr, key, lib_path: str = LIB):
+    c = np.ascontiguousarray(ctr, dtype=np.uint64)
+    k = np.ascontiguousarray(key, dtype=np.uint64)
+    out = np.zeros(4, np.uint64)
+    load(lib_path).avo_philox4x64(_ptr(c), _ptr(k), _ptr(out))
+    return out
+
+
 def run(wl, maps, rules, actions, nthreads: int = 1, B=None, lib_path: str = LIB,
-        rule_mode: int = 0):
+        rule_mode: int = 0, control=None):
     """Step a workload's arrays for len(actions) steps; returns the per-step trajectory
-    (maps [T][B][C][H][W], rewards [T][B], done [T][B])."""
+    (maps [T][B][C][H][W], rewards [T][B], done [T][B]).  control: None or
+    (limit, inhibit, order, seed) for set_rule_control."""
     B = maps.shape[0] if B is None else B
     o = Oracle.for_workload(wl, B=B, lib_path=lib_path, rule_mode=rule_mode)
     o.load_rules(*rules)
+    if control is not None:
+        o.set_rule_control(*control)
     o.reset(maps)
     T = actions.shape[0]
     out_maps = np.zeros((T,) + maps.shape, dtype=np.uint8)

@@ -27,6 +27,10 @@
  *     In sequential mode (the paper's alternative "sequence of convolutions" reading),
  *     steps 4-7 run once per rule in list order instead: each rule is matched on the map
  *     the rules before it left, and its own votes are applied before the next rule.
+ *     With rule application control (Sec. 2.1.1), a loaded rule's matches are first
+ *     filtered: matches whose patch overlaps an applied match of an inhibiting earlier rule
+ *     are dropped, and of the rest only the `limit` ones with the largest index-channel
+ *     value are kept; rewards and votes use the kept matches.
  *  8. F is dropped.  The step counter advances; the episode is done when no player tile
  *     is left (a kill rule, Sec. 2.2.1) or the counter reaches the episode length.
  *     A done environment is reset to its initial map within the same step.
@@ -53,6 +57,11 @@ struct avo_batch {
     uint8_t *maps;       /* [B][C][H][W] */
     uint8_t *init_maps;  /* [B][C][H][W] */
     int32_t *t;          /* [B] steps since the last reset */
+    int32_t *limit;      /* [S][R] or NULL: matches applied per step, 0 = all */
+    uint8_t *inhibit;    /* [S][R][R] or NULL: [q][r] = rule q inhibits rule r */
+    int site_order;      /* 0 row-major, 1 random index channel */
+    uint64_t seed;       /* key of the random index channel */
+    uint64_t step_no;    /* batch steps since avo_reset */
 };
 
 /* A rule as the step uses it: patterns over C+1 channels, n x m, with its reward. */
@@ -125,7 +134,10 @@ int avo_load_rules(avo_batch *ab, int R, const int32_t *shape, const int8_t *in_
         if (worst >= AVO_REWARD_LIMIT) return AVO_EINVAL;
     }
     free(ab->shape); free(ab->in_pat); free(ab->out_pat); free(ab->reward);
+    free(ab->limit); free(ab->inhibit);
     ab->shape = NULL; ab->in_pat = NULL; ab->out_pat = NULL; ab->reward = NULL;
+    ab->limit = NULL; ab->inhibit = NULL;
+    ab->site_order = 0; ab->seed = 0;
     ab->R = R;
     size_t nr = (size_t)S * R;
     if (nr > 0) {
@@ -152,6 +164,7 @@ int avo_reset(avo_batch *ab, const uint8_t *init_maps)
         ab->maps[k] = ab->init_maps[k];
     }
     memset(ab->t, 0, (size_t)ab->B * sizeof(int32_t));
+    ab->step_no = 0;
     ab->have_maps = 1;
     return AVO_OK;
 }
@@ -199,8 +212,71 @@ static int rule_matches(const uint8_t *X, int H, int W, const rule_view *rv, int
     return 1;
 }
 
+/* Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC 2011): ten rounds of two 64 x 64 -> 128-bit
+ * multiplications with a Weyl-sequence key schedule. */
+void avo_philox4x64(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4])
+{
+    uint64_t x0 = ctr[0], x1 = ctr[1], x2 = ctr[2], x3 = ctr[3];
+    uint64_t k0 = key[0], k1 = key[1];
+    for (int round = 0; round < 10; round++) {
+        unsigned __int128 p0 = (unsigned __int128)0xD2E7470EE14C6C93ULL * x0;
+        unsigned __int128 p1 = (unsigned __int128)0xCA5A826395121157ULL * x2;
+        uint64_t hi0 = (uint64_t)(p0 >> 64), lo0 = (uint64_t)p0;
+        uint64_t hi1 = (uint64_t)(p1 >> 64), lo1 = (uint64_t)p1;
+        x0 = hi1 ^ x1 ^ k0;
+        x1 = lo1;
+        x2 = hi0 ^ x3 ^ k1;
+        x3 = lo0;
+        k0 += 0x9E3779B97F4A7C15ULL;
+        k1 += 0xBB67AE8584CAA73BULL;
+    }
+    out[0] = x0; out[1] = x1; out[2] = x2; out[3] = x3;
+}
+
+uint32_t avo_site_key(int order, uint64_t seed, uint64_t n, int b, int pos)
+{
+    uint32_t rank = (uint32_t)(4095 - pos);
+    if (order == 0) return rank;
+    uint64_t ctr[4] = {(uint64_t)(pos / 8), n, (uint64_t)b, 0};
+    uint64_t key[2] = {seed, 0};
+    uint64_t out[4];
+    avo_philox4x64(ctr, key, out);
+    int word = pos % 8;
+    uint32_t u = (uint32_t)(out[word / 2] >> (32 * (word % 2)));
+    return (u & 0xFFFFF000u) | rank;
+}
+
+/* Is the match of loaded rule r (set s) at (ay, ax), an n x m patch, inhibited: does its
+ * patch overlap the patch of an applied match of some rule q < r that inhibits r?
+ * applied[q] holds the applied anchors of loaded rule q in this step. */
+static int inhibited(const avo_batch *ab, int s, int r, int n, int m, int ay, int ax,
+                     const uint8_t *applied)
+{
+    const int H = ab->H, W = ab->W, R = ab->R;
+    const size_t plane = (size_t)H * W;
+    for (int q = 0; q < r; q++) {
+        if (!ab->inhibit[((size_t)s * R + q) * R + r]) continue;
+        int nq = ab->shape[((size_t)s * R + q) * 2 + 0];
+        int mq = ab->shape[((size_t)s * R + q) * 2 + 1];
+        /* patches [by, by+nq) x [bx, bx+mq) and [ay, ay+n) x [ax, ax+m) overlap */
+        for (int by = 0; by + nq <= H; by++)
+            for (int bx = 0; bx + mq <= W; bx++) {
+                if (!applied[(size_t)q * plane + (size_t)by * W + bx]) continue;
+                if (by < ay + n && ay < by + nq && bx < ax + m && ax < bx + mq) return 1;
+            }
+    }
+    return 0;
+}
+
+static int cmp_desc_u32(const void *a, const void *b)
+{
+    uint32_t x = *(const uint32_t *)a, y = *(const uint32_t *)b;
+    return x < y ? 1 : (x > y ? -1 : 0);
+}
+
 static void step_env(avo_batch *ab, int b, uint8_t action, float *reward_out,
-                     uint8_t *done_out, uint8_t *X, int32_t *delta)
+                     uint8_t *done_out, uint8_t *X, int32_t *delta, uint8_t *applied,
+                     uint32_t *keys)
 {
     const int H = ab->H, W = ab->W, C = ab->C, C1 = C + 1, F = C;
     const size_t plane = (size_t)H * W;
@@ -247,18 +323,46 @@ static void step_env(avo_batch *ab, int b, uint8_t action, float *reward_out,
             rv.in = ab->in_pat + k * pat; rv.out = ab->out_pat + k * pat;
             rv.ph = ab->max_h; rv.pw = ab->max_w;
         }
+        /* the rule's matches; with application control, filtered (Sec. 2.1.1) */
+        const int loaded = r >= 4;
+        uint8_t *A = applied + (size_t)(loaded ? r - 4 : ab->R) * plane;  /* moves: last slot */
+        const int lim = (loaded && ab->limit) ? ab->limit[(size_t)s * ab->R + (r - 4)] : 0;
+        int count = 0;
+        memset(A, 0, plane);
         for (int ay = 0; ay + rv.n <= H; ay++)
             for (int ax = 0; ax + rv.m <= W; ax++) {
-                if (!rule_matches(X, H, W, &rv, C1, ay, ax)) continue;
-                rho += rv.reward;
-                for (int c = 0; c < C1; c++)
-                    for (int i = 0; i < rv.n; i++)
-                        for (int j = 0; j < rv.m; j++) {
-                            int k = kernel_out(pat_at(rv.in, rv.ph, rv.pw, c, i, j),
-                                               pat_at(rv.out, rv.ph, rv.pw, c, i, j));
-                            delta[(size_t)c * plane + (size_t)(ay + i) * W + ax + j] += k;
-                        }
+                int hit = rule_matches(X, H, W, &rv, C1, ay, ax);
+                if (hit && loaded && ab->inhibit &&
+                    inhibited(ab, s, r - 4, rv.n, rv.m, ay, ax, applied))
+                    hit = 0;
+                if (!hit) continue;
+                A[(size_t)ay * W + ax] = 1;
+                count++;
             }
+        if (lim > 0 && count > lim) {
+            /* keep the lim matches with the largest keys: find the lim-th largest key */
+            int nk = 0;
+            for (size_t p = 0; p < plane; p++)
+                if (A[p]) keys[nk++] = avo_site_key(ab->site_order, ab->seed, ab->step_no, b, (int)p);
+            qsort(keys, (size_t)nk, sizeof(uint32_t), cmp_desc_u32);
+            uint32_t cut = keys[lim - 1];
+            for (size_t p = 0; p < plane; p++)
+                if (A[p] && avo_site_key(ab->site_order, ab->seed, ab->step_no, b, (int)p) < cut)
+                    A[p] = 0;
+        }
+        /* 5-6. reward and votes of the applied matches */
+        for (size_t p = 0; p < plane; p++) {
+            if (!A[p]) continue;
+            const int ay = (int)(p / W), ax = (int)(p % W);
+            rho += rv.reward;
+            for (int c = 0; c < C1; c++)
+                for (int i = 0; i < rv.n; i++)
+                    for (int j = 0; j < rv.m; j++) {
+                        int k = kernel_out(pat_at(rv.in, rv.ph, rv.pw, c, i, j),
+                                           pat_at(rv.out, rv.ph, rv.pw, c, i, j));
+                        delta[(size_t)c * plane + (size_t)(ay + i) * W + ax + j] += k;
+                    }
+        }
         if (ab->rule_mode == 1) {   /* sequential: this rule's votes take effect now */
             for (size_t k = 0; k < (size_t)C1 * plane; k++) {
                 X[k] = (X[k] + delta[k] >= 1) ? 1 : 0;
@@ -295,11 +399,19 @@ int avo_step(avo_batch *ab, const uint8_t *actions, float *rewards, uint8_t *don
 #ifndef _OPENMP
     nthreads = 1;
 #endif
-    /* per-thread scratch: the extended map and the vote sums */
-    const size_t ext = (size_t)(ab->C + 1) * ab->H * ab->W;
+    /* per-thread scratch: the extended map, the vote sums, the applied anchors of every
+     * loaded rule and the keys of one rule's matches */
+    const size_t plane = (size_t)ab->H * ab->W;
+    const size_t ext = (size_t)(ab->C + 1) * plane;
+    const size_t app = (size_t)(ab->R + 1) * plane;
     uint8_t *X = (uint8_t *)malloc(ext * nthreads);
     int32_t *delta = (int32_t *)malloc(ext * nthreads * sizeof(int32_t));
-    if (!X || !delta) { free(X); free(delta); return AVO_ENOMEM; }
+    uint8_t *applied = (uint8_t *)malloc(app * nthreads);
+    uint32_t *keys = (uint32_t *)malloc(plane * nthreads * sizeof(uint32_t));
+    if (!X || !delta || !applied || !keys) {
+        free(X); free(delta); free(applied); free(keys);
+        return AVO_ENOMEM;
+    }
     int got = 1;
 #ifdef _OPENMP
 #pragma omp parallel for num_threads(nthreads) schedule(static)
@@ -311,10 +423,14 @@ int avo_step(avo_batch *ab, const uint8_t *actions, float *rewards, uint8_t *don
         if (tid == 0) got = omp_get_num_threads();
 #endif
         step_env(ab, b, actions[b], rewards, done, X + (size_t)tid * ext,
-                 delta + (size_t)tid * ext);
+                 delta + (size_t)tid * ext, applied + (size_t)tid * app,
+                 keys + (size_t)tid * plane);
     }
+    ab->step_no += 1;
     free(X);
     free(delta);
+    free(applied);
+    free(keys);
     if (used) *used = got;
     return AVO_OK;
 }
@@ -323,6 +439,38 @@ int avo_set_rule_mode(avo_batch *ab, int mode)
 {
     if (!ab || (mode != 0 && mode != 1)) return AVO_EINVAL;
     ab->rule_mode = mode;
+    return AVO_OK;
+}
+
+int avo_set_rule_control(avo_batch *ab, const int32_t *limit, const uint8_t *inhibit,
+                         int order, uint64_t seed)
+{
+    if (!ab || (order != 0 && order != 1)) return AVO_EINVAL;
+    if (!ab->have_rules) return AVO_ESTATE;
+    const int R = ab->R;
+    const size_t S = ab->per_env ? (size_t)ab->B : 1;
+    if (limit)
+        for (size_t k = 0; k < S * R; k++)
+            if (limit[k] < 0) return AVO_EINVAL;
+    if (inhibit)
+        for (size_t s = 0; s < S; s++)
+            for (int q = 0; q < R; q++)
+                for (int r = 0; r <= q; r++)
+                    if (inhibit[(s * R + q) * R + r]) return AVO_EINVAL;
+    free(ab->limit); free(ab->inhibit);
+    ab->limit = NULL; ab->inhibit = NULL;
+    if (limit && R > 0) {
+        ab->limit = (int32_t *)malloc(S * R * sizeof(int32_t));
+        if (!ab->limit) return AVO_ENOMEM;
+        memcpy(ab->limit, limit, S * R * sizeof(int32_t));
+    }
+    if (inhibit && R > 0) {
+        ab->inhibit = (uint8_t *)malloc(S * R * R);
+        if (!ab->inhibit) return AVO_ENOMEM;
+        memcpy(ab->inhibit, inhibit, S * R * R);
+    }
+    ab->site_order = order;
+    ab->seed = seed;
     return AVO_OK;
 }
 
@@ -389,5 +537,6 @@ void avo_destroy(avo_batch *ab)
     if (!ab) return;
     free(ab->shape); free(ab->in_pat); free(ab->out_pat); free(ab->reward);
     free(ab->maps); free(ab->init_maps); free(ab->t);
+    free(ab->limit); free(ab->inhibit);
     free(ab);
 }

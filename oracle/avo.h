@@ -51,6 +51,30 @@ int  avo_step(avo_batch *ab, const uint8_t *actions, float *rewards, uint8_t *do
  * in list order, each matching the map the previous ones left; a rule's own matches are
  * applied together). */
 int  avo_set_rule_mode(avo_batch *ab, int mode);
+/* Rule application control (paper Sec. 2.1.1: rules may be made to apply only once or a
+ * fixed number of times, in an ordered or a random order, by taking the maximum of an extra
+ * channel of index values; masks can make some rules inhibit others).  Applies to the
+ * loaded rules only (never to the four moves) and is cleared by avo_load_rules.
+ *   limit    int32 [S][R] or NULL: at most limit matches of the rule apply per step;
+ *            0 = every match applies.  Negative values are rejected.
+ *   inhibit  uint8 [S][R][R] or NULL: inhibit[s][q][r] != 0 means a match of rule r is
+ *            dropped when its patch overlaps the patch of an applied match of rule q in the
+ *            same step.  Only q < r is allowed (rule index is priority).
+ *   order    0: the kept matches are the first ones in row-major anchor order;
+ *            1: they are the ones with the largest random index value (avo_site_key).
+ *   seed     key of the random index channel.
+ * Per rule and step: match, drop inhibited matches, keep the `limit` matches with the
+ * largest keys, then pay rewards and vote with the kept ones. */
+int  avo_set_rule_control(avo_batch *ab, const int32_t *limit, const uint8_t *inhibit,
+                          int order, uint64_t seed);
+/* The index-channel value of anchor (y, x) of environment b at batch step number n (steps
+ * since avo_reset, all environments counted together): with pos = y * W + x, order 0 gives
+ * 4095 - pos; order 1 gives the high 20 bits of a Philox4x64-10 word (Salmon et al. 2011;
+ * counter (pos / 8, n, b, 0), key (seed, 0), 32-bit word pos % 8 of the output, low half of
+ * each 64-bit word first) above 4095 - pos, so that keys never tie. */
+uint32_t avo_site_key(int order, uint64_t seed, uint64_t n, int b, int pos);
+/* Philox4x64-10 block function, exported so that tests can pin it. */
+void avo_philox4x64(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4]);
 int  avo_get_maps(const avo_batch *ab, uint8_t *dst);
 /* Player-centred observation of the current maps (paper Sec. 2.2.2: a local patch of tiles
  * around the player's position; Table 1 uses windows of 5, 10, 20 and 31 cells).

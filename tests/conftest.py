@@ -19,6 +19,10 @@ def pytest_configure(config):
 @pytest.fixture(scope="session")
 def oracle_lib():
     import oracle
-    if not os.path.exists(oracle.LIB):
+    stale = (not os.path.exists(oracle.LIB) or
+             os.path.getmtime(oracle.LIB) < max(os.path.getmtime(oracle.SRC),
+                                                os.path.getmtime(os.path.join(oracle.HERE,
+                                                                              "avo.h"))))
+    if stale:
         oracle.build()
     return oracle

@@ -63,23 +63,83 @@ def force_plane(P: torch.Tensor, actions: np.ndarray) -> torch.Tensor:
     return F
 
 
-def step(maps: np.ndarray, rules, actions: np.ndarray, sequential: bool = False):
+def site_keys(order: int, seed: int, n: int, b: int, H: int, W: int) -> np.ndarray:
+    """Index channel of env b at batch step n over all H*W anchor cells, row-major.
+    Row-major order: 4095 - pos.  Random order: numpy's Philox4x64-10 generator with key
+    (seed, 0), 32-bit word pos % 8 of the block for counter (pos // 8, n, b, 0) in the high
+    20 bits (numpy advances the counter before each block, hence the counter - 1)."""
+    pos = np.arange(H * W, dtype=np.int64)
+    rank = (4095 - pos).astype(np.uint64)
+    if order == 0:
+        return rank
+    out = np.zeros(H * W, np.uint64)
+    for g in range((H * W + 7) // 8):
+        ctr = g + (n << 64) + (b << 128)
+        bg = np.random.Philox(key=seed, counter=(ctr - 1) % (1 << 256))
+        words = bg.random_raw(4)
+        for j in range(8):
+            p = 8 * g + j
+            if p < H * W:
+                u = (int(words[j // 2]) >> (32 * (j % 2))) & 0xFFFFFFFF
+                out[p] = (u & 0xFFFFF000) | int(rank[p])
+    return out
+
+
+def _overlap_hits(applied_q: torch.Tensor, nq: int, mq: int, n: int, m: int) -> torch.Tensor:
+    """applied_q [B][H][W] anchors of an inhibiting rule (n_q x m_q patches); returns
+    [B][H][W] > 0 where an n x m patch anchored there overlaps one of those patches."""
+    padded = Fn.pad(applied_q[:, None], (mq - 1, m - 1, nq - 1, n - 1))
+    ones = torch.ones((1, 1, nq + n - 1, mq + m - 1), dtype=torch.float64)
+    return Fn.conv2d(padded, ones)[:, 0]
+
+
+def step(maps: np.ndarray, rules, actions: np.ndarray, sequential: bool = False,
+         control=None, n_step: int = 0, envs=None):
     """One step with one rule list shared by all envs; no episode logic.
     maps uint8 [B][C][H][W]; rules: list of (n, m, I [C+1][n][m], O, reward).
     sequential: each rule's convolution pair is applied (and clamped) before the next rule
     is matched, instead of summing all rules' writes onto the same map.
+    control: None or (limit [R], inhibit [R][R], order, seed) for the loaded rules, with
+    n_step the batch step number and envs the env indices of the B maps (random keys).
     Returns (maps after, before any reset) uint8, rewards float64 [B]."""
     B, C, H, W = maps.shape
+    envs = np.arange(B) if envs is None else envs
     X = torch.zeros((B, C + 1, H, W), dtype=torch.float64)
     X[:, :C] = torch.from_numpy(maps.astype(np.float64))
     X[:, C] = force_plane(X[:, PLAYER], actions)
     delta = torch.zeros_like(X)
     rho = torch.zeros(B, dtype=torch.float64)
-    for n, m, I, O, rew in move_rules(C) + list(rules):
+    keys = None
+    if control is not None:
+        keys = [torch.from_numpy(site_keys(control[2], control[3], n_step, int(b), H, W)
+                                 .astype(np.float64)).reshape(H, W) for b in envs]
+    applied = []              # per loaded rule: [B][H][W] applied anchors
+    for idx, (n, m, I, O, rew) in enumerate(move_rules(C) + list(rules)):
+        r = idx - 4
         if n > H or m > W:      # no anchor where the pattern lies on the map
+            if r >= 0:
+                applied.append(torch.zeros((B, H, W), dtype=torch.float64))
             continue
         k_in, thr, k_out = kernels(I[:, :n, :m], O[:, :n, :m])
         act = torch.relu(Fn.conv2d(X, k_in) - thr + 1.0)          # [B][1][H-n+1][W-m+1]
+        if control is not None and r >= 0:
+            limit, inhibit = control[0], control[1]
+            full = torch.zeros((B, H, W), dtype=torch.float64)
+            full[:, :H - n + 1, :W - m + 1] = act[:, 0]
+            for q in range(r):
+                if inhibit[q][r]:
+                    nq, mq = rules[q][0], rules[q][1]
+                    full[_overlap_hits(applied[q], nq, mq, n, m) > 0] = 0.0
+            if limit[r] > 0:
+                for bi in range(B):
+                    idxs = torch.nonzero(full[bi].flatten()).flatten()
+                    if len(idxs) > limit[r]:
+                        kv = keys[bi].flatten()[idxs]
+                        order = torch.argsort(kv, descending=True)
+                        drop = idxs[order[limit[r]:]]
+                        full[bi].view(-1)[drop] = 0.0
+            applied.append(full)
+            act = full[:, None, :H - n + 1, :W - m + 1].contiguous()
         rho += rew * act.sum(dim=(1, 2, 3))
         delta += Fn.conv_transpose2d(act, k_out)                  # [B][C+1][H][W]
         if sequential:
@@ -98,10 +158,17 @@ def rules_from_abi(shape, in_pat, out_pat, reward, s: int = 0):
     return out
 
 
-def run(maps, rules_abi, actions, L: int = 0, per_env: bool = False, sequential: bool = False):
+def run(maps, rules_abi, actions, L: int = 0, per_env: bool = False, sequential: bool = False,
+        control=None):
     """Episode-level stepping on top of `step`: done when no player is left or the counter
     reaches L; done envs return to their initial maps.  Returns per-step maps, rewards,
-    done like oracle.run."""
+    done like oracle.run.  control: None or (limit [S][R], inhibit [S][R][R], order, seed)."""
+
+    def ctl(s):
+        if control is None:
+            return None
+        return control[0][s], control[1][s], control[2], control[3]
+
     shape, in_pat, out_pat, reward = rules_abi
     B = maps.shape[0]
     cur = maps.copy()
@@ -116,11 +183,11 @@ def run(maps, rules_abi, actions, L: int = 0, per_env: bool = False, sequential:
             rho = np.zeros(B)
             for b in range(B):
                 nb, rb = step(cur[b:b + 1], rules_from_abi(shape, in_pat, out_pat, reward, b),
-                              actions[k, b:b + 1], sequential)
+                              actions[k, b:b + 1], sequential, ctl(b), k, [b])
                 nxt[b], rho[b] = nb[0], rb[0]
         else:
             nxt, rho = step(cur, rules_from_abi(shape, in_pat, out_pat, reward), actions[k],
-                            sequential)
+                            sequential, ctl(0), k)
         t += 1
         done = (nxt[:, PLAYER].reshape(B, -1).sum(1) == 0) | ((L > 0) & (t == L))
         nxt[done] = maps[done]

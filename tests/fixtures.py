@@ -5,9 +5,13 @@ Format (line based, '#' starts a comment):
     mode sequential              optional: rules applied one after another (default parallel)
     channels <C>                 stored channels; tiles E W P G a b c ... (0, 1, 2, 3, 4 ...)
     episode <L>                  optional episode length (default 0 = none)
+    order rowmajor|random        optional rule application control (site order, default
+    seed <s>                     row-major) and the key of the random index channel
     rule <n>x<m> reward <r>      one block per loaded rule, in index order
     in  <i>,<j> <T>=<v> ... | <i>,<j> <T>=<v> ...     specified input entries
     out <i>,<j> <T>=<v> ... | ...                     specified output entries
+    limit <K>                    optional: at most K matches of this rule apply per step
+    inhibits <q>                 optional: this rule is inhibited by earlier rule q
     map                          the initial map follows, one line per row
     step <action>                one block per step: the map after the step follows,
     reward <r>                   then the step's reward
@@ -51,6 +55,10 @@ class Fixture:
     C: int
     L: int
     mode: int = 0                                # 0 parallel, 1 sequential
+    order: int = 0                               # 0 row-major, 1 random index channel
+    seed: int = 0
+    limits: dict = field(default_factory=dict)   # rule -> K
+    inhibits: list = field(default_factory=list)  # (q, r): q inhibits r
     rules: list = field(default_factory=list)   # (n, m, in [C+1][n][m], out, reward)
     init: np.ndarray = None                      # [C][H][W]
     steps: List[Step] = field(default_factory=list)
@@ -78,6 +86,22 @@ class Fixture:
             op[0, k, :, :n, :m] = o_
             rw[0, k] = r_
         return shape, ip, op, rw, mh, mw
+
+
+    @property
+    def has_control(self):
+        return bool(self.limits or self.inhibits or self.order)
+
+    def abi_control(self):
+        """(limit [1][R], inhibit [1][R][R], order, seed) for one shared set."""
+        R = len(self.rules)
+        limit = np.zeros((1, R), np.int32)
+        inhibit = np.zeros((1, R, R), np.uint8)
+        for r, k in self.limits.items():
+            limit[0, r] = k
+        for q, r in self.inhibits:
+            inhibit[0, q, r] = 1
+        return limit, inhibit, self.order, self.seed
 
 
 def _parse_cells(line: str, C: int, W: int = None) -> np.ndarray:
@@ -116,7 +140,7 @@ def parse(path: str) -> Fixture:
     fx = Fixture(name=name, C=0, L=0)
     k = 0
     keywords = ("mode", "channels", "episode", "rule", "in", "out", "map", "step", "reward",
-                "done")
+                "done", "limit", "inhibits", "order", "seed")
 
     def grab_rows(k):
         rows = []
@@ -131,6 +155,14 @@ def parse(path: str) -> Fixture:
         k += 1
         if head == "mode":
             fx.mode = {"parallel": 0, "sequential": 1}[rest.strip()]
+        elif head == "order":
+            fx.order = {"rowmajor": 0, "random": 1}[rest.strip()]
+        elif head == "seed":
+            fx.seed = int(rest)
+        elif head == "limit":
+            fx.limits[len(fx.rules) - 1] = int(rest)
+        elif head == "inhibits":
+            fx.inhibits.append((int(rest), len(fx.rules) - 1))
         elif head == "channels":
             fx.C = int(rest)
         elif head == "episode":

@@ -20,6 +20,8 @@ def run_oracle(fx):
     o = oracle.Oracle(1, fx.H, fx.W, fx.C, max(len(fx.rules), 1), mh, mw, False, fx.L,
                       rule_mode=fx.mode)
     o.load_rules(shape, ip, op, rw)
+    if fx.has_control:
+        o.set_rule_control(*fx.abi_control())
     o.reset(fx.init[None])
     got = []
     for st in fx.steps:
@@ -45,7 +47,8 @@ def test_conv_form_matches_worked_case(path):
     shape, ip, op, rw, _, _ = fx.abi_rules()
     acts = np.array([[st.action] for st in fx.steps], np.uint8)
     maps, rewards, done = e3_conv.run(fx.init[None], (shape, ip, op, rw), acts, L=fx.L,
-                                      sequential=bool(fx.mode))
+                                      sequential=bool(fx.mode),
+                                      control=fx.abi_control() if fx.has_control else None)
     for k, st in enumerate(fx.steps):
         np.testing.assert_array_equal(maps[k, 0], st.after, err_msg=f"{fx.name} step {k}")
         assert rewards[k, 0] == st.reward
@@ -57,5 +60,6 @@ def test_fixture_set_is_complete():
     # a single rule firing, a don't-care cell, overlapping matches, a move into a wall
     for need in ("w01_single_rule", "w02_dont_care", "w03_overlap", "w04_move_into_wall",
                  "w06_food", "w07_kill", "w08_edge", "w10_vote_count", "ws01_food_sequential",
-                 "ws02_chain_sequential"):
+                 "ws02_chain_sequential", "wc01_once_rowmajor", "wc03_inhibit_overlap",
+                 "wc04_inhibit_2d"):
         assert need in names

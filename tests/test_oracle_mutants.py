@@ -65,6 +65,8 @@ def pin_worked_cases(lib):
         o = oracle.Oracle(1, fx.H, fx.W, fx.C, max(len(fx.rules), 1), mh, mw, False, fx.L,
                           lib_path=lib, rule_mode=fx.mode)
         o.load_rules(shape, ip, op, rw)
+        if fx.has_control:
+            o.set_rule_control(*fx.abi_control())
         o.reset(fx.init[None])
         for st in fx.steps:
             r, d = o.step(np.array([st.action], np.uint8))
