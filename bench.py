@@ -65,7 +65,7 @@ def measured_traffic(workload: str, engine: int, engine_name: str):
 
 
 def cpu_baseline(wl, maps, rules, actions, budget_s: float, threads: int,
-                 rule_mode: str = "parallel"):
+                 rule_mode: str = "parallel", control=None):
     import oracle
     from paper_2407_04221_amd import inputs
     nb = min(wl.B, 4096)
@@ -73,6 +73,10 @@ def cpu_baseline(wl, maps, rules, actions, budget_s: float, threads: int,
     m, r, a = inputs.subset_envs(wl, maps, rules, actions, envs)
     o = oracle.Oracle.for_workload(wl, B=nb, rule_mode=int(rule_mode == "sequential"))
     o.load_rules(*r)
+    if control is not None:
+        limit, inhibit, order, seed = control
+        S = nb if wl.per_env else 1
+        o.set_rule_control(limit[:S], inhibit[:S], order, seed)
     o.reset(m)
     steps = 0
     t0 = time.perf_counter()
@@ -96,6 +100,11 @@ def main():
     ap.add_argument("--variant", default="literal", choices=["literal", "planted", "dense"])
     ap.add_argument("--engine", default="auto", choices=["auto", "generic", "lane16", "wave"])
     ap.add_argument("--rule-mode", default="parallel", choices=["parallel", "sequential"])
+    ap.add_argument("--limit", type=int, default=0,
+                    help="rule application control: cap every loaded rule at K matches per step")
+    ap.add_argument("--inhibit-chain", action="store_true",
+                    help="rule application control: loaded rule r is inhibited by rule r - 1")
+    ap.add_argument("--site-order", default="rowmajor", choices=["rowmajor", "random"])
     ap.add_argument("--chunk", type=int, default=1000, help="steps per av_step_n launch")
     ap.add_argument("--launch-steps", type=int, default=0,
                     help="also time this many steps with one launch per step (av_step)")
@@ -135,6 +144,16 @@ def main():
     acts = torch.from_numpy(actions).cuda()
     b = av.Batch.for_workload(wl, engine=args.engine, rule_mode=args.rule_mode)
     b.load_rules(*rules)
+    control = None
+    if args.limit or args.inhibit_chain:
+        S = wl.B if wl.per_env else 1
+        limit = np.full((S, wl.R), args.limit, np.int32)
+        inhibit = np.zeros((S, wl.R, wl.R), np.uint8)
+        if args.inhibit_chain:
+            for r in range(1, wl.R):
+                inhibit[:, r - 1, r] = 1
+        control = (limit, inhibit, av.SITE_ORDERS[args.site_order], args.seed)
+        b.set_rule_control(*control)
     b.reset(maps)
     engine = b.info["engine"]
     engine_name = av.ENGINE_NAMES[engine]
@@ -214,7 +233,8 @@ def main():
     cpu = None
     if not args.no_cpu:
         cpu = cpu_baseline(wl, maps, rules, actions, args.cpu_seconds,
-                           threads=min(16, os.cpu_count() or 1), rule_mode=args.rule_mode)
+                           threads=min(16, os.cpu_count() or 1), rule_mode=args.rule_mode,
+                           control=control)
 
     traffic = measured_traffic(args.workload, engine, engine_name)
     out = {
@@ -238,6 +258,9 @@ def main():
             "B": wl.B, "H": wl.H, "W": wl.W, "C": wl.C, "R": wl.R, "variant": args.variant,
             "engine": engine_name, "api": "av_step_n", "steps_per_launch": chunk,
             "rule_mode": args.rule_mode,
+            "control": None if control is None else {
+                "limit": args.limit, "inhibit_chain": args.inhibit_chain,
+                "site_order": args.site_order},
         },
         "cell_rule_updates_per_sec": value * wl.H * wl.W * wl.R,
         "pct_hbm_roofline": 100.0 * value / roof_env_steps,

@@ -123,9 +123,38 @@ av_status av_create_batch(const av_config *cfg, av_batch_t *out);
 av_status av_load_rules(av_batch_t b, int32_t num_rules, const int32_t *shape,
                         const int8_t *in_pat, const int8_t *out_pat, const int32_t *reward);
 
+/* Site order of rule application control (av_set_rule_control). */
+typedef enum {
+    AV_SITES_ROW_MAJOR = 0,   /* a capped rule keeps its first matches in row-major order */
+    AV_SITES_RANDOM = 1       /* ... the matches with the largest random index value */
+} av_site_order;
+
+/* Rule application control (paper Sec. 2.1.1: a rule can be made to apply only once or a
+ * fixed number of times, in an ordered or a random order, by taking the maximum over an
+ * extra channel of index values; masks let some rules inhibit others).  Applies to the
+ * loaded rules only (the four moves are never capped or inhibited).  Per loaded rule, in
+ * index order, every step: its matches whose n x m patch overlaps the patch of an applied
+ * match of an inhibiting earlier rule are dropped; of the rest at most limit are kept,
+ * those with the largest index value; rewards and votes use the kept matches.
+ *   limit    host int32 [S][R] or NULL (all 0): 0 = every match applies, K > 0 = at most K
+ *   inhibit  host uint8 [S][R][R] or NULL (none): inhibit[s][q][r] != 0 means rule q
+ *            inhibits rule r; only q < r is allowed (rule index is priority)
+ *   order    av_site_order.  Index value of anchor pos = y * W + x: row-major rank
+ *            4095 - pos; random: the high 20 bits of 32-bit word pos % 8 (low half of each
+ *            64-bit word first) of Philox4x64-10 (Salmon et al., SC 2011) with counter
+ *            (pos / 8, n, env, 0) and key (seed, 0), above that rank, where n is the batch
+ *            step number (steps since av_reset, all environments counted together)
+ *   seed     key of the random index channel
+ * AV_ESTATE before av_load_rules (which clears the control); AV_EINVAL for a negative
+ * limit, an inhibition with q >= r, an unknown order, or an explicit lane16 or wave engine
+ * (the control runs on the generic engine: a batch created with AV_ENGINE_AUTO switches to
+ * it while some limit or inhibition is set).  Synchronises the stream. */
+av_status av_set_rule_control(av_batch_t b, const int32_t *limit, const uint8_t *inhibit,
+                              int32_t order, uint64_t seed);
+
 /* Set every environment's initial map and current map to init_maps (device, uint8
- * [B][C][H][W], nonzero = tile present) and its step counter to 0.  Environments that end
- * an episode return to these maps.  May synchronise. */
+ * [B][C][H][W], nonzero = tile present), its step counter and the batch step number to 0.
+ * Environments that end an episode return to these maps.  May synchronise. */
 av_status av_reset(av_batch_t b, const uint8_t *init_maps);
 
 /* One step of all B environments.  actions: device uint8 [B]; rewards: device float
@@ -164,8 +193,8 @@ const void *av_state_ptr(av_batch_t b);
 
 av_status av_get_info(av_batch_t b, av_info *info);
 
-/* Checkpoint and resume.  av_get_state copies the packed current maps, initial maps and
- * step counters into host_blob; *bytes holds its capacity on entry and the size written
+/* Checkpoint and resume.  av_get_state copies the packed current maps, initial maps, step
+ * counters and the batch step number into host_blob; *bytes holds its capacity on entry and the size written
  * on return (call with host_blob = NULL to query).  av_set_state restores them; stepping
  * on from a restored blob is bit-identical to stepping on from where it was taken.  The
  * blob records B, H, W, C and is refused (AV_EINVAL) by a batch of another shape.

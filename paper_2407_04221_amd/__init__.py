@@ -24,9 +24,12 @@ ENGINES = {"auto": AV_ENGINE_AUTO, "generic": AV_ENGINE_GENERIC, "lane16": AV_EN
 ENGINE_NAMES = {v: k for k, v in ENGINES.items()}
 AV_RULES_PARALLEL, AV_RULES_SEQUENTIAL = 0, 1
 RULE_MODES = {"parallel": AV_RULES_PARALLEL, "sequential": AV_RULES_SEQUENTIAL}
+AV_SITES_ROW_MAJOR, AV_SITES_RANDOM = 0, 1
+SITE_ORDERS = {"rowmajor": AV_SITES_ROW_MAJOR, "random": AV_SITES_RANDOM}
 
 # Every symbol include/autoverse.h declares.
-ABI_SYMBOLS = ("av_create_batch", "av_load_rules", "av_reset", "av_step", "av_step_n",
+ABI_SYMBOLS = ("av_create_batch", "av_load_rules", "av_set_rule_control", "av_reset",
+               "av_step", "av_step_n",
                "av_get_maps", "av_observe", "av_rule_features", "av_state_ptr", "av_get_info",
                "av_get_state", "av_set_state", "av_set_stream", "av_destroy_batch",
                "av_last_error")
@@ -72,6 +75,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     sig = {
         "av_create_batch": ([ctypes.POINTER(av_config), ctypes.POINTER(P)], ctypes.c_int),
         "av_load_rules": ([P, I32, P, P, P, P], ctypes.c_int),
+        "av_set_rule_control": ([P, P, P, I32, ctypes.c_uint64], ctypes.c_int),
         "av_reset": ([P, P], ctypes.c_int),
         "av_step": ([P, P, P, P], ctypes.c_int),
         "av_step_n": ([P, I32, P, P, P], ctypes.c_int),
@@ -160,6 +164,19 @@ def av_load_rules(batch, shape, in_pat, out_pat, reward):
     reward, pr = _host(reward, np.int32, "reward")
     R = shape.shape[1] if shape.ndim == 3 else 0
     _check("av_load_rules", load_library().av_load_rules(batch, R, ps, pi, po, pr))
+
+
+def av_set_rule_control(batch, limit=None, inhibit=None, order=AV_SITES_ROW_MAJOR, seed=0):
+    """Host arrays or None: limit int32 [S][R] (0 = every match), inhibit uint8 [S][R][R]
+    ([q][r]: q inhibits r, q < r); order AV_SITES_ROW_MAJOR / AV_SITES_RANDOM or its name."""
+    pl = pi = None
+    if limit is not None:
+        limit, pl = _host(limit, np.int32, "limit")
+    if inhibit is not None:
+        inhibit, pi = _host(inhibit, np.uint8, "inhibit")
+    order = SITE_ORDERS.get(order, order) if isinstance(order, str) else order
+    _check("av_set_rule_control",
+           load_library().av_set_rule_control(batch, pl, pi, int(order), int(seed)))
 
 
 def av_reset(batch, init_maps):
@@ -278,6 +295,16 @@ class Batch:
 
     def load_rules(self, shape, in_pat, out_pat, reward):
         av_load_rules(self.h, shape, in_pat, out_pat, reward)
+        self.S, self.R = (np.shape(shape)[0], np.shape(shape)[1]) if np.ndim(shape) == 3 \
+            else (1, 0)
+
+    def set_rule_control(self, limit=None, inhibit=None, order="rowmajor", seed=0):
+        S, R = getattr(self, "S", 1), getattr(self, "R", 0)
+        if limit is not None and np.shape(limit) != (S, R):
+            raise ValueError(f"limit must have shape {(S, R)}, got {np.shape(limit)}")
+        if inhibit is not None and np.shape(inhibit) != (S, R, R):
+            raise ValueError(f"inhibit must have shape {(S, R, R)}, got {np.shape(inhibit)}")
+        av_set_rule_control(self.h, limit, inhibit, order, seed)
 
     def reset(self, init_maps):
         torch = _torch()

@@ -40,12 +40,13 @@ av_status fail(av_status st, const char *fmt, ...) {
             return fail(AV_EDEVICE, "%s failed: %s", #call, hipGetErrorString(e_));  \
     } while (0)
 
-constexpr char kBlobMagic[8] = {'A', 'V', 'S', 'T', 'A', 'T', 'E', '1'};
+constexpr char kBlobMagic[8] = {'A', 'V', 'S', 'T', 'A', 'T', 'E', '2'};
 
 struct BlobHeader {
     char magic[8];
     int32_t B, H, W, C, row_bytes, reserved;
     uint64_t state_bytes;
+    uint64_t step_no;
 };
 
 }  // namespace
@@ -59,8 +60,11 @@ struct av_batch_s {
     void *d_init = nullptr;
     int32_t *d_t = nullptr;
     int envs_per_block = 1;
-    int engine = AV_ENGINE_GENERIC;
+    int engine = AV_ENGINE_GENERIC;   // engine used by the next step
+    int plain_engine = AV_ENGINE_GENERIC;   // engine without rule application control
     bool have_rules = false, have_maps = false;
+    uint64_t step_no = 0;            // batch steps since av_reset
+    CtlArgs ctl;                     // rule application control (device arrays owned)
     int32_t R = 0;
     std::vector<uint8_t> features;   // binary rule features, [S][R][2][2][C+1][mh][mw]
     GenericProgram prog;
@@ -83,6 +87,13 @@ void free_device_program(av_batch_t b) {
     dev_free(b->dprog.rvote);
     b->dprog = DeviceProgram{};
     lane16_free(b->dlprog);
+}
+
+void free_control(av_batch_t b) {
+    dev_free(const_cast<int32_t *>(b->ctl.limit));
+    dev_free(const_cast<uint32_t *>(b->ctl.inhibit));
+    b->ctl = CtlArgs{};
+    b->engine = b->plain_engine;
 }
 
 // Output-kernel entry K_O = O - I; unspecified output: no vote; unspecified input: the
@@ -280,6 +291,7 @@ av_status av_create_batch(const av_config *cfg, av_batch_t *out) {
     b->envs_per_block = std::max(1, std::min(256 / c.height, int(kLdsBudget / env_lds)));
     if (c.engine != AV_ENGINE_AUTO) b->engine = c.engine;
     else b->engine = lane16_ok ? AV_ENGINE_LANE16 : (wave_ok ? AV_ENGINE_WAVE : AV_ENGINE_GENERIC);
+    b->plain_engine = b->engine;
     hipError_t e = hipMalloc(&b->d_state, b->state_bytes);
     if (e == hipSuccess) e = hipMalloc(&b->d_init, b->state_bytes);
     if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&b->d_t), sizeof(int32_t) * c.num_envs);
@@ -358,6 +370,7 @@ av_status av_load_rules(av_batch_t b, int32_t R, const int32_t *shape, const int
     if (av_status st = set_device(b)) return st;
     AV_HIP(hipStreamSynchronize(b->stream));   // no step may still read the old program
     free_device_program(b);
+    free_control(b);
     b->have_rules = false;
     compile_generic(sets, c.channels, c.rule_mode == AV_RULES_SEQUENTIAL, b->prog);
     if (av_status st = upload(&b->dprog.hdr, b->prog.hdr)) return st;
@@ -402,6 +415,72 @@ av_status av_reset(av_batch_t b, const uint8_t *init_maps) {
                        b->row_bytes, b->stream));
     AV_HIP(hipMemsetAsync(b->d_t, 0, sizeof(int32_t) * c.num_envs, b->stream));
     b->have_maps = true;
+    b->step_no = 0;
+    return AV_OK;
+}
+
+av_status av_set_rule_control(av_batch_t b, const int32_t *limit, const uint8_t *inhibit,
+                              int32_t order, uint64_t seed) {
+    g_last_error.clear();
+    if (av_status st = check_batch(b)) return st;
+    if (!b->have_rules) return fail(AV_ESTATE, "call av_load_rules first");
+    if (order != AV_SITES_ROW_MAJOR && order != AV_SITES_RANDOM)
+        return fail(AV_EINVAL, "unknown site order %d", order);
+    const av_config &c = b->cfg;
+    const int S = c.per_env_rules ? c.num_envs : 1, R = b->R, Rt = R + kMoveRules;
+    bool active = false;
+    if (limit)
+        for (size_t k = 0; k < size_t(S) * R; ++k) {
+            if (limit[k] < 0)
+                return fail(AV_EINVAL, "set %zu rule %zu: negative limit %d", k / R, k % R, limit[k]);
+            active |= limit[k] > 0;
+        }
+    if (inhibit)
+        for (size_t s = 0; s < size_t(S); ++s)
+            for (int q = 0; q < R; ++q)
+                for (int r = 0; r < R; ++r)
+                    if (inhibit[(s * R + q) * R + r]) {
+                        if (q >= r)
+                            return fail(AV_EINVAL, "set %zu: rule %d may not inhibit rule %d "
+                                        "(only earlier rules inhibit later ones)", s, q, r);
+                        active = true;
+                    }
+    if (active && c.engine != AV_ENGINE_AUTO && c.engine != AV_ENGINE_GENERIC)
+        return fail(AV_EINVAL, "rule application control runs on the generic engine; create "
+                    "the batch with AV_ENGINE_AUTO or AV_ENGINE_GENERIC");
+    const bool random = order == AV_SITES_RANDOM;
+    const size_t env_lds = generic_env_lds_bytes(c.height, c.width, c.channels, Rt, true, random);
+    if (active && env_lds > size_t(kLdsBudget))
+        return fail(AV_EINVAL, "rule application control needs %zu bytes of LDS per environment "
+                    "(limit %d)", env_lds, kLdsBudget);
+    if (av_status st = set_device(b)) return st;
+    AV_HIP(hipStreamSynchronize(b->stream));   // no step may still read the old arrays
+    free_control(b);
+    if (!active) return AV_OK;
+    const int words = (Rt + 31) / 32;
+    std::vector<int32_t> lim(size_t(S) * Rt, 0);
+    std::vector<uint32_t> inh(size_t(S) * Rt * words, 0);
+    for (size_t s = 0; s < size_t(S); ++s)
+        for (int r = 0; r < R; ++r) {
+            if (limit) lim[s * Rt + kMoveRules + r] = limit[s * R + r];
+            if (inhibit)
+                for (int q = 0; q < r; ++q)
+                    if (inhibit[(s * R + q) * R + r]) {
+                        const int qi = kMoveRules + q;
+                        inh[(s * Rt + kMoveRules + r) * words + qi / 32] |= 1u << (qi % 32);
+                    }
+        }
+    int32_t *d_lim = nullptr;
+    uint32_t *d_inh = nullptr;
+    if (av_status st = upload(&d_lim, lim)) return st;
+    b->ctl.limit = d_lim;
+    if (av_status st = upload(&d_inh, inh)) { free_control(b); return st; }
+    b->ctl.inhibit = d_inh;
+    b->ctl.words = words;
+    b->ctl.active = 1;
+    b->ctl.random = random;
+    b->ctl.seed = seed;
+    b->engine = AV_ENGINE_GENERIC;
     return AV_OK;
 }
 
@@ -422,12 +501,23 @@ static av_status step_k(av_batch_t b, int32_t k, const uint8_t *actions, float *
     a.state = b->d_state; a.init = b->d_init; a.t = b->d_t;
     a.actions = actions; a.rewards = rewards; a.done = done;
     a.prog = b->dprog;
-    if (b->engine == AV_ENGINE_LANE16)
+    a.ctl = b->ctl;
+    a.ctl.step_base = b->step_no;
+    if (b->engine == AV_ENGINE_LANE16) {
         AV_HIP(launch_lane16_step(a, b->dlprog, b->stream));
-    else if (b->engine == AV_ENGINE_WAVE)
+    } else if (b->engine == AV_ENGINE_WAVE) {
         AV_HIP(launch_wave_step(a, b->stream));
-    else
-        AV_HIP(launch_generic_step(a, b->envs_per_block, b->stream));
+    } else {
+        int G = b->envs_per_block;
+        if (a.ctl.active) {
+            const size_t env_lds = generic_env_lds_bytes(c.height, c.width, c.channels,
+                                                         b->dprog.rules_per_set, true,
+                                                         a.ctl.random);
+            G = std::max(1, std::min(256 / c.height, int(kLdsBudget / env_lds)));
+        }
+        AV_HIP(launch_generic_step(a, G, b->stream));
+    }
+    b->step_no += uint64_t(k);
     return AV_OK;
 }
 
@@ -512,6 +602,7 @@ av_status av_get_state(av_batch_t b, void *host_blob, size_t *bytes) {
     std::memcpy(h.magic, kBlobMagic, 8);
     h.B = b->cfg.num_envs; h.H = b->cfg.height; h.W = b->cfg.width; h.C = b->cfg.channels;
     h.row_bytes = b->row_bytes; h.state_bytes = b->state_bytes;
+    h.step_no = b->step_no;
     char *p = static_cast<char *>(host_blob);
     std::memcpy(p, &h, sizeof h);
     AV_HIP(hipStreamSynchronize(b->stream));
@@ -542,6 +633,7 @@ av_status av_set_state(av_batch_t b, const void *host_blob, size_t bytes) {
     AV_HIP(hipMemcpy(b->d_init, p + sizeof h + b->state_bytes, b->state_bytes, hipMemcpyHostToDevice));
     AV_HIP(hipMemcpy(b->d_t, p + sizeof h + 2 * b->state_bytes, sizeof(int32_t) * b->cfg.num_envs,
                      hipMemcpyHostToDevice));
+    b->step_no = h.step_no;
     b->have_maps = true;
     return AV_OK;
 }
@@ -562,6 +654,7 @@ av_status av_destroy_batch(av_batch_t b) {
         hipError_t e = hipStreamSynchronize(b->stream);
         if (e != hipSuccess) st = fail(AV_EDEVICE, "hipStreamSynchronize: %s", hipGetErrorString(e));
         free_device_program(b);
+        free_control(b);
         dev_free(b->d_state);
         dev_free(b->d_init);
         dev_free(b->d_t);

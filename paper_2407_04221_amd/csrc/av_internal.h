@@ -78,6 +78,19 @@ struct DeviceProgram {
     int32_t any_reward = 0;           // some rule of some set pays a nonzero reward
 };
 
+// Rule application control (paper Sec. 2.1.1): per loaded rule a cap on the matches applied
+// per step, chosen by the largest index-channel value, and rules that inhibit later ones.
+// Arrays are indexed by the set's internal rule index (moves 0..3 carry no control).
+struct CtlArgs {
+    const int32_t *limit = nullptr;     // [S][R+4]; 0 = every match applies
+    const uint32_t *inhibit = nullptr;  // [S][R+4][words]; bit q of rule r: q inhibits r
+    int32_t words = 0;                  // inhibitor mask words per rule
+    int32_t active = 0;                 // some limit or inhibition is set
+    int32_t random = 0;                 // index channel: 0 row-major rank, 1 random
+    uint64_t seed = 0;                  // key of the random index channel
+    uint64_t step_base = 0;             // batch step number of the launch's first step
+};
+
 // Everything a step kernel needs, passed by value.
 struct StepArgs {
     int32_t B, H, W, C, L;
@@ -92,6 +105,7 @@ struct StepArgs {
     float *rewards;                  // [k][B]
     uint8_t *done;                   // [k][B]
     DeviceProgram prog;
+    CtlArgs ctl;
 };
 
 // Launchers (k_generic.hip).  All return hipSuccess or the launch error.
@@ -100,7 +114,8 @@ hipError_t launch_pack(const uint8_t *src, void *dst, void *dst2, int B, int C, 
 hipError_t launch_unpack(const void *src, uint8_t *dst, int B, int C, int H, int W,
                          int row_bytes, hipStream_t s);
 hipError_t launch_generic_step(const StepArgs &a, int envs_per_block, hipStream_t s);
-size_t generic_env_lds_bytes(int H, int W, int C, int rules_per_set);
+size_t generic_env_lds_bytes(int H, int W, int C, int rules_per_set, bool control = false,
+                             bool random = false);
 
 // Player-centred observation window (k_observe.hip).
 hipError_t launch_observe(const void *state, int B, int C, int H, int W, int row_bytes, int w,

@@ -10,6 +10,10 @@
 //   match     M_r[y] = AND over the rule's specified input entries of the plane row
 //             y + i shifted right by j (bit x then holds cell x + j), complemented for
 //             must-be-0 entries, masked to anchors where the pattern lies on the map;
+//   control   (optional, Sec. 2.1.1) per loaded rule in index order: drop matches whose
+//             patch overlaps an applied match of an inhibiting earlier rule, then keep the
+//             `limit` matches with the largest index-channel value (radix select over the
+//             32-bit keys, 8 bits per pass, through an LDS histogram per environment);
 //   reward    sum over rules of reward_r * popcount(M_r), reduced per environment;
 //   (order)   all rules match the same map (parallel mode), or in sequential mode each rule
 //             is matched, and its votes applied, before the next one;
@@ -47,6 +51,23 @@ __device__ inline RowT low_mask(int bits) {
     return bits >= int(8 * sizeof(RowT)) ? ~RowT(0) : ((RowT(1) << bits) - 1);
 }
 
+// Philox4x64-10 block function (Salmon, Moraes, Dror, Shaw, SC 2011).
+__device__ inline void philox4x64_10(uint64_t x[4], uint64_t k0, uint64_t k1) {
+    for (int round = 0; round < 10; ++round) {
+        const uint64_t m0 = 0xD2E7470EE14C6C93ull, m1 = 0xCA5A826395121157ull;
+        const uint64_t lo0 = m0 * x[0], hi0 = __umul64hi(m0, x[0]);
+        const uint64_t lo1 = m1 * x[2], hi1 = __umul64hi(m1, x[2]);
+        const uint64_t y0 = hi1 ^ x[1] ^ k0, y2 = hi0 ^ x[3] ^ k1;
+        x[0] = y0; x[1] = lo1; x[2] = y2; x[3] = lo0;
+        k0 += 0x9E3779B97F4A7C15ull;
+        k1 += 0xBB67AE8584CAA73Bull;
+    }
+}
+
+// Index-channel value of cell pos: row-major rank 4095 - pos, or, for the random channel,
+// the high 20 bits of the cell's Philox word above that rank (keys never tie).
+__device__ inline uint32_t rank_key(int pos) { return uint32_t(4095 - pos); }
+
 template <typename RowT>
 __global__ void __launch_bounds__(256) generic_step(StepArgs a, int G) {
     extern __shared__ __align__(16) unsigned char lds[];
@@ -63,6 +84,10 @@ __global__ void __launch_bounds__(256) generic_step(StepArgs a, int G) {
     int *red = reinterpret_cast<int *>(M + size_t(G) * Rt * H);  // [G] reward sums
     int *anyp = red + G;                                  // [G] player bits left
     int *dflag = anyp + G;                                // [G] done this step
+    int *cnt = dflag + G;                                 // [G] matches of one rule
+    int *hist = cnt + G;                                  // [G][256] radix histogram
+    uint32_t *keys = reinterpret_cast<uint32_t *>(hist + (a.ctl.active ? G * 256 : 0));
+    const int HW = H * W;                                 // keys: [G][H*W] random channel
 
     const RowT rowmask = low_mask<RowT>(W);
     RowT *my = planes + size_t(g) * C1 * H;               // this env's planes
@@ -93,6 +118,19 @@ __global__ void __launch_bounds__(256) generic_step(StepArgs a, int G) {
             else if (act == 4) f = P[y] >> 1;
             my[C * H + y] = f;
         }
+        if (a.ctl.active && a.ctl.random && live) {
+            // this step's random index channel, eight cells per Philox block
+            const uint64_t n = a.ctl.step_base + uint64_t(k);
+            for (int gi = y; gi * 8 < HW; gi += H) {
+                uint64_t x[4] = {uint64_t(gi), n, uint64_t(b), 0};
+                philox4x64_10(x, a.ctl.seed, 0);
+                for (int j = 0; j < 8 && gi * 8 + j < HW; ++j) {
+                    const int pos = gi * 8 + j;
+                    const uint32_t u = uint32_t(x[j >> 1] >> (32 * (j & 1)));
+                    keys[size_t(g) * HW + pos] = (u & 0xFFFFF000u) | rank_key(pos);
+                }
+            }
+        }
         __syncthreads();
 
         // Rules in batches: all of them at once (parallel mode) or one at a time
@@ -112,10 +150,98 @@ __global__ void __launch_bounds__(256) generic_step(StepArgs a, int G) {
                         acc &= ((en >> 24) & 1) ? v : RowT(~v);
                     }
                     myM[r * H + y] = acc;
-                    rsum += h.reward * popc(acc);
+                    if (!a.ctl.active) rsum += h.reward * popc(acc);
                 }
             }
             __syncthreads();
+
+            if (a.ctl.active) {
+                // loaded rules of the batch in index order: inhibition, then the limit
+                for (int r = r0 < kMoveRules ? kMoveRules : r0; r < r1; ++r) {
+                    if (tid < G) cnt[tid] = 0;
+                    const size_t cr = size_t(s) * Rt + r;
+                    RowT acc = live ? myM[r * H + y] : RowT(0);
+                    if (live && acc) {
+                        const RuleHdr h = hdr[r];
+                        const uint32_t *inh = a.ctl.inhibit + cr * a.ctl.words;
+                        for (int w = 0; w < a.ctl.words; ++w) {
+                            uint32_t bits = inh[w];
+                            while (bits) {
+                                const int q = w * 32 + __ffs(bits) - 1;
+                                bits &= bits - 1;
+                                const int nq = hdr[q].n, mq = hdr[q].m;
+                                // anchors of q whose patch overlaps an n x m patch at row y:
+                                // rows y - nq + 1 .. y + n - 1, columns x - mq + 1 .. x + m - 1
+                                RowT o = 0;
+                                const int ylo = y - nq + 1 < 0 ? 0 : y - nq + 1;
+                                const int yhi = y + h.n - 1 > H - 1 ? H - 1 : y + h.n - 1;
+                                for (int yy = ylo; yy <= yhi; ++yy) o |= myM[q * H + yy];
+                                RowT dil = o;
+                                for (int d = 1; d < h.m; ++d) dil |= o >> d;
+                                for (int d = 1; d < mq; ++d) dil |= o << d;
+                                acc &= ~dil;
+                            }
+                        }
+                    }
+                    __syncthreads();                 // cnt cleared; rows q < r all read
+                    if (live) {
+                        myM[r * H + y] = acc;
+                        atomicAdd(&cnt[g], popc(acc));
+                    }
+                    __syncthreads();
+                    const int lim = live ? a.ctl.limit[cr] : 0;
+                    const bool sel = live && lim > 0 && cnt[g] > lim;
+                    if (__syncthreads_or(sel)) {
+                        // radix select of the lim-th largest key among the matches
+                        uint32_t prefix = 0, pmask = 0;
+                        int need = lim;
+                        for (int shift = 24; shift >= 0; shift -= 8) {
+                            for (int i = tid; i < G * 256; i += blockDim.x) hist[i] = 0;
+                            __syncthreads();
+                            if (sel) {
+                                RowT rest = acc;
+                                while (rest) {
+                                    const int x = lowbit(rest);
+                                    rest &= rest - 1;
+                                    const int pos = y * W + x;
+                                    const uint32_t key = a.ctl.random ? keys[size_t(g) * HW + pos]
+                                                                      : rank_key(pos);
+                                    if ((key & pmask) == prefix)
+                                        atomicAdd(&hist[g * 256 + ((key >> shift) & 255)], 1);
+                                }
+                            }
+                            __syncthreads();
+                            if (sel) {
+                                int above = 0, d = 255;
+                                for (; d > 0; --d) {
+                                    const int c = hist[g * 256 + d];
+                                    if (above + c >= need) break;
+                                    above += c;
+                                }
+                                prefix |= uint32_t(d) << shift;
+                                pmask |= 255u << shift;
+                                need -= above;
+                            }
+                            __syncthreads();         // before the next pass clears hist
+                        }
+                        if (sel) {
+                            RowT rest = acc, keep = 0;
+                            while (rest) {
+                                const int x = lowbit(rest);
+                                rest &= rest - 1;
+                                const int pos = y * W + x;
+                                const uint32_t key = a.ctl.random ? keys[size_t(g) * HW + pos]
+                                                                  : rank_key(pos);
+                                if (key >= prefix) keep |= RowT(1) << x;
+                            }
+                            myM[r * H + y] = keep;
+                        }
+                    }
+                }
+                if (live)
+                    for (int r = r0; r < r1; ++r) rsum += hdr[r].reward * popc(myM[r * H + y]);
+                __syncthreads();
+            }
 
             // votes of this batch and clamp, one channel at a time; each thread rewrites
             // only its own row
@@ -208,15 +334,19 @@ __global__ void unpack_rows(const void *src, uint8_t *dst, int B, int C, int H, 
 
 }  // namespace
 
-size_t generic_env_lds_bytes(int H, int W, int C, int rules_per_set) {
+size_t generic_env_lds_bytes(int H, int W, int C, int rules_per_set, bool control,
+                             bool random) {
     const size_t rowb = W <= 32 ? 4 : 8;
-    return size_t(C + 1 + rules_per_set) * H * rowb + 3 * sizeof(int);
+    size_t bytes = size_t(C + 1 + rules_per_set) * H * rowb + 4 * sizeof(int);
+    if (control) bytes += 256 * sizeof(int) + (random ? size_t(H) * W * sizeof(uint32_t) : 0);
+    return bytes;
 }
 
 hipError_t launch_generic_step(const StepArgs &a, int G, hipStream_t s) {
     const int threads = G * a.H;
     const int blocks = (a.B + G - 1) / G;
-    const size_t lds = size_t(G) * generic_env_lds_bytes(a.H, a.W, a.C, a.prog.rules_per_set);
+    const size_t lds = size_t(G) * generic_env_lds_bytes(a.H, a.W, a.C, a.prog.rules_per_set,
+                                                         a.ctl.active, a.ctl.random);
     if (a.W <= 32)
         hipLaunchKernelGGL(generic_step<uint32_t>, dim3(blocks), dim3(threads), lds, s, a, G);
     else

@@ -21,14 +21,16 @@ def say(msg):
 
 
 def gpu_run(wl, maps, rules, actions, engine="auto", mode="step", chunk=7, B=None,
-            per_step_maps=True, rule_mode="parallel"):
+            per_step_maps=True, rule_mode="parallel", control=None):
     """Returns (maps per step or None, final maps, rewards [T][B], done [T][B]) as numpy,
-    and the engine the batch used."""
+    and the engine the batch used.  control: None or (limit, inhibit, order, seed)."""
     import torch
     B = maps.shape[0] if B is None else B
     b = av.Batch.for_workload(wl, B=B, engine=engine, rule_mode=rule_mode)
     try:
         b.load_rules(*rules)
+        if control is not None:
+            b.set_rule_control(*control)
         b.reset(maps)
         T = actions.shape[0]
         acts = torch.from_numpy(np.ascontiguousarray(actions)).cuda()

@@ -94,6 +94,7 @@ def test_null_arguments_are_rejected(lib):
     assert lib.av_get_maps(None, None) == av.AV_EINVAL
     assert lib.av_observe(None, 5, None) == av.AV_EINVAL
     assert lib.av_rule_features(None, None) == av.AV_EINVAL
+    assert lib.av_set_rule_control(None, None, None, 0, 0) == av.AV_EINVAL
     assert lib.av_state_ptr(None) is None
     info = av.av_info()
     assert lib.av_get_info(None, ctypes.byref(info)) == av.AV_EINVAL

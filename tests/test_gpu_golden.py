@@ -18,9 +18,12 @@ def _cases():
     for path in FIXTURES:
         fx = fixtures.parse(path)
         name = path.rsplit("/", 1)[-1][:-3]
-        engines = ["generic", "wave"]
-        if fx.H <= 16 and fx.W <= 16:
-            engines.append("lane16")
+        if fx.has_control:      # rule application control runs on the generic engine
+            engines = ["generic", "auto"]
+        else:
+            engines = ["generic", "wave"]
+            if fx.H <= 16 and fx.W <= 16:
+                engines.append("lane16")
         out += [(name, path, e) for e in engines]
     return out
 
@@ -36,7 +39,8 @@ def test_gpu_matches_worked_case(name, path, engine):
     acts = np.array([[st.action] for st in fx.steps], np.uint8)
     say(f"[golden] {name} engine={engine}")
     seq, final, r, d, _ = gpu_run(wl, fx.init[None], (shape, ip, op, rw), acts, engine=engine,
-                                  mode="step", rule_mode="sequential" if fx.mode else "parallel")
+                                  mode="step", rule_mode="sequential" if fx.mode else "parallel",
+                                  control=fx.abi_control() if fx.has_control else None)
     for k, st in enumerate(fx.steps):
         np.testing.assert_array_equal(seq[k][0], st.after, err_msg=f"{name} step {k}")
         assert r[k, 0] == st.reward, f"{name} step {k} reward"

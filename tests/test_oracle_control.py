@@ -18,6 +18,7 @@ import pytest
 
 import e3_conv
 import fixtures
+from ctl_util import random_control
 import oracle
 from paper_2407_04221_amd import inputs
 
@@ -50,13 +51,6 @@ def test_site_keys_match_numpy(oracle_lib, seed):
     # keys never tie: the low 12 bits hold 4095 - pos
     ks = e3_conv.site_keys(1, seed, 3, 1, 64, 64)
     assert len(np.unique(ks)) == 64 * 64
-
-
-def random_control(g, S, R, p_limit=0.6, p_inh=0.3, kmax=3):
-    limit = np.where(g.random((S, R)) < p_limit, g.integers(1, kmax + 1, (S, R)), 0)
-    inhibit = (g.random((S, R, R)) < p_inh).astype(np.uint8)
-    inhibit *= np.triu(np.ones((R, R), np.uint8), 1)[None]
-    return limit.astype(np.int32), inhibit
 
 
 CASES = [
