@@ -29,6 +29,16 @@ def build(out: str = LIB, src: str = SRC, extra=()) -> str:
 _libs = {}
 
 
+class Mutation(ctypes.Structure):
+    """avo_mutation: 32-bit probability thresholds (event iff word < p32), channel masks,
+    reward range, and the key / generation of the random streams."""
+    _fields_ = [("seed", ctypes.c_uint64), ("generation", ctypes.c_uint64),
+                ("map_flip_p32", ctypes.c_uint32), ("map_channels", ctypes.c_uint32),
+                ("entry_p32", ctypes.c_uint32), ("entry_channels", ctypes.c_uint32),
+                ("reward_p32", ctypes.c_uint32), ("reward_lo", ctypes.c_int32),
+                ("reward_hi", ctypes.c_int32)]
+
+
 def load(path: str = LIB) -> ctypes.CDLL:
     if path in _libs:
         return _libs[path]
@@ -48,6 +58,11 @@ def load(path: str = LIB) -> ctypes.CDLL:
     lib.avo_site_key.restype = ctypes.c_uint32
     lib.avo_philox4x64.argtypes = [P, P, P]
     lib.avo_philox4x64.restype = None
+    lib.avo_random_word.argtypes = [ctypes.c_uint64] * 5
+    lib.avo_random_word.restype = ctypes.c_uint32
+    lib.avo_mutate_maps.argtypes = [P, P, I, I, I, I, ctypes.POINTER(Mutation)]
+    lib.avo_mutate_rules.argtypes = [I, I, I, I, I, P, P, P, P, P, P, P,
+                                     ctypes.POINTER(Mutation)]
     lib.avo_observe.argtypes = [P, I, P]
     lib.avo_rule_features.argtypes = [P, P]
     lib.avo_get_maps.argtypes = [P, P]
@@ -56,7 +71,7 @@ def load(path: str = LIB) -> ctypes.CDLL:
     lib.avo_destroy.restype = None
     for f in ("avo_create", "avo_load_rules", "avo_reset", "avo_step", "avo_get_maps",
               "avo_get_counters", "avo_set_rule_mode", "avo_observe", "avo_rule_features",
-              "avo_set_rule_control"):
+              "avo_set_rule_control", "avo_mutate_maps", "avo_mutate_rules"):
         getattr(lib, f).restype = I
     _libs[path] = lib
     return lib
@@ -188,6 +203,37 @@ def philox4x64(ctr, key, lib_path: str = LIB):
     out = np.zeros(4, np.uint64)
     load(lib_path).avo_philox4x64(_ptr(c), _ptr(k), _ptr(out))
     return out
+
+
+def random_word(seed, generation, individual, stream, word, lib_path: str = LIB) -> int:
+    return int(load(lib_path).avo_random_word(seed, generation, individual, stream, word))
+
+
+def mutate_maps(maps, m: Mutation, lib_path: str = LIB):
+    """maps uint8 [n][C][H][W] -> mutated copy (0/1)."""
+    src = np.ascontiguousarray(maps, dtype=np.uint8)
+    dst = np.empty_like(src)
+    n, C, H, W = src.shape
+    rc = load(lib_path).avo_mutate_maps(_ptr(src), _ptr(dst), n, C, H, W, ctypes.byref(m))
+    if rc != AVO_OK:
+        raise OracleError("avo_mutate_maps", rc)
+    return dst
+
+
+def mutate_rules(shape, in_pat, out_pat, reward, m: Mutation, lib_path: str = LIB):
+    """Rules in the av_load_rules layout -> mutated (in_pat, out_pat, reward)."""
+    shape = np.ascontiguousarray(shape, dtype=np.int32)
+    ip = np.ascontiguousarray(in_pat, dtype=np.int8)
+    op = np.ascontiguousarray(out_pat, dtype=np.int8)
+    rw = np.ascontiguousarray(reward, dtype=np.int32)
+    S, R, C1, mh, mw = ip.shape
+    ip2, op2, rw2 = np.empty_like(ip), np.empty_like(op), np.empty_like(rw)
+    rc = load(lib_path).avo_mutate_rules(S, R, C1 - 1, mh, mw, _ptr(shape), _ptr(ip), _ptr(op),
+                                         _ptr(rw), _ptr(ip2), _ptr(op2), _ptr(rw2),
+                                         ctypes.byref(m))
+    if rc != AVO_OK:
+        raise OracleError("avo_mutate_rules", rc)
+    return ip2, op2, rw2
 
 
 def run(wl, maps, rules, actions, nthreads: int = 1, B=None, lib_path: str = LIB,

@@ -233,16 +233,23 @@ void avo_philox4x64(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4
     out[0] = x0; out[1] = x1; out[2] = x2; out[3] = x3;
 }
 
+uint32_t avo_random_word(uint64_t seed, uint64_t generation, uint64_t individual,
+                         uint64_t stream, uint64_t word)
+{
+    uint64_t ctr[4] = {word / 8, generation, individual, stream};
+    uint64_t key[2] = {seed, 0};
+    uint64_t out[4];
+    avo_philox4x64(ctr, key, out);
+    int w = (int)(word % 8);
+    return (uint32_t)(out[w / 2] >> (32 * (w % 2)));
+}
+
 uint32_t avo_site_key(int order, uint64_t seed, uint64_t n, int b, int pos)
 {
     uint32_t rank = (uint32_t)(4095 - pos);
     if (order == 0) return rank;
-    uint64_t ctr[4] = {(uint64_t)(pos / 8), n, (uint64_t)b, 0};
-    uint64_t key[2] = {seed, 0};
-    uint64_t out[4];
-    avo_philox4x64(ctr, key, out);
-    int word = pos % 8;
-    uint32_t u = (uint32_t)(out[word / 2] >> (32 * (word % 2)));
+    /* the site channel is stream 0 with the batch step number in the generation word */
+    uint32_t u = avo_random_word(seed, n, (uint64_t)b, 0, (uint64_t)pos);
     return (u & 0xFFFFF000u) | rank;
 }
 
@@ -471,6 +478,79 @@ int avo_set_rule_control(avo_batch *ab, const int32_t *limit, const uint8_t *inh
     }
     ab->site_order = order;
     ab->seed = seed;
+    return AVO_OK;
+}
+
+int avo_mutate_maps(const uint8_t *src, uint8_t *dst, int n, int C, int H, int W,
+                    const avo_mutation *m)
+{
+    if (!src || !dst || !m || n < 0 || C < 1 || H < 1 || W < 1) return AVO_EINVAL;
+    const size_t per = (size_t)C * H * W;
+    for (int k = 0; k < n; k++)
+        for (size_t e = 0; e < per; e++) {
+            int c = (int)(e / ((size_t)H * W));
+            int bit = src[(size_t)k * per + e] != 0;
+            int flip = ((m->map_channels >> c) & 1) &&
+                       avo_random_word(m->seed, m->generation, (uint64_t)k, 1, e) < m->map_flip_p32;
+            dst[(size_t)k * per + e] = (uint8_t)(bit ^ flip);
+        }
+    return AVO_OK;
+}
+
+/* The value a changed entry takes: the lower or the higher of the two others. */
+static int8_t other_value(int8_t old, int higher)
+{
+    int v = (old == -1 || old == 0) ? old : 1;
+    int lo = v == -1 ? 0 : -1;          /* the two values of {-1, 0, 1} other than v */
+    int hi = v == 1 ? 0 : 1;
+    return (int8_t)(higher ? hi : lo);
+}
+
+int avo_mutate_rules(int S, int R, int C, int mh, int mw, const int32_t *shape,
+                     const int8_t *in_src, const int8_t *out_src, const int32_t *reward_src,
+                     int8_t *in_dst, int8_t *out_dst, int32_t *reward_dst,
+                     const avo_mutation *m)
+{
+    if (!m || S < 0 || R < 0 || C < 1 || C > 31 || mh < 1 || mw < 1) return AVO_EINVAL;
+    if (m->reward_lo > m->reward_hi) return AVO_EINVAL;
+    if ((size_t)S * R > 0 && (!shape || !in_src || !out_src || !reward_src || !in_dst ||
+                              !out_dst || !reward_dst))
+        return AVO_EINVAL;
+    const int C1 = C + 1;
+    const size_t pat = (size_t)C1 * mh * mw;
+    const uint64_t span = (uint64_t)((int64_t)m->reward_hi - (int64_t)m->reward_lo + 1);
+    for (int s = 0; s < S; s++)
+        for (int r = 0; r < R; r++) {
+            const size_t k = (size_t)s * R + r;
+            const int n = shape[k * 2 + 0], mm = shape[k * 2 + 1];
+            for (int io = 0; io < 2; io++) {
+                const int8_t *src = (io ? out_src : in_src) + k * pat;
+                int8_t *dst = (io ? out_dst : in_dst) + k * pat;
+                for (int c = 0; c < C1; c++)
+                    for (int i = 0; i < mh; i++)
+                        for (int j = 0; j < mw; j++) {
+                            const size_t at = ((size_t)c * mh + i) * mw + j;
+                            const uint64_t e = ((((uint64_t)r * 2 + io) * C1 + c) * mh + i) * mw + j;
+                            int8_t v = src[at];
+                            if (i < n && j < mm && ((m->entry_channels >> c) & 1) &&
+                                avo_random_word(m->seed, m->generation, (uint64_t)s, 2, 2 * e) <
+                                    m->entry_p32) {
+                                uint32_t pick = avo_random_word(m->seed, m->generation,
+                                                                (uint64_t)s, 2, 2 * e + 1);
+                                v = other_value(v, (int)(pick & 1));
+                            }
+                            dst[at] = v;
+                        }
+            }
+            int32_t rw = reward_src[k];
+            if (avo_random_word(m->seed, m->generation, (uint64_t)s, 3, 2 * (uint64_t)r) <
+                m->reward_p32) {
+                uint32_t u = avo_random_word(m->seed, m->generation, (uint64_t)s, 3,
+                                             2 * (uint64_t)r + 1);
+                rw = (int32_t)((int64_t)m->reward_lo + (int64_t)(u % span));
+            }
+            reward_dst[k] = rw;
+        }
     return AVO_OK;
 }
 

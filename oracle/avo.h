@@ -75,6 +75,43 @@ int  avo_set_rule_control(avo_batch *ab, const int32_t *limit, const uint8_t *in
 uint32_t avo_site_key(int order, uint64_t seed, uint64_t n, int b, int pos);
 /* Philox4x64-10 block function, exported so that tests can pin it. */
 void avo_philox4x64(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4]);
+/* Mutation operators (paper Sec. 2.2.1 and the Fig. 2b caption: environments are mutated
+ * by flipping bits of the initial multi-hot map, by changing entries of the rules' input
+ * and output patterns, and by changing the rules' rewards).  Every random draw is a 32-bit
+ * word of Philox4x64-10 (avo_random_word) with key (seed, 0) and counter
+ * (word / 8, generation, individual, stream); stream 1 = map bits, 2 = pattern entries,
+ * 3 = rewards.  Probabilities are 32-bit thresholds: an event with threshold p happens iff
+ * its word is < p (probability p / 2^32). */
+typedef struct {
+    uint64_t seed, generation;
+    uint32_t map_flip_p32;     /* per map bit */
+    uint32_t map_channels;     /* bit c set: channel c of the map may flip */
+    uint32_t entry_p32;        /* per pattern entry inside the rule's n x m */
+    uint32_t entry_channels;   /* bit c set: entries of channel c (C = force) may change */
+    uint32_t reward_p32;       /* per rule */
+    int32_t reward_lo, reward_hi;
+} avo_mutation;
+
+/* 32-bit word `word` (pos % 8 of the block pos / 8, low half of each 64-bit word first). */
+uint32_t avo_random_word(uint64_t seed, uint64_t generation, uint64_t individual,
+                         uint64_t stream, uint64_t word);
+/* Maps uint8 [n][C][H][W] (nonzero = tile): bit e = (c * H + y) * W + x of individual k
+ * flips iff channel c is in map_channels and word e of stream 1 is < map_flip_p32.
+ * dst holds 0/1; dst may equal src. */
+int  avo_mutate_maps(const uint8_t *src, uint8_t *dst, int n, int C, int H, int W,
+                     const avo_mutation *m);
+/* Rules in the av_load_rules layout: shape [S][R][2], patterns [S][R][C+1][mh][mw],
+ * rewards [S][R]; individual = set s.  Entry e = (((r * 2 + io) * (C+1) + c) * mh + i) * mw + j
+ * (io 0 = input, 1 = output) with i < n, j < m of its rule and channel c in entry_channels
+ * changes iff word 2e of stream 2 is < entry_p32; it then takes the lower (word 2e + 1 even)
+ * or higher (odd) of the two values of {-1, 0, 1} other than its own (a value outside the
+ * set counts as 1).  Reward r is redrawn iff word 2r of stream 3 is < reward_p32, to
+ * reward_lo + (word 2r + 1) mod (reward_hi - reward_lo + 1).  Destinations may equal the
+ * sources.  AVO_EINVAL if reward_lo > reward_hi. */
+int  avo_mutate_rules(int S, int R, int C, int mh, int mw, const int32_t *shape,
+                      const int8_t *in_src, const int8_t *out_src, const int32_t *reward_src,
+                      int8_t *in_dst, int8_t *out_dst, int32_t *reward_dst,
+                      const avo_mutation *m);
 int  avo_get_maps(const avo_batch *ab, uint8_t *dst);
 /* Player-centred observation of the current maps (paper Sec. 2.2.2: a local patch of tiles
  * around the player's position; Table 1 uses windows of 5, 10, 20 and 31 cells).
