@@ -180,9 +180,10 @@ MUTANTS = {
     "overlap_cols_short": ("bx < ax + m && ax < bx + mq", "bx < ax + m && ax + 1 < bx + mq"),
     "order_reversed": ("uint32_t rank = (uint32_t)(4095 - pos);", "uint32_t rank = (uint32_t)pos;"),
     "limit_off_by_one": ("uint32_t cut = keys[lim - 1];", "uint32_t cut = keys[lim];"),
-    "random_word_high_half_only": ("out[word / 2] >> (32 * (word % 2))", "out[word / 2] >> 32"),
+    "random_word_high_half_only": ("out[w / 2] >> (32 * (w % 2))", "out[w / 2] >> 32"),
     "step_number_frozen": ("    ab->step_no += 1;\n", ""),
-    "env_not_in_counter": ("(uint64_t)(pos / 8), n, (uint64_t)b, 0", "(uint64_t)(pos / 8), n, 0, 0"),
+    "env_not_in_counter": ("avo_random_word(seed, n, (uint64_t)b, 0, (uint64_t)pos)",
+                           "avo_random_word(seed, n, 0, 0, (uint64_t)pos)"),
     "keys_sorted_ascending": ("return x < y ? 1 : (x > y ? -1 : 0);",
                               "return x < y ? -1 : (x > y ? 1 : 0);"),
     "moves_limited_too": ("const int lim = (loaded && ab->limit)", "const int lim = (ab->limit)"),
