@@ -90,6 +90,45 @@ def cpu_baseline(wl, maps, rules, actions, budget_s: float, threads: int,
             "sample": f"first {nb} of {wl.B} envs x {steps} steps ({dt:.1f} s, {used} threads)"}
 
 
+def _time_us(fn, stream, torch, reps=100):
+    fn()
+    torch.cuda.synchronize()
+    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    g0.record(stream)
+    for _ in range(reps):
+        fn()
+    g1.record(stream)
+    torch.cuda.synchronize()
+    return g0.elapsed_time(g1) * 1e3 / reps
+
+
+def bench_mutation(av, torch, wl, maps, rules, stream, seed):
+    """av_mutate_maps over the population's initial maps (uint8, read + written once) and
+    av_mutate_rules over its rule arrays; HBM bytes are the arrays read and written."""
+    m = av.mutation(seed=seed, generation=1, map_flip=0.01, entry=0.05, reward=0.1)
+    src = torch.from_numpy(maps).cuda()
+    dst = torch.empty_like(src)
+    us_maps = _time_us(lambda: av.av_mutate_maps(src, dst, m), stream, torch)
+    map_bytes = 2 * maps.size
+    dev = [torch.from_numpy(np.ascontiguousarray(x)).cuda() for x in rules]
+    out = [torch.empty_like(x) for x in dev[1:]]
+    us_rules = _time_us(lambda: av.av_mutate_rules(*dev, *out, m), stream, torch)
+    rule_bytes = (2 * (rules[1].size + rules[2].size) + 2 * 4 * rules[3].size
+                  + 4 * rules[0].size)
+
+    def roof(nbytes, us):
+        gbs = nbytes / (us * 1e-6) / 1e9
+        return {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": gbs / HBM_PEAK_GBS, "bytes_per_call": int(nbytes)}
+
+    return {"maps": {"api": "av_mutate_maps", "individuals": int(maps.shape[0]),
+                     "us_per_call": us_maps, "individuals_per_sec": maps.shape[0] / (us_maps * 1e-6),
+                     "philox_blocks_per_call": int(maps.shape[0] * ((maps[0].size + 7) // 8)),
+                     "roofline": roof(map_bytes, us_maps)},
+            "rules": {"api": "av_mutate_rules", "sets": int(rules[1].shape[0]),
+                      "us_per_call": us_rules, "roofline": roof(rule_bytes, us_rules)}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -113,6 +152,8 @@ def main():
                          "reference for the HBM byte counters)")
     ap.add_argument("--observe", type=int, default=0, metavar="W",
                     help="also time av_observe with a W x W window (HBM-bound gather)")
+    ap.add_argument("--mutate", action="store_true",
+                    help="also time the mutation operators on the workload's population")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
@@ -230,6 +271,10 @@ def main():
                                 "frac": moved / (us * 1e-6) / 1e9 / HBM_PEAK_GBS,
                                 "bytes_per_call": moved}}
 
+    mutate = None
+    if args.mutate:
+        mutate = bench_mutation(av, torch, wl, maps, rules, stream, args.seed)
+
     cpu = None
     if not args.no_cpu:
         cpu = cpu_baseline(wl, maps, rules, actions, args.cpu_seconds,
@@ -280,6 +325,7 @@ def main():
             "peak_lane_ops": 256 * 4 * 16 * 2.4e9, "source": traffic["source"]},
         "per_launch_path": per_launch,
         "observe": observe,
+        "mutate": mutate,
         "cpu_baseline": cpu,
     }
     b.close()

@@ -185,6 +185,54 @@ av_status av_observe(av_batch_t b, int32_t w, uint8_t *dst);
  * specified).  AV_ESTATE before av_load_rules.  May synchronise. */
 av_status av_rule_features(av_batch_t b, uint8_t *dst);
 
+/* Mutation operators (paper Sec. 2.2.1 and the Fig. 2b caption: environments are mutated by
+ * flipping bits of the initial multi-hot map, by changing entries of the rules' input and
+ * output patterns, and by changing the rules' rewards), batched over a population of
+ * individuals.  They work on caller-owned device arrays in the layouts av_reset and
+ * av_load_rules take (so a generation is mutated on the GPU and then loaded), need no batch,
+ * and run on `stream` of `device`; asynchronous.  Destinations may equal their sources.
+ *
+ * Randomness: a 32-bit word w of stream t for individual k is half (w % 2, low half first)
+ * of 64-bit output word (w % 8) / 2 of Philox4x64-10 (Salmon et al., SC 2011) at counter
+ * (w / 8, generation, k, t) with key (seed, 0).  An event with threshold p (a *_p32 field)
+ * happens iff its word is < p, i.e. with probability p / 2^32. */
+typedef struct {
+    uint64_t seed;              /* key of every stream */
+    uint64_t generation;        /* counter word: a fresh draw per generation */
+    uint32_t map_flip_p32;      /* per map bit (stream 1) */
+    uint32_t map_channels;      /* bit c set: map channel c may flip */
+    uint32_t entry_p32;         /* per pattern entry inside its rule's n x m (stream 2) */
+    uint32_t entry_channels;    /* bit c set: pattern channel c (C = force) may change */
+    uint32_t reward_p32;        /* per rule reward (stream 3) */
+    int32_t reward_lo, reward_hi; /* a redrawn reward is uniform-by-modulo in [lo, hi] */
+} av_mutation;
+
+/* Map mutation: src, dst device uint8 [n][C][H][W] (nonzero = tile; dst gets 0/1).  Bit
+ * e = (c * H + y) * W + x of individual k flips iff bit c of map_channels is set and word e
+ * of stream 1 is below map_flip_p32.  n >= 0; C in [1, 31]; H, W in [1, 64].  AV_EINVAL for a
+ * NULL pointer (with n > 0), sizes out of range or m == NULL; AV_EDEVICE on a launch
+ * failure. */
+av_status av_mutate_maps(const uint8_t *src, uint8_t *dst, int32_t n, int32_t channels,
+                         int32_t height, int32_t width, const av_mutation *m, int32_t device,
+                         void *stream);
+
+/* Rule mutation in the av_load_rules layout, all device arrays: shape int32 [S][R][2],
+ * in/out patterns int8 [S][R][C+1][max_pat_h][max_pat_w], rewards int32 [S][R]; individual
+ * = set s.  Entry e = (((r * 2 + io) * (C + 1) + c) * max_pat_h + i) * max_pat_w + j (io 0 =
+ * input, 1 = output) with i < n, j < m of its rule and bit c of entry_channels set changes
+ * iff word 2e of stream 2 is below entry_p32; it then takes the lower (word 2e + 1 even) or
+ * higher (odd) of the two values of {-1, 0, 1} other than its own (a value outside that set
+ * counts as 1).  Reward r is redrawn iff word 2r of stream 3 is below reward_p32, to
+ * reward_lo + (word 2r + 1) mod (reward_hi - reward_lo + 1).  Mutated rewards are not
+ * checked against the 2^24 bound here; av_load_rules checks them.  AV_EINVAL for NULL
+ * pointers (with S * R > 0), sizes out of range (S >= 0; R in [0, 252]; C in [1, 31]; pattern
+ * extents in [1, 16]), reward_lo > reward_hi or m == NULL. */
+av_status av_mutate_rules(int32_t num_sets, int32_t num_rules, int32_t channels,
+                          int32_t max_pat_h, int32_t max_pat_w, const int32_t *shape,
+                          const int8_t *in_src, const int8_t *out_src, const int32_t *reward_src,
+                          int8_t *in_dst, int8_t *out_dst, int32_t *reward_dst,
+                          const av_mutation *m, int32_t device, void *stream);
+
 /* Device pointer to the packed current maps, owned by the batch and valid until the
  * next av_reset / av_set_state / av_destroy_batch.  Layout: rows of row_bytes bytes,
  * index [c][env][y] (channel-major over the whole batch); cell (env, c, y, x) is bit x

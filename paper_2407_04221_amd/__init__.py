@@ -32,7 +32,7 @@ ABI_SYMBOLS = ("av_create_batch", "av_load_rules", "av_set_rule_control", "av_re
                "av_step", "av_step_n",
                "av_get_maps", "av_observe", "av_rule_features", "av_state_ptr", "av_get_info",
                "av_get_state", "av_set_state", "av_set_stream", "av_destroy_batch",
-               "av_last_error")
+               "av_mutate_maps", "av_mutate_rules", "av_last_error")
 
 
 class av_config(ctypes.Structure):
@@ -43,6 +43,29 @@ class av_config(ctypes.Structure):
                 ("max_episode_steps", ctypes.c_int32), ("device", ctypes.c_int32),
                 ("engine", ctypes.c_int32), ("rule_mode", ctypes.c_int32),
                 ("stream", ctypes.c_void_p)]
+
+
+class av_mutation(ctypes.Structure):
+    _fields_ = [("seed", ctypes.c_uint64), ("generation", ctypes.c_uint64),
+                ("map_flip_p32", ctypes.c_uint32), ("map_channels", ctypes.c_uint32),
+                ("entry_p32", ctypes.c_uint32), ("entry_channels", ctypes.c_uint32),
+                ("reward_p32", ctypes.c_uint32), ("reward_lo", ctypes.c_int32),
+                ("reward_hi", ctypes.c_int32)]
+
+
+def p32(p: float) -> int:
+    """Probability -> 32-bit threshold (an event happens iff its random word is below it)."""
+    return max(0, min(0xFFFFFFFF, int(round(p * 2**32))))
+
+
+def mutation(seed=0, generation=0, map_flip=0.0, map_channels=0xFFFFFFFF, entry=0.0,
+             entry_channels=0xFFFFFFFF, reward=0.0, reward_lo=-1, reward_hi=1) -> av_mutation:
+    m = av_mutation()
+    m.seed, m.generation = seed, generation
+    m.map_flip_p32, m.map_channels = p32(map_flip), map_channels
+    m.entry_p32, m.entry_channels = p32(entry), entry_channels
+    m.reward_p32, m.reward_lo, m.reward_hi = p32(reward), reward_lo, reward_hi
+    return m
 
 
 class av_info(ctypes.Structure):
@@ -88,6 +111,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "av_set_state": ([P, P, SZ], ctypes.c_int),
         "av_set_stream": ([P, P], ctypes.c_int),
         "av_destroy_batch": ([P], ctypes.c_int),
+        "av_mutate_maps": ([P, P, I32, I32, I32, I32, ctypes.POINTER(av_mutation), I32, P],
+                           ctypes.c_int),
+        "av_mutate_rules": ([I32, I32, I32, I32, I32, P, P, P, P, P, P, P,
+                             ctypes.POINTER(av_mutation), I32, P], ctypes.c_int),
         "av_last_error": ([], ctypes.c_char_p),
     }
     for name, (args, res) in sig.items():
@@ -177,6 +204,39 @@ def av_set_rule_control(batch, limit=None, inhibit=None, order=AV_SITES_ROW_MAJO
     order = SITE_ORDERS.get(order, order) if isinstance(order, str) else order
     _check("av_set_rule_control",
            load_library().av_set_rule_control(batch, pl, pi, int(order), int(seed)))
+
+
+def av_mutate_maps(src, dst, m: av_mutation):
+    """src, dst: device uint8 tensors [n][C][H][W] (may be the same tensor); runs on the
+    current stream of their device."""
+    torch = _torch()
+    shp = tuple(src.shape)
+    if len(shp) != 4:
+        raise ValueError("maps must be [n][C][H][W]")
+    n, C, H, W = shp
+    ps = _dev_ptr(src, torch.uint8, shp, "src")
+    pd = _dev_ptr(dst, torch.uint8, shp, "dst")
+    _check("av_mutate_maps",
+           load_library().av_mutate_maps(ps, pd, n, C, H, W, ctypes.byref(m), src.device.index,
+                                         current_stream_handle()))
+
+
+def av_mutate_rules(shape, in_src, out_src, reward_src, in_dst, out_dst, reward_dst,
+                    m: av_mutation):
+    """Device tensors in the av_load_rules layout: shape int32 [S][R][2], patterns int8
+    [S][R][C+1][mh][mw], rewards int32 [S][R]; destinations may be the sources."""
+    torch = _torch()
+    S, R, C1, mh, mw = tuple(in_src.shape)
+    args = [_dev_ptr(shape, torch.int32, (S, R, 2), "shape"),
+            _dev_ptr(in_src, torch.int8, (S, R, C1, mh, mw), "in_src"),
+            _dev_ptr(out_src, torch.int8, (S, R, C1, mh, mw), "out_src"),
+            _dev_ptr(reward_src, torch.int32, (S, R), "reward_src"),
+            _dev_ptr(in_dst, torch.int8, (S, R, C1, mh, mw), "in_dst"),
+            _dev_ptr(out_dst, torch.int8, (S, R, C1, mh, mw), "out_dst"),
+            _dev_ptr(reward_dst, torch.int32, (S, R), "reward_dst")]
+    _check("av_mutate_rules",
+           load_library().av_mutate_rules(S, R, C1 - 1, mh, mw, *args, ctypes.byref(m),
+                                          in_src.device.index, current_stream_handle()))
 
 
 def av_reset(batch, init_maps):

@@ -569,6 +569,55 @@ av_status av_rule_features(av_batch_t b, uint8_t *dst) {
     return AV_OK;
 }
 
+static MutateArgs mutate_args(const av_mutation &m) {
+    MutateArgs a;
+    a.seed = m.seed; a.generation = m.generation;
+    a.map_flip_p32 = m.map_flip_p32; a.map_channels = m.map_channels;
+    a.entry_p32 = m.entry_p32; a.entry_channels = m.entry_channels;
+    a.reward_p32 = m.reward_p32; a.reward_lo = m.reward_lo; a.reward_hi = m.reward_hi;
+    return a;
+}
+
+av_status av_mutate_maps(const uint8_t *src, uint8_t *dst, int32_t n, int32_t channels,
+                         int32_t height, int32_t width, const av_mutation *m, int32_t device,
+                         void *stream) {
+    g_last_error.clear();
+    if (!m) return fail(AV_EINVAL, "mutation parameters are NULL");
+    if (n < 0 || channels < 1 || channels > 31 || height < 1 || height > kMaxDim || width < 1 ||
+        width > kMaxDim)
+        return fail(AV_EINVAL, "sizes out of range: n %d, C %d, H %d, W %d", n, channels, height,
+                    width);
+    if (n > 0 && (!src || !dst)) return fail(AV_EINVAL, "src and dst must not be NULL");
+    AV_HIP(hipSetDevice(device));
+    AV_HIP(launch_mutate_maps(src, dst, n, channels, height, width, mutate_args(*m),
+                              static_cast<hipStream_t>(stream)));
+    return AV_OK;
+}
+
+av_status av_mutate_rules(int32_t num_sets, int32_t num_rules, int32_t channels,
+                          int32_t max_pat_h, int32_t max_pat_w, const int32_t *shape,
+                          const int8_t *in_src, const int8_t *out_src, const int32_t *reward_src,
+                          int8_t *in_dst, int8_t *out_dst, int32_t *reward_dst,
+                          const av_mutation *m, int32_t device, void *stream) {
+    g_last_error.clear();
+    if (!m) return fail(AV_EINVAL, "mutation parameters are NULL");
+    if (num_sets < 0 || num_rules < 0 || num_rules > kMaxRules || channels < 1 || channels > 31 ||
+        max_pat_h < 1 ||
+        max_pat_h > kMaxPat || max_pat_w < 1 || max_pat_w > kMaxPat)
+        return fail(AV_EINVAL, "sizes out of range: S %d, R %d, C %d, pattern %d x %d", num_sets,
+                    num_rules, channels, max_pat_h, max_pat_w);
+    if (m->reward_lo > m->reward_hi)
+        return fail(AV_EINVAL, "reward_lo %d > reward_hi %d", m->reward_lo, m->reward_hi);
+    if (int64_t(num_sets) * num_rules > 0 &&
+        (!shape || !in_src || !out_src || !reward_src || !in_dst || !out_dst || !reward_dst))
+        return fail(AV_EINVAL, "rule arrays must not be NULL");
+    AV_HIP(hipSetDevice(device));
+    AV_HIP(launch_mutate_rules(num_sets, num_rules, channels, max_pat_h, max_pat_w, shape, in_src,
+                               out_src, reward_src, in_dst, out_dst, reward_dst, mutate_args(*m),
+                               static_cast<hipStream_t>(stream)));
+    return AV_OK;
+}
+
 const void *av_state_ptr(av_batch_t b) {
     g_last_error.clear();
     if (!b) { fail(AV_EINVAL, "batch handle is NULL"); return nullptr; }

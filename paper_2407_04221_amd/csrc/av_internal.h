@@ -117,6 +117,21 @@ hipError_t launch_generic_step(const StepArgs &a, int envs_per_block, hipStream_
 size_t generic_env_lds_bytes(int H, int W, int C, int rules_per_set, bool control = false,
                              bool random = false);
 
+// Mutation operators (k_mutate.hip); MutateArgs mirrors av_mutation.
+struct MutateArgs {
+    uint64_t seed, generation;
+    uint32_t map_flip_p32, map_channels;
+    uint32_t entry_p32, entry_channels;
+    uint32_t reward_p32;
+    int32_t reward_lo, reward_hi;
+};
+hipError_t launch_mutate_maps(const uint8_t *src, uint8_t *dst, int n, int C, int H, int W,
+                              const MutateArgs &m, hipStream_t s);
+hipError_t launch_mutate_rules(int S, int R, int C, int mh, int mw, const int32_t *shape,
+                               const int8_t *in_src, const int8_t *out_src,
+                               const int32_t *reward_src, int8_t *in_dst, int8_t *out_dst,
+                               int32_t *reward_dst, const MutateArgs &m, hipStream_t s);
+
 // Player-centred observation window (k_observe.hip).
 hipError_t launch_observe(const void *state, int B, int C, int H, int W, int row_bytes, int w,
                           uint8_t *dst, hipStream_t s);

@@ -23,6 +23,7 @@
 //   end       done when no player bit is left or the counter reaches L; done
 //             environments reload their initial rows.
 #include "av_internal.h"
+#include "philox.h"
 
 namespace av {
 namespace {
@@ -49,19 +50,6 @@ __device__ inline int lowbit(uint64_t v) { return __ffsll(static_cast<unsigned l
 template <typename RowT>
 __device__ inline RowT low_mask(int bits) {
     return bits >= int(8 * sizeof(RowT)) ? ~RowT(0) : ((RowT(1) << bits) - 1);
-}
-
-// Philox4x64-10 block function (Salmon, Moraes, Dror, Shaw, SC 2011).
-__device__ inline void philox4x64_10(uint64_t x[4], uint64_t k0, uint64_t k1) {
-    for (int round = 0; round < 10; ++round) {
-        const uint64_t m0 = 0xD2E7470EE14C6C93ull, m1 = 0xCA5A826395121157ull;
-        const uint64_t lo0 = m0 * x[0], hi0 = __umul64hi(m0, x[0]);
-        const uint64_t lo1 = m1 * x[2], hi1 = __umul64hi(m1, x[2]);
-        const uint64_t y0 = hi1 ^ x[1] ^ k0, y2 = hi0 ^ x[3] ^ k1;
-        x[0] = y0; x[1] = lo1; x[2] = y2; x[3] = lo0;
-        k0 += 0x9E3779B97F4A7C15ull;
-        k1 += 0xBB67AE8584CAA73Bull;
-    }
 }
 
 // Index-channel value of cell pos: row-major rank 4095 - pos, or, for the random channel,
@@ -122,12 +110,11 @@ __global__ void __launch_bounds__(256) generic_step(StepArgs a, int G) {
             // this step's random index channel, eight cells per Philox block
             const uint64_t n = a.ctl.step_base + uint64_t(k);
             for (int gi = y; gi * 8 < HW; gi += H) {
-                uint64_t x[4] = {uint64_t(gi), n, uint64_t(b), 0};
-                philox4x64_10(x, a.ctl.seed, 0);
+                uint32_t u[8];
+                philox_words(a.ctl.seed, n, uint64_t(b), 0, uint64_t(gi), u);
                 for (int j = 0; j < 8 && gi * 8 + j < HW; ++j) {
                     const int pos = gi * 8 + j;
-                    const uint32_t u = uint32_t(x[j >> 1] >> (32 * (j & 1)));
-                    keys[size_t(g) * HW + pos] = (u & 0xFFFFF000u) | rank_key(pos);
+                    keys[size_t(g) * HW + pos] = (u[j] & 0xFFFFF000u) | rank_key(pos);
                 }
             }
         }

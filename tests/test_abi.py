@@ -95,6 +95,18 @@ def test_null_arguments_are_rejected(lib):
     assert lib.av_observe(None, 5, None) == av.AV_EINVAL
     assert lib.av_rule_features(None, None) == av.AV_EINVAL
     assert lib.av_set_rule_control(None, None, None, 0, 0) == av.AV_EINVAL
+    m = av.mutation()
+    assert lib.av_mutate_maps(None, None, 1, 4, 4, 4, m, 0, None) == av.AV_EINVAL
+    assert lib.av_mutate_maps(None, None, 1, 4, 4, 4, None, 0, None) == av.AV_EINVAL
+    assert lib.av_mutate_maps(None, None, -1, 4, 4, 4, m, 0, None) == av.AV_EINVAL
+    assert lib.av_mutate_maps(None, None, 1, 32, 4, 4, m, 0, None) == av.AV_EINVAL
+    assert lib.av_mutate_rules(1, 1, 4, 3, 3, None, None, None, None, None, None, None, m, 0,
+                               None) == av.AV_EINVAL
+    assert lib.av_mutate_rules(1, 1, 4, 17, 3, None, None, None, None, None, None, None, m, 0,
+                               None) == av.AV_EINVAL
+    bad = av.mutation(reward_lo=2, reward_hi=1)
+    assert lib.av_mutate_rules(0, 0, 4, 3, 3, None, None, None, None, None, None, None, bad, 0,
+                               None) == av.AV_EINVAL
     assert lib.av_state_ptr(None) is None
     info = av.av_info()
     assert lib.av_get_info(None, ctypes.byref(info)) == av.AV_EINVAL
