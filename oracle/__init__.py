@@ -67,11 +67,13 @@ def load(path: str = LIB) -> ctypes.CDLL:
     lib.avo_rule_features.argtypes = [P, P]
     lib.avo_get_maps.argtypes = [P, P]
     lib.avo_get_counters.argtypes = [P, P]
+    lib.avo_set_counters.argtypes = [P, P]
     lib.avo_destroy.argtypes = [P]
     lib.avo_destroy.restype = None
     for f in ("avo_create", "avo_load_rules", "avo_reset", "avo_step", "avo_get_maps",
               "avo_get_counters", "avo_set_rule_mode", "avo_observe", "avo_rule_features",
-              "avo_set_rule_control", "avo_mutate_maps", "avo_mutate_rules"):
+              "avo_set_rule_control", "avo_mutate_maps", "avo_mutate_rules",
+              "avo_set_counters"):
         getattr(lib, f).restype = I
     _libs[path] = lib
     return lib
@@ -183,6 +185,13 @@ class Oracle:
         if rc != AVO_OK:
             raise OracleError("avo_rule_features", rc)
         return out
+
+    def set_counters(self, t):
+        t = np.ascontiguousarray(t, dtype=np.int32)
+        assert t.shape == (self.B,), t.shape
+        rc = self.lib.avo_set_counters(self.h, _ptr(t))
+        if rc != AVO_OK:
+            raise OracleError("avo_set_counters", rc)
 
     def counters(self):
         out = np.zeros(self.B, dtype=np.int32)

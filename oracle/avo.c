@@ -612,6 +612,15 @@ int avo_get_counters(const avo_batch *ab, int32_t *dst)
     return AVO_OK;
 }
 
+int avo_set_counters(avo_batch *ab, const int32_t *src)
+{
+    if (!ab || !src) return AVO_EINVAL;
+    for (int b = 0; b < ab->B; b++)
+        if (src[b] < 0) return AVO_EINVAL;
+    memcpy(ab->t, src, (size_t)ab->B * sizeof(int32_t));
+    return AVO_OK;
+}
+
 void avo_destroy(avo_batch *ab)
 {
     if (!ab) return;

@@ -124,6 +124,8 @@ int  avo_observe(const avo_batch *ab, int w, uint8_t *dst);
  * [.][.][0 = input, 1 = output][0 = entry specified, 1 = entry value (0 when unspecified)]. */
 int  avo_rule_features(const avo_batch *ab, uint8_t *dst);
 int  avo_get_counters(const avo_batch *ab, int32_t *dst);
+/* Set every environment's step counter (t[b] >= 0), e.g. to a search node's depth. */
+int  avo_set_counters(avo_batch *ab, const int32_t *src);
 void avo_destroy(avo_batch *ab);
 
 #ifdef __cplusplus
