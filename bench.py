@@ -129,6 +129,41 @@ def bench_mutation(av, torch, wl, maps, rules, stream, seed):
                       "us_per_call": us_rules, "roofline": roof(rule_bytes, us_rules)}}
 
 
+def bench_search(av, torch, wl, args):
+    """av_search_* from environment 0's map and rule set: levels until the frontier empties or
+    the budget of visits is spent.  Timed with the host clock around the whole search (each
+    level synchronises once).  Bytes per visit: the packed state S = C x H x row bytes moved
+    five times (gathered in, stepped in and out, hashed, copied to the frontier) plus 28 bytes
+    of table slot and 20 of per-child metadata."""
+    from paper_2407_04221_amd import inputs
+    maps, rules, _ = inputs.make_all(wl, args.seed, args.search_variant, T=1)
+    rules = tuple(x[:1] for x in rules)
+    table_log2 = max(10, min(30, int(np.ceil(np.log2(max(2 * args.search, 16))))))
+    g = av.Search(wl.H, wl.W, wl.C, wl.R, wl.max_h, wl.max_w, wl.L, num_actions=5,
+                  max_frontier=args.search_frontier, table_log2=table_log2)
+    g.load_rules(*rules)
+    g.run(maps[0], min(args.search, 20000))          # warm-up (kernels, JIT)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    levels = g.run(maps[0], args.search)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    g.close()
+    visited = levels[-1]["visited"] if levels else 0
+    row_bytes = 2 if wl.W <= 16 else (4 if wl.W <= 32 else 8)
+    S = wl.C * wl.H * row_bytes
+    per_visit = 5 * S + 48
+    gbs = visited * per_visit / dt / 1e9
+    return {"api": "av_search_expand", "variant": args.search_variant, "budget": args.search,
+            "visited": visited, "levels": len(levels), "seconds": dt,
+            "visits_per_sec": visited / dt, "best_reward": levels[-1]["best_reward"] if levels else 0,
+            "best_visit": levels[-1]["best_visit"] if levels else 0,
+            "frontier_peak": max((lv["frontier"] for lv in levels), default=0),
+            "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": gbs / HBM_PEAK_GBS, "bytes_per_visit": per_visit},
+            "level_sizes": [lv["children"] for lv in levels]}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -154,6 +189,10 @@ def main():
                     help="also time av_observe with a W x W window (HBM-bound gather)")
     ap.add_argument("--mutate", action="store_true",
                     help="also time the mutation operators on the workload's population")
+    ap.add_argument("--search", type=int, default=0, metavar="BUDGET",
+                    help="also time the batched search from environment 0 with this many visits")
+    ap.add_argument("--search-variant", default="dense", choices=["literal", "planted", "dense"])
+    ap.add_argument("--search-frontier", type=int, default=1 << 20)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--seed", type=int, default=0)
@@ -271,6 +310,10 @@ def main():
                                 "frac": moved / (us * 1e-6) / 1e9 / HBM_PEAK_GBS,
                                 "bytes_per_call": moved}}
 
+    search = None
+    if args.search:
+        search = bench_search(av, torch, wl, args)
+
     mutate = None
     if args.mutate:
         mutate = bench_mutation(av, torch, wl, maps, rules, stream, args.seed)
@@ -326,6 +369,7 @@ def main():
         "per_launch_path": per_launch,
         "observe": observe,
         "mutate": mutate,
+        "search": search,
         "cpu_baseline": cpu,
     }
     b.close()

@@ -233,6 +233,85 @@ av_status av_mutate_rules(int32_t num_sets, int32_t num_rules, int32_t channels,
                           int8_t *in_dst, int8_t *out_dst, int32_t *reward_dst,
                           const av_mutation *m, int32_t device, void *stream);
 
+/* ---------------------------------------------------------------------------------------
+ * Batched search (paper Sec. 2.2.1: an environment is scored by searching the player's
+ * action sequences; a node is a game state — the map, which holds the player's position,
+ * and the reward accumulated so far — an edge is an action; a state equal to one seen
+ * before keeps the node with the higher reward, then the shallower one).
+ *
+ * The search is level-synchronous (breadth-first, which the paper also names): one
+ * av_search_expand steps every (frontier node, action) pair of the level as one batch with
+ * the step engines above.  Level d:
+ *   - children: frontier nodes in order, for each the actions in order (0..4, or 1..4 with
+ *     num_actions = 4), cut to max_children; child i of a level is visit number
+ *     visited + 1 + i (the root is visit 0);
+ *   - a child is its parent's map stepped once with its action, its step counter starting
+ *     at the parent's depth (so a child of depth max_episode_steps ends its episode); its
+ *     reward is the parent's plus the step's; the best node is the one with the highest
+ *     reward, earliest visit first (the root, reward 0, counts);
+ *   - children whose episode ended are terminal: counted, never expanded;
+ *   - the others are keyed by a 64-bit hash of their packed map (SplitMix64's finalizer
+ *     chained over the rows; equal hashes are taken as equal states).  A child survives iff
+ *     it has the best (reward, -depth) of its key in this level, lowest index among equals,
+ *     and its key is new or it beats the (reward, -depth) stored for the key; survivors in
+ *     index order, cut to max_frontier, are the next frontier.
+ * ------------------------------------------------------------------------------------- */
+typedef struct av_search_s *av_search_t;
+
+typedef struct {
+    int32_t height, width, channels;   /* map shape; limits as av_config */
+    int32_t max_rules, max_pat_h, max_pat_w;
+    int32_t max_episode_steps;         /* L >= 0; 0 = episodes end only without a player */
+    int32_t num_actions;               /* 5 (actions 0..4) or 4 (actions 1..4) */
+    int32_t max_frontier;              /* most nodes kept per level, in [1, 2^24] */
+    int32_t table_log2;                /* hash table of 2^table_log2 slots, in [4, 31] */
+    int32_t device, engine, rule_mode; /* as av_config; engine AUTO picks as for a batch */
+    void *stream;                      /* hipStream_t; NULL = null stream */
+} av_search_config;
+
+typedef struct {
+    int64_t level;          /* levels expanded since av_search_begin */
+    int64_t parents;        /* frontier nodes this call started from */
+    int64_t children;       /* states visited (stepped) by this call */
+    int64_t terminal;       /* of them, episode ends */
+    int64_t survivors;      /* new or improved states, before the max_frontier cut */
+    int64_t frontier;       /* nodes in the frontier now */
+    int64_t visited;        /* states visited since av_search_begin */
+    int64_t best_visit;     /* visit number of the best node (0 = the root) */
+    int32_t best_reward;    /* its accumulated reward */
+    int32_t reserved;
+} av_search_info;
+
+/* Create a search: a children batch of num_actions x max_frontier environments, frontier
+ * buffers and the hash table (28 bytes per slot) on cfg->device.  AV_EINVAL for sizes out of
+ * range, AV_ENOMEM if the device allocations fail. */
+av_status av_search_create(const av_search_config *cfg, av_search_t *out);
+
+/* The rule set searched (one set, host arrays, layouts and checks as av_load_rules with
+ * S = 1).  Synchronises. */
+av_status av_search_load_rules(av_search_t s, int32_t num_rules, const int32_t *shape,
+                               const int8_t *in_pat, const int8_t *out_pat,
+                               const int32_t *reward);
+
+/* Start from root (device uint8 [C][H][W], nonzero = tile): frontier = {root} at depth 0
+ * and reward 0, table = {root}, no visits.  AV_ESTATE before av_search_load_rules. */
+av_status av_search_begin(av_search_t s, const uint8_t *root);
+
+/* Expand one level (above) with at most max_children >= 0 children; fills *info (host).
+ * An empty frontier or max_children = 0 expands nothing and keeps the frontier.  A search
+ * visits at most 2^32 - 2 states (AV_EINVAL beyond).
+ * Synchronises (the next level's size is needed on the host).  AV_ENOMEM when an insertion
+ * finds 4096 consecutive slots taken by other keys (the table is too full): the search must
+ * then be restarted with av_search_begin. */
+av_status av_search_expand(av_search_t s, int64_t max_children, av_search_info *info);
+
+/* The current frontier: maps device uint8 [N][C][H][W], reward and depth device int32 [N],
+ * N = info.frontier; any pointer may be NULL to skip it.  Asynchronous. */
+av_status av_search_frontier(av_search_t s, uint8_t *maps, int32_t *reward, int32_t *depth);
+
+/* Free the search; NULL is a no-op.  Synchronises. */
+av_status av_search_destroy(av_search_t s);
+
 /* Device pointer to the packed current maps, owned by the batch and valid until the
  * next av_reset / av_set_state / av_destroy_batch.  Layout: rows of row_bytes bytes,
  * index [c][env][y] (channel-major over the whole batch); cell (env, c, y, x) is bit x

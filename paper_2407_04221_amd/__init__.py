@@ -32,7 +32,9 @@ ABI_SYMBOLS = ("av_create_batch", "av_load_rules", "av_set_rule_control", "av_re
                "av_step", "av_step_n",
                "av_get_maps", "av_observe", "av_rule_features", "av_state_ptr", "av_get_info",
                "av_get_state", "av_set_state", "av_set_stream", "av_destroy_batch",
-               "av_mutate_maps", "av_mutate_rules", "av_last_error")
+               "av_mutate_maps", "av_mutate_rules", "av_search_create", "av_search_load_rules",
+               "av_search_begin", "av_search_expand", "av_search_frontier", "av_search_destroy",
+               "av_last_error")
 
 
 class av_config(ctypes.Structure):
@@ -66,6 +68,19 @@ def mutation(seed=0, generation=0, map_flip=0.0, map_channels=0xFFFFFFFF, entry=
     m.entry_p32, m.entry_channels = p32(entry), entry_channels
     m.reward_p32, m.reward_lo, m.reward_hi = p32(reward), reward_lo, reward_hi
     return m
+
+
+class av_search_config(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "height", "width", "channels", "max_rules", "max_pat_h", "max_pat_w",
+        "max_episode_steps", "num_actions", "max_frontier", "table_log2", "device", "engine",
+        "rule_mode")] + [("stream", ctypes.c_void_p)]
+
+
+class av_search_info(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in (
+        "level", "parents", "children", "terminal", "survivors", "frontier", "visited",
+        "best_visit")] + [("best_reward", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 class av_info(ctypes.Structure):
@@ -115,6 +130,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                            ctypes.c_int),
         "av_mutate_rules": ([I32, I32, I32, I32, I32, P, P, P, P, P, P, P,
                              ctypes.POINTER(av_mutation), I32, P], ctypes.c_int),
+        "av_search_create": ([ctypes.POINTER(av_search_config), ctypes.POINTER(P)], ctypes.c_int),
+        "av_search_load_rules": ([P, I32, P, P, P, P], ctypes.c_int),
+        "av_search_begin": ([P, P], ctypes.c_int),
+        "av_search_expand": ([P, ctypes.c_int64, ctypes.POINTER(av_search_info)], ctypes.c_int),
+        "av_search_frontier": ([P, P, P, P], ctypes.c_int),
+        "av_search_destroy": ([P], ctypes.c_int),
         "av_last_error": ([], ctypes.c_char_p),
     }
     for name, (args, res) in sig.items():
@@ -415,6 +436,91 @@ class Batch:
     def close(self):
         if getattr(self, "h", None) is not None:
             av_destroy_batch(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Search:
+    """Level-synchronous search over action sequences on one GPU (av_search_*): every level
+    steps all (frontier node, action) pairs as one batch and deduplicates states in a device
+    hash table.  The methods marshal arguments only."""
+
+    def __init__(self, height, width, channels, max_rules, max_pat_h, max_pat_w,
+                 max_episode_steps=0, num_actions=5, max_frontier=1 << 16, table_log2=20,
+                 device=None, engine="auto", rule_mode="parallel"):
+        torch = _torch()
+        self.device = torch.device("cuda", torch.cuda.current_device() if device is None
+                                   else device)
+        self.H, self.W, self.C = height, width, channels
+        cfg = av_search_config(height, width, channels, max_rules, max_pat_h, max_pat_w,
+                               max_episode_steps, num_actions, max_frontier, table_log2,
+                               self.device.index, ENGINES[engine] if isinstance(engine, str)
+                               else engine, RULE_MODES[rule_mode] if isinstance(rule_mode, str)
+                               else rule_mode, current_stream_handle())
+        h = ctypes.c_void_p()
+        _check("av_search_create", load_library().av_search_create(ctypes.byref(cfg),
+                                                                   ctypes.byref(h)))
+        self.h = h
+        self.n_front = 0
+
+    def load_rules(self, shape, in_pat, out_pat, reward):
+        shape, ps = _host(shape, np.int32, "shape")
+        in_pat, pi = _host(in_pat, np.int8, "in_pat")
+        out_pat, po = _host(out_pat, np.int8, "out_pat")
+        reward, pr = _host(reward, np.int32, "reward")
+        if shape.ndim == 3 and shape.shape[0] != 1:
+            raise ValueError("a search takes one rule set (S = 1)")
+        R = shape.shape[1] if shape.ndim == 3 else 0
+        _check("av_search_load_rules",
+               load_library().av_search_load_rules(self.h, R, ps, pi, po, pr))
+
+    def begin(self, root):
+        torch = _torch()
+        if not isinstance(root, torch.Tensor):
+            root = torch.from_numpy(np.ascontiguousarray(root, dtype=np.uint8))
+        root = root.to(self.device).contiguous()
+        p = _dev_ptr(root, torch.uint8, (self.C, self.H, self.W), "root")
+        _check("av_search_begin", load_library().av_search_begin(self.h, p))
+        self.n_front = 1
+
+    def expand(self, max_children) -> dict:
+        info = av_search_info()
+        _check("av_search_expand",
+               load_library().av_search_expand(self.h, int(max_children), ctypes.byref(info)))
+        self.n_front = info.frontier
+        return {k: getattr(info, k) for k, _ in av_search_info._fields_ if k != "reserved"}
+
+    def frontier(self):
+        """(maps uint8 [N][C][H][W], reward int32 [N], depth int32 [N]) device tensors."""
+        torch = _torch()
+        n = self.n_front
+        maps = torch.empty((n, self.C, self.H, self.W), dtype=torch.uint8, device=self.device)
+        reward = torch.empty(n, dtype=torch.int32, device=self.device)
+        depth = torch.empty(n, dtype=torch.int32, device=self.device)
+        if n:
+            _check("av_search_frontier", load_library().av_search_frontier(
+                self.h, ctypes.c_void_p(maps.data_ptr()), ctypes.c_void_p(reward.data_ptr()),
+                ctypes.c_void_p(depth.data_ptr())))
+        return maps, reward, depth
+
+    def run(self, root, budget, max_levels=1 << 30):
+        self.begin(root)
+        out = []
+        visited = 0
+        while self.n_front and visited < budget and len(out) < max_levels:
+            info = self.expand(budget - visited)
+            visited = info["visited"]
+            out.append(info)
+        return out
+
+    def close(self):
+        if getattr(self, "h", None) is not None:
+            load_library().av_search_destroy(self.h)
             self.h = None
 
     def __del__(self):

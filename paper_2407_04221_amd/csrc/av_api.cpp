@@ -234,6 +234,37 @@ av_status set_device(av_batch_t b) {
 
 }  // namespace
 
+namespace av {
+
+void *batch_state(av_batch_t b) { return b->d_state; }
+int32_t *batch_counters(av_batch_t b) { return b->d_t; }
+int batch_row_bytes(av_batch_t b) { return b->row_bytes; }
+av_status set_error(av_status st, const char *msg) { return fail(st, "%s", msg); }
+
+av_status step_prefix(av_batch_t b, int n, const uint8_t *actions, float *rewards,
+                      uint8_t *done) {
+    const av_config &c = b->cfg;
+    if (n < 1 || n > c.num_envs) return fail(AV_EINVAL, "prefix of %d environments", n);
+    if (!b->have_rules) return fail(AV_ESTATE, "no rules loaded");
+    StepArgs a{};
+    a.B = n; a.H = c.height; a.W = c.width; a.C = c.channels;
+    a.L = c.max_episode_steps; a.per_env = 0; a.k = 1;
+    a.sequential = c.rule_mode == AV_RULES_SEQUENTIAL;
+    a.row_bytes = b->row_bytes;
+    a.state = b->d_state; a.init = b->d_init; a.t = b->d_t;
+    a.actions = actions; a.rewards = rewards; a.done = done;
+    a.prog = b->dprog;
+    if (b->engine == AV_ENGINE_LANE16)
+        AV_HIP(launch_lane16_step(a, b->dlprog, b->stream));
+    else if (b->engine == AV_ENGINE_WAVE)
+        AV_HIP(launch_wave_step(a, b->stream));
+    else
+        AV_HIP(launch_generic_step(a, b->envs_per_block, b->stream));
+    return AV_OK;
+}
+
+}  // namespace av
+
 extern "C" {
 
 const char *av_last_error(void) { return g_last_error.c_str(); }

@@ -132,6 +132,40 @@ hipError_t launch_mutate_rules(int S, int R, int C, int mh, int mw, const int32_
                                const int32_t *reward_src, int8_t *in_dst, int8_t *out_dst,
                                int32_t *reward_dst, const MutateArgs &m, hipStream_t s);
 
+// Batched search (k_search.hip, av_search.cpp).  One level's device arrays and sizes.
+struct SearchArgs {
+    int32_t n = 0, A = 5, C = 0, H = 0, cap = 0;   // children, actions, channels, rows, frontier cap
+    uint64_t visited = 0;                          // visits before this level
+    uint32_t cur_epoch = 0;                        // this level's stamp (levels count from 1)
+    const int32_t *front_reward = nullptr, *front_depth = nullptr;   // [nf]
+    const float *rew = nullptr;                    // [n] step rewards of the children
+    const uint8_t *done = nullptr;                 // [n]
+    int32_t *kid_reward = nullptr, *kid_depth = nullptr;             // [n]
+    uint64_t *kid_val = nullptr;                   // [n] packed (reward, -depth)
+    int64_t *slot = nullptr;                       // [n] table slot, -1 if none
+    uint64_t *keys = nullptr, *vals = nullptr, *claim = nullptr;     // [slots]
+    uint32_t *epoch = nullptr;                     // [slots]
+    uint64_t mask = 0;                             // slots - 1
+    uint64_t *best = nullptr;                      // packed (reward, -visit)
+    uint32_t *counts = nullptr;                    // terminal, overflow, survivors
+    int32_t *block_count = nullptr;                // [ceil(n / 256)]
+    int32_t *src_of = nullptr;                     // [cap] child of each next-frontier node
+    int32_t *next_reward = nullptr, *next_depth = nullptr;           // [cap]
+    void *next = nullptr;                          // next frontier rows [C][nn][H]
+};
+// phase 0 gather, 1 post/claim/flag/scan/place, 2 copy rows (nn nodes), 3 root insert.
+hipError_t launch_search_phase(const SearchArgs &a, int row_bytes, const void *front, int nf,
+                               void *kids, int32_t *kid_t, hipStream_t s, int phase, int nn);
+
+// Internal access to a batch for the search (av_api.cpp).
+void *batch_state(av_batch_t b);
+int32_t *batch_counters(av_batch_t b);
+int batch_row_bytes(av_batch_t b);
+// One step of the first n environments of b, whose state rows are laid out [C][n][H].
+av_status step_prefix(av_batch_t b, int n, const uint8_t *actions, float *rewards,
+                      uint8_t *done);
+av_status set_error(av_status st, const char *msg);
+
 // Player-centred observation window (k_observe.hip).
 hipError_t launch_observe(const void *state, int B, int C, int H, int W, int row_bytes, int w,
                           uint8_t *dst, hipStream_t s);

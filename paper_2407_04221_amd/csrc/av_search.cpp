@@ -1,0 +1,278 @@
+// Batched search (include/autoverse.h, av_search_*): host side.  Owns a children batch
+// (stepped with the batch engines), two frontier buffers, the hash table and the per-level
+// scratch arrays; each level runs gather -> step -> post/claim/flag/scan/place -> copy on the
+// search's stream with one synchronisation to learn the next frontier's size.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <new>
+#include <vector>
+
+#include "av_internal.h"
+
+using namespace av;
+
+struct av_search_s {
+    av_search_config cfg{};
+    hipStream_t stream = nullptr;
+    av_batch_t kids = nullptr;       // num_actions x max_frontier environments
+    int row_bytes = 0;
+    int A = 5;
+    int64_t cap = 0;                 // max_frontier
+    uint64_t slots = 0;
+    void *front[2] = {nullptr, nullptr};
+    int32_t *reward[2] = {nullptr, nullptr}, *depth[2] = {nullptr, nullptr};
+    int cur = 0;                     // which frontier buffer is current
+    int64_t n_front = 0;
+    uint8_t *actions = nullptr;      // [A * cap]: child i takes action i % A (+1 for A = 4)
+    float *rew = nullptr;
+    uint8_t *done = nullptr;
+    int32_t *kid_reward = nullptr, *kid_depth = nullptr, *block_count = nullptr, *src_of = nullptr;
+    uint64_t *kid_val = nullptr;
+    int64_t *slot = nullptr;
+    uint64_t *keys = nullptr, *vals = nullptr, *claim = nullptr, *best = nullptr;
+    uint32_t *epoch = nullptr, *counts = nullptr;
+    bool have_rules = false, begun = false;
+    int64_t level = 0, visited = 0;
+};
+
+namespace {
+
+#define SEARCH_HIP(call)                                                                 \
+    do {                                                                                 \
+        hipError_t e_ = (call);                                                          \
+        if (e_ != hipSuccess) {                                                          \
+            char m_[256];                                                                \
+            std::snprintf(m_, sizeof m_, "%s failed: %s", #call, hipGetErrorString(e_)); \
+            return set_error(e_ == hipErrorOutOfMemory ? AV_ENOMEM : AV_EDEVICE, m_);    \
+        }                                                                                \
+    } while (0)
+
+template <typename T>
+hipError_t alloc(T **p, size_t count) {
+    return hipMalloc(reinterpret_cast<void **>(p), std::max<size_t>(count, 1) * sizeof(T));
+}
+
+void release(av_search_t s) {
+    void *ptrs[] = {s->front[0], s->front[1], s->reward[0], s->reward[1], s->depth[0], s->depth[1],
+                    s->actions, s->rew, s->done, s->kid_reward, s->kid_depth, s->block_count,
+                    s->src_of, s->kid_val, s->slot, s->keys, s->vals, s->claim, s->best, s->epoch,
+                    s->counts};
+    for (void *p : ptrs)
+        if (p) (void)hipFree(p);
+    if (s->kids) av_destroy_batch(s->kids);
+}
+
+SearchArgs level_args(av_search_t s, int n) {
+    SearchArgs a;
+    a.n = n; a.A = s->A; a.C = s->cfg.channels; a.H = s->cfg.height; a.cap = int(s->cap);
+    a.visited = uint64_t(s->visited);
+    a.cur_epoch = uint32_t(s->level + 1);
+    a.front_reward = s->reward[s->cur]; a.front_depth = s->depth[s->cur];
+    a.rew = s->rew; a.done = s->done;
+    a.kid_reward = s->kid_reward; a.kid_depth = s->kid_depth; a.kid_val = s->kid_val;
+    a.slot = s->slot;
+    a.keys = s->keys; a.vals = s->vals; a.claim = s->claim; a.epoch = s->epoch;
+    a.mask = s->slots - 1;
+    a.best = s->best; a.counts = s->counts;
+    a.block_count = s->block_count; a.src_of = s->src_of;
+    a.next_reward = s->reward[1 - s->cur]; a.next_depth = s->depth[1 - s->cur];
+    a.next = s->front[1 - s->cur];
+    return a;
+}
+
+av_status read_best(av_search_t s, av_search_info *info) {
+    uint64_t best = 0;
+    SEARCH_HIP(hipMemcpyAsync(&best, s->best, sizeof best, hipMemcpyDeviceToHost, s->stream));
+    SEARCH_HIP(hipStreamSynchronize(s->stream));
+    info->best_reward = int32_t(uint32_t(best >> 32) ^ 0x80000000u);
+    info->best_visit = int64_t(0xFFFFFFFFull - (best & 0xFFFFFFFFull));
+    return AV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+av_status av_search_create(const av_search_config *cfg, av_search_t *out) {
+    if (!out) return set_error(AV_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (!cfg) return set_error(AV_EINVAL, "cfg is NULL");
+    const av_search_config &c = *cfg;
+    if (c.num_actions != 4 && c.num_actions != 5)
+        return set_error(AV_EINVAL, "num_actions must be 4 or 5");
+    if (c.max_frontier < 1 || c.max_frontier > (1 << 24))
+        return set_error(AV_EINVAL, "max_frontier must be in [1, 2^24]");
+    if (c.table_log2 < 4 || c.table_log2 > 31)
+        return set_error(AV_EINVAL, "table_log2 must be in [4, 31]");
+    av_config bc{};
+    bc.num_envs = c.num_actions * c.max_frontier;
+    bc.height = c.height; bc.width = c.width; bc.channels = c.channels;
+    bc.max_rules = c.max_rules; bc.max_pat_h = c.max_pat_h; bc.max_pat_w = c.max_pat_w;
+    bc.per_env_rules = 0; bc.max_episode_steps = c.max_episode_steps;
+    bc.device = c.device; bc.engine = c.engine; bc.rule_mode = c.rule_mode; bc.stream = c.stream;
+    av_batch_t kids = nullptr;
+    if (av_status st = av_create_batch(&bc, &kids)) return st;   // checks the shared limits
+    av_search_s *s = new (std::nothrow) av_search_s;
+    if (!s) {
+        av_destroy_batch(kids);
+        return set_error(AV_ENOMEM, "host allocation failed");
+    }
+    s->cfg = c;
+    s->stream = static_cast<hipStream_t>(c.stream);
+    s->kids = kids;
+    s->row_bytes = batch_row_bytes(kids);
+    s->A = c.num_actions;
+    s->cap = c.max_frontier;
+    s->slots = uint64_t(1) << c.table_log2;
+    const size_t nk = size_t(s->A) * s->cap;
+    const size_t fbytes = size_t(c.channels) * s->cap * c.height * s->row_bytes;
+    hipError_t e = hipSuccess;
+    for (int k = 0; k < 2 && e == hipSuccess; ++k) {
+        e = hipMalloc(&s->front[k], fbytes);
+        if (e == hipSuccess) e = alloc(&s->reward[k], s->cap);
+        if (e == hipSuccess) e = alloc(&s->depth[k], s->cap);
+    }
+    if (e == hipSuccess) e = alloc(&s->actions, nk);
+    if (e == hipSuccess) e = alloc(&s->rew, nk);
+    if (e == hipSuccess) e = alloc(&s->done, nk);
+    if (e == hipSuccess) e = alloc(&s->kid_reward, nk);
+    if (e == hipSuccess) e = alloc(&s->kid_depth, nk);
+    if (e == hipSuccess) e = alloc(&s->kid_val, nk);
+    if (e == hipSuccess) e = alloc(&s->slot, nk);
+    if (e == hipSuccess) e = alloc(&s->block_count, (nk + 255) / 256);
+    if (e == hipSuccess) e = alloc(&s->src_of, s->cap);
+    if (e == hipSuccess) e = alloc(&s->keys, s->slots);
+    if (e == hipSuccess) e = alloc(&s->vals, s->slots);
+    if (e == hipSuccess) e = alloc(&s->claim, s->slots);
+    if (e == hipSuccess) e = alloc(&s->epoch, s->slots);
+    if (e == hipSuccess) e = alloc(&s->best, 1);
+    if (e == hipSuccess) e = alloc(&s->counts, 3);
+    if (e == hipSuccess) {
+        std::vector<uint8_t> acts(nk);
+        for (size_t i = 0; i < nk; ++i) acts[i] = uint8_t(i % s->A + (s->A == 4 ? 1 : 0));
+        e = hipMemcpy(s->actions, acts.data(), nk, hipMemcpyHostToDevice);
+    }
+    if (e != hipSuccess) {
+        release(s);
+        delete s;
+        char m[160];
+        std::snprintf(m, sizeof m, "search allocation: %s", hipGetErrorString(e));
+        return set_error(e == hipErrorOutOfMemory ? AV_ENOMEM : AV_EDEVICE, m);
+    }
+    *out = s;
+    return AV_OK;
+}
+
+av_status av_search_load_rules(av_search_t s, int32_t num_rules, const int32_t *shape,
+                               const int8_t *in_pat, const int8_t *out_pat,
+                               const int32_t *reward) {
+    if (!s) return set_error(AV_EINVAL, "search handle is NULL");
+    if (av_status st = av_load_rules(s->kids, num_rules, shape, in_pat, out_pat, reward)) return st;
+    s->have_rules = true;
+    return AV_OK;
+}
+
+av_status av_search_begin(av_search_t s, const uint8_t *root) {
+    if (!s) return set_error(AV_EINVAL, "search handle is NULL");
+    if (!root) return set_error(AV_EINVAL, "root is NULL");
+    if (!s->have_rules) return set_error(AV_ESTATE, "call av_search_load_rules first");
+    const av_search_config &c = s->cfg;
+    SEARCH_HIP(hipSetDevice(c.device));
+    s->cur = 0;
+    SEARCH_HIP(launch_pack(root, s->front[0], nullptr, 1, c.channels, c.height, c.width,
+                           s->row_bytes, s->stream));
+    SEARCH_HIP(hipMemsetAsync(s->reward[0], 0, sizeof(int32_t), s->stream));
+    SEARCH_HIP(hipMemsetAsync(s->depth[0], 0, sizeof(int32_t), s->stream));
+    SEARCH_HIP(hipMemsetAsync(s->keys, 0, s->slots * sizeof(uint64_t), s->stream));
+    SEARCH_HIP(hipMemsetAsync(s->vals, 0, s->slots * sizeof(uint64_t), s->stream));
+    SEARCH_HIP(hipMemsetAsync(s->claim, 0, s->slots * sizeof(uint64_t), s->stream));
+    SEARCH_HIP(hipMemsetAsync(s->epoch, 0, s->slots * sizeof(uint32_t), s->stream));
+    SEARCH_HIP(hipMemsetAsync(s->counts, 0, 3 * sizeof(uint32_t), s->stream));
+    SearchArgs a = level_args(s, 1);
+    SEARCH_HIP(launch_search_phase(a, s->row_bytes, s->front[0], 1, nullptr, nullptr, s->stream, 3,
+                                   0));
+    s->n_front = 1;
+    s->level = 0;
+    s->visited = 0;
+    s->begun = true;
+    return AV_OK;
+}
+
+av_status av_search_expand(av_search_t s, int64_t max_children, av_search_info *info) {
+    if (!s) return set_error(AV_EINVAL, "search handle is NULL");
+    if (!info) return set_error(AV_EINVAL, "info is NULL");
+    if (max_children < 0) return set_error(AV_EINVAL, "max_children must be >= 0");
+    if (!s->begun) return set_error(AV_ESTATE, "call av_search_begin first");
+    SEARCH_HIP(hipSetDevice(s->cfg.device));
+    *info = av_search_info{};
+    info->parents = s->n_front;
+    const int64_t n = std::min<int64_t>(int64_t(s->A) * s->n_front, max_children);
+    if (s->visited + n > int64_t(0xFFFFFFFEll))
+        return set_error(AV_EINVAL, "a search may visit at most 2^32 - 2 states");
+    if (n > 0) {
+        const av_search_config &c = s->cfg;
+        SearchArgs a = level_args(s, int(n));
+        void *kst = batch_state(s->kids);
+        SEARCH_HIP(hipMemsetAsync(s->counts, 0, 3 * sizeof(uint32_t), s->stream));
+        SEARCH_HIP(launch_search_phase(a, s->row_bytes, s->front[s->cur], int(s->n_front), kst,
+                                       batch_counters(s->kids), s->stream, 0, 0));
+        if (av_status st = step_prefix(s->kids, int(n), s->actions, s->rew, s->done)) return st;
+        SEARCH_HIP(launch_search_phase(a, s->row_bytes, s->front[s->cur], int(s->n_front), kst,
+                                       nullptr, s->stream, 1, 0));
+        uint32_t counts[3];
+        SEARCH_HIP(hipMemcpyAsync(counts, s->counts, sizeof counts, hipMemcpyDeviceToHost,
+                                  s->stream));
+        SEARCH_HIP(hipStreamSynchronize(s->stream));
+        if (counts[1]) {
+            s->begun = false;
+            return set_error(AV_ENOMEM, "search table too full (an insertion probed 4096 slots); "
+                                        "use a larger table_log2 and call av_search_begin again");
+        }
+        const int64_t nn = std::min<int64_t>(counts[2], s->cap);
+        SEARCH_HIP(launch_search_phase(a, s->row_bytes, s->front[s->cur], int(s->n_front), kst,
+                                       nullptr, s->stream, 2, int(nn)));
+        s->cur = 1 - s->cur;
+        s->n_front = nn;
+        s->visited += n;
+        s->level += 1;
+        info->children = n;
+        info->terminal = counts[0];
+        info->survivors = counts[2];
+        (void)c;
+    }
+    info->level = s->level;
+    info->frontier = s->n_front;
+    info->visited = s->visited;
+    return read_best(s, info);
+}
+
+av_status av_search_frontier(av_search_t s, uint8_t *maps, int32_t *reward, int32_t *depth) {
+    if (!s) return set_error(AV_EINVAL, "search handle is NULL");
+    if (!s->begun) return set_error(AV_ESTATE, "call av_search_begin first");
+    const av_search_config &c = s->cfg;
+    SEARCH_HIP(hipSetDevice(c.device));
+    const int n = int(s->n_front);
+    if (n == 0) return AV_OK;
+    if (maps)
+        SEARCH_HIP(launch_unpack(s->front[s->cur], maps, n, c.channels, c.height, c.width,
+                                 s->row_bytes, s->stream));
+    if (reward)
+        SEARCH_HIP(hipMemcpyAsync(reward, s->reward[s->cur], n * sizeof(int32_t),
+                                  hipMemcpyDeviceToDevice, s->stream));
+    if (depth)
+        SEARCH_HIP(hipMemcpyAsync(depth, s->depth[s->cur], n * sizeof(int32_t),
+                                  hipMemcpyDeviceToDevice, s->stream));
+    return AV_OK;
+}
+
+av_status av_search_destroy(av_search_t s) {
+    if (!s) return AV_OK;
+    if (hipSetDevice(s->cfg.device) == hipSuccess) (void)hipStreamSynchronize(s->stream);
+    release(s);
+    delete s;
+    return AV_OK;
+}
+
+}  // extern "C"

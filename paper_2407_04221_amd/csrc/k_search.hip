@@ -1,0 +1,314 @@
+// Kernels of the batched search (paper Sec. 2.2.1: environments are scored by searching the
+// player's action sequences; a node is a game state, an edge an action, and a state equal to
+// one seen before keeps the node with the higher reward, then the shallower one).
+//
+// One level of a level-synchronous search over n children (parent i / A, action i % A):
+//   gather    the frontier's packed rows are copied into the children batch, child i from
+//             parent i / A, and the child's step counter starts at the parent's depth;
+//   (step)    the children batch takes one step with the batch engines;
+//   post      reward and depth are accumulated, the best (highest reward, earliest visit)
+//             is kept with one 64-bit atomicMax, terminal children are counted, and every
+//             other child hashes its packed map and inserts it into the open-addressing
+//             table: the slot's value becomes the max of (reward, -depth) packed in 64 bits;
+//             a child that raised it stamps the slot with this level's epoch;
+//   claim     children whose value is the slot's value, in a slot stamped this level, claim
+//             it with atomicMax(epoch, ~index): the lowest index among the best wins;
+//   flag      a child survives iff it holds its slot's claim; per-block survivor counts;
+//   scan      exclusive prefix sum of the block counts (one workgroup);
+//   place     survivors get their frontier position (block offset + in-block prefix);
+//   copy      the next frontier's rows, reward and depth are gathered from the survivors.
+// Keys are 64-bit hashes of the packed map (equal hash is taken as equal state).
+#include <algorithm>
+
+#include "av_internal.h"
+
+namespace av {
+namespace {
+
+constexpr uint32_t kMaxProbe = 4096;   // longest probe sequence before the table counts as full
+
+template <typename RowT>
+__device__ inline uint64_t row_at(const void *base, size_t idx) {
+    return uint64_t(static_cast<const RowT *>(base)[idx]);
+}
+
+// SplitMix64 finalizer (Steele, Lea, Flood, OOPSLA 2014): a bijective 64-bit mixer.
+__device__ inline uint64_t mix64(uint64_t z) {
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+// Hash of environment i's map in a packed [C][n][H] buffer: chained mixing of the rows in
+// (channel, row) order; 0 is reserved for empty slots.  When an environment's rows of one
+// channel fill whole 16-byte words they are read 16 bytes at a time (same rows, same order).
+template <typename RowT>
+__device__ inline uint64_t map_hash(const void *state, int i, int n, int C, int H) {
+    uint64_t h = 0x9E3779B97F4A7C15ull;
+    constexpr int per16 = 16 / sizeof(RowT);
+    if (H % per16 == 0) {
+        for (int c = 0; c < C; ++c) {
+            const uint4 *blk = reinterpret_cast<const uint4 *>(
+                static_cast<const RowT *>(state) + (size_t(c) * n + i) * H);
+            for (int v = 0; v < H / per16; ++v) {
+                const uint4 w = blk[v];
+                const uint64_t q[2] = {uint64_t(w.x) | (uint64_t(w.y) << 32),
+                                       uint64_t(w.z) | (uint64_t(w.w) << 32)};
+                for (int k = 0; k < per16; ++k) {
+                    const int bits = 8 * int(sizeof(RowT));
+                    const uint64_t word = q[(k * bits) / 64];
+                    const uint64_t row = bits == 64 ? word : (word >> ((k * bits) % 64)) &
+                                                                 ((uint64_t(1) << bits) - 1);
+                    h = mix64(h ^ row);
+                }
+            }
+        }
+    } else {
+        for (int c = 0; c < C; ++c)
+            for (int y = 0; y < H; ++y)
+                h = mix64(h ^ row_at<RowT>(state, (size_t(c) * n + i) * H + y));
+    }
+    return h ? h : 1;
+}
+
+// Copy environment blocks (one channel's H rows) 16 bytes per thread: destination block
+// (c, i) of a [C][n][H] buffer comes from source block (c, from(i)) of a [C][nsrc][H] buffer,
+// with from(i) = i / A (parents of the children) or src_of[i] (survivors).
+__global__ void __launch_bounds__(256) copy16_kernel(const uint4 *src, int nsrc, uint4 *dst, int n,
+                                                     int C, int chunks, int A,
+                                                     const int32_t *src_of, int32_t *kid_t,
+                                                     const int32_t *fdepth) {
+    const size_t t = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (kid_t && t < size_t(n)) kid_t[t] = fdepth[t / A];
+    if (t >= size_t(C) * n * chunks) return;
+    const int k = int(t % chunks);
+    const size_t ci = t / chunks;
+    const int i = int(ci % n), c = int(ci / n);
+    const int from = src_of ? src_of[i] : i / A;
+    dst[t] = src[(size_t(c) * nsrc + from) * chunks + k];
+}
+
+__device__ inline uint64_t pack_value(int32_t reward, int32_t depth) {
+    return (uint64_t(uint32_t(reward) ^ 0x80000000u) << 32) | uint64_t(0xFFFFFFFFu - uint32_t(depth));
+}
+
+// Find or claim the slot of key h; returns -1 when kMaxProbe slots are all taken by others.
+__device__ inline int64_t probe(uint64_t *keys, uint64_t mask, uint64_t h) {
+    uint64_t s = h & mask;
+    for (uint32_t k = 0; k < kMaxProbe; ++k) {
+        const uint64_t prev = atomicCAS(reinterpret_cast<unsigned long long *>(&keys[s]), 0ull,
+                                        static_cast<unsigned long long>(h));
+        if (prev == 0 || prev == h) return int64_t(s);
+        s = (s + 1) & mask;
+    }
+    return -1;
+}
+
+template <typename RowT>
+__global__ void __launch_bounds__(256) gather_kernel(const void *front, int nf, const int32_t *fdepth,
+                                                     void *kids, int32_t *kid_t, int n, int A,
+                                                     int C, int H) {
+    const size_t r = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    const size_t rows = size_t(C) * n * H;
+    if (r < size_t(n)) kid_t[r] = fdepth[r / A];
+    if (r >= rows) return;
+    const int y = int(r % H);
+    const size_t ci = r / H;
+    const int i = int(ci % n), c = int(ci / n);
+    const int p = i / A;
+    static_cast<RowT *>(kids)[r] = static_cast<const RowT *>(front)[(size_t(c) * nf + p) * H + y];
+}
+
+template <typename RowT>
+__global__ void __launch_bounds__(256) post_kernel(SearchArgs a, const void *kids, const float *rew,
+                                                   const uint8_t *done) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= a.n) return;
+    const int p = i / a.A;
+    const int32_t reward = a.front_reward[p] + int32_t(rew[i]);
+    const int32_t depth = a.front_depth[p] + 1;
+    const uint64_t visit = a.visited + 1 + uint64_t(i);
+    atomicMax(reinterpret_cast<unsigned long long *>(a.best),
+              static_cast<unsigned long long>((uint64_t(uint32_t(reward) ^ 0x80000000u) << 32) |
+                                              (0xFFFFFFFFull - visit)));
+    a.kid_reward[i] = reward;
+    a.kid_depth[i] = depth;
+    a.slot[i] = -1;
+    if (done[i]) {
+        atomicAdd(&a.counts[0], 1u);
+        return;
+    }
+    const uint64_t h = map_hash<RowT>(kids, i, a.n, a.C, a.H);
+    const int64_t s = probe(a.keys, a.mask, h);
+    if (s < 0) {
+        atomicOr(&a.counts[1], 1u);
+        return;
+    }
+    const uint64_t v = pack_value(reward, depth);
+    const uint64_t old = atomicMax(reinterpret_cast<unsigned long long *>(&a.vals[s]),
+                                   static_cast<unsigned long long>(v));
+    if (old < v) a.epoch[s] = a.cur_epoch;
+    a.slot[i] = s;
+    a.kid_val[i] = v;
+}
+
+__global__ void __launch_bounds__(256) claim_kernel(SearchArgs a) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= a.n) return;
+    const int64_t s = a.slot[i];
+    if (s < 0) return;
+    if (a.vals[s] == a.kid_val[i] && a.epoch[s] == a.cur_epoch)
+        atomicMax(reinterpret_cast<unsigned long long *>(&a.claim[s]),
+                  static_cast<unsigned long long>((uint64_t(a.cur_epoch) << 32) |
+                                                  (0xFFFFFFFFu - uint32_t(i))));
+}
+
+__device__ inline bool survives(const SearchArgs &a, int i) {
+    const int64_t s = a.slot[i];
+    return s >= 0 && a.vals[s] == a.kid_val[i] && a.epoch[s] == a.cur_epoch &&
+           a.claim[s] == ((uint64_t(a.cur_epoch) << 32) | (0xFFFFFFFFu - uint32_t(i)));
+}
+
+// In-block exclusive prefix of 0/1 flags (256 threads, four waves); returns the block total.
+__device__ inline int block_prefix(int flag, int *sums, int &prefix) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const uint64_t ballot = __ballot(flag);
+    const int in_wave = __popcll(ballot & ((lane ? (~0ull >> (64 - lane)) : 0ull)));
+    if (lane == 0) sums[wave] = __popcll(ballot);
+    __syncthreads();
+    int before = 0, total = 0;
+    for (int w = 0; w < 4; ++w) {
+        if (w < wave) before += sums[w];
+        total += sums[w];
+    }
+    prefix = before + in_wave;
+    return total;
+}
+
+__global__ void __launch_bounds__(256) flag_kernel(SearchArgs a) {
+    __shared__ int sums[4];
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    const int flag = i < a.n && survives(a, i);
+    int prefix;
+    const int total = block_prefix(flag, sums, prefix);
+    if (threadIdx.x == 0) a.block_count[blockIdx.x] = total;
+}
+
+// Exclusive scan of the per-block counts; one workgroup of 256 threads; also the total.
+__global__ void __launch_bounds__(256) scan_kernel(int32_t *block_count, int nb, uint32_t *total) {
+    __shared__ int part[256];
+    const int t = threadIdx.x;
+    const int per = (nb + 255) / 256;
+    const int lo = t * per, hi = lo + per < nb ? lo + per : nb;
+    int sum = 0;
+    for (int k = lo; k < hi; ++k) sum += block_count[k];
+    part[t] = sum;
+    __syncthreads();
+    if (t == 0) {
+        int run = 0;
+        for (int k = 0; k < 256; ++k) {
+            const int v = part[k];
+            part[k] = run;
+            run += v;
+        }
+        *total = uint32_t(run);
+    }
+    __syncthreads();
+    int run = part[t];
+    for (int k = lo; k < hi; ++k) {
+        const int v = block_count[k];
+        block_count[k] = run;
+        run += v;
+    }
+}
+
+__global__ void __launch_bounds__(256) place_kernel(SearchArgs a, int cap) {
+    __shared__ int sums[4];
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    const int flag = i < a.n && survives(a, i);
+    int prefix;
+    block_prefix(flag, sums, prefix);
+    if (!flag) return;
+    const int pos = a.block_count[blockIdx.x] + prefix;
+    if (pos >= cap) return;
+    a.src_of[pos] = i;
+    a.next_reward[pos] = a.kid_reward[i];
+    a.next_depth[pos] = a.kid_depth[i];
+}
+
+template <typename RowT>
+__global__ void __launch_bounds__(256) copy_kernel(const void *kids, int n, void *next, int nn,
+                                                   const int32_t *src_of, int C, int H) {
+    const size_t r = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (r >= size_t(C) * nn * H) return;
+    const int y = int(r % H);
+    const size_t cq = r / H;
+    const int q = int(cq % nn), c = int(cq / nn);
+    static_cast<RowT *>(next)[r] = static_cast<const RowT *>(kids)[(size_t(c) * n + src_of[q]) * H + y];
+}
+
+template <typename RowT>
+__global__ void root_kernel(SearchArgs a, const void *front) {
+    if (blockIdx.x != 0 || threadIdx.x != 0) return;
+    const uint64_t h = map_hash<RowT>(front, 0, 1, a.C, a.H);
+    const int64_t s = probe(a.keys, a.mask, h);
+    if (s < 0) { a.counts[1] = 1; return; }
+    a.vals[s] = pack_value(0, 0);
+    *a.best = (uint64_t(0x80000000u) << 32) | 0xFFFFFFFFull;
+}
+
+unsigned blocks_for(size_t threads) { return unsigned((threads + 255) / 256); }
+
+template <typename RowT>
+hipError_t level_impl(const SearchArgs &a, const void *front, int nf, void *kids, int32_t *kid_t,
+                      hipStream_t s, int phase, int nn) {
+    const int block_bytes = a.H * int(sizeof(RowT));
+    const bool by16 = block_bytes % 16 == 0;
+    const int chunks = block_bytes / 16;
+    if (phase == 0) {
+        if (by16) {
+            const size_t threads = std::max(size_t(a.C) * a.n * chunks, size_t(a.n));
+            hipLaunchKernelGGL(copy16_kernel, dim3(blocks_for(threads)), dim3(256), 0, s,
+                               static_cast<const uint4 *>(front), nf, static_cast<uint4 *>(kids),
+                               a.n, a.C, chunks, a.A, static_cast<const int32_t *>(nullptr),
+                               kid_t, a.front_depth);
+        } else {
+            const size_t rows = std::max(size_t(a.C) * a.n * a.H, size_t(a.n));
+            hipLaunchKernelGGL(gather_kernel<RowT>, dim3(blocks_for(rows)), dim3(256), 0, s, front,
+                               nf, a.front_depth, kids, kid_t, a.n, a.A, a.C, a.H);
+        }
+    } else if (phase == 1) {
+        const unsigned nb = blocks_for(size_t(a.n));
+        hipLaunchKernelGGL(post_kernel<RowT>, dim3(nb), dim3(256), 0, s, a, kids, a.rew, a.done);
+        hipLaunchKernelGGL(claim_kernel, dim3(nb), dim3(256), 0, s, a);
+        hipLaunchKernelGGL(flag_kernel, dim3(nb), dim3(256), 0, s, a);
+        hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(256), 0, s, a.block_count, int(nb),
+                           &a.counts[2]);
+        hipLaunchKernelGGL(place_kernel, dim3(nb), dim3(256), 0, s, a, a.cap);
+    } else if (phase == 2) {
+        if (nn > 0 && by16)
+            hipLaunchKernelGGL(copy16_kernel, dim3(blocks_for(size_t(a.C) * nn * chunks)), dim3(256),
+                               0, s, static_cast<const uint4 *>(kids), a.n,
+                               static_cast<uint4 *>(a.next), nn, a.C, chunks, 1,
+                               static_cast<const int32_t *>(a.src_of),
+                               static_cast<int32_t *>(nullptr),
+                               static_cast<const int32_t *>(nullptr));
+        else if (nn > 0)
+            hipLaunchKernelGGL(copy_kernel<RowT>, dim3(blocks_for(size_t(a.C) * nn * a.H)), dim3(256),
+                               0, s, kids, a.n, a.next, nn, a.src_of, a.C, a.H);
+    } else {
+        hipLaunchKernelGGL(root_kernel<RowT>, dim3(1), dim3(64), 0, s, a, front);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_search_phase(const SearchArgs &a, int row_bytes, const void *front, int nf,
+                               void *kids, int32_t *kid_t, hipStream_t s, int phase, int nn) {
+    if (row_bytes == 2) return level_impl<uint16_t>(a, front, nf, kids, kid_t, s, phase, nn);
+    if (row_bytes == 4) return level_impl<uint32_t>(a, front, nf, kids, kid_t, s, phase, nn);
+    return level_impl<uint64_t>(a, front, nf, kids, kid_t, s, phase, nn);
+}
+
+}  // namespace av

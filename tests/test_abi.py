@@ -104,6 +104,12 @@ def test_null_arguments_are_rejected(lib):
                                None) == av.AV_EINVAL
     assert lib.av_mutate_rules(1, 1, 4, 17, 3, None, None, None, None, None, None, None, m, 0,
                                None) == av.AV_EINVAL
+    assert lib.av_search_create(None, None) == av.AV_EINVAL
+    assert lib.av_search_load_rules(None, 0, None, None, None, None) == av.AV_EINVAL
+    assert lib.av_search_begin(None, None) == av.AV_EINVAL
+    assert lib.av_search_expand(None, 1, None) == av.AV_EINVAL
+    assert lib.av_search_frontier(None, None, None, None) == av.AV_EINVAL
+    assert lib.av_search_destroy(None) == av.AV_OK
     bad = av.mutation(reward_lo=2, reward_hi=1)
     assert lib.av_mutate_rules(0, 0, 4, 3, 3, None, None, None, None, None, None, None, bad, 0,
                                None) == av.AV_EINVAL

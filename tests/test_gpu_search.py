@@ -1,0 +1,107 @@
+"""Batched search on the GPU (av_search_*) vs the oracle's level-synchronous search
+(oracle/search.py): every level's counts, best reward and visit, and the whole frontier
+(maps, rewards, depths, in order) compared exactly, for every workload's map shape and rule
+set, both action sets, episode ends, frontier and budget cuts, both rule orders and every
+step engine; plus a table that overflows (an error, not a fault)."""
+import numpy as np
+import pytest
+
+from gpu_util import require_gpu, say
+import paper_2407_04221_amd as av
+from paper_2407_04221_amd import inputs
+from oracle import search as osearch
+
+pytestmark = pytest.mark.gpu
+
+
+def one_set(rules):
+    shape, ip, op, rw = rules
+    return shape[:1], ip[:1], op[:1], rw[:1]
+
+
+def compare(wl, root, rules, budget, levels, A=5, cap=1 << 12, L=None, engine="auto",
+            rule_mode="parallel", table_log2=18):
+    L = wl.L if L is None else L
+    mode = int(rule_mode == "sequential")
+    o = osearch.Search(wl.H, wl.W, wl.C, rules, L, num_actions=A, max_frontier=cap,
+                       rule_mode=mode)
+    g = av.Search(wl.H, wl.W, wl.C, wl.R, wl.max_h, wl.max_w, L, num_actions=A,
+                  max_frontier=cap, table_log2=table_log2, engine=engine, rule_mode=rule_mode)
+    try:
+        g.load_rules(*rules)
+        o.begin(root)
+        g.begin(root)
+        for lv in range(levels):
+            left = budget - o.visited
+            want = o.expand(left)
+            got = g.expand(left)
+            assert got == want, f"level {lv + 1}: {got} != {want}"
+            gm, gr, gd = (x.cpu().numpy() for x in g.frontier())
+            om, orw, od = o.frontier_arrays()
+            np.testing.assert_array_equal(gm, om, err_msg=f"level {lv + 1} maps")
+            np.testing.assert_array_equal(gr, orw, err_msg=f"level {lv + 1} rewards")
+            np.testing.assert_array_equal(gd, od, err_msg=f"level {lv + 1} depths")
+            if want["frontier"] == 0 or want["visited"] >= budget:
+                break
+        return want
+    finally:
+        g.close()
+
+
+CASES = [("c1", 4000, 12), ("c2", 3000, 10), ("c3", 2000, 6), ("c4", 4000, 12), ("c5", 600, 4)]
+
+
+@pytest.mark.parametrize("variant", ["planted", "dense"])
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_search_matches_oracle(case, variant):
+    require_gpu()
+    name, budget, levels = case
+    wl = inputs.WORKLOADS[name].with_(B=1)
+    say(f"[search] {name} {variant}")
+    maps, rules, _ = inputs.make_all(wl, 7, variant)
+    last = compare(wl, maps[0], one_set(rules), budget, levels)
+    assert last["visited"] > 0
+
+
+@pytest.mark.parametrize("engine", ["generic", "wave", "lane16"])
+def test_search_engines_and_options(engine):
+    require_gpu()
+    wl = inputs.WORKLOADS["c4"].with_(B=1)
+    say(f"[search options] engine={engine}")
+    maps, rules, _ = inputs.make_all(wl, 3, "planted")
+    rules = one_set(rules)
+    compare(wl, maps[0], rules, 3000, 10, engine=engine)
+    compare(wl, maps[0], rules, 3000, 10, A=4, engine=engine)
+    compare(wl, maps[0], rules, 2500, 8, cap=37, engine=engine)          # frontier cut
+    compare(wl, maps[0], rules, 777, 8, engine=engine)                    # budget cut mid-level
+    compare(wl, maps[0], rules, 3000, 8, L=3, engine=engine)              # level-3 terminal
+    compare(wl, maps[0], rules, 3000, 8, engine=engine, rule_mode="sequential")
+
+
+def test_search_odd_shapes():
+    require_gpu()
+    for H, W, C in ((5, 7, 5), (33, 9, 4), (2, 64, 6)):
+        wl = inputs.Workload("odd", 90 + H, B=1, H=H, W=W, C=C, R=4,
+                             shapes=((1, 2), (2, 1), (2, 2)), p_dc=0.5, per_env=False, T=1, L=9)
+        say(f"[search odd] {H}x{W} C={C}")
+        maps, rules, _ = inputs.make_all(wl, 1, "dense")
+        compare(wl, maps[0], rules, 1500, 8)
+
+
+def test_search_table_overflow_is_an_error():
+    require_gpu()
+    wl = inputs.WORKLOADS["c1"].with_(B=1)
+    maps, rules, _ = inputs.make_all(wl, 0, "planted")
+    g = av.Search(wl.H, wl.W, wl.C, wl.R, wl.max_h, wl.max_w, 100, max_frontier=4096,
+                  table_log2=4)
+    try:
+        g.load_rules(*rules)
+        g.begin(maps[0])
+        with pytest.raises(av.AvError) as e:
+            for _ in range(20):
+                g.expand(10**6)
+        assert e.value.status == av.AV_ENOMEM
+        g.begin(maps[0])                          # a fresh start works again
+        assert g.expand(5)["children"] == 5
+    finally:
+        g.close()
