@@ -14,6 +14,10 @@ if HERE not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU")
     config.addinivalue_line("markers", "slow: long-running CPU test")
+    # the tests' torch CPU work is small convolutions: one thread each keeps parallel test
+    # workers from oversubscribing the cores
+    import torch
+    torch.set_num_threads(1)
 
 
 @pytest.fixture(scope="session")

@@ -63,25 +63,28 @@ def test_corridor_worked_case(oracle_lib):
 
 
 def brute_force(root, rules_list, D, actions):
-    """Every action sequence of length <= D, stepped with the conv form; episodes end when
-    no player is left.  Returns (first depth of every non-terminal state, best reward)."""
+    """Every action sequence of length <= D, stepped with the conv form (all sequences of one
+    length as one batch); a sequence stops when its episode ends (no player left).  Returns
+    (first depth of every non-terminal state, best reward over all sequences and prefixes)."""
     first = {root.tobytes(): 0}
     best = 0
+    maps = root[None].copy()                  # live sequences of the current length
+    totals = np.zeros(1, np.int64)
     for length in range(1, D + 1):
-        for seq in itertools.product(actions, repeat=length):
-            cur = root[None].copy()
-            total = 0
-            ok = True
-            for k, a in enumerate(seq):
-                cur, rho = e3_conv.step(cur, rules_list, np.array([a]))
-                total += int(rho[0])
-                best = max(best, total)
-                if cur[0, P].sum() == 0:                  # terminal: nothing follows
-                    ok = k == length - 1 and False
-                    break
-            if ok:
-                key = cur[0].tobytes()
-                first[key] = min(first.get(key, length), length)
+        if len(maps) == 0:
+            break
+        A = len(actions)
+        maps = np.repeat(maps, A, axis=0)
+        totals = np.repeat(totals, A)
+        acts = np.tile(np.array(list(actions)), len(maps) // A)
+        maps, rho = e3_conv.step(maps, rules_list, acts)
+        totals = totals + rho.astype(np.int64)
+        if len(totals):
+            best = max(best, int(totals.max()))
+        alive = maps[:, P].reshape(len(maps), -1).sum(1) > 0
+        maps, totals = maps[alive], totals[alive]
+        for m in maps:
+            first.setdefault(m.tobytes(), length)
     return first, best
 
 
