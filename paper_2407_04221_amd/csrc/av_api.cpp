@@ -71,6 +71,10 @@ struct av_batch_s {
     DeviceProgram dprog;
     Lane16Program lprog;           // compiled form for the lane16 engine (when chosen)
     Lane16Device dlprog;
+    std::vector<std::vector<Lane16Rule>> lsets;   // the rule list the lane16 programs come from
+    Lane16Program lprog_ctl;       // lane16 program with rule application control compiled in
+    Lane16Device dlprog_ctl;
+    bool lane16_ctl = false;       // steps use dlprog_ctl
 };
 
 namespace {
@@ -94,6 +98,8 @@ void free_control(av_batch_t b) {
     dev_free(const_cast<uint32_t *>(b->ctl.inhibit));
     b->ctl = CtlArgs{};
     b->engine = b->plain_engine;
+    b->lane16_ctl = false;
+    lane16_free(b->dlprog_ctl);
 }
 
 // Output-kernel entry K_O = O - I; unspecified output: no vote; unspecified input: the
@@ -429,6 +435,7 @@ av_status av_load_rules(av_batch_t b, int32_t R, const int32_t *shape, const int
         hipError_t e = lane16_upload(b->lprog, b->dlprog, &log);
         if (e != hipSuccess)
             return fail(AV_EDEVICE, "lane16 kernel build: %s %s", hipGetErrorString(e), log.c_str());
+        b->lsets.swap(lsets);
     }
     b->R = R;
     b->features.swap(feats);
@@ -476,10 +483,14 @@ av_status av_set_rule_control(av_batch_t b, const int32_t *limit, const uint8_t 
                                         "(only earlier rules inhibit later ones)", s, q, r);
                         active = true;
                     }
-    if (active && c.engine != AV_ENGINE_AUTO && c.engine != AV_ENGINE_GENERIC)
-        return fail(AV_EINVAL, "rule application control runs on the generic engine; create "
-                    "the batch with AV_ENGINE_AUTO or AV_ENGINE_GENERIC");
     const bool random = order == AV_SITES_RANDOM;
+    // row-major control compiles into the lane16 program; anything else runs on the generic
+    // engine
+    const bool on_lane16 = b->plain_engine == AV_ENGINE_LANE16 && !random;
+    if (active && !on_lane16 && c.engine != AV_ENGINE_AUTO && c.engine != AV_ENGINE_GENERIC)
+        return fail(AV_EINVAL, "rule application control with this engine and site order runs on "
+                    "the generic engine; create the batch with AV_ENGINE_AUTO or "
+                    "AV_ENGINE_GENERIC (lane16 takes row-major order only)");
     const size_t env_lds = generic_env_lds_bytes(c.height, c.width, c.channels, Rt, true, random);
     if (active && env_lds > size_t(kLdsBudget))
         return fail(AV_EINVAL, "rule application control needs %zu bytes of LDS per environment "
@@ -511,7 +522,29 @@ av_status av_set_rule_control(av_batch_t b, const int32_t *limit, const uint8_t 
     b->ctl.active = 1;
     b->ctl.random = random;
     b->ctl.seed = seed;
-    b->engine = AV_ENGINE_GENERIC;
+    if (on_lane16) {
+        Lane16Control lc;
+        lc.limit.assign(Rt, 0);
+        lc.inhibitors.assign(Rt, {});
+        for (int r = 0; r < R; ++r) {
+            if (limit) lc.limit[kMoveRules + r] = limit[r];
+            if (inhibit)
+                for (int q = 0; q < r; ++q)
+                    if (inhibit[size_t(q) * R + r]) lc.inhibitors[kMoveRules + r].push_back(kMoveRules + q);
+        }
+        lane16_compile(b->lsets, c.channels, c.height, c.width, c.max_episode_steps,
+                       c.rule_mode == AV_RULES_SEQUENTIAL, b->lprog_ctl, &lc);
+        std::string log;
+        hipError_t e = lane16_upload(b->lprog_ctl, b->dlprog_ctl, &log);
+        if (e != hipSuccess) {
+            free_control(b);
+            return fail(AV_EDEVICE, "lane16 kernel build: %s %s", hipGetErrorString(e), log.c_str());
+        }
+        b->lane16_ctl = true;
+        b->engine = AV_ENGINE_LANE16;
+    } else {
+        b->engine = AV_ENGINE_GENERIC;
+    }
     return AV_OK;
 }
 
@@ -535,7 +568,7 @@ static av_status step_k(av_batch_t b, int32_t k, const uint8_t *actions, float *
     a.ctl = b->ctl;
     a.ctl.step_base = b->step_no;
     if (b->engine == AV_ENGINE_LANE16) {
-        AV_HIP(launch_lane16_step(a, b->dlprog, b->stream));
+        AV_HIP(launch_lane16_step(a, b->lane16_ctl ? b->dlprog_ctl : b->dlprog, b->stream));
     } else if (b->engine == AV_ENGINE_WAVE) {
         AV_HIP(launch_wave_step(a, b->stream));
     } else {

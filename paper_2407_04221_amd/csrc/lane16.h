@@ -20,6 +20,14 @@ struct Lane16Rule {
     std::vector<int8_t> in, out;   // [C+1][n][m]
 };
 
+// Rule application control compiled into the lane16 body (row-major site order only):
+// per rule of the list (moves included, never controlled), a cap on applied matches (0 = all)
+// and the earlier rules that inhibit it.
+struct Lane16Control {
+    std::vector<int> limit;
+    std::vector<std::vector<int>> inhibitors;
+};
+
 struct Lane16Program {
     std::string source;            // the complete kernel source for this rule set
 };
@@ -36,7 +44,8 @@ bool lane16_eligible(const av_config &c);
 // rule order (parallel or sequential) and a rule list (the four moves first, then the
 // loaded rules).
 void lane16_compile(const std::vector<std::vector<Lane16Rule>> &sets, int C, int H, int W,
-                    int L, bool sequential, Lane16Program &p);
+                    int L, bool sequential, Lane16Program &p,
+                    const Lane16Control *ctl = nullptr);
 
 // Compile (hipRTC, gfx950) and load the program on the current device, reusing an
 // identical earlier build.  On failure returns an error and the compiler log in *log.
@@ -47,6 +56,7 @@ inline void lane16_free(Lane16Device &d) { d.fn = nullptr; }
 hipError_t launch_lane16_step(const StepArgs &a, const Lane16Device &d, hipStream_t s);
 
 // The generated straight-line rule code alone (exposed for tests of the generator).
-std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule> &rules);
+std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule> &rules,
+                              const Lane16Control *ctl = nullptr);
 
 }  // namespace av

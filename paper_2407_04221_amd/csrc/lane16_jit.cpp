@@ -107,6 +107,57 @@ class Gen {
     }
 };
 
+// Rule application control for rule r on its match word `M` (paper Sec. 2.1.1), after its
+// matches are complete and before its reward and votes.  `applied(q)` names the final match
+// word of an earlier rule q.
+//   inhibition: anchors of r whose n x m patch overlaps the patch of an applied match of q:
+//     rows y - nq + 1 .. y + n - 1 of q OR-ed (DPP row shifts), then dilated over columns
+//     x - mq + 1 .. x + m - 1 inside each 16-bit half, and cleared from M;
+//   cap K: per half, an inclusive prefix sum of the lanes' popcounts across the 16-lane row
+//     (Hillis-Steele with DPP row shifts; two 16-bit counters in one word); a lane whose
+//     prefix exceeds K keeps only the lowest K - (exclusive prefix) bits of its half, so the
+//     first K matches in row-major order survive.
+template <typename Applied>
+void emit_control(std::ostringstream &o, int r, const std::string &M,
+                  const std::vector<Lane16Rule> &rules, const Lane16Control &ctl,
+                  Applied applied) {
+    const Lane16Rule &ru = rules[r];
+    for (int q : ctl.inhibitors[r]) {
+        const Lane16Rule &rq = rules[q];
+        o << "{ // rule " << q << " inhibits rule " << r << "\n";
+        o << "u32 O = " << applied(q) << ";\n";
+        for (int d = 1; d < ru.n; ++d) o << "O |= DPP_SHL(" << applied(q) << ", " << d << ");\n";
+        for (int d = 1; d < rq.n; ++d) o << "O |= DPP_SHR(" << applied(q) << ", " << d << ");\n";
+        o << "u32 D = O;\n";
+        for (int k = 1; k < ru.m; ++k) o << "D |= (O >> " << k << ") & BOTH(0xFFFFu >> " << k << ");\n";
+        for (int k = 1; k < rq.m; ++k)
+            o << "D |= (O << " << k << ") & BOTH((0xFFFFu << " << k << ") & 0xFFFFu);\n";
+        o << M << " &= ~D;\n}\n";
+    }
+    const int K = ctl.limit[r];
+    if (K > 0) {
+        o << "{ // rule " << r << ": at most " << K << " matches, first in row-major order\n";
+        o << "const u32 cnt = (u32)__popc(" << M << " & 0xFFFFu) | ((u32)__popc(" << M << " >> 16) << 16);\n";
+        o << "u32 inc = cnt;\ninc += DPP_SHR(inc, 1);\ninc += DPP_SHR(inc, 2);\n"
+             "inc += DPP_SHR(inc, 4);\ninc += DPP_SHR(inc, 8);\n";
+        o << "const int incA = int(inc & 0xFFFFu), incB = int(inc >> 16);\n";
+        o << "if (ANY(u32((incA > " << K << ") | (incB > " << K << ")))) {\n";
+        o << "int kA = " << K << " - (incA - int(cnt & 0xFFFFu)), kB = " << K
+          << " - (incB - int(cnt >> 16));\n";
+        o << "u32 xa = " << M << " & 0xFFFFu, xb = " << M << " >> 16, keep = 0u;\n";
+        o << "for (int t = 0; t < 16; ++t) {\n"
+             "const u32 ba = xa & (0u - xa), bb = xb & (0u - xb);\n"
+             "if (kA > 0 && ba) { keep |= ba; --kA; }\n"
+             "if (kB > 0 && bb) { keep |= bb << 16; --kB; }\n"
+             "xa ^= ba; xb ^= bb;\n}\n";
+        o << M << " = keep;\n}\n}\n";
+    }
+}
+
+bool controlled(const Lane16Control *ctl, int r) {
+    return ctl && (ctl->limit[r] > 0 || !ctl->inhibitors[r].empty());
+}
+
 }  // namespace
 
 bool lane16_eligible(const av_config &c) {
@@ -114,7 +165,8 @@ bool lane16_eligible(const av_config &c) {
            c.max_pat_w <= 16;
 }
 
-std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule> &rules) {
+std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule> &rules,
+                              const Lane16Control *ctl) {
     Gen g;
     std::ostringstream &o = g.o;
     const int C1 = C + 1, R = int(rules.size());
@@ -231,6 +283,22 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
         for (int r = n_fixed; r < R; ++r) {
             const std::string M = "M" + std::to_string(r);
             const size_t probe = std::min<size_t>(2, ents[r].size());
+            if (controlled(ctl, r)) {
+                // complete the matches, filter them, then pay and vote with what is left
+                if (ents[r].size() > probe) {
+                    o << "if (ANY(" << M << ")) {\n";
+                    emit_rows(M, std::vector<Entry>(ents[r].begin() + probe, ents[r].end()));
+                    o << "}\n";
+                }
+                o << "if (ANY(" << M << ")) {\n";
+                emit_control(o, r, M, rules, *ctl,
+                             [](int q) { return "M" + std::to_string(q); });
+                o << "if (ANY(" << M << ")) {\n";
+                emit_reward(r);
+                emit_votes(r);
+                o << "}\n}\n";
+                continue;
+            }
             o << "if (ANY(" << M << ")) {\n";
             if (ents[r].size() > probe) {
                 emit_rows(M, std::vector<Entry>(ents[r].begin() + probe, ents[r].end()));
@@ -301,7 +369,8 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
 // planes from the map as the rules before it left it (force plane included), matches the
 // rule, and applies its votes (exactly counted where its own matches overlap with both
 // signs) before the next block.
-std::string lane16_rules_body_sequential(int C, int H, int W, const std::vector<Lane16Rule> &rules) {
+std::string lane16_rules_body_sequential(int C, int H, int W, const std::vector<Lane16Rule> &rules,
+                                         const Lane16Control *ctl = nullptr) {
     Gen g;
     std::ostringstream &o = g.o;
     const int C1 = C + 1, R = int(rules.size());
@@ -317,6 +386,14 @@ std::string lane16_rules_body_sequential(int C, int H, int W, const std::vector<
     for (auto &s : shapes)
         o << "const u32 V" << s.first << "_" << s.second << " = (y <= " << (H - s.first)
           << ") ? BOTH(COLMASK(" << std::max(0, W - s.second + 1) << ")) : 0u;\n";
+
+    // final match words of the rules that inhibit later ones
+    std::vector<bool> inhibits(R, false);
+    if (ctl)
+        for (int r = 0; r < R; ++r)
+            for (int q : ctl->inhibitors[r]) inhibits[q] = true;
+    for (int r = 0; r < R; ++r)
+        if (inhibits[r]) o << "u32 A" << r << " = 0u;\n";
 
     for (int r = 0; r < R; ++r) {
         const Lane16Rule &ru = rules[r];
@@ -358,7 +435,7 @@ std::string lane16_rules_body_sequential(int C, int H, int W, const std::vector<
         };
         bool writes = false;
         for (int c = 0; c < C1; ++c) writes |= !plus[c].empty() || !minus[c].empty();
-        if (!writes && ru.reward == 0) continue;   // a rule that neither writes nor pays
+        if (!writes && ru.reward == 0 && !inhibits[r]) continue;   // no effect at all
 
         o << "{ // rule " << r << "\n";
         for (auto &x : xs)
@@ -384,6 +461,9 @@ std::string lane16_rules_body_sequential(int C, int H, int W, const std::vector<
                 ++open;
             }
         }
+        if (controlled(ctl, r))
+            emit_control(o, r, "M", rules, *ctl, [](int q) { return "A" + std::to_string(q); });
+        if (inhibits[r]) o << "A" << r << " = M;\n";
         if (ru.reward != 0)
             o << "rA += " << ru.reward << " * (int)__popc(M & 0xFFFFu); rB += " << ru.reward
               << " * (int)__popc(M >> 16);\n";
@@ -446,7 +526,7 @@ std::string lane16_rules_body_sequential(int C, int H, int W, const std::vector<
 }
 
 void lane16_compile(const std::vector<std::vector<Lane16Rule>> &sets, int C, int H, int W, int L,
-                    bool sequential, Lane16Program &p) {
+                    bool sequential, Lane16Program &p, const Lane16Control *ctl) {
     std::string src = kLane16Template;
     std::ostringstream d;
     d << "#define AV_C " << C << "\n#define AV_H " << H << "\n#define AV_W " << W << "\n#define AV_L "
@@ -459,8 +539,8 @@ void lane16_compile(const std::vector<std::vector<Lane16Rule>> &sets, int C, int
         if (at != std::string::npos) src.replace(at, marker.size(), text);
     };
     put("/*@DEFINES@*/", d.str());
-    put("/*@RULES@*/", sequential ? lane16_rules_body_sequential(C, H, W, sets.at(0))
-                                  : lane16_rules_body(C, H, W, sets.at(0)));
+    put("/*@RULES@*/", sequential ? lane16_rules_body_sequential(C, H, W, sets.at(0), ctl)
+                                  : lane16_rules_body(C, H, W, sets.at(0), ctl));
     p.source = std::move(src);
 }
 

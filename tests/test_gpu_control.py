@@ -38,7 +38,8 @@ def test_control_step_matches_oracle(case, mode, order, variant):
                                         rule_mode=int(mode == "sequential"), control=ctl)
     seq, final, r, d, eng = gpu_run(wl, maps, rules, actions, engine="auto", mode="step",
                                     rule_mode=mode, control=ctl)
-    assert av.ENGINE_NAMES[eng] == "generic"
+    lane16_ok = wl.H <= 16 and wl.W <= 16 and not wl.per_env
+    assert av.ENGINE_NAMES[eng] == ("lane16" if lane16_ok and order == 0 else "generic")
     for t in range(T):
         assert first_mismatch(seq[t], want_m[t]) is None, \
             f"maps differ at step {t}, index {first_mismatch(seq[t], want_m[t])}"
@@ -61,6 +62,46 @@ def test_control_step_n_matches_oracle(case, order):
     np.testing.assert_array_equal(r, want_r)
     np.testing.assert_array_equal(d, want_d)
     np.testing.assert_array_equal(final, want_m[-1])
+
+
+LANE16_CASES = [("c1", 1, 40), ("c4", 77, 30),
+                ("sq16", 45, 20), ("odd", 29, 25)]
+LANE16_EXTRA = {
+    "sq16": inputs.Workload("sq16", 63, B=45, H=16, W=16, C=7, R=9,
+                            shapes=((3, 3), (1, 2), (4, 1)), p_dc=0.5, per_env=False, T=20, L=7),
+    "odd": inputs.Workload("odd", 61, B=29, H=5, W=11, C=5, R=6,
+                           shapes=((1, 1), (2, 3), (3, 2)), p_dc=0.5, per_env=False, T=25, L=6),
+}
+
+
+@pytest.mark.parametrize("variant", ["planted", "dense"])
+@pytest.mark.parametrize("mode", ["parallel", "sequential"])
+@pytest.mark.parametrize("case", LANE16_CASES, ids=[c[0] for c in LANE16_CASES])
+def test_lane16_control_matches_oracle(case, mode, variant):
+    """Row-major caps and inhibition compiled into the lane16 program, stepped one launch per
+    step and in multi-step launches."""
+    require_gpu()
+    name, B, T = case
+    wl = LANE16_EXTRA[name] if name in LANE16_EXTRA else inputs.WORKLOADS[name].with_(B=B, T=T,
+                                                                                      L=9)
+    say(f"[lane16 control] {name} mode={mode} variant={variant}")
+    maps, rules, actions = inputs.make_all(wl, 6, variant)
+    for kmax, seed in ((1, 0), (4, 1)):
+        ctl = control_for(wl, wl.B, seed, 0, kmax=kmax)
+        want_m, want_r, want_d = oracle.run(wl, maps, rules, actions, nthreads=8,
+                                            rule_mode=int(mode == "sequential"), control=ctl)
+        seq, final, r, d, eng = gpu_run(wl, maps, rules, actions, engine="lane16", mode="step",
+                                        rule_mode=mode, control=ctl)
+        assert av.ENGINE_NAMES[eng] == "lane16"
+        for t in range(wl.T):
+            assert first_mismatch(seq[t], want_m[t]) is None, f"kmax {kmax}: maps differ, step {t}"
+            np.testing.assert_array_equal(r[t], want_r[t], err_msg=f"kmax {kmax}: rewards {t}")
+            np.testing.assert_array_equal(d[t], want_d[t], err_msg=f"kmax {kmax}: done {t}")
+        _, final, r, d, _ = gpu_run(wl, maps, rules, actions, engine="lane16", mode="step_n",
+                                    chunk=6, rule_mode=mode, control=ctl)
+        np.testing.assert_array_equal(r, want_r)
+        np.testing.assert_array_equal(d, want_d)
+        np.testing.assert_array_equal(final, want_m[-1])
 
 
 def test_control_full_size_c4_prefix():
@@ -142,7 +183,9 @@ def test_control_engine_switch_and_errors():
         b.set_rule_control(lim, None, "random", 1)          # nothing active: engine kept
         assert b.info["engine"] == av.AV_ENGINE_LANE16
         lim[0, 2] = 1
-        b.set_rule_control(lim, None, "rowmajor", 0)
+        b.set_rule_control(lim, None, "rowmajor", 0)           # compiled into lane16
+        assert b.info["engine"] == av.AV_ENGINE_LANE16
+        b.set_rule_control(lim, None, "random", 0)             # random order: generic
         assert b.info["engine"] == av.AV_ENGINE_GENERIC
         b.set_rule_control(None, None)
         assert b.info["engine"] == av.AV_ENGINE_LANE16
@@ -166,8 +209,17 @@ def test_control_engine_switch_and_errors():
     try:
         b.load_rules(*rules)
         lim = np.ones((1, R), np.int32)
+        b.set_rule_control(lim, None)                          # row-major: fine on lane16
         with pytest.raises(av.AvError) as e:
-            b.set_rule_control(lim, None)
+            b.set_rule_control(lim, None, "random", 0)
+        assert e.value.status == av.AV_EINVAL
+    finally:
+        b.close()
+    b = av.Batch.for_workload(wl, engine="wave")
+    try:
+        b.load_rules(*rules)
+        with pytest.raises(av.AvError) as e:
+            b.set_rule_control(np.ones((1, R), np.int32), None)
         assert e.value.status == av.AV_EINVAL
     finally:
         b.close()

@@ -18,8 +18,10 @@ def _cases():
     for path in FIXTURES:
         fx = fixtures.parse(path)
         name = path.rsplit("/", 1)[-1][:-3]
-        if fx.has_control:      # rule application control runs on the generic engine
+        if fx.has_control:      # rule application control: generic, and lane16 (row-major)
             engines = ["generic", "auto"]
+            if fx.H <= 16 and fx.W <= 16 and fx.order == 0:
+                engines.append("lane16")
         else:
             engines = ["generic", "wave"]
             if fx.H <= 16 and fx.W <= 16:
