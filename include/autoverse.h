@@ -145,10 +145,10 @@ typedef enum {
  *            (pos / 8, n, env, 0) and key (seed, 0), above that rank, where n is the batch
  *            step number (steps since av_reset, all environments counted together)
  *   seed     key of the random index channel
- * Engines: on a lane16 batch, row-major control is compiled into the lane16 program (a
- * new program per call); random order, and any control on a wave batch, runs on the generic
- * engine, to which a batch created with AV_ENGINE_AUTO switches while some limit or
- * inhibition is set (an explicit lane16 or wave engine then gives AV_EINVAL).
+ * Engines: on a lane16 batch the control is compiled into the lane16 program (a new
+ * program per call); on a wave batch it runs on the generic engine, to which a batch
+ * created with AV_ENGINE_AUTO switches while some limit or inhibition is set (an explicit
+ * wave engine then gives AV_EINVAL).
  * AV_ESTATE before av_load_rules (which clears the control); AV_EINVAL for a negative
  * limit, an inhibition with q >= r or an unknown order.  Synchronises the stream. */
 av_status av_set_rule_control(av_batch_t b, const int32_t *limit, const uint8_t *inhibit,

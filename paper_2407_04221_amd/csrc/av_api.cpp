@@ -484,13 +484,11 @@ av_status av_set_rule_control(av_batch_t b, const int32_t *limit, const uint8_t 
                         active = true;
                     }
     const bool random = order == AV_SITES_RANDOM;
-    // row-major control compiles into the lane16 program; anything else runs on the generic
-    // engine
-    const bool on_lane16 = b->plain_engine == AV_ENGINE_LANE16 && !random;
+    // control compiles into the lane16 program; on other batches it runs on the generic engine
+    const bool on_lane16 = b->plain_engine == AV_ENGINE_LANE16;
     if (active && !on_lane16 && c.engine != AV_ENGINE_AUTO && c.engine != AV_ENGINE_GENERIC)
-        return fail(AV_EINVAL, "rule application control with this engine and site order runs on "
-                    "the generic engine; create the batch with AV_ENGINE_AUTO or "
-                    "AV_ENGINE_GENERIC (lane16 takes row-major order only)");
+        return fail(AV_EINVAL, "rule application control on a wave batch runs on the generic "
+                    "engine; create the batch with AV_ENGINE_AUTO or AV_ENGINE_GENERIC");
     const size_t env_lds = generic_env_lds_bytes(c.height, c.width, c.channels, Rt, true, random);
     if (active && env_lds > size_t(kLdsBudget))
         return fail(AV_EINVAL, "rule application control needs %zu bytes of LDS per environment "
@@ -524,6 +522,7 @@ av_status av_set_rule_control(av_batch_t b, const int32_t *limit, const uint8_t 
     b->ctl.seed = seed;
     if (on_lane16) {
         Lane16Control lc;
+        lc.random = random;
         lc.limit.assign(Rt, 0);
         lc.inhibitors.assign(Rt, {});
         for (int r = 0; r < R; ++r) {

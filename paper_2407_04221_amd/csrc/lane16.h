@@ -20,12 +20,13 @@ struct Lane16Rule {
     std::vector<int8_t> in, out;   // [C+1][n][m]
 };
 
-// Rule application control compiled into the lane16 body (row-major site order only):
+// Rule application control compiled into the lane16 body:
 // per rule of the list (moves included, never controlled), a cap on applied matches (0 = all)
 // and the earlier rules that inhibit it.
 struct Lane16Control {
     std::vector<int> limit;
     std::vector<std::vector<int>> inhibitors;
+    bool random = false;           // keep the matches with the largest random index
 };
 
 struct Lane16Program {

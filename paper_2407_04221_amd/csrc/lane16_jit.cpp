@@ -135,7 +135,34 @@ void emit_control(std::ostringstream &o, int r, const std::string &M,
         o << M << " &= ~D;\n}\n";
     }
     const int K = ctl.limit[r];
-    if (K > 0) {
+    if (K > 0 && ctl.random) {
+        // random site order: K rounds of a row-wide maximum over the random keys of the
+        // remaining matches of each environment whose match count exceeds K
+        o << "{ // rule " << r << ": at most " << K << " matches, largest random index first\n";
+        o << "const u32 cnt = (u32)__popc(" << M << " & 0xFFFFu) | ((u32)__popc(" << M << " >> 16) << 16);\n";
+        o << "u32 tot = cnt;\ntot += (u32)DPP_ROR((int)tot, 1);\ntot += (u32)DPP_ROR((int)tot, 2);\n"
+             "tot += (u32)DPP_ROR((int)tot, 4);\ntot += (u32)DPP_ROR((int)tot, 8);\n";
+        o << "const bool exA = (tot & 0xFFFFu) > " << K << "u, exB = (tot >> 16) > " << K << "u;\n";
+        o << "if (ANY(u32(exA || exB))) {\n";
+        o << "if (!keys_ready) { site_keys(kb, y, eA, eB, hasA, hasB, nstep, seed); keys_ready = true; }\n";
+        o << "u32 remA = exA ? (" << M << " & 0xFFFFu) : 0u, remB = exB ? (" << M << " >> 16) : 0u;\n";
+        o << "u32 keep = (exA ? 0u : (" << M << " & 0xFFFFu)) | (exB ? 0u : (" << M << " & 0xFFFF0000u));\n";
+        o << "for (int t = 0; t < " << K << "; ++t) {\n"
+             "u32 bA = 0u, bB = 0u;\n"
+             "for (u32 x = remA; x; x &= x - 1u) bA = max(bA, kb[__ffs(x) - 1]);\n"
+             "for (u32 x = remB; x; x &= x - 1u) bB = max(bB, kb[16 + __ffs(x) - 1]);\n"
+             "u32 mA = bA, mB = bB;\n";
+        for (int d : {1, 2, 4, 8})
+            o << "mA = max(mA, (u32)DPP_ROR((int)mA, " << d << ")); mB = max(mB, (u32)DPP_ROR((int)mB, "
+              << d << "));\n";
+        o << "if (bA != 0u && bA == mA)\n"
+             "for (u32 x = remA; x; x &= x - 1u) { const u32 b = x & (0u - x); "
+             "if (kb[__ffs(x) - 1] == mA) { remA ^= b; keep |= b; break; } }\n";
+        o << "if (bB != 0u && bB == mB)\n"
+             "for (u32 x = remB; x; x &= x - 1u) { const u32 b = x & (0u - x); "
+             "if (kb[16 + __ffs(x) - 1] == mB) { remB ^= b; keep |= b << 16; break; } }\n";
+        o << "}\n" << M << " = keep;\n}\n}\n";
+    } else if (K > 0) {
         o << "{ // rule " << r << ": at most " << K << " matches, first in row-major order\n";
         o << "const u32 cnt = (u32)__popc(" << M << " & 0xFFFFu) | ((u32)__popc(" << M << " >> 16) << 16);\n";
         o << "u32 inc = cnt;\ninc += DPP_SHR(inc, 1);\ninc += DPP_SHR(inc, 2);\n"
@@ -538,7 +565,11 @@ void lane16_compile(const std::vector<std::vector<Lane16Rule>> &sets, int C, int
         const size_t at = src.find(marker);
         if (at != std::string::npos) src.replace(at, marker.size(), text);
     };
+    bool random = false;
+    if (ctl && ctl->random)
+        for (size_t r = 0; r < ctl->limit.size(); ++r) random |= ctl->limit[r] > 0;
     put("/*@DEFINES@*/", d.str());
+    put("/*@PHILOX@*/", random ? std::string("#define AV_RANDOM_SITES 1\n") + kPhiloxSource : std::string());
     put("/*@RULES@*/", sequential ? lane16_rules_body_sequential(C, H, W, sets.at(0), ctl)
                                   : lane16_rules_body(C, H, W, sets.at(0), ctl));
     p.source = std::move(src);
@@ -603,7 +634,8 @@ hipError_t launch_lane16_step(const StepArgs &a, const Lane16Device &d, hipStrea
     float *rewards = a.rewards;
     uint8_t *done = a.done;
     int B = a.B, K = a.k;
-    void *args[] = {&state, &init, &t, &actions, &rewards, &done, &B, &K};
+    unsigned long long seed = a.ctl.seed, step_base = a.ctl.step_base;
+    void *args[] = {&state, &init, &t, &actions, &rewards, &done, &B, &K, &seed, &step_base};
     return hipModuleLaunchKernel(d.fn, blocks, 1, 1, 256, 1, 1, 0, s, args, nullptr);
 }
 

@@ -38,6 +38,30 @@
 
 typedef unsigned int u32;
 
+/*@PHILOX@*/
+#ifdef AV_RANDOM_SITES
+// The random index channel of rule application control for this lane's row of both
+// environments: kb[e * 16 + x] = high 20 bits of the Philox word of cell pos = y * W + x
+// (stream 0, generation = batch step number, individual = environment) above 4095 - pos.
+__device__ inline void site_keys(u32 *kb, int y, int eA, int eB, bool hasA, bool hasB,
+                                 unsigned long long n, unsigned long long seed) {
+    if (y >= AV_H) return;
+    const int p0 = y * AV_W, p1 = p0 + AV_W;
+    for (int e = 0; e < 2; ++e) {
+        if (!(e ? hasB : hasA)) continue;
+        const unsigned long long env = (unsigned long long)(e ? eB : eA);
+        for (int blk = p0 / 8; blk * 8 < p1; ++blk) {
+            unsigned int w[8];
+            av::philox_words(seed, n, env, 0, (unsigned long long)blk, w);
+            for (int j = 0; j < 8; ++j) {
+                const int pos = blk * 8 + j;
+                if (pos >= p0 && pos < p1) kb[e * 16 + pos - p0] = (w[j] & 0xFFFFF000u) | u32(4095 - pos);
+            }
+        }
+    }
+}
+#endif
+
 #define AV_PLAYER 2
 // lane y <- lane y + i (row shift left), lane y <- lane y - i (row shift right), rotate
 #define DPP_SHL(x, i) ((u32)__builtin_amdgcn_update_dpp(0, (int)(x), 0x100 + (i), 0xF, 0xF, true))
@@ -51,7 +75,8 @@ typedef unsigned int u32;
 extern "C" __global__ void __launch_bounds__(256)
 av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restrict__ init,
                int *__restrict__ tctr, const unsigned char *__restrict__ actions,
-               float *__restrict__ rewards, unsigned char *__restrict__ done, int B, int K) {
+               float *__restrict__ rewards, unsigned char *__restrict__ done, int B, int K,
+               unsigned long long seed, unsigned long long step_base) {
     const int lane = threadIdx.x & 63;
     const int wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
     const int y = lane & 15;
@@ -65,6 +90,13 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
     // safe (clamped) environment indices for loads; values of absent envs are masked off
     const int iA = hasA ? eA : 0, iB = hasB ? eB : 0;
 
+#ifdef AV_RANDOM_SITES
+    __shared__ u32 kbuf[256 * 32];                  // per lane: the site keys of its row
+    u32 *const kb = kbuf + threadIdx.x * 32;
+#else
+    (void)seed;
+    (void)step_base;
+#endif
     u32 p[AV_C], q[AV_C];   // current rows, initial rows (kept for automatic resets)
 #pragma unroll
     for (int c = 0; c < AV_C; ++c) {
@@ -113,6 +145,10 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
         }
 
         int rA = 0, rB = 0;
+#ifdef AV_RANDOM_SITES
+        const unsigned long long nstep = step_base + (unsigned long long)k;
+        bool keys_ready = false;
+#endif
         /*@RULES@*/
 
         // episode end: any player bit left in each half of this 16-lane row

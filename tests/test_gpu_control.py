@@ -39,7 +39,7 @@ def test_control_step_matches_oracle(case, mode, order, variant):
     seq, final, r, d, eng = gpu_run(wl, maps, rules, actions, engine="auto", mode="step",
                                     rule_mode=mode, control=ctl)
     lane16_ok = wl.H <= 16 and wl.W <= 16 and not wl.per_env
-    assert av.ENGINE_NAMES[eng] == ("lane16" if lane16_ok and order == 0 else "generic")
+    assert av.ENGINE_NAMES[eng] == ("lane16" if lane16_ok else "generic")
     for t in range(T):
         assert first_mismatch(seq[t], want_m[t]) is None, \
             f"maps differ at step {t}, index {first_mismatch(seq[t], want_m[t])}"
@@ -74,20 +74,22 @@ LANE16_EXTRA = {
 }
 
 
+@pytest.mark.parametrize("order", [0, 1])
 @pytest.mark.parametrize("variant", ["planted", "dense"])
 @pytest.mark.parametrize("mode", ["parallel", "sequential"])
 @pytest.mark.parametrize("case", LANE16_CASES, ids=[c[0] for c in LANE16_CASES])
-def test_lane16_control_matches_oracle(case, mode, variant):
-    """Row-major caps and inhibition compiled into the lane16 program, stepped one launch per
-    step and in multi-step launches."""
+def test_lane16_control_matches_oracle(case, mode, variant, order):
+    """Caps (row-major and random order) and inhibition compiled into the lane16 program,
+    stepped one launch per step and in multi-step launches (the random channel follows the
+    batch step number inside a launch)."""
     require_gpu()
     name, B, T = case
     wl = LANE16_EXTRA[name] if name in LANE16_EXTRA else inputs.WORKLOADS[name].with_(B=B, T=T,
                                                                                       L=9)
-    say(f"[lane16 control] {name} mode={mode} variant={variant}")
+    say(f"[lane16 control] {name} mode={mode} variant={variant} order={order}")
     maps, rules, actions = inputs.make_all(wl, 6, variant)
     for kmax, seed in ((1, 0), (4, 1)):
-        ctl = control_for(wl, wl.B, seed, 0, kmax=kmax)
+        ctl = control_for(wl, wl.B, seed, order, kmax=kmax)
         want_m, want_r, want_d = oracle.run(wl, maps, rules, actions, nthreads=8,
                                             rule_mode=int(mode == "sequential"), control=ctl)
         seq, final, r, d, eng = gpu_run(wl, maps, rules, actions, engine="lane16", mode="step",
@@ -133,11 +135,13 @@ def test_control_full_size_c4_prefix():
         b.close()
 
 
-def test_control_checkpoint_resume():
-    """The blob carries the batch step number: resuming from it repeats the random picks."""
+@pytest.mark.parametrize("name", ["c2", "c4"])
+def test_control_checkpoint_resume(name):
+    """The blob carries the batch step number: resuming from it repeats the random picks
+    (generic engine for c2's per-environment rules, lane16 for c4)."""
     require_gpu()
     import torch
-    wl = inputs.WORKLOADS["c2"].with_(B=40, T=12, L=50)
+    wl = inputs.WORKLOADS[name].with_(B=40, T=12, L=50)
     maps, rules, actions = inputs.make_all(wl, 1, "dense")
     ctl = control_for(wl, wl.B, 3, 1)
     acts = torch.from_numpy(actions).cuda()
@@ -185,10 +189,22 @@ def test_control_engine_switch_and_errors():
         lim[0, 2] = 1
         b.set_rule_control(lim, None, "rowmajor", 0)           # compiled into lane16
         assert b.info["engine"] == av.AV_ENGINE_LANE16
-        b.set_rule_control(lim, None, "random", 0)             # random order: generic
-        assert b.info["engine"] == av.AV_ENGINE_GENERIC
+        b.set_rule_control(lim, None, "random", 0)             # so is the random order
+        assert b.info["engine"] == av.AV_ENGINE_LANE16
         b.set_rule_control(None, None)
         assert b.info["engine"] == av.AV_ENGINE_LANE16
+    finally:
+        b.close()
+    b = av.Batch.for_workload(wl, engine="generic")
+    try:
+        b.load_rules(*rules)
+        b.set_rule_control(np.ones((1, R), np.int32), None, "random", 0)
+        assert b.info["engine"] == av.AV_ENGINE_GENERIC
+    finally:
+        b.close()
+    b = av.Batch.for_workload(wl)
+    try:
+        b.load_rules(*rules)
         b.set_rule_control(lim, None)
         b.load_rules(*rules)                                 # clears the control
         assert b.info["engine"] == av.AV_ENGINE_LANE16
@@ -209,10 +225,9 @@ def test_control_engine_switch_and_errors():
     try:
         b.load_rules(*rules)
         lim = np.ones((1, R), np.int32)
-        b.set_rule_control(lim, None)                          # row-major: fine on lane16
-        with pytest.raises(av.AvError) as e:
-            b.set_rule_control(lim, None, "random", 0)
-        assert e.value.status == av.AV_EINVAL
+        b.set_rule_control(lim, None)                          # both orders run on lane16
+        b.set_rule_control(lim, None, "random", 0)
+        assert b.info["engine"] == av.AV_ENGINE_LANE16
     finally:
         b.close()
     b = av.Batch.for_workload(wl, engine="wave")

@@ -18,9 +18,9 @@ def _cases():
     for path in FIXTURES:
         fx = fixtures.parse(path)
         name = path.rsplit("/", 1)[-1][:-3]
-        if fx.has_control:      # rule application control: generic, and lane16 (row-major)
+        if fx.has_control:      # rule application control: generic and lane16
             engines = ["generic", "auto"]
-            if fx.H <= 16 and fx.W <= 16 and fx.order == 0:
+            if fx.H <= 16 and fx.W <= 16:
                 engines.append("lane16")
         else:
             engines = ["generic", "wave"]
