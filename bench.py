@@ -303,7 +303,19 @@ def main():
         torch.cuda.synchronize()
         us = g0.elapsed_time(g1) * 1e3 / reps
         moved = wl.B * (wl.C * w * w + wl.C * wl.H * wl.W // 8)   # window out, packed maps in
+        # one step and its observation per call, as an agent needs them: fused (the lane16
+        # kernel writes the window from its registers) against a step then av_observe
+        a1 = acts[:1]
+        r1 = torch.empty((1, wl.B), dtype=torch.float32, device="cuda")
+        d1 = torch.empty((1, wl.B), dtype=torch.uint8, device="cuda")
+        us_fused = _time_us(lambda: av.av_step_observe(b.h, 1, a1, r1, d1, w, obs), stream, torch)
+
+        def separate():
+            av.av_step_n(b.h, 1, a1, r1, d1)
+            av.av_observe(b.h, w, obs)
+        us_sep = _time_us(separate, stream, torch)
         observe = {"api": "av_observe", "w": w, "us_per_call": us,
+                   "step_observe_us": us_fused, "step_then_observe_us": us_sep,
                    "obs_per_sec": wl.B / (us * 1e-6),
                    "roofline": {"bound": "hbm", "achieved": moved / (us * 1e-6) / 1e9,
                                 "peak": HBM_PEAK_GBS, "unit": "GB/s",

@@ -169,6 +169,15 @@ av_status av_step(av_batch_t b, const uint8_t *actions, float *rewards, uint8_t 
 av_status av_step_n(av_batch_t b, int32_t k, const uint8_t *actions, float *rewards,
                     uint8_t *done);
 
+/* k steps (as av_step_n) followed by the observation of the resulting maps (as av_observe,
+ * paper Sec. 2.2.2), for agents that act on every step's observation.  On the lane16 engine
+ * with w <= 12 the window is written by the step kernel itself from the maps it holds in
+ * registers (one launch, no re-read of the maps); otherwise the observation kernel follows
+ * the step on the same stream.  obs: device uint8 [B][C][w][w], w in [1, 255].
+ * Asynchronous. */
+av_status av_step_observe(av_batch_t b, int32_t k, const uint8_t *actions, float *rewards,
+                          uint8_t *done, int32_t w, uint8_t *obs);
+
 /* Current maps as device uint8 [B][C][H][W] (0/1) written to dst.  Asynchronous. */
 av_status av_get_maps(av_batch_t b, uint8_t *dst);
 

@@ -29,7 +29,7 @@ SITE_ORDERS = {"rowmajor": AV_SITES_ROW_MAJOR, "random": AV_SITES_RANDOM}
 
 # Every symbol include/autoverse.h declares.
 ABI_SYMBOLS = ("av_create_batch", "av_load_rules", "av_set_rule_control", "av_reset",
-               "av_step", "av_step_n",
+               "av_step", "av_step_n", "av_step_observe",
                "av_get_maps", "av_observe", "av_rule_features", "av_state_ptr", "av_get_info",
                "av_get_state", "av_set_state", "av_set_stream", "av_destroy_batch",
                "av_mutate_maps", "av_mutate_rules", "av_search_create", "av_search_load_rules",
@@ -117,6 +117,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "av_reset": ([P, P], ctypes.c_int),
         "av_step": ([P, P, P, P], ctypes.c_int),
         "av_step_n": ([P, I32, P, P, P], ctypes.c_int),
+        "av_step_observe": ([P, I32, P, P, P, I32, P], ctypes.c_int),
         "av_get_maps": ([P, P], ctypes.c_int),
         "av_observe": ([P, I32, P], ctypes.c_int),
         "av_rule_features": ([P, P], ctypes.c_int),
@@ -286,6 +287,19 @@ def av_step_n(batch, k, actions, rewards, done):
         _dev_ptr(done, torch.uint8, (k, B), "done")))
 
 
+def av_step_observe(batch, k, actions, rewards, done, w, obs):
+    """actions [k][B] uint8, rewards [k][B] float32, done [k][B] uint8, obs [B][C][w][w]
+    uint8, all device tensors."""
+    torch = _torch()
+    info = av_get_info(batch)
+    B, C = info["num_envs"], info["channels"]
+    pa = _dev_ptr(actions, torch.uint8, (k, B), "actions")
+    pr = _dev_ptr(rewards, torch.float32, (k, B), "rewards")
+    pd = _dev_ptr(done, torch.uint8, (k, B), "done")
+    po = _dev_ptr(obs, torch.uint8, (B, C, w, w), "obs")
+    _check("av_step_observe", load_library().av_step_observe(batch, k, pa, pr, pd, w, po))
+
+
 def av_get_maps(batch, dst):
     info = av_get_info(batch)
     shp = (info["num_envs"], info["channels"], info["height"], info["width"])
@@ -408,6 +422,20 @@ class Batch:
             done = torch.empty((k, self.B), dtype=torch.uint8, device=self.device)
         av_step_n(self.h, k, actions, rewards, done)
         return rewards, done
+
+    def step_observe(self, actions, w, obs=None, rewards=None, done=None):
+        """actions [k][B] on the device; returns (rewards [k][B], done [k][B], obs [B][C][w][w])
+        with obs taken after the k-th step."""
+        torch = _torch()
+        k = actions.shape[0]
+        if rewards is None:
+            rewards = torch.empty((k, self.B), dtype=torch.float32, device=self.device)
+        if done is None:
+            done = torch.empty((k, self.B), dtype=torch.uint8, device=self.device)
+        if obs is None:
+            obs = torch.empty((self.B, self.C, w, w), dtype=torch.uint8, device=self.device)
+        av_step_observe(self.h, k, actions, rewards, done, w, obs)
+        return rewards, done, obs
 
     def maps(self, out=None):
         torch = _torch()

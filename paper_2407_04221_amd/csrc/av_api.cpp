@@ -548,7 +548,7 @@ av_status av_set_rule_control(av_batch_t b, const int32_t *limit, const uint8_t 
 }
 
 static av_status step_k(av_batch_t b, int32_t k, const uint8_t *actions, float *rewards,
-                        uint8_t *done) {
+                        uint8_t *done, uint8_t *obs = nullptr, int32_t w = 0) {
     if (av_status st = check_batch(b)) return st;
     if (k < 1) return fail(AV_EINVAL, "k must be >= 1 (got %d)", k);
     if (!actions || !rewards || !done) return fail(AV_EINVAL, "actions, rewards and done must not be NULL");
@@ -566,6 +566,18 @@ static av_status step_k(av_batch_t b, int32_t k, const uint8_t *actions, float *
     a.prog = b->dprog;
     a.ctl = b->ctl;
     a.ctl.step_base = b->step_no;
+    // the lane16 kernel writes small windows itself (one byte per lane and store); larger
+    // windows are faster through the observation kernel's 16-byte stores
+    // LDS of the fused path: its window buffers, the staged rows (1 KiB per channel) and
+    // player cells, and with random-order control the site keys (32 KiB)
+    const int fused_lds = 4 * ((8 * c.channels * w * w + 16 + 15) & ~15) + c.channels * 1024 +
+                          128 + (b->lane16_ctl && b->ctl.random ? 32 * 1024 : 0);
+    const bool fused = obs && b->engine == AV_ENGINE_LANE16 && w <= kFusedObserveMax &&
+                       fused_lds <= kLdsBudget;
+    if (fused) {
+        a.obs = obs;
+        a.obs_w = w;
+    }
     if (b->engine == AV_ENGINE_LANE16) {
         AV_HIP(launch_lane16_step(a, b->lane16_ctl ? b->dlprog_ctl : b->dlprog, b->stream));
     } else if (b->engine == AV_ENGINE_WAVE) {
@@ -581,6 +593,9 @@ static av_status step_k(av_batch_t b, int32_t k, const uint8_t *actions, float *
         AV_HIP(launch_generic_step(a, G, b->stream));
     }
     b->step_no += uint64_t(k);
+    if (obs && !fused)
+        AV_HIP(launch_observe(b->d_state, c.num_envs, c.channels, c.height, c.width, b->row_bytes,
+                              w, obs, b->stream));
     return AV_OK;
 }
 
@@ -593,6 +608,15 @@ av_status av_step_n(av_batch_t b, int32_t k, const uint8_t *actions, float *rewa
                     uint8_t *done) {
     g_last_error.clear();
     return step_k(b, k, actions, rewards, done);
+}
+
+av_status av_step_observe(av_batch_t b, int32_t k, const uint8_t *actions, float *rewards,
+                          uint8_t *done, int32_t w, uint8_t *obs) {
+    g_last_error.clear();
+    if (!b) return fail(AV_EINVAL, "batch handle is NULL");
+    if (!obs) return fail(AV_EINVAL, "obs is NULL");
+    if (w < 1 || w > 255) return fail(AV_EINVAL, "window size %d outside [1, 255]", w);
+    return step_k(b, k, actions, rewards, done, obs, w);
 }
 
 av_status av_get_maps(av_batch_t b, uint8_t *dst) {

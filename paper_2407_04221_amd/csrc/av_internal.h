@@ -20,6 +20,7 @@ constexpr int kMaxRules = 252;    // loaded rules; with the moves a rule index f
 constexpr int kMaxDim = 64;       // largest H and W
 constexpr int kMaxPat = 16;       // largest pattern rows / cols
 constexpr int kLdsBudget = 64 * 1024;
+constexpr int kFusedObserveMax = 12;   // largest window the lane16 step kernel writes itself
 
 // ---------------------------------------------------------------------------------
 // Compiled rules, generic form.  Built on the host from the tri-valued patterns; one
@@ -106,6 +107,8 @@ struct StepArgs {
     uint8_t *done;                   // [k][B]
     DeviceProgram prog;
     CtlArgs ctl;
+    uint8_t *obs = nullptr;          // lane16 only: observation of the final maps, [B][C][w][w]
+    int32_t obs_w = 0;               // window size, <= 64
 };
 
 // Launchers (k_generic.hip).  All return hipSuccess or the launch error.

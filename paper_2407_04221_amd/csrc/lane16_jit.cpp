@@ -635,8 +635,13 @@ hipError_t launch_lane16_step(const StepArgs &a, const Lane16Device &d, hipStrea
     uint8_t *done = a.done;
     int B = a.B, K = a.k;
     unsigned long long seed = a.ctl.seed, step_base = a.ctl.step_base;
-    void *args[] = {&state, &init, &t, &actions, &rewards, &done, &B, &K, &seed, &step_base};
-    return hipModuleLaunchKernel(d.fn, blocks, 1, 1, 256, 1, 1, 0, s, args, nullptr);
+    uint8_t *obs = a.obs;
+    int w = a.obs_w;
+    void *args[] = {&state, &init, &t, &actions, &rewards, &done, &B, &K, &seed, &step_base,
+                    &obs, &w};
+    // dynamic LDS: the fused observation's window buffers, four waves of eight environments
+    const unsigned lds = obs ? unsigned(4 * ((8 * a.C * w * w + 16 + 15) & ~15)) : 0u;
+    return hipModuleLaunchKernel(d.fn, blocks, 1, 1, 256, 1, 1, lds, s, args, nullptr);
 }
 
 }  // namespace av

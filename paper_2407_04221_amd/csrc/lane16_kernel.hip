@@ -76,7 +76,8 @@ extern "C" __global__ void __launch_bounds__(256)
 av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restrict__ init,
                int *__restrict__ tctr, const unsigned char *__restrict__ actions,
                float *__restrict__ rewards, unsigned char *__restrict__ done, int B, int K,
-               unsigned long long seed, unsigned long long step_base) {
+               unsigned long long seed, unsigned long long step_base,
+               unsigned char *__restrict__ obs, int w) {
     const int lane = threadIdx.x & 63;
     const int wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
     const int y = lane & 15;
@@ -196,6 +197,76 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
     for (int c = 0; c < AV_C; ++c) {
         if (hasA && rowok) state[(size_t(c) * B + eA) * AV_H + y] = (unsigned short)(p[c] & 0xFFFFu);
         if (hasB && rowok) state[(size_t(c) * B + eB) * AV_H + y] = (unsigned short)(p[c] >> 16);
+    }
+
+    // Observation of the final maps (paper Sec. 2.2.2): for each environment, the w x w window
+    // of every channel centred on its first player cell in row-major order, 0 off the map and
+    // for environments without a player; obs [B][C][w][w] bytes.  The wave's rows and player
+    // cells go through LDS; the windows of the wave's eight environments (contiguous in obs)
+    // are built in LDS one window row per lane, at the same offset modulo 16 as their global
+    // address, and copied out with aligned 16-byte stores.  Dynamic LDS: four waves x
+    // (8 C w^2 + 16) bytes, rounded up to 16.
+    if (obs) {
+        extern __shared__ __align__(16) unsigned char obuf[];
+        __shared__ u32 orow[4][AV_C][64];
+        __shared__ int opos[4][8];
+        const int wv = threadIdx.x >> 6;
+#pragma unroll
+        for (int c = 0; c < AV_C; ++c) orow[wv][c][lane] = p[c];
+        const u32 P = p[AV_PLAYER];
+        u32 pa = (P & 0xFFFFu) ? u32(y << 4) | u32(__ffs(P & 0xFFFFu) - 1) : 0xFFFFu;
+        u32 pb = (P >> 16) ? u32(y << 4) | u32(__ffs(P >> 16) - 1) : 0xFFFFu;
+        pa = min(pa, (u32)DPP_ROR((int)pa, 1));
+        pb = min(pb, (u32)DPP_ROR((int)pb, 1));
+        pa = min(pa, (u32)DPP_ROR((int)pa, 2));
+        pb = min(pb, (u32)DPP_ROR((int)pb, 2));
+        pa = min(pa, (u32)DPP_ROR((int)pa, 4));
+        pb = min(pb, (u32)DPP_ROR((int)pb, 4));
+        pa = min(pa, (u32)DPP_ROR((int)pa, 8));
+        pb = min(pb, (u32)DPP_ROR((int)pb, 8));
+        if (y == 0) {
+            opos[wv][2 * (lane >> 4)] = int(pa);
+            opos[wv][2 * (lane >> 4) + 1] = int(pb);
+        }
+        __syncthreads();
+        const int e0 = 2 * (wave * 4);             // first environment of the wave
+        const int nenv = B - e0 < 8 ? B - e0 : 8;
+        const int per = AV_C * w * w;
+        const int region = (8 * per + 16 + 15) & ~15;
+        unsigned char *const wbuf = obuf + wv * region;
+        unsigned char *const gdst = obs + size_t(e0 > 0 ? e0 : 0) * per;
+        const int shift = int(reinterpret_cast<unsigned long long>(gdst) & 15ull);
+        unsigned char *const mine = wbuf + shift;
+        const int rows = (nenv > 0 ? nenv : 0) * AV_C * w;
+        // window row R = (e * C + c) * w + wy, one per lane, stepping by 64
+        int e = lane / (AV_C * w), rem = lane - e * (AV_C * w);
+        int c = rem / w, wy = rem - c * w;
+        for (int R = lane; R < rows; R += 64) {
+            const int pos = opos[wv][e];
+            const bool has = pos != 0xFFFF;
+            const int yy = (pos >> 4) - w / 2 + wy, x0 = (pos & 15) - w / 2;
+            const u32 row = (has && yy >= 0 && yy < AV_H) ? orow[wv][c][(e >> 1) * 16 + yy] : 0u;
+            const int half = (e & 1) * 16;
+            unsigned char *o = mine + size_t(R) * w;
+            for (int wx = 0; wx < w; ++wx) {
+                const int xx = x0 + wx;
+                o[wx] = (unsigned char)((xx >= 0 && xx < AV_W) ? (row >> (half + xx)) & 1u : 0u);
+            }
+            wy += 64;
+            while (wy >= w) {
+                wy -= w;
+                if (++c == AV_C) { c = 0; ++e; }
+            }
+        }
+        __syncthreads();
+        const int total = rows * w;
+        const int head = shift ? (16 - shift < total ? 16 - shift : total) : 0;
+        for (int i = lane; i < head; i += 64) gdst[i] = mine[i];
+        const int nch = (total - head) / 16;
+        for (int k = lane; k < nch; k += 64)
+            *reinterpret_cast<uint4 *>(gdst + head + 16 * k) =
+                *reinterpret_cast<const uint4 *>(mine + head + 16 * k);
+        for (int i = head + 16 * nch + lane; i < total; i += 64) gdst[i] = mine[i];
     }
     if (y == 0) {
         if (hasA) tctr[eA] = tA;

@@ -95,6 +95,7 @@ def test_null_arguments_are_rejected(lib):
     assert lib.av_observe(None, 5, None) == av.AV_EINVAL
     assert lib.av_rule_features(None, None) == av.AV_EINVAL
     assert lib.av_set_rule_control(None, None, None, 0, 0) == av.AV_EINVAL
+    assert lib.av_step_observe(None, 1, None, None, None, 5, None) == av.AV_EINVAL
     m = av.mutation()
     assert lib.av_mutate_maps(None, None, 1, 4, 4, 4, m, 0, None) == av.AV_EINVAL
     assert lib.av_mutate_maps(None, None, 1, 4, 4, 4, None, 0, None) == av.AV_EINVAL

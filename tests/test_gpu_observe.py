@@ -77,3 +77,77 @@ def test_observe_rejects_bad_window():
     assert lib.av_observe(b.h, 0, ctypes.c_void_p(dst.data_ptr())) == av.AV_EINVAL
     assert lib.av_observe(b.h, 256, ctypes.c_void_p(dst.data_ptr())) == av.AV_EINVAL
     b.close()
+
+
+STEP_OBS = [("c1", 1, 6), ("c2", 70, 5), ("c4", 301, 7), ("c4", 13, 4), ("c5", 2, 4)]
+
+
+@pytest.mark.parametrize("engine", ["auto", "lane16", "generic", "wave"])
+@pytest.mark.parametrize("case", STEP_OBS, ids=[f"{c[0]}-B{c[1]}" for c in STEP_OBS])
+def test_step_observe_matches_oracle(case, engine):
+    """av_step_observe (the observation written by the lane16 step kernel itself for w <= 64,
+    else the observation kernel after the step) against the oracle stepping then observing,
+    after every call, with one and several steps per call."""
+    require_gpu()
+    import torch
+    name, B, T = case
+    wl = inputs.WORKLOADS[name].with_(B=B, T=T, L=4)
+    lane16_ok = wl.H <= 16 and wl.W <= 16 and not wl.per_env
+    if engine == "lane16" and not lane16_ok:
+        pytest.skip("lane16 takes maps of at most 16 x 16 with one shared rule set")
+    maps, rules, actions = inputs.make_all(wl, 2, "planted")
+    wins = (1, 2, 5, 10, 20, 31, 64) + ((100,) if wl.H <= 16 else ())
+    for w in wins:
+        say(f"[step_observe] {name} B={B} engine={engine} w={w}")
+        o = oracle.Oracle.for_workload(wl)
+        o.load_rules(*rules)
+        o.reset(maps)
+        b = av.Batch.for_workload(wl, engine=engine)
+        b.load_rules(*rules)
+        b.reset(maps)
+        acts = torch.from_numpy(actions).cuda()
+        t = 0
+        for k in (1, 2, T - 3):
+            want_r = np.zeros((k, wl.B), np.float32)
+            want_d = np.zeros((k, wl.B), np.uint8)
+            for j in range(k):
+                want_r[j], want_d[j] = o.step(actions[t + j])
+            r, d, obs = b.step_observe(acts[t:t + k], w)
+            t += k
+            np.testing.assert_array_equal(r.cpu().numpy(), want_r, err_msg=f"w={w} rewards")
+            np.testing.assert_array_equal(d.cpu().numpy(), want_d, err_msg=f"w={w} done")
+            np.testing.assert_array_equal(b.maps().cpu().numpy(), o.maps(), err_msg=f"w={w} maps")
+            np.testing.assert_array_equal(obs.cpu().numpy(), o.observe(w), err_msg=f"w={w} obs")
+        o.close()
+        b.close()
+
+
+@pytest.mark.parametrize("w", [5, 12])
+def test_step_observe_with_random_control(w):
+    """The fused observation next to the random-order control's LDS keys (w = 5 fits both in
+    LDS; w = 12 falls back to the observation kernel)."""
+    require_gpu()
+    import torch
+    from ctl_util import random_control
+    wl = inputs.WORKLOADS["c4"].with_(B=77, T=6, L=4)
+    maps, rules, actions = inputs.make_all(wl, 3, "dense")
+    limit, inhibit = random_control(np.random.default_rng(9), 1, wl.R, kmax=3)
+    ctl = (limit, inhibit, 1, 77)
+    o = oracle.Oracle.for_workload(wl)
+    o.load_rules(*rules)
+    o.set_rule_control(*ctl)
+    o.reset(maps)
+    b = av.Batch.for_workload(wl)
+    b.load_rules(*rules)
+    b.set_rule_control(*ctl)
+    b.reset(maps)
+    assert b.info["engine"] == av.AV_ENGINE_LANE16
+    acts = torch.from_numpy(actions).cuda()
+    for t in range(wl.T):
+        want_r, want_d = o.step(actions[t])
+        r, d, obs = b.step_observe(acts[t:t + 1], w)
+        np.testing.assert_array_equal(r.cpu().numpy()[0], want_r)
+        np.testing.assert_array_equal(d.cpu().numpy()[0], want_d)
+        np.testing.assert_array_equal(obs.cpu().numpy(), o.observe(w), err_msg=f"step {t}")
+    o.close()
+    b.close()
