@@ -262,7 +262,8 @@ av_status av_mutate_rules(int32_t num_sets, int32_t num_rules, int32_t channels,
  *     reward, earliest visit first (the root, reward 0, counts);
  *   - children whose episode ended are terminal: counted, never expanded;
  *   - the others are keyed by a 64-bit hash of their packed map (SplitMix64's finalizer
- *     chained over the rows; equal hashes are taken as equal states).  A child survives iff
+ *     chained over each channel's rows read as 64-bit words; equal hashes are taken as equal
+ *     states).  A child survives iff
  *     it has the best (reward, -depth) of its key in this level, lowest index among equals,
  *     and its key is new or it beats the (reward, -depth) stored for the key; survivors in
  *     index order, cut to max_frontier, are the next frontier.

@@ -247,8 +247,10 @@ int32_t *batch_counters(av_batch_t b) { return b->d_t; }
 int batch_row_bytes(av_batch_t b) { return b->row_bytes; }
 av_status set_error(av_status st, const char *msg) { return fail(st, "%s", msg); }
 
+int batch_engine(av_batch_t b) { return b->engine; }
+
 av_status step_prefix(av_batch_t b, int n, const uint8_t *actions, float *rewards,
-                      uint8_t *done) {
+                      uint8_t *done, const void *gsrc, int gnf, int gA, const int32_t *gdepth) {
     const av_config &c = b->cfg;
     if (n < 1 || n > c.num_envs) return fail(AV_EINVAL, "prefix of %d environments", n);
     if (!b->have_rules) return fail(AV_ESTATE, "no rules loaded");
@@ -260,6 +262,9 @@ av_status step_prefix(av_batch_t b, int n, const uint8_t *actions, float *reward
     a.state = b->d_state; a.init = b->d_init; a.t = b->d_t;
     a.actions = actions; a.rewards = rewards; a.done = done;
     a.prog = b->dprog;
+    if (gsrc && b->engine != AV_ENGINE_LANE16)
+        return fail(AV_EINVAL, "gathering step on a non-lane16 batch");
+    a.gsrc = gsrc; a.gnf = gnf; a.gA = gA; a.gdepth = gdepth;
     if (b->engine == AV_ENGINE_LANE16)
         AV_HIP(launch_lane16_step(a, b->dlprog, b->stream));
     else if (b->engine == AV_ENGINE_WAVE)

@@ -109,6 +109,11 @@ struct StepArgs {
     CtlArgs ctl;
     uint8_t *obs = nullptr;          // lane16 only: observation of the final maps, [B][C][w][w]
     int32_t obs_w = 0;               // window size, <= 64
+    // lane16 only, search expansion: environment e starts from row block e / gA of gsrc
+    // ([C][gnf][H]) with counter gdepth[e / gA] and no initial maps
+    const void *gsrc = nullptr;
+    int32_t gnf = 0, gA = 1;
+    const int32_t *gdepth = nullptr;
 };
 
 // Launchers (k_generic.hip).  All return hipSuccess or the launch error.
@@ -165,8 +170,12 @@ void *batch_state(av_batch_t b);
 int32_t *batch_counters(av_batch_t b);
 int batch_row_bytes(av_batch_t b);
 // One step of the first n environments of b, whose state rows are laid out [C][n][H].
+// With gsrc (lane16 batches only), environment e's rows are read from block e / gA of gsrc
+// ([C][gnf][H]) and its counter from gdepth[e / gA] instead.
 av_status step_prefix(av_batch_t b, int n, const uint8_t *actions, float *rewards,
-                      uint8_t *done);
+                      uint8_t *done, const void *gsrc = nullptr, int gnf = 0, int gA = 1,
+                      const int32_t *gdepth = nullptr);
+int batch_engine(av_batch_t b);
 av_status set_error(av_status st, const char *msg);
 
 // Player-centred observation window (k_observe.hip).

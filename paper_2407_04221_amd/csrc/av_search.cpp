@@ -216,9 +216,17 @@ av_status av_search_expand(av_search_t s, int64_t max_children, av_search_info *
         SearchArgs a = level_args(s, int(n));
         void *kst = batch_state(s->kids);
         SEARCH_HIP(hipMemsetAsync(s->counts, 0, 3 * sizeof(uint32_t), s->stream));
-        SEARCH_HIP(launch_search_phase(a, s->row_bytes, s->front[s->cur], int(s->n_front), kst,
-                                       batch_counters(s->kids), s->stream, 0, 0));
-        if (av_status st = step_prefix(s->kids, int(n), s->actions, s->rew, s->done)) return st;
+        if (batch_engine(s->kids) == AV_ENGINE_LANE16) {
+            // the lane16 step reads each child's parent rows and depth itself
+            if (av_status st = step_prefix(s->kids, int(n), s->actions, s->rew, s->done,
+                                           s->front[s->cur], int(s->n_front), s->A,
+                                           s->depth[s->cur]))
+                return st;
+        } else {
+            SEARCH_HIP(launch_search_phase(a, s->row_bytes, s->front[s->cur], int(s->n_front), kst,
+                                           batch_counters(s->kids), s->stream, 0, 0));
+            if (av_status st = step_prefix(s->kids, int(n), s->actions, s->rew, s->done)) return st;
+        }
         SEARCH_HIP(launch_search_phase(a, s->row_bytes, s->front[s->cur], int(s->n_front), kst,
                                        nullptr, s->stream, 1, 0));
         uint32_t counts[3];

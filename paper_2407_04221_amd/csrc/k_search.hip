@@ -39,34 +39,32 @@ __device__ inline uint64_t mix64(uint64_t z) {
     return z ^ (z >> 31);
 }
 
-// Hash of environment i's map in a packed [C][n][H] buffer: chained mixing of the rows in
-// (channel, row) order; 0 is reserved for empty slots.  When an environment's rows of one
-// channel fill whole 16-byte words they are read 16 bytes at a time (same rows, same order).
+// Hash of environment i's map in a packed [C][n][H] buffer: one channel's H rows are H x
+// sizeof(RowT) consecutive bytes; they are read as 64-bit little-endian words (the last one
+// zero-padded) and the words of all channels, in channel order, are chained through the
+// mixer: h = mix64(h ^ word).  0 is reserved for empty slots.
 template <typename RowT>
 __device__ inline uint64_t map_hash(const void *state, int i, int n, int C, int H) {
     uint64_t h = 0x9E3779B97F4A7C15ull;
-    constexpr int per16 = 16 / sizeof(RowT);
-    if (H % per16 == 0) {
-        for (int c = 0; c < C; ++c) {
-            const uint4 *blk = reinterpret_cast<const uint4 *>(
-                static_cast<const RowT *>(state) + (size_t(c) * n + i) * H);
-            for (int v = 0; v < H / per16; ++v) {
-                const uint4 w = blk[v];
-                const uint64_t q[2] = {uint64_t(w.x) | (uint64_t(w.y) << 32),
-                                       uint64_t(w.z) | (uint64_t(w.w) << 32)};
-                for (int k = 0; k < per16; ++k) {
-                    const int bits = 8 * int(sizeof(RowT));
-                    const uint64_t word = q[(k * bits) / 64];
-                    const uint64_t row = bits == 64 ? word : (word >> ((k * bits) % 64)) &
-                                                                 ((uint64_t(1) << bits) - 1);
-                    h = mix64(h ^ row);
-                }
+    const int bytes = H * int(sizeof(RowT));
+    for (int c = 0; c < C; ++c) {
+        const RowT *blk = static_cast<const RowT *>(state) + (size_t(c) * n + i) * H;
+        if (bytes % 16 == 0) {
+            const uint4 *v = reinterpret_cast<const uint4 *>(blk);
+            for (int k = 0; k < bytes / 16; ++k) {
+                const uint4 q = v[k];
+                h = mix64(h ^ (uint64_t(q.x) | (uint64_t(q.y) << 32)));
+                h = mix64(h ^ (uint64_t(q.z) | (uint64_t(q.w) << 32)));
+            }
+        } else {
+            constexpr int per = 8 / int(sizeof(RowT));
+            for (int y0 = 0; y0 < H; y0 += per) {
+                uint64_t word = 0;
+                for (int k = 0; k < per && y0 + k < H; ++k)
+                    word |= uint64_t(blk[y0 + k]) << (8 * int(sizeof(RowT)) * k);
+                h = mix64(h ^ word);
             }
         }
-    } else {
-        for (int c = 0; c < C; ++c)
-            for (int y = 0; y < H; ++y)
-                h = mix64(h ^ row_at<RowT>(state, (size_t(c) * n + i) * H + y));
     }
     return h ? h : 1;
 }

@@ -637,8 +637,11 @@ hipError_t launch_lane16_step(const StepArgs &a, const Lane16Device &d, hipStrea
     unsigned long long seed = a.ctl.seed, step_base = a.ctl.step_base;
     uint8_t *obs = a.obs;
     int w = a.obs_w;
+    const void *gsrc = a.gsrc;
+    int gnf = a.gnf, gA = a.gA;
+    const int32_t *gdepth = a.gdepth;
     void *args[] = {&state, &init, &t, &actions, &rewards, &done, &B, &K, &seed, &step_base,
-                    &obs, &w};
+                    &obs, &w, &gsrc, &gnf, &gA, &gdepth};
     // dynamic LDS: the fused observation's window buffers, four waves of eight environments
     const unsigned lds = obs ? unsigned(4 * ((8 * a.C * w * w + 16 + 15) & ~15)) : 0u;
     return hipModuleLaunchKernel(d.fn, blocks, 1, 1, 256, 1, 1, lds, s, args, nullptr);

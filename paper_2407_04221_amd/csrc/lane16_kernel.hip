@@ -77,7 +77,9 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
                int *__restrict__ tctr, const unsigned char *__restrict__ actions,
                float *__restrict__ rewards, unsigned char *__restrict__ done, int B, int K,
                unsigned long long seed, unsigned long long step_base,
-               unsigned char *__restrict__ obs, int w) {
+               unsigned char *__restrict__ obs, int w,
+               const unsigned short *__restrict__ gsrc, int gnf, int gA,
+               const int *__restrict__ gdepth) {
     const int lane = threadIdx.x & 63;
     const int wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
     const int y = lane & 15;
@@ -98,20 +100,30 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
     (void)seed;
     (void)step_base;
 #endif
+    // Search expansion (gsrc set): environment e starts from row block e / gA of gsrc, laid
+    // out [C][gnf][H], with its step counter at gdepth[e / gA]; there are no initial maps to
+    // return to (an ended episode is never expanded further).
     u32 p[AV_C], q[AV_C];   // current rows, initial rows (kept for automatic resets)
+    const unsigned short *const src = gsrc ? gsrc : state;
+    const int sstride = gsrc ? gnf : B;
+    const int sA = gsrc ? iA / gA : iA, sB = gsrc ? iB / gA : iB;
 #pragma unroll
     for (int c = 0; c < AV_C; ++c) {
-        const size_t row = size_t(c) * B;
         const int yy = rowok ? y : 0;
-        const u32 lo = u32(state[(row + iA) * AV_H + yy]);
-        const u32 hi = u32(state[(row + iB) * AV_H + yy]);
-        const u32 ilo = u32(init[(row + iA) * AV_H + yy]);
-        const u32 ihi = u32(init[(row + iB) * AV_H + yy]);
+        const u32 lo = u32(src[(size_t(c) * sstride + sA) * AV_H + yy]);
+        const u32 hi = u32(src[(size_t(c) * sstride + sB) * AV_H + yy]);
         const u32 keep = HALF(hasA && rowok, hasB && rowok);
         p[c] = (lo | (hi << 16)) & keep;
-        q[c] = (ilo | (ihi << 16)) & keep;
+        if (gsrc) {
+            q[c] = p[c];
+        } else {
+            const size_t row = size_t(c) * B;
+            const u32 ilo = u32(init[(row + iA) * AV_H + yy]);
+            const u32 ihi = u32(init[(row + iB) * AV_H + yy]);
+            q[c] = (ilo | (ihi << 16)) & keep;
+        }
     }
-    int tA = tctr[iA], tB = tctr[iB];
+    int tA = gsrc ? gdepth[sA] : tctr[iA], tB = gsrc ? gdepth[sB] : tctr[iB];
 
     // Actions arrive 16 steps at a time: lane y of a row holds step k0 + y of its pair
     // (env A in byte 0, env B in byte 1); each step reads its entry across the row.
