@@ -129,3 +129,39 @@ def test_last_error_is_cleared_by_a_successful_call(lib):
     assert av.av_last_error()
     assert lib.av_destroy_batch(None) == av.AV_OK
     assert av.av_last_error() == ""
+
+
+def test_missing_library_fails_loudly():
+    """No fallback: without libautoverse.so the binding raises instead of computing anything."""
+    import subprocess
+    import sys
+    code = ("import paper_2407_04221_amd as av\n"
+            "try:\n    av.load_library('/nonexistent/libautoverse.so')\n"
+            "except RuntimeError as e:\n    print('raised', e)\n")
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True,
+                         cwd=os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    assert out.stdout.startswith("raised"), out.stdout + out.stderr
+
+
+def test_product_and_oracle_share_no_code():
+    """The library's sources and binding never name the oracle, the oracle never names the
+    library's sources, and the built library needs no oracle symbol."""
+    import re
+    import subprocess
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    pkg = os.path.join(root, "paper_2407_04221_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".cpp", ".hip", ".h", ".inc")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert not re.search(r"\bimport oracle\b|from oracle\b|avo_|avo\.h", text), f
+    for f in os.listdir(os.path.join(root, "oracle")):
+        if f.endswith((".c", ".h", ".py")):
+            text = open(os.path.join(root, "oracle", f)).read()
+            assert "csrc" not in text and "paper_2407_04221_amd" not in text.replace(
+                "from paper_2407_04221_amd import inputs", ""), f
+    lib = av.LIB_PATH
+    if os.path.exists(lib):
+        und = subprocess.run(["nm", "-D", "--undefined-only", lib], capture_output=True,
+                             text=True).stdout
+        assert "avo_" not in und
