@@ -146,9 +146,10 @@ typedef enum {
  *            step number (steps since av_reset, all environments counted together)
  *   seed     key of the random index channel
  * Engines: on a lane16 batch the control is compiled into the lane16 program (a new
- * program per call); on a wave batch it runs on the generic engine, to which a batch
- * created with AV_ENGINE_AUTO switches while some limit or inhibition is set (an explicit
- * wave engine then gives AV_EINVAL).
+ * program per call); the wave engine runs it when its scratch (about 1.3 KiB, plus 4 bytes
+ * per cell for the random channel) still fits its 64 KiB of LDS; otherwise it runs on the
+ * generic engine, to which a batch created with AV_ENGINE_AUTO switches while some limit or
+ * inhibition is set (an explicit wave engine then gives AV_EINVAL).
  * AV_ESTATE before av_load_rules (which clears the control); AV_EINVAL for a negative
  * limit, an inhibition with q >= r or an unknown order.  Synchronises the stream. */
 av_status av_set_rule_control(av_batch_t b, const int32_t *limit, const uint8_t *inhibit,

@@ -489,11 +489,16 @@ av_status av_set_rule_control(av_batch_t b, const int32_t *limit, const uint8_t 
                         active = true;
                     }
     const bool random = order == AV_SITES_RANDOM;
-    // control compiles into the lane16 program; on other batches it runs on the generic engine
+    // control compiles into the lane16 program; the wave engine runs it when its scratch fits
+    // in LDS; otherwise it runs on the generic engine
     const bool on_lane16 = b->plain_engine == AV_ENGINE_LANE16;
-    if (active && !on_lane16 && c.engine != AV_ENGINE_AUTO && c.engine != AV_ENGINE_GENERIC)
-        return fail(AV_EINVAL, "rule application control on a wave batch runs on the generic "
-                    "engine; create the batch with AV_ENGINE_AUTO or AV_ENGINE_GENERIC");
+    const bool on_wave = b->plain_engine == AV_ENGINE_WAVE &&
+                         wave_lds_bytes(c.height, c.width, c.channels, R + kMoveRules, true,
+                                        random) <= size_t(kLdsBudget);
+    if (active && !on_lane16 && !on_wave && c.engine != AV_ENGINE_AUTO &&
+        c.engine != AV_ENGINE_GENERIC)
+        return fail(AV_EINVAL, "rule application control does not fit this wave batch's LDS; "
+                    "create the batch with AV_ENGINE_AUTO or AV_ENGINE_GENERIC");
     const size_t env_lds = generic_env_lds_bytes(c.height, c.width, c.channels, Rt, true, random);
     if (active && env_lds > size_t(kLdsBudget))
         return fail(AV_EINVAL, "rule application control needs %zu bytes of LDS per environment "
@@ -546,6 +551,8 @@ av_status av_set_rule_control(av_batch_t b, const int32_t *limit, const uint8_t 
         }
         b->lane16_ctl = true;
         b->engine = AV_ENGINE_LANE16;
+    } else if (on_wave) {
+        b->engine = AV_ENGINE_WAVE;
     } else {
         b->engine = AV_ENGINE_GENERIC;
     }

@@ -183,7 +183,8 @@ hipError_t launch_observe(const void *state, int B, int C, int H, int W, int row
                           uint8_t *dst, hipStream_t s);
 
 // The wave engine (k_wave.hip): one environment per workgroup.
-size_t wave_lds_bytes(int H, int W, int C, int rules_per_set);
+size_t wave_lds_bytes(int H, int W, int C, int rules_per_set, bool control = false,
+                      bool random = false);
 hipError_t launch_wave_step(const StepArgs &a, hipStream_t s);
 
 }  // namespace av

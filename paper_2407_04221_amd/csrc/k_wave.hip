@@ -29,7 +29,14 @@
 //           minus votes: new = (old + #plus > #minus) = (old + sum >= 1);
 //   end     done when no player bit is left or the counter reaches L; reward = sum over
 //           fired rules of reward * popcount; done environments reload their initial rows.
+// With rule application control (Sec. 2.1.1), the loaded rules of a batch only record their
+// matches; group 0 (one lane per row) then filters them in index order — inhibition by the
+// applied matches of earlier rules (rows OR-ed, then dilated over columns), a cap through a
+// row-major prefix of per-row counts or, for the random index channel (Philox keys computed
+// into LDS once per step), a radix select over a 256-bin LDS histogram — and the groups cast
+// the filtered rules' votes and rewards before the write.
 #include "av_internal.h"
+#include "philox.h"
 
 namespace av {
 namespace {
@@ -135,7 +142,13 @@ struct WaveLayout {
     int Hq;          // lanes per group (16, 32 or 64)
     int prog_lds;    // 1 if the rule program is copied into LDS
     int hdr_words, match_words, vote_words;
+    int ctl_words;   // LDS words of the control scratch (0 without control)
 };
+
+// rowcnt [64], count [4], histogram [256], keys [H*W] (random order only)
+int ctl_scratch_words(int H, int W, bool control, bool random) {
+    return control ? 64 + 4 + 256 + (random ? H * W : 0) : 0;
+}
 
 template <typename RowT>
 __global__ void __launch_bounds__(256) wave_step(StepArgs a, WaveLayout L) {
@@ -156,7 +169,11 @@ __global__ void __launch_bounds__(256) wave_step(StepArgs a, WaveLayout L) {
     RowT *MI = PL + size_t(C1) * 64;              // [C1][64]
     int *fired = reinterpret_cast<int *>(MI + size_t(C1) * 64);  // [Rt]
     int *red = fired + Rt;                        // [1] reward sum
-    uint32_t *pcopy = reinterpret_cast<uint32_t *>(red + 2);   // program copy (8-byte aligned)
+    int *rowcnt = red + 2;                        // control scratch (ctl_words words)
+    int *ccnt = rowcnt + 64;
+    int *hist = ccnt + 4;
+    uint32_t *keys = reinterpret_cast<uint32_t *>(hist + 256);
+    uint32_t *pcopy = reinterpret_cast<uint32_t *>(red + 2 + L.ctl_words);   // program copy
 
     const size_t words = size_t(C1) * Hp + size_t(Rt) * kMRows + size_t(2) * C1 * 64;
     for (size_t w = tid; w < words; w += nthreads) P[w] = 0;
@@ -196,6 +213,16 @@ __global__ void __launch_bounds__(256) wave_step(StepArgs a, WaveLayout L) {
             else if (act == 4) f = Pp[ry] >> 1;
             if (row) P[C * Hp + y] = f;
         }
+        if (a.ctl.active && a.ctl.random) {
+            // this step's random index channel, eight cells per Philox block
+            const uint64_t n = a.ctl.step_base + uint64_t(k);
+            for (int gi = tid; gi * 8 < H * W; gi += nthreads) {
+                uint32_t u[8];
+                philox_words(a.ctl.seed, n, uint64_t(b), 0, uint64_t(gi), u);
+                for (int j = 0; j < 8 && gi * 8 + j < H * W; ++j)
+                    keys[gi * 8 + j] = (u[j] & 0xFFFFF000u) | uint32_t(4095 - (gi * 8 + j));
+            }
+        }
         __syncthreads();
 
         // Rules in batches: all at once (parallel mode) or one at a time (sequential mode,
@@ -232,6 +259,7 @@ __global__ void __launch_bounds__(256) wave_step(StepArgs a, WaveLayout L) {
                 if (group_any(acc != 0, Hq, lane)) {
                     M[size_t(r) * kMRows + kPad + y] = acc;
                     if (y == 0) fired[r] = 1;
+                    if (a.ctl.active && r >= kMoveRules) continue;   // filtered, then applied
                     rsum += hreward * popc(acc);
                     for (int ev = 0; ev < vcnt; ++ev) {
                         const uint32_t v = vent[voff + ev];
@@ -243,6 +271,115 @@ __global__ void __launch_bounds__(256) wave_step(StepArgs a, WaveLayout L) {
                 }
             }
             __syncthreads();
+
+            if (a.ctl.active) {
+                // filter the batch's loaded rules in index order (group 0, lane = row)
+                const int r0 = rb < kMoveRules ? kMoveRules : rb;
+                for (int r = r0; r < re; ++r) {
+                    if (!fired[r]) continue;                 // uniform: set before the last barrier
+                    if (tid == 0) *ccnt = 0;
+                    __syncthreads();
+                    const size_t cr = size_t(s) * Rt + r;
+                    const bool mine = g == 0 && row && fired[r];
+                    RowT acc = mine ? M[size_t(r) * kMRows + kPad + y] : RowT(0);
+                    if (mine && acc) {
+                        const uint32_t *hw = hdrw + r * kHdrWords;
+                        const int hn = int(hw[0]), hm = int(hw[1]);
+                        const uint32_t *inh = a.ctl.inhibit + cr * a.ctl.words;
+                        for (int w = 0; w < a.ctl.words; ++w) {
+                            uint32_t bits = inh[w];
+                            while (bits) {
+                                const int q = w * 32 + __ffs(bits) - 1;
+                                bits &= bits - 1;
+                                if (!fired[q]) continue;
+                                const uint32_t *qw = hdrw + q * kHdrWords;
+                                const int nq = int(qw[0]), mq = int(qw[1]);
+                                // anchors of q whose patch overlaps an hn x hm patch at row y
+                                RowT o = 0;
+                                const int ylo = y - nq + 1 < 0 ? 0 : y - nq + 1;
+                                const int yhi = y + hn - 1 > H - 1 ? H - 1 : y + hn - 1;
+                                for (int yy = ylo; yy <= yhi; ++yy) o |= M[size_t(q) * kMRows + kPad + yy];
+                                RowT dil = o;
+                                for (int d = 1; d < hm; ++d) dil |= o >> d;
+                                for (int d = 1; d < mq; ++d) dil |= o << d;
+                                acc &= ~dil;
+                            }
+                        }
+                    }
+                    if (g == 0) {
+                        if (row && fired[r]) M[size_t(r) * kMRows + kPad + y] = acc;
+                        if (y < 64) rowcnt[y] = row ? popc(acc) : 0;
+                        if (acc) atomicAdd(ccnt, popc(acc));
+                    }
+                    __syncthreads();
+                    const int lim = a.ctl.limit[cr];
+                    if (lim > 0 && *ccnt > lim) {            // uniform: every thread reads ccnt
+                        if (!a.ctl.random) {
+                            if (mine) {
+                                int before = 0;
+                                for (int yy = 0; yy < y; ++yy) before += rowcnt[yy];
+                                RowT keep = 0, rest = acc;
+                                for (int kk = lim - before; kk > 0 && rest; --kk) {
+                                    const RowT lb = rest & (~rest + 1);
+                                    keep |= lb;
+                                    rest ^= lb;
+                                }
+                                acc = keep;
+                                M[size_t(r) * kMRows + kPad + y] = acc;
+                            }
+                        } else {
+                            // radix select of the lim-th largest key among the matches
+                            uint32_t prefix = 0, pmask = 0;
+                            int need = lim;
+                            for (int shift = 24; shift >= 0; shift -= 8) {
+                                for (int i = tid; i < 256; i += nthreads) hist[i] = 0;
+                                __syncthreads();
+                                for (RowT rest = mine ? acc : RowT(0); rest; rest &= rest - 1) {
+                                    const uint32_t key = keys[y * W + lowbit(rest)];
+                                    if ((key & pmask) == prefix)
+                                        atomicAdd(&hist[(key >> shift) & 255], 1);
+                                }
+                                __syncthreads();
+                                int above = 0, d = 255;
+                                for (; d > 0; --d) {
+                                    const int cnt = hist[d];
+                                    if (above + cnt >= need) break;
+                                    above += cnt;
+                                }
+                                prefix |= uint32_t(d) << shift;
+                                pmask |= 255u << shift;
+                                need -= above;
+                                __syncthreads();             // before the next pass clears hist
+                            }
+                            if (mine) {
+                                RowT keep = 0;
+                                for (RowT rest = acc; rest; rest &= rest - 1) {
+                                    const int x = lowbit(rest);
+                                    if (keys[y * W + x] >= prefix) keep |= RowT(1) << x;
+                                }
+                                acc = keep;
+                                M[size_t(r) * kMRows + kPad + y] = acc;
+                            }
+                        }
+                    }
+                    __syncthreads();
+                }
+                // rewards and votes of the filtered loaded rules, group g taking rules g, g+4, ...
+                for (int r = r0 + ((g - r0 % kGroups + kGroups) % kGroups); r < re; r += kGroups) {
+                    if (!fired[r]) continue;
+                    const uint32_t *hw = hdrw + r * kHdrWords;
+                    const int hreward = int(hw[2]), voff = int(hw[5]), vcnt = int(hw[6]);
+                    const RowT *Mr = M + size_t(r) * kMRows + kPad;
+                    if (row) rsum += hreward * popc(Mr[y]);
+                    for (int ev = 0; ev < vcnt; ++ev) {
+                        const uint32_t v = vent[voff + ev];
+                        const int c = v & 255, i = (v >> 8) & 255, j = (v >> 16) & 255;
+                        const RowT t = RowT(Mr[y - i] << j);          // kPad zero rows above
+                        if (row && t) lds_or(((v >> 24) & 1 ? PL : MI) + c * 64 + y, t);
+                    }
+                }
+                __syncthreads();
+            }
 
             // new rows: group g rewrites planes g, g+4, ... (each lane its own row)
             for (int c = g; c < Cw; c += kGroups) {
@@ -292,8 +429,9 @@ size_t wave_base_bytes(int H, int W, int C, int rules_per_set) {
 
 }  // namespace
 
-size_t wave_lds_bytes(int H, int W, int C, int rules_per_set) {
-    return wave_base_bytes(H, W, C, rules_per_set);
+size_t wave_lds_bytes(int H, int W, int C, int rules_per_set, bool control, bool random) {
+    return wave_base_bytes(H, W, C, rules_per_set) +
+           sizeof(int) * size_t(ctl_scratch_words(H, W, control, random));
 }
 
 hipError_t launch_wave_step(const StepArgs &a, hipStream_t s) {
@@ -302,7 +440,9 @@ hipError_t launch_wave_step(const StepArgs &a, hipStream_t s) {
     L.hdr_words = int(a.prog.rules_per_set * (sizeof(RuleHdr) / 4));
     L.match_words = a.prog.match_stride;
     L.vote_words = a.prog.rvote_stride;
-    const size_t base = wave_base_bytes(a.H, a.W, a.C, a.prog.rules_per_set);
+    L.ctl_words = ctl_scratch_words(a.H, a.W, a.ctl.active != 0, a.ctl.random != 0);
+    const size_t base = wave_lds_bytes(a.H, a.W, a.C, a.prog.rules_per_set, a.ctl.active != 0,
+                                       a.ctl.random != 0);
     const size_t prog = size_t(L.hdr_words + L.match_words + L.vote_words) * 4;
     L.prog_lds = base + prog <= size_t(kLdsBudget) ? 1 : 0;
     const size_t lds = base + (L.prog_lds ? prog : 0);
