@@ -217,7 +217,6 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
                     const int w = in_at(ru, c, i, j);
                     if (w >= 0) {
                         ents[r].push_back({c, i, j, w, rank_of(c, w, C)});
-                        if (j > 0) xs.insert({c, j});
                     }
                     const int k = c < C ? kout(w, out_at(ru, c, i, j)) : 0;
                     if (k > 0) plus[c].push_back({r, i, j});
@@ -226,6 +225,14 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
                 }
         std::stable_sort(ents[r].begin(), ents[r].end(),
                          [](const Entry &a, const Entry &b) { return a.rank < b.rank; });
+    }
+    // Column-shifted planes read on every step (by the moves and by the loaded rules' probe
+    // entries) are computed once up front; the others only inside the branches that need them.
+    const int n_top = std::min(R, kMoveRules);
+    for (int r = 0; r < R; ++r) {
+        const size_t used = r < n_top ? ents[r].size() : std::min<size_t>(2, ents[r].size());
+        for (size_t e = 0; e < used; ++e)
+            if (ents[r][e].j > 0) xs.insert({ents[r][e].c, ents[r][e].j});
     }
 
     o << "// ---- generated: " << R << " rules over " << C1 << " planes ----\n";
@@ -237,7 +244,9 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
           << ") ? BOTH(COLMASK(" << std::max(0, W - s.second + 1) << ")) : 0u;\n";
 
     auto base = [&](const Entry &e) {
-        return e.j ? "X" + std::to_string(e.c) + "_" + std::to_string(e.j) : plane(e.c, C);
+        if (!e.j) return plane(e.c, C);
+        if (xs.count({e.c, e.j})) return "X" + std::to_string(e.c) + "_" + std::to_string(e.j);
+        return "(" + plane(e.c, C) + " >> " + std::to_string(e.j) + ")";
     };
 
     auto row_and = [&](const std::vector<Entry> &es) {
