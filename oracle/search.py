@@ -55,36 +55,30 @@ class Search:
         self.best = (0, 0)                             # (reward, visit index)
 
     def expand(self, max_children):
-        A = len(self.actions)
-        pairs = [(p, a) for p in range(len(self.frontier)) for a in self.actions]
-        pairs = pairs[:max(0, max_children)]
-        n = len(pairs)
-        info = dict(parents=len(self.frontier), children=n, terminal=0, survivors=0)
-        if n == 0:                                      # nothing expanded: frontier kept
-            info.update(level=self.level, frontier=0, visited=self.visited,
-                        best_reward=self.best[0], best_visit=self.best[1])
-            return info
-        o = _oracle.Oracle(n, self.H, self.W, self.C, max(self.R, 1), self.mh, self.mw, False,
-                           self.L, lib_path=self.lib_path, rule_mode=self.rule_mode)
-        o.load_rules(*self.rules)
-        o.reset(np.stack([self.frontier[p][0] for p, _ in pairs]))
-        o.set_counters(np.array([self.frontier[p][2] for p, _ in pairs], np.int32))
-        r, d = o.step(np.array([a for _, a in pairs], np.uint8))
-        maps = o.maps()
-        o.close()
+        info = dict(parents=len(self.frontier), children=0, terminal=0, survivors=0)
+        kids = self._children(self.frontier, max_children)
+        if kids:                                        # nothing expanded: frontier kept
+            survivors = self._absorb(kids, info)
+            self.frontier = [kids[i][:3] for i in survivors[:self.max_frontier]]
+            self.level += 1
+        info.update(level=self.level, frontier=len(self.frontier), visited=self.visited,
+                    best_reward=self.best[0], best_visit=self.best[1])
+        return info
+
+    def _absorb(self, kids, info):
+        """Count the visits of one expansion's children (in order), track the best node,
+        set terminal ones aside and deduplicate the rest against each other and the table.
+        Returns the surviving children's indices in increasing order."""
+        info["children"] = len(kids)
         best_in_level = {}                             # map -> ((reward, -depth), index)
-        kids = []
-        for i, (p, a) in enumerate(pairs):
-            reward = self.frontier[p][1] + int(r[i])
-            depth = self.frontier[p][2] + 1
+        for i, (m, reward, depth, done) in enumerate(kids):
             visit = self.visited + 1 + i
             if reward > self.best[0]:
                 self.best = (reward, visit)
-            kids.append((maps[i], reward, depth))
-            if d[i]:
+            if done:
                 info["terminal"] += 1
                 continue
-            key = maps[i].tobytes()
+            key = m.tobytes()
             val = (reward, -depth)
             if key not in best_in_level or val > best_in_level[key][0]:
                 best_in_level[key] = (val, i)
@@ -96,12 +90,26 @@ class Search:
                 survivors.append(i)
         survivors.sort()
         info["survivors"] = len(survivors)
-        self.frontier = [kids[i] for i in survivors[:self.max_frontier]]
-        self.visited += n
-        self.level += 1
-        info.update(level=self.level, frontier=len(self.frontier), visited=self.visited,
-                    best_reward=self.best[0], best_visit=self.best[1])
-        return info
+        self.visited += len(kids)
+        return survivors
+
+    def _children(self, parents, max_children):
+        """Step every (parent, action) pair, parents in the given order, cut to max_children.
+        parents: list of (map, reward, depth).  Returns [(map, reward, depth, done)]."""
+        pairs = [(p, a) for p in range(len(parents)) for a in self.actions][:max(0, max_children)]
+        n = len(pairs)
+        if n == 0:
+            return []
+        o = _oracle.Oracle(n, self.H, self.W, self.C, max(self.R, 1), self.mh, self.mw, False,
+                           self.L, lib_path=self.lib_path, rule_mode=self.rule_mode)
+        o.load_rules(*self.rules)
+        o.reset(np.stack([parents[p][0] for p, _ in pairs]))
+        o.set_counters(np.array([parents[p][2] for p, _ in pairs], np.int32))
+        r, d = o.step(np.array([a for _, a in pairs], np.uint8))
+        maps = o.maps()
+        o.close()
+        return [(maps[i], parents[p][1] + int(r[i]), parents[p][2] + 1, bool(d[i]))
+                for i, (p, _) in enumerate(pairs)]
 
     def frontier_arrays(self):
         """(maps uint8 [N][C][H][W], reward int32 [N], depth int32 [N]) in frontier order."""
@@ -118,5 +126,74 @@ class Search:
         self.begin(root)
         out = []
         while self.frontier and self.visited < budget and self.level < max_levels:
+            out.append(self.expand(budget - self.visited))
+        return out
+
+
+class BestFirst(Search):
+    """Batched best-first search (the paper scores environments with best-first search that
+    prioritises higher reward, Sec. 2.2.1).  Open nodes are ordered by (higher reward, then
+    smaller depth, then smaller node id); every iteration pops the k first open nodes (k = 1
+    is plain best-first), drops those whose state has since been reached with a better
+    (reward, -depth) (the deeper or lower-reward node is pruned), and expands the rest in
+    node-id order exactly as one level of Search: children in (parent, action) order cut to
+    the remaining budget, terminal children counted and never opened, in-iteration duplicates
+    resolved by (reward, -depth) then lowest child index, and a child kept iff its state is new
+    or it beats the stored (reward, -depth).  Kept children become open nodes with the next
+    ids, in child order.  The root is node 0."""
+
+    def __init__(self, H, W, C, rules, L, k=1, num_actions=5, rule_mode=0,
+                 lib_path=_oracle.LIB):
+        super().__init__(H, W, C, rules, L, num_actions=num_actions, rule_mode=rule_mode,
+                         lib_path=lib_path)
+        assert k >= 1
+        self.k = k
+
+    def begin(self, root):
+        super().begin(root)
+        root = self.frontier[0][0]
+        self.nodes = [(root, 0, 0)]          # id -> (map, reward, depth)
+        self.open = [0]
+        self.expanded = []                   # ids of the expanded nodes, in order
+
+    def expand(self, max_children):
+        info = dict(parents=0, children=0, terminal=0, survivors=0)
+        if max_children <= 0 or not self.open:
+            info.update(level=self.level, frontier=len(self.open), visited=self.visited,
+                        best_reward=self.best[0], best_visit=self.best[1])
+            return info
+        self.open.sort(key=lambda i: (-self.nodes[i][1], self.nodes[i][2], i))
+        popped, self.open = self.open[:self.k], self.open[self.k:]
+        alive = sorted(i for i in popped
+                       if self.table[self.nodes[i][0].tobytes()] == (self.nodes[i][1],
+                                                                     -self.nodes[i][2]))
+        parents = [self.nodes[i] for i in alive]
+        self.expanded.extend(alive)
+        kids = self._children(parents, max_children)
+        info["parents"] = len(parents)
+        for i in self._absorb(kids, info):
+            m, reward, depth, _ = kids[i]
+            self.open.append(len(self.nodes))
+            self.nodes.append((m, reward, depth))
+        self.level += 1
+        info.update(level=self.level, frontier=len(self.open), visited=self.visited,
+                    best_reward=self.best[0], best_visit=self.best[1])
+        return info
+
+    def open_arrays(self):
+        """The open nodes in priority order: (maps, reward, depth, node id)."""
+        order = sorted(self.open, key=lambda i: (-self.nodes[i][1], self.nodes[i][2], i))
+        if not order:
+            return (np.zeros((0, self.C, self.H, self.W), np.uint8), np.zeros(0, np.int32),
+                    np.zeros(0, np.int32), np.zeros(0, np.int64))
+        return (np.stack([self.nodes[i][0] for i in order]),
+                np.array([self.nodes[i][1] for i in order], np.int32),
+                np.array([self.nodes[i][2] for i in order], np.int32),
+                np.array(order, np.int64))
+
+    def run(self, root, budget, max_levels=1 << 30):
+        self.begin(root)
+        out = []
+        while self.open and self.visited < budget and self.level < max_levels:
             out.append(self.expand(budget - self.visited))
         return out
