@@ -140,7 +140,8 @@ def bench_search(av, torch, wl, args):
     rules = tuple(x[:1] for x in rules)
     table_log2 = max(10, min(30, int(np.ceil(np.log2(max(2 * args.search, 16))))))
     g = av.Search(wl.H, wl.W, wl.C, wl.R, wl.max_h, wl.max_w, wl.L, num_actions=5,
-                  max_frontier=args.search_frontier, table_log2=table_log2)
+                  max_frontier=args.search_frontier, table_log2=table_log2,
+                  best_first_k=args.search_k, max_nodes=max(16, args.search + 1))
     g.load_rules(*rules)
     g.run(maps[0], min(args.search, 20000))          # warm-up (kernels, JIT)
     torch.cuda.synchronize()
@@ -155,13 +156,14 @@ def bench_search(av, torch, wl, args):
     per_visit = 5 * S + 48
     gbs = visited * per_visit / dt / 1e9
     return {"api": "av_search_expand", "variant": args.search_variant, "budget": args.search,
+            "order": f"best-first k={args.search_k}" if args.search_k else "level",
             "visited": visited, "levels": len(levels), "seconds": dt,
             "visits_per_sec": visited / dt, "best_reward": levels[-1]["best_reward"] if levels else 0,
             "best_visit": levels[-1]["best_visit"] if levels else 0,
             "frontier_peak": max((lv["frontier"] for lv in levels), default=0),
             "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                          "frac": gbs / HBM_PEAK_GBS, "bytes_per_visit": per_visit},
-            "level_sizes": [lv["children"] for lv in levels]}
+            "level_sizes": [lv["children"] for lv in levels][:64]}
 
 
 def main():
@@ -193,6 +195,8 @@ def main():
                     help="also time the batched search from environment 0 with this many visits")
     ap.add_argument("--search-variant", default="dense", choices=["literal", "planted", "dense"])
     ap.add_argument("--search-frontier", type=int, default=1 << 20)
+    ap.add_argument("--search-k", type=int, default=0,
+                    help="batched best-first popping K nodes per iteration (0: level order)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--seed", type=int, default=0)

@@ -251,9 +251,15 @@ av_status av_mutate_rules(int32_t num_sets, int32_t num_rules, int32_t channels,
  * and the reward accumulated so far — an edge is an action; a state equal to one seen
  * before keeps the node with the higher reward, then the shallower one).
  *
- * The search is level-synchronous (breadth-first, which the paper also names): one
- * av_search_expand steps every (frontier node, action) pair of the level as one batch with
- * the step engines above.  Level d:
+ * Two orders.  Level order (best_first_k = 0; breadth-first, which the paper also names):
+ * one av_search_expand steps every (frontier node, action) pair of the level as one batch
+ * with the step engines above.  Batched best-first (best_first_k = k >= 1; the paper's
+ * fitness search prioritises higher reward): open nodes are ordered by higher reward, then
+ * smaller depth, then smaller node id (the root is node 0, kept children get the next ids in
+ * child order); one av_search_expand pops the first k open nodes, drops those whose state
+ * has since been reached with a better (reward, -depth), and expands the rest, in id order,
+ * exactly like one level below; the kept children are opened.  k = 1 is plain best-first.
+ * Level d (or one best-first iteration):
  *   - children: frontier nodes in order, for each the actions in order (0..4, or 1..4 with
  *     num_actions = 4), cut to max_children; child i of a level is visit number
  *     visited + 1 + i (the root is visit 0);
@@ -276,9 +282,11 @@ typedef struct {
     int32_t max_rules, max_pat_h, max_pat_w;
     int32_t max_episode_steps;         /* L >= 0; 0 = episodes end only without a player */
     int32_t num_actions;               /* 5 (actions 0..4) or 4 (actions 1..4) */
-    int32_t max_frontier;              /* most nodes kept per level, in [1, 2^24] */
+    int32_t max_frontier;              /* level order: most nodes kept per level, [1, 2^24] */
     int32_t table_log2;                /* hash table of 2^table_log2 slots, in [4, 31] */
     int32_t device, engine, rule_mode; /* as av_config; engine AUTO picks as for a batch */
+    int32_t best_first_k;              /* 0: level order; k in [1, 512]: batched best-first */
+    int32_t max_nodes;                 /* best-first: node pool capacity, in [1, 2^26] */
     void *stream;                      /* hipStream_t; NULL = null stream */
 } av_search_config;
 
@@ -288,7 +296,7 @@ typedef struct {
     int64_t children;       /* states visited (stepped) by this call */
     int64_t terminal;       /* of them, episode ends */
     int64_t survivors;      /* new or improved states, before the max_frontier cut */
-    int64_t frontier;       /* nodes in the frontier now */
+    int64_t frontier;       /* nodes in the frontier now (best-first: open nodes) */
     int64_t visited;        /* states visited since av_search_begin */
     int64_t best_visit;     /* visit number of the best node (0 = the root) */
     int32_t best_reward;    /* its accumulated reward */
@@ -314,12 +322,13 @@ av_status av_search_begin(av_search_t s, const uint8_t *root);
  * An empty frontier or max_children = 0 expands nothing and keeps the frontier.  A search
  * visits at most 2^32 - 2 states (AV_EINVAL beyond).
  * Synchronises (the next level's size is needed on the host).  AV_ENOMEM when an insertion
- * finds 4096 consecutive slots taken by other keys (the table is too full): the search must
- * then be restarted with av_search_begin. */
+ * finds 4096 consecutive slots taken by other keys (the table is too full) or, best-first,
+ * when the node pool is full: the search must then be restarted with av_search_begin. */
 av_status av_search_expand(av_search_t s, int64_t max_children, av_search_info *info);
 
-/* The current frontier: maps device uint8 [N][C][H][W], reward and depth device int32 [N],
- * N = info.frontier; any pointer may be NULL to skip it.  Asynchronous. */
+/* The current frontier (level order) or the open list in priority order (best-first):
+ * maps device uint8 [N][C][H][W], reward and depth device int32 [N], N = info.frontier; any
+ * pointer may be NULL to skip it.  Asynchronous. */
 av_status av_search_frontier(av_search_t s, uint8_t *maps, int32_t *reward, int32_t *depth);
 
 /* Free the search; NULL is a no-op.  Synchronises. */

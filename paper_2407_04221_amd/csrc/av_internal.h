@@ -159,11 +159,33 @@ struct SearchArgs {
     int32_t *block_count = nullptr;                // [ceil(n / 256)]
     int32_t *src_of = nullptr;                     // [cap] child of each next-frontier node
     int32_t *next_reward = nullptr, *next_depth = nullptr;           // [cap]
-    void *next = nullptr;                          // next frontier rows [C][nn][H]
+    void *next = nullptr;                          // next frontier rows [C][next_n][H]
+    int32_t next_n = 0, next_off = 0;              // its block count and first block written
+    int64_t *root_slot = nullptr;                  // root_kernel: the root's table slot
 };
 // phase 0 gather, 1 post/claim/flag/scan/place, 2 copy rows (nn nodes), 3 root insert.
 hipError_t launch_search_phase(const SearchArgs &a, int row_bytes, const void *front, int nf,
                                void *kids, int32_t *kid_t, hipStream_t s, int phase, int nn);
+
+// Batched best-first pieces (k_search.hip).
+hipError_t launch_copy_rows(int row_bytes, const void *src, int nsrc, const int32_t *src_of,
+                            void *dst, int ndst, int off, int n, int C, int H, hipStream_t s);
+hipError_t launch_bf_pop(const uint32_t *open_ids, int kp, const int64_t *pool_slot,
+                         const uint64_t *pool_val, const uint64_t *vals, int32_t *parents,
+                         uint32_t *n_par, hipStream_t s);
+hipError_t launch_bf_gather_meta(const int32_t *parents, int np, const int32_t *pool_reward,
+                                 const int32_t *pool_depth, int32_t *front_reward,
+                                 int32_t *front_depth, hipStream_t s);
+hipError_t launch_bf_append(const int32_t *src_of, int nn, int pool_n, const uint64_t *kid_val,
+                            const int64_t *slot, uint64_t *pool_val, int64_t *pool_slot,
+                            uint64_t *new_keys, uint32_t *new_ids, hipStream_t s);
+hipError_t launch_bf_merge(const uint64_t *ok, const uint32_t *oi, int m, const uint64_t *nk,
+                           const uint32_t *ni, int nn, uint64_t *outk, uint32_t *outi,
+                           hipStream_t s);
+hipError_t launch_bf_open(int row_bytes, const void *pool, int pcap, const uint32_t *ids, int n,
+                          int C, int H, int W, uint8_t *maps, const int32_t *pool_reward,
+                          const int32_t *pool_depth, int32_t *reward, int32_t *depth,
+                          hipStream_t s);
 
 // Internal access to a batch for the search (av_api.cpp).
 void *batch_state(av_batch_t b);

@@ -35,6 +35,16 @@ struct av_search_s {
     uint32_t *epoch = nullptr, *counts = nullptr;
     bool have_rules = false, begun = false;
     int64_t level = 0, visited = 0;
+    // batched best-first (K > 0): node pool, open list (value, id) sorted, popped parents
+    int K = 0;
+    int64_t pcap = 0, pool_n = 0, open_n = 0;
+    void *pool = nullptr;
+    int32_t *pool_reward = nullptr, *pool_depth = nullptr, *parents = nullptr;
+    uint64_t *pool_val = nullptr, *new_keys = nullptr;
+    int64_t *pool_slot = nullptr;
+    uint64_t *okeys[2] = {nullptr, nullptr};
+    uint32_t *oids[2] = {nullptr, nullptr}, *new_ids = nullptr, *n_par = nullptr;
+    int ocur = 0;
 };
 
 namespace {
@@ -58,7 +68,9 @@ void release(av_search_t s) {
     void *ptrs[] = {s->front[0], s->front[1], s->reward[0], s->reward[1], s->depth[0], s->depth[1],
                     s->actions, s->rew, s->done, s->kid_reward, s->kid_depth, s->block_count,
                     s->src_of, s->kid_val, s->slot, s->keys, s->vals, s->claim, s->best, s->epoch,
-                    s->counts};
+                    s->counts, s->pool, s->pool_reward, s->pool_depth, s->parents, s->pool_val,
+                    s->new_keys, s->pool_slot, s->okeys[0], s->okeys[1], s->oids[0], s->oids[1],
+                    s->new_ids, s->n_par};
     for (void *p : ptrs)
         if (p) (void)hipFree(p);
     if (s->kids) av_destroy_batch(s->kids);
@@ -106,8 +118,13 @@ av_status av_search_create(const av_search_config *cfg, av_search_t *out) {
         return set_error(AV_EINVAL, "max_frontier must be in [1, 2^24]");
     if (c.table_log2 < 4 || c.table_log2 > 31)
         return set_error(AV_EINVAL, "table_log2 must be in [4, 31]");
+    if (c.best_first_k < 0 || c.best_first_k > 512)
+        return set_error(AV_EINVAL, "best_first_k must be in [0, 512]");
+    if (c.best_first_k > 0 && (c.max_nodes < 1 || c.max_nodes > (1 << 26)))
+        return set_error(AV_EINVAL, "max_nodes must be in [1, 2^26]");
+    const int fcap = c.best_first_k > 0 ? c.best_first_k : c.max_frontier;   // parents per level
     av_config bc{};
-    bc.num_envs = c.num_actions * c.max_frontier;
+    bc.num_envs = c.num_actions * fcap;
     bc.height = c.height; bc.width = c.width; bc.channels = c.channels;
     bc.max_rules = c.max_rules; bc.max_pat_h = c.max_pat_h; bc.max_pat_w = c.max_pat_w;
     bc.per_env_rules = 0; bc.max_episode_steps = c.max_episode_steps;
@@ -124,7 +141,8 @@ av_status av_search_create(const av_search_config *cfg, av_search_t *out) {
     s->kids = kids;
     s->row_bytes = batch_row_bytes(kids);
     s->A = c.num_actions;
-    s->cap = c.max_frontier;
+    s->cap = fcap;
+    s->K = c.best_first_k;
     s->slots = uint64_t(1) << c.table_log2;
     const size_t nk = size_t(s->A) * s->cap;
     const size_t fbytes = size_t(c.channels) * s->cap * c.height * s->row_bytes;
@@ -142,13 +160,30 @@ av_status av_search_create(const av_search_config *cfg, av_search_t *out) {
     if (e == hipSuccess) e = alloc(&s->kid_val, nk);
     if (e == hipSuccess) e = alloc(&s->slot, nk);
     if (e == hipSuccess) e = alloc(&s->block_count, (nk + 255) / 256);
-    if (e == hipSuccess) e = alloc(&s->src_of, s->cap);
+    if (e == hipSuccess) e = alloc(&s->src_of, nk);      // survivors of one level: <= children
     if (e == hipSuccess) e = alloc(&s->keys, s->slots);
     if (e == hipSuccess) e = alloc(&s->vals, s->slots);
     if (e == hipSuccess) e = alloc(&s->claim, s->slots);
     if (e == hipSuccess) e = alloc(&s->epoch, s->slots);
     if (e == hipSuccess) e = alloc(&s->best, 1);
     if (e == hipSuccess) e = alloc(&s->counts, 3);
+    if (e == hipSuccess && s->K > 0) {
+        s->pcap = c.max_nodes;
+        const size_t pbytes = size_t(c.channels) * s->pcap * c.height * s->row_bytes;
+        e = hipMalloc(&s->pool, pbytes);
+        if (e == hipSuccess) e = alloc(&s->pool_reward, s->pcap);
+        if (e == hipSuccess) e = alloc(&s->pool_depth, s->pcap);
+        if (e == hipSuccess) e = alloc(&s->pool_val, s->pcap);
+        if (e == hipSuccess) e = alloc(&s->pool_slot, s->pcap);
+        for (int k = 0; k < 2 && e == hipSuccess; ++k) {
+            e = alloc(&s->okeys[k], s->pcap);
+            if (e == hipSuccess) e = alloc(&s->oids[k], s->pcap);
+        }
+        if (e == hipSuccess) e = alloc(&s->new_keys, nk);
+        if (e == hipSuccess) e = alloc(&s->new_ids, nk);
+        if (e == hipSuccess) e = alloc(&s->parents, 512);
+        if (e == hipSuccess) e = alloc(&s->n_par, 1);
+    }
     if (e == hipSuccess) {
         std::vector<uint8_t> acts(nk);
         for (size_t i = 0; i < nk; ++i) acts[i] = uint8_t(i % s->A + (s->A == 4 ? 1 : 0));
@@ -191,14 +226,116 @@ av_status av_search_begin(av_search_t s, const uint8_t *root) {
     SEARCH_HIP(hipMemsetAsync(s->epoch, 0, s->slots * sizeof(uint32_t), s->stream));
     SEARCH_HIP(hipMemsetAsync(s->counts, 0, 3 * sizeof(uint32_t), s->stream));
     SearchArgs a = level_args(s, 1);
+    if (s->K > 0) a.root_slot = s->pool_slot;            // the root is pool node 0
     SEARCH_HIP(launch_search_phase(a, s->row_bytes, s->front[0], 1, nullptr, nullptr, s->stream, 3,
                                    0));
+    if (s->K > 0) {
+        const uint64_t v0 = (uint64_t(0x80000000u) << 32) | 0xFFFFFFFFull;   // (reward 0, depth 0)
+        SEARCH_HIP(hipMemsetAsync(s->parents, 0, sizeof(int32_t), s->stream));
+        SEARCH_HIP(launch_copy_rows(s->row_bytes, s->front[0], 1, s->parents, s->pool, int(s->pcap),
+                                    0, 1, c.channels, c.height, s->stream));
+        SEARCH_HIP(hipMemsetAsync(s->pool_reward, 0, sizeof(int32_t), s->stream));
+        SEARCH_HIP(hipMemsetAsync(s->pool_depth, 0, sizeof(int32_t), s->stream));
+        SEARCH_HIP(hipMemcpyAsync(s->pool_val, &v0, sizeof v0, hipMemcpyHostToDevice, s->stream));
+        SEARCH_HIP(hipMemcpyAsync(s->okeys[0], &v0, sizeof v0, hipMemcpyHostToDevice, s->stream));
+        SEARCH_HIP(hipMemsetAsync(s->oids[0], 0, sizeof(uint32_t), s->stream));
+        SEARCH_HIP(hipStreamSynchronize(s->stream));      // v0 lives on this stack frame
+        s->ocur = 0;
+        s->pool_n = 1;
+        s->open_n = 1;
+    }
     s->n_front = 1;
     s->level = 0;
     s->visited = 0;
     s->begun = true;
     return AV_OK;
 }
+
+namespace {
+
+// One iteration of batched best-first (av_search_expand with best_first_k > 0).
+av_status expand_best_first(av_search_t s, int64_t max_children, av_search_info *info) {
+    const av_search_config &c = s->cfg;
+    info->parents = 0;
+    const int kp = int(std::min<int64_t>(s->K, s->open_n));
+    if (kp == 0 || max_children == 0) {
+        info->level = s->level;
+        info->frontier = s->open_n;
+        info->visited = s->visited;
+        return read_best(s, info);
+    }
+    uint32_t npar = 0;
+    SEARCH_HIP(launch_bf_pop(s->oids[s->ocur], kp, s->pool_slot, s->pool_val, s->vals, s->parents,
+                             s->n_par, s->stream));
+    SEARCH_HIP(hipMemcpyAsync(&npar, s->n_par, sizeof npar, hipMemcpyDeviceToHost, s->stream));
+    SEARCH_HIP(hipStreamSynchronize(s->stream));
+    const int64_t n = std::min<int64_t>(int64_t(s->A) * npar, max_children);
+    if (s->visited + n > int64_t(0xFFFFFFFEll))
+        return set_error(AV_EINVAL, "a search may visit at most 2^32 - 2 states");
+    int64_t nn = 0;
+    uint32_t counts[3] = {0, 0, 0};
+    if (n > 0) {
+        s->cur = 0;
+        SEARCH_HIP(launch_copy_rows(s->row_bytes, s->pool, int(s->pcap), s->parents, s->front[0],
+                                    int(npar), 0, int(npar), c.channels, c.height, s->stream));
+        SEARCH_HIP(launch_bf_gather_meta(s->parents, int(npar), s->pool_reward, s->pool_depth,
+                                         s->reward[0], s->depth[0], s->stream));
+        SearchArgs a = level_args(s, int(n));
+        a.cap = int(s->pcap - s->pool_n);
+        a.next_reward = s->pool_reward + s->pool_n;
+        a.next_depth = s->pool_depth + s->pool_n;
+        void *kst = batch_state(s->kids);
+        SEARCH_HIP(hipMemsetAsync(s->counts, 0, 3 * sizeof(uint32_t), s->stream));
+        if (batch_engine(s->kids) == AV_ENGINE_LANE16) {
+            if (av_status st = step_prefix(s->kids, int(n), s->actions, s->rew, s->done,
+                                           s->front[0], int(npar), s->A, s->depth[0]))
+                return st;
+        } else {
+            SEARCH_HIP(launch_search_phase(a, s->row_bytes, s->front[0], int(npar), kst,
+                                           batch_counters(s->kids), s->stream, 0, 0));
+            if (av_status st = step_prefix(s->kids, int(n), s->actions, s->rew, s->done)) return st;
+        }
+        SEARCH_HIP(launch_search_phase(a, s->row_bytes, s->front[0], int(npar), kst, nullptr,
+                                       s->stream, 1, 0));
+        SEARCH_HIP(hipMemcpyAsync(counts, s->counts, sizeof counts, hipMemcpyDeviceToHost,
+                                  s->stream));
+        SEARCH_HIP(hipStreamSynchronize(s->stream));
+        if (counts[1] || int64_t(counts[2]) > s->pcap - s->pool_n) {
+            s->begun = false;
+            return set_error(AV_ENOMEM, counts[1]
+                                            ? "search table too full (an insertion probed 4096 "
+                                              "slots); use a larger table_log2 and call "
+                                              "av_search_begin again"
+                                            : "best-first node pool full; use a larger max_nodes "
+                                              "and call av_search_begin again");
+        }
+        nn = counts[2];
+        SEARCH_HIP(launch_copy_rows(s->row_bytes, kst, int(n), s->src_of, s->pool, int(s->pcap),
+                                    int(s->pool_n), int(nn), c.channels, c.height, s->stream));
+        SEARCH_HIP(launch_bf_append(s->src_of, int(nn), int(s->pool_n), s->kid_val, s->slot,
+                                    s->pool_val, s->pool_slot, s->new_keys, s->new_ids,
+                                    s->stream));
+        s->pool_n += nn;
+    }
+    const int64_t m = s->open_n - kp;
+    SEARCH_HIP(launch_bf_merge(s->okeys[s->ocur] + kp, s->oids[s->ocur] + kp, int(m), s->new_keys,
+                               s->new_ids, int(nn), s->okeys[1 - s->ocur], s->oids[1 - s->ocur],
+                               s->stream));
+    s->ocur = 1 - s->ocur;
+    s->open_n = m + nn;
+    s->visited += n;
+    s->level += 1;
+    info->parents = npar;
+    info->children = n;
+    info->terminal = counts[0];
+    info->survivors = nn;
+    info->level = s->level;
+    info->frontier = s->open_n;
+    info->visited = s->visited;
+    return read_best(s, info);
+}
+
+}  // namespace
 
 av_status av_search_expand(av_search_t s, int64_t max_children, av_search_info *info) {
     if (!s) return set_error(AV_EINVAL, "search handle is NULL");
@@ -207,6 +344,7 @@ av_status av_search_expand(av_search_t s, int64_t max_children, av_search_info *
     if (!s->begun) return set_error(AV_ESTATE, "call av_search_begin first");
     SEARCH_HIP(hipSetDevice(s->cfg.device));
     *info = av_search_info{};
+    if (s->K > 0) return expand_best_first(s, max_children, info);
     info->parents = s->n_front;
     const int64_t n = std::min<int64_t>(int64_t(s->A) * s->n_front, max_children);
     if (s->visited + n > int64_t(0xFFFFFFFEll))
@@ -239,6 +377,8 @@ av_status av_search_expand(av_search_t s, int64_t max_children, av_search_info *
                                         "use a larger table_log2 and call av_search_begin again");
         }
         const int64_t nn = std::min<int64_t>(counts[2], s->cap);
+        a.next_n = int(nn);
+        a.next_off = 0;
         SEARCH_HIP(launch_search_phase(a, s->row_bytes, s->front[s->cur], int(s->n_front), kst,
                                        nullptr, s->stream, 2, int(nn)));
         s->cur = 1 - s->cur;
@@ -261,6 +401,12 @@ av_status av_search_frontier(av_search_t s, uint8_t *maps, int32_t *reward, int3
     if (!s->begun) return set_error(AV_ESTATE, "call av_search_begin first");
     const av_search_config &c = s->cfg;
     SEARCH_HIP(hipSetDevice(c.device));
+    if (s->K > 0) {
+        SEARCH_HIP(launch_bf_open(s->row_bytes, s->pool, int(s->pcap), s->oids[s->ocur],
+                                  int(s->open_n), c.channels, c.height, c.width, maps,
+                                  s->pool_reward, s->pool_depth, reward, depth, s->stream));
+        return AV_OK;
+    }
     const int n = int(s->n_front);
     if (n == 0) return AV_OK;
     if (maps)

@@ -72,10 +72,11 @@ __device__ inline uint64_t map_hash(const void *state, int i, int n, int C, int 
 // Copy environment blocks (one channel's H rows) 16 bytes per thread: destination block
 // (c, i) of a [C][n][H] buffer comes from source block (c, from(i)) of a [C][nsrc][H] buffer,
 // with from(i) = i / A (parents of the children) or src_of[i] (survivors).
+// The destination is a [C][ndst][H] buffer written at blocks off .. off + n - 1.
 __global__ void __launch_bounds__(256) copy16_kernel(const uint4 *src, int nsrc, uint4 *dst, int n,
                                                      int C, int chunks, int A,
                                                      const int32_t *src_of, int32_t *kid_t,
-                                                     const int32_t *fdepth) {
+                                                     const int32_t *fdepth, int ndst, int off) {
     const size_t t = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (kid_t && t < size_t(n)) kid_t[t] = fdepth[t / A];
     if (t >= size_t(C) * n * chunks) return;
@@ -83,7 +84,7 @@ __global__ void __launch_bounds__(256) copy16_kernel(const uint4 *src, int nsrc,
     const size_t ci = t / chunks;
     const int i = int(ci % n), c = int(ci / n);
     const int from = src_of ? src_of[i] : i / A;
-    dst[t] = src[(size_t(c) * nsrc + from) * chunks + k];
+    dst[(size_t(c) * ndst + off + i) * chunks + k] = src[(size_t(c) * nsrc + from) * chunks + k];
 }
 
 __device__ inline uint64_t pack_value(int32_t reward, int32_t depth) {
@@ -234,15 +235,18 @@ __global__ void __launch_bounds__(256) place_kernel(SearchArgs a, int cap) {
     a.next_depth[pos] = a.kid_depth[i];
 }
 
+// Rows of blocks src_of[q] of a [C][n][H] buffer into blocks off + q of a [C][ndst][H] one.
 template <typename RowT>
 __global__ void __launch_bounds__(256) copy_kernel(const void *kids, int n, void *next, int nn,
-                                                   const int32_t *src_of, int C, int H) {
+                                                   const int32_t *src_of, int C, int H, int ndst,
+                                                   int off) {
     const size_t r = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (r >= size_t(C) * nn * H) return;
     const int y = int(r % H);
     const size_t cq = r / H;
     const int q = int(cq % nn), c = int(cq / nn);
-    static_cast<RowT *>(next)[r] = static_cast<const RowT *>(kids)[(size_t(c) * n + src_of[q]) * H + y];
+    static_cast<RowT *>(next)[(size_t(c) * ndst + off + q) * H + y] =
+        static_cast<const RowT *>(kids)[(size_t(c) * n + src_of[q]) * H + y];
 }
 
 template <typename RowT>
@@ -253,6 +257,179 @@ __global__ void root_kernel(SearchArgs a, const void *front) {
     if (s < 0) { a.counts[1] = 1; return; }
     a.vals[s] = pack_value(0, 0);
     *a.best = (uint64_t(0x80000000u) << 32) | 0xFFFFFFFFull;
+    if (a.root_slot) *a.root_slot = s;
+}
+
+// ---------------------------------------------------------------------------------------
+// Batched best-first (av_search_config.best_first_k > 0).  Nodes live in a pool ([C][P][H]
+// rows plus reward, depth, packed (reward, -depth) value and table slot per node id); the
+// open list holds (value, id) pairs sorted by value descending, ties by id ascending.  An
+// iteration pops its first k entries, keeps those whose value is still their slot's value
+// (the others were beaten by a later copy of their state), expands them in id order with the
+// level kernels above, appends the survivors to the pool with the next ids, sorts them, and
+// merges them into the rest of the open list.
+
+// In-block exclusive prefix of 0/1 flags for any multiple of 64 threads (up to 1024).
+__device__ inline int block_prefix_any(int flag, int *sums, int &prefix) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    const uint64_t ballot = __ballot(flag);
+    const int in_wave = __popcll(ballot & ((lane ? (~0ull >> (64 - lane)) : 0ull)));
+    if (lane == 0) sums[wave] = __popcll(ballot);
+    __syncthreads();
+    int before = 0, total = 0;
+    for (int w = 0; w < nw; ++w) {
+        if (w < wave) before += sums[w];
+        total += sums[w];
+    }
+    prefix = before + in_wave;
+    return total;
+}
+
+// Pop: the first kp open ids, sorted ascending (bitonic, 512 slots), those still alive
+// compacted into parents[]; *n_par = their number.  One workgroup of 512 threads.
+__global__ void __launch_bounds__(512) bf_pop_kernel(const uint32_t *open_ids, int kp,
+                                                     const int64_t *pool_slot,
+                                                     const uint64_t *pool_val,
+                                                     const uint64_t *vals, int32_t *parents,
+                                                     uint32_t *n_par) {
+    __shared__ uint32_t ids[512];
+    __shared__ int sums[8];
+    const int t = threadIdx.x;
+    ids[t] = t < kp ? open_ids[t] : 0xFFFFFFFFu;
+    __syncthreads();
+    for (int k = 2; k <= 512; k <<= 1)
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            const int o = t ^ j;
+            if (o > t) {
+                const uint32_t a = ids[t], b = ids[o];
+                const bool up = (t & k) == 0;
+                if ((a > b) == up) {
+                    ids[t] = b;
+                    ids[o] = a;
+                }
+            }
+            __syncthreads();
+        }
+    const uint32_t id = ids[t];
+    const int alive = id != 0xFFFFFFFFu && vals[pool_slot[id]] == pool_val[id];
+    int prefix;
+    const int total = block_prefix_any(alive, sums, prefix);
+    if (alive) parents[prefix] = int32_t(id);
+    if (t == 0) *n_par = uint32_t(total);
+}
+
+__global__ void __launch_bounds__(256) bf_gather_meta(const int32_t *parents, int np,
+                                                      const int32_t *pool_reward,
+                                                      const int32_t *pool_depth,
+                                                      int32_t *front_reward, int32_t *front_depth) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= np) return;
+    front_reward[i] = pool_reward[parents[i]];
+    front_depth[i] = pool_depth[parents[i]];
+}
+
+// New nodes pool_n + q (q < nn) from survivor children src_of[q]: value and slot, and the
+// (value, id) pairs to sort.  Reward and depth were written by place_kernel.
+__global__ void __launch_bounds__(256) bf_append_meta(const int32_t *src_of, int nn, int pool_n,
+                                                      const uint64_t *kid_val, const int64_t *slot,
+                                                      uint64_t *pool_val, int64_t *pool_slot,
+                                                      uint64_t *new_keys, uint32_t *new_ids) {
+    const int q = blockIdx.x * blockDim.x + threadIdx.x;
+    if (q >= nn) return;
+    const int i = src_of[q];
+    pool_val[pool_n + q] = kid_val[i];
+    pool_slot[pool_n + q] = slot[i];
+    new_keys[q] = kid_val[i];
+    new_ids[q] = uint32_t(pool_n + q);
+}
+
+// Sort nn <= 4096 (value, id) pairs: value descending, id ascending (bitonic in LDS).
+__global__ void __launch_bounds__(1024) bf_sort_kernel(uint64_t *keys, uint32_t *ids, int nn) {
+    __shared__ uint64_t k_[4096];
+    __shared__ uint32_t i_[4096];
+    int P = 1;
+    while (P < nn) P <<= 1;
+    for (int t = threadIdx.x; t < P; t += blockDim.x) {
+        k_[t] = t < nn ? keys[t] : 0ull;
+        i_[t] = t < nn ? ids[t] : 0xFFFFFFFFu;
+    }
+    __syncthreads();
+    for (int k = 2; k <= P; k <<= 1)
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            for (int t = threadIdx.x; t < P; t += blockDim.x) {
+                const int o = t ^ j;
+                if (o > t) {
+                    // "a before b": larger value, or equal value and smaller id
+                    const bool b_first = k_[o] > k_[t] || (k_[o] == k_[t] && i_[o] < i_[t]);
+                    const bool up = (t & k) == 0;
+                    if (b_first == up) {
+                        const uint64_t kk = k_[t];
+                        k_[t] = k_[o];
+                        k_[o] = kk;
+                        const uint32_t ii = i_[t];
+                        i_[t] = i_[o];
+                        i_[o] = ii;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+    for (int t = threadIdx.x; t < nn; t += blockDim.x) {
+        keys[t] = k_[t];
+        ids[t] = i_[t];
+    }
+}
+
+// Merge the old open list (m pairs) with the sorted new pairs (nn) into out: old entries
+// come before new ones of equal value (their ids are smaller).
+__global__ void __launch_bounds__(256) bf_merge_kernel(const uint64_t *ok, const uint32_t *oi, int m,
+                                                       const uint64_t *nk, const uint32_t *ni, int nn,
+                                                       uint64_t *outk, uint32_t *outi) {
+    const int t = blockIdx.x * blockDim.x + threadIdx.x;
+    if (t < m) {
+        const uint64_t key = ok[t];
+        int lo = 0, hi = nn;                       // new entries with a larger value
+        while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if (nk[mid] > key) lo = mid + 1; else hi = mid;
+        }
+        outk[t + lo] = key;
+        outi[t + lo] = oi[t];
+    } else if (t < m + nn) {
+        const int q = t - m;
+        const uint64_t key = nk[q];
+        int lo = 0, hi = m;                        // old entries with a value >= this one
+        while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if (ok[mid] >= key) lo = mid + 1; else hi = mid;
+        }
+        outk[q + lo] = key;
+        outi[q + lo] = ni[q];
+    }
+}
+
+template <typename RowT>
+__global__ void __launch_bounds__(256) bf_unpack_kernel(const void *pool, int pcap,
+                                                        const uint32_t *ids, int n, int C, int H,
+                                                        int W, uint8_t *maps) {
+    const size_t r = size_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (r >= size_t(n) * C * H) return;
+    const int y = int(r % H);
+    const size_t qc = r / H;
+    const int c = int(qc % C), q = int(qc / C);
+    const uint64_t v = uint64_t(static_cast<const RowT *>(pool)[(size_t(c) * pcap + ids[q]) * H + y]);
+    uint8_t *o = maps + r * W;
+    for (int x = 0; x < W; ++x) o[x] = uint8_t((v >> x) & 1u);
+}
+
+__global__ void __launch_bounds__(256) bf_open_meta(const uint32_t *ids, int n,
+                                                    const int32_t *pool_reward,
+                                                    const int32_t *pool_depth, int32_t *reward,
+                                                    int32_t *depth) {
+    const int q = blockIdx.x * blockDim.x + threadIdx.x;
+    if (q >= n) return;
+    if (reward) reward[q] = pool_reward[ids[q]];
+    if (depth) depth[q] = pool_depth[ids[q]];
 }
 
 unsigned blocks_for(size_t threads) { return unsigned((threads + 255) / 256); }
@@ -269,7 +446,7 @@ hipError_t level_impl(const SearchArgs &a, const void *front, int nf, void *kids
             hipLaunchKernelGGL(copy16_kernel, dim3(blocks_for(threads)), dim3(256), 0, s,
                                static_cast<const uint4 *>(front), nf, static_cast<uint4 *>(kids),
                                a.n, a.C, chunks, a.A, static_cast<const int32_t *>(nullptr),
-                               kid_t, a.front_depth);
+                               kid_t, a.front_depth, a.n, 0);
         } else {
             const size_t rows = std::max(size_t(a.C) * a.n * a.H, size_t(a.n));
             hipLaunchKernelGGL(gather_kernel<RowT>, dim3(blocks_for(rows)), dim3(256), 0, s, front,
@@ -290,17 +467,106 @@ hipError_t level_impl(const SearchArgs &a, const void *front, int nf, void *kids
                                static_cast<uint4 *>(a.next), nn, a.C, chunks, 1,
                                static_cast<const int32_t *>(a.src_of),
                                static_cast<int32_t *>(nullptr),
-                               static_cast<const int32_t *>(nullptr));
+                               static_cast<const int32_t *>(nullptr), a.next_n, a.next_off);
         else if (nn > 0)
             hipLaunchKernelGGL(copy_kernel<RowT>, dim3(blocks_for(size_t(a.C) * nn * a.H)), dim3(256),
-                               0, s, kids, a.n, a.next, nn, a.src_of, a.C, a.H);
+                               0, s, kids, a.n, a.next, nn, a.src_of, a.C, a.H, a.next_n,
+                               a.next_off);
     } else {
         hipLaunchKernelGGL(root_kernel<RowT>, dim3(1), dim3(64), 0, s, a, front);
     }
     return hipGetLastError();
 }
 
+template <typename RowT>
+hipError_t copy_rows(const void *src, int nsrc, const int32_t *src_of, void *dst, int ndst,
+                     int off, int n, int C, int H, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    const int block_bytes = H * int(sizeof(RowT));
+    if (block_bytes % 16 == 0) {
+        const int chunks = block_bytes / 16;
+        hipLaunchKernelGGL(copy16_kernel, dim3(blocks_for(size_t(C) * n * chunks)), dim3(256), 0, s,
+                           static_cast<const uint4 *>(src), nsrc, static_cast<uint4 *>(dst), n, C,
+                           chunks, 1, src_of, static_cast<int32_t *>(nullptr),
+                           static_cast<const int32_t *>(nullptr), ndst, off);
+    } else {
+        hipLaunchKernelGGL(copy_kernel<RowT>, dim3(blocks_for(size_t(C) * n * H)), dim3(256), 0, s,
+                           src, nsrc, dst, n, src_of, C, H, ndst, off);
+    }
+    return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t launch_copy_rows(int row_bytes, const void *src, int nsrc, const int32_t *src_of,
+                            void *dst, int ndst, int off, int n, int C, int H, hipStream_t s) {
+    if (row_bytes == 2) return copy_rows<uint16_t>(src, nsrc, src_of, dst, ndst, off, n, C, H, s);
+    if (row_bytes == 4) return copy_rows<uint32_t>(src, nsrc, src_of, dst, ndst, off, n, C, H, s);
+    return copy_rows<uint64_t>(src, nsrc, src_of, dst, ndst, off, n, C, H, s);
+}
+
+hipError_t launch_bf_pop(const uint32_t *open_ids, int kp, const int64_t *pool_slot,
+                         const uint64_t *pool_val, const uint64_t *vals, int32_t *parents,
+                         uint32_t *n_par, hipStream_t s) {
+    hipLaunchKernelGGL(bf_pop_kernel, dim3(1), dim3(512), 0, s, open_ids, kp, pool_slot, pool_val,
+                       vals, parents, n_par);
+    return hipGetLastError();
+}
+
+hipError_t launch_bf_gather_meta(const int32_t *parents, int np, const int32_t *pool_reward,
+                                 const int32_t *pool_depth, int32_t *front_reward,
+                                 int32_t *front_depth, hipStream_t s) {
+    if (np <= 0) return hipSuccess;
+    hipLaunchKernelGGL(bf_gather_meta, dim3(blocks_for(size_t(np))), dim3(256), 0, s, parents, np,
+                       pool_reward, pool_depth, front_reward, front_depth);
+    return hipGetLastError();
+}
+
+hipError_t launch_bf_append(const int32_t *src_of, int nn, int pool_n, const uint64_t *kid_val,
+                            const int64_t *slot, uint64_t *pool_val, int64_t *pool_slot,
+                            uint64_t *new_keys, uint32_t *new_ids, hipStream_t s) {
+    if (nn <= 0) return hipSuccess;
+    hipLaunchKernelGGL(bf_append_meta, dim3(blocks_for(size_t(nn))), dim3(256), 0, s, src_of, nn,
+                       pool_n, kid_val, slot, pool_val, pool_slot, new_keys, new_ids);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(bf_sort_kernel, dim3(1), dim3(1024), 0, s, new_keys, new_ids, nn);
+    return hipGetLastError();
+}
+
+hipError_t launch_bf_merge(const uint64_t *ok, const uint32_t *oi, int m, const uint64_t *nk,
+                           const uint32_t *ni, int nn, uint64_t *outk, uint32_t *outi,
+                           hipStream_t s) {
+    if (m + nn <= 0) return hipSuccess;
+    hipLaunchKernelGGL(bf_merge_kernel, dim3(blocks_for(size_t(m) + nn)), dim3(256), 0, s, ok, oi, m,
+                       nk, ni, nn, outk, outi);
+    return hipGetLastError();
+}
+
+hipError_t launch_bf_open(int row_bytes, const void *pool, int pcap, const uint32_t *ids, int n,
+                          int C, int H, int W, uint8_t *maps, const int32_t *pool_reward,
+                          const int32_t *pool_depth, int32_t *reward, int32_t *depth,
+                          hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    if (maps) {
+        const unsigned nb = blocks_for(size_t(n) * C * H);
+        if (row_bytes == 2)
+            hipLaunchKernelGGL(bf_unpack_kernel<uint16_t>, dim3(nb), dim3(256), 0, s, pool, pcap, ids,
+                               n, C, H, W, maps);
+        else if (row_bytes == 4)
+            hipLaunchKernelGGL(bf_unpack_kernel<uint32_t>, dim3(nb), dim3(256), 0, s, pool, pcap, ids,
+                               n, C, H, W, maps);
+        else
+            hipLaunchKernelGGL(bf_unpack_kernel<uint64_t>, dim3(nb), dim3(256), 0, s, pool, pcap, ids,
+                               n, C, H, W, maps);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (reward || depth)
+        hipLaunchKernelGGL(bf_open_meta, dim3(blocks_for(size_t(n))), dim3(256), 0, s, ids, n,
+                           pool_reward, pool_depth, reward, depth);
+    return hipGetLastError();
+}
 
 hipError_t launch_search_phase(const SearchArgs &a, int row_bytes, const void *front, int nf,
                                void *kids, int32_t *kid_t, hipStream_t s, int phase, int nn) {

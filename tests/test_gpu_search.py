@@ -105,3 +105,94 @@ def test_search_table_overflow_is_an_error():
         assert g.expand(5)["children"] == 5
     finally:
         g.close()
+
+
+def compare_best_first(wl, root, rules, budget, iters, k, A=5, L=None, engine="auto",
+                       rule_mode="parallel", max_nodes=1 << 16, table_log2=18):
+    L = wl.L if L is None else L
+    mode = int(rule_mode == "sequential")
+    o = osearch.BestFirst(wl.H, wl.W, wl.C, rules, L, k=k, num_actions=A, rule_mode=mode)
+    g = av.Search(wl.H, wl.W, wl.C, wl.R, wl.max_h, wl.max_w, L, num_actions=A,
+                  table_log2=table_log2, engine=engine, rule_mode=rule_mode, best_first_k=k,
+                  max_nodes=max_nodes)
+    try:
+        g.load_rules(*rules)
+        o.begin(root)
+        g.begin(root)
+        want = None
+        for it in range(iters):
+            left = budget - o.visited
+            want = o.expand(left)
+            got = g.expand(left)
+            assert got == want, f"iteration {it + 1}: {got} != {want}"
+            gm, gr, gd = (x.cpu().numpy() for x in g.frontier())
+            om, orw, od, _ = o.open_arrays()
+            np.testing.assert_array_equal(gr, orw, err_msg=f"iteration {it + 1} rewards")
+            np.testing.assert_array_equal(gd, od, err_msg=f"iteration {it + 1} depths")
+            np.testing.assert_array_equal(gm, om, err_msg=f"iteration {it + 1} maps")
+            if want["frontier"] == 0 or want["visited"] >= budget:
+                break
+        return want
+    finally:
+        g.close()
+
+
+BF_CASES = [("c1", 3000, 30), ("c2", 2000, 25), ("c3", 1500, 12), ("c4", 3000, 30), ("c5", 400, 6)]
+
+
+@pytest.mark.parametrize("k", [1, 7, 64, 512])
+@pytest.mark.parametrize("variant", ["planted", "dense"])
+@pytest.mark.parametrize("case", BF_CASES, ids=[c[0] for c in BF_CASES])
+def test_best_first_matches_oracle(case, variant, k):
+    require_gpu()
+    name, budget, iters = case
+    wl = inputs.WORKLOADS[name].with_(B=1)
+    say(f"[best-first] {name} {variant} k={k}")
+    maps, rules, _ = inputs.make_all(wl, 5, variant)
+    last = compare_best_first(wl, maps[0], one_set(rules), budget, iters, k)
+    assert last["visited"] > 0
+
+
+@pytest.mark.parametrize("engine", ["generic", "wave", "lane16"])
+def test_best_first_engines_and_options(engine):
+    require_gpu()
+    wl = inputs.WORKLOADS["c4"].with_(B=1)
+    say(f"[best-first options] engine={engine}")
+    maps, rules, _ = inputs.make_all(wl, 3, "planted")
+    rules = one_set(rules)
+    compare_best_first(wl, maps[0], rules, 2000, 20, 16, engine=engine)
+    compare_best_first(wl, maps[0], rules, 2000, 20, 16, A=4, engine=engine)
+    compare_best_first(wl, maps[0], rules, 333, 20, 64, engine=engine)          # budget cut
+    compare_best_first(wl, maps[0], rules, 2000, 20, 8, L=3, engine=engine)     # terminal
+    compare_best_first(wl, maps[0], rules, 2000, 12, 8, engine=engine, rule_mode="sequential")
+
+
+def test_best_first_pool_full_is_an_error():
+    require_gpu()
+    wl = inputs.WORKLOADS["c1"].with_(B=1)
+    maps, rules, _ = inputs.make_all(wl, 0, "planted")
+    g = av.Search(wl.H, wl.W, wl.C, wl.R, wl.max_h, wl.max_w, 100, best_first_k=32,
+                  max_nodes=40)
+    try:
+        g.load_rules(*rules)
+        g.begin(maps[0])
+        with pytest.raises(av.AvError) as e:
+            for _ in range(50):
+                g.expand(10**6)
+        assert e.value.status == av.AV_ENOMEM
+        g.begin(maps[0])
+        assert g.expand(5)["children"] == 5
+    finally:
+        g.close()
+
+
+def test_best_first_force_pays_skips_dominated_nodes():
+    """A rule that pays for every force tile re-reaches states with more reward all the time;
+    the earlier open copies are popped and skipped (iterations with no parent)."""
+    require_gpu()
+    import test_oracle_search as tos
+    root, rules = tos.force_pays()
+    wl = inputs.Workload("fp", 1, B=1, H=1, W=3, C=4, R=1, shapes=((1, 1),), p_dc=0.0,
+                         per_env=False, T=1, L=5)
+    last = compare_best_first(wl, root, rules, 200, 100, 1, L=5)
+    assert last["frontier"] == 0
