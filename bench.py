@@ -31,6 +31,7 @@ METRIC = "env-steps/sec and cell-rule-updates/sec at 1 MI355X; % of HBM roofline
 KERNEL_SOURCES = {
     "generic": ("paper_2407_04221_amd/csrc/k_generic.hip",),
     "wave": ("paper_2407_04221_amd/csrc/k_wave.hip",),
+    "rows": ("paper_2407_04221_amd/csrc/k_rows.hip",),
     "lane16": ("paper_2407_04221_amd/csrc/lane16_kernel.hip",
                "paper_2407_04221_amd/csrc/lane16_jit.cpp"),
 }
@@ -174,7 +175,7 @@ def main():
                     help="untimed steps before timing (default: one launch of --chunk steps)")
     ap.add_argument("--workload", default="c4")
     ap.add_argument("--variant", default="literal", choices=["literal", "planted", "dense"])
-    ap.add_argument("--engine", default="auto", choices=["auto", "generic", "lane16", "wave"])
+    ap.add_argument("--engine", default="auto", choices=["auto", "generic", "lane16", "wave", "rows"])
     ap.add_argument("--rule-mode", default="parallel", choices=["parallel", "sequential"])
     ap.add_argument("--limit", type=int, default=0,
                     help="rule application control: cap every loaded rule at K matches per step")

@@ -56,17 +56,25 @@ typedef enum {
     AV_ESTATE = 4    /* call out of order, e.g. av_step before av_load_rules and av_reset */
 } av_status;
 
-/* Kernel family used by av_step / av_step_n.  AUTO picks lane16 when eligible, else wave
- * when its LDS working set (C + 1 padded planes, one match plane per rule, two vote
- * accumulators per stored channel) fits in 64 KiB, else generic. */
+/* Kernel family used by av_step / av_step_n.  AUTO picks lane16 when eligible; else rows
+ * when eligible, unless the rule sets are per environment and H > 16 (then wave, the faster
+ * of the two there); else wave when its LDS working set (C + 1 padded planes, one match
+ * plane per rule, two vote accumulators per plane) fits in 64 KiB; else generic. */
 typedef enum {
     AV_ENGINE_AUTO = 0,
     AV_ENGINE_GENERIC = 1,  /* any size within the limits below; maps staged in LDS */
     AV_ENGINE_LANE16 = 2,   /* maps of at most 16 x 16 and one shared rule set: one map
                                row per lane, two maps per 32-bit lane word, rows shifted
                                across lanes with DPP, the rule set compiled into the kernel */
-    AV_ENGINE_WAVE = 3      /* one environment per 64-lane wave, map rows in LDS; rule
-                               programs read with scalar loads (per-environment rules) */
+    AV_ENGINE_WAVE = 3,     /* one environment per workgroup, map rows in LDS; four groups
+                               of lanes match four of its rules at once */
+    AV_ENGINE_ROWS = 4      /* one environment per 64-lane wave with no barriers, map row y
+                               in lane y, planes in the wave's LDS; one lane per rule tests
+                               every rule's rarest entries at once, so only rules that can
+                               match are visited.  Needs R + 4 <= 64 and, within 64 KiB of
+                               LDS, (3 C + 4) planes of H + 16 rows plus R + 4 match planes
+                               of H + 32 rows (4 bytes per row for W <= 32, else 8); no rule
+                               application control */
 } av_engine;
 
 /* Order in which the rules of one step are applied. */

@@ -72,6 +72,8 @@ struct av_batch_s {
     Lane16Program lprog;           // compiled form for the lane16 engine (when chosen)
     Lane16Device dlprog;
     std::vector<std::vector<Lane16Rule>> lsets;   // the rule list the lane16 programs come from
+    RowsProgram rprog;             // compiled form for the rows engine (when chosen)
+    uint32_t *d_rows = nullptr;
     Lane16Program lprog_ctl;       // lane16 program with rule application control compiled in
     Lane16Device dlprog_ctl;
     bool lane16_ctl = false;       // steps use dlprog_ctl
@@ -90,6 +92,8 @@ void free_device_program(av_batch_t b) {
     dev_free(b->dprog.vote);
     dev_free(b->dprog.rvote);
     b->dprog = DeviceProgram{};
+    dev_free(b->d_rows);
+    b->d_rows = nullptr;
     lane16_free(b->dlprog);
 }
 
@@ -267,6 +271,8 @@ av_status step_prefix(av_batch_t b, int n, const uint8_t *actions, float *reward
     a.gsrc = gsrc; a.gnf = gnf; a.gA = gA; a.gdepth = gdepth;
     if (b->engine == AV_ENGINE_LANE16)
         AV_HIP(launch_lane16_step(a, b->dlprog, b->stream));
+    else if (b->engine == AV_ENGINE_ROWS)
+        AV_HIP(launch_rows_step(a, b->d_rows, b->rprog.set_words, b->rprog.rules, b->stream));
     else if (b->engine == AV_ENGINE_WAVE)
         AV_HIP(launch_wave_step(a, b->stream));
     else
@@ -301,7 +307,7 @@ av_status av_create_batch(const av_config *cfg, av_batch_t *out) {
     if (c.max_episode_steps < 0) return fail(AV_EINVAL, "max_episode_steps must be >= 0");
     if (c.rule_mode != AV_RULES_PARALLEL && c.rule_mode != AV_RULES_SEQUENTIAL)
         return fail(AV_EINVAL, "unknown rule_mode %d", c.rule_mode);
-    if (c.engine < AV_ENGINE_AUTO || c.engine > AV_ENGINE_WAVE)
+    if (c.engine < AV_ENGINE_AUTO || c.engine > AV_ENGINE_ROWS)
         return fail(AV_EINVAL, "unknown engine %d", c.engine);
     const size_t env_lds = generic_env_lds_bytes(c.height, c.width, c.channels,
                                                  c.max_rules + kMoveRules);
@@ -317,6 +323,10 @@ av_status av_create_batch(const av_config *cfg, av_batch_t *out) {
     if (c.engine == AV_ENGINE_WAVE && !wave_ok)
         return fail(AV_EINVAL, "the wave engine needs %zu bytes of LDS (limit %d)", wave_lds,
                     kLdsBudget);
+    const bool rows_ok = rows_eligible(c.height, c.width, c.channels, c.max_rules + kMoveRules);
+    if (c.engine == AV_ENGINE_ROWS && !rows_ok)
+        return fail(AV_EINVAL, "the rows engine needs at most 60 rules and %zu bytes of LDS (limit %d)",
+                    rows_lds_bytes(c.height, c.width, c.channels, c.max_rules + kMoveRules), kLdsBudget);
 
     int dev_count = 0;
     AV_HIP(hipGetDeviceCount(&dev_count));
@@ -332,7 +342,13 @@ av_status av_create_batch(const av_config *cfg, av_batch_t *out) {
     b->state_bytes = size_t(c.channels) * c.num_envs * c.height * b->row_bytes;
     b->envs_per_block = std::max(1, std::min(256 / c.height, int(kLdsBudget / env_lds)));
     if (c.engine != AV_ENGINE_AUTO) b->engine = c.engine;
-    else b->engine = lane16_ok ? AV_ENGINE_LANE16 : (wave_ok ? AV_ENGINE_WAVE : AV_ENGINE_GENERIC);
+    else if (lane16_ok) b->engine = AV_ENGINE_LANE16;
+    // measured on MI355X: rows is the faster engine except for per-environment rule sets on
+    // maps taller than 16 rows, where a few crowded environments (many player cells, most
+    // rules partly matching) set the launch time and the wave engine's four rule groups per
+    // environment finish them sooner
+    else if (rows_ok && !(c.per_env_rules && c.height > 16 && wave_ok)) b->engine = AV_ENGINE_ROWS;
+    else b->engine = wave_ok ? AV_ENGINE_WAVE : AV_ENGINE_GENERIC;
     b->plain_engine = b->engine;
     hipError_t e = hipMalloc(&b->d_state, b->state_bytes);
     if (e == hipSuccess) e = hipMalloc(&b->d_init, b->state_bytes);
@@ -425,6 +441,10 @@ av_status av_load_rules(av_batch_t b, int32_t R, const int32_t *shape, const int
     b->dprog.vote_stride = b->prog.vote_stride;
     b->dprog.rvote_stride = b->prog.rvote_stride;
     b->dprog.any_reward = b->prog.any_reward;
+    if (b->plain_engine == AV_ENGINE_ROWS) {
+        compile_rows(b->prog, c.channels, b->rprog);
+        if (av_status st = upload(&b->d_rows, b->rprog.words)) return st;
+    }
     if (b->engine == AV_ENGINE_LANE16) {
         std::vector<std::vector<Lane16Rule>> lsets(S);
         for (int s = 0; s < S; ++s)
@@ -491,10 +511,17 @@ av_status av_set_rule_control(av_batch_t b, const int32_t *limit, const uint8_t 
     const bool random = order == AV_SITES_RANDOM;
     // control compiles into the lane16 program; the wave engine runs it when its scratch fits
     // in LDS; otherwise it runs on the generic engine
+    // (a rows batch created with AV_ENGINE_AUTO switches like a wave batch; an explicit rows
+    // batch has no control)
     const bool on_lane16 = b->plain_engine == AV_ENGINE_LANE16;
-    const bool on_wave = b->plain_engine == AV_ENGINE_WAVE &&
+    const bool wave_like = b->plain_engine == AV_ENGINE_WAVE ||
+                           (b->plain_engine == AV_ENGINE_ROWS && c.engine == AV_ENGINE_AUTO);
+    const bool on_wave = wave_like &&
                          wave_lds_bytes(c.height, c.width, c.channels, R + kMoveRules, true,
                                         random) <= size_t(kLdsBudget);
+    if (active && c.engine == AV_ENGINE_ROWS)
+        return fail(AV_EINVAL, "the rows engine has no rule application control; create the "
+                    "batch with AV_ENGINE_AUTO, AV_ENGINE_WAVE or AV_ENGINE_GENERIC");
     if (active && !on_lane16 && !on_wave && c.engine != AV_ENGINE_AUTO &&
         c.engine != AV_ENGINE_GENERIC)
         return fail(AV_EINVAL, "rule application control does not fit this wave batch's LDS; "
@@ -592,6 +619,8 @@ static av_status step_k(av_batch_t b, int32_t k, const uint8_t *actions, float *
     }
     if (b->engine == AV_ENGINE_LANE16) {
         AV_HIP(launch_lane16_step(a, b->lane16_ctl ? b->dlprog_ctl : b->dlprog, b->stream));
+    } else if (b->engine == AV_ENGINE_ROWS) {
+        AV_HIP(launch_rows_step(a, b->d_rows, b->rprog.set_words, b->rprog.rules, b->stream));
     } else if (b->engine == AV_ENGINE_WAVE) {
         AV_HIP(launch_wave_step(a, b->stream));
     } else {

@@ -204,6 +204,18 @@ av_status set_error(av_status st, const char *msg);
 hipError_t launch_observe(const void *state, int B, int C, int H, int W, int row_bytes, int w,
                           uint8_t *dst, hipStream_t s);
 
+// The rows engine (k_rows.hip): one environment per wave, planes in registers, and its
+// program: per set, rule headers, probe and row-ordered match entries, row-ordered votes.
+struct RowsProgram {
+    int32_t rules = 0, sets = 0, set_words = 0;
+    std::vector<uint32_t> words;      // [S][set_words]
+};
+void compile_rows(const GenericProgram &g, int C, RowsProgram &out);
+size_t rows_lds_bytes(int H, int W, int C, int rules_per_set);
+bool rows_eligible(int H, int W, int C, int rules_per_set);
+hipError_t launch_rows_step(const StepArgs &a, const uint32_t *words, int set_words, int rules,
+                            hipStream_t s);
+
 // The wave engine (k_wave.hip): one environment per workgroup.
 size_t wave_lds_bytes(int H, int W, int C, int rules_per_set, bool control = false,
                       bool random = false);

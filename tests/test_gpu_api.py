@@ -70,7 +70,7 @@ def test_rule_validation():
     b.close()
 
 
-@pytest.mark.parametrize("engine", ["generic", "wave", "auto"])
+@pytest.mark.parametrize("engine", ["generic", "wave", "rows", "auto"])
 def test_checkpoint_resume_is_bit_identical(engine):
     require_gpu()
     import torch
@@ -97,7 +97,7 @@ def test_checkpoint_resume_is_bit_identical(engine):
         x.close()
 
 
-@pytest.mark.parametrize("engine", ["generic", "wave", "auto"])
+@pytest.mark.parametrize("engine", ["generic", "wave", "rows", "auto"])
 def test_two_runs_are_identical(engine):
     require_gpu()
     wl = inputs.WORKLOADS["c2"].with_(B=150, T=30)
@@ -138,7 +138,7 @@ def test_packed_state_layout(W):
     b.close()
 
 
-@pytest.mark.parametrize("engine", ["generic", "wave", "auto"])
+@pytest.mark.parametrize("engine", ["generic", "wave", "rows", "auto"])
 def test_exhaustive_4x4_rules_against_oracle(engine):
     """Every 4x4 goal plane x a sample of tri-valued 1x2 / 2x1 rules, 65536 envs each."""
     require_gpu()
@@ -167,7 +167,7 @@ def test_exhaustive_4x4_rules_against_oracle(engine):
             np.testing.assert_array_equal(d, want[2])
 
 
-@pytest.mark.parametrize("engine", ["generic", "wave", "auto"])
+@pytest.mark.parametrize("engine", ["generic", "wave", "rows", "auto"])
 def test_exhaustive_4x4_moves_against_oracle(engine):
     """Every 4x4 wall plane x 3 player cells x 5 actions, no loaded rules."""
     require_gpu()

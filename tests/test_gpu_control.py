@@ -275,3 +275,42 @@ def test_control_engine_switch_and_errors():
         assert b.info["engine"] == av.AV_ENGINE_WAVE
     finally:
         b.close()
+
+
+def test_control_on_rows_batches():
+    """An AUTO batch on the rows engine runs rule application control on the wave engine and
+    returns to rows when the control is cleared; an explicit rows batch refuses it; both
+    against the oracle."""
+    require_gpu()
+    wl = inputs.WORKLOADS["c5"].with_(B=3, T=6, L=5)
+    maps, rules, actions = inputs.make_all(wl, 8, "dense")
+    ctl = control_for(wl, 3, 4, 0, kmax=3)
+    R = wl.R
+    b = av.Batch.for_workload(wl)
+    try:
+        b.load_rules(*rules)
+        assert b.info["engine"] == av.AV_ENGINE_ROWS
+        b.set_rule_control(*ctl)
+        assert b.info["engine"] == av.AV_ENGINE_WAVE
+        b.set_rule_control(None, None)
+        assert b.info["engine"] == av.AV_ENGINE_ROWS
+    finally:
+        b.close()
+    b = av.Batch.for_workload(wl, engine="rows")
+    try:
+        b.load_rules(*rules)
+        with pytest.raises(av.AvError) as e:
+            b.set_rule_control(np.ones((1, R), np.int32), None)
+        assert e.value.status == av.AV_EINVAL
+        b.set_rule_control(np.zeros((1, R), np.int32), None)     # no control: accepted
+        assert b.info["engine"] == av.AV_ENGINE_ROWS
+    finally:
+        b.close()
+    want_m, want_r, want_d = oracle.run(wl, maps, rules, actions, nthreads=8, control=ctl)
+    seq, final, r, d, eng = gpu_run(wl, maps, rules, actions, engine="auto", mode="step",
+                                    control=ctl)
+    assert av.ENGINE_NAMES[eng] == "wave"
+    for t in range(wl.T):
+        assert first_mismatch(seq[t], want_m[t]) is None, f"maps differ at step {t}"
+        np.testing.assert_array_equal(r[t], want_r[t], err_msg=f"rewards, step {t}")
+        np.testing.assert_array_equal(d[t], want_d[t], err_msg=f"done, step {t}")

@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 import oracle
-from gpu_util import first_mismatch, gpu_run, require_gpu, say
+from gpu_util import first_mismatch, gpu_run, require_gpu, rows_ok, say
 from paper_2407_04221_amd import inputs
 
 pytestmark = pytest.mark.gpu
@@ -36,7 +36,8 @@ LANE16 = {n for n, w in CASES.items() if w.H <= 16 and w.W <= 16 and not w.per_e
 
 
 def engines(name):
-    return ["generic", "wave", "lane16"] if name in LANE16 else ["generic", "wave"]
+    out = ["generic", "wave", "lane16"] if name in LANE16 else ["generic", "wave"]
+    return out + (["rows"] if rows_ok(CASES[name]) else [])
 
 
 def check(wl, maps, rules, actions, engine):
@@ -60,7 +61,7 @@ def test_edge_case(name, engine, variant):
     check(wl, maps, rules, actions, engine)
 
 
-@pytest.mark.parametrize("engine", ["generic", "lane16", "wave"])
+@pytest.mark.parametrize("engine", ["generic", "lane16", "wave", "rows"])
 def test_rules_with_no_specified_input(engine):
     """An all-don't-care input matches at every anchor (the paper's empty "no-op" rules,
     Sec. 2.2.1); with outputs it writes everywhere, with heavily overlapping votes."""
@@ -74,7 +75,7 @@ def test_rules_with_no_specified_input(engine):
     assert (r != 0).all()
 
 
-@pytest.mark.parametrize("engine", ["generic", "lane16", "wave"])
+@pytest.mark.parametrize("engine", ["generic", "lane16", "wave", "rows"])
 def test_no_loaded_rules(engine):
     require_gpu()
     wl = W_("moves", 52, B=41, H=13, W=16, C=4, R=0, shapes=((1, 1),), T=30, L=0)
@@ -85,7 +86,7 @@ def test_no_loaded_rules(engine):
     check(wl, maps, empty, actions, engine)
 
 
-@pytest.mark.parametrize("engine", ["generic", "lane16", "wave"])
+@pytest.mark.parametrize("engine", ["generic", "lane16", "wave", "rows"])
 def test_out_of_range_actions_are_no_ops(engine):
     require_gpu()
     wl = W_("acts", 53, B=24, H=8, W=8, C=4, R=2, shapes=((1, 2),), T=10)

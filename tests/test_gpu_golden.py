@@ -23,7 +23,7 @@ def _cases():
             if fx.H <= 16 and fx.W <= 16:
                 engines.append("lane16")
         else:
-            engines = ["generic", "wave"]
+            engines = ["generic", "wave", "rows"]
             if fx.H <= 16 and fx.W <= 16:
                 engines.append("lane16")
         out += [(name, path, e) for e in engines]

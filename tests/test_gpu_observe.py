@@ -82,7 +82,7 @@ def test_observe_rejects_bad_window():
 STEP_OBS = [("c1", 1, 6), ("c2", 70, 5), ("c4", 301, 7), ("c4", 13, 4), ("c5", 2, 4)]
 
 
-@pytest.mark.parametrize("engine", ["auto", "lane16", "generic", "wave"])
+@pytest.mark.parametrize("engine", ["auto", "lane16", "generic", "wave", "rows"])
 @pytest.mark.parametrize("case", STEP_OBS, ids=[f"{c[0]}-B{c[1]}" for c in STEP_OBS])
 def test_step_observe_matches_oracle(case, engine):
     """av_step_observe (the observation written by the lane16 step kernel itself for w <= 64,

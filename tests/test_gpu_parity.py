@@ -22,7 +22,7 @@ def _case_ids():
 
 @pytest.mark.parametrize("variant", inputs.VARIANTS)
 @pytest.mark.parametrize("seed", [0, 1])
-@pytest.mark.parametrize("engine", ["generic", "wave", "auto"])
+@pytest.mark.parametrize("engine", ["generic", "wave", "rows", "auto"])
 @pytest.mark.parametrize("case", CASES, ids=_case_ids())
 def test_step_matches_oracle(case, engine, seed, variant):
     require_gpu()
@@ -41,7 +41,7 @@ def test_step_matches_oracle(case, engine, seed, variant):
 
 
 @pytest.mark.parametrize("variant", ["literal", "dense"])
-@pytest.mark.parametrize("engine", ["generic", "wave", "auto"])
+@pytest.mark.parametrize("engine", ["generic", "wave", "rows", "auto"])
 @pytest.mark.parametrize("case", CASES, ids=_case_ids())
 def test_step_n_matches_oracle(case, engine, variant):
     require_gpu()
@@ -72,7 +72,7 @@ EDGE = {
 
 
 @pytest.mark.parametrize("variant", inputs.VARIANTS)
-@pytest.mark.parametrize("engine", ["generic", "lane16", "wave"])
+@pytest.mark.parametrize("engine", ["generic", "lane16", "wave", "rows"])
 @pytest.mark.parametrize("name", sorted(EDGE))
 def test_edge_shapes_match_oracle(name, engine, variant):
     require_gpu()

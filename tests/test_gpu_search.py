@@ -63,7 +63,7 @@ def test_search_matches_oracle(case, variant):
     assert last["visited"] > 0
 
 
-@pytest.mark.parametrize("engine", ["generic", "wave", "lane16"])
+@pytest.mark.parametrize("engine", ["generic", "wave", "lane16", "rows"])
 def test_search_engines_and_options(engine):
     require_gpu()
     wl = inputs.WORKLOADS["c4"].with_(B=1)
@@ -153,7 +153,7 @@ def test_best_first_matches_oracle(case, variant, k):
     assert last["visited"] > 0
 
 
-@pytest.mark.parametrize("engine", ["generic", "wave", "lane16"])
+@pytest.mark.parametrize("engine", ["generic", "wave", "lane16", "rows"])
 def test_best_first_engines_and_options(engine):
     require_gpu()
     wl = inputs.WORKLOADS["c4"].with_(B=1)

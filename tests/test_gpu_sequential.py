@@ -25,7 +25,7 @@ LANE16 = {n for n, w in EXTRA.items() if w.H <= 16 and w.W <= 16 and not w.per_e
 
 
 @pytest.mark.parametrize("variant", inputs.VARIANTS)
-@pytest.mark.parametrize("engine", ["generic", "wave", "auto"])
+@pytest.mark.parametrize("engine", ["generic", "wave", "rows", "auto"])
 @pytest.mark.parametrize("case", CASES, ids=[f"{n}-B{b}-T{t}" for n, b, t in CASES])
 def test_sequential_step_matches_oracle(case, engine, variant):
     require_gpu()
@@ -43,7 +43,7 @@ def test_sequential_step_matches_oracle(case, engine, variant):
         np.testing.assert_array_equal(d[t], want_d[t], err_msg=f"done, step {t}")
 
 
-@pytest.mark.parametrize("engine", ["generic", "wave", "lane16"])
+@pytest.mark.parametrize("engine", ["generic", "wave", "lane16", "rows"])
 @pytest.mark.parametrize("name", sorted(EXTRA))
 def test_sequential_step_n_matches_oracle(name, engine):
     require_gpu()
