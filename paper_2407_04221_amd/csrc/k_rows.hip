@@ -32,7 +32,9 @@ namespace av {
 namespace {
 
 constexpr int kPad = 16;              // zero rows around each LDS plane (patterns are <= 16)
-constexpr int kBits = 12;             // exact counts up to 4095 votes per cell and sign
+// exact counts: a cell gets at most one vote per (rule, i, j), so with the old value at most
+// 1 + 4 + 60 x 16 x 16 = 15365 < 2^14 votes of one sign
+constexpr int kBits = 14;
 
 __device__ inline bool wave_any(bool p) { return __builtin_amdgcn_ballot_w64(p) != 0ull; }
 __device__ inline int popc(uint32_t v) { return __popc(v); }

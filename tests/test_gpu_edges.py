@@ -94,3 +94,24 @@ def test_out_of_range_actions_are_no_ops(engine):
     actions = np.random.default_rng(5).integers(0, 256, size=(wl.T, wl.B)).astype(np.uint8)
     actions[:, ::3] = 0
     check(wl, maps, rules, actions, engine)
+
+
+@pytest.mark.parametrize("engine", ["rows", "wave", "generic"])
+def test_vote_counts_beyond_4096(engine):
+    """16 all-don't-care 16 x 16 rules vote +1 and 15 vote -1 on the goal plane of a 64 x 64
+    map: a cell away from the edges is covered by 256 anchors of each rule, so it gets
+    4096 plus and 3840 minus votes (plus its old value), and the exact counts need more than
+    12 bits (a 12-bit count of the plus votes would wrap to 0 and clear the cell)."""
+    require_gpu()
+    R = 31
+    wl = W_("votes", 54, B=2, H=64, W=64, C=4, R=R, shapes=((16, 16),), T=2, L=0)
+    maps, (shape, ip, op, rw), actions = inputs.make_all(wl, 0, "literal")
+    ip[:] = -1
+    op[:] = -1
+    op[:, :16, 3] = 1
+    op[:, 16:, 3] = 0
+    rw[:] = 0
+    actions[:] = 0
+    want_m, want_r, want_d = oracle.run(wl, maps, (shape, ip, op, rw), actions, nthreads=8)
+    assert want_m[0][:, 3, 15:49, 15:49].all()      # the interior became (or stayed) goal
+    check(wl, maps, (shape, ip, op, rw), actions, engine)
