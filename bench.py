@@ -167,6 +167,38 @@ def bench_search(av, torch, wl, args):
             "level_sizes": [lv["children"] for lv in levels][:64]}
 
 
+def graph_step_us(av, torch, b, maps, acts, rew, don, n):
+    """Capture n av_step calls (one launch each) in a HIP graph on a side stream and time its
+    replays: the GPU-side cost of a one-step launch without the Python call."""
+    if n < 1:
+        return None
+    b.reset(maps)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    try:
+        with torch.cuda.stream(s):
+            av.av_set_stream(b.h, s)
+            with torch.cuda.graph(g, stream=s):
+                for t in range(n):
+                    av.av_step(b.h, acts[t % acts.shape[0]], rew[t % rew.shape[0]],
+                               don[t % don.shape[0]])
+    finally:
+        torch.cuda.current_stream().wait_stream(s)
+        av.av_set_stream(b.h, torch.cuda.current_stream())
+    g.replay()
+    torch.cuda.synchronize()
+    reps = 10
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / (reps * n)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -289,9 +321,17 @@ def main():
         f1.record(stream)
         torch.cuda.synchronize()
         ms1 = f0.elapsed_time(f1)
+        graph_us = graph_step_us(av, torch, b, maps, acts, rew, don, min(n, 100))
         per_launch = {"api": "av_step", "steps": n, "ms_per_step": ms1 / n,
                       "env_steps_per_sec": wl.B * n / (ms1 / 1e3),
-                      "frac_hbm_roofline": wl.B * n / (ms1 / 1e3) / roof_env_steps}
+                      "frac_hbm_roofline": wl.B * n / (ms1 / 1e3) / roof_env_steps,
+                      "graph_us_per_step": graph_us,
+                      "graph_frac_hbm_roofline": None if graph_us is None else
+                      wl.B / (graph_us * 1e-6) / roof_env_steps,
+                      "note": "ms_per_step: one av_step call per step from Python (ctypes "
+                              "marshalling + launch); graph_us_per_step: the same calls "
+                              "captured once in a HIP graph and replayed (GPU-side cost of a "
+                              "one-step launch)"}
 
     observe = None
     if args.observe:

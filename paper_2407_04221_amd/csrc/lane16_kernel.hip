@@ -12,8 +12,9 @@
 // half are kept zero.
 //
 // Environments of a wave that do not exist (B not a multiple of 8) compute on zero rows and
-// are never stored.  The initial rows stay in registers for resets; actions are fetched 16
-// steps at a time and broadcast per step across each row with ds_bpermute.
+// are never stored.  The initial rows stay in registers for resets (a single-step launch
+// reads them only when one of the wave's environments ends its episode); actions are fetched
+// 16 steps at a time and broadcast per step across each row with ds_bpermute.
 //
 // One step, per the paper (Sec. 2.1, Sec. 2.1.1, Sec. 2.2.1):
 //   force    F = the player plane moved one cell in each environment's action direction;
@@ -103,26 +104,33 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
     // Search expansion (gsrc set): environment e starts from row block e / gA of gsrc, laid
     // out [C][gnf][H], with its step counter at gdepth[e / gA]; there are no initial maps to
     // return to (an ended episode is never expanded further).
-    u32 p[AV_C], q[AV_C];   // current rows, initial rows (kept for automatic resets)
+    // Current rows, and the initial rows for automatic resets.  A launch of several steps
+    // keeps the initial rows in registers from the start; a single-step launch reads them
+    // only if one of the wave's environments ends its episode.
+    u32 p[AV_C], q[AV_C];
     const unsigned short *const src = gsrc ? gsrc : state;
     const int sstride = gsrc ? gnf : B;
     const int sA = gsrc ? iA / gA : iA, sB = gsrc ? iB / gA : iB;
+    const int yy = rowok ? y : 0;
+    const u32 keep = HALF(hasA && rowok, hasB && rowok);
+    auto load_init = [&]() {
 #pragma unroll
-    for (int c = 0; c < AV_C; ++c) {
-        const int yy = rowok ? y : 0;
-        const u32 lo = u32(src[(size_t(c) * sstride + sA) * AV_H + yy]);
-        const u32 hi = u32(src[(size_t(c) * sstride + sB) * AV_H + yy]);
-        const u32 keep = HALF(hasA && rowok, hasB && rowok);
-        p[c] = (lo | (hi << 16)) & keep;
-        if (gsrc) {
-            q[c] = p[c];
-        } else {
+        for (int c = 0; c < AV_C; ++c) {
             const size_t row = size_t(c) * B;
             const u32 ilo = u32(init[(row + iA) * AV_H + yy]);
             const u32 ihi = u32(init[(row + iB) * AV_H + yy]);
             q[c] = (ilo | (ihi << 16)) & keep;
         }
+    };
+#pragma unroll
+    for (int c = 0; c < AV_C; ++c) {
+        const u32 lo = u32(src[(size_t(c) * sstride + sA) * AV_H + yy]);
+        const u32 hi = u32(src[(size_t(c) * sstride + sB) * AV_H + yy]);
+        p[c] = (lo | (hi << 16)) & keep;
+        q[c] = p[c];
     }
+    const bool lazy_init = K == 1 && !gsrc;
+    if (!gsrc && !lazy_init) load_init();
     int tA = gsrc ? gdepth[sA] : tctr[iA], tB = gsrc ? gdepth[sB] : tctr[iB];
 
     // Actions arrive 16 steps at a time: lane y of a row holds step k0 + y of its pair
@@ -199,6 +207,7 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
 
         // automatic reset to the initial map
         if (ANY(u32(dA || dB))) {
+            if (lazy_init) load_init();     // the launch's only step
             const u32 dm = HALF(dA, dB);
 #pragma unroll
             for (int c = 0; c < AV_C; ++c) p[c] = (q[c] & dm) | (p[c] & ~dm);
