@@ -65,30 +65,51 @@ def measured_traffic(workload: str, engine: int, engine_name: str):
     return rec
 
 
+def host_cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(wl, maps, rules, actions, budget_s: float, threads: int,
                  rule_mode: str = "parallel", control=None):
+    """The oracle as it stands on a bounded sample of the workload (the first 4096
+    environments, as many steps as fit in budget_s), OpenMP over environments on `threads`
+    host threads, then single-threaded for a quarter of the budget."""
     import oracle
     from paper_2407_04221_amd import inputs
     nb = min(wl.B, 4096)
     envs = np.arange(nb)
     m, r, a = inputs.subset_envs(wl, maps, rules, actions, envs)
-    o = oracle.Oracle.for_workload(wl, B=nb, rule_mode=int(rule_mode == "sequential"))
-    o.load_rules(*r)
-    if control is not None:
-        limit, inhibit, order, seed = control
-        S = nb if wl.per_env else 1
-        o.set_rule_control(limit[:S], inhibit[:S], order, seed)
-    o.reset(m)
-    steps = 0
-    t0 = time.perf_counter()
-    while steps < a.shape[0] and time.perf_counter() - t0 < budget_s:
-        o.step(a[steps], nthreads=threads)
-        steps += 1
-    dt = time.perf_counter() - t0
-    used = o.threads_used
-    o.close()
-    return {"value": nb * steps / dt, "unit": "env-steps/s", "cores": used, "kind": "oracle",
-            "sample": f"first {nb} of {wl.B} envs x {steps} steps ({dt:.1f} s, {used} threads)"}
+
+    def timed(nthreads, budget):
+        o = oracle.Oracle.for_workload(wl, B=nb, rule_mode=int(rule_mode == "sequential"))
+        o.load_rules(*r)
+        if control is not None:
+            limit, inhibit, order, seed = control
+            S = nb if wl.per_env else 1
+            o.set_rule_control(limit[:S], inhibit[:S], order, seed)
+        o.reset(m)
+        steps = 0
+        t0 = time.perf_counter()
+        while steps < a.shape[0] and time.perf_counter() - t0 < budget:
+            o.step(a[steps], nthreads=nthreads)
+            steps += 1
+        dt = time.perf_counter() - t0
+        used = o.threads_used
+        o.close()
+        return nb * steps / dt, steps, dt, used
+
+    value, steps, dt, used = timed(threads, budget_s)
+    v1, s1, dt1, _ = timed(1, budget_s / 4)
+    return {"value": value, "unit": "env-steps/s", "cores": used, "kind": "oracle",
+            "sample": f"first {nb} of {wl.B} envs x {steps} steps ({dt:.1f} s, {used} threads "
+                      f"of {os.cpu_count()} on {host_cpu_model()})",
+            "single_thread": {"value": v1, "sample": f"first {nb} envs x {s1} steps ({dt1:.1f} s)"}}
 
 
 def _time_us(fn, stream, torch, reps=100):
