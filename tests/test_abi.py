@@ -64,6 +64,9 @@ def _cfg(**kw):
     dict(num_envs=0), dict(height=0), dict(width=65), dict(height=65), dict(channels=3),
     dict(channels=32), dict(max_rules=-1), dict(max_rules=253), dict(max_pat_h=0),
     dict(max_pat_w=17), dict(per_env_rules=2), dict(max_episode_steps=-1), dict(engine=9),
+    dict(engine=5), dict(engine=-1),
+    # the rows engine takes at most 60 loaded rules and its LDS set within 64 KiB
+    dict(engine=4, max_rules=61), dict(engine=4, height=64, width=64, channels=31, max_rules=60),
     # lane16 needs maps of at most 16 x 16 and one shared rule set
     dict(engine=2, height=32, width=32), dict(engine=2, per_env_rules=1),
     dict(rule_mode=2), dict(rule_mode=-1),
