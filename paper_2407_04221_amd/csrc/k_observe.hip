@@ -2,110 +2,113 @@
 // (paper Sec. 2.2.2: a local patch of tiles around the player's position; Table 1 uses
 // windows of 5, 10, 20 and 31 cells).
 //
-// One workgroup per environment (one wave per environment, four to a workgroup, when the
-// window has at most 64 rows in all).  Its packed rows are staged in LDS; the first player cell
-// in row-major order is found with an LDS atomicMin over rows (then the row's lowest set
-// bit).  The environment's C x w x w output bytes are built in LDS one window row per thread
-// (one map row read, bits shifted to the window's first column), placed at the same offset
-// modulo 16 as their global address, and copied out with aligned 16-byte stores (bytes
-// only at the two unaligned ends).  Windows too large for LDS are written byte by byte.
-// Window cell (wy, wx) shows map cell (py - w/2 + wy, px - w/2 + wx); cells off the map, and
-// the whole window of a map without a player, are 0.
+// 16, 32 or 64 lanes per environment (about one per 16-byte chunk of its output), 256 lanes
+// to a workgroup.  The environment's packed rows are staged in
+// LDS; the first player cell in row-major order is found with an LDS atomicMin over rows
+// (then the row's lowest set bit).  The environment's C x w x w output bytes are then written
+// straight from the staged rows in 16-byte chunks on the global 16-byte grid, one chunk per
+// thread and pass: the chunk's 16 cells are gathered as a 16-bit mask, one shift of a staged
+// row per window row the chunk touches, and every 4 bits are spread into 4 bytes with one
+// multiply (bit i of v & 15 lands in byte i of (v & 15) * 0x204081); the bytes before the
+// first and after the last full chunk are written one by one.  Window cell (wy, wx) shows
+// map cell (py - w/2 + wy, px - w/2 + wx); cells off the map, and the whole window of a map
+// without a player, are 0 (packed rows hold no bits at x >= W).
 #include "av_internal.h"
 
 namespace av {
 namespace {
 
-template <typename RowT>
-__device__ inline RowT load_row(const void *base, size_t idx, int row_bytes) {
+__device__ inline uint64_t load_row(const void *base, size_t idx, int row_bytes) {
     if (row_bytes == 2) return static_cast<const uint16_t *>(base)[idx];
     if (row_bytes == 4) return static_cast<const uint32_t *>(base)[idx];
-    return static_cast<RowT>(static_cast<const uint64_t *>(base)[idx]);
+    return static_cast<const uint64_t *>(base)[idx];
 }
 
 __device__ inline int lowbit(uint64_t v) { return __ffsll(static_cast<unsigned long long>(v)) - 1; }
 
-// Stage the packed rows and find the first player cell; returns (py, px), py = H if none.
-// tid / T: this thread's index among the T threads that serve the environment.
-__device__ inline void stage_rows(const void *state, int B, int C, int H, int row_bytes, int b,
-                                  uint64_t *rows, int *first, int &py, int &px, int tid, int T,
-                                  bool live) {
+// Map bits x0 .. x0 + 63 of a row as the low bits of the result (0 outside the row).
+__device__ inline uint64_t row_from(uint64_t row, int x0) {
+    if (x0 >= 64 || x0 <= -64) return 0ull;
+    return x0 >= 0 ? row >> x0 : row << -x0;
+}
+
+// The window cells of output bytes [o, o + n) of one environment (n <= 16) as a mask, bit k
+// for byte o + k.  rows: its staged planes [C][H]; (y0, x0) the window's top-left map cell.
+// (One environment's output is at most 31 x 255 x 255 bytes, so offsets fit 32 bits.)
+__device__ inline uint32_t window_bits(const uint64_t *rows, int H, int w, bool has, int y0,
+                                       int x0, uint32_t o, int n) {
+    const uint32_t ww = uint32_t(w) * uint32_t(w);
+    int c = int(o / ww);
+    const uint32_t rem = o - uint32_t(c) * ww;
+    int wy = int(rem / uint32_t(w)), wx = int(rem - uint32_t(wy) * uint32_t(w));
+    uint32_t m = 0;
+    for (int k = 0; k < n;) {
+        const int len = min(n - k, w - wx);
+        const int y = y0 + wy;
+        const uint64_t row = (has && y >= 0 && y < H) ? rows[size_t(c) * H + y] : 0ull;
+        m |= uint32_t(row_from(row, x0 + wx) & ((1ull << len) - 1ull)) << k;
+        k += len;
+        wx += len;
+        if (wx == w) {
+            wx = 0;
+            if (++wy == w) {
+                wy = 0;
+                ++c;
+            }
+        }
+    }
+    return m;
+}
+
+// Four bytes 0/1 from the low 4 bits of v (bit i -> byte i).
+__device__ inline uint32_t spread4(uint32_t v) { return ((v & 15u) * 0x204081u) & 0x01010101u; }
+
+// T threads per environment, 256 / T environments per workgroup, `region` LDS bytes each.
+template <int T>
+__global__ void __launch_bounds__(256) observe_env(const void *state, int B, int C, int H, int W,
+                                                   int row_bytes, int w, uint8_t *dst, int region) {
+    extern __shared__ __align__(16) unsigned char lds[];
+    constexpr int G = 256 / T;
+    const int tid = threadIdx.x % T, slot = threadIdx.x / T;
+    const int b = blockIdx.x * G + slot;
+    const bool live = b < B;
+    uint64_t *rows = reinterpret_cast<uint64_t *>(lds + size_t(slot) * region);   // [C][H]
+    int *first = reinterpret_cast<int *>(rows + size_t(C) * H);
     if (tid == 0) *first = H;
     if (live)
         for (int r = tid; r < C * H; r += T) {
             const int c = r / H, y = r - c * H;
-            rows[r] = load_row<uint64_t>(state, (size_t(c) * B + b) * H + y, row_bytes);
+            rows[r] = load_row(state, (size_t(c) * B + b) * H + y, row_bytes);
         }
     __syncthreads();
     if (live)
         for (int y = tid; y < H; y += T)
             if (rows[size_t(kChPlayer) * H + y]) atomicMin(first, y);
     __syncthreads();
-    py = *first;
-    px = (live && py < H) ? lowbit(rows[size_t(kChPlayer) * H + py]) : 0;
-}
-
-// T threads per environment, 256 / T environments per workgroup, `region` LDS bytes each.
-template <int T>
-__global__ void __launch_bounds__(256) observe_staged(const void *state, int B, int C, int H, int W,
-                                                      int row_bytes, int w, uint8_t *dst,
-                                                      int region) {
-    extern __shared__ __align__(16) unsigned char lds[];
-    const int G = 256 / T;
-    const int tid = threadIdx.x % T, slot = threadIdx.x / T;
-    const int b = blockIdx.x * G + slot;
-    const bool live = b < B;
-    unsigned char *base = lds + size_t(slot) * region;
-    uint64_t *rows = reinterpret_cast<uint64_t *>(base);   // [C][H]
-    int *first = reinterpret_cast<int *>(rows + size_t(C) * H);
-    unsigned char *win = base + ((size_t(C) * H * 8 + 4 + 15) & ~size_t(15));
-    int py, px;
-    stage_rows(state, B, C, H, row_bytes, b, rows, first, py, px, tid, T, live);
-    const bool has = py < H;
-    const int y0 = py - w / 2, x0 = px - w / 2;
-    const size_t per = size_t(C) * w * w;
-    uint8_t *out = dst + size_t(live ? b : 0) * per;
-    const int shift = int(reinterpret_cast<uintptr_t>(out) & 15);
-    unsigned char *mine = win + shift;                       // same offset modulo 16 as out
-    if (live)
-        for (int q = tid; q < C * w; q += T) {               // one window row per thread
-            const int c = q / w, wy = q - c * w, y = y0 + wy;
-            const uint64_t row = (has && y >= 0 && y < H) ? rows[size_t(c) * H + y] : 0ull;
-            unsigned char *o = mine + size_t(q) * w;
-            for (int wx = 0; wx < w; ++wx) {
-                const int x = x0 + wx;
-                o[wx] = uint8_t(unsigned(x) < unsigned(W) ? (row >> x) & 1ull : 0ull);
-            }
-        }
-    __syncthreads();
     if (!live) return;
-    const size_t head = shift ? (16 - shift < per ? size_t(16 - shift) : per) : 0;
-    for (size_t i = tid; i < head; i += T) out[i] = mine[i];
-    const size_t nch = (per - head) / 16;
-    for (size_t k = tid; k < nch; k += T)
-        *reinterpret_cast<uint4 *>(out + head + 16 * k) =
-            *reinterpret_cast<const uint4 *>(mine + head + 16 * k);
-    for (size_t i = head + 16 * nch + tid; i < per; i += T) out[i] = mine[i];
-}
-
-__global__ void __launch_bounds__(256) observe_bytes(const void *state, int B, int C, int H, int W,
-                                                     int row_bytes, int w, uint8_t *dst) {
-    extern __shared__ __align__(16) unsigned char lds[];
-    uint64_t *rows = reinterpret_cast<uint64_t *>(lds);   // [C][H]
-    int *first = reinterpret_cast<int *>(rows + size_t(C) * H);
-    const int b = blockIdx.x, tid = threadIdx.x;
-    int py, px;
-    stage_rows(state, B, C, H, row_bytes, b, rows, first, py, px, tid, int(blockDim.x), true);
+    const int py = *first;
     const bool has = py < H;
+    const int px = has ? lowbit(rows[size_t(kChPlayer) * H + py]) : 0;
     const int y0 = py - w / 2, x0 = px - w / 2;
-    const int per = C * w * w;
-    uint8_t *out = dst + size_t(b) * per;
-    for (int o = tid; o < per; o += blockDim.x) {
-        const int c = o / (w * w), rem = o - c * w * w, wy = rem / w, wx = rem - wy * w;
-        const int y = y0 + wy, x = x0 + wx;
-        uint8_t v = 0;
-        if (has && y >= 0 && y < H && x >= 0 && x < W) v = uint8_t((rows[size_t(c) * H + y] >> x) & 1);
-        out[o] = v;
+    (void)W;
+
+    const uint32_t per = uint32_t(C) * uint32_t(w) * uint32_t(w);
+    uint8_t *const out = dst + size_t(b) * per;
+    const uint32_t head = uint32_t(16 - (reinterpret_cast<uintptr_t>(out) & 15)) & 15u;
+    const uint32_t h = head < per ? head : per;
+    const uint32_t chunks = (per - h) / 16;
+    for (uint32_t k = tid; k < chunks; k += T) {
+        const uint32_t o = h + 16 * k;
+        const uint32_t m = window_bits(rows, H, w, has, y0, x0, o, 16);
+        *reinterpret_cast<uint4 *>(out + o) =
+            make_uint4(spread4(m), spread4(m >> 4), spread4(m >> 8), spread4(m >> 12));
+    }
+    // the bytes before the first and after the last full chunk (at most 30), one per thread
+    const uint32_t tail = h + 16 * chunks;
+    const int loose = int(h + (per - tail));
+    for (int i = tid; i < loose; i += T) {
+        const uint32_t o = uint32_t(i) < h ? uint32_t(i) : tail + (uint32_t(i) - h);
+        out[o] = uint8_t(window_bits(rows, H, w, has, y0, x0, o, 1));
     }
 }
 
@@ -113,17 +116,23 @@ __global__ void __launch_bounds__(256) observe_bytes(const void *state, int B, i
 
 hipError_t launch_observe(const void *state, int B, int C, int H, int W, int row_bytes, int w,
                           uint8_t *dst, hipStream_t s) {
-    const size_t rows = (size_t(C) * H * sizeof(uint64_t) + 4 + 15) & ~size_t(15);
-    const size_t staged = (rows + size_t(C) * w * w + 16 + 15) & ~size_t(15);
-    if (C * w <= 64 && 4 * staged <= size_t(kLdsBudget))      // small windows: a wave each
-        hipLaunchKernelGGL(observe_staged<64>, dim3((B + 3) / 4), dim3(256), 4 * staged, s, state, B,
-                           C, H, W, row_bytes, w, dst, int(staged));
-    else if (staged <= size_t(kLdsBudget))
-        hipLaunchKernelGGL(observe_staged<256>, dim3(B), dim3(256), staged, s, state, B, C, H, W,
-                           row_bytes, w, dst, int(staged));
+    const size_t region = (size_t(C) * H * sizeof(uint64_t) + 4 + 15) & ~size_t(15);
+    // lanes per environment: about one per 16-byte chunk of its output (16, 32 or 64), as
+    // long as the workgroup's staged rows fit the LDS budget
+    const size_t per = size_t(C) * w * w;
+    int T = per <= 16 * 16 ? 16 : (per <= 32 * 16 ? 32 : 64);
+    while (T < 64 && size_t(256 / T) * region > size_t(kLdsBudget)) T *= 2;
+    const int G = 256 / T;
+    const dim3 grid((B + G - 1) / G);
+    if (T == 16)
+        hipLaunchKernelGGL(observe_env<16>, grid, dim3(256), G * region, s, state, B, C, H, W,
+                           row_bytes, w, dst, int(region));
+    else if (T == 32)
+        hipLaunchKernelGGL(observe_env<32>, grid, dim3(256), G * region, s, state, B, C, H, W,
+                           row_bytes, w, dst, int(region));
     else
-        hipLaunchKernelGGL(observe_bytes, dim3(B), dim3(256), rows, s, state, B, C, H, W, row_bytes,
-                           w, dst);
+        hipLaunchKernelGGL(observe_env<64>, grid, dim3(256), G * region, s, state, B, C, H, W,
+                           row_bytes, w, dst, int(region));
     return hipGetLastError();
 }
 

@@ -151,3 +151,34 @@ def test_step_observe_with_random_control(w):
         np.testing.assert_array_equal(obs.cpu().numpy(), o.observe(w), err_msg=f"step {t}")
     o.close()
     b.close()
+
+
+def test_observe_without_player_several_players_and_unaligned_output():
+    """Maps with no player (all-zero windows), several players (the first in row-major order
+    centres the window), and an output that starts 3 bytes past a 16-byte boundary."""
+    require_gpu()
+    import torch
+    wl = inputs.Workload("obsedge", 72, B=11, H=13, W=10, C=5, R=1, shapes=((1, 1),), p_dc=0.5,
+                         per_env=False, T=1)
+    maps, rules, _ = inputs.make_all(wl, 0)
+    maps[::3, 2] = 0                              # no player
+    maps[1::3, 2, 4, 7] = 1                       # a second player
+    maps[1::3, 2, 9, 0] = 1                       # and a third
+    o = oracle.Oracle.for_workload(wl)
+    o.load_rules(*rules)
+    o.reset(maps)
+    b = av.Batch.for_workload(wl)
+    b.load_rules(*rules)
+    b.reset(maps)
+    for w in (1, 3, 7, 16, 29):
+        n = wl.B * wl.C * w * w
+        buf = torch.full((n + 40,), 7, dtype=torch.uint8, device="cuda")
+        dst = buf[3:3 + n].view(wl.B, wl.C, w, w)
+        av.av_observe(b.h, w, dst)
+        want = o.observe(w)
+        assert not want[::3].any()
+        np.testing.assert_array_equal(dst.cpu().numpy(), want, err_msg=f"w={w}")
+        rest = buf.cpu().numpy()
+        assert (rest[:3] == 7).all() and (rest[3 + n:] == 7).all(), "wrote outside the output"
+    o.close()
+    b.close()
