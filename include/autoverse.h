@@ -113,8 +113,9 @@ typedef struct {
 
 /* Create a batch on cfg->device.  Maps start empty; av_load_rules and av_reset must both
  * be called before the first step.  Fails with AV_EINVAL for sizes outside the limits in
- * av_config, or when one environment's working set (its C + 1 planes and one match plane
- * per rule, 64-bit rows for W > 32) exceeds 64 KiB of LDS. */
+ * av_config, when one environment's working set (its C + 1 planes and one match plane per
+ * rule, 64-bit rows for W > 32) exceeds 64 KiB of LDS, or when an explicitly requested
+ * engine cannot take the configuration (the limits given with av_engine). */
 av_status av_create_batch(const av_config *cfg, av_batch_t *out);
 
 /* Load the rules (paper Sec. 2.1: a rule is an n x m input pattern I, an n x m output
