@@ -193,16 +193,19 @@ __global__ void __launch_bounds__(64) rows_step(StepArgs a, RowsArgs rp) {
     const size_t plane = size_t(B) * H;
     const size_t lrow = size_t(b) * H + size_t(ry);
 
-    const int words = int((size_t(C + 2) * hp + size_t(2) * (C + 1) * hp + size_t(Rt) * hs) *
-                          (sizeof(RowT) / 4));
-    for (int w = y; w < words; w += 64) reinterpret_cast<uint32_t *>(lds)[w] = 0u;
+    // zero: the planes with their pad rows, the vote accumulators, and the pad rows above
+    // every match plane (the rows below them are written before they are read)
+    const int pwords = int(size_t(3 * C + 4) * hp * (sizeof(RowT) / 4));
+    for (int w = y; w < pwords; w += 64) reinterpret_cast<uint32_t *>(lds)[w] = 0u;
+    for (int w = y; w < Rt * kPad; w += 64) Ms[size_t(w / kPad) * hs + (w % kPad)] = 0;
     if (rp.body_lds)
         for (int w = y; w < rp.set_words; w += 64) lprog[w] = gprog[w];
     const uint32_t *const lbody = rp.body_lds ? lprog : nullptr;
-    // probe records: lane l of pt[g] holds word 64 g + l, i.e. word l % 4 of rule 16 g + l / 4
-    uint32_t pt[4];
+    // probe records (8 words per rule): lane l of pt[g] holds word 64 g + l, i.e. word l % 8
+    // of rule 8 g + l / 8
+    uint32_t pt[8];
 #pragma unroll
-    for (int g = 0; g < 4; ++g) pt[g] = (64 * g + y < 4 * Rt) ? gprog[64 * g + y] : 0u;
+    for (int g = 0; g < 8; ++g) pt[g] = (64 * g + y < 8 * Rt) ? gprog[64 * g + y] : 0u;
     // Lane-parallel probes (parallel rule order): lane r tests the first two (or, on a
     // second pass, four) entries of rule r's rarest-first list together at every anchor row;
     // a missing entry reads the zero plane C + 1 complemented, which passes everywhere.
@@ -215,15 +218,17 @@ __global__ void __launch_bounds__(64) rows_step(StepArgs a, RowsArgs rp) {
         pinv[e] = ~RowT(0);
     }
     if (y < Rt) {
-        const uint32_t w0 = gprog[4 * y], bo = gprog[4 * y + 3];
+        const uint32_t *rec = gprog + 8 * y;
+        const uint32_t w0 = rec[0];
         const int n = int(w0 & 255u), m = int((w0 >> 8) & 255u);
-        const int ecnt = int(gprog[bo + 1]);
+        const int ecnt = int(rec[4]);
+        const uint32_t first[4] = {rec[1], rec[2], rec[5], rec[6]};
         pmax = H - n;
         pcol = low_mask<RowT>(W - m + 1);
 #pragma unroll
         for (int e = 0; e < 4; ++e)
             if (e < ecnt) {
-                const uint32_t q = gprog[bo + 4 + e];
+                const uint32_t q = first[e];
                 pa[e] = int(q & 255u) * hp + int((q >> 8) & 255u);
                 pj[e] = int((q >> 16) & 255u);
                 pinv[e] = ((q >> 24) & 1u) ? RowT(0) : ~RowT(0);
@@ -287,8 +292,8 @@ __global__ void __launch_bounds__(64) rows_step(StepArgs a, RowsArgs rp) {
                 // match rule r; if it fires, record it, pay its reward and OR its votes
                 const int r = int(__builtin_ctzll(todo));
                 todo &= todo - 1ull;
-                const uint32_t ptr = pt[r >> 4];
-                const int lb = (r & 15) * 4;
+                const uint32_t ptr = pt[r >> 3];
+                const int lb = (r & 7) * 8;
                 const uint32_t w0 = uint32_t(__builtin_amdgcn_readlane(int(ptr), lb));
                 const int n = int(w0 & 255u), m = int((w0 >> 8) & 255u);
                 const int bo = __builtin_amdgcn_readlane(int(ptr), lb + 3);
@@ -378,8 +383,9 @@ __global__ void __launch_bounds__(64) rows_step(StepArgs a, RowsArgs rp) {
 // ---------------------------------------------------------------------------------
 // Host side: the rows program, one block of words per rule set, built from the generic
 // program.  Block layout (word offsets from the block start):
-//   [4 r, 4 r + 4)  probe record of rule r: n | m << 8 | probes << 16, the first two
-//                   entries of its rarest-first list (0 if fewer), the body offset
+//   [8 r, 8 r + 8)  probe record of rule r: n | m << 8 | probes << 16, its first two
+//                   entries rarest first (0 if fewer), the body offset, the entry count,
+//                   its third and fourth entries, 0
 //   body of rule r: reward, entry count, vote count, 0; every specified entry, rarest
 //                   first; the votes; per channel c of C + 1 two words: the offset (from the
 //                   body start) of c's votes and their counts (plus | minus << 16); those
@@ -409,7 +415,7 @@ void compile_rows(const GenericProgram &g, int C, RowsProgram &out) {
     std::vector<std::vector<uint32_t>> sets(S);
     for (int s = 0; s < S; ++s) {
         std::vector<uint32_t> &w = sets[s];
-        w.assign(size_t(Rt) * 4, 0);
+        w.assign(size_t(Rt) * 8, 0);
         for (int r = 0; r < Rt; ++r) {
             const RuleHdr &h = g.hdr[size_t(s) * Rt + r];
             const uint32_t *ms = g.match.data() + size_t(s) * g.match_stride + h.match_off;
@@ -421,10 +427,14 @@ void compile_rows(const GenericProgram &g, int C, RowsProgram &out) {
             const std::vector<uint32_t> votes(vs, vs + h.vote_cnt);
             const int probes = std::min(2, h.match_cnt);
             const size_t body = w.size();
-            w[size_t(r) * 4 + 0] = uint32_t(h.n) | (uint32_t(h.m) << 8) | (uint32_t(probes) << 16);
-            w[size_t(r) * 4 + 1] = probes > 0 ? ents[0] : 0u;
-            w[size_t(r) * 4 + 2] = probes > 1 ? ents[1] : 0u;
-            w[size_t(r) * 4 + 3] = uint32_t(body);
+            uint32_t *rec = &w[size_t(r) * 8];
+            rec[0] = uint32_t(h.n) | (uint32_t(h.m) << 8) | (uint32_t(probes) << 16);
+            rec[1] = probes > 0 ? ents[0] : 0u;
+            rec[2] = probes > 1 ? ents[1] : 0u;
+            rec[3] = uint32_t(body);
+            rec[4] = uint32_t(ents.size());
+            rec[5] = ents.size() > 2 ? ents[2] : 0u;
+            rec[6] = ents.size() > 3 ? ents[3] : 0u;
             w.push_back(uint32_t(h.reward));
             w.push_back(uint32_t(ents.size()));
             w.push_back(uint32_t(votes.size()));
@@ -475,12 +485,14 @@ hipError_t launch_rows_step(const StepArgs &a, const uint32_t *words, int set_wo
                             hipStream_t s) {
     if (!rows_eligible(a.H, a.W, a.C, rules)) return hipErrorInvalidValue;
     size_t lds = rows_lds_bytes(a.H, a.W, a.C, rules);
-    // Stage the program in LDS when it fits and does not cost occupancy: with more than one
+    // Stage the program in LDS for launches of 16 steps or more, when it fits and does not
+    // cost occupancy: with more than one
     // workgroup per CU to place (256 CUs, 160 KiB of LDS each), the staged wave must still
     // leave room for its share of them.
     const size_t staged = lds + sizeof(uint32_t) * size_t(set_words);
     const size_t per_cu = (size_t(a.B) + 255) / 256;
-    const int body_lds = staged <= size_t(kLdsBudget) && staged * per_cu <= size_t(160) * 1024;
+    const int body_lds = a.k >= 16 && staged <= size_t(kLdsBudget) &&
+                         staged * per_cu <= size_t(160) * 1024;
     if (body_lds) lds = staged;
     RowsArgs rp{words, set_words, rules, body_lds};
     if (a.row_bytes == 2)

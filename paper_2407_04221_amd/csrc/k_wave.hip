@@ -444,7 +444,8 @@ hipError_t launch_wave_step(const StepArgs &a, hipStream_t s) {
     const size_t base = wave_lds_bytes(a.H, a.W, a.C, a.prog.rules_per_set, a.ctl.active != 0,
                                        a.ctl.random != 0);
     const size_t prog = size_t(L.hdr_words + L.match_words + L.vote_words) * 4;
-    L.prog_lds = base + prog <= size_t(kLdsBudget) ? 1 : 0;
+    // the copy pays for itself over a launch of many steps, not over one
+    L.prog_lds = a.k >= 16 && base + prog <= size_t(kLdsBudget) ? 1 : 0;
     const size_t lds = base + (L.prog_lds ? prog : 0);
     const int threads = kGroups * L.Hq;
     if (a.W <= 32)
