@@ -73,8 +73,8 @@ typedef enum {
                                every rule's rarest entries at once, so only rules that can
                                match are visited.  Needs R + 4 <= 64 and, within 64 KiB of
                                LDS, (3 C + 4) planes of H + 16 rows plus R + 4 match planes
-                               of H + 32 rows (4 bytes per row for W <= 32, else 8); no rule
-                               application control */
+                               of H + 32 rows (4 bytes per row for W <= 32, else 8) and 36
+                               bytes per rule; no rule application control */
 } av_engine;
 
 /* Order in which the rules of one step are applied. */

@@ -37,6 +37,11 @@ constexpr int kPad = 16;              // zero rows around each LDS plane (patter
 constexpr int kBits = 14;
 
 __device__ inline bool wave_any(bool p) { return __builtin_amdgcn_ballot_w64(p) != 0ull; }
+// Does any lane of group g (lanes g hq .. g hq + hq - 1) hold p?
+__device__ inline bool group_any(bool p, int hq, int g) {
+    const uint64_t bal = __builtin_amdgcn_ballot_w64(p);
+    return hq >= 64 ? bal != 0ull : ((bal >> (g * hq)) & ((1ull << hq) - 1ull)) != 0ull;
+}
 __device__ inline int popc(uint32_t v) { return __popc(v); }
 __device__ inline int popc(uint64_t v) { return __popcll(v); }
 __device__ inline void lds_or(uint32_t *p, uint32_t v) { atomicOr(p, v); }
@@ -186,7 +191,8 @@ __global__ void __launch_bounds__(64) rows_step(StepArgs a, RowsArgs rp) {
     RowT *Ms = Vm + size_t(C + 1) * hp;                    // [Rt][kPad + hp]: match planes
     const int hs = kPad + hp;
     int *fired = reinterpret_cast<int *>(Ms + size_t(Rt) * hs);   // [Rt]
-    uint32_t *lprog = reinterpret_cast<uint32_t *>(fired + Rt);    // [set_words] if staged
+    uint32_t *prob = reinterpret_cast<uint32_t *>(fired + Rt);     // [8 Rt] probe records
+    uint32_t *lprog = prob + 8 * Rt;                                // [set_words] if staged
     const uint32_t *gprog = rp.words + size_t(a.per_env ? b : 0) * size_t(rp.set_words);
     const RowT wmask = low_mask<RowT>(W);
     // row y of environment b in channel c is element c * plane + lrow of the [C][B][H] arrays
@@ -198,6 +204,7 @@ __global__ void __launch_bounds__(64) rows_step(StepArgs a, RowsArgs rp) {
     const int pwords = int(size_t(3 * C + 4) * hp * (sizeof(RowT) / 4));
     for (int w = y; w < pwords; w += 64) reinterpret_cast<uint32_t *>(lds)[w] = 0u;
     for (int w = y; w < Rt * kPad; w += 64) Ms[size_t(w / kPad) * hs + (w % kPad)] = 0;
+    for (int w = y; w < 8 * Rt; w += 64) prob[w] = gprog[w];
     if (rp.body_lds)
         for (int w = y; w < rp.set_words; w += 64) lprog[w] = gprog[w];
     const uint32_t *const lbody = rp.body_lds ? lprog : nullptr;
@@ -283,6 +290,85 @@ __global__ void __launch_bounds__(64) rows_step(StepArgs a, RowsArgs rp) {
                     hit |= yy <= pmax ? t : RowT(0);
                 }
                 todo &= __builtin_amdgcn_ballot_w64((hit & pcol) != 0);
+            }
+            if (H <= 32 && __popcll(todo) > 2) {
+                // Several candidates on a map of at most 32 rows: the wave splits into groups
+                // of hq lanes (lane gy of a group on map row gy) that match one candidate each
+                // at the same time.  A group reads its rule's entries and votes from its own
+                // hq-word chunk of the program (lane gy holds word base + gy, taken out with
+                // ds_bpermute) and leaves the rule when none of its anchors survives.
+                const int hq = H <= 16 ? 16 : 32, G = 64 / hq;
+                const int g = y / hq, gy = y - g * hq;
+                const bool grow = gy < H;
+                const int gry = grow ? gy : 0;
+                const uint32_t *const body = lbody ? lbody : gprog;
+                uint32_t tmask = 0;
+                while (todo) {
+                    int rsel = -1;
+                    for (int q = 0; q < G && todo; ++q) {
+                        const int r = int(__builtin_ctzll(todo));
+                        todo &= todo - 1ull;
+                        if (g == q) rsel = r;
+                    }
+                    const bool mine = rsel >= 0;
+                    const int rr = mine ? rsel : 0;
+                    const uint32_t w0 = prob[8 * rr];
+                    const int bo = int(prob[8 * rr + 3]);
+                    const int n = int(w0 & 255u), m = int((w0 >> 8) & 255u);
+                    const uint32_t *const bp = body + bo;
+                    const int reward = int(bp[0]), ecnt = mine ? int(bp[1]) : 0;
+                    const int vcnt = int(bp[2]);
+                    RowT M = (mine && gy + n <= H) ? low_mask<RowT>(W - m + 1) : RowT(0);
+                    bool alive = mine;
+                    int cb = 0;
+                    uint32_t cv = bp[4 + gy];          // every set block ends with 64 zero words
+                    for (int e = 0; wave_any(alive && e < ecnt);) {
+                        if (e - cb >= hq) {
+                            cb = e;
+                            cv = bp[4 + cb + gy];
+                        }
+                        const int lim = min(e == 0 ? 2 : 4, cb + hq - e);
+                        for (int u = 0; u < lim; ++u) {
+                            const uint32_t q = uint32_t(__builtin_amdgcn_ds_bpermute(
+                                (g * hq + e + u - cb) << 2, int(cv)));
+                            if (e + u < ecnt) M &= entry_test<RowT>(Pl, hp, q, gry);
+                        }
+                        e += lim;
+                        alive = group_any(M != 0, hq, g);
+                    }
+                    const bool hit = mine && group_any(M != 0, hq, g);
+                    if (hit) {
+                        if (grow) Ms[size_t(rr) * hs + kPad + gy] = M;
+                        rsum += reward * popc(M);
+                    }
+                    cb = 0;
+                    cv = bp[4 + ecnt + gy];
+                    for (int v = 0; wave_any(hit && v < vcnt); ++v) {
+                        if (v - cb >= hq) {
+                            cb = v;
+                            cv = bp[4 + ecnt + cb + gy];
+                        }
+                        const uint32_t q = uint32_t(__builtin_amdgcn_ds_bpermute(
+                            (g * hq + v - cb) << 2, int(cv)));
+                        if (hit && v < vcnt && grow) {
+                            const int c = int(q & 255u), i = int((q >> 8) & 255u);
+                            const int j = int((q >> 16) & 255u);
+                            lds_or((((q >> 24) & 1u) ? Vp : Vm) + c * hp + gy + i, RowT(M << j));
+                            tmask |= 1u << c;
+                        }
+                    }
+                    // record the rules that fired (rule index | body offset << 8)
+                    const uint64_t hits = __builtin_amdgcn_ballot_w64(hit);
+                    for (int q = 0; q < G; ++q)
+                        if ((hits >> (q * hq)) & 1ull) {
+                            const int rq = __builtin_amdgcn_readlane(rsel, q * hq);
+                            const int bq = __builtin_amdgcn_readlane(bo, q * hq);
+                            if (y == 0) fired[nf] = rq | (bq << 8);
+                            ++nf;
+                        }
+                }
+                for (int off = 1; off < 64; off <<= 1) tmask |= uint32_t(__shfl_xor(int(tmask), off, 64));
+                touched |= uint32_t(__builtin_amdgcn_readfirstlane(int(tmask)));
             }
         }
         for (;;) {
@@ -468,12 +554,12 @@ void compile_rows(const GenericProgram &g, int C, RowsProgram &out) {
 }
 
 // LDS of one wave: C + 2 planes, 2 (C + 1) vote accumulators and one match plane per rule
-// (H + 16 rows each, the match planes 16 more), and the fired list.
+// (H + 16 rows each, the match planes 16 more), the fired list and the probe records.
 size_t rows_lds_bytes(int H, int W, int C, int rules_per_set) {
     const size_t rowb = W <= 32 ? 4 : 8, hp = size_t(H) + kPad;
     return ((size_t(C + 2) + size_t(2) * (C + 1)) * hp + size_t(rules_per_set) * (hp + kPad)) *
                rowb +
-           sizeof(int) * size_t(rules_per_set);
+           (sizeof(int) + 8 * sizeof(uint32_t)) * size_t(rules_per_set);
 }
 
 bool rows_eligible(int H, int W, int C, int rules_per_set) {
