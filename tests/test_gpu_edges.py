@@ -31,13 +31,21 @@ CASES = {
     "big64": W_("big64", 49, B=3, H=64, W=64, C=20, R=40, shapes=((5, 5), (2, 3)), T=4),
     "per_env_small": W_("per_env_small", 50, B=13, H=10, W=12, C=5, R=5,
                         shapes=((3, 3), (1, 2)), per_env=True),
+    "max_rules": W_("max_rules", 55, B=5, H=8, W=8, C=4, R=252, shapes=((1, 1), (2, 2)), T=4),
 }
 LANE16 = {n for n, w in CASES.items() if w.H <= 16 and w.W <= 16 and not w.per_env}
 
 
 def engines(name):
-    out = ["generic", "wave", "lane16"] if name in LANE16 else ["generic", "wave"]
-    return out + (["rows"] if rows_ok(CASES[name]) else [])
+    wl = CASES[name]
+    out = ["generic", "lane16"] if name in LANE16 else ["generic"]
+    # the wave engine: C + 1 planes of H + 16 rows, one 80-row match plane per rule, two
+    # 64-row vote accumulators per plane (4-byte rows for W <= 32, else 8) and a word per rule
+    # within 64 KiB
+    rowb, rt = (4 if wl.W <= 32 else 8), wl.R + 4
+    if ((wl.C + 1) * (wl.H + 16) + rt * 80 + 2 * (wl.C + 1) * 64) * rowb + 4 * (rt + 2) <= 65536:
+        out.append("wave")
+    return out + (["rows"] if rows_ok(wl) else [])
 
 
 def check(wl, maps, rules, actions, engine):

@@ -46,3 +46,22 @@ def test_full_size_sampled(name, variant):
     assert set(np.unique(final)) <= {0, 1}
     assert d.max() <= 1
     assert np.array_equal(r, np.round(r))
+
+
+def test_quarter_million_environments_sampled():
+    """A batch 16 times the throughput workload's (262144 environments of c4's shape) in the
+    launch shape bench.py times: grid indexing past the workload's size, sampled envs against
+    the oracle over every step."""
+    require_gpu()
+    wl = inputs.WORKLOADS["c4"].with_(B=1 << 18, T=60, L=25)
+    say(f"[fullsize] c4 x16: B={wl.B} T={wl.T}")
+    maps, rules, actions = inputs.make_all(wl, 3, "planted")
+    _, final, r, d, eng = gpu_run(wl, maps, rules, actions, mode="step_n", chunk=1000)
+    assert eng == 2                         # lane16
+    envs = sample_envs(wl.B, 24, seed=99)
+    m_s, r_s, a_s = inputs.subset_envs(wl, maps, rules, actions, envs)
+    want_m, want_r, want_d = oracle.run(wl, m_s, r_s, a_s, nthreads=8)
+    np.testing.assert_array_equal(r[:, envs], want_r, err_msg="rewards")
+    np.testing.assert_array_equal(d[:, envs], want_d, err_msg="done")
+    np.testing.assert_array_equal(final[envs], want_m[-1], err_msg="final maps")
+    assert want_d.any() and (want_r != 0).any()
