@@ -21,6 +21,7 @@
 #include <hip/hiprtc.h>
 
 #include <algorithm>
+#include <cstdlib>
 #include <deque>
 #include <map>
 #include <mutex>
@@ -63,6 +64,39 @@ int kout(int in, int out) {
 struct Vote {
     int r, i, j;
 };
+
+// Number of entries a loaded rule is probed with before the wave-wide test: at least two, at
+// most four, more while a static guess of the share of waves (eight maps each) in which some
+// anchor passes them stays above 10 %.  The guess uses the synthetic maps' statistics: one
+// player cell per map with its force cell beside it, walls on 30 % of the cells, the other
+// tile types sharing the rest evenly.  It only decides how much of a rule runs before the
+// test, never what the rule computes.
+size_t probe_len(const std::vector<Entry> &es, int C, int H, int W, int n, int m) {
+    const double cells = double(H) * W, anchors = double(H - n + 1) * (W - m + 1);
+    const size_t lo = std::min<size_t>(2, es.size()), hi = std::min<size_t>(4, es.size());
+    size_t k = 0;
+    double p = anchors;
+    for (; k < hi; ++k) {
+        if (k >= lo && 8.0 * p <= 0.1) break;
+        const Entry &en = es[k];
+        double q1;
+        if (en.c == C || en.c == kChPlayer) {
+            q1 = 1.0 / cells;
+            for (size_t f = 0; f < k; ++f) {            // a force cell beside a player cell
+                const Entry &o = es[f];
+                const bool pair = (en.c == C && o.c == kChPlayer) || (en.c == kChPlayer && o.c == C);
+                if (pair && o.want && en.want && std::abs(o.i - en.i) + std::abs(o.j - en.j) == 1)
+                    q1 = 0.25;
+            }
+        } else if (en.c == kChWall) {
+            q1 = 0.3;
+        } else {
+            q1 = 0.7 / std::max(1, C - 2);
+        }
+        p *= en.want ? q1 : 1.0 - q1;
+    }
+    return k;
+}
 
 class Gen {
   public:
@@ -228,10 +262,12 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
     }
     // Column-shifted planes read on every step (by the moves and by the loaded rules' probe
     // entries) are computed once up front; the others only inside the branches that need them.
-    const int n_top = std::min(R, kMoveRules);
+    const int n_fixed = std::min(R, kMoveRules);
+    std::vector<size_t> probe(R);
     for (int r = 0; r < R; ++r) {
-        const size_t used = r < n_top ? ents[r].size() : std::min<size_t>(2, ents[r].size());
-        for (size_t e = 0; e < used; ++e)
+        probe[r] = r < n_fixed ? ents[r].size()
+                               : probe_len(ents[r], C, H, W, rules[r].n, rules[r].m);
+        for (size_t e = 0; e < probe[r]; ++e)
             if (ents[r][e].j > 0) xs.insert({ents[r][e].c, ents[r][e].j});
     }
 
@@ -265,6 +301,8 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
             else o << M << " &= DPP_SHL(" << row_and(row.second) << ", " << row.first << ");\n";
         }
     };
+    // a loaded rule that casts votes marks the step (wave-uniform: set only under ballots)
+    const bool track = R > n_fixed;
     auto emit_votes = [&](int r) {
         const std::string M = "M" + std::to_string(r);
         std::set<int> js;
@@ -278,6 +316,7 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
             const std::string t = v.first.i ? "DPP_SHR(" + src + ", " + std::to_string(v.first.i) + ")" : src;
             o << (pl ? "PL" : "MI") << c << " |= " << t << ";\n";
         }
+        if (r >= n_fixed && !rule_votes[r].empty()) o << "lf = true;\n";
     };
     auto emit_reward = [&](int r) {
         const std::string M = "M" + std::to_string(r);
@@ -287,9 +326,8 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
     };
 
     // The built-in moves (rules 0..3) are cheap and fire in most waves: evaluated in full,
-    // without branches.  Loaded rules are probed with their two rarest entries; one
-    // wave-uniform test over all probes skips the rest when no anchor survives anywhere.
-    const int n_fixed = std::min(R, kMoveRules);
+    // without branches.  Loaded rules are probed with their rarest entries; one wave-uniform
+    // test over all probes skips the rest when no anchor survives anywhere.
     for (int r = 0; r < R; ++r) {
         const Lane16Rule &ru = rules[r];
         const std::string M = "M" + std::to_string(r);
@@ -298,8 +336,7 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
             emit_rows(M, ents[r]);
             continue;
         }
-        const size_t probe = std::min<size_t>(2, ents[r].size());
-        for (size_t e = 0; e < probe; ++e) {
+        for (size_t e = 0; e < probe[r]; ++e) {
             const Entry &en = ents[r][e];
             const std::string t = en.i ? "DPP_SHL(" + base(en) + ", " + std::to_string(en.i) + ")" : base(en);
             o << M << " &= " << (en.want ? "" : "~") << t << ";\n";
@@ -312,18 +349,19 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
         emit_reward(r);
         emit_votes(r);
     }
-    if (R > n_fixed) {
+    if (track) {
+        o << "bool lf = false;\n";
         o << "if (ANY(";
         for (int r = n_fixed; r < R; ++r) o << (r > n_fixed ? " | " : "") << "M" << r;
         o << ")) {\n";
         for (int r = n_fixed; r < R; ++r) {
             const std::string M = "M" + std::to_string(r);
-            const size_t probe = std::min<size_t>(2, ents[r].size());
+            const size_t pr = probe[r];
             if (controlled(ctl, r)) {
                 // complete the matches, filter them, then pay and vote with what is left
-                if (ents[r].size() > probe) {
+                if (ents[r].size() > pr) {
                     o << "if (ANY(" << M << ")) {\n";
-                    emit_rows(M, std::vector<Entry>(ents[r].begin() + probe, ents[r].end()));
+                    emit_rows(M, std::vector<Entry>(ents[r].begin() + pr, ents[r].end()));
                     o << "}\n";
                 }
                 o << "if (ANY(" << M << ")) {\n";
@@ -336,67 +374,95 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
                 continue;
             }
             o << "if (ANY(" << M << ")) {\n";
-            if (ents[r].size() > probe) {
-                emit_rows(M, std::vector<Entry>(ents[r].begin() + probe, ents[r].end()));
+            if (ents[r].size() > pr) {
+                emit_rows(M, std::vector<Entry>(ents[r].begin() + pr, ents[r].end()));
                 o << "if (ANY(" << M << ")) {\n";
             }
             emit_reward(r);
             emit_votes(r);
-            if (ents[r].size() > probe) o << "}\n";
+            if (ents[r].size() > pr) o << "}\n";
             o << "}\n";
         }
-        o << "}\n";
     }
-    std::vector<int> both;
-    for (int c = 0; c < C; ++c)
-        if (!plus[c].empty() && !minus[c].empty()) both.push_back(c);
-    for (int c = 0; c < C; ++c)
-        if (!plus[c].empty() || !minus[c].empty())
-            o << "u32 N" << c << " = (p[" << c << "] | PL" << c << ") & ~MI" << c << ";\n";
 
-    // votes, exact path: some cell of the wave got votes of both signs
-    if (!both.empty()) {
-        o << "u32 CF = 0u;\n";
-        for (int c : both) o << "CF |= PL" << c << " & MI" << c << ";\n";
-        o << "if (ANY(CF)) {\n";
-        std::set<std::pair<int, int>> shifts;
-        std::set<std::tuple<int, int, int>> terms;
-        for (int c : both)
-            for (auto *lst : {&plus[c], &minus[c]})
-                for (const Vote &v : *lst) {
-                    if (v.j) shifts.insert({v.r, v.j});
-                    terms.insert({v.r, v.i, v.j});
-                }
-        for (auto &s : shifts)
-            o << "const u32 E" << s.first << "_" << s.second << " = M" << s.first << " << " << s.second << ";\n";
-        auto tname = [](int r, int i, int j) {
-            return "T" + std::to_string(r) + "_" + std::to_string(i) + "_" + std::to_string(j);
-        };
-        for (auto &t : terms) {
-            const int r = std::get<0>(t), i = std::get<1>(t), j = std::get<2>(t);
-            const std::string src = j ? "E" + std::to_string(r) + "_" + std::to_string(j) : "M" + std::to_string(r);
-            o << "const u32 " << tname(r, i, j) << " = "
-              << (i ? "DPP_SHR(" + src + ", " + std::to_string(i) + ")" : src) << ";\n";
+    // The write.  A cell with votes of one sign only takes that sign's value; if some cell of
+    // the wave got votes of both signs on a channel, the channel's votes are counted exactly.
+    // `pl` / `mi` list the votes that can be nonzero on the path being emitted.
+    auto emit_write = [&](const std::vector<std::vector<Vote>> &pl,
+                          const std::vector<std::vector<Vote>> &mi) {
+        std::vector<int> voted, both;
+        for (int c = 0; c < C; ++c) {
+            if (pl[c].empty() && mi[c].empty()) continue;
+            voted.push_back(c);
+            if (!pl[c].empty() && !mi[c].empty()) both.push_back(c);
         }
-        for (int c : both) {
-            std::vector<std::string> pt{"p[" + std::to_string(c) + "]"}, mt;
-            for (const Vote &v : plus[c]) pt.push_back(tname(v.r, v.i, v.j));
-            for (const Vote &v : minus[c]) mt.push_back(tname(v.r, v.i, v.j));
-            o << "{ // channel " << c << ": " << pt.size() - 1 << " + votes, " << mt.size() << " - votes\n";
-            const std::vector<std::string> P = g.count(pt), Nn = g.count(mt);
-            const size_t K = std::max(P.size(), Nn.size());
-            o << "u32 GT = 0u, EQ = 0xFFFFFFFFu;\n";
-            for (size_t k = K; k-- > 0;) {
-                const std::string pk = k < P.size() ? P[k] : "0u", nk = k < Nn.size() ? Nn[k] : "0u";
-                o << "GT |= EQ & " << pk << " & ~" << nk << ";\n";
-                o << "EQ &= ~(" << pk << " ^ " << nk << ");\n";
+        for (int c : voted)
+            o << "u32 N" << c << " = (p[" << c << "] | PL" << c << ") & ~MI" << c << ";\n";
+        if (!both.empty()) {
+            o << "u32 CF = 0u;\n";
+            for (int c : both) o << "CF |= PL" << c << " & MI" << c << ";\n";
+            o << "if (ANY(CF)) {\n";
+            std::set<std::pair<int, int>> shifts;
+            std::set<std::tuple<int, int, int>> terms;
+            for (int c : both)
+                for (auto *lst : {&pl[c], &mi[c]})
+                    for (const Vote &v : *lst) {
+                        if (v.j) shifts.insert({v.r, v.j});
+                        terms.insert({v.r, v.i, v.j});
+                    }
+            for (auto &sh : shifts)
+                o << "const u32 E" << sh.first << "_" << sh.second << " = M" << sh.first << " << "
+                  << sh.second << ";\n";
+            auto tname = [](int r, int i, int j) {
+                return "T" + std::to_string(r) + "_" + std::to_string(i) + "_" + std::to_string(j);
+            };
+            for (auto &t : terms) {
+                const int r = std::get<0>(t), i = std::get<1>(t), j = std::get<2>(t);
+                const std::string src = j ? "E" + std::to_string(r) + "_" + std::to_string(j) : "M" + std::to_string(r);
+                o << "const u32 " << tname(r, i, j) << " = "
+                  << (i ? "DPP_SHR(" + src + ", " + std::to_string(i) + ")" : src) << ";\n";
             }
-            o << "N" << c << " = GT;\n}\n";
+            for (int c : both) {
+                std::vector<std::string> pt{"p[" + std::to_string(c) + "]"}, mt;
+                for (const Vote &v : pl[c]) pt.push_back(tname(v.r, v.i, v.j));
+                for (const Vote &v : mi[c]) mt.push_back(tname(v.r, v.i, v.j));
+                o << "{ // channel " << c << ": " << pt.size() - 1 << " + votes, " << mt.size() << " - votes\n";
+                const std::vector<std::string> P = g.count(pt), Nn = g.count(mt);
+                const size_t K = std::max(P.size(), Nn.size());
+                o << "u32 GT = 0u, EQ = 0xFFFFFFFFu;\n";
+                for (size_t k = K; k-- > 0;) {
+                    const std::string pk = k < P.size() ? P[k] : "0u", nk = k < Nn.size() ? Nn[k] : "0u";
+                    o << "GT |= EQ & " << pk << " & ~" << nk << ";\n";
+                    o << "EQ &= ~(" << pk << " ^ " << nk << ");\n";
+                }
+                o << "N" << c << " = GT;\n}\n";
+            }
+            o << "}\n";
         }
+        for (int c : voted) o << "p[" << c << "] = N" << c << ";\n";
+    };
+    if (track) {
+        // Steps where no loaded rule voted (most steps of sparse rule sets) write only the
+        // moves' channels and count only the moves' votes.  The probe test's branch is still
+        // open here: its "no" side gets a copy of the moves' write of its own, so that the
+        // loaded rules' vote words never need a value on that side.
+        std::vector<std::vector<Vote>> mpl(C), mmi(C);
+        for (int c = 0; c < C; ++c) {
+            for (const Vote &v : plus[c])
+                if (v.r < n_fixed) mpl[c].push_back(v);
+            for (const Vote &v : minus[c])
+                if (v.r < n_fixed) mmi[c].push_back(v);
+        }
+        o << "if (lf) {\n";
+        emit_write(plus, minus);
+        o << "} else {\n";
+        emit_write(mpl, mmi);
+        o << "}\n} else {\n";
+        emit_write(mpl, mmi);
         o << "}\n";
+    } else {
+        emit_write(plus, minus);
     }
-    for (int c = 0; c < C; ++c)
-        if (!plus[c].empty() || !minus[c].empty()) o << "p[" << c << "] = N" << c << ";\n";
     o << "(void)F;\n";
     return o.str();
 }
