@@ -13,8 +13,10 @@
 //
 // Environments of a wave that do not exist (B not a multiple of 8) compute on zero rows and
 // are never stored.  The initial rows stay in registers for resets (a single-step launch
-// reads them only when one of the wave's environments ends its episode); actions are fetched
-// 16 steps at a time and broadcast per step across each row with ds_bpermute.
+// reads them only when one of the wave's environments ends its episode).  Actions are read 16
+// steps at a time and turned into per-direction force masks, which each step fetches across
+// its row with ds_bpermute one step ahead; rewards and done flags are kept in registers for 16
+// steps and stored together.
 //
 // One step, per the paper (Sec. 2.1, Sec. 2.1.1, Sec. 2.2.1):
 //   force    F = the player plane moved one cell in each environment's action direction;
@@ -133,36 +135,68 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
     if (!gsrc && !lazy_init) load_init();
     int tA = gsrc ? gdepth[sA] : tctr[iA], tB = gsrc ? gdepth[sB] : tctr[iB];
 
-    // Actions arrive 16 steps at a time: lane y of a row holds step k0 + y of its pair
-    // (env A in byte 0, env B in byte 1); each step reads its entry across the row.
-    auto load_block = [&](int k0) -> u32 {
+    // Actions arrive 16 steps at a time and become force masks: lane y of a row holds, for
+    // step k0 + y of its pair, one mask per direction (up, right, down, left) that is all ones
+    // over the columns of each environment whose action is that direction and that can take a
+    // force cell from that move (the right / left masks leave out the first / last column, so
+    // no bit crosses between the two halves).  A step's four masks are fetched across the row
+    // with ds_bpermute during the step before.  Blocks: `cur` the current 16 steps, `nxt` the
+    // next 16, `raw` the action bytes of the 16 after those.
+    // (the two action bytes are loaded unconditionally, from step 0 past the end and from the
+    // clamped environment index for absent environments, and stay untouched until their
+    // masks are built 16 steps later, so that no step waits for them; masks of steps past the
+    // end are never used and absent environments have no player cell)
+    auto raw_block = [&](int k0, u32 &ra, u32 &rb) {
         const int k = k0 + y;
-        if (k >= K) return 0u;
-        const unsigned char *row = actions + size_t(k) * B;
-        return (hasA ? u32(row[iA]) : 0u) | (hasB ? (u32(row[iB]) << 8) : 0u);
+        const unsigned char *row = actions + size_t(k < K ? k : 0) * B;
+        ra = u32(row[iA]);
+        rb = u32(row[iB]);
     };
-    u32 ablk = load_block(0);
-    u32 anext = load_block(16);
+    const u32 COLS = BOTH(COLMASK(AV_W));
+    auto dir_masks = [&](u32 aA, u32 aB, u32 *m) {
+        m[0] = HALF(aA == 1u, aB == 1u) & COLS;
+        m[1] = HALF(aA == 2u, aB == 2u) & COLS & ~BOTH(1u);
+        m[2] = HALF(aA == 3u, aB == 3u) & COLS;
+        m[3] = HALF(aA == 4u, aB == 4u) & COLS & ~BOTH(1u << (AV_W - 1));
+    };
+    u32 cur[4], nxt[4], g[4], ra, rb;
+    raw_block(0, ra, rb);
+    dir_masks(ra, rb, cur);
+    raw_block(16, ra, rb);
+    dir_masks(ra, rb, nxt);
+    raw_block(32, ra, rb);
     const int src_base = (lane & 48) << 2;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) g[d] = u32(__builtin_amdgcn_ds_bpermute(src_base, int(cur[d])));
+    // Every load above has been consumed except the step counters and the third action
+    // block: wait for the vector memory counter here, once, rather than inside the loop.
+    __builtin_amdgcn_s_waitcnt(0x0F70);             // vmcnt(0); expcnt, lgkmcnt untouched
+
+    // rewards and done flags of 16 steps: lane y of a row keeps step k0 + y of its pair
+    int rbA = 0, rbB = 0;
+    u32 dbuf = 0u;
 
     for (int k = 0; k < K; ++k) {
         const int s = k & 15;
-        if (s == 0 && k > 0) {
-            ablk = anext;
-            anext = load_block(k + 16);
-        }
-        const u32 act = u32(__builtin_amdgcn_ds_bpermute(src_base + (s << 2), int(ablk)));
-        const u32 aA = act & 0xFFu, aB = act >> 8;
-
         // force tiles next to every player cell, toward each environment's action
         u32 F;
         {
             const u32 P = p[AV_PLAYER];
-            u32 f = DPP_SHL(P, 1) & HALF(aA == 1u, aB == 1u);
-            f |= (P << 1) & RT_MASK & HALF(aA == 2u, aB == 2u);
-            f |= DPP_SHR(P, 1) & HALF(aA == 3u, aB == 3u);
-            f |= (P >> 1) & LF_MASK & HALF(aA == 4u, aB == 4u);
-            F = f & CELL;
+            F = ((DPP_SHL(P, 1) & g[0]) | ((P << 1) & g[1]) | (DPP_SHR(P, 1) & g[2]) |
+                 ((P >> 1) & g[3])) & CELL;
+        }
+        // the next step's masks
+        {
+            const int s1 = (k + 1) & 15;
+            if (s1 == 0) {
+#pragma unroll
+                for (int d = 0; d < 4; ++d) cur[d] = nxt[d];
+                dir_masks(ra, rb, nxt);
+                raw_block(k + 33, ra, rb);
+            }
+#pragma unroll
+            for (int d = 0; d < 4; ++d)
+                g[d] = u32(__builtin_amdgcn_ds_bpermute(src_base + (s1 << 2), int(cur[d])));
         }
 
         int rA = 0, rB = 0;
@@ -198,11 +232,24 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
             rB += DPP_ROR(rB, 8);
         }
 #endif
-        // lane 0 of the row reports env A, lane 1 env B
-        if (y < 2 && (y ? hasB : hasA)) {
-            const int e = y ? eB : eA;
-            rewards[size_t(k) * B + e] = float(y ? rB : rA);
-            done[size_t(k) * B + e] = (unsigned char)(y ? dB : dA);
+        // keep this step's results in lane s; store 16 steps at once
+        if (y == s) {
+            rbA = rA;
+            rbB = rB;
+            dbuf = u32(dA) | (u32(dB) << 1);
+        }
+        if (s == 15 || k == K - 1) {
+            if (y <= s) {
+                const size_t at = size_t(k - s + y) * B;
+                if (hasA) {
+                    rewards[at + eA] = float(rbA);
+                    done[at + eA] = (unsigned char)(dbuf & 1u);
+                }
+                if (hasB) {
+                    rewards[at + eB] = float(rbB);
+                    done[at + eB] = (unsigned char)(dbuf >> 1);
+                }
+            }
         }
 
         // automatic reset to the initial map
