@@ -342,8 +342,19 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
             o << M << " &= " << (en.want ? "" : "~") << t << ";\n";
         }
     }
+    // The moves' vote words live for the whole step; those of channels only loaded rules vote
+    // on exist inside the probe test's branch only.
+    std::vector<std::vector<Vote>> mpl(C), mmi(C);
+    for (int c = 0; c < C; ++c) {
+        for (const Vote &v : plus[c])
+            if (v.r < n_fixed) mpl[c].push_back(v);
+        for (const Vote &v : minus[c])
+            if (v.r < n_fixed) mmi[c].push_back(v);
+    }
+    auto moves_vote = [&](int c) { return !mpl[c].empty() || !mmi[c].empty(); };
+    auto any_vote = [&](int c) { return !plus[c].empty() || !minus[c].empty(); };
     for (int c = 0; c < C; ++c)
-        if (!plus[c].empty() || !minus[c].empty())
+        if (track ? moves_vote(c) : any_vote(c))
             o << "u32 PL" << c << " = 0u, MI" << c << " = 0u;\n";
     for (int r = 0; r < n_fixed; ++r) {
         emit_reward(r);
@@ -354,6 +365,8 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
         o << "if (ANY(";
         for (int r = n_fixed; r < R; ++r) o << (r > n_fixed ? " | " : "") << "M" << r;
         o << ")) {\n";
+        for (int c = 0; c < C; ++c)
+            if (any_vote(c) && !moves_vote(c)) o << "u32 PL" << c << " = 0u, MI" << c << " = 0u;\n";
         for (int r = n_fixed; r < R; ++r) {
             const std::string M = "M" + std::to_string(r);
             const size_t pr = probe[r];
@@ -396,6 +409,7 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
             voted.push_back(c);
             if (!pl[c].empty() && !mi[c].empty()) both.push_back(c);
         }
+        // the one-sign result of every plane comes first, off the exact-count branch's path
         for (int c : voted)
             o << "u32 N" << c << " = (p[" << c << "] | PL" << c << ") & ~MI" << c << ";\n";
         if (!both.empty()) {
@@ -442,22 +456,12 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
         for (int c : voted) o << "p[" << c << "] = N" << c << ";\n";
     };
     if (track) {
-        // Steps where no loaded rule voted (most steps of sparse rule sets) write only the
-        // moves' channels and count only the moves' votes.  The probe test's branch is still
-        // open here: its "no" side gets a copy of the moves' write of its own, so that the
-        // loaded rules' vote words never need a value on that side.
-        std::vector<std::vector<Vote>> mpl(C), mmi(C);
-        for (int c = 0; c < C; ++c) {
-            for (const Vote &v : plus[c])
-                if (v.r < n_fixed) mpl[c].push_back(v);
-            for (const Vote &v : minus[c])
-                if (v.r < n_fixed) mmi[c].push_back(v);
-        }
+        // Steps where a loaded rule voted write inside the probe test's branch; all others
+        // (most steps of sparse rule sets) write only the moves' channels and count only the
+        // moves' votes.
         o << "if (lf) {\n";
         emit_write(plus, minus);
-        o << "} else {\n";
-        emit_write(mpl, mmi);
-        o << "}\n} else {\n";
+        o << "}\n}\nif (!lf) {\n";
         emit_write(mpl, mmi);
         o << "}\n";
     } else {
