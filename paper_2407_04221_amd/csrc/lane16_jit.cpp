@@ -322,7 +322,7 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
         const std::string M = "M" + std::to_string(r);
         if (rules[r].reward != 0)
             o << "rA += " << rules[r].reward << " * (int)__popc(" << M << " & 0xFFFFu); rB += "
-              << rules[r].reward << " * (int)__popc(" << M << " >> 16);\n";
+              << rules[r].reward << " * (int)__popc(" << M << " >> 16); paid = true;\n";
     };
 
     // The built-in moves (rules 0..3) are cheap and fire in most waves: evaluated in full,
@@ -572,7 +572,7 @@ std::string lane16_rules_body_sequential(int C, int H, int W, const std::vector<
         if (inhibits[r]) o << "A" << r << " = M;\n";
         if (ru.reward != 0)
             o << "rA += " << ru.reward << " * (int)__popc(M & 0xFFFFu); rB += " << ru.reward
-              << " * (int)__popc(M >> 16);\n";
+              << " * (int)__popc(M >> 16); paid = true;\n";
         // votes of this rule
         std::set<int> js;
         std::vector<int> touched, both;

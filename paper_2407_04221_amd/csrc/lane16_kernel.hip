@@ -199,7 +199,10 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
                 g[d] = u32(__builtin_amdgcn_ds_bpermute(src_base + (s1 << 2), int(cur[d])));
         }
 
+        // per-lane reward sums; `paid`: some rule with a reward matched somewhere in the wave
+        // (set by the generated code, only under wave-uniform branches)
         int rA = 0, rB = 0;
+        bool paid = false;
 #ifdef AV_RANDOM_SITES
         const unsigned long long nstep = step_base + (unsigned long long)k;
         bool keys_ready = false;
@@ -221,7 +224,7 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
 
 #ifndef AV_NO_REWARD
         // reward: sum of the row's 16 lanes
-        if (ANY(u32(rA | rB))) {
+        if (paid) {
             rA += DPP_ROR(rA, 1);
             rA += DPP_ROR(rA, 2);
             rA += DPP_ROR(rA, 4);
@@ -231,6 +234,8 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
             rB += DPP_ROR(rB, 4);
             rB += DPP_ROR(rB, 8);
         }
+#else
+        (void)paid;
 #endif
         // keep this step's results in lane s; store 16 steps at once
         if (y == s) {
