@@ -409,49 +409,45 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
             voted.push_back(c);
             if (!pl[c].empty() && !mi[c].empty()) both.push_back(c);
         }
-        // the one-sign result of every plane comes first, off the exact-count branch's path
+        // the one-sign result of every plane comes first, off the exact-count branches' path;
+        // each channel with votes of both signs is then recounted only in waves where some
+        // cell of that channel got both
         for (int c : voted)
             o << "u32 N" << c << " = (p[" << c << "] | PL" << c << ") & ~MI" << c << ";\n";
-        if (!both.empty()) {
-            o << "u32 CF = 0u;\n";
-            for (int c : both) o << "CF |= PL" << c << " & MI" << c << ";\n";
-            o << "if (ANY(CF)) {\n";
+        auto tname = [](int r, int i, int j) {
+            return "T" + std::to_string(r) + "_" + std::to_string(i) + "_" + std::to_string(j);
+        };
+        for (int c : both) {
+            o << "if (ANY(PL" << c << " & MI" << c << ")) { // channel " << c << ": " << pl[c].size()
+              << " + votes, " << mi[c].size() << " - votes\n";
             std::set<std::pair<int, int>> shifts;
             std::set<std::tuple<int, int, int>> terms;
-            for (int c : both)
-                for (auto *lst : {&pl[c], &mi[c]})
-                    for (const Vote &v : *lst) {
-                        if (v.j) shifts.insert({v.r, v.j});
-                        terms.insert({v.r, v.i, v.j});
-                    }
+            for (auto *lst : {&pl[c], &mi[c]})
+                for (const Vote &v : *lst) {
+                    if (v.j) shifts.insert({v.r, v.j});
+                    terms.insert({v.r, v.i, v.j});
+                }
             for (auto &sh : shifts)
                 o << "const u32 E" << sh.first << "_" << sh.second << " = M" << sh.first << " << "
                   << sh.second << ";\n";
-            auto tname = [](int r, int i, int j) {
-                return "T" + std::to_string(r) + "_" + std::to_string(i) + "_" + std::to_string(j);
-            };
             for (auto &t : terms) {
                 const int r = std::get<0>(t), i = std::get<1>(t), j = std::get<2>(t);
                 const std::string src = j ? "E" + std::to_string(r) + "_" + std::to_string(j) : "M" + std::to_string(r);
                 o << "const u32 " << tname(r, i, j) << " = "
                   << (i ? "DPP_SHR(" + src + ", " + std::to_string(i) + ")" : src) << ";\n";
             }
-            for (int c : both) {
-                std::vector<std::string> pt{"p[" + std::to_string(c) + "]"}, mt;
-                for (const Vote &v : pl[c]) pt.push_back(tname(v.r, v.i, v.j));
-                for (const Vote &v : mi[c]) mt.push_back(tname(v.r, v.i, v.j));
-                o << "{ // channel " << c << ": " << pt.size() - 1 << " + votes, " << mt.size() << " - votes\n";
-                const std::vector<std::string> P = g.count(pt), Nn = g.count(mt);
-                const size_t K = std::max(P.size(), Nn.size());
-                o << "u32 GT = 0u, EQ = 0xFFFFFFFFu;\n";
-                for (size_t k = K; k-- > 0;) {
-                    const std::string pk = k < P.size() ? P[k] : "0u", nk = k < Nn.size() ? Nn[k] : "0u";
-                    o << "GT |= EQ & " << pk << " & ~" << nk << ";\n";
-                    o << "EQ &= ~(" << pk << " ^ " << nk << ");\n";
-                }
-                o << "N" << c << " = GT;\n}\n";
+            std::vector<std::string> pt{"p[" + std::to_string(c) + "]"}, mt;
+            for (const Vote &v : pl[c]) pt.push_back(tname(v.r, v.i, v.j));
+            for (const Vote &v : mi[c]) mt.push_back(tname(v.r, v.i, v.j));
+            const std::vector<std::string> P = g.count(pt), Nn = g.count(mt);
+            const size_t K = std::max(P.size(), Nn.size());
+            o << "u32 GT = 0u, EQ = 0xFFFFFFFFu;\n";
+            for (size_t k = K; k-- > 0;) {
+                const std::string pk = k < P.size() ? P[k] : "0u", nk = k < Nn.size() ? Nn[k] : "0u";
+                o << "GT |= EQ & " << pk << " & ~" << nk << ";\n";
+                o << "EQ &= ~(" << pk << " ^ " << nk << ");\n";
             }
-            o << "}\n";
+            o << "N" << c << " = GT;\n}\n";
         }
         for (int c : voted) o << "p[" << c << "] = N" << c << ";\n";
     };
