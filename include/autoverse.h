@@ -56,18 +56,19 @@ typedef enum {
     AV_ESTATE = 4    /* call out of order, e.g. av_step before av_load_rules and av_reset */
 } av_status;
 
-/* Kernel family used by av_step / av_step_n.  AUTO picks lane16 when eligible; else rows
- * when eligible, unless the rule sets are per environment and H > 16 (then wave, the faster
- * of the two there); else wave when its LDS working set (C + 1 padded planes, one match
- * plane per rule, two vote accumulators per plane) fits in 64 KiB; else generic. */
+/* Kernel family used by av_step / av_step_n.  AUTO picks lane16 when eligible; else, for
+ * per-environment rule sets, wave when its LDS working set (C + 1 padded planes, one match
+ * plane per rule, two vote accumulators per plane) fits in 64 KiB; else rows when eligible;
+ * else wave when it fits; else generic. */
 typedef enum {
     AV_ENGINE_AUTO = 0,
     AV_ENGINE_GENERIC = 1,  /* any size within the limits below; maps staged in LDS */
     AV_ENGINE_LANE16 = 2,   /* maps of at most 16 x 16 and one shared rule set: one map
                                row per lane, two maps per 32-bit lane word, rows shifted
                                across lanes with DPP, the rule set compiled into the kernel */
-    AV_ENGINE_WAVE = 3,     /* one environment per workgroup, map rows in LDS; four groups
-                               of lanes match four of its rules at once */
+    AV_ENGINE_WAVE = 3,     /* one environment per workgroup, map rows in LDS; groups of
+                               lanes (16 on maps of at most 16 rows, else 4) match that many
+                               of its rules at once */
     AV_ENGINE_ROWS = 4      /* one environment per 64-lane wave with no barriers, map row y
                                in lane y, planes in the wave's LDS; one lane per rule tests
                                every rule's rarest entries at once, so only rules that can

@@ -343,11 +343,12 @@ av_status av_create_batch(const av_config *cfg, av_batch_t *out) {
     b->envs_per_block = std::max(1, std::min(256 / c.height, int(kLdsBudget / env_lds)));
     if (c.engine != AV_ENGINE_AUTO) b->engine = c.engine;
     else if (lane16_ok) b->engine = AV_ENGINE_LANE16;
-    // measured on MI355X: rows is the faster engine except for per-environment rule sets on
-    // maps taller than 16 rows, where a few crowded environments (many player cells, most
-    // rules partly matching) set the launch time and the wave engine's four rule groups per
-    // environment finish them sooner
-    else if (rows_ok && !(c.per_env_rules && c.height > 16 && wave_ok)) b->engine = AV_ENGINE_ROWS;
+    // measured on MI355X: per-environment rule sets run faster on the wave engine (its rule
+    // groups match many rules of a crowded environment at once: c3 literal, c2 with rules
+    // that fire; c2 literal is within 3 % of rows), shared sets the lane16 engine cannot
+    // take on rows (c5: 3.2 against 7.7 us per step)
+    else if (c.per_env_rules && wave_ok) b->engine = AV_ENGINE_WAVE;
+    else if (rows_ok) b->engine = AV_ENGINE_ROWS;
     else b->engine = wave_ok ? AV_ENGINE_WAVE : AV_ENGINE_GENERIC;
     b->plain_engine = b->engine;
     hipError_t e = hipMalloc(&b->d_state, b->state_bytes);

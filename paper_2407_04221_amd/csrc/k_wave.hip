@@ -1,9 +1,9 @@
-// wave engine: one environment per workgroup, its rules split over four row groups.
+// wave engine: one environment per workgroup, its rules split over row groups.
 //
-// A workgroup holds one environment.  Its threads form four groups of Hq lanes (Hq = 16,
-// 32 or 64 rows, the map height rounded up); lane y of every group owns map row y.  Group
-// g evaluates rules g, g+4, g+8, ... so four rules are matched at once, and with one
-// environment per workgroup the environment's own rules need no per-lane selection:
+// A workgroup holds one environment.  Its threads form G groups of Hq lanes (Hq = 16, 32 or
+// 64 rows, the map height rounded up; G from 4 up to 256 / Hq, the most for which the whole
+// batch fits the device's wave slots at once); lane y of every group owns map row y.  Group g evaluates rules g, g+G, g+2G, ... so G rules are matched at once, and
+// with one environment per workgroup the environment's own rules need no per-lane selection:
 // every lane of a group reads the same rule entry.  The rule program (headers, input
 // entries rarest first, rule-major votes) is copied into LDS once per launch when it fits.
 //
@@ -35,6 +35,8 @@
 // row-major prefix of per-row counts or, for the random index channel (Philox keys computed
 // into LDS once per step), a radix select over a 256-bin LDS histogram — and the groups cast
 // the filtered rules' votes and rewards before the write.
+#include <atomic>
+
 #include "av_internal.h"
 #include "philox.h"
 
@@ -43,7 +45,6 @@ namespace {
 
 constexpr int kPad = 16;       // zero rows below the planes and above the match planes
 constexpr int kMRows = kPad + 64;
-constexpr int kGroups = 4;
 
 template <typename RowT>
 __device__ inline RowT load_row(const void *base, size_t idx, int row_bytes) {
@@ -140,6 +141,7 @@ __device__ RowT exact_channel(int c, RowT old, int rb, int re, const int *fired,
 
 struct WaveLayout {
     int Hq;          // lanes per group (16, 32 or 64)
+    int G;           // groups of Hq lanes
     int prog_lds;    // 1 if the rule program is copied into LDS
     int hdr_words, match_words, vote_words;
     int ctl_words;   // LDS words of the control scratch (0 without control)
@@ -153,7 +155,7 @@ int ctl_scratch_words(int H, int W, bool control, bool random) {
 template <typename RowT>
 __global__ void __launch_bounds__(256) wave_step(StepArgs a, WaveLayout L) {
     extern __shared__ __align__(16) unsigned char lds[];
-    const int H = a.H, W = a.W, C = a.C, C1 = C + 1, Hp = a.H + kPad, Hq = L.Hq;
+    const int H = a.H, W = a.W, C = a.C, C1 = C + 1, Hp = a.H + kPad, Hq = L.Hq, G = L.G;
     const int Rt = a.prog.rules_per_set;
     const int tid = threadIdx.x, nthreads = blockDim.x;
     const int g = tid / Hq, y = tid - g * Hq;
@@ -193,7 +195,7 @@ __global__ void __launch_bounds__(256) wave_step(StepArgs a, WaveLayout L) {
     }
     __syncthreads();
     if (row)
-        for (int c = g; c < C; c += kGroups)
+        for (int c = g; c < C; c += G)
             P[c * Hp + y] = load_row<RowT>(a.state, (size_t(c) * a.B + b) * H + y, a.row_bytes);
     int t_env = a.t[b];
     const RowT rowmask = low_mask<RowT>(W);
@@ -232,8 +234,8 @@ __global__ void __launch_bounds__(256) wave_step(StepArgs a, WaveLayout L) {
         for (int rb = 0, re = 0; rb < Rt; rb = re) {
             re = a.sequential ? rb + 1 : Rt;
             if (rb > 0) __syncthreads();          // the previous batch's rows are all written
-            // group g takes rules rb+g, rb+g+4, ...; a rule that fired casts its votes at once
-            for (int r = rb + g; r < re; r += kGroups) {
+            // group g takes rules rb+g, rb+g+G, ...; a rule that fired casts its votes at once
+            for (int r = rb + g; r < re; r += G) {
                 const uint32_t *hw = hdrw + r * kHdrWords;
                 const int hn = int(hw[0]), hm = int(hw[1]), hreward = int(hw[2]);
                 const int moff = int(hw[3]), mcnt = int(hw[4]), voff = int(hw[5]), vcnt = int(hw[6]);
@@ -364,8 +366,8 @@ __global__ void __launch_bounds__(256) wave_step(StepArgs a, WaveLayout L) {
                     }
                     __syncthreads();
                 }
-                // rewards and votes of the filtered loaded rules, group g taking rules g, g+4, ...
-                for (int r = r0 + ((g - r0 % kGroups + kGroups) % kGroups); r < re; r += kGroups) {
+                // rewards and votes of the filtered loaded rules, group g taking rules g, g+G, ...
+                for (int r = r0 + ((g - r0 % G + G) % G); r < re; r += G) {
                     if (!fired[r]) continue;
                     const uint32_t *hw = hdrw + r * kHdrWords;
                     const int hreward = int(hw[2]), voff = int(hw[5]), vcnt = int(hw[6]);
@@ -381,8 +383,8 @@ __global__ void __launch_bounds__(256) wave_step(StepArgs a, WaveLayout L) {
                 __syncthreads();
             }
 
-            // new rows: group g rewrites planes g, g+4, ... (each lane its own row)
-            for (int c = g; c < Cw; c += kGroups) {
+            // new rows: group g rewrites planes g, g+G, ... (each lane its own row)
+            for (int c = g; c < Cw; c += G) {
                 const RowT old = P[c * Hp + ry];
                 const RowT pl = PL[c * 64 + y], mi = MI[c * 64 + y];
                 RowT nw = (old | pl) & ~mi;
@@ -397,7 +399,7 @@ __global__ void __launch_bounds__(256) wave_step(StepArgs a, WaveLayout L) {
         if (rsum) atomicAdd(red, rsum);
 
         // episode end, reward, outputs, reset
-        const bool anyp = __syncthreads_or(g == kChPlayer % kGroups && row &&
+        const bool anyp = __syncthreads_or(g == kChPlayer % G && row &&
                                            P[kChPlayer * Hp + y] != 0) != 0;
         t_env += 1;
         const bool d = !anyp || (a.L > 0 && t_env == a.L);
@@ -407,18 +409,39 @@ __global__ void __launch_bounds__(256) wave_step(StepArgs a, WaveLayout L) {
             a.done[size_t(k) * a.B + b] = uint8_t(d);
         }
         if (d && row)
-            for (int c = g; c < C; c += kGroups)
+            for (int c = g; c < C; c += G)
                 P[c * Hp + y] = load_row<RowT>(a.init, (size_t(c) * a.B + b) * H + y, a.row_bytes);
     }
 
     __syncthreads();
     if (row)
-        for (int c = g; c < C; c += kGroups)
+        for (int c = g; c < C; c += G)
             store_row<RowT>(a.state, (size_t(c) * a.B + b) * H + y, a.row_bytes, P[c * Hp + y]);
     if (tid == 0) a.t[b] = t_env;
 }
 
 int rows_per_group(int H) { return H <= 16 ? 16 : (H <= 32 ? 32 : 64); }
+
+// Groups per workgroup: the most (up to 256 threads) for which the whole batch still fits the
+// device's wave slots (8 waves per SIMD, 4 SIMDs per CU) at once, else 4.  More groups match
+// more of a crowded environment's rules at once (c2, 1024 environments: 16 groups are 28-43 %
+// faster than 4), but past that point they only add rounds of workgroups (c4 on this engine,
+// 16384 environments: 36 against 18 us per step; c3, 4096: 8 groups 10 % slower than 4).
+int wave_groups(int B, int Hq) {
+    static std::atomic<int> cus[64];                 // per device, 0 until first asked
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 4;
+    int n = cus[dev].load(std::memory_order_relaxed);
+    if (!n) {
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+            return 4;
+        cus[dev].store(n, std::memory_order_relaxed);
+    }
+    const long long slots = 32LL * n;
+    for (int G = 256 / Hq; G > 4; G /= 2)
+        if (static_cast<long long>(B) * (G * Hq / 64) <= slots) return G;
+    return 4;
+}
 
 size_t wave_base_bytes(int H, int W, int C, int rules_per_set) {
     const size_t rowb = W <= 32 ? 4 : 8;
@@ -437,6 +460,7 @@ size_t wave_lds_bytes(int H, int W, int C, int rules_per_set, bool control, bool
 hipError_t launch_wave_step(const StepArgs &a, hipStream_t s) {
     WaveLayout L;
     L.Hq = rows_per_group(a.H);
+    L.G = wave_groups(a.B, L.Hq);
     L.hdr_words = int(a.prog.rules_per_set * (sizeof(RuleHdr) / 4));
     L.match_words = a.prog.match_stride;
     L.vote_words = a.prog.rvote_stride;
@@ -447,7 +471,7 @@ hipError_t launch_wave_step(const StepArgs &a, hipStream_t s) {
     // the copy pays for itself over a launch of many steps, not over one
     L.prog_lds = a.k >= 16 && base + prog <= size_t(kLdsBudget) ? 1 : 0;
     const size_t lds = base + (L.prog_lds ? prog : 0);
-    const int threads = kGroups * L.Hq;
+    const int threads = L.G * L.Hq;
     if (a.W <= 32)
         hipLaunchKernelGGL(wave_step<uint32_t>, dim3(a.B), dim3(threads), lds, s, a, L);
     else
