@@ -66,9 +66,9 @@ typedef enum {
     AV_ENGINE_LANE16 = 2,   /* maps of at most 16 x 16 and one shared rule set: one map
                                row per lane, two maps per 32-bit lane word, rows shifted
                                across lanes with DPP, the rule set compiled into the kernel */
-    AV_ENGINE_WAVE = 3,     /* one environment per workgroup, map rows in LDS; groups of
-                               lanes (16 on maps of at most 16 rows, else 4) match that many
-                               of its rules at once */
+    AV_ENGINE_WAVE = 3,     /* one environment per workgroup, map rows in LDS; 4 to 64
+                               groups of lanes (as many as the batch's size leaves room for)
+                               match that many of its rules at once */
     AV_ENGINE_ROWS = 4      /* one environment per 64-lane wave with no barriers, map row y
                                in lane y, planes in the wave's LDS; one lane per rule tests
                                every rule's rarest entries at once, so only rules that can

@@ -1,8 +1,9 @@
 // wave engine: one environment per workgroup, its rules split over row groups.
 //
 // A workgroup holds one environment.  Its threads form G groups of Hq lanes (Hq = 16, 32 or
-// 64 rows, the map height rounded up; G from 4 up to 256 / Hq, the most for which the whole
-// batch fits the device's wave slots at once); lane y of every group owns map row y.  Group g evaluates rules g, g+G, g+2G, ... so G rules are matched at once, and
+// 64 rows, the map height rounded up; G from 4 up to 1024 / Hq threads for 32-bit rows, 512 /
+// Hq for 64-bit rows, the most for which the whole batch fits the device's wave slots at
+// once, and no more than the rules need); lane y of every group owns map row y.  Group g evaluates rules g, g+G, g+2G, ... so G rules are matched at once, and
 // with one environment per workgroup the environment's own rules need no per-lane selection:
 // every lane of a group reads the same rule entry.  The rule program (headers, input
 // entries rarest first, rule-major votes) is copied into LDS once per launch when it fits.
@@ -35,6 +36,7 @@
 // row-major prefix of per-row counts or, for the random index channel (Philox keys computed
 // into LDS once per step), a radix select over a 256-bin LDS histogram — and the groups cast
 // the filtered rules' votes and rewards before the write.
+#include <algorithm>
 #include <atomic>
 
 #include "av_internal.h"
@@ -152,8 +154,10 @@ int ctl_scratch_words(int H, int W, bool control, bool random) {
     return control ? 64 + 4 + 256 + (random ? H * W : 0) : 0;
 }
 
-template <typename RowT>
-__global__ void __launch_bounds__(256) wave_step(StepArgs a, WaveLayout L) {
+// kMaxThreads: 1024 for 32-bit rows, 512 for 64-bit rows (their registers fit two waves per
+// SIMD, not four)
+template <typename RowT, int kMaxThreads>
+__global__ void __launch_bounds__(kMaxThreads) wave_step(StepArgs a, WaveLayout L) {
     extern __shared__ __align__(16) unsigned char lds[];
     const int H = a.H, W = a.W, C = a.C, C1 = C + 1, Hp = a.H + kPad, Hq = L.Hq, G = L.G;
     const int Rt = a.prog.rules_per_set;
@@ -422,12 +426,13 @@ __global__ void __launch_bounds__(256) wave_step(StepArgs a, WaveLayout L) {
 
 int rows_per_group(int H) { return H <= 16 ? 16 : (H <= 32 ? 32 : 64); }
 
-// Groups per workgroup: the most (up to 256 threads) for which the whole batch still fits the
-// device's wave slots (8 waves per SIMD, 4 SIMDs per CU) at once, else 4.  More groups match
-// more of a crowded environment's rules at once (c2, 1024 environments: 16 groups are 28-43 %
-// faster than 4), but past that point they only add rounds of workgroups (c4 on this engine,
-// 16384 environments: 36 against 18 us per step; c3, 4096: 8 groups 10 % slower than 4).
-int wave_groups(int B, int Hq) {
+// Groups per workgroup: the most for which the whole batch still fits the device's wave
+// slots (8 waves per SIMD, 4 SIMDs per CU) at once, at most max_threads / Hq and at most the
+// rule count rounded up to a power of two; else 4.  More groups match more of an
+// environment's rules at once (c2, 1024 environments: 16 groups are 28-43 % faster than 4),
+// but past the wave slots they only add rounds of workgroups (c4 on this engine, 16384
+// environments: 36 against 18 us per step; c3, 4096: 8 groups 10 % slower than 4).
+int wave_groups(int B, int Hq, int rules, int max_threads) {
     static std::atomic<int> cus[64];                 // per device, 0 until first asked
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 4;
@@ -438,7 +443,9 @@ int wave_groups(int B, int Hq) {
         cus[dev].store(n, std::memory_order_relaxed);
     }
     const long long slots = 32LL * n;
-    for (int G = 256 / Hq; G > 4; G /= 2)
+    int cap = 4;
+    while (cap < rules) cap *= 2;
+    for (int G = std::min(max_threads / Hq, cap); G > 4; G /= 2)
         if (static_cast<long long>(B) * (G * Hq / 64) <= slots) return G;
     return 4;
 }
@@ -460,7 +467,8 @@ size_t wave_lds_bytes(int H, int W, int C, int rules_per_set, bool control, bool
 hipError_t launch_wave_step(const StepArgs &a, hipStream_t s) {
     WaveLayout L;
     L.Hq = rows_per_group(a.H);
-    L.G = wave_groups(a.B, L.Hq);
+    const int max_threads = a.W <= 32 ? 1024 : 512;
+    L.G = wave_groups(a.B, L.Hq, a.prog.rules_per_set, max_threads);
     L.hdr_words = int(a.prog.rules_per_set * (sizeof(RuleHdr) / 4));
     L.match_words = a.prog.match_stride;
     L.vote_words = a.prog.rvote_stride;
@@ -473,9 +481,9 @@ hipError_t launch_wave_step(const StepArgs &a, hipStream_t s) {
     const size_t lds = base + (L.prog_lds ? prog : 0);
     const int threads = L.G * L.Hq;
     if (a.W <= 32)
-        hipLaunchKernelGGL(wave_step<uint32_t>, dim3(a.B), dim3(threads), lds, s, a, L);
+        hipLaunchKernelGGL((wave_step<uint32_t, 1024>), dim3(a.B), dim3(threads), lds, s, a, L);
     else
-        hipLaunchKernelGGL(wave_step<uint64_t>, dim3(a.B), dim3(threads), lds, s, a, L);
+        hipLaunchKernelGGL((wave_step<uint64_t, 512>), dim3(a.B), dim3(threads), lds, s, a, L);
     return hipGetLastError();
 }
 
