@@ -47,6 +47,7 @@ namespace {
 
 constexpr int kPad = 16;       // zero rows below the planes and above the match planes
 constexpr int kMRows = kPad + 64;
+constexpr int kBlock = 64;      // steps per block of actions, rewards and done flags
 
 template <typename RowT>
 __device__ inline RowT load_row(const void *base, size_t idx, int row_bytes) {
@@ -175,11 +176,18 @@ __global__ void __launch_bounds__(kMaxThreads) wave_step(StepArgs a, WaveLayout 
     RowT *MI = PL + size_t(C1) * 64;              // [C1][64]
     int *fired = reinterpret_cast<int *>(MI + size_t(C1) * 64);  // [Rt]
     int *red = fired + Rt;                        // [1] reward sum
-    int *rowcnt = red + 2;                        // control scratch (ctl_words words)
+    // Per block of 64 steps: the environment's actions, loaded at the block's first step,
+    // and its rewards and done flags, stored after its last; a barrier waits for every
+    // outstanding global access of the workgroup, so one load and one store per step would
+    // each cost a memory latency per step.
+    int *acts = red + 2;                          // [64]
+    float *rblk = reinterpret_cast<float *>(acts + kBlock);    // [64]
+    int *dblk = acts + 2 * kBlock;                // [64]
+    int *rowcnt = acts + 3 * kBlock;              // control scratch (ctl_words words)
     int *ccnt = rowcnt + 64;
     int *hist = ccnt + 4;
     uint32_t *keys = reinterpret_cast<uint32_t *>(hist + 256);
-    uint32_t *pcopy = reinterpret_cast<uint32_t *>(red + 2 + L.ctl_words);   // program copy
+    uint32_t *pcopy = reinterpret_cast<uint32_t *>(rowcnt + L.ctl_words);   // program copy
 
     const size_t words = size_t(C1) * Hp + size_t(Rt) * kMRows + size_t(2) * C1 * 64;
     for (size_t w = tid; w < words; w += nthreads) P[w] = 0;
@@ -205,12 +213,24 @@ __global__ void __launch_bounds__(kMaxThreads) wave_step(StepArgs a, WaveLayout 
     const RowT rowmask = low_mask<RowT>(W);
     constexpr int kHdrWords = sizeof(RuleHdr) / 4;
 
+    // rewards and done flags of the block of 64 steps that ends before step k0
+    auto flush = [&](int k0, int n) {
+        if (tid < n) {
+            a.rewards[size_t(k0 + tid) * a.B + b] = rblk[tid];
+            a.done[size_t(k0 + tid) * a.B + b] = uint8_t(dblk[tid]);
+        }
+    };
     for (int k = 0; k < a.k; ++k) {
         for (int r = tid; r < Rt; r += nthreads) fired[r] = 0;
         if (tid == 0) *red = 0;
+        const int kb = k & (kBlock - 1);
+        if (kb == 0 && tid < kBlock && k + tid < a.k) acts[tid] = a.actions[size_t(k + tid) * a.B + b];
         __syncthreads();                          // previous step's rows are all written
+        // the previous block's results (thread 0 wrote the last one after step k-1's final
+        // barrier, so only after this one may other threads read it)
+        if (kb == 0 && k > 0) flush(k - kBlock, kBlock);
         if (g == 0) {
-            const int act = a.actions[size_t(k) * a.B + b];
+            const int act = acts[kb];
             const RowT *Pp = P + kChPlayer * Hp;
             RowT f = 0;
             if (act == 1) f = Pp[ry + 1];         // row H is a zero pad row
@@ -409,8 +429,8 @@ __global__ void __launch_bounds__(kMaxThreads) wave_step(StepArgs a, WaveLayout 
         const bool d = !anyp || (a.L > 0 && t_env == a.L);
         if (d) t_env = 0;
         if (tid == 0) {
-            a.rewards[size_t(k) * a.B + b] = float(*red);
-            a.done[size_t(k) * a.B + b] = uint8_t(d);
+            rblk[kb] = float(*red);
+            dblk[kb] = d ? 1 : 0;
         }
         if (d && row)
             for (int c = g; c < C; c += G)
@@ -418,6 +438,10 @@ __global__ void __launch_bounds__(kMaxThreads) wave_step(StepArgs a, WaveLayout 
     }
 
     __syncthreads();
+    if (a.k > 0) {
+        const int n = ((a.k - 1) & (kBlock - 1)) + 1;
+        flush(a.k - n, n);
+    }
     if (row)
         for (int c = g; c < C; c += G)
             store_row<RowT>(a.state, (size_t(c) * a.B + b) * H + y, a.row_bytes, P[c * Hp + y]);
@@ -454,7 +478,7 @@ size_t wave_base_bytes(int H, int W, int C, int rules_per_set) {
     const size_t rowb = W <= 32 ? 4 : 8;
     return (size_t(C + 1) * (H + kPad) + size_t(rules_per_set) * kMRows + size_t(2) * (C + 1) * 64) *
                rowb +
-           sizeof(int) * (size_t(rules_per_set) + 2);
+           sizeof(int) * (size_t(rules_per_set) + 2 + 3 * kBlock);
 }
 
 }  // namespace

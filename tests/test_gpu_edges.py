@@ -40,10 +40,10 @@ def engines(name):
     wl = CASES[name]
     out = ["generic", "lane16"] if name in LANE16 else ["generic"]
     # the wave engine: C + 1 planes of H + 16 rows, one 80-row match plane per rule, two
-    # 64-row vote accumulators per plane (4-byte rows for W <= 32, else 8) and a word per rule
-    # within 64 KiB
+    # 64-row vote accumulators per plane (4-byte rows for W <= 32, else 8), a word per rule
+    # and three 64-word step blocks within 64 KiB
     rowb, rt = (4 if wl.W <= 32 else 8), wl.R + 4
-    if ((wl.C + 1) * (wl.H + 16) + rt * 80 + 2 * (wl.C + 1) * 64) * rowb + 4 * (rt + 2) <= 65536:
+    if ((wl.C + 1) * (wl.H + 16) + rt * 80 + 2 * (wl.C + 1) * 64) * rowb + 4 * (rt + 2 + 192) <= 65536:
         out.append("wave")
     return out + (["rows"] if rows_ok(wl) else [])
 
