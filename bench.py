@@ -33,7 +33,8 @@ KERNEL_SOURCES = {
     "wave": ("paper_2407_04221_amd/csrc/k_wave.hip",),
     "rows": ("paper_2407_04221_amd/csrc/k_rows.hip",),
     "lane16": ("paper_2407_04221_amd/csrc/lane16_kernel.hip",
-               "paper_2407_04221_amd/csrc/lane16_jit.cpp"),
+               "paper_2407_04221_amd/csrc/lane16_jit.cpp",
+               "paper_2407_04221_amd/csrc/codegen.h"),
 }
 
 

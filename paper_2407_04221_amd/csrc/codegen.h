@@ -1,0 +1,139 @@
+// Pieces of the rule-set-to-kernel-code generator (lane16): pattern entries in rarest-first
+// order, the vote of one pattern cell, how many entries a rule is probed with, and the
+// emitter of bit-sliced vote counts.
+#pragma once
+
+#include <algorithm>
+#include <cstdlib>
+#include <deque>
+#include <sstream>
+#include <string>
+#include <vector>
+
+#include "av_internal.h"
+
+namespace av {
+namespace codegen {
+
+// One specified input entry of a rule: channel c (C = the force plane) at pattern row i,
+// column j must be `want`; `rank` orders entries rarest first.
+struct Entry {
+    int c, i, j, want, rank;
+};
+
+// Rarest evidence first: force and player bits are rare, walls and empty tiles common;
+// a must-be-1 entry rejects more anchors than a must-be-0 entry.
+inline int rank_of(int c, int want, int C) {
+    int ch;
+    if (c == C) ch = 0;
+    else if (c == kChPlayer) ch = 1;
+    else if (c == kChGoal || c >= 4) ch = 2;
+    else if (c == kChWall) ch = 3;
+    else ch = 4;
+    return (want ? 0 : 8) + ch;
+}
+
+// The vote K_O of one pattern cell-channel: +1, -1 or 0 (in, out in {-1 = don't care, 0, 1}).
+inline int kout(int in, int out) {
+    if (out < 0) return 0;
+    if (out == 1) return in == 1 ? 0 : 1;
+    return in == 0 ? 0 : -1;
+}
+
+// A vote of rule r at pattern row i, column j.
+struct Vote {
+    int r, i, j;
+};
+
+// Number of entries a loaded rule is probed with before the wave-wide test: at least two, at
+// most four, more while a static guess of the share of waves (`maps` maps each) in which
+// some anchor passes them stays above 10 %.  The guess uses the synthetic maps' statistics:
+// one player cell per map with its force cell beside it, walls on 30 % of the cells, the
+// other tile types sharing the rest evenly.  It only decides how much of a rule runs before
+// the test, never what the rule computes.
+inline size_t probe_len(const std::vector<Entry> &es, int C, int H, int W, int n, int m, int maps) {
+    const double cells = double(H) * W, anchors = double(H - n + 1) * (W - m + 1);
+    const size_t lo = std::min<size_t>(2, es.size()), hi = std::min<size_t>(4, es.size());
+    size_t k = 0;
+    double p = anchors;
+    for (; k < hi; ++k) {
+        if (k >= lo && maps * p <= 0.1) break;
+        const Entry &en = es[k];
+        double q1;
+        if (en.c == C || en.c == kChPlayer) {
+            q1 = 1.0 / cells;
+            for (size_t f = 0; f < k; ++f) {            // a force cell beside a player cell
+                const Entry &o = es[f];
+                const bool pair = (en.c == C && o.c == kChPlayer) || (en.c == kChPlayer && o.c == C);
+                if (pair && o.want && en.want && std::abs(o.i - en.i) + std::abs(o.j - en.j) == 1)
+                    q1 = 0.25;
+            }
+        } else if (en.c == kChWall) {
+            q1 = 0.3;
+        } else {
+            q1 = 0.7 / std::max(1, C - 2);
+        }
+        p *= en.want ? q1 : 1.0 - q1;
+    }
+    return k;
+}
+
+// Emits straight-line code into `o`; `type` is the lane word type of the generated kernel.
+class Gen {
+  public:
+    std::ostringstream o;
+    std::string type = "u32";
+    int tmp = 0;
+    std::string fresh() { return "t" + std::to_string(tmp++); }
+
+    // Bit-sliced population count of `terms` (each a plane word): returns the count's bits,
+    // least significant first, built from full and half adders.
+    std::vector<std::string> count(const std::vector<std::string> &terms) {
+        std::vector<std::deque<std::string>> lv(1, std::deque<std::string>(terms.begin(), terms.end()));
+        std::vector<std::string> bits;
+        for (size_t k = 0; k < lv.size(); ++k) {
+            std::deque<std::string> q = lv[k];
+            std::vector<std::string> carries;
+            while (q.size() >= 3) {
+                const std::string a = q[0], b = q[1], c = q[2];
+                q.pop_front(); q.pop_front(); q.pop_front();
+                const std::string s = fresh(), cy = fresh();
+                o << "const " << type << " " << s << " = " << a << " ^ " << b << " ^ " << c << ";\n";
+                o << "const " << type << " " << cy << " = (" << a << " & " << b << ") | (" << c
+                  << " & (" << a << " ^ " << b << "));\n";
+                q.push_back(s);
+                carries.push_back(cy);
+            }
+            if (q.size() == 2) {
+                const std::string a = q[0], b = q[1];
+                const std::string s = fresh(), cy = fresh();
+                o << "const " << type << " " << s << " = " << a << " ^ " << b << ";\n";
+                o << "const " << type << " " << cy << " = " << a << " & " << b << ";\n";
+                q.clear();
+                q.push_back(s);
+                carries.push_back(cy);
+            }
+            bits.push_back(q.empty() ? std::string("0") : q.front());
+            if (!carries.empty()) {
+                if (lv.size() == k + 1) lv.emplace_back();
+                lv[k + 1].insert(lv[k + 1].end(), carries.begin(), carries.end());
+            }
+        }
+        return bits;
+    }
+
+    // The cells where old + #plus > #minus: a bit-sliced comparison of two counts (bits least
+    // significant first), emitted as GT; the caller declares nothing.
+    void greater(const std::vector<std::string> &P, const std::vector<std::string> &N) {
+        const size_t K = std::max(P.size(), N.size());
+        o << type << " GT = 0, EQ = ~(" << type << ")0;\n";
+        for (size_t k = K; k-- > 0;) {
+            const std::string pk = k < P.size() ? P[k] : "0", nk = k < N.size() ? N[k] : "0";
+            o << "GT |= EQ & " << pk << " & ~" << nk << ";\n";
+            o << "EQ &= ~(" << pk << " ^ " << nk << ");\n";
+        }
+    }
+};
+
+}  // namespace codegen
+}  // namespace av

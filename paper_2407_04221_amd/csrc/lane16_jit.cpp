@@ -18,128 +18,30 @@
 //          old + sum >= 1 (Sec. 2.1 transposed-convolution write, clamped to {0, 1}).
 //   The force plane's own votes are not evaluated: the plane is dropped after the step.
 #include <hip/hip_runtime.h>
-#include <hip/hiprtc.h>
 
 #include <algorithm>
-#include <cstdlib>
-#include <deque>
 #include <map>
-#include <mutex>
 #include <set>
 #include <sstream>
 #include <string>
 #include <vector>
 
+#include "codegen.h"
+#include "jit.h"
 #include "lane16.h"
 
 namespace av {
 namespace {
 
+using codegen::Entry;
+using codegen::Gen;
+using codegen::Vote;
+using codegen::kout;
+using codegen::rank_of;
+
 #include "_lane16_template.inc"   // kLane16Template: lane16_kernel.hip as a string
 
 std::string plane(int c, int C) { return c == C ? std::string("F") : "p[" + std::to_string(c) + "]"; }
-
-struct Entry {
-    int c, i, j, want, rank;
-};
-
-// Rarest evidence first: force and player bits are rare, walls and empty tiles common;
-// a must-be-1 entry rejects more anchors than a must-be-0 entry.
-int rank_of(int c, int want, int C) {
-    int ch;
-    if (c == C) ch = 0;
-    else if (c == kChPlayer) ch = 1;
-    else if (c == kChGoal || c >= 4) ch = 2;
-    else if (c == kChWall) ch = 3;
-    else ch = 4;
-    return (want ? 0 : 8) + ch;
-}
-
-int kout(int in, int out) {
-    if (out < 0) return 0;
-    if (out == 1) return in == 1 ? 0 : 1;
-    return in == 0 ? 0 : -1;
-}
-
-struct Vote {
-    int r, i, j;
-};
-
-// Number of entries a loaded rule is probed with before the wave-wide test: at least two, at
-// most four, more while a static guess of the share of waves (eight maps each) in which some
-// anchor passes them stays above 10 %.  The guess uses the synthetic maps' statistics: one
-// player cell per map with its force cell beside it, walls on 30 % of the cells, the other
-// tile types sharing the rest evenly.  It only decides how much of a rule runs before the
-// test, never what the rule computes.
-size_t probe_len(const std::vector<Entry> &es, int C, int H, int W, int n, int m) {
-    const double cells = double(H) * W, anchors = double(H - n + 1) * (W - m + 1);
-    const size_t lo = std::min<size_t>(2, es.size()), hi = std::min<size_t>(4, es.size());
-    size_t k = 0;
-    double p = anchors;
-    for (; k < hi; ++k) {
-        if (k >= lo && 8.0 * p <= 0.1) break;
-        const Entry &en = es[k];
-        double q1;
-        if (en.c == C || en.c == kChPlayer) {
-            q1 = 1.0 / cells;
-            for (size_t f = 0; f < k; ++f) {            // a force cell beside a player cell
-                const Entry &o = es[f];
-                const bool pair = (en.c == C && o.c == kChPlayer) || (en.c == kChPlayer && o.c == C);
-                if (pair && o.want && en.want && std::abs(o.i - en.i) + std::abs(o.j - en.j) == 1)
-                    q1 = 0.25;
-            }
-        } else if (en.c == kChWall) {
-            q1 = 0.3;
-        } else {
-            q1 = 0.7 / std::max(1, C - 2);
-        }
-        p *= en.want ? q1 : 1.0 - q1;
-    }
-    return k;
-}
-
-class Gen {
-  public:
-    std::ostringstream o;
-    int tmp = 0;
-    std::string fresh() { return "t" + std::to_string(tmp++); }
-
-    // Bit-sliced population count of `terms` (each a 32-bit plane): returns the count's
-    // bits, least significant first, built from full and half adders.
-    std::vector<std::string> count(const std::vector<std::string> &terms) {
-        std::vector<std::deque<std::string>> lv(1, std::deque<std::string>(terms.begin(), terms.end()));
-        std::vector<std::string> bits;
-        for (size_t k = 0; k < lv.size(); ++k) {
-            std::deque<std::string> q = lv[k];
-            std::vector<std::string> carries;
-            while (q.size() >= 3) {
-                const std::string a = q[0], b = q[1], c = q[2];
-                q.pop_front(); q.pop_front(); q.pop_front();
-                const std::string s = fresh(), cy = fresh();
-                o << "const u32 " << s << " = " << a << " ^ " << b << " ^ " << c << ";\n";
-                o << "const u32 " << cy << " = (" << a << " & " << b << ") | (" << c << " & (" << a
-                  << " ^ " << b << "));\n";
-                q.push_back(s);
-                carries.push_back(cy);
-            }
-            if (q.size() == 2) {
-                const std::string a = q[0], b = q[1];
-                const std::string s = fresh(), cy = fresh();
-                o << "const u32 " << s << " = " << a << " ^ " << b << ";\n";
-                o << "const u32 " << cy << " = " << a << " & " << b << ";\n";
-                q.clear();
-                q.push_back(s);
-                carries.push_back(cy);
-            }
-            bits.push_back(q.empty() ? std::string("0u") : q.front());
-            if (!carries.empty()) {
-                if (lv.size() == k + 1) lv.emplace_back();
-                lv[k + 1].insert(lv[k + 1].end(), carries.begin(), carries.end());
-            }
-        }
-        return bits;
-    }
-};
 
 // Rule application control for rule r on its match word `M` (paper Sec. 2.1.1), after its
 // matches are complete and before its reward and votes.  `applied(q)` names the final match
@@ -266,7 +168,7 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
     std::vector<size_t> probe(R);
     for (int r = 0; r < R; ++r) {
         probe[r] = r < n_fixed ? ents[r].size()
-                               : probe_len(ents[r], C, H, W, rules[r].n, rules[r].m);
+                               : codegen::probe_len(ents[r], C, H, W, rules[r].n, rules[r].m, 8);
         for (size_t e = 0; e < probe[r]; ++e)
             if (ents[r][e].j > 0) xs.insert({ents[r][e].c, ents[r][e].j});
     }
@@ -439,14 +341,7 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
             std::vector<std::string> pt{"p[" + std::to_string(c) + "]"}, mt;
             for (const Vote &v : pl[c]) pt.push_back(tname(v.r, v.i, v.j));
             for (const Vote &v : mi[c]) mt.push_back(tname(v.r, v.i, v.j));
-            const std::vector<std::string> P = g.count(pt), Nn = g.count(mt);
-            const size_t K = std::max(P.size(), Nn.size());
-            o << "u32 GT = 0u, EQ = 0xFFFFFFFFu;\n";
-            for (size_t k = K; k-- > 0;) {
-                const std::string pk = k < P.size() ? P[k] : "0u", nk = k < Nn.size() ? Nn[k] : "0u";
-                o << "GT |= EQ & " << pk << " & ~" << nk << ";\n";
-                o << "EQ &= ~(" << pk << " ^ " << nk << ");\n";
-            }
+            g.greater(g.count(pt), g.count(mt));
             o << "N" << c << " = GT;\n}\n";
         }
         for (int c : voted) o << "p[" << c << "] = N" << c << ";\n";
@@ -608,14 +503,7 @@ std::string lane16_rules_body_sequential(int C, int H, int W, const std::vector<
                 for (const Vote &v : plus[c]) pt.push_back(tname(v.i, v.j));
                 for (const Vote &v : minus[c]) mt.push_back(tname(v.i, v.j));
                 o << "{ // plane " << c << "\n";
-                const std::vector<std::string> Pb = g.count(pt), Nb = g.count(mt);
-                const size_t K = std::max(Pb.size(), Nb.size());
-                o << "u32 GT = 0u, EQ = 0xFFFFFFFFu;\n";
-                for (size_t k = K; k-- > 0;) {
-                    const std::string pk = k < Pb.size() ? Pb[k] : "0u", nk = k < Nb.size() ? Nb[k] : "0u";
-                    o << "GT |= EQ & " << pk << " & ~" << nk << ";\n";
-                    o << "EQ &= ~(" << pk << " ^ " << nk << ");\n";
-                }
+                g.greater(g.count(pt), g.count(mt));
                 o << "N" << c << " = GT;\n}\n";
             }
             o << "}\n";
@@ -650,52 +538,8 @@ void lane16_compile(const std::vector<std::vector<Lane16Rule>> &sets, int C, int
     p.source = std::move(src);
 }
 
-namespace {
-std::mutex g_mu;
-std::map<std::string, hipFunction_t> g_cache;   // (device, source) -> kernel; kept for the process
-}  // namespace
-
 hipError_t lane16_upload(const Lane16Program &p, Lane16Device &d, std::string *log) {
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return e;
-    const std::string key = std::to_string(dev) + '\n' + p.source;
-    std::lock_guard<std::mutex> lock(g_mu);
-    auto it = g_cache.find(key);
-    if (it != g_cache.end()) {
-        d.fn = it->second;
-        return hipSuccess;
-    }
-    hiprtcProgram prog;
-    if (hiprtcCreateProgram(&prog, p.source.c_str(), "av_lane16.hip", 0, nullptr, nullptr) !=
-        HIPRTC_SUCCESS)
-        return hipErrorInvalidValue;
-    const char *opts[] = {"--offload-arch=gfx950", "-O3", "-std=c++17", "-Xclang", "-target-feature",
-                          "-Xclang", "-packed-fp32-ops"};
-    const hiprtcResult rc = hiprtcCompileProgram(prog, int(sizeof opts / sizeof opts[0]), opts);
-    if (rc != HIPRTC_SUCCESS) {
-        size_t n = 0;
-        hiprtcGetProgramLogSize(prog, &n);
-        std::string text(n, '\0');
-        if (n) hiprtcGetProgramLog(prog, &text[0]);
-        if (log) *log = std::string(hiprtcGetErrorString(rc)) + ": " + text;
-        hiprtcDestroyProgram(&prog);
-        return hipErrorInvalidKernelFile;
-    }
-    size_t n = 0;
-    hiprtcGetCodeSize(prog, &n);
-    std::vector<char> code(n);
-    hiprtcGetCode(prog, code.data());
-    hiprtcDestroyProgram(&prog);
-    hipModule_t mod;
-    e = hipModuleLoadData(&mod, code.data());
-    if (e != hipSuccess) return e;
-    hipFunction_t fn;
-    e = hipModuleGetFunction(&fn, mod, "av_lane16_step");
-    if (e != hipSuccess) return e;
-    g_cache[key] = fn;
-    d.fn = fn;
-    return hipSuccess;
+    return jit_kernel(p.source, "av_lane16.hip", "av_lane16_step", &d.fn, log);
 }
 
 hipError_t launch_lane16_step(const StepArgs &a, const Lane16Device &d, hipStream_t s) {
