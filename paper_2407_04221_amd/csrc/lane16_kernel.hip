@@ -172,7 +172,8 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
     // block: wait for the vector memory counter here, once, rather than inside the loop.
     __builtin_amdgcn_s_waitcnt(0x0F70);             // vmcnt(0); expcnt, lgkmcnt untouched
 
-    // rewards and done flags of 16 steps: lane y of a row keeps step k0 + y of its pair
+    // rewards and done flags of 16 steps: lane y of a row keeps step k0 + y of its pair (zero
+    // unless that step paid a reward or ended an episode)
     int rbA = 0, rbB = 0;
     u32 dbuf = 0u;
 
@@ -223,7 +224,7 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
         if (dB) tB = 0;
 
 #ifndef AV_NO_REWARD
-        // reward: sum of the row's 16 lanes
+        // reward: sum of the row's 16 lanes, kept by lane s
         if (paid) {
             rA += DPP_ROR(rA, 1);
             rA += DPP_ROR(rA, 2);
@@ -233,16 +234,24 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
             rB += DPP_ROR(rB, 2);
             rB += DPP_ROR(rB, 4);
             rB += DPP_ROR(rB, 8);
+            if (y == s) {
+                rbA = rA;
+                rbB = rB;
+            }
         }
 #else
         (void)paid;
 #endif
-        // keep this step's results in lane s; store 16 steps at once
-        if (y == s) {
-            rbA = rA;
-            rbB = rB;
-            dbuf = u32(dA) | (u32(dB) << 1);
+        // automatic reset to the initial map; lane s keeps the step's done flags
+        if (ANY(u32(dA || dB))) {
+            if (y == s) dbuf = u32(dA) | (u32(dB) << 1);
+            if (lazy_init) load_init();     // the launch's only step
+            const u32 dm = HALF(dA, dB);
+#pragma unroll
+            for (int c = 0; c < AV_C; ++c) p[c] = (q[c] & dm) | (p[c] & ~dm);
         }
+        // store 16 steps at once; the buffers then start again from zero (a step without a
+        // reward or an ended episode leaves them untouched)
         if (s == 15 || k == K - 1) {
             if (y <= s) {
                 const size_t at = size_t(k - s + y) * B;
@@ -255,14 +264,9 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
                     done[at + eB] = (unsigned char)(dbuf >> 1);
                 }
             }
-        }
-
-        // automatic reset to the initial map
-        if (ANY(u32(dA || dB))) {
-            if (lazy_init) load_init();     // the launch's only step
-            const u32 dm = HALF(dA, dB);
-#pragma unroll
-            for (int c = 0; c < AV_C; ++c) p[c] = (q[c] & dm) | (p[c] & ~dm);
+            rbA = 0;
+            rbB = 0;
+            dbuf = 0u;
         }
     }
 
