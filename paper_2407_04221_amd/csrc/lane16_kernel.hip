@@ -220,8 +220,6 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
         tB += 1;
         const bool dA = ((o & 0xFFFFu) == 0u) || (AV_L > 0 && tA == AV_L);
         const bool dB = ((o >> 16) == 0u) || (AV_L > 0 && tB == AV_L);
-        if (dA) tA = 0;
-        if (dB) tB = 0;
 
 #ifndef AV_NO_REWARD
         // reward: sum of the row's 16 lanes, kept by lane s
@@ -242,8 +240,11 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
 #else
         (void)paid;
 #endif
-        // automatic reset to the initial map; lane s keeps the step's done flags
+        // automatic reset to the initial map and the step counter; lane s keeps the step's
+        // done flags
         if (ANY(u32(dA || dB))) {
+            if (dA) tA = 0;
+            if (dB) tB = 0;
             if (y == s) dbuf = u32(dA) | (u32(dB) << 1);
             if (lazy_init) load_init();     // the launch's only step
             const u32 dm = HALF(dA, dB);
