@@ -216,6 +216,10 @@ bool rows_eligible(int H, int W, int C, int rules_per_set);
 hipError_t launch_rows_step(const StepArgs &a, const uint32_t *words, int set_words, int rules,
                             hipStream_t s);
 
+// Wave slots of the current device (8 waves per SIMD, 4 SIMDs per CU; 0 if it cannot be
+// asked): the most waves resident at once.
+long long device_wave_slots();
+
 // The wave engine (k_wave.hip): one environment per workgroup.
 size_t wave_lds_bytes(int H, int W, int C, int rules_per_set, bool control = false,
                       bool random = false);

@@ -174,12 +174,17 @@ struct RowsArgs {
     int32_t body_lds;        // 1: each wave copies its set's words into LDS first
 };
 
-template <typename RowT, int RB>
-__global__ void __launch_bounds__(64) rows_step(StepArgs a, RowsArgs rp) {
+// kWaves waves per environment: wave 0 runs the step; with kWaves = 4 the other three only
+// help with the probe pass (each takes a quarter of the anchor rows) and meet wave 0 at two
+// barriers per step.
+template <typename RowT, int RB, int kWaves>
+__global__ void __launch_bounds__(64 * kWaves) rows_step(StepArgs a, RowsArgs rp) {
     using ST = typename RowStore<RB>::T;
     extern __shared__ __align__(16) unsigned char lds[];
     const int Rt = rp.rules;
-    const int y = int(threadIdx.x);
+    constexpr int nw = kWaves;
+    const int y = int(threadIdx.x & 63u);
+    const int wv = nw == 1 ? 0 : __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
     const int b = int(blockIdx.x);
     const int H = a.H, W = a.W, C = a.C, B = a.B;
     const int hp = H + kPad;          // rows per LDS plane
@@ -192,7 +197,8 @@ __global__ void __launch_bounds__(64) rows_step(StepArgs a, RowsArgs rp) {
     const int hs = kPad + hp;
     int *fired = reinterpret_cast<int *>(Ms + size_t(Rt) * hs);   // [Rt]
     uint32_t *prob = reinterpret_cast<uint32_t *>(fired + Rt);     // [8 Rt] probe records
-    uint32_t *lprog = prob + 8 * Rt;                                // [set_words] if staged
+    uint32_t *tslot = prob + 8 * Rt;                                // [4][2]: waves' candidates
+    uint32_t *lprog = tslot + 8;                                    // [set_words] if staged
     const uint32_t *gprog = rp.words + size_t(a.per_env ? b : 0) * size_t(rp.set_words);
     const RowT wmask = low_mask<RowT>(W);
     // row y of environment b in channel c is element c * plane + lrow of the [C][B][H] arrays
@@ -202,11 +208,13 @@ __global__ void __launch_bounds__(64) rows_step(StepArgs a, RowsArgs rp) {
     // zero: the planes with their pad rows, the vote accumulators, and the pad rows above
     // every match plane (the rows below them are written before they are read)
     const int pwords = int(size_t(3 * C + 4) * hp * (sizeof(RowT) / 4));
-    for (int w = y; w < pwords; w += 64) reinterpret_cast<uint32_t *>(lds)[w] = 0u;
-    for (int w = y; w < Rt * kPad; w += 64) Ms[size_t(w / kPad) * hs + (w % kPad)] = 0;
-    for (int w = y; w < 8 * Rt; w += 64) prob[w] = gprog[w];
-    if (rp.body_lds)
-        for (int w = y; w < rp.set_words; w += 64) lprog[w] = gprog[w];
+    if (wv == 0) {
+        for (int w = y; w < pwords; w += 64) reinterpret_cast<uint32_t *>(lds)[w] = 0u;
+        for (int w = y; w < Rt * kPad; w += 64) Ms[size_t(w / kPad) * hs + (w % kPad)] = 0;
+        for (int w = y; w < 8 * Rt; w += 64) prob[w] = gprog[w];
+        if (rp.body_lds)
+            for (int w = y; w < rp.set_words; w += 64) lprog[w] = gprog[w];
+    }
     const uint32_t *const lbody = rp.body_lds ? lprog : nullptr;
     // probe records (8 words per rule): lane l of pt[g] holds word 64 g + l, i.e. word l % 8
     // of rule 8 g + l / 8
@@ -242,8 +250,11 @@ __global__ void __launch_bounds__(64) rows_step(StepArgs a, RowsArgs rp) {
             }
     }
     __syncthreads();
-    for (int c = 0; c < C; ++c)
-        if (row) Pl[c * hp + y] = RowT(static_cast<const ST *>(a.state)[c * plane + lrow]);
+    if (wv == 0)
+        for (int c = 0; c < C; ++c)
+            if (row) Pl[c * hp + y] = RowT(static_cast<const ST *>(a.state)[c * plane + lrow]);
+    // this wave's share of the probe pass's anchor rows
+    const int y0 = wv * H / nw, y1 = (wv + 1) * H / nw;
 
     int t_env = a.t[b];
     uint32_t ablk = 0;
@@ -254,6 +265,7 @@ __global__ void __launch_bounds__(64) rows_step(StepArgs a, RowsArgs rp) {
     const RowT *const P = Pl + size_t(kChPlayer) * hp;
 
     for (int k = 0; k < a.k; ++k) {
+        if (wv == 0) {
         // actions come 64 steps at a time: lane l holds step k0 + l
         if ((k & 63) == 0) ablk = (k + y < a.k) ? uint32_t(a.actions[size_t(k + y) * B + b]) : 0u;
         const int act = __builtin_amdgcn_readlane(int(ablk), k & 63);
@@ -265,6 +277,8 @@ __global__ void __launch_bounds__(64) rows_step(StepArgs a, RowsArgs rp) {
             else if (act == 4) f = P[ry] >> 1;
             if (row) F[y] = f;
         }
+        }
+        if (nw > 1) __syncthreads();             // the map and this step's force plane are set
         int rsum = 0, nf = 0;
         uint32_t touched = 0;   // planes that received votes in the current batch
         // The rules to visit: in sequential order every rule, one batch each (each matches the
@@ -273,15 +287,29 @@ __global__ void __launch_bounds__(64) rows_step(StepArgs a, RowsArgs rp) {
         uint64_t todo = all_rules;
         if (!a.sequential) {
             RowT hit = 0;
-            for (int yy = 0; yy < H; ++yy) {
+            for (int yy = y0; yy < y1; ++yy) {
                 const RowT t = ((Pl[pa[0] + yy] >> pj[0]) ^ pinv[0]) &
                                ((Pl[pa[1] + yy] >> pj[1]) ^ pinv[1]);
                 hit |= yy <= pmax ? t : RowT(0);
             }
             todo = __builtin_amdgcn_ballot_w64((hit & pcol) != 0);
+            if (nw > 1) {
+                // the waves' candidates, OR-ed (wave 0 reads the slots before the next step)
+                if (y == 0) {
+                    tslot[2 * wv] = uint32_t(todo);
+                    tslot[2 * wv + 1] = uint32_t(todo >> 32);
+                }
+                __syncthreads();
+                todo = 0;
+                for (int w = 0; w < nw; ++w)
+                    todo |= uint64_t(tslot[2 * w]) | (uint64_t(tslot[2 * w + 1]) << 32);
+            }
+        }
+        if (wv != 0) continue;                    // helper waves: only the probe pass
+        if (!a.sequential) {
             if (__popcll(todo) > 2) {
                 // many candidates (crowded maps): filter them with four entries at once
-                hit = 0;
+                RowT hit = 0;
                 for (int yy = 0; yy < H; ++yy) {
                     const RowT t = ((Pl[pa[0] + yy] >> pj[0]) ^ pinv[0]) &
                                    ((Pl[pa[1] + yy] >> pj[1]) ^ pinv[1]) &
@@ -459,6 +487,7 @@ __global__ void __launch_bounds__(64) rows_step(StepArgs a, RowsArgs rp) {
                 if (row) Pl[c * hp + y] = RowT(static_cast<const ST *>(a.init)[c * plane + lrow]);
     }
 
+    if (wv != 0) return;
     for (int c = 0; c < C; ++c)
         if (row) static_cast<ST *>(a.state)[c * plane + lrow] = ST(Pl[c * hp + y]);
     if (y == 0) a.t[b] = t_env;
@@ -559,7 +588,7 @@ size_t rows_lds_bytes(int H, int W, int C, int rules_per_set) {
     const size_t rowb = W <= 32 ? 4 : 8, hp = size_t(H) + kPad;
     return ((size_t(C + 2) + size_t(2) * (C + 1)) * hp + size_t(rules_per_set) * (hp + kPad)) *
                rowb +
-           (sizeof(int) + 8 * sizeof(uint32_t)) * size_t(rules_per_set);
+           (sizeof(int) + 8 * sizeof(uint32_t)) * size_t(rules_per_set) + 8 * sizeof(uint32_t);
 }
 
 bool rows_eligible(int H, int W, int C, int rules_per_set) {
@@ -580,13 +609,22 @@ hipError_t launch_rows_step(const StepArgs &a, const uint32_t *words, int set_wo
     const int body_lds = a.k >= 16 && staged <= size_t(kLdsBudget) &&
                          staged * per_cu <= size_t(160) * 1024;
     if (body_lds) lds = staged;
+    // On maps taller than 32 rows the probe pass (a loop over every anchor row) is most of a
+    // step; when the batch leaves the wave slots for it, three more waves per environment
+    // take three quarters of its rows.
+    const bool helpers = a.H > 32 && !a.sequential && 4LL * a.B <= device_wave_slots();
     RowsArgs rp{words, set_words, rules, body_lds};
+    // (built for 4- and 8-byte rows; maps of at most 16 columns keep one wave)
     if (a.row_bytes == 2)
-        hipLaunchKernelGGL((rows_step<uint32_t, 2>), dim3(a.B), dim3(64), lds, s, a, rp);
+        hipLaunchKernelGGL((rows_step<uint32_t, 2, 1>), dim3(a.B), dim3(64), lds, s, a, rp);
+    else if (a.row_bytes == 4 && !helpers)
+        hipLaunchKernelGGL((rows_step<uint32_t, 4, 1>), dim3(a.B), dim3(64), lds, s, a, rp);
     else if (a.row_bytes == 4)
-        hipLaunchKernelGGL((rows_step<uint32_t, 4>), dim3(a.B), dim3(64), lds, s, a, rp);
+        hipLaunchKernelGGL((rows_step<uint32_t, 4, 4>), dim3(a.B), dim3(256), lds, s, a, rp);
+    else if (!helpers)
+        hipLaunchKernelGGL((rows_step<uint64_t, 8, 1>), dim3(a.B), dim3(64), lds, s, a, rp);
     else
-        hipLaunchKernelGGL((rows_step<uint64_t, 8>), dim3(a.B), dim3(64), lds, s, a, rp);
+        hipLaunchKernelGGL((rows_step<uint64_t, 8, 4>), dim3(a.B), dim3(256), lds, s, a, rp);
     return hipGetLastError();
 }
 

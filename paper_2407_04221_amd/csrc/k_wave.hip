@@ -457,16 +457,8 @@ int rows_per_group(int H) { return H <= 16 ? 16 : (H <= 32 ? 32 : 64); }
 // but past the wave slots they only add rounds of workgroups (c4 on this engine, 16384
 // environments: 36 against 18 us per step; c3, 4096: 8 groups 10 % slower than 4).
 int wave_groups(int B, int Hq, int rules, int max_threads) {
-    static std::atomic<int> cus[64];                 // per device, 0 until first asked
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 4;
-    int n = cus[dev].load(std::memory_order_relaxed);
-    if (!n) {
-        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
-            return 4;
-        cus[dev].store(n, std::memory_order_relaxed);
-    }
-    const long long slots = 32LL * n;
+    const long long slots = device_wave_slots();
+    if (slots <= 0) return 4;
     int cap = 4;
     while (cap < rules) cap *= 2;
     for (int G = std::min(max_threads / Hq, cap); G > 4; G /= 2)
@@ -482,6 +474,19 @@ size_t wave_base_bytes(int H, int W, int C, int rules_per_set) {
 }
 
 }  // namespace
+
+long long device_wave_slots() {
+    static std::atomic<int> cus[64];                 // per device, 0 until first asked
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+    int n = cus[dev].load(std::memory_order_relaxed);
+    if (!n) {
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+            return 0;
+        cus[dev].store(n, std::memory_order_relaxed);
+    }
+    return 32LL * n;
+}
 
 size_t wave_lds_bytes(int H, int W, int C, int rules_per_set, bool control, bool random) {
     return wave_base_bytes(H, W, C, rules_per_set) +
