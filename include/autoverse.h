@@ -69,13 +69,16 @@ typedef enum {
     AV_ENGINE_WAVE = 3,     /* one environment per workgroup, map rows in LDS; 4 to 64
                                groups of lanes (as many as the batch's size leaves room for)
                                match that many of its rules at once */
-    AV_ENGINE_ROWS = 4      /* one environment per 64-lane wave with no barriers, map row y
-                               in lane y, planes in the wave's LDS; one lane per rule tests
-                               every rule's rarest entries at once, so only rules that can
-                               match are visited.  Needs R + 4 <= 64 and, within 64 KiB of
-                               LDS, (3 C + 4) planes of H + 16 rows plus R + 4 match planes
-                               of H + 32 rows (4 bytes per row for W <= 32, else 8) and 36
-                               bytes per rule; no rule application control */
+    AV_ENGINE_ROWS = 4      /* one environment per 64-lane wave, map row y in lane y,
+                               planes in the workgroup's LDS; one lane per rule tests every
+                               rule's rarest entries at once, so only rules that can match
+                               are visited.  On maps above 32 rows, in parallel rule order,
+                               with 4 B waves within the device's wave slots, three more
+                               waves per environment share the probe and the matching.
+                               Needs R + 4 <= 64 and, within 64 KiB of LDS, (3 C + 4) planes
+                               of H + 16 rows plus R + 4 match planes of H + 32 rows (4 bytes
+                               per row for W <= 32, else 8), 36 bytes per rule and 96 more;
+                               no rule application control */
 } av_engine;
 
 /* Order in which the rules of one step are applied. */

@@ -3,8 +3,9 @@
 // A wave of 64 lanes holds one environment.  Lane y owns row y of every plane (the C stored
 // channels and the force plane); the planes live in the wave's own LDS as 32-bit rows for
 // W <= 32 and 64-bit rows for W <= 64, each plane followed by 16 zero rows, so row y + i of
-// any pattern entry is a plain LDS read.  Nothing is shared between waves (one wave per
-// workgroup, no barriers in the step loop).  The environment's rule program (its own set,
+// any pattern entry is a plain LDS read.  With one wave per workgroup nothing is shared and the
+// step loop has no barriers; the four-wave variant for tall maps is described at the kernel.
+// The environment's rule program (its own set,
 // or the shared one) is read 64 words at a time into a register and taken apart with
 // v_readlane; each rule's probe record stays in registers for the whole launch.
 //
@@ -174,9 +175,13 @@ struct RowsArgs {
     int32_t body_lds;        // 1: each wave copies its set's words into LDS first
 };
 
-// kWaves waves per environment: wave 0 runs the step; with kWaves = 4 the other three only
-// help with the probe pass (each takes a quarter of the anchor rows) and meet wave 0 at two
-// barriers per step.
+// kWaves waves per environment: wave 0 runs the step; with kWaves = 4 (parallel rule order)
+// the other three help with the probe pass and the four-entry filter (each wave takes a
+// quarter of the anchor rows) and with matching the candidates (each wave takes every fourth
+// one, ORs its votes into the shared accumulators and adds its reward, rule count and voted
+// planes to three shared counters); wave 0 then writes the planes.  The waves meet at a
+// barrier after the force, after the probe, after the filter (when it runs) and after the
+// match (when there are candidates).
 template <typename RowT, int RB, int kWaves>
 __global__ void __launch_bounds__(64 * kWaves) rows_step(StepArgs a, RowsArgs rp) {
     using ST = typename RowStore<RB>::T;
@@ -198,7 +203,9 @@ __global__ void __launch_bounds__(64 * kWaves) rows_step(StepArgs a, RowsArgs rp
     int *fired = reinterpret_cast<int *>(Ms + size_t(Rt) * hs);   // [Rt]
     uint32_t *prob = reinterpret_cast<uint32_t *>(fired + Rt);     // [8 Rt] probe records
     uint32_t *tslot = prob + 8 * Rt;                                // [4][2]: waves' candidates
-    uint32_t *lprog = tslot + 8;                                    // [set_words] if staged
+    uint32_t *tfilt = tslot + 8;                                    // [4][2]: after the filter
+    int *lcnt = reinterpret_cast<int *>(tfilt + 8);   // fired rules, voted planes, reward
+    uint32_t *lprog = tslot + 24;                                   // [set_words] if staged
     const uint32_t *gprog = rp.words + size_t(a.per_env ? b : 0) * size_t(rp.set_words);
     const RowT wmask = low_mask<RowT>(W);
     // row y of environment b in channel c is element c * plane + lrow of the [C][B][H] arrays
@@ -277,6 +284,7 @@ __global__ void __launch_bounds__(64 * kWaves) rows_step(StepArgs a, RowsArgs rp
             else if (act == 4) f = P[ry] >> 1;
             if (row) F[y] = f;
         }
+        if (nw > 1 && y < 3) lcnt[y] = 0;
         }
         if (nw > 1) __syncthreads();             // the map and this step's force plane are set
         int rsum = 0, nf = 0;
@@ -305,21 +313,31 @@ __global__ void __launch_bounds__(64 * kWaves) rows_step(StepArgs a, RowsArgs rp
                     todo |= uint64_t(tslot[2 * w]) | (uint64_t(tslot[2 * w + 1]) << 32);
             }
         }
-        if (wv != 0) continue;                    // helper waves: only the probe pass
         if (!a.sequential) {
             if (__popcll(todo) > 2) {
                 // many candidates (crowded maps): filter them with four entries at once
                 RowT hit = 0;
-                for (int yy = 0; yy < H; ++yy) {
+                for (int yy = nw > 1 ? y0 : 0; yy < (nw > 1 ? y1 : H); ++yy) {
                     const RowT t = ((Pl[pa[0] + yy] >> pj[0]) ^ pinv[0]) &
                                    ((Pl[pa[1] + yy] >> pj[1]) ^ pinv[1]) &
                                    ((Pl[pa[2] + yy] >> pj[2]) ^ pinv[2]) &
                                    ((Pl[pa[3] + yy] >> pj[3]) ^ pinv[3]);
                     hit |= yy <= pmax ? t : RowT(0);
                 }
-                todo &= __builtin_amdgcn_ballot_w64((hit & pcol) != 0);
+                uint64_t keep = __builtin_amdgcn_ballot_w64((hit & pcol) != 0);
+                if (nw > 1) {
+                    if (y == 0) {
+                        tfilt[2 * wv] = uint32_t(keep);
+                        tfilt[2 * wv + 1] = uint32_t(keep >> 32);
+                    }
+                    __syncthreads();
+                    keep = 0;
+                    for (int w = 0; w < nw; ++w)
+                        keep |= uint64_t(tfilt[2 * w]) | (uint64_t(tfilt[2 * w + 1]) << 32);
+                }
+                todo &= keep;
             }
-            if (H <= 32 && __popcll(todo) > 2) {
+            if (nw == 1 && H <= 32 && __popcll(todo) > 2) {
                 // Several candidates on a map of at most 32 rows: the wave splits into groups
                 // of hq lanes (lane gy of a group on map row gy) that match one candidate each
                 // at the same time.  A group reads its rule's entries and votes from its own
@@ -399,6 +417,17 @@ __global__ void __launch_bounds__(64 * kWaves) rows_step(StepArgs a, RowsArgs rp
                 touched |= uint32_t(__builtin_amdgcn_readfirstlane(int(tmask)));
             }
         }
+        // with helper waves, wave w matches every nw-th candidate from the w-th on
+        const bool shared = nw > 1 && todo != 0ull;
+        if (shared) {
+            uint64_t mine = 0;
+            int q = 0;
+            for (uint64_t t = todo; t; t &= t - 1ull, ++q)
+                if ((q & (nw - 1)) == wv) mine |= t & (0ull - t);
+            todo = mine;
+        } else if (wv != 0) {
+            todo = 0ull;
+        }
         for (;;) {
             const bool last = todo == 0ull;
             do {
@@ -427,7 +456,7 @@ __global__ void __launch_bounds__(64 * kWaves) rows_step(StepArgs a, RowsArgs rp
                 if (!alive || !wave_any(M != 0)) break;
 
                 if (row) Ms[size_t(r) * hs + kPad + y] = M;
-                if (y == 0) fired[nf] = r | (bo << 8);
+                if (y == 0) fired[shared ? atomicAdd(&lcnt[0], 1) : nf] = r | (bo << 8);
                 ++nf;
                 rsum += reward * popc(M);
                 // votes: the match row, shifted left by j, into row y + i of the accumulator
@@ -440,17 +469,31 @@ __global__ void __launch_bounds__(64 * kWaves) rows_step(StepArgs a, RowsArgs rp
                     touched |= 1u << c;
                 }
             } while (false);
+            if (shared && last) {
+                // every wave adds its share; wave 0 goes on with the totals
+                if (wave_any(rsum != 0))
+                    for (int off = 32; off > 0; off >>= 1) rsum += __shfl_xor(rsum, off, 64);
+                if (y == 0) {
+                    if (rsum != 0) atomicAdd(&lcnt[2], rsum);
+                    if (touched != 0) atomicOr(reinterpret_cast<unsigned *>(&lcnt[1]), touched);
+                }
+                __syncthreads();
+                if (wv != 0) break;
+                nf = lcnt[0];
+                touched = uint32_t(lcnt[1]);
+                rsum = y == 0 ? lcnt[2] : 0;
+            }
             if (nf > 0 && (a.sequential || last)) {
                 // write the planes the batch's rules voted on; planes where some cell got
                 // votes of both signs are recounted exactly
                 for (uint32_t t = touched; t; t &= t - 1) {
                     const int c = __builtin_ctz(t);
                     const RowT old = Pl[c * hp + ry], pl = Vp[c * hp + ry], mi = Vm[c * hp + ry];
-                    RowT nw = (old | pl) & ~mi;
+                    RowT nv = (old | pl) & ~mi;
                     if (wave_any((pl & mi) != 0))
-                        nw = exact_plane<RowT>(c, old, fired, nf, lbody, gprog, Ms, hs, y, ry);
+                        nv = exact_plane<RowT>(c, old, fired, nf, lbody, gprog, Ms, hs, y, ry);
                     if (row) {
-                        Pl[c * hp + y] = nw;
+                        Pl[c * hp + y] = nv;
                         Vp[c * hp + y] = 0;
                         Vm[c * hp + y] = 0;
                     }
@@ -460,6 +503,7 @@ __global__ void __launch_bounds__(64 * kWaves) rows_step(StepArgs a, RowsArgs rp
             }
             if (last) break;
         }
+        if (wv != 0) continue;                    // helper waves: the rest is wave 0's
 
         // reward: wave sum of the lanes' counts
         int total = 0;
@@ -588,7 +632,7 @@ size_t rows_lds_bytes(int H, int W, int C, int rules_per_set) {
     const size_t rowb = W <= 32 ? 4 : 8, hp = size_t(H) + kPad;
     return ((size_t(C + 2) + size_t(2) * (C + 1)) * hp + size_t(rules_per_set) * (hp + kPad)) *
                rowb +
-           (sizeof(int) + 8 * sizeof(uint32_t)) * size_t(rules_per_set) + 8 * sizeof(uint32_t);
+           (sizeof(int) + 8 * sizeof(uint32_t)) * size_t(rules_per_set) + 24 * sizeof(uint32_t);
 }
 
 bool rows_eligible(int H, int W, int C, int rules_per_set) {
@@ -610,8 +654,9 @@ hipError_t launch_rows_step(const StepArgs &a, const uint32_t *words, int set_wo
                          staged * per_cu <= size_t(160) * 1024;
     if (body_lds) lds = staged;
     // On maps taller than 32 rows the probe pass (a loop over every anchor row) is most of a
-    // step; when the batch leaves the wave slots for it, three more waves per environment
-    // take three quarters of its rows.
+    // step, and a crowded map has many candidates to match one after another; when the batch
+    // leaves the wave slots for it, three more waves per environment take three quarters of
+    // the probe's rows and of the candidates.
     const bool helpers = a.H > 32 && !a.sequential && 4LL * a.B <= device_wave_slots();
     RowsArgs rp{words, set_words, rules, body_lds};
     // (built for 4- and 8-byte rows; maps of at most 16 columns keep one wave)

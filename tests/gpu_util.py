@@ -11,12 +11,12 @@ import paper_2407_04221_amd as av
 def rows_ok(wl):
     """The rows engine takes at most 64 rules with the moves and, within 64 KiB of LDS,
     C + 2 planes, 2 (C + 1) vote planes and one match plane per rule (H + 16 rows each, the
-    match planes 16 more; 4 bytes per row for W <= 32, else 8) plus 36 bytes per rule and 32
-    for the probe waves' candidate masks."""
+    match planes 16 more; 4 bytes per row for W <= 32, else 8) plus 36 bytes per rule and 96
+    for the helper waves' candidate masks and shared counters."""
     rt = wl.R + 4
     rowb = 4 if wl.W <= 32 else 8
     hp = wl.H + 16
-    lds = ((wl.C + 2 + 2 * (wl.C + 1)) * hp + rt * (hp + 16)) * rowb + 36 * rt + 32
+    lds = ((wl.C + 2 + 2 * (wl.C + 1)) * hp + rt * (hp + 16)) * rowb + 36 * rt + 96
     return rt <= 64 and lds <= 65536
 
 
