@@ -2,9 +2,8 @@
 // (paper Sec. 2.2.2: a local patch of tiles around the player's position; Table 1 uses
 // windows of 5, 10, 20 and 31 cells).
 //
-// 16, 32 or 64 lanes per environment (about one per 16-byte chunk of its output), 256 lanes
-// to a workgroup.  The environment's packed rows are staged in
-// LDS; the first player cell in row-major order is found with an LDS atomicMin over rows
+// 16, 32 or 64 lanes per environment (more for larger outputs), 256 lanes to a workgroup.
+// The environment's packed rows are staged in LDS; the first player cell in row-major order is found with an LDS atomicMin over rows
 // (then the row's lowest set bit).  The environment's C x w x w output bytes are then written
 // straight from the staged rows in 16-byte chunks on the global 16-byte grid, one chunk per
 // thread and pass: the chunk's 16 cells are gathered as a 16-bit mask, one shift of a staged
@@ -32,15 +31,25 @@ __device__ inline uint64_t row_from(uint64_t row, int x0) {
     return x0 >= 0 ? row >> x0 : row << -x0;
 }
 
-// The window cells of output bytes [o, o + n) of one environment (n <= 16) as a mask, bit k
-// for byte o + k.  rows: its staged planes [C][H]; (y0, x0) the window's top-left map cell.
+// Position of output byte o of one environment: channel c, window row wy, column wx.
 // (One environment's output is at most 31 x 255 x 255 bytes, so offsets fit 32 bits.)
-__device__ inline uint32_t window_bits(const uint64_t *rows, int H, int w, bool has, int y0,
-                                       int x0, uint32_t o, int n) {
+struct WinPos {
+    int c, wy, wx;
+};
+__device__ inline WinPos win_pos(uint32_t o, int w) {
     const uint32_t ww = uint32_t(w) * uint32_t(w);
-    int c = int(o / ww);
+    const int c = int(o / ww);
     const uint32_t rem = o - uint32_t(c) * ww;
-    int wy = int(rem / uint32_t(w)), wx = int(rem - uint32_t(wy) * uint32_t(w));
+    const int wy = int(rem / uint32_t(w));
+    return {c, wy, int(rem - uint32_t(wy) * uint32_t(w))};
+}
+
+// The window cells of n output bytes (n <= 16) from position (c, wy, wx) on, as a mask, bit k
+// for the k-th byte.  rows: the environment's staged planes [C][H]; (y0, x0) the window's
+// top-left map cell.
+__device__ inline uint32_t window_bits(const uint64_t *rows, int H, int w, bool has, int y0,
+                                       int x0, WinPos p, int n) {
+    int c = p.c, wy = p.wy, wx = p.wx;
     uint32_t m = 0;
     for (int k = 0; k < n;) {
         const int len = min(n - k, w - wx);
@@ -97,18 +106,33 @@ __global__ void __launch_bounds__(256) observe_env(const void *state, int B, int
     const uint32_t head = uint32_t(16 - (reinterpret_cast<uintptr_t>(out) & 15)) & 15u;
     const uint32_t h = head < per ? head : per;
     const uint32_t chunks = (per - h) / 16;
+    // a thread's chunks are 16 T bytes apart: its window position advances by sq rows and sr
+    // columns per chunk, so only the first position takes a division
+    const uint32_t sq = 16u * T / uint32_t(w), sr = 16u * T - sq * uint32_t(w);
+    WinPos p = win_pos(h + 16u * uint32_t(tid), w);
     for (uint32_t k = tid; k < chunks; k += T) {
         const uint32_t o = h + 16 * k;
-        const uint32_t m = window_bits(rows, H, w, has, y0, x0, o, 16);
+        const uint32_t m = window_bits(rows, H, w, has, y0, x0, p, 16);
         *reinterpret_cast<uint4 *>(out + o) =
             make_uint4(spread4(m), spread4(m >> 4), spread4(m >> 8), spread4(m >> 12));
+        if (k + T >= chunks) break;
+        p.wx += int(sr);
+        p.wy += int(sq);
+        if (p.wx >= w) {
+            p.wx -= w;
+            ++p.wy;
+        }
+        while (p.wy >= w) {
+            p.wy -= w;
+            ++p.c;
+        }
     }
     // the bytes before the first and after the last full chunk (at most 30), one per thread
     const uint32_t tail = h + 16 * chunks;
     const int loose = int(h + (per - tail));
     for (int i = tid; i < loose; i += T) {
         const uint32_t o = uint32_t(i) < h ? uint32_t(i) : tail + (uint32_t(i) - h);
-        out[o] = uint8_t(window_bits(rows, H, w, has, y0, x0, o, 1));
+        out[o] = uint8_t(window_bits(rows, H, w, has, y0, x0, win_pos(o, w), 1));
     }
 }
 
@@ -117,10 +141,11 @@ __global__ void __launch_bounds__(256) observe_env(const void *state, int B, int
 hipError_t launch_observe(const void *state, int B, int C, int H, int W, int row_bytes, int w,
                           uint8_t *dst, hipStream_t s) {
     const size_t region = (size_t(C) * H * sizeof(uint64_t) + 4 + 15) & ~size_t(15);
-    // lanes per environment: about one per 16-byte chunk of its output (16, 32 or 64), as
-    // long as the workgroup's staged rows fit the LDS budget
+    // lanes per environment: 16 up to 64 chunks of 16 bytes, 32 up to 1024, else 64 (measured
+    // on 16 x 16 maps with C = 6: windows of 10, 20 and 31 cells), as long as the workgroup's
+    // staged rows fit the LDS budget
     const size_t per = size_t(C) * w * w;
-    int T = per <= 16 * 16 ? 16 : (per <= 32 * 16 ? 32 : 64);
+    int T = per <= 1024 ? 16 : (per <= 16384 ? 32 : 64);
     while (T < 64 && size_t(256 / T) * region > size_t(kLdsBudget)) T *= 2;
     const int G = 256 / T;
     const dim3 grid((B + G - 1) / G);
