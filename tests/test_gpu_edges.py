@@ -32,6 +32,11 @@ CASES = {
     "per_env_small": W_("per_env_small", 50, B=13, H=10, W=12, C=5, R=5,
                         shapes=((3, 3), (1, 2)), per_env=True),
     "max_rules": W_("max_rules", 55, B=5, H=8, W=8, C=4, R=252, shapes=((1, 1), (2, 2)), T=4),
+    # maps above 32 rows: the rows engine's four-wave variant, with 4-byte rows and with
+    # per-environment rule sets
+    "tall40x20": W_("tall40x20", 56, B=7, H=40, W=20, C=6, R=12, shapes=((3, 3), (2, 1)), T=10),
+    "tall_per_env": W_("tall_per_env", 57, B=5, H=48, W=40, C=5, R=8,
+                       shapes=((3, 3), (1, 2)), per_env=True, T=10),
 }
 LANE16 = {n for n, w in CASES.items() if w.H <= 16 and w.W <= 16 and not w.per_env}
 
@@ -67,6 +72,28 @@ def test_edge_case(name, engine, variant):
     say(f"[edge] {name} engine={engine} variant={variant}")
     maps, rules, actions = inputs.make_all(wl, 0, variant)
     check(wl, maps, rules, actions, engine)
+
+
+@pytest.mark.parametrize("variant", ["planted", "dense"])
+@pytest.mark.parametrize("name", ["tall40x20", "tall_per_env", "wide33", "c5", "c5_per_env"])
+def test_tall_maps_in_long_launches(name, variant):
+    """Rows engine on maps above 32 rows in launches of 20 steps (the rule program staged in
+    LDS, four waves per environment sharing the probe, the filter and the matching)."""
+    require_gpu()
+    if name.startswith("c5"):
+        wl = inputs.WORKLOADS["c5"].with_(B=3, T=40, L=5, per_env=name == "c5_per_env")
+    else:
+        wl = CASES[name].with_(T=40)
+    if not rows_ok(wl):
+        pytest.skip("not eligible for the rows engine")
+    say(f"[tall step_n] {name} variant={variant}")
+    maps, rules, actions = inputs.make_all(wl, 3, variant)
+    want_m, want_r, want_d = oracle.run(wl, maps, rules, actions, nthreads=8)
+    _, final, r, d, eng = gpu_run(wl, maps, rules, actions, engine="rows", mode="step_n",
+                                  chunk=20)
+    np.testing.assert_array_equal(r, want_r)
+    np.testing.assert_array_equal(d, want_d)
+    np.testing.assert_array_equal(final, want_m[-1])
 
 
 @pytest.mark.parametrize("engine", ["generic", "lane16", "wave", "rows"])
