@@ -417,8 +417,9 @@ __global__ void __launch_bounds__(64 * kWaves) rows_step(StepArgs a, RowsArgs rp
                 touched |= uint32_t(__builtin_amdgcn_readfirstlane(int(tmask)));
             }
         }
-        // with helper waves, wave w matches every nw-th candidate from the w-th on
-        const bool shared = nw > 1 && todo != 0ull;
+        // with helper waves and two or more candidates, wave w matches every nw-th candidate
+        // from the w-th on (a lone candidate is wave 0's, without meeting the others)
+        const bool shared = nw > 1 && (todo & (todo - 1ull)) != 0ull;
         if (shared) {
             uint64_t mine = 0;
             int q = 0;
@@ -470,18 +471,21 @@ __global__ void __launch_bounds__(64 * kWaves) rows_step(StepArgs a, RowsArgs rp
                 }
             } while (false);
             if (shared && last) {
-                // every wave adds its share; wave 0 goes on with the totals
-                if (wave_any(rsum != 0))
-                    for (int off = 32; off > 0; off >>= 1) rsum += __shfl_xor(rsum, off, 64);
-                if (y == 0) {
-                    if (rsum != 0) atomicAdd(&lcnt[2], rsum);
-                    if (touched != 0) atomicOr(reinterpret_cast<unsigned *>(&lcnt[1]), touched);
+                // the helper waves add their rewards and voted planes to the shared counters;
+                // wave 0 goes on with the totals (its own rewards stay in its lanes)
+                if (wv != 0) {
+                    if (wave_any(rsum != 0))
+                        for (int off = 32; off > 0; off >>= 1) rsum += __shfl_xor(rsum, off, 64);
+                    if (y == 0) {
+                        if (rsum != 0) atomicAdd(&lcnt[2], rsum);
+                        if (touched != 0) atomicOr(reinterpret_cast<unsigned *>(&lcnt[1]), touched);
+                    }
                 }
                 __syncthreads();
                 if (wv != 0) break;
                 nf = lcnt[0];
-                touched = uint32_t(lcnt[1]);
-                rsum = y == 0 ? lcnt[2] : 0;
+                touched |= uint32_t(lcnt[1]);
+                if (y == 0) rsum += lcnt[2];
             }
             if (nf > 0 && (a.sequential || last)) {
                 // write the planes the batch's rules voted on; planes where some cell got
