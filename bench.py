@@ -6,10 +6,16 @@ workload.  Prints one JSON line with env-steps/s (whole batch), cell-rule-update
 fraction of the HBM roofline for the step kernel, and the CPU oracle's rate on a bounded
 sample of the same workload on this host.
 
-Roofline: algorithmic bytes per env-step A = 2*C*H*W/8 (packed maps in and out) + 6
-(action u8, reward f32, done u8); a launch of k steps over B envs moves k*B*A algorithmic
-bytes; achieved = that / the launch's average duration (HIP events on the launch stream);
-peak = 8 TB/s.
+Timing: `--steps` steps in av_step_n launches of up to `--chunk` steps, repeated (at least
+five times) after `--warmup` untimed steps; each repeat is bracketed by HIP events on the
+launch stream, and the median is reported with every repeat listed.
+
+Roofline of the multi-step launch: VALU-bound (the maps stay on chip between its steps), so
+`roofline` is VALU lane-ops per launch (from committed counters of the same launch shape) over
+the launch's duration against 256 CUs x 64 lanes x 2.4 GHz.  The workload metric's HBM
+normaliser, A = 2*C*H*W/8 (packed maps in and out) + 6 (action u8, reward f32, done u8) bytes
+per env-step at 8 TB/s, is reported beside it and for the one-launch-per-step path
+(`per_launch_path`), which does move A bytes per env-step.
 """
 from __future__ import annotations
 
@@ -51,15 +57,16 @@ def algorithmic_bytes(wl) -> int:
     return 2 * wl.C * wl.H * wl.W // 8 + 6
 
 
-def measured_traffic(workload: str, engine: int, engine_name: str):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if it was taken
-    on the current sources of that engine's kernel; otherwise None."""
-    path = os.path.join(ROOT, "profiles", "traffic.json")
+def counter_record(key: str, engine_name: str):
+    """Per-launch hardware counters of one launch shape (`workload/engine/variant/k=steps per
+    launch`) from the committed rocprofv3 summaries, if they were taken on the current sources
+    of that engine's kernel; otherwise None."""
+    path = os.path.join(ROOT, "profiles", "counters.json")
     if not os.path.exists(path):
         return None
     try:
-        rec = json.load(open(path)).get(f"{workload}/{engine}")
-    except Exception:
+        rec = json.load(open(path)).get(key)
+    except (OSError, ValueError):
         return None
     if not rec or rec.get("kernel_hash") != kernel_hash(engine_name):
         return None
@@ -198,36 +205,75 @@ def bench_search(av, torch, wl, args):
             "level_sizes": [lv["children"] for lv in levels][:64]}
 
 
-def graph_step_us(av, torch, b, maps, acts, rew, don, n):
-    """Capture n av_step calls (one launch each) in a HIP graph on a side stream and time its
-    replays: the GPU-side cost of a one-step launch without the Python call."""
-    if n < 1:
+VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12   # 32-bit lane-ops/s: CUs x SIMDs x lanes x clock
+
+
+def make_hold(torch):
+    """A short device-side wait queued before a timed region: the launches of the region are
+    queued behind it while it runs, so the region's start event fires with the work already
+    queued and the events bracket device time, not the host's submission of the launches."""
+    sleep = getattr(torch.cuda, "_sleep", None)
+    if sleep is None:
         return None
-    b.reset(maps)
-    torch.cuda.synchronize()
+    return lambda: sleep(2_000_000)
+
+
+def timed_repeats(torch, stream, fn, repeats, hold):
+    """Run fn() `repeats` times, each between two HIP events on `stream` (synchronised on both
+    sides, a hold queued before the start event); returns the per-repeat times in ms."""
+    out = []
+    for _ in range(repeats):
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        if hold:
+            hold()
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        out.append(e0.elapsed_time(e1))
+    return out
+
+
+def per_launch_path(av, torch, b, acts, n, repeats, hold, roof_env_steps, B):
+    """One av_step launch per step for n steps: captured once in a HIP graph and replayed
+    (device cost of a one-step launch), and called from Python (what a Python agent loop
+    pays: ctypes marshalling and launch per step)."""
+    rew = torch.empty((n, B), dtype=torch.float32, device="cuda")
+    don = torch.empty((n, B), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
     g = torch.cuda.CUDAGraph()
     s = torch.cuda.Stream()
-    s.wait_stream(torch.cuda.current_stream())
+    s.wait_stream(stream)
     try:
         with torch.cuda.stream(s):
             av.av_set_stream(b.h, s)
             with torch.cuda.graph(g, stream=s):
                 for t in range(n):
-                    av.av_step(b.h, acts[t % acts.shape[0]], rew[t % rew.shape[0]],
-                               don[t % don.shape[0]])
+                    av.av_step(b.h, acts[t % acts.shape[0]], rew[t], don[t])
     finally:
-        torch.cuda.current_stream().wait_stream(s)
-        av.av_set_stream(b.h, torch.cuda.current_stream())
+        stream.wait_stream(s)
+        av.av_set_stream(b.h, stream)
     g.replay()
-    torch.cuda.synchronize()
-    reps = 10
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(reps):
-        g.replay()
-    e1.record()
-    torch.cuda.synchronize()
-    return e0.elapsed_time(e1) * 1e3 / (reps * n)
+    graph_ms = timed_repeats(torch, stream, g.replay, repeats, hold)
+
+    def eager():
+        for t in range(n):
+            av.av_step(b.h, acts[t % acts.shape[0]], rew[t], don[t])
+    eager()
+    py_ms = timed_repeats(torch, stream, eager, repeats, None)
+    g_us = float(np.median(graph_ms)) * 1e3 / n
+    p_us = float(np.median(py_ms)) * 1e3 / n
+    return {"api": "av_step", "steps": n,
+            "graph_us_per_step": g_us, "graph_repeats_ms": graph_ms,
+            "graph_env_steps_per_sec": B / (g_us * 1e-6),
+            "graph_frac_hbm_roofline": B / (g_us * 1e-6) / roof_env_steps,
+            "python_us_per_step": p_us, "python_repeats_ms": py_ms,
+            "python_frac_hbm_roofline": B / (p_us * 1e-6) / roof_env_steps,
+            "note": "one launch per step moves A bytes per env-step through memory (maps in "
+                    "and out, action, reward, done), so this path is measured against the HBM "
+                    "roofline; graph: n launches captured once and replayed (device time, a "
+                    "hold queued first); python: n av_step calls from Python per repeat"}
 
 
 def main():
@@ -236,6 +282,8 @@ def main():
     ap.add_argument("--steps", type=int, default=None, help="timed steps (default: workload T)")
     ap.add_argument("--warmup", type=int, default=None,
                     help="untimed steps before timing (default: one launch of --chunk steps)")
+    ap.add_argument("--repeats", type=int, default=7,
+                    help="timed repeats of the --steps region; the median is reported")
     ap.add_argument("--workload", default="c4")
     ap.add_argument("--variant", default="literal", choices=["literal", "planted", "dense"])
     ap.add_argument("--engine", default="auto", choices=["auto", "generic", "lane16", "wave", "rows"])
@@ -246,8 +294,9 @@ def main():
                     help="rule application control: loaded rule r is inhibited by rule r - 1")
     ap.add_argument("--site-order", default="rowmajor", choices=["rowmajor", "random"])
     ap.add_argument("--chunk", type=int, default=1000, help="steps per av_step_n launch")
-    ap.add_argument("--launch-steps", type=int, default=0,
-                    help="also time this many steps with one launch per step (av_step)")
+    ap.add_argument("--launch-steps", type=int, default=None,
+                    help="steps of the one-launch-per-step path (av_step; default: --steps, at "
+                         "most 100; 0 = skip)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="before timing, copy MIB MiB with a plain device copy (a known-size "
                          "reference for the HBM byte counters)")
@@ -280,6 +329,7 @@ def main():
     T = wl.T if args.steps is None else args.steps
     if args.warmup is None:
         args.warmup = min(args.chunk, T)
+    repeats = max(5, args.repeats)
     torch.cuda.set_device(0)
     if args.copy_calibration:
         n = args.copy_calibration << 20
@@ -308,61 +358,53 @@ def main():
     chunk = max(1, min(args.chunk, T))
     rew = torch.empty((chunk, wl.B), dtype=torch.float32, device="cuda")
     don = torch.empty((chunk, wl.B), dtype=torch.uint8, device="cuda")
+    pos = [0]                                   # next action row (the actions repeat)
 
-    def run(n_steps, base=0):
+    def run(n_steps):
         launches = 0
         t = 0
         while t < n_steps:
-            k = min(chunk, n_steps - t)
-            lo = (base + t) % actions.shape[0]
-            k = min(k, actions.shape[0] - lo)
+            lo = pos[0] % actions.shape[0]
+            k = min(chunk, n_steps - t, actions.shape[0] - lo)
             av.av_step_n(b.h, k, acts[lo:lo + k], rew[:k], don[:k])
             t += k
+            pos[0] += k
             launches += 1
         return launches
 
     if args.warmup:
         run(args.warmup)
     b.reset(maps)
+    pos[0] = 0
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    launches = run(T)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1)
+    hold = make_hold(torch)
+    launches = [0]
+
+    def region():
+        launches[0] = run(T)
+    rep_ms = timed_repeats(torch, stream, region, repeats, hold)
+    ms = float(np.median(rep_ms))
 
     env_steps = wl.B * T
     value = env_steps / (ms / 1e3)
     A = algorithmic_bytes(wl)
-    launch_ms = ms / launches
-    achieved = A * wl.B * (T / launches) / (launch_ms / 1e3) / 1e9
+    launch_ms = ms / launches[0]
     roof_env_steps = HBM_PEAK_GBS * 1e9 / A
+    steps_per_launch = T / launches[0]
+    key = f"{args.workload}/{engine_name}/{args.variant}/k={chunk}"
+    plain = control is None and args.rule_mode == "parallel" and args.seed == 0
+    rec = counter_record(key, engine_name) if plain and T % chunk == 0 else None
+    kernel = rec["kernel"] if rec else f"av_{engine_name}_step"
+    valu_ops = rec["valu_insts_per_launch"] * 64 if rec else None
+    achieved = valu_ops / (launch_ms * 1e-3) / 1e12 if valu_ops else None
 
     per_launch = None
-    if args.launch_steps:
-        n = args.launch_steps
+    n1 = min(T, 100) if args.launch_steps is None else args.launch_steps
+    if n1:
         b.reset(maps)
         torch.cuda.synchronize()
-        f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        f0.record(stream)
-        for t in range(n):
-            av.av_step(b.h, acts[t % actions.shape[0]], b.rewards, b.done)
-        f1.record(stream)
-        torch.cuda.synchronize()
-        ms1 = f0.elapsed_time(f1)
-        graph_us = graph_step_us(av, torch, b, maps, acts, rew, don, min(n, 100))
-        per_launch = {"api": "av_step", "steps": n, "ms_per_step": ms1 / n,
-                      "env_steps_per_sec": wl.B * n / (ms1 / 1e3),
-                      "frac_hbm_roofline": wl.B * n / (ms1 / 1e3) / roof_env_steps,
-                      "graph_us_per_step": graph_us,
-                      "graph_frac_hbm_roofline": None if graph_us is None else
-                      wl.B / (graph_us * 1e-6) / roof_env_steps,
-                      "note": "ms_per_step: one av_step call per step from Python (ctypes "
-                              "marshalling + launch); graph_us_per_step: the same calls "
-                              "captured once in a HIP graph and replayed (GPU-side cost of a "
-                              "one-step launch)"}
+        per_launch = per_launch_path(av, torch, b, acts, n1, repeats, hold, roof_env_steps, wl.B)
 
     observe = None
     if args.observe:
@@ -370,14 +412,7 @@ def main():
         obs = torch.empty((wl.B, wl.C, w, w), dtype=torch.uint8, device="cuda")
         av.av_observe(b.h, w, obs)
         torch.cuda.synchronize()
-        reps = 200
-        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        g0.record(stream)
-        for _ in range(reps):
-            av.av_observe(b.h, w, obs)
-        g1.record(stream)
-        torch.cuda.synchronize()
-        us = g0.elapsed_time(g1) * 1e3 / reps
+        us = _time_us(lambda: av.av_observe(b.h, w, obs), stream, torch, reps=200)
         moved = wl.B * (wl.C * w * w + wl.C * wl.H * wl.W // 8)   # window out, packed maps in
         # one step and its observation per call, as an agent needs them: fused (the lane16
         # kernel writes the window from its registers) against a step then av_observe
@@ -412,7 +447,6 @@ def main():
                            threads=min(16, os.cpu_count() or 1), rule_mode=args.rule_mode,
                            control=control)
 
-    traffic = measured_traffic(args.workload, engine, engine_name)
     out = {
         "metric": METRIC,
         "value": value,
@@ -432,28 +466,37 @@ def main():
                         f"{'/'.join(f'{n}x{m}' for n, m in wl.shapes)}, p_dc={wl.p_dc:.2f}, "
                         f"{args.variant}, episode {wl.L} steps",
             "B": wl.B, "H": wl.H, "W": wl.W, "C": wl.C, "R": wl.R, "variant": args.variant,
-            "engine": engine_name, "api": "av_step_n", "steps_per_launch": chunk,
-            "rule_mode": args.rule_mode,
+            "engine": engine_name, "api": "av_step_n", "steps_per_launch": steps_per_launch,
+            "launches_per_repeat": launches[0], "rule_mode": args.rule_mode,
             "control": None if control is None else {
                 "limit": args.limit, "inhibit_chain": args.inhibit_chain,
                 "site_order": args.site_order},
         },
+        "repeats_ms": rep_ms,
+        "timing": "median of the repeats; each repeat times exactly `steps` steps between HIP "
+                  "events on the launch stream, synchronised on both sides, with a device-side "
+                  "hold queued before the start event so the launches are queued when it fires"
+                  + ("" if hold else " (no hold available: host submission is inside the window)"),
         "cell_rule_updates_per_sec": value * wl.H * wl.W * wl.R,
         "pct_hbm_roofline": 100.0 * value / roof_env_steps,
         "roofline": {
-            "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBS,
-            "traffic": None if traffic is None else traffic["bytes_per_launch"],
-            "kernel": f"av_{engine_name}_step", "launch_ms": launch_ms,
-            "algorithmic_bytes_per_env_step": A,
-            "note": "achieved = A x B x (steps per launch) / launch time, A = maps in and out "
-                    "once per step + action + reward + done; av_step_n keeps the maps on chip "
-                    "across the launch, so the HBM traffic actually moved is `traffic` and frac "
-                    "may exceed 1",
+            "bound": "alu", "achieved": achieved, "peak": VALU_PEAK_TOPS, "unit": "Tlane-op/s",
+            "frac": None if achieved is None else achieved / VALU_PEAK_TOPS,
+            "traffic": rec["bytes_per_launch"] if rec else None,
+            "kernel": kernel, "launch_ms": launch_ms,
+            "valu_lane_ops_per_launch": valu_ops,
+            "counters": rec["source"] if rec else None,
+            "hbm_normaliser": {"algorithmic_bytes_per_env_step": A,
+                               "achieved_gbs": A * value / 1e9,
+                               "frac": A * value / 1e9 / HBM_PEAK_GBS},
+            "note": "av_step_n keeps the maps on chip for the whole launch, so HBM carries only "
+                    "actions, outputs and the maps once in and out (`traffic`); what bounds the "
+                    "launch is VALU issue: achieved = VALU lane-ops per launch (SQ_INSTS_VALU x "
+                    "64 from counters of this launch shape on these kernel sources) / the "
+                    "launch's duration, against 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz; "
+                    "hbm_normaliser is the workload metric's A bytes per env-step, which this "
+                    "path does not move (one-launch-per-step: per_launch_path)",
         },
-        "valu": None if traffic is None or "valu_busy" not in traffic else {
-            "busy": traffic["valu_busy"], "insts_per_wave_step": traffic["valu_insts_per_wave_step"],
-            "peak_lane_ops": 256 * 4 * 16 * 2.4e9, "source": traffic["source"]},
         "per_launch_path": per_launch,
         "observe": observe,
         "mutate": mutate,

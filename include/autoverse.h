@@ -281,12 +281,14 @@ av_status av_mutate_rules(int32_t num_sets, int32_t num_rules, int32_t channels,
  *     reward is the parent's plus the step's; the best node is the one with the highest
  *     reward, earliest visit first (the root, reward 0, counts);
  *   - children whose episode ended are terminal: counted, never expanded;
- *   - the others are keyed by a 64-bit hash of their packed map (SplitMix64's finalizer
- *     chained over each channel's rows read as 64-bit words; equal hashes are taken as equal
- *     states).  A child survives iff
- *     it has the best (reward, -depth) of its key in this level, lowest index among equals,
- *     and its key is new or it beats the (reward, -depth) stored for the key; survivors in
- *     index order, cut to max_frontier, are the next frontier.
+ *   - the others are deduplicated by state: two children, or a child and an earlier node,
+ *     hold the same state iff their maps are equal cell for cell.  A 64-bit hash of the
+ *     packed map (SplitMix64's finalizer chained over each channel's rows read as 64-bit
+ *     words) only chooses where the state is looked up in the table; maps with equal hashes
+ *     are compared and kept apart when they differ.  A child survives iff it has the best
+ *     (reward, -depth) of its state in this level, lowest index among equals, and its state
+ *     is new or it beats the (reward, -depth) stored for the state; survivors in index
+ *     order, cut to max_frontier, are the next frontier.
  * ------------------------------------------------------------------------------------- */
 typedef struct av_search_s *av_search_t;
 
@@ -300,6 +302,9 @@ typedef struct {
     int32_t device, engine, rule_mode; /* as av_config; engine AUTO picks as for a batch */
     int32_t best_first_k;              /* 0: level order; k in [1, 512]: batched best-first */
     int32_t max_nodes;                 /* best-first: node pool capacity, in [1, 2^26] */
+    int32_t hash_bits;                 /* 0: the full 64-bit map hash; h in [1, 63]: only its
+                                          low h bits (more maps share a hash; results do not
+                                          change, since states are compared exactly) */
     void *stream;                      /* hipStream_t; NULL = null stream */
 } av_search_config;
 
@@ -317,8 +322,9 @@ typedef struct {
 } av_search_info;
 
 /* Create a search: a children batch of num_actions x max_frontier environments, frontier
- * buffers and the hash table (28 bytes per slot) on cfg->device.  AV_EINVAL for sizes out of
- * range, AV_ENOMEM if the device allocations fail. */
+ * buffers and the state table (28 bytes per slot plus the slot's packed map, C x H x
+ * row_bytes bytes, where row_bytes is 2, 4 or 8 for W up to 16, 32 or 64) on cfg->device.
+ * AV_EINVAL for sizes out of range, AV_ENOMEM if the device allocations fail. */
 av_status av_search_create(const av_search_config *cfg, av_search_t *out);
 
 /* The rule set searched (one set, host arrays, layouts and checks as av_load_rules with

@@ -74,7 +74,7 @@ class av_search_config(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "height", "width", "channels", "max_rules", "max_pat_h", "max_pat_w",
         "max_episode_steps", "num_actions", "max_frontier", "table_log2", "device", "engine",
-        "rule_mode", "best_first_k", "max_nodes")] + [("stream", ctypes.c_void_p)]
+        "rule_mode", "best_first_k", "max_nodes", "hash_bits")] + [("stream", ctypes.c_void_p)]
 
 
 class av_search_info(ctypes.Structure):
@@ -481,7 +481,7 @@ class Search:
     def __init__(self, height, width, channels, max_rules, max_pat_h, max_pat_w,
                  max_episode_steps=0, num_actions=5, max_frontier=1 << 16, table_log2=20,
                  device=None, engine="auto", rule_mode="parallel", best_first_k=0,
-                 max_nodes=1 << 20):
+                 max_nodes=1 << 20, hash_bits=0):
         torch = _torch()
         self.device = torch.device("cuda", torch.cuda.current_device() if device is None
                                    else device)
@@ -490,7 +490,8 @@ class Search:
                                max_episode_steps, num_actions, max_frontier, table_log2,
                                self.device.index, ENGINES[engine] if isinstance(engine, str)
                                else engine, RULE_MODES[rule_mode] if isinstance(rule_mode, str)
-                               else rule_mode, best_first_k, max_nodes, current_stream_handle())
+                               else rule_mode, best_first_k, max_nodes, hash_bits,
+                               current_stream_handle())
         h = ctypes.c_void_p()
         _check("av_search_create", load_library().av_search_create(ctypes.byref(cfg),
                                                                    ctypes.byref(h)))

@@ -59,11 +59,11 @@ struct av_batch_s {
     void *d_state = nullptr;
     void *d_init = nullptr;
     int32_t *d_t = nullptr;
+    uint64_t *d_n = nullptr;         // batch step numbers, one copy per launch unit (B + 8)
     int envs_per_block = 1;
     int engine = AV_ENGINE_GENERIC;   // engine used by the next step
     int plain_engine = AV_ENGINE_GENERIC;   // engine without rule application control
     bool have_rules = false, have_maps = false;
-    uint64_t step_no = 0;            // batch steps since av_reset
     CtlArgs ctl;                     // rule application control (device arrays owned)
     int32_t R = 0;
     std::vector<uint8_t> features;   // binary rule features, [S][R][2][2][C+1][mh][mw]
@@ -232,6 +232,10 @@ av_status upload(T **dst, const std::vector<T> &src) {
     return AV_OK;
 }
 
+// Copies of the batch step number: one per launch unit (at most one per environment, and
+// the lane16 engine's last workgroup may hold up to three waves past the batch), plus slack.
+int step_copies(int B) { return B + 8; }
+
 av_status check_batch(av_batch_t b) {
     if (!b) return fail(AV_EINVAL, "batch handle is NULL");
     return AV_OK;
@@ -263,7 +267,7 @@ av_status step_prefix(av_batch_t b, int n, const uint8_t *actions, float *reward
     a.L = c.max_episode_steps; a.per_env = 0; a.k = 1;
     a.sequential = c.rule_mode == AV_RULES_SEQUENTIAL;
     a.row_bytes = b->row_bytes;
-    a.state = b->d_state; a.init = b->d_init; a.t = b->d_t;
+    a.state = b->d_state; a.init = b->d_init; a.t = b->d_t; a.nctr = b->d_n;
     a.actions = actions; a.rewards = rewards; a.done = done;
     a.prog = b->dprog;
     if (gsrc && b->engine != AV_ENGINE_LANE16)
@@ -354,11 +358,14 @@ av_status av_create_batch(const av_config *cfg, av_batch_t *out) {
     hipError_t e = hipMalloc(&b->d_state, b->state_bytes);
     if (e == hipSuccess) e = hipMalloc(&b->d_init, b->state_bytes);
     if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&b->d_t), sizeof(int32_t) * c.num_envs);
+    if (e == hipSuccess)
+        e = hipMalloc(reinterpret_cast<void **>(&b->d_n), sizeof(uint64_t) * step_copies(c.num_envs));
     if (e == hipSuccess) e = hipMemset(b->d_state, 0, b->state_bytes);
     if (e == hipSuccess) e = hipMemset(b->d_init, 0, b->state_bytes);
     if (e == hipSuccess) e = hipMemset(b->d_t, 0, sizeof(int32_t) * c.num_envs);
+    if (e == hipSuccess) e = hipMemset(b->d_n, 0, sizeof(uint64_t) * step_copies(c.num_envs));
     if (e != hipSuccess) {
-        dev_free(b->d_state); dev_free(b->d_init); dev_free(b->d_t);
+        dev_free(b->d_state); dev_free(b->d_init); dev_free(b->d_t); dev_free(b->d_n);
         delete b;
         return fail(e == hipErrorOutOfMemory ? AV_ENOMEM : AV_EDEVICE, "device allocation: %s",
                     hipGetErrorString(e));
@@ -477,9 +484,10 @@ av_status av_reset(av_batch_t b, const uint8_t *init_maps) {
     const av_config &c = b->cfg;
     AV_HIP(launch_pack(init_maps, b->d_init, b->d_state, c.num_envs, c.channels, c.height, c.width,
                        b->row_bytes, b->stream));
-    AV_HIP(hipMemsetAsync(b->d_t, 0, sizeof(int32_t) * c.num_envs, b->stream));
+    // step counters and batch step numbers to 0 with a kernel (no memset node under capture)
+    AV_HIP(launch_fill_counters(b->d_t, c.num_envs, b->d_n, step_copies(c.num_envs), 0, 0,
+                                b->stream));
     b->have_maps = true;
-    b->step_no = 0;
     return AV_OK;
 }
 
@@ -534,6 +542,9 @@ av_status av_set_rule_control(av_batch_t b, const int32_t *limit, const uint8_t 
     if (av_status st = set_device(b)) return st;
     AV_HIP(hipStreamSynchronize(b->stream));   // no step may still read the old arrays
     free_control(b);
+    // the engine, or its workgroup shape, may change below: every launch unit's copy of the
+    // batch step number takes copy 0's value, which every engine keeps current
+    AV_HIP(launch_fill_counters(nullptr, 0, b->d_n, step_copies(c.num_envs), 1, 0, b->stream));
     if (!active) return AV_OK;
     const int words = (Rt + 31) / 32;
     std::vector<int32_t> lim(size_t(S) * Rt, 0);
@@ -601,11 +612,10 @@ static av_status step_k(av_batch_t b, int32_t k, const uint8_t *actions, float *
     a.L = c.max_episode_steps; a.per_env = c.per_env_rules; a.k = k;
     a.sequential = c.rule_mode == AV_RULES_SEQUENTIAL;
     a.row_bytes = b->row_bytes;
-    a.state = b->d_state; a.init = b->d_init; a.t = b->d_t;
+    a.state = b->d_state; a.init = b->d_init; a.t = b->d_t; a.nctr = b->d_n;
     a.actions = actions; a.rewards = rewards; a.done = done;
     a.prog = b->dprog;
     a.ctl = b->ctl;
-    a.ctl.step_base = b->step_no;
     // the lane16 kernel writes small windows itself (one byte per lane and store); larger
     // windows are faster through the observation kernel's 16-byte stores
     // LDS of the fused path: its window buffers, the staged rows (1 KiB per channel) and
@@ -634,7 +644,6 @@ static av_status step_k(av_batch_t b, int32_t k, const uint8_t *actions, float *
         }
         AV_HIP(launch_generic_step(a, G, b->stream));
     }
-    b->step_no += uint64_t(k);
     if (obs && !fused)
         AV_HIP(launch_observe(b->d_state, c.num_envs, c.channels, c.height, c.width, b->row_bytes,
                               w, obs, b->stream));
@@ -780,10 +789,10 @@ av_status av_get_state(av_batch_t b, void *host_blob, size_t *bytes) {
     std::memcpy(h.magic, kBlobMagic, 8);
     h.B = b->cfg.num_envs; h.H = b->cfg.height; h.W = b->cfg.width; h.C = b->cfg.channels;
     h.row_bytes = b->row_bytes; h.state_bytes = b->state_bytes;
-    h.step_no = b->step_no;
     char *p = static_cast<char *>(host_blob);
-    std::memcpy(p, &h, sizeof h);
     AV_HIP(hipStreamSynchronize(b->stream));
+    AV_HIP(hipMemcpy(&h.step_no, b->d_n, sizeof(uint64_t), hipMemcpyDeviceToHost));   // copy 0
+    std::memcpy(p, &h, sizeof h);
     AV_HIP(hipMemcpy(p + sizeof h, b->d_state, b->state_bytes, hipMemcpyDeviceToHost));
     AV_HIP(hipMemcpy(p + sizeof h + b->state_bytes, b->d_init, b->state_bytes, hipMemcpyDeviceToHost));
     AV_HIP(hipMemcpy(p + sizeof h + 2 * b->state_bytes, b->d_t, sizeof(int32_t) * b->cfg.num_envs,
@@ -811,7 +820,9 @@ av_status av_set_state(av_batch_t b, const void *host_blob, size_t bytes) {
     AV_HIP(hipMemcpy(b->d_init, p + sizeof h + b->state_bytes, b->state_bytes, hipMemcpyHostToDevice));
     AV_HIP(hipMemcpy(b->d_t, p + sizeof h + 2 * b->state_bytes, sizeof(int32_t) * b->cfg.num_envs,
                      hipMemcpyHostToDevice));
-    b->step_no = h.step_no;
+    AV_HIP(launch_fill_counters(nullptr, 0, b->d_n, step_copies(b->cfg.num_envs), 0, h.step_no,
+                                b->stream));
+    AV_HIP(hipStreamSynchronize(b->stream));
     b->have_maps = true;
     return AV_OK;
 }
@@ -836,6 +847,7 @@ av_status av_destroy_batch(av_batch_t b) {
         dev_free(b->d_state);
         dev_free(b->d_init);
         dev_free(b->d_t);
+        dev_free(b->d_n);
     }
     delete b;
     return st;

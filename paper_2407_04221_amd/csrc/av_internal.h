@@ -89,7 +89,6 @@ struct CtlArgs {
     int32_t active = 0;                 // some limit or inhibition is set
     int32_t random = 0;                 // index channel: 0 row-major rank, 1 random
     uint64_t seed = 0;                  // key of the random index channel
-    uint64_t step_base = 0;             // batch step number of the launch's first step
 };
 
 // Everything a step kernel needs, passed by value.
@@ -102,6 +101,13 @@ struct StepArgs {
     void *state;                     // [C][B][H] rows
     const void *init;                // [C][B][H] rows
     int32_t *t;                      // [B] step counters
+    // Batch step numbers (steps since av_reset, the random index channel's counter word),
+    // one copy per launch unit: per wave on lane16, per workgroup on the other engines.
+    // Every unit reads its copy at the start of a launch and stores it advanced by k at the
+    // end, so the number lives on the device and captured launches replay correctly; all
+    // copies a unit index reaches hold the same value (av_api re-broadcasts copy 0 whenever
+    // the engine or its launch shape changes).  B + 8 entries.
+    uint64_t *nctr;
     const uint8_t *actions;          // [k][B]
     float *rewards;                  // [k][B]
     uint8_t *done;                   // [k][B]
@@ -121,6 +127,11 @@ hipError_t launch_pack(const uint8_t *src, void *dst, void *dst2, int B, int C, 
                        int row_bytes, hipStream_t s);
 hipError_t launch_unpack(const void *src, uint8_t *dst, int B, int C, int H, int W,
                          int row_bytes, hipStream_t s);
+// Step counters and batch step numbers without hipMemsetAsync (a fill kernel is safe under
+// stream capture): t[0..B) = 0 when t is given; nctr[0..n) = value, or = nctr[0] when
+// broadcast is set.
+hipError_t launch_fill_counters(int32_t *t, int B, uint64_t *nctr, int n, int broadcast,
+                                uint64_t value, hipStream_t s);
 hipError_t launch_generic_step(const StepArgs &a, int envs_per_block, hipStream_t s);
 size_t generic_env_lds_bytes(int H, int W, int C, int rules_per_set, bool control = false,
                              bool random = false);
@@ -153,7 +164,9 @@ struct SearchArgs {
     int64_t *slot = nullptr;                       // [n] table slot, -1 if none
     uint64_t *keys = nullptr, *vals = nullptr, *claim = nullptr;     // [slots]
     uint32_t *epoch = nullptr;                     // [slots]
+    void *store = nullptr;                         // [slots][C][H] rows: each slot's map
     uint64_t mask = 0;                             // slots - 1
+    uint64_t hash_mask = ~0ull;                    // bits of the map hash that are used
     uint64_t *best = nullptr;                      // packed (reward, -visit)
     uint32_t *counts = nullptr;                    // terminal, overflow, survivors
     int32_t *block_count = nullptr;                // [ceil(n / 256)]

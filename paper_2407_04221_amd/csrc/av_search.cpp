@@ -33,6 +33,7 @@ struct av_search_s {
     int64_t *slot = nullptr;
     uint64_t *keys = nullptr, *vals = nullptr, *claim = nullptr, *best = nullptr;
     uint32_t *epoch = nullptr, *counts = nullptr;
+    void *store = nullptr;           // [slots][C][H] rows: the map of each slot's state
     bool have_rules = false, begun = false;
     int64_t level = 0, visited = 0;
     // batched best-first (K > 0): node pool, open list (value, id) sorted, popped parents
@@ -68,7 +69,8 @@ void release(av_search_t s) {
     void *ptrs[] = {s->front[0], s->front[1], s->reward[0], s->reward[1], s->depth[0], s->depth[1],
                     s->actions, s->rew, s->done, s->kid_reward, s->kid_depth, s->block_count,
                     s->src_of, s->kid_val, s->slot, s->keys, s->vals, s->claim, s->best, s->epoch,
-                    s->counts, s->pool, s->pool_reward, s->pool_depth, s->parents, s->pool_val,
+                    s->counts, s->store, s->pool, s->pool_reward, s->pool_depth, s->parents,
+                    s->pool_val,
                     s->new_keys, s->pool_slot, s->okeys[0], s->okeys[1], s->oids[0], s->oids[1],
                     s->new_ids, s->n_par};
     for (void *p : ptrs)
@@ -86,7 +88,9 @@ SearchArgs level_args(av_search_t s, int n) {
     a.kid_reward = s->kid_reward; a.kid_depth = s->kid_depth; a.kid_val = s->kid_val;
     a.slot = s->slot;
     a.keys = s->keys; a.vals = s->vals; a.claim = s->claim; a.epoch = s->epoch;
+    a.store = s->store;
     a.mask = s->slots - 1;
+    a.hash_mask = s->cfg.hash_bits == 0 ? ~0ull : (1ull << s->cfg.hash_bits) - 1;
     a.best = s->best; a.counts = s->counts;
     a.block_count = s->block_count; a.src_of = s->src_of;
     a.next_reward = s->reward[1 - s->cur]; a.next_depth = s->depth[1 - s->cur];
@@ -122,6 +126,8 @@ av_status av_search_create(const av_search_config *cfg, av_search_t *out) {
         return set_error(AV_EINVAL, "best_first_k must be in [0, 512]");
     if (c.best_first_k > 0 && (c.max_nodes < 1 || c.max_nodes > (1 << 26)))
         return set_error(AV_EINVAL, "max_nodes must be in [1, 2^26]");
+    if (c.hash_bits < 0 || c.hash_bits > 63)
+        return set_error(AV_EINVAL, "hash_bits must be in [0, 63]");
     const int fcap = c.best_first_k > 0 ? c.best_first_k : c.max_frontier;   // parents per level
     av_config bc{};
     bc.num_envs = c.num_actions * fcap;
@@ -165,6 +171,8 @@ av_status av_search_create(const av_search_config *cfg, av_search_t *out) {
     if (e == hipSuccess) e = alloc(&s->vals, s->slots);
     if (e == hipSuccess) e = alloc(&s->claim, s->slots);
     if (e == hipSuccess) e = alloc(&s->epoch, s->slots);
+    if (e == hipSuccess)
+        e = hipMalloc(&s->store, s->slots * size_t(c.channels) * c.height * s->row_bytes);
     if (e == hipSuccess) e = alloc(&s->best, 1);
     if (e == hipSuccess) e = alloc(&s->counts, 3);
     if (e == hipSuccess && s->K > 0) {

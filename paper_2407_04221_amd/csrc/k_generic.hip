@@ -22,6 +22,8 @@
 //             with both signs count the votes exactly: new = (old + sum >= 1);
 //   end       done when no player bit is left or the counter reaches L; done
 //             environments reload their initial rows.
+#include <algorithm>
+
 #include "av_internal.h"
 #include "philox.h"
 
@@ -85,6 +87,9 @@ __global__ void __launch_bounds__(256) generic_step(StepArgs a, int G) {
         for (int c = 0; c < C; ++c)
             my[c * H + y] = load_row<RowT>(a.state, (size_t(c) * a.B + b) * H + y, a.row_bytes);
     int t_env = (live && y == 0) ? a.t[b] : 0;
+    // this workgroup's copy of the batch step number (read here, before the first barrier;
+    // thread 0 stores it advanced by k after the last one)
+    const uint64_t nbase = a.nctr[blockIdx.x];
 
     const RuleHdr *hdr = a.prog.hdr + size_t(s) * Rt;
     const uint32_t *ment = a.prog.match + size_t(s) * a.prog.match_stride;
@@ -108,7 +113,7 @@ __global__ void __launch_bounds__(256) generic_step(StepArgs a, int G) {
         }
         if (a.ctl.active && a.ctl.random && live) {
             // this step's random index channel, eight cells per Philox block
-            const uint64_t n = a.ctl.step_base + uint64_t(k);
+            const uint64_t n = nbase + uint64_t(k);
             for (int gi = y; gi * 8 < HW; gi += H) {
                 uint32_t u[8];
                 philox_words(a.ctl.seed, n, uint64_t(b), 0, uint64_t(gi), u);
@@ -287,6 +292,7 @@ __global__ void __launch_bounds__(256) generic_step(StepArgs a, int G) {
             store_row<RowT>(a.state, (size_t(c) * a.B + b) * H + y, a.row_bytes, my[c * H + y]);
         if (y == 0) a.t[b] = t_env;
     }
+    if (tid == 0) a.nctr[blockIdx.x] = nbase + uint64_t(a.k);
 }
 
 // uint8 [B][C][H][W] -> packed rows [C][B][H]; one thread per row.
@@ -303,6 +309,18 @@ __global__ void pack_rows(const uint8_t *src, void *dst, void *dst2, int B, int 
     for (int x = 0; x < W; ++x) v |= uint64_t(p[x] != 0) << x;
     store_row<uint64_t>(dst, row, row_bytes, v);
     if (dst2) store_row<uint64_t>(dst2, row, row_bytes, v);
+}
+
+// t[0..B) = 0 (when t is given) and nctr[0..n) = value, or nctr[0] when broadcasting
+// (thread 0 then leaves nctr[0] alone, so every thread reads the same value).
+__global__ void fill_counters(int32_t *t, int B, uint64_t *nctr, int n, int broadcast,
+                              uint64_t value) {
+    const int i = int(blockIdx.x * blockDim.x + threadIdx.x);
+    if (t && i < B) t[i] = 0;
+    if (i < n) {
+        if (!broadcast) nctr[i] = value;
+        else if (i > 0) nctr[i] = nctr[0];
+    }
 }
 
 // packed rows [C][B][H] -> uint8 [B][C][H][W]; one thread per row.
@@ -348,6 +366,15 @@ hipError_t launch_pack(const uint8_t *src, void *dst, void *dst2, int B, int C, 
     const unsigned blocks = unsigned((rows + threads - 1) / threads);
     hipLaunchKernelGGL(pack_rows, dim3(blocks), dim3(threads), 0, s, src, dst, dst2, B, C, H, W,
                        row_bytes);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_counters(int32_t *t, int B, uint64_t *nctr, int n, int broadcast,
+                                uint64_t value, hipStream_t s) {
+    const int m = std::max(t ? B : 0, n);
+    if (m <= 0) return hipSuccess;
+    hipLaunchKernelGGL(fill_counters, dim3(unsigned((m + 255) / 256)), dim3(256), 0, s, t, B, nctr,
+                       n, broadcast, value);
     return hipGetLastError();
 }
 

@@ -538,7 +538,10 @@ __global__ void __launch_bounds__(64 * kWaves) rows_step(StepArgs a, RowsArgs rp
     if (wv != 0) return;
     for (int c = 0; c < C; ++c)
         if (row) static_cast<ST *>(a.state)[c * plane + lrow] = ST(Pl[c * hp + y]);
-    if (y == 0) a.t[b] = t_env;
+    if (y == 0) {
+        a.t[b] = t_env;
+        a.nctr[b] += uint64_t(a.k);     // the batch step number (no rule control here)
+    }
 }
 
 }  // namespace

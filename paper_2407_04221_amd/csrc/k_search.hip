@@ -8,16 +8,26 @@
 //   (step)    the children batch takes one step with the batch engines;
 //   post      reward and depth are accumulated, the best (highest reward, earliest visit)
 //             is kept with one 64-bit atomicMax, terminal children are counted, and every
-//             other child hashes its packed map and inserts it into the open-addressing
-//             table: the slot's value becomes the max of (reward, -depth) packed in 64 bits;
-//             a child that raised it stamps the slot with this level's epoch;
-//   claim     children whose value is the slot's value, in a slot stamped this level, claim
-//             it with atomicMax(epoch, ~index): the lowest index among the best wins;
+//             other child hashes its packed map and finds its state's slot in the
+//             open-addressing table (below): the slot's value becomes the max of
+//             (reward, -depth) packed in 64 bits; a child that raised it stamps the slot with
+//             this level's epoch;
+//   claim     a child that took a fresh slot copies its map into the slot's map store and
+//             marks the slot published; children whose value is the slot's value, in a slot
+//             stamped this level, claim it with atomicMax(epoch, ~index): the lowest index
+//             among the best wins;
 //   flag      a child survives iff it holds its slot's claim; per-block survivor counts;
 //   scan      exclusive prefix sum of the block counts (one workgroup);
 //   place     survivors get their frontier position (block offset + in-block prefix);
 //   copy      the next frontier's rows, reward and depth are gathered from the survivors.
-// Keys are 64-bit hashes of the packed map (equal hash is taken as equal state).
+// Table slots hold one state each and states are compared exactly: a slot's 64-bit key word
+// is (32-bit tag of the map's hash) << 32 | owner, where the owner is kPending | child index
+// while the slot was taken by a child of the running level (its map is that child's rows in
+// the children batch) and kPublished once the map is in the slot's store entry.  A child
+// probes from hash & mask: an empty slot is taken with one compare-and-swap of the whole
+// word (tag and owner become visible together); a slot with its tag is the child's state iff
+// the owner's map equals the child's map row for row; anything else probes the next slot.
+// Equal hashes of different maps therefore never merge states; they only cost a comparison.
 #include <algorithm>
 
 #include "av_internal.h"
@@ -26,6 +36,8 @@ namespace av {
 namespace {
 
 constexpr uint32_t kMaxProbe = 4096;   // longest probe sequence before the table counts as full
+constexpr uint32_t kPending = 0x80000000u;     // owner word: taken this level by child (low bits)
+constexpr uint32_t kPublished = 0x40000000u;   // owner word: the map is in the slot's store entry
 
 template <typename RowT>
 __device__ inline uint64_t row_at(const void *base, size_t idx) {
@@ -91,14 +103,54 @@ __device__ inline uint64_t pack_value(int32_t reward, int32_t depth) {
     return (uint64_t(uint32_t(reward) ^ 0x80000000u) << 32) | uint64_t(0xFFFFFFFFu - uint32_t(depth));
 }
 
-// Find or claim the slot of key h; returns -1 when kMaxProbe slots are all taken by others.
-__device__ inline int64_t probe(uint64_t *keys, uint64_t mask, uint64_t h) {
-    uint64_t s = h & mask;
+__device__ inline uint32_t hash_tag(uint64_t h) { return uint32_t(h >> 32) ^ uint32_t(h); }
+
+// Do environment i of the packed [C][n][H] buffer `kids` and the map `other` hold the same
+// rows?  `other` is environment j of the same buffer (j >= 0) or a store entry ([C][H] rows).
+template <typename RowT>
+__device__ inline bool same_map(const void *kids, int n, int i, int j, const void *other, int C,
+                                int H) {
+    const RowT *a = static_cast<const RowT *>(kids);
+    const RowT *b = j >= 0 ? a : static_cast<const RowT *>(other);
+    for (int c = 0; c < C; ++c) {
+        const RowT *ra = a + (size_t(c) * n + i) * H;
+        const RowT *rb = j >= 0 ? b + (size_t(c) * n + j) * H : b + size_t(c) * H;
+        for (int y = 0; y < H; ++y)
+            if (ra[y] != rb[y]) return false;
+    }
+    return true;
+}
+
+// The slot of child i's state (hash h): an equal map found on its probe path, or the first
+// empty slot, taken for child i (*fresh = true).  -1 when kMaxProbe slots all hold other
+// states.
+template <typename RowT>
+__device__ inline int64_t probe_exact(const SearchArgs &a, const void *kids, int i, uint64_t h,
+                                      bool *fresh) {
+    const uint32_t tag = hash_tag(h);
+    const unsigned long long mine =
+        (static_cast<unsigned long long>(tag) << 32) | (kPending | uint32_t(i));
+    const size_t sbytes = size_t(a.C) * a.H * sizeof(RowT);
+    uint64_t s = h & a.mask;
+    *fresh = false;
     for (uint32_t k = 0; k < kMaxProbe; ++k) {
-        const uint64_t prev = atomicCAS(reinterpret_cast<unsigned long long *>(&keys[s]), 0ull,
-                                        static_cast<unsigned long long>(h));
-        if (prev == 0 || prev == h) return int64_t(s);
-        s = (s + 1) & mask;
+        const uint64_t prev =
+            atomicCAS(reinterpret_cast<unsigned long long *>(&a.keys[s]), 0ull, mine);
+        if (prev == 0) {
+            *fresh = true;
+            return int64_t(s);
+        }
+        if (uint32_t(prev >> 32) == tag) {
+            const uint32_t own = uint32_t(prev);
+            const bool eq = (own & kPending)
+                                ? same_map<RowT>(kids, a.n, i, int(own & ~kPending), nullptr,
+                                                 a.C, a.H)
+                                : same_map<RowT>(kids, a.n, i, -1,
+                                                 static_cast<const char *>(a.store) + s * sbytes,
+                                                 a.C, a.H);
+            if (eq) return int64_t(s);
+        }
+        s = (s + 1) & a.mask;
     }
     return -1;
 }
@@ -137,8 +189,9 @@ __global__ void __launch_bounds__(256) post_kernel(SearchArgs a, const void *kid
         atomicAdd(&a.counts[0], 1u);
         return;
     }
-    const uint64_t h = map_hash<RowT>(kids, i, a.n, a.C, a.H);
-    const int64_t s = probe(a.keys, a.mask, h);
+    const uint64_t h = map_hash<RowT>(kids, i, a.n, a.C, a.H) & a.hash_mask;
+    bool fresh;
+    const int64_t s = probe_exact<RowT>(a, kids, i, h, &fresh);
     if (s < 0) {
         atomicOr(&a.counts[1], 1u);
         return;
@@ -151,11 +204,24 @@ __global__ void __launch_bounds__(256) post_kernel(SearchArgs a, const void *kid
     a.kid_val[i] = v;
 }
 
-__global__ void __launch_bounds__(256) claim_kernel(SearchArgs a) {
+template <typename RowT>
+__global__ void __launch_bounds__(256) claim_kernel(SearchArgs a, const void *kids) {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= a.n) return;
     const int64_t s = a.slot[i];
     if (s < 0) return;
+    // publish a slot this child took: its map into the store, then the owner word (in this
+    // kernel the store is not read, and the other children of the slot read the key word
+    // only to see that it is not theirs; the next level sees both)
+    const uint64_t key = a.keys[s];
+    if (uint32_t(key) == (kPending | uint32_t(i))) {
+        RowT *dst = reinterpret_cast<RowT *>(static_cast<char *>(a.store) +
+                                             size_t(s) * a.C * a.H * sizeof(RowT));
+        const RowT *src = static_cast<const RowT *>(kids);
+        for (int c = 0; c < a.C; ++c)
+            for (int y = 0; y < a.H; ++y) dst[c * a.H + y] = src[(size_t(c) * a.n + i) * a.H + y];
+        a.keys[s] = (key & 0xFFFFFFFF00000000ull) | kPublished;
+    }
     if (a.vals[s] == a.kid_val[i] && a.epoch[s] == a.cur_epoch)
         atomicMax(reinterpret_cast<unsigned long long *>(&a.claim[s]),
                   static_cast<unsigned long long>((uint64_t(a.cur_epoch) << 32) |
@@ -252,9 +318,13 @@ __global__ void __launch_bounds__(256) copy_kernel(const void *kids, int n, void
 template <typename RowT>
 __global__ void root_kernel(SearchArgs a, const void *front) {
     if (blockIdx.x != 0 || threadIdx.x != 0) return;
-    const uint64_t h = map_hash<RowT>(front, 0, 1, a.C, a.H);
-    const int64_t s = probe(a.keys, a.mask, h);
-    if (s < 0) { a.counts[1] = 1; return; }
+    // the table is empty: the root takes its home slot, published at once
+    const uint64_t h = map_hash<RowT>(front, 0, 1, a.C, a.H) & a.hash_mask;
+    const uint64_t s = h & a.mask;
+    RowT *dst = reinterpret_cast<RowT *>(static_cast<char *>(a.store) +
+                                         size_t(s) * a.C * a.H * sizeof(RowT));
+    for (int r = 0; r < a.C * a.H; ++r) dst[r] = static_cast<const RowT *>(front)[r];
+    a.keys[s] = (uint64_t(hash_tag(h)) << 32) | kPublished;
     a.vals[s] = pack_value(0, 0);
     *a.best = (uint64_t(0x80000000u) << 32) | 0xFFFFFFFFull;
     if (a.root_slot) *a.root_slot = s;
@@ -455,7 +525,7 @@ hipError_t level_impl(const SearchArgs &a, const void *front, int nf, void *kids
     } else if (phase == 1) {
         const unsigned nb = blocks_for(size_t(a.n));
         hipLaunchKernelGGL(post_kernel<RowT>, dim3(nb), dim3(256), 0, s, a, kids, a.rew, a.done);
-        hipLaunchKernelGGL(claim_kernel, dim3(nb), dim3(256), 0, s, a);
+        hipLaunchKernelGGL(claim_kernel<RowT>, dim3(nb), dim3(256), 0, s, a, kids);
         hipLaunchKernelGGL(flag_kernel, dim3(nb), dim3(256), 0, s, a);
         hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(256), 0, s, a.block_count, int(nb),
                            &a.counts[2]);

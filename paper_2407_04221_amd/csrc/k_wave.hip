@@ -210,6 +210,9 @@ __global__ void __launch_bounds__(kMaxThreads) wave_step(StepArgs a, WaveLayout 
         for (int c = g; c < C; c += G)
             P[c * Hp + y] = load_row<RowT>(a.state, (size_t(c) * a.B + b) * H + y, a.row_bytes);
     int t_env = a.t[b];
+    // this workgroup's copy of the batch step number (read before the step loop's first
+    // barrier; thread 0 stores it advanced by k after the last one)
+    const uint64_t nbase = a.nctr[b];
     const RowT rowmask = low_mask<RowT>(W);
     constexpr int kHdrWords = sizeof(RuleHdr) / 4;
 
@@ -241,7 +244,7 @@ __global__ void __launch_bounds__(kMaxThreads) wave_step(StepArgs a, WaveLayout 
         }
         if (a.ctl.active && a.ctl.random) {
             // this step's random index channel, eight cells per Philox block
-            const uint64_t n = a.ctl.step_base + uint64_t(k);
+            const uint64_t n = nbase + uint64_t(k);
             for (int gi = tid; gi * 8 < H * W; gi += nthreads) {
                 uint32_t u[8];
                 philox_words(a.ctl.seed, n, uint64_t(b), 0, uint64_t(gi), u);
@@ -445,7 +448,10 @@ __global__ void __launch_bounds__(kMaxThreads) wave_step(StepArgs a, WaveLayout 
     if (row)
         for (int c = g; c < C; c += G)
             store_row<RowT>(a.state, (size_t(c) * a.B + b) * H + y, a.row_bytes, P[c * Hp + y]);
-    if (tid == 0) a.t[b] = t_env;
+    if (tid == 0) {
+        a.t[b] = t_env;
+        a.nctr[b] = nbase + uint64_t(a.k);
+    }
 }
 
 int rows_per_group(int H) { return H <= 16 ? 16 : (H <= 32 ? 32 : 64); }

@@ -553,13 +553,14 @@ hipError_t launch_lane16_step(const StepArgs &a, const Lane16Device &d, hipStrea
     float *rewards = a.rewards;
     uint8_t *done = a.done;
     int B = a.B, K = a.k;
-    unsigned long long seed = a.ctl.seed, step_base = a.ctl.step_base;
+    unsigned long long seed = a.ctl.seed;
+    uint64_t *nctr = a.nctr;
     uint8_t *obs = a.obs;
     int w = a.obs_w;
     const void *gsrc = a.gsrc;
     int gnf = a.gnf, gA = a.gA;
     const int32_t *gdepth = a.gdepth;
-    void *args[] = {&state, &init, &t, &actions, &rewards, &done, &B, &K, &seed, &step_base,
+    void *args[] = {&state, &init, &t, &actions, &rewards, &done, &B, &K, &seed, &nctr,
                     &obs, &w, &gsrc, &gnf, &gA, &gdepth};
     // dynamic LDS: the fused observation's window buffers, four waves of eight environments
     const unsigned lds = obs ? unsigned(4 * ((8 * a.C * w * w + 16 + 15) & ~15)) : 0u;

@@ -79,7 +79,7 @@ extern "C" __global__ void __launch_bounds__(256)
 av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restrict__ init,
                int *__restrict__ tctr, const unsigned char *__restrict__ actions,
                float *__restrict__ rewards, unsigned char *__restrict__ done, int B, int K,
-               unsigned long long seed, unsigned long long step_base,
+               unsigned long long seed, unsigned long long *__restrict__ nctr,
                unsigned char *__restrict__ obs, int w,
                const unsigned short *__restrict__ gsrc, int gnf, int gA,
                const int *__restrict__ gdepth) {
@@ -95,13 +95,17 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
     const u32 LF_MASK = CELL & ~BOTH(1u << (AV_W - 1));        // column W-1 receives nothing
     // safe (clamped) environment indices for loads; values of absent envs are masked off
     const int iA = hasA ? eA : 0, iB = hasB ? eB : 0;
+    // This wave's copy of the batch step number (steps since the reset, all environments
+    // together): read here, stored advanced by K at the end by lane 0.  Waves past the
+    // batch's last environment own no copy.
+    const bool unit = 8 * wave < B;
+    const unsigned long long nbase = unit ? nctr[wave] : 0ull;
 
 #ifdef AV_RANDOM_SITES
     __shared__ u32 kbuf[256 * 32];                  // per lane: the site keys of its row
     u32 *const kb = kbuf + threadIdx.x * 32;
 #else
     (void)seed;
-    (void)step_base;
 #endif
     // Search expansion (gsrc set): environment e starts from row block e / gA of gsrc, laid
     // out [C][gnf][H], with its step counter at gdepth[e / gA]; there are no initial maps to
@@ -205,7 +209,7 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
         int rA = 0, rB = 0;
         bool paid = false;
 #ifdef AV_RANDOM_SITES
-        const unsigned long long nstep = step_base + (unsigned long long)k;
+        const unsigned long long nstep = nbase + (unsigned long long)k;
         bool keys_ready = false;
 #endif
         /*@RULES@*/
@@ -350,4 +354,5 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
         if (hasA) tctr[eA] = tA;
         if (hasB) tctr[eB] = tB;
     }
+    if (unit && lane == 0) nctr[wave] = nbase + (unsigned long long)K;
 }

@@ -40,20 +40,32 @@ def test_step_matches_oracle(case, engine, seed, variant):
     assert (want_r != 0).any() or variant == "literal" or name == "c5"
 
 
+# (workload, B, T) for multi-step launches: long enough that launches of 70 steps cross the
+# engines' blocks of actions and results (16 steps on lane16, 64 on the wave and rows engines)
+STEP_N_CASES = [("c1", 1, 150), ("c2", 203, 150), ("c3", 37, 80), ("c4", 333, 160),
+                ("c5", 5, 75)]
+
+
+@pytest.mark.parametrize("chunk", [7, 70])
 @pytest.mark.parametrize("variant", ["literal", "dense"])
 @pytest.mark.parametrize("engine", ["generic", "wave", "rows", "auto"])
-@pytest.mark.parametrize("case", CASES, ids=_case_ids())
-def test_step_n_matches_oracle(case, engine, variant):
+@pytest.mark.parametrize("case", STEP_N_CASES, ids=[f"{n}-B{b}-T{t}" for n, b, t in STEP_N_CASES])
+def test_step_n_matches_oracle(case, engine, variant, chunk):
     require_gpu()
     name, B, T = case
     wl = inputs.WORKLOADS[name].with_(B=B, T=T, L=25)
-    say(f"[parity step_n] {name} B={B} T={T} engine={engine} variant={variant}")
+    say(f"[parity step_n] {name} B={B} T={T} engine={engine} variant={variant} chunk={chunk}")
     maps, rules, actions = inputs.make_all(wl, 2, variant)
     want_m, want_r, want_d = oracle.run(wl, maps, rules, actions, nthreads=8)
-    _, final, r, d, _ = gpu_run(wl, maps, rules, actions, engine=engine, mode="step_n", chunk=7)
+    _, final, r, d, _ = gpu_run(wl, maps, rules, actions, engine=engine, mode="step_n",
+                                chunk=chunk)
     np.testing.assert_array_equal(r, want_r)
     np.testing.assert_array_equal(d, want_d)
     np.testing.assert_array_equal(final, want_m[-1])
+    if T % 25 == 0:        # the last step is an episode-length reset step: check one before
+        _, f2, _, _, _ = gpu_run(wl, maps, rules, actions[:T - 3], engine=engine, mode="step_n",
+                                 chunk=chunk)
+        np.testing.assert_array_equal(f2, want_m[T - 4])
 
 
 # Shapes that stress the row-per-lane engine's edges: odd B (a half-empty lane word),

@@ -20,13 +20,14 @@ def one_set(rules):
 
 
 def compare(wl, root, rules, budget, levels, A=5, cap=1 << 12, L=None, engine="auto",
-            rule_mode="parallel", table_log2=18):
+            rule_mode="parallel", table_log2=18, hash_bits=0):
     L = wl.L if L is None else L
     mode = int(rule_mode == "sequential")
     o = osearch.Search(wl.H, wl.W, wl.C, rules, L, num_actions=A, max_frontier=cap,
                        rule_mode=mode)
     g = av.Search(wl.H, wl.W, wl.C, wl.R, wl.max_h, wl.max_w, L, num_actions=A,
-                  max_frontier=cap, table_log2=table_log2, engine=engine, rule_mode=rule_mode)
+                  max_frontier=cap, table_log2=table_log2, engine=engine, rule_mode=rule_mode,
+                  hash_bits=hash_bits)
     try:
         g.load_rules(*rules)
         o.begin(root)
@@ -88,6 +89,21 @@ def test_search_odd_shapes():
         compare(wl, maps[0], rules, 1500, 8)
 
 
+@pytest.mark.parametrize("hash_bits", [1, 3, 10])
+@pytest.mark.parametrize("name", ["c4", "c3"])
+def test_search_states_compared_exactly(name, hash_bits):
+    """With only the low 1, 3 or 10 bits of the map hash kept, most distinct states share a
+    hash with others (paper Sec. 2.2.1 prunes equal states only): the levels must still equal
+    the oracle's, which compares maps exactly."""
+    require_gpu()
+    wl = inputs.WORKLOADS[name].with_(B=1)
+    say(f"[search exact] {name} hash_bits={hash_bits}")
+    maps, rules, _ = inputs.make_all(wl, 5, "dense")
+    budget = 2500 if name == "c4" else 1200
+    last = compare(wl, maps[0], one_set(rules), budget, 10, hash_bits=hash_bits)
+    assert last["visited"] > 0 and last["survivors"] > 1
+
+
 def test_search_table_overflow_is_an_error():
     require_gpu()
     wl = inputs.WORKLOADS["c1"].with_(B=1)
@@ -108,13 +124,13 @@ def test_search_table_overflow_is_an_error():
 
 
 def compare_best_first(wl, root, rules, budget, iters, k, A=5, L=None, engine="auto",
-                       rule_mode="parallel", max_nodes=1 << 16, table_log2=18):
+                       rule_mode="parallel", max_nodes=1 << 16, table_log2=18, hash_bits=0):
     L = wl.L if L is None else L
     mode = int(rule_mode == "sequential")
     o = osearch.BestFirst(wl.H, wl.W, wl.C, rules, L, k=k, num_actions=A, rule_mode=mode)
     g = av.Search(wl.H, wl.W, wl.C, wl.R, wl.max_h, wl.max_w, L, num_actions=A,
                   table_log2=table_log2, engine=engine, rule_mode=rule_mode, best_first_k=k,
-                  max_nodes=max_nodes)
+                  max_nodes=max_nodes, hash_bits=hash_bits)
     try:
         g.load_rules(*rules)
         o.begin(root)
@@ -165,6 +181,18 @@ def test_best_first_engines_and_options(engine):
     compare_best_first(wl, maps[0], rules, 333, 20, 64, engine=engine)          # budget cut
     compare_best_first(wl, maps[0], rules, 2000, 20, 8, L=3, engine=engine)     # terminal
     compare_best_first(wl, maps[0], rules, 2000, 12, 8, engine=engine, rule_mode="sequential")
+
+
+@pytest.mark.parametrize("hash_bits", [2, 12])
+def test_best_first_states_compared_exactly(hash_bits):
+    """Best-first with most states sharing a truncated map hash: the iterations, including
+    the liveness test of popped nodes against their state's slot, equal the oracle's."""
+    require_gpu()
+    wl = inputs.WORKLOADS["c4"].with_(B=1)
+    say(f"[best-first exact] hash_bits={hash_bits}")
+    maps, rules, _ = inputs.make_all(wl, 5, "dense")
+    last = compare_best_first(wl, maps[0], one_set(rules), 2000, 25, 16, hash_bits=hash_bits)
+    assert last["visited"] > 0
 
 
 def test_best_first_pool_full_is_an_error():
