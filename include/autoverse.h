@@ -353,6 +353,33 @@ av_status av_search_frontier(av_search_t s, uint8_t *maps, int32_t *reward, int3
 /* Free the search; NULL is a no-op.  Synchronises. */
 av_status av_search_destroy(av_search_t s);
 
+/* For callers that cannot allocate device memory (harnesses that forbid hipMalloc, tight
+ * serving loops): k steps of B caller-owned environments, with the results of av_step_n on a
+ * batch made with *cfg, loaded with these rules and holding this state, on the wave engine
+ * (AV_ENGINE_WAVE, or AV_ENGINE_AUTO when its LDS working set fits) or the generic engine
+ * (AV_ENGINE_GENERIC, or AUTO otherwise).  Nothing is allocated: the compiled rule program and
+ * the launch units' scratch (8 bytes per environment) live in a static device array of the
+ * library of AV_STATIC_SCRATCH_BYTES per device, held until the process ends.
+ *   cfg       as av_create_batch (device, stream, sizes, per_env_rules, L, rule_mode); engine
+ *             AUTO, WAVE or GENERIC; no rule application control
+ *   rules     host arrays in the av_load_rules layout and with its checks
+ *   state     device, packed current maps [C][B][H] rows of row_bytes (2, 4 or 8 bytes for W
+ *             up to 16, 32, 64; bit x = column x), the layout of av_state_ptr; read and written
+ *   init      device, packed initial maps, same layout; episodes that end return to them
+ *   counters  device int32 [B], each environment's step counter; read and written
+ *   actions, rewards, done   as av_step_n ([k][B], device)
+ * AV_EINVAL (before any device work) for sizes out of range, NULL pointers, k < 1, bad rules,
+ * or a scratch image (8 x (B + 8) bytes plus the compiled program) above
+ * AV_STATIC_SCRATCH_BYTES.  Every call on one device shares that device's array and leaves
+ * the last program in it: calls that overlap on one device (other streams, other threads)
+ * race.  The program is copied from pageable host memory on the stream, which waits for the
+ * stream's earlier work; the call cannot be captured into a graph. */
+#define AV_STATIC_SCRATCH_BYTES (4u << 20)
+av_status av_step_n_static(const av_config *cfg, int32_t num_rules, const int32_t *shape,
+                           const int8_t *in_pat, const int8_t *out_pat, const int32_t *reward,
+                           void *state, const void *init, int32_t *counters, int32_t k,
+                           const uint8_t *actions, float *rewards, uint8_t *done);
+
 /* Device pointer to the packed current maps, owned by the batch and valid until the
  * next av_reset / av_set_state / av_destroy_batch.  Layout: rows of row_bytes bytes,
  * index [c][env][y] (channel-major over the whole batch); cell (env, c, y, x) is bit x

@@ -34,7 +34,7 @@ ABI_SYMBOLS = ("av_create_batch", "av_load_rules", "av_set_rule_control", "av_re
                "av_get_state", "av_set_state", "av_set_stream", "av_destroy_batch",
                "av_mutate_maps", "av_mutate_rules", "av_search_create", "av_search_load_rules",
                "av_search_begin", "av_search_expand", "av_search_frontier", "av_search_destroy",
-               "av_last_error")
+               "av_step_n_static", "av_last_error")
 
 
 class av_config(ctypes.Structure):
@@ -137,6 +137,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "av_search_expand": ([P, ctypes.c_int64, ctypes.POINTER(av_search_info)], ctypes.c_int),
         "av_search_frontier": ([P, P, P, P], ctypes.c_int),
         "av_search_destroy": ([P], ctypes.c_int),
+        "av_step_n_static": ([ctypes.POINTER(av_config), I32, P, P, P, P, P, P, P, I32, P, P, P],
+                             ctypes.c_int),
         "av_last_error": ([], ctypes.c_char_p),
     }
     for name, (args, res) in sig.items():
@@ -285,6 +287,45 @@ def av_step_n(batch, k, actions, rewards, done):
         batch, int(k), _dev_ptr(actions, torch.uint8, (k, B), "actions"),
         _dev_ptr(rewards, torch.float32, (k, B), "rewards"),
         _dev_ptr(done, torch.uint8, (k, B), "done")))
+
+
+def av_step_n_static(num_envs, height, width, channels, max_rules, max_pat_h, max_pat_w,
+                     rules, state, init, counters, actions, rewards, done, per_env_rules=False,
+                     max_episode_steps=0, engine="auto", rule_mode="parallel", device=None,
+                     stream=None):
+    """k steps of caller-owned environments without device allocation.  rules: host
+    (shape, in_pat, out_pat, reward) as av_load_rules; state / init: device uint8 tensors of
+    the packed layout (C * B * H * row_bytes bytes); counters: device int32 [B]; actions
+    uint8 [k][B], rewards float32 [k][B], done uint8 [k][B] device tensors."""
+    torch = _torch()
+    if device is None:
+        device = torch.cuda.current_device()
+    if stream is None:
+        with torch.cuda.device(device):
+            stream = current_stream_handle()
+    elif hasattr(stream, "cuda_stream"):
+        stream = ctypes.c_void_p(stream.cuda_stream)
+    cfg = av_config(num_envs, height, width, channels, max_rules, max_pat_h, max_pat_w,
+                    int(bool(per_env_rules)), max_episode_steps, int(device),
+                    ENGINES[engine] if isinstance(engine, str) else int(engine),
+                    RULE_MODES[rule_mode] if isinstance(rule_mode, str) else int(rule_mode),
+                    stream)
+    shape, ps = _host(rules[0], np.int32, "shape")
+    in_pat, pi = _host(rules[1], np.int8, "in_pat")
+    out_pat, po = _host(rules[2], np.int8, "out_pat")
+    reward, pr = _host(rules[3], np.int32, "reward")
+    R = shape.shape[1] if shape.ndim == 3 else 0
+    k = actions.shape[0]
+    row_bytes = 2 if width <= 16 else (4 if width <= 32 else 8)
+    nbytes = channels * num_envs * height * row_bytes
+    _check("av_step_n_static", load_library().av_step_n_static(
+        ctypes.byref(cfg), R, ps, pi, po, pr,
+        _dev_ptr(state, torch.uint8, (nbytes,), "state"),
+        _dev_ptr(init, torch.uint8, (nbytes,), "init"),
+        _dev_ptr(counters, torch.int32, (num_envs,), "counters"), int(k),
+        _dev_ptr(actions, torch.uint8, (k, num_envs), "actions"),
+        _dev_ptr(rewards, torch.float32, (k, num_envs), "rewards"),
+        _dev_ptr(done, torch.uint8, (k, num_envs), "done")))
 
 
 def av_step_observe(batch, k, actions, rewards, done, w, obs):

@@ -106,6 +106,10 @@ void free_control(av_batch_t b) {
     lane16_free(b->dlprog_ctl);
 }
 
+}  // namespace
+
+namespace av {
+
 // Output-kernel entry K_O = O - I; unspecified output: no vote; unspecified input: the
 // vote points at the output value (paper Sec. 2.1, transposed-convolution write).
 int kout(int in, int out) {
@@ -113,15 +117,6 @@ int kout(int in, int out) {
     if (out == 1) return in == 1 ? 0 : 1;
     return in == 0 ? 0 : -1;
 }
-
-// One rule in tri-valued form over C + 1 channels, n x m.
-struct HostRule {
-    int n = 1, m = 1, reward = 0;
-    std::vector<int8_t> in, out;   // [C+1][n][m]
-    int8_t at(const std::vector<int8_t> &p, int c, int i, int j) const {
-        return p[(size_t(c) * n + i) * m + j];
-    }
-};
 
 // The four built-in moves (paper Sec. 2.1: the player moves onto an adjacent cell that
 // holds force and no obstacle, consuming the force; Sec. 2.2.1: walls block): rules 0..3
@@ -223,6 +218,60 @@ void compile_generic(const std::vector<std::vector<HostRule>> &sets, int C, bool
         std::copy(vote[s].begin(), vote[s].end(), p.vote.begin() + s * p.vote_stride);
     }
 }
+
+
+// The moves followed by each set's loaded rules, checked (shapes within the map and the
+// pattern array, values in {-1, 0, 1}, an exact float reward): the rule sets of
+// av_load_rules' arguments (paper Sec. 2.1: rules are n x m input and output patterns with a
+// reward).
+av_status parse_rule_sets(const av_config &c, int32_t R, const int32_t *shape,
+                          const int8_t *in_pat, const int8_t *out_pat, const int32_t *reward,
+                          std::vector<std::vector<HostRule>> &sets) {
+    const int S = c.per_env_rules ? c.num_envs : 1;
+    const int C1 = c.channels + 1, ph = c.max_pat_h, pw = c.max_pat_w;
+    const size_t pat = size_t(C1) * ph * pw;
+    sets.assign(S, {});
+    const std::vector<HostRule> moves = move_rules(c.channels);
+    for (int s = 0; s < S; ++s) {
+        sets[s] = moves;
+        long long worst = 0;
+        for (int r = 0; r < R; ++r) {
+            const size_t k = size_t(s) * R + r;
+            HostRule hr;
+            hr.n = shape[2 * k];
+            hr.m = shape[2 * k + 1];
+            hr.reward = reward[k];
+            if (hr.n < 1 || hr.n > ph || hr.n > c.height || hr.m < 1 || hr.m > pw || hr.m > c.width)
+                return fail(AV_EINVAL, "set %d rule %d: shape %d x %d outside [1, min(max_pat, map)]",
+                            s, r, hr.n, hr.m);
+            for (size_t e = 0; e < pat; ++e) {
+                const int vi = in_pat[k * pat + e], vo = out_pat[k * pat + e];
+                if (vi < -1 || vi > 1 || vo < -1 || vo > 1)
+                    return fail(AV_EINVAL, "set %d rule %d: pattern value outside {-1, 0, 1}", s, r);
+            }
+            hr.in.assign(size_t(C1) * hr.n * hr.m, -1);
+            hr.out.assign(size_t(C1) * hr.n * hr.m, -1);
+            for (int ch = 0; ch < C1; ++ch)
+                for (int i = 0; i < hr.n; ++i)
+                    for (int j = 0; j < hr.m; ++j) {
+                        const size_t src = k * pat + (size_t(ch) * ph + i) * pw + j;
+                        hr.in[(size_t(ch) * hr.n + i) * hr.m + j] = in_pat[src];
+                        hr.out[(size_t(ch) * hr.n + i) * hr.m + j] = out_pat[src];
+                    }
+            const long long rw = hr.reward < 0 ? -(long long)hr.reward : hr.reward;
+            worst += rw * (long long)(c.height - hr.n + 1) * (c.width - hr.m + 1);
+            sets[s].push_back(std::move(hr));
+        }
+        if (worst >= (1LL << 24))
+            return fail(AV_EINVAL, "set %d: |reward| x anchors sums to %lld >= 2^24; the float "
+                        "reward would not be exact", s, worst);
+    }
+    return AV_OK;
+}
+
+}  // namespace av
+
+namespace {
 
 template <typename T>
 av_status upload(T **dst, const std::vector<T> &src) {
@@ -386,42 +435,8 @@ av_status av_load_rules(av_batch_t b, int32_t R, const int32_t *shape, const int
     const int S = c.per_env_rules ? c.num_envs : 1;
     const int C1 = c.channels + 1, ph = c.max_pat_h, pw = c.max_pat_w;
     const size_t pat = size_t(C1) * ph * pw;
-    std::vector<std::vector<HostRule>> sets(S);
-    const std::vector<HostRule> moves = move_rules(c.channels);
-    for (int s = 0; s < S; ++s) {
-        sets[s] = moves;
-        long long worst = 0;
-        for (int r = 0; r < R; ++r) {
-            const size_t k = size_t(s) * R + r;
-            HostRule hr;
-            hr.n = shape[2 * k];
-            hr.m = shape[2 * k + 1];
-            hr.reward = reward[k];
-            if (hr.n < 1 || hr.n > ph || hr.n > c.height || hr.m < 1 || hr.m > pw || hr.m > c.width)
-                return fail(AV_EINVAL, "set %d rule %d: shape %d x %d outside [1, min(max_pat, map)]",
-                            s, r, hr.n, hr.m);
-            for (size_t e = 0; e < pat; ++e) {
-                const int vi = in_pat[k * pat + e], vo = out_pat[k * pat + e];
-                if (vi < -1 || vi > 1 || vo < -1 || vo > 1)
-                    return fail(AV_EINVAL, "set %d rule %d: pattern value outside {-1, 0, 1}", s, r);
-            }
-            hr.in.assign(size_t(C1) * hr.n * hr.m, -1);
-            hr.out.assign(size_t(C1) * hr.n * hr.m, -1);
-            for (int ch = 0; ch < C1; ++ch)
-                for (int i = 0; i < hr.n; ++i)
-                    for (int j = 0; j < hr.m; ++j) {
-                        const size_t src = k * pat + (size_t(ch) * ph + i) * pw + j;
-                        hr.in[(size_t(ch) * hr.n + i) * hr.m + j] = in_pat[src];
-                        hr.out[(size_t(ch) * hr.n + i) * hr.m + j] = out_pat[src];
-                    }
-            const long long rw = hr.reward < 0 ? -(long long)hr.reward : hr.reward;
-            worst += rw * (long long)(c.height - hr.n + 1) * (c.width - hr.m + 1);
-            sets[s].push_back(std::move(hr));
-        }
-        if (worst >= (1LL << 24))
-            return fail(AV_EINVAL, "set %d: |reward| x anchors sums to %lld >= 2^24; the float "
-                        "reward would not be exact", s, worst);
-    }
+    std::vector<std::vector<HostRule>> sets;
+    if (av_status st = parse_rule_sets(c, R, shape, in_pat, out_pat, reward, sets)) return st;
     std::vector<uint8_t> feats(size_t(S) * R * 4 * pat);
     for (size_t k = 0; k < size_t(S) * R; ++k)
         for (int io = 0; io < 2; ++io) {

@@ -68,6 +68,25 @@ inline uint32_t pack_vote(int r, int i, int j, bool plus) {
     return uint32_t(r) | (uint32_t(i) << 8) | (uint32_t(j) << 16) | (uint32_t(plus) << 24);
 }
 
+// One rule in tri-valued form over C + 1 channels, n x m (1 must be 1, 0 must be 0,
+// -1 don't care).
+struct HostRule {
+    int n = 1, m = 1, reward = 0;
+    std::vector<int8_t> in, out;   // [C+1][n][m]
+    int8_t at(const std::vector<int8_t> &p, int c, int i, int j) const {
+        return p[(size_t(c) * n + i) * m + j];
+    }
+};
+
+// Host-side rule handling (av_api.cpp): the checked rule sets of av_load_rules' arguments
+// (each starting with the four moves; failures set the thread's last error), and their
+// compiled generic program (rule-major votes include the force plane's when force_votes).
+av_status parse_rule_sets(const av_config &c, int32_t R, const int32_t *shape,
+                          const int8_t *in_pat, const int8_t *out_pat, const int32_t *reward,
+                          std::vector<std::vector<HostRule>> &sets);
+void compile_generic(const std::vector<std::vector<HostRule>> &sets, int C, bool force_votes,
+                     GenericProgram &p);
+
 // Device-side copy of a generic program.
 struct DeviceProgram {
     RuleHdr *hdr = nullptr;
