@@ -122,6 +122,79 @@ class Gen {
         return bits;
     }
 
+    // One term of a bit-sliced sum: a plane word, possibly complemented.
+    struct Bit {
+        std::string name;
+        bool inv = false;
+        std::string expr() const { return inv ? "(~" + name + ")" : name; }
+    };
+
+    // v_bitop3 truth table of f over three operands, each possibly complemented: bit
+    // (4 a + 2 b + c) of the table is f(a, b, c) for operand bits a, b, c (the first operand
+    // is the table index's high bit).
+    template <typename F>
+    static int table3(F f, bool i0, bool i1, bool i2) {
+        int t = 0;
+        for (int k = 0; k < 8; ++k) {
+            const int a = ((k >> 2) & 1) ^ int(i0), b = ((k >> 1) & 1) ^ int(i1), c = (k & 1) ^ int(i2);
+            t |= (f(a, b, c) & 1) << k;
+        }
+        return t;
+    }
+
+    // The cells where the number of set terms is at least K (K >= 1): the terms are added
+    // with a carry-save tree of full adders (sum and carry are one v_bitop3 each, with the
+    // terms' complements folded into the truth tables) and the count's bits are compared with
+    // the constant K; emitted as GT.
+    void at_least(const std::vector<Bit> &terms, long K) {
+        std::vector<std::deque<Bit>> lv(1, std::deque<Bit>(terms.begin(), terms.end()));
+        std::vector<Bit> bits;
+        auto op3 = [&](const Bit &a, const Bit &b, const Bit &c, int table) {
+            const std::string r = fresh();
+            o << "const " << type << " " << r << " = __builtin_amdgcn_bitop3_b32(" << a.name << ", "
+              << b.name << ", " << c.name << ", 0x" << std::hex << table << std::dec << ");\n";
+            return Bit{r, false};
+        };
+        auto sum3 = [](int a, int b, int c) { return a ^ b ^ c; };
+        auto maj3 = [](int a, int b, int c) { return (a & b) | (a & c) | (b & c); };
+        auto xor2 = [](int a, int b, int) { return a ^ b; };
+        auto and2 = [](int a, int b, int) { return a & b; };
+        for (size_t k = 0; k < lv.size(); ++k) {
+            std::deque<Bit> q = lv[k];
+            std::vector<Bit> carries;
+            while (q.size() >= 3) {
+                const Bit a = q[0], b = q[1], c = q[2];
+                q.pop_front(); q.pop_front(); q.pop_front();
+                q.push_back(op3(a, b, c, table3(sum3, a.inv, b.inv, c.inv)));
+                carries.push_back(op3(a, b, c, table3(maj3, a.inv, b.inv, c.inv)));
+            }
+            if (q.size() == 2) {
+                const Bit a = q[0], b = q[1];
+                q.clear();
+                q.push_back(op3(a, b, a, table3(xor2, a.inv, b.inv, a.inv)));
+                carries.push_back(op3(a, b, a, table3(and2, a.inv, b.inv, a.inv)));
+            }
+            bits.push_back(q.empty() ? Bit{"0u", false} : q.front());
+            if (!carries.empty()) {
+                if (lv.size() == k + 1) lv.emplace_back();
+                lv[k + 1].insert(lv[k + 1].end(), carries.begin(), carries.end());
+            }
+        }
+        const size_t m = bits.size();
+        if (m < 63 && K >= (1L << m)) {
+            o << type << " GT = 0u;\n";
+            return;
+        }
+        // count >= K: from the high bit down, EQ holds where the count's bits so far equal K's,
+        // GE where they already exceed them
+        o << type << " GT = 0u, EQ = ~(" << type << ")0u;\n";
+        for (size_t k = m; k-- > 0;) {
+            if ((K >> k) & 1) o << "EQ &= " << bits[k].expr() << ";\n";
+            else o << "GT |= EQ & " << bits[k].expr() << ";\n";
+        }
+        o << "GT |= EQ;\n";
+    }
+
     // The cells where old + #plus > #minus: a bit-sliced comparison of two counts (bits least
     // significant first), emitted as GT; the caller declares nothing.
     void greater(const std::vector<std::string> &P, const std::vector<std::string> &N) {

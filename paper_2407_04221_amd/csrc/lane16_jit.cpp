@@ -14,8 +14,9 @@
 //          columns onto the cells it writes; +1 votes are OR-ed into PL_c, -1 votes into
 //          MI_c.  A cell with votes of one sign only takes that sign's value; if some cell
 //          of the wave has votes of both signs, the channel's votes are counted exactly with
-//          carry-save adders and the cell becomes 1 iff old + #plus > #minus, i.e. iff
-//          old + sum >= 1 (Sec. 2.1 transposed-convolution write, clamped to {0, 1}).
+//          carry-save adders and the cell becomes 1 iff old + sum >= 1 (Sec. 2.1
+//          transposed-convolution write, clamped to {0, 1}), counted as old + #plus +
+//          #(minus terms that are 0) >= #minus + 1.
 //   The force plane's own votes are not evaluated: the plane is dropped after the step.
 #include <hip/hip_runtime.h>
 
@@ -311,24 +312,29 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
             voted.push_back(c);
             if (!pl[c].empty() && !mi[c].empty()) both.push_back(c);
         }
-        // the one-sign result of every plane comes first, off the exact-count branches' path;
-        // each channel with votes of both signs is then recounted only in waves where some
-        // cell of that channel got both
+        // the one-sign result of every plane comes first, off the exact-count branch's path
         for (int c : voted)
             o << "u32 N" << c << " = (p[" << c << "] | PL" << c << ") & ~MI" << c << ";\n";
         auto tname = [](int r, int i, int j) {
             return "T" + std::to_string(r) + "_" + std::to_string(i) + "_" + std::to_string(j);
         };
-        for (int c : both) {
-            o << "if (ANY(PL" << c << " & MI" << c << ")) { // channel " << c << ": " << pl[c].size()
-              << " + votes, " << mi[c].size() << " - votes\n";
+        if (!both.empty()) {
+            // Exact counts, in waves where some cell of some channel got votes of both signs.
+            // Every match word moved onto the cells it votes on is formed once for all the
+            // channels; then each mixed channel becomes old + #plus - #minus >= 1, counted as
+            // old + #plus + #(minus terms that are 0) >= #minus + 1 (one carry-save count).
+            o << "if (ANY(";
+            for (size_t k = 0; k < both.size(); ++k)
+                o << (k ? " | " : "") << "(PL" << both[k] << " & MI" << both[k] << ")";
+            o << ")) {\n";
             std::set<std::pair<int, int>> shifts;
             std::set<std::tuple<int, int, int>> terms;
-            for (auto *lst : {&pl[c], &mi[c]})
-                for (const Vote &v : *lst) {
-                    if (v.j) shifts.insert({v.r, v.j});
-                    terms.insert({v.r, v.i, v.j});
-                }
+            for (int c : both)
+                for (auto *lst : {&pl[c], &mi[c]})
+                    for (const Vote &v : *lst) {
+                        if (v.j) shifts.insert({v.r, v.j});
+                        terms.insert({v.r, v.i, v.j});
+                    }
             for (auto &sh : shifts)
                 o << "const u32 E" << sh.first << "_" << sh.second << " = M" << sh.first << " << "
                   << sh.second << ";\n";
@@ -338,11 +344,16 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
                 o << "const u32 " << tname(r, i, j) << " = "
                   << (i ? "DPP_SHR(" + src + ", " + std::to_string(i) + ")" : src) << ";\n";
             }
-            std::vector<std::string> pt{"p[" + std::to_string(c) + "]"}, mt;
-            for (const Vote &v : pl[c]) pt.push_back(tname(v.r, v.i, v.j));
-            for (const Vote &v : mi[c]) mt.push_back(tname(v.r, v.i, v.j));
-            g.greater(g.count(pt), g.count(mt));
-            o << "N" << c << " = GT;\n}\n";
+            for (int c : both) {
+                o << "if (ANY(PL" << c << " & MI" << c << ")) { // channel " << c << ": "
+                  << pl[c].size() << " + votes, " << mi[c].size() << " - votes\n";
+                std::vector<Gen::Bit> cnt{{"p[" + std::to_string(c) + "]", false}};
+                for (const Vote &v : pl[c]) cnt.push_back({tname(v.r, v.i, v.j), false});
+                for (const Vote &v : mi[c]) cnt.push_back({tname(v.r, v.i, v.j), true});
+                g.at_least(cnt, long(mi[c].size()) + 1);
+                o << "N" << c << " = GT;\n}\n";
+            }
+            o << "}\n";
         }
         for (int c : voted) o << "p[" << c << "] = N" << c << ";\n";
     };
@@ -499,11 +510,13 @@ std::string lane16_rules_body_sequential(int C, int H, int W, const std::vector<
                 o << "const u32 " << tname(t.first, t.second) << " = " << term(Vote{r, t.first, t.second})
                   << ";\n";
             for (int c : both) {
-                std::vector<std::string> pt{plane(c, C)}, mt;
-                for (const Vote &v : plus[c]) pt.push_back(tname(v.i, v.j));
-                for (const Vote &v : minus[c]) mt.push_back(tname(v.i, v.j));
+                // old + #plus - #minus >= 1, counted as old + #plus + #(minus terms that are
+                // 0) >= #minus + 1
+                std::vector<Gen::Bit> cnt{{plane(c, C), false}};
+                for (const Vote &v : plus[c]) cnt.push_back({tname(v.i, v.j), false});
+                for (const Vote &v : minus[c]) cnt.push_back({tname(v.i, v.j), true});
                 o << "{ // plane " << c << "\n";
-                g.greater(g.count(pt), g.count(mt));
+                g.at_least(cnt, long(minus[c].size()) + 1);
                 o << "N" << c << " = GT;\n}\n";
             }
             o << "}\n";

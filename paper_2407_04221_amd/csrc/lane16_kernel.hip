@@ -12,11 +12,12 @@
 // half are kept zero.
 //
 // Environments of a wave that do not exist (B not a multiple of 8) compute on zero rows and
-// are never stored.  The initial rows stay in registers for resets (a single-step launch
-// reads them only when one of the wave's environments ends its episode).  Actions are read 16
-// steps at a time and turned into per-direction force masks, which each step fetches across
-// its row with ds_bpermute one step ahead; rewards and done flags are kept in registers for 16
-// steps and stored together.
+// are never stored.  The launch issues all of its first loads (current and initial rows, step
+// counters, three blocks of actions) before using any, so it waits for memory once; the
+// initial rows then stay in registers for resets.  Actions are read 16 steps at a time and
+// turned into per-direction force masks, which each step fetches across its row with
+// ds_bpermute one step ahead; rewards and done flags are kept in registers for 16 steps and
+// stored together.
 //
 // One step, per the paper (Sec. 2.1, Sec. 2.1.1, Sec. 2.2.1):
 //   force    F = the player plane moved one cell in each environment's action direction;
@@ -110,34 +111,14 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
     // Search expansion (gsrc set): environment e starts from row block e / gA of gsrc, laid
     // out [C][gnf][H], with its step counter at gdepth[e / gA]; there are no initial maps to
     // return to (an ended episode is never expanded further).
-    // Current rows, and the initial rows for automatic resets.  A launch of several steps
-    // keeps the initial rows in registers from the start; a single-step launch reads them
-    // only if one of the wave's environments ends its episode.
+    // Current rows, and the initial rows for automatic resets, held in registers for the whole
+    // launch.
     u32 p[AV_C], q[AV_C];
     const unsigned short *const src = gsrc ? gsrc : state;
     const int sstride = gsrc ? gnf : B;
     const int sA = gsrc ? iA / gA : iA, sB = gsrc ? iB / gA : iB;
     const int yy = rowok ? y : 0;
     const u32 keep = HALF(hasA && rowok, hasB && rowok);
-    auto load_init = [&]() {
-#pragma unroll
-        for (int c = 0; c < AV_C; ++c) {
-            const size_t row = size_t(c) * B;
-            const u32 ilo = u32(init[(row + iA) * AV_H + yy]);
-            const u32 ihi = u32(init[(row + iB) * AV_H + yy]);
-            q[c] = (ilo | (ihi << 16)) & keep;
-        }
-    };
-#pragma unroll
-    for (int c = 0; c < AV_C; ++c) {
-        const u32 lo = u32(src[(size_t(c) * sstride + sA) * AV_H + yy]);
-        const u32 hi = u32(src[(size_t(c) * sstride + sB) * AV_H + yy]);
-        p[c] = (lo | (hi << 16)) & keep;
-        q[c] = p[c];
-    }
-    const bool lazy_init = K == 1 && !gsrc;
-    if (!gsrc && !lazy_init) load_init();
-    int tA = gsrc ? gdepth[sA] : tctr[iA], tB = gsrc ? gdepth[sB] : tctr[iB];
 
     // Actions arrive 16 steps at a time and become force masks: lane y of a row holds, for
     // step k0 + y of its pair, one mask per direction (up, right, down, left) that is all ones
@@ -156,6 +137,34 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
         ra = u32(row[iA]);
         rb = u32(row[iB]);
     };
+    // Every global load the launch starts with is issued before any of them is used, so the
+    // prologue waits for memory once: the current and initial rows, the step counters and
+    // three blocks of actions.
+    u32 slo[AV_C], shi[AV_C], ilo[AV_C], ihi[AV_C];
+#pragma unroll
+    for (int c = 0; c < AV_C; ++c) {
+        slo[c] = u32(src[(size_t(c) * sstride + sA) * AV_H + yy]);
+        shi[c] = u32(src[(size_t(c) * sstride + sB) * AV_H + yy]);
+    }
+    // (a search expansion loads the batch's initial rows too, without a branch, and ignores
+    // them)
+#pragma unroll
+    for (int c = 0; c < AV_C; ++c) {
+        ilo[c] = u32(init[(size_t(c) * B + iA) * AV_H + yy]);
+        ihi[c] = u32(init[(size_t(c) * B + iB) * AV_H + yy]);
+    }
+    const int *const tsrc = gsrc ? gdepth : tctr;
+    int tA = tsrc[sA], tB = tsrc[sB];
+    u32 ra0, rb0, ra1, rb1, ra, rb;
+    raw_block(0, ra0, rb0);
+    raw_block(16, ra1, rb1);
+    raw_block(32, ra, rb);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int c = 0; c < AV_C; ++c) {
+        p[c] = (slo[c] | (shi[c] << 16)) & keep;
+        q[c] = gsrc ? p[c] : (ilo[c] | (ihi[c] << 16)) & keep;
+    }
     const u32 COLS = BOTH(COLMASK(AV_W));
     auto dir_masks = [&](u32 aA, u32 aB, u32 *m) {
         m[0] = HALF(aA == 1u, aB == 1u) & COLS;
@@ -163,12 +172,9 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
         m[2] = HALF(aA == 3u, aB == 3u) & COLS;
         m[3] = HALF(aA == 4u, aB == 4u) & COLS & ~BOTH(1u << (AV_W - 1));
     };
-    u32 cur[4], nxt[4], g[4], ra, rb;
-    raw_block(0, ra, rb);
-    dir_masks(ra, rb, cur);
-    raw_block(16, ra, rb);
-    dir_masks(ra, rb, nxt);
-    raw_block(32, ra, rb);
+    u32 cur[4], nxt[4], g[4];
+    dir_masks(ra0, rb0, cur);
+    dir_masks(ra1, rb1, nxt);
     const int src_base = (lane & 48) << 2;
 #pragma unroll
     for (int d = 0; d < 4; ++d) g[d] = u32(__builtin_amdgcn_ds_bpermute(src_base, int(cur[d])));
@@ -181,7 +187,10 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
     int rbA = 0, rbB = 0;
     u32 dbuf = 0u;
 
-    for (int k = 0; k < K; ++k) {
+    // (K >= 1 always: a loop with no entry test keeps the prologue's loads in the first block,
+    // where they are issued together, instead of next to their first use in the loop)
+    int k = 0;
+    do {
         const int s = k & 15;
         // force tiles next to every player cell, toward each environment's action
         u32 F;
@@ -250,7 +259,6 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
             if (dA) tA = 0;
             if (dB) tB = 0;
             if (y == s) dbuf = u32(dA) | (u32(dB) << 1);
-            if (lazy_init) load_init();     // the launch's only step
             const u32 dm = HALF(dA, dB);
 #pragma unroll
             for (int c = 0; c < AV_C; ++c) p[c] = (q[c] & dm) | (p[c] & ~dm);
@@ -273,7 +281,7 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
             rbB = 0;
             dbuf = 0u;
         }
-    }
+    } while (++k < K);
 
 #pragma unroll
     for (int c = 0; c < AV_C; ++c) {
