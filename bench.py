@@ -38,6 +38,7 @@ KERNEL_SOURCES = {
     "generic": ("paper_2407_04221_amd/csrc/k_generic.hip",),
     "wave": ("paper_2407_04221_amd/csrc/k_wave.hip",),
     "rows": ("paper_2407_04221_amd/csrc/k_rows.hip",),
+    "group": ("paper_2407_04221_amd/csrc/k_group.hip",),
     "lane16": ("paper_2407_04221_amd/csrc/lane16_kernel.hip",
                "paper_2407_04221_amd/csrc/lane16_jit.cpp",
                "paper_2407_04221_amd/csrc/codegen.h"),
@@ -286,7 +287,8 @@ def main():
                     help="timed repeats of the --steps region; the median is reported")
     ap.add_argument("--workload", default="c4")
     ap.add_argument("--variant", default="literal", choices=["literal", "planted", "dense"])
-    ap.add_argument("--engine", default="auto", choices=["auto", "generic", "lane16", "wave", "rows"])
+    ap.add_argument("--engine", default="auto",
+                    choices=["auto", "generic", "lane16", "wave", "rows", "group"])
     ap.add_argument("--rule-mode", default="parallel", choices=["parallel", "sequential"])
     ap.add_argument("--limit", type=int, default=0,
                     help="rule application control: cap every loaded rule at K matches per step")

@@ -57,9 +57,11 @@ typedef enum {
 } av_status;
 
 /* Kernel family used by av_step / av_step_n.  AUTO picks lane16 when eligible; else, for
- * per-environment rule sets, wave when its LDS working set (C + 1 padded planes, one match
- * plane per rule, two vote accumulators per plane) fits in 64 KiB; else rows when eligible;
- * else wave when it fits; else generic. */
+ * per-environment rule sets, group when eligible, else wave when its LDS working set (C + 1
+ * padded planes, one match plane per rule, two vote accumulators per plane) fits in 64 KiB;
+ * else rows when eligible; else wave when it fits; else generic.  With rule application
+ * control (av_set_rule_control) a batch created with AUTO runs lane16, or wave when the control
+ * scratch fits its LDS, or generic. */
 typedef enum {
     AV_ENGINE_AUTO = 0,
     AV_ENGINE_GENERIC = 1,  /* any size within the limits below; maps staged in LDS */
@@ -69,7 +71,7 @@ typedef enum {
     AV_ENGINE_WAVE = 3,     /* one environment per workgroup, map rows in LDS; 4 to 64
                                groups of lanes (as many as the batch's size leaves room for)
                                match that many of its rules at once */
-    AV_ENGINE_ROWS = 4      /* one environment per 64-lane wave, map row y in lane y,
+    AV_ENGINE_ROWS = 4,     /* one environment per 64-lane wave, map row y in lane y,
                                planes in the workgroup's LDS; one lane per rule tests every
                                rule's rarest entries at once, so only rules that can match
                                are visited.  On maps above 32 rows, in parallel rule order,
@@ -79,6 +81,18 @@ typedef enum {
                                of H + 16 rows plus R + 4 match planes of H + 32 rows (4 bytes
                                per row for W <= 32, else 8), 36 bytes per rule and 96 more;
                                no rule application control */
+    AV_ENGINE_GROUP = 5     /* one environment per 64-lane wave, no barriers: 4 groups of 16
+                               lanes (maps of up to 16 rows) or 2 of 32 (up to 32 rows),
+                               lane y of each owning map row y, group g matching rules g,
+                               g + 4 (or g + 2), ...; every rule's first four input entries
+                               are tested in one round of LDS reads, and only rules that pass
+                               somewhere read the rest.  Needs parallel rule order, H, W <= 32,
+                               (max_rules + 4) x max_pat_h x max_pat_w <= 254, at most 8
+                               channels per lane group and, within 64 KiB of LDS, C + 2 planes
+                               and R + 4 match planes of Hq + max_pat_h - 1 rows (rounded up to
+                               4), 3 C rows of Hq, 8 words per rule plus 8, and C (R + 4)
+                               words, 4 bytes each (Hq = 16 or 32); no rule application
+                               control */
 } av_engine;
 
 /* Order in which the rules of one step are applied. */

@@ -19,8 +19,9 @@ LIB_PATH = os.path.join(HERE, "libautoverse.so")
 
 AV_OK, AV_EINVAL, AV_ENOMEM, AV_EDEVICE, AV_ESTATE = 0, 1, 2, 3, 4
 AV_ENGINE_AUTO, AV_ENGINE_GENERIC, AV_ENGINE_LANE16, AV_ENGINE_WAVE, AV_ENGINE_ROWS = 0, 1, 2, 3, 4
+AV_ENGINE_GROUP = 5
 ENGINES = {"auto": AV_ENGINE_AUTO, "generic": AV_ENGINE_GENERIC, "lane16": AV_ENGINE_LANE16,
-           "wave": AV_ENGINE_WAVE, "rows": AV_ENGINE_ROWS}
+           "wave": AV_ENGINE_WAVE, "rows": AV_ENGINE_ROWS, "group": AV_ENGINE_GROUP}
 ENGINE_NAMES = {v: k for k, v in ENGINES.items()}
 AV_RULES_PARALLEL, AV_RULES_SEQUENTIAL = 0, 1
 RULE_MODES = {"parallel": AV_RULES_PARALLEL, "sequential": AV_RULES_SEQUENTIAL}

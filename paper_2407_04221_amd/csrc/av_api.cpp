@@ -189,6 +189,9 @@ void compile_generic(const std::vector<std::vector<HostRule>> &sets, int C, bool
                         if (k) rvote[s].push_back(pack_vote(c, i, j, k > 0));
                     }
             h.vote_cnt = int(rvote[s].size()) - h.vote_off;
+            h.pad = 0;                    // bit c: the rule casts a rule-major vote on channel c
+            for (int e = h.vote_off; e < int(rvote[s].size()); ++e)
+                if ((rvote[s][e] & 255u) < 32u) h.pad |= int32_t(1u << (rvote[s][e] & 255u));
             if (hr.reward != 0) p.any_reward = 1;
             std::stable_sort(ents.begin(), ents.end(),
                              [](auto &a, auto &b) { return a.first < b.first; });
@@ -315,7 +318,7 @@ av_status step_prefix(av_batch_t b, int n, const uint8_t *actions, float *reward
     a.B = n; a.H = c.height; a.W = c.width; a.C = c.channels;
     a.L = c.max_episode_steps; a.per_env = 0; a.k = 1;
     a.sequential = c.rule_mode == AV_RULES_SEQUENTIAL;
-    a.row_bytes = b->row_bytes;
+    a.row_bytes = b->row_bytes; a.max_pat_h = c.max_pat_h;
     a.state = b->d_state; a.init = b->d_init; a.t = b->d_t; a.nctr = b->d_n;
     a.actions = actions; a.rewards = rewards; a.done = done;
     a.prog = b->dprog;
@@ -328,6 +331,8 @@ av_status step_prefix(av_batch_t b, int n, const uint8_t *actions, float *reward
         AV_HIP(launch_rows_step(a, b->d_rows, b->rprog.set_words, b->rprog.rules, b->stream));
     else if (b->engine == AV_ENGINE_WAVE)
         AV_HIP(launch_wave_step(a, b->stream));
+    else if (b->engine == AV_ENGINE_GROUP)
+        AV_HIP(launch_group_step(a, b->stream));
     else
         AV_HIP(launch_generic_step(a, b->envs_per_block, b->stream));
     return AV_OK;
@@ -360,7 +365,7 @@ av_status av_create_batch(const av_config *cfg, av_batch_t *out) {
     if (c.max_episode_steps < 0) return fail(AV_EINVAL, "max_episode_steps must be >= 0");
     if (c.rule_mode != AV_RULES_PARALLEL && c.rule_mode != AV_RULES_SEQUENTIAL)
         return fail(AV_EINVAL, "unknown rule_mode %d", c.rule_mode);
-    if (c.engine < AV_ENGINE_AUTO || c.engine > AV_ENGINE_ROWS)
+    if (c.engine < AV_ENGINE_AUTO || c.engine > AV_ENGINE_GROUP)
         return fail(AV_EINVAL, "unknown engine %d", c.engine);
     const size_t env_lds = generic_env_lds_bytes(c.height, c.width, c.channels,
                                                  c.max_rules + kMoveRules);
@@ -376,6 +381,13 @@ av_status av_create_batch(const av_config *cfg, av_batch_t *out) {
     if (c.engine == AV_ENGINE_WAVE && !wave_ok)
         return fail(AV_EINVAL, "the wave engine needs %zu bytes of LDS (limit %d)", wave_lds,
                     kLdsBudget);
+    const bool group_ok = c.rule_mode == AV_RULES_PARALLEL &&
+                          group_eligible(c.height, c.width, c.channels, c.max_rules + kMoveRules,
+                                         c.max_pat_h, c.max_pat_w);
+    if (c.engine == AV_ENGINE_GROUP && !group_ok)
+        return fail(AV_EINVAL, "the group engine needs parallel rule order, H, W <= 32, "
+                    "(max_rules + 4) x max_pat_h x max_pat_w <= 254 and a working set within "
+                    "64 KiB of LDS");
     const bool rows_ok = rows_eligible(c.height, c.width, c.channels, c.max_rules + kMoveRules);
     if (c.engine == AV_ENGINE_ROWS && !rows_ok)
         return fail(AV_EINVAL, "the rows engine needs at most 60 rules and %zu bytes of LDS (limit %d)",
@@ -396,10 +408,13 @@ av_status av_create_batch(const av_config *cfg, av_batch_t *out) {
     b->envs_per_block = std::max(1, std::min(256 / c.height, int(kLdsBudget / env_lds)));
     if (c.engine != AV_ENGINE_AUTO) b->engine = c.engine;
     else if (lane16_ok) b->engine = AV_ENGINE_LANE16;
-    // measured on MI355X: per-environment rule sets run faster on the wave engine (its rule
-    // groups match many rules of a crowded environment at once: c3 literal, c2 with rules
-    // that fire; c2 literal is within 3 % of rows), shared sets the lane16 engine cannot
-    // take on rows (c5: 3.2 against 7.7 us per step)
+    // measured on MI355X: per-environment rule sets in parallel order run fastest on the group
+    // engine (16 x 16, 8 rules: 1.5 / 5.0 / 26 us per step with literal / planted / dense
+    // rules against the wave engine's 2.7 / 4.5 / 69; 32 x 32, 16 rules: 11.8 / 24.7 / 113
+    // against 17.6 / 31.0 / 228), otherwise on the wave engine (its rule groups match many
+    // rules of a crowded environment at once); shared sets the lane16 engine cannot take run
+    // on rows (64 x 64, 32 rules: 3.2 against the wave engine's 7.7 us per step)
+    else if (c.per_env_rules && group_ok) b->engine = AV_ENGINE_GROUP;
     else if (c.per_env_rules && wave_ok) b->engine = AV_ENGINE_WAVE;
     else if (rows_ok) b->engine = AV_ENGINE_ROWS;
     else b->engine = wave_ok ? AV_ENGINE_WAVE : AV_ENGINE_GENERIC;
@@ -535,17 +550,19 @@ av_status av_set_rule_control(av_batch_t b, const int32_t *limit, const uint8_t 
     const bool random = order == AV_SITES_RANDOM;
     // control compiles into the lane16 program; the wave engine runs it when its scratch fits
     // in LDS; otherwise it runs on the generic engine
-    // (a rows batch created with AV_ENGINE_AUTO switches like a wave batch; an explicit rows
-    // batch has no control)
+    // (a rows or group batch created with AV_ENGINE_AUTO switches like a wave batch; an
+    // explicit rows or group batch has no control)
     const bool on_lane16 = b->plain_engine == AV_ENGINE_LANE16;
     const bool wave_like = b->plain_engine == AV_ENGINE_WAVE ||
-                           (b->plain_engine == AV_ENGINE_ROWS && c.engine == AV_ENGINE_AUTO);
+                           ((b->plain_engine == AV_ENGINE_ROWS ||
+                             b->plain_engine == AV_ENGINE_GROUP) && c.engine == AV_ENGINE_AUTO);
     const bool on_wave = wave_like &&
                          wave_lds_bytes(c.height, c.width, c.channels, R + kMoveRules, true,
                                         random) <= size_t(kLdsBudget);
-    if (active && c.engine == AV_ENGINE_ROWS)
-        return fail(AV_EINVAL, "the rows engine has no rule application control; create the "
-                    "batch with AV_ENGINE_AUTO, AV_ENGINE_WAVE or AV_ENGINE_GENERIC");
+    if (active && (c.engine == AV_ENGINE_ROWS || c.engine == AV_ENGINE_GROUP))
+        return fail(AV_EINVAL, "the %s engine has no rule application control; create the "
+                    "batch with AV_ENGINE_AUTO, AV_ENGINE_WAVE or AV_ENGINE_GENERIC",
+                    c.engine == AV_ENGINE_ROWS ? "rows" : "group");
     if (active && !on_lane16 && !on_wave && c.engine != AV_ENGINE_AUTO &&
         c.engine != AV_ENGINE_GENERIC)
         return fail(AV_EINVAL, "rule application control does not fit this wave batch's LDS; "
@@ -626,7 +643,7 @@ static av_status step_k(av_batch_t b, int32_t k, const uint8_t *actions, float *
     a.B = c.num_envs; a.H = c.height; a.W = c.width; a.C = c.channels;
     a.L = c.max_episode_steps; a.per_env = c.per_env_rules; a.k = k;
     a.sequential = c.rule_mode == AV_RULES_SEQUENTIAL;
-    a.row_bytes = b->row_bytes;
+    a.row_bytes = b->row_bytes; a.max_pat_h = c.max_pat_h;
     a.state = b->d_state; a.init = b->d_init; a.t = b->d_t; a.nctr = b->d_n;
     a.actions = actions; a.rewards = rewards; a.done = done;
     a.prog = b->dprog;
@@ -647,6 +664,8 @@ static av_status step_k(av_batch_t b, int32_t k, const uint8_t *actions, float *
         AV_HIP(launch_lane16_step(a, b->lane16_ctl ? b->dlprog_ctl : b->dlprog, b->stream));
     } else if (b->engine == AV_ENGINE_ROWS) {
         AV_HIP(launch_rows_step(a, b->d_rows, b->rprog.set_words, b->rprog.rules, b->stream));
+    } else if (b->engine == AV_ENGINE_GROUP) {
+        AV_HIP(launch_group_step(a, b->stream));
     } else if (b->engine == AV_ENGINE_WAVE) {
         AV_HIP(launch_wave_step(a, b->stream));
     } else {

@@ -40,7 +40,7 @@ struct RuleHdr {
     int32_t match_cnt;
     int32_t vote_off;     // into the set's rule-major vote entries
     int32_t vote_cnt;
-    int32_t pad;
+    int32_t pad;          // bit c: some rule-major vote of the rule is on channel c (c < 32)
 };
 
 struct VoteList {
@@ -117,6 +117,7 @@ struct StepArgs {
     int32_t sequential;              // rules applied one after another (else in parallel)
     int32_t k;                       // steps in this launch
     int32_t row_bytes;
+    int32_t max_pat_h = 1;           // largest pattern rows a loaded rule may have
     void *state;                     // [C][B][H] rows
     const void *init;                // [C][B][H] rows
     int32_t *t;                      // [B] step counters
@@ -247,6 +248,11 @@ size_t rows_lds_bytes(int H, int W, int C, int rules_per_set);
 bool rows_eligible(int H, int W, int C, int rules_per_set);
 hipError_t launch_rows_step(const StepArgs &a, const uint32_t *words, int set_words, int rules,
                             hipStream_t s);
+
+// The group engine (k_group.hip): one environment per wave, its rules dealt to 2 or 4 groups
+// of lanes; parallel rule order, no rule application control.
+bool group_eligible(int H, int W, int C, int rules_per_set, int max_pat_h, int max_pat_w);
+hipError_t launch_group_step(const StepArgs &a, hipStream_t s);
 
 // Wave slots of the current device (8 waves per SIMD, 4 SIMDs per CU; 0 if it cannot be
 // asked): the most waves resident at once.

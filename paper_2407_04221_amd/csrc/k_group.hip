@@ -1,0 +1,553 @@
+// group engine: one environment per wave, its rules dealt to groups of lanes.
+//
+// The wave's 64 lanes form G = 64 / Hq groups of Hq lanes (Hq = 16 for maps of up to 16 rows,
+// 32 for up to 32); lane y of every group owns map row y (a 32-bit word, bit x = column x), and
+// group g matches rules g, g + G, g + 2G, ...  One workgroup is one wave, so a step needs no
+// barrier: the wave's LDS operations take effect in the order it issues them.
+//
+// The four built-in moves are computed in registers from the lanes' own rows of the player,
+// wall and force planes and the rows next to them (DPP row shifts within 16-lane groups,
+// ds_bpermute within 32-lane groups).  Each loaded rule's first four entries of its
+// rarest-first input list sit in a probe table that a step reads together with the player and
+// wall rows, so the probe of every loaded rule is one more round of LDS reads with no branch
+// between the rules; only rules that pass it somewhere read the rest of their entries, and only
+// channels that received votes are rewritten.
+//
+// LDS (32-bit rows):
+//   P    [C+2][PR]     the map, the force plane (channel C) and a zero plane (an entry that
+//                      always passes reads it); PR = Hq + ph - 1 rounded up to 4 rows (ph: the
+//                      largest pattern's rows), so a lane reads row y + i of any pattern entry
+//                      without a bounds test (rows H .. PR - 1 stay zero)
+//   M    [R+4][PR]     match planes of the rules that fired, row y at ph - 1 + y: the zero rows
+//                      above let a vote read match row y - i without a test
+//   PL, MI [C][Hq]     per stored channel, the OR of the +1 and of the -1 votes
+//   I0   [C][Hq]       the initial rows, for resets
+//   PT   [R+5][8]      probe table: per loaded rule its first four input entries and its
+//                      anchor rows and columns (row R + 4: zeros, read by
+//                      groups with fewer rules than others)
+//   RS   [C][R+4]      per channel and rule, the range of the rule's votes in the channel's
+//                      vote list (for exact recounts)
+//   program            (when it fits, see the launcher) the environment's rule headers, input
+//                      entries, rule-major votes and channel-major vote lists
+//
+// Per step (paper Sec. 2.1, Sec. 2.1.1, Sec. 2.2.1):
+//   force  F[y] = the player row moved one cell toward the action (group 0 writes it);
+//   moves  right P & (F >> 1) & ~(W >> 1), left F & ~W & (P >> 1), down P & F' & ~W', up
+//          F & ~W & P' (primes: the next row); their votes on the player plane are OR-ed in
+//          registers (-1 on the source cell, +1 on the target);
+//   match  per loaded rule, AND over its specified entries of plane row y + i shifted right by j,
+//          complemented for must-be-0, within the valid-anchor mask; a group leaves a rule as
+//          soon as no lane of the group has an anchor left;
+//   votes  a rule that fired stores its match plane and ORs match row y - i, shifted left by
+//          j, into the plus or minus row of each nonzero K_O = O - I entry's channel;
+//   write  group g rewrites channels g, g + G, ...: new = (old | plus) & ~minus where no cell
+//          got votes of both signs; a channel with such cells is recounted exactly with
+//          bit-sliced counters over every fired rule's votes: new = (old + #plus > #minus);
+//   end    done when no player bit is left or the counter reaches L; reward = sum over fired
+//          rules of reward * popcount; done environments return to their initial rows.
+// Parallel rule order only, without rule application control.
+#include <algorithm>
+
+#include "av_internal.h"
+
+namespace av {
+namespace {
+
+constexpr int kMaxRulesPerGroup = 16;   // rules a group holds in registers, at most
+constexpr int kMaxChanPerGroup = 8;     // stored channels a group writes, at most
+constexpr int kCountBits = 8;           // votes of one sign a cell-channel can get: <= 255
+                                        // (eligibility: rules x pattern cells <= 255)
+constexpr int kHdrWords = int(sizeof(RuleHdr) / 4);
+constexpr int kProbeEntries = 4;        // input entries of every rule tested in one round
+constexpr int kProbeWords = 8;          // probe table row: 4 entries, anchor word, pad
+
+__device__ inline uint32_t low_mask(int bits) { return bits >= 32 ? ~0u : ((1u << bits) - 1u); }
+
+// Does any lane of this lane's group hold a nonzero?
+template <int Hq>
+__device__ inline bool group_any(bool p, int lane) {
+    const unsigned long long bal = __builtin_amdgcn_ballot_w64(p);
+    if (Hq >= 64) return bal != 0ull;
+    const int base = lane & ~(Hq - 1);
+    return ((bal >> base) & ((1ull << Hq) - 1ull)) != 0ull;
+}
+
+// Row y + 1 (next) and y - 1 (prev) of the lane's group, 0 past the group's ends: a DPP row
+// shift within 16-lane groups, ds_bpermute within 32-lane groups.
+template <int Hq>
+__device__ inline uint32_t next_row(uint32_t v, int lane, int y) {
+    if (Hq == 16) return uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x101, 0xF, 0xF, true));
+    const uint32_t u = uint32_t(__builtin_amdgcn_ds_bpermute((lane + 1) << 2, int(v)));
+    return y + 1 < Hq ? u : 0u;
+}
+template <int Hq>
+__device__ inline uint32_t prev_row(uint32_t v, int lane, int y) {
+    if (Hq == 16) return uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x111, 0xF, 0xF, true));
+    const uint32_t u = uint32_t(__builtin_amdgcn_ds_bpermute((lane > 0 ? lane - 1 : 0) << 2, int(v)));
+    return y > 0 ? u : 0u;
+}
+
+// Add the one-bit plane t to the bit-sliced counter cnt; the carry ripples only as far as some
+// lane of the group still carries.
+template <int Hq>
+__device__ inline void count_add(uint32_t (&cnt)[kCountBits], uint32_t t, int lane) {
+#pragma unroll
+    for (int k = 0; k < kCountBits; ++k) {
+        if (!group_any<Hq>(t != 0u, lane)) break;
+        const uint32_t carry = cnt[k] & t;
+        cnt[k] ^= t;
+        t = carry;
+    }
+}
+
+// The exact write of channel c for this lane's row (needed only where some cell of the group
+// got votes of both signs): counts the votes on c of every rule in `fired` (the channel's vote
+// list `vl`, packed r | i << 8 | j << 16 | plus << 24 and ordered by rule; rule r's votes are
+// vl[rsc[r] & 0xFFFF .. rsc[r] >> 16)) with the old value as a plus vote, and
+// returns the cells where old + #plus > #minus, i.e. old + sum of votes >= 1.  Counts are
+// 4-bit planes per sign; only if some cell of the group reaches 16 votes of one sign are they
+// recounted with kCountBits-bit counters.
+template <int Hq>
+__device__ inline uint32_t exact_channel(uint32_t old, uint64_t fired, const uint32_t *vl,
+                                         const uint32_t *rsc, const uint32_t *M, int MS, int pad,
+                                         int y, bool row, int lane) {
+    uint32_t pc[4] = {row ? old : 0u, 0u, 0u, 0u}, nc[4] = {0u, 0u, 0u, 0u};
+    uint32_t ovf = 0u;
+    for (uint64_t fr = fired; fr; fr &= fr - 1) {
+        const int r = __builtin_ctzll(fr);
+        const uint32_t rs = rsc[r];
+        const int lo = int(rs & 0xFFFFu), hi = int(rs >> 16);
+        for (int ev = lo; ev < hi; ev += 4) {
+            uint32_t v[4], t[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) v[u] = vl[min(ev + u, hi - 1)];
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                t[u] = (row && ev + u < hi)
+                           ? M[r * MS + pad + y - int((v[u] >> 8) & 255u)] << ((v[u] >> 16) & 255u)
+                           : 0u;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const bool plus = (v[u] >> 24) & 1u;
+                uint32_t xp = plus ? t[u] : 0u, xn = plus ? 0u : t[u];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const uint32_t cp = pc[q] & xp, cn = nc[q] & xn;
+                    pc[q] ^= xp;
+                    nc[q] ^= xn;
+                    xp = cp;
+                    xn = cn;
+                }
+                ovf |= xp | xn;
+            }
+        }
+    }
+    if (!group_any<Hq>(ovf != 0u, lane)) {
+        uint32_t gt = 0u, eq = ~0u;
+#pragma unroll
+        for (int q = 3; q >= 0; --q) {
+            gt |= eq & pc[q] & ~nc[q];
+            eq &= ~(pc[q] ^ nc[q]);
+        }
+        return gt;
+    }
+    uint32_t pw[kCountBits], nw[kCountBits];
+#pragma unroll
+    for (int u = 0; u < kCountBits; ++u) pw[u] = nw[u] = 0u;
+    count_add<Hq>(pw, row ? old : 0u, lane);
+    for (uint64_t fr = fired; fr; fr &= fr - 1) {
+        const int r = __builtin_ctzll(fr);
+        const uint32_t rs = rsc[r];
+        for (int ev = int(rs & 0xFFFFu); ev < int(rs >> 16); ++ev) {
+            const uint32_t v = vl[ev];
+            const uint32_t t = row ? M[r * MS + pad + y - int((v >> 8) & 255u)] << ((v >> 16) & 255u)
+                                   : 0u;
+            const bool plus = (v >> 24) & 1u;
+            count_add<Hq>(pw, plus ? t : 0u, lane);
+            count_add<Hq>(nw, plus ? 0u : t, lane);
+        }
+    }
+    uint32_t gt = 0u, eq = ~0u;
+#pragma unroll
+    for (int u = kCountBits - 1; u >= 0; --u) {
+        gt |= eq & pw[u] & ~nw[u];
+        eq &= ~(pw[u] ^ nw[u]);
+    }
+    return gt;
+}
+
+// NR: rules a group holds (a bound on this launch's ceil(R / G)).
+template <int Hq, int NR>
+__global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, int prog_lds) {
+    constexpr int G = 64 / Hq;
+    constexpr int kChunk = 4;                 // entries or votes of a rule read in one round
+    extern __shared__ __align__(16) uint32_t lds[];
+    const int lane = int(threadIdx.x), g = lane / Hq, y = lane % Hq;
+    const int b = int(blockIdx.x);
+    const int H = a.H, W = a.W, C = a.C, C1 = C + 1, Rt = a.prog.rules_per_set;
+    // pattern rows beyond a lane's row: plane rows y + i and match rows y - i, i <= PAD, are
+    // read without a bounds test; rows of 4 words keep the probe table 16-byte aligned
+    const int PAD = a.max_pat_h - 1;
+    const int PR = (Hq + PAD + 3) & ~3, MS = PR;
+    const int s = a.per_env ? b : 0;
+    const bool row = y < H;
+    const int ry = row ? y : 0;
+    const uint32_t wmask = low_mask(W);
+
+    uint32_t *P = lds;                             // [C1 + 1][PR]
+    uint32_t *M = P + (C1 + 1) * PR;               // [Rt][MS]
+    uint32_t *PL = M + Rt * MS;                    // [C][Hq]
+    uint32_t *MI = PL + C * Hq;                    // [C][Hq]
+    uint32_t *I0 = MI + C * Hq;                    // [C][Hq] initial rows
+    uint32_t *PT = I0 + C * Hq;                    // [Rt + 1][kProbeWords] probe table
+    uint32_t *RS = PT + (Rt + 1) * kProbeWords;    // [C][Rt] rule ranges of channel lists
+    uint32_t *lprog = RS + C * Rt;                 // program copy (prog_lds)
+
+    const uint32_t *ghdr = reinterpret_cast<const uint32_t *>(a.prog.hdr + size_t(s) * Rt);
+    const uint32_t *gment = a.prog.match + size_t(s) * a.prog.match_stride;
+    const uint32_t *gvent = a.prog.rvote + size_t(s) * a.prog.rvote_stride;
+    const uint32_t *gvl = reinterpret_cast<const uint32_t *>(a.prog.votes + size_t(s) * C1);
+    const uint32_t *gvote = a.prog.vote + size_t(s) * a.prog.vote_stride;
+    const int hdr_words = Rt * kHdrWords;
+    const uint32_t *hdrw = ghdr, *ment = gment, *vent = gvent, *vlw = gvl, *vote = gvote;
+    if (prog_lds) {
+        uint32_t *ph = lprog, *pm = ph + hdr_words, *pv = pm + a.prog.match_stride;
+        uint32_t *pl = pv + a.prog.rvote_stride, *pc = pl + 2 * C1;
+        for (int w = lane; w < hdr_words; w += 64) ph[w] = ghdr[w];
+        for (int w = lane; w < a.prog.match_stride; w += 64) pm[w] = gment[w];
+        for (int w = lane; w < a.prog.rvote_stride; w += 64) pv[w] = gvent[w];
+        for (int w = lane; w < 2 * C1; w += 64) pl[w] = gvl[w];
+        for (int w = lane; w < a.prog.vote_stride; w += 64) pc[w] = gvote[w];
+        hdrw = ph;
+        ment = pm;
+        vent = pv;
+        vlw = pl;
+        vote = pc;
+    }
+    {
+        const int words = (C1 + 1) * PR + Rt * MS + 3 * C * Hq + (Rt + 1) * kProbeWords + C * Rt;
+        for (int w = lane; w < words; w += 64) lds[w] = 0u;
+    }
+
+    // rule ranges of the channel vote lists (each list is ordered by rule): RS[c][r] = first |
+    // end << 16 of rule r's votes on channel c, 0 when it has none
+    for (int c = 0; c < C; ++c) {
+        const uint32_t *vc = vote + int(vlw[2 * c]);
+        const int n = int(vlw[2 * c + 1]);
+        for (int k = lane; k < n; k += 64) {
+            const uint32_t r = vc[k] & 255u;
+            uint32_t w = 0u;
+            if (k == 0 || (vc[k - 1] & 255u) != r) w |= uint32_t(k);
+            if (k == n - 1 || (vc[k + 1] & 255u) != r) w |= uint32_t(k + 1) << 16;
+            atomicOr(RS + c * Rt + int(r), w);
+        }
+    }
+    // probe table: per loaded rule, its first four input entries (a missing entry is one that
+    // always passes: must-be-0 on the zero plane) and its anchor rows and columns
+    const int nl = Rt - kMoveRules;               // loaded rules
+    const int nr = (nl - g + G - 1) / G;          // this group's loaded rule count
+    for (int r = kMoveRules + lane; r < Rt; r += 64) {
+        const uint32_t *hw = ghdr + r * kHdrWords;
+        const int n = int(hw[0]), m = int(hw[1]);
+        const int moff = int(hw[3]), mcnt = int(hw[4]);
+        const uint32_t pass = uint32_t(C1);       // plane C + 1 is all zeros
+        uint32_t *pt = PT + r * kProbeWords;
+#pragma unroll
+        for (int e = 0; e < kProbeEntries; ++e) pt[e] = e < mcnt ? gment[moff + e] : pass;
+        // anchors: columns 0 .. W - m (the low W - m + 1 bits: ~0 >> (32 - (W - m + 1))) of
+        // rows 0 .. H - n
+        const int cols = W - m + 1, rows = H - n + 1;
+        pt[4] = (cols >= 1 && rows >= 1) ? uint32_t(32 - cols) | (uint32_t(rows) << 8) : 0u;
+        pt[5] = pt[6] = pt[7] = 0u;
+    }
+#pragma unroll
+    for (int q = 0; q < kMaxChanPerGroup; ++q) {
+        const int c = g + G * q;
+        if (c < C && row) {
+            const size_t at = (size_t(c) * a.B + b) * H + y;
+            P[c * PR + y] = a.row_bytes == 2 ? uint32_t(static_cast<const uint16_t *>(a.state)[at])
+                                             : static_cast<const uint32_t *>(a.state)[at];
+            I0[c * Hq + y] = a.row_bytes == 2 ? uint32_t(static_cast<const uint16_t *>(a.init)[at])
+                                              : static_cast<const uint32_t *>(a.init)[at];
+        }
+    }
+    __syncthreads();   // (one wave: orders the set-up's LDS writes before the step's reads)
+    int t_env = a.t[b];
+    const uint64_t nbase = a.nctr[b];
+
+    // entry e (packed c | i << 8 | j << 16 | want << 24) at this lane's row: 1 where the plane
+    // row y + i, moved right by j, holds the wanted value
+    auto entry = [&](uint32_t e) {
+        const uint32_t v = P[int(e & 255u) * PR + ry + int((e >> 8) & 255u)] >> ((e >> 16) & 255u);
+        return ((e >> 24) & 1u) ? v : ~v;
+    };
+
+    uint32_t ablk = 0u;     // lane l: action of step k0 + l of the current block of 64
+    float rbuf = 0.f;       // lane l: reward of step k0 + l
+    uint32_t dbuf = 0u;     // lane l: done flag of step k0 + l
+    uint32_t *const F = P + C * PR;
+    const uint32_t *const P2 = P + kChPlayer * PR;
+
+    const uint32_t cm1 = low_mask(W - 1);         // anchors of a 1 x 2 pattern
+    const uint32_t vrow2 = (y + 2 <= H) ? wmask : 0u;   // rows of a 2 x 1 pattern's anchors
+    const int pown = kChPlayer % G;               // the group that writes the player plane
+    for (int k = 0; k < a.k; ++k) {
+        const int kb = k & 63;
+        if (kb == 0) ablk = (k + lane < a.k) ? uint32_t(a.actions[size_t(k + lane) * a.B + b]) : 0u;
+        const int act = __builtin_amdgcn_readlane(int(ablk), kb);
+        // the lane's rows of the player and wall planes (0 past the map), and the probe table
+        // rows of the group's rules (they do not depend on the map: read with the rows)
+        const uint32_t Py = row ? P2[y] : 0u, Wy = row ? P[kChWall * PR + y] : 0u;
+        uint4 pe[NR];
+        uint32_t pv[NR];
+#pragma unroll
+        for (int kr = 0; kr < NR; ++kr) {
+            const int r = kr < nr ? kMoveRules + g + G * kr : kMoveRules;
+            pe[kr] = *reinterpret_cast<const uint4 *>(PT + r * kProbeWords);
+            pv[kr] = PT[r * kProbeWords + 4];
+        }
+        // the rows next to them and the force row
+        const uint32_t Pn = next_row<Hq>(Py, lane, y), Wn = next_row<Hq>(Wy, lane, y);
+        const uint32_t Pp = prev_row<Hq>(Py, lane, y);
+        const uint32_t Fy = act == 1 ? Pn : act == 3 ? Pp : act == 2 ? ((Py << 1) & wmask)
+                          : act == 4 ? (Py >> 1) : 0u;
+        if (g == 0 && row) F[y] = Fy;
+        const uint32_t Fn = next_row<Hq>(Fy, lane, y);
+        // the four moves (rules 0..3: right, left, down, up) and their votes on the player
+        // plane; group 0 stores their match rows for an exact recount
+        const uint32_t m0 = Py & (Fy >> 1) & ~(Wy >> 1) & cm1;
+        const uint32_t m1 = Fy & ~Wy & (Py >> 1) & cm1;
+        const uint32_t m2 = Py & Fn & ~Wn & vrow2;
+        const uint32_t m3 = Fy & ~Wy & Pn & vrow2;
+        const uint32_t mplus = (m0 << 1) | m1 | prev_row<Hq>(m2, lane, y) | m3;
+        const uint32_t mminus = m0 | (m1 << 1) | m2 | prev_row<Hq>(m3, lane, y);
+        if (g == 0) {
+            M[0 * MS + PAD + y] = m0;
+            M[1 * MS + PAD + y] = m1;
+            M[2 * MS + PAD + y] = m2;
+            M[3 * MS + PAD + y] = m3;
+        }
+        uint64_t fired = (__builtin_amdgcn_ballot_w64(m0 != 0u) ? 1ull : 0ull) |
+                         (__builtin_amdgcn_ballot_w64(m1 != 0u) ? 2ull : 0ull) |
+                         (__builtin_amdgcn_ballot_w64(m2 != 0u) ? 4ull : 0ull) |
+                         (__builtin_amdgcn_ballot_w64(m3 != 0u) ? 8ull : 0ull);
+
+        // probe: every loaded rule of the group with its first four entries, all reads at once
+        // (no branch between the rules); the results go to the rules' match rows, and a
+        // wave-uniform mask of the rule indices kr whose probe passed in some group
+        uint32_t mk[NR];
+#pragma unroll
+        for (int kr = 0; kr < NR; ++kr) {
+            const uint32_t vm = (kr < nr && y < int(pv[kr] >> 8)) ? ~0u >> (pv[kr] & 255u) : 0u;
+            mk[kr] = vm & entry(pe[kr].x) & entry(pe[kr].y) & entry(pe[kr].z) & entry(pe[kr].w);
+        }
+        uint32_t cand = 0u;
+#pragma unroll
+        for (int kr = 0; kr < NR; ++kr) {
+            if (kr < nr) M[(kMoveRules + g + G * kr) * MS + PAD + y] = mk[kr];
+            cand |= __builtin_amdgcn_ballot_w64(mk[kr] != 0u) ? 1u << kr : 0u;
+        }
+
+        // loaded rules whose probe passed somewhere in their group: the remaining entries,
+        // then the rule's reward and votes
+        int rsum = 0;
+        uint32_t voted = 0u;                      // bit c: a loaded rule voted on channel c
+        for (uint32_t cl = cand; cl; cl &= cl - 1u) {
+            const int kr = __builtin_ctz(cl);
+            const int r = kMoveRules + g + G * kr;
+            uint32_t m = 0u;                      // mk[kr] (kr is wave-uniform)
+#pragma unroll
+            for (int kk = 0; kk < NR; ++kk) m = kk == kr ? mk[kk] : m;
+            if (kr < nr && group_any<Hq>(m != 0u, lane)) {
+                const uint32_t *hw = hdrw + r * kHdrWords;
+                const uint32_t *en = ment + int(hw[3]);
+                const int cnt = int(hw[4]);
+                // the rest of the entries kChunk at a time, the next chunk read while the
+                // current one's plane rows are; indices past the last entry repeat it (AND is
+                // idempotent), which keeps every read inside the rule's list
+                int e = kProbeEntries;
+                const int last = cnt - 1;
+                uint32_t x[kChunk];
+#pragma unroll
+                for (int u = 0; u < kChunk; ++u) x[u] = en[min(e + u, last)];
+                while (e < cnt && group_any<Hq>(m != 0u, lane)) {
+                    uint32_t cur[kChunk];
+#pragma unroll
+                    for (int u = 0; u < kChunk; ++u) cur[u] = x[u];
+                    e += kChunk;
+                    if (e < cnt) {
+#pragma unroll
+                        for (int u = 0; u < kChunk; ++u) x[u] = en[min(e + u, last)];
+                    }
+#pragma unroll
+                    for (int u = 0; u < kChunk; ++u) m &= entry(cur[u]);
+                }
+                if (group_any<Hq>(m != 0u, lane)) {
+                    M[r * MS + PAD + y] = m;
+                    fired |= 1ull << r;
+                    voted |= hw[7];
+                    rsum += int(hw[2]) * __popc(m);
+                    // votes kChunk at a time, the next chunk read with the current one's match
+                    // rows (a repeated last vote ORs the same bits again)
+                    const uint32_t *ve = vent + int(hw[5]);
+                    const int vcnt = int(hw[6]), vlast = vcnt - 1;
+                    uint32_t v[kChunk];
+                    if (vcnt > 0) {
+#pragma unroll
+                        for (int u = 0; u < kChunk; ++u) v[u] = ve[min(u, vlast)];
+                    }
+                    for (int ev = 0; ev < vcnt; ev += kChunk) {
+                        uint32_t cv[kChunk], tv[kChunk];
+#pragma unroll
+                        for (int u = 0; u < kChunk; ++u) cv[u] = v[u];
+                        if (ev + kChunk < vcnt) {
+#pragma unroll
+                            for (int u = 0; u < kChunk; ++u) v[u] = ve[min(ev + kChunk + u, vlast)];
+                        }
+#pragma unroll
+                        for (int u = 0; u < kChunk; ++u)
+                            tv[u] = M[r * MS + PAD + y - int((cv[u] >> 8) & 255u)] << ((cv[u] >> 16) & 255u);
+#pragma unroll
+                        for (int u = 0; u < kChunk; ++u)
+                            if (row && tv[u])
+                                atomicOr(((cv[u] >> 24) & 1u ? PL : MI) + int(cv[u] & 255u) * Hq + y, tv[u]);
+                    }
+                }
+            }
+        }
+        // every rule that fired anywhere in the wave and every channel a loaded rule voted on
+        // (the groups' masks OR-ed)
+        uint64_t fired_all = 0;
+        uint32_t lvoted = 0u;                     // channels the loaded rules voted on
+#pragma unroll
+        for (int gg = 0; gg < G; ++gg) {
+            const uint32_t lo = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(fired)), gg * Hq));
+            const uint32_t hi = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(fired >> 32)), gg * Hq));
+            fired_all |= uint64_t(lo) | (uint64_t(hi) << 32);
+            lvoted |= uint32_t(__builtin_amdgcn_readlane(int(voted), gg * Hq));
+        }
+        const uint32_t voted_all = lvoted | ((fired_all & 15ull) ? 1u << kChPlayer : 0u);
+
+        // new rows of the channels that received votes: group g rewrites channels g, g + G, ...
+        // (the moves' votes on the player plane are in registers, the loaded rules' in LDS)
+        bool pl_any = g == pown && row && Py != 0u;   // a player bit after the write
+        if (voted_all) {
+#pragma unroll 1
+            for (int c = g; c < C; c += G) {
+                if (!((voted_all >> c) & 1u)) continue;
+                const uint32_t old = c == kChPlayer ? Py : P[c * PR + ry];
+                const bool lv = (lvoted >> c) & 1u;
+                uint32_t pl = lv ? PL[c * Hq + y] : 0u, mi = lv ? MI[c * Hq + y] : 0u;
+                if (c == kChPlayer) {
+                    pl |= mplus;
+                    mi |= mminus;
+                }
+                uint32_t nw = (old | pl) & ~mi;
+                if (group_any<Hq>((pl & mi) != 0u, lane))
+                    nw = exact_channel<Hq>(old, fired_all, vote + int(vlw[2 * c]),
+                                           RS + c * Rt, M, MS, PAD, y, row, lane);
+                if (row) P[c * PR + y] = nw;
+                if (c == kChPlayer) pl_any = row && nw != 0u;
+                if (lv) {
+                    PL[c * Hq + y] = 0u;
+                    MI[c * Hq + y] = 0u;
+                }
+            }
+        }
+
+        // reward: the lanes' sums over the wave
+        if (__builtin_amdgcn_ballot_w64(rsum != 0)) {
+#pragma unroll
+            for (int off = 32; off > 0; off >>= 1) rsum += __shfl_xor(rsum, off);
+        }
+        // episode end: a player bit left anywhere (the writing group's lanes hold the rows)
+        const bool anyp = __builtin_amdgcn_ballot_w64(pl_any) != 0ull;
+        t_env += 1;
+        const bool d = !anyp || (a.L > 0 && t_env == a.L);
+        if (d) {                                  // back to the initial rows
+            t_env = 0;
+            if (row) {
+#pragma unroll 1
+                for (int c = g; c < C; c += G) P[c * PR + y] = I0[c * Hq + y];
+            }
+        }
+        if (lane == kb) {
+            rbuf = float(rsum);
+            dbuf = d ? 1u : 0u;
+        }
+        if (kb == 63 || k == a.k - 1) {
+            const int k0 = k - kb;
+            if (lane <= kb) {
+                a.rewards[size_t(k0 + lane) * a.B + b] = rbuf;
+                a.done[size_t(k0 + lane) * a.B + b] = uint8_t(dbuf);
+            }
+        }
+    }
+
+#pragma unroll
+    for (int q = 0; q < kMaxChanPerGroup; ++q) {
+        const int c = g + G * q;
+        if (c < C && row) {
+            const size_t at = (size_t(c) * a.B + b) * H + y;
+            if (a.row_bytes == 2) static_cast<uint16_t *>(a.state)[at] = uint16_t(P[c * PR + y]);
+            else static_cast<uint32_t *>(a.state)[at] = P[c * PR + y];
+        }
+    }
+    if (lane == 0) {
+        a.t[b] = t_env;
+        a.nctr[b] = nbase + uint64_t(a.k);
+    }
+}
+
+}  // namespace
+
+int group_lanes(int H) { return H <= 16 ? 16 : 32; }
+
+size_t group_lds_bytes(int H, int C, int rules_per_set, int max_pat_h) {
+    const int Hq = group_lanes(H), PR = (Hq + max_pat_h - 1 + 3) & ~3;
+    return sizeof(uint32_t) * (size_t(C + 2) * PR + size_t(rules_per_set) * PR +
+                               size_t(3) * C * Hq + size_t(rules_per_set + 1) * kProbeWords +
+                               size_t(C) * rules_per_set);
+}
+
+bool group_eligible(int H, int W, int C, int rules_per_set, int max_pat_h, int max_pat_w) {
+    if (H > 32 || W > 32) return false;
+    // every vote a cell-channel gets comes from a distinct (rule, pattern cell): the 8-bit
+    // counts of the exact write hold them (plus the old value) when there are at most 255
+    if (long(rules_per_set) * max_pat_h * max_pat_w > 254) return false;
+    const int G = 64 / group_lanes(H);
+    return rules_per_set <= kMaxRulesPerGroup * G && rules_per_set <= 64 &&
+           C <= kMaxChanPerGroup * G &&
+           group_lds_bytes(H, C, rules_per_set, max_pat_h) <= size_t(kLdsBudget);
+}
+
+namespace {
+template <int Hq>
+void launch_hq(const StepArgs &a, size_t lds, int prog_lds, hipStream_t s) {
+    constexpr int G = 64 / Hq;
+    const int nrmax = (a.prog.rules_per_set - kMoveRules + G - 1) / G;
+    if (nrmax <= 2) hipLaunchKernelGGL((group_step<Hq, 2>), dim3(a.B), dim3(64), lds, s, a, prog_lds);
+    else if (nrmax <= 4) hipLaunchKernelGGL((group_step<Hq, 4>), dim3(a.B), dim3(64), lds, s, a, prog_lds);
+    else if (nrmax <= 8) hipLaunchKernelGGL((group_step<Hq, 8>), dim3(a.B), dim3(64), lds, s, a, prog_lds);
+    else if (nrmax <= 12) hipLaunchKernelGGL((group_step<Hq, 12>), dim3(a.B), dim3(64), lds, s, a, prog_lds);
+    else hipLaunchKernelGGL((group_step<Hq, 16>), dim3(a.B), dim3(64), lds, s, a, prog_lds);
+}
+}  // namespace
+
+hipError_t launch_group_step(const StepArgs &a, hipStream_t s) {
+    const size_t base = group_lds_bytes(a.H, a.C, a.prog.rules_per_set, a.max_pat_h);
+    const size_t prog = sizeof(uint32_t) * (size_t(a.prog.rules_per_set) * kHdrWords +
+                                            a.prog.match_stride + a.prog.rvote_stride +
+                                            2 * (a.C + 1) + a.prog.vote_stride);
+    // the program goes to LDS when it fits and leaves room for as many waves per CU (160 KiB
+    // of LDS) as the batch can use, up to 16 (4 per SIMD)
+    const size_t need = size_t(std::min(16, (a.B + 255) / 256));
+    const int prog_lds = base + prog <= size_t(kLdsBudget) &&
+                         (base + prog) * need <= size_t(160) * 1024 ? 1 : 0;
+    const size_t lds = base + (prog_lds ? prog : 0);
+    if (group_lanes(a.H) == 16) launch_hq<16>(a, lds, prog_lds, s);
+    else launch_hq<32>(a, lds, prog_lds, s);
+    return hipGetLastError();
+}
+
+}  // namespace av

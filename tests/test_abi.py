@@ -64,7 +64,11 @@ def _cfg(**kw):
     dict(num_envs=0), dict(height=0), dict(width=65), dict(height=65), dict(channels=3),
     dict(channels=32), dict(max_rules=-1), dict(max_rules=253), dict(max_pat_h=0),
     dict(max_pat_w=17), dict(per_env_rules=2), dict(max_episode_steps=-1), dict(engine=9),
-    dict(engine=5), dict(engine=-1),
+    dict(engine=6), dict(engine=-1),
+    # the group engine: parallel rule order, maps of at most 32 x 32, (R + 4) x pattern cells
+    # <= 254
+    dict(engine=5, rule_mode=1), dict(engine=5, height=33, width=20),
+    dict(engine=5, max_rules=25), dict(engine=5, max_pat_h=16, max_pat_w=16, max_rules=1),
     # the rows engine takes at most 60 loaded rules and its LDS set within 64 KiB
     dict(engine=4, max_rules=61), dict(engine=4, height=64, width=64, channels=31, max_rules=60),
     # lane16 needs maps of at most 16 x 16 and one shared rule set

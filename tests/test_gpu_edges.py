@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 import oracle
-from gpu_util import first_mismatch, gpu_run, require_gpu, rows_ok, say
+from gpu_util import first_mismatch, gpu_run, group_ok, require_gpu, rows_ok, say
 from paper_2407_04221_amd import inputs
 
 pytestmark = pytest.mark.gpu
@@ -50,7 +50,7 @@ def engines(name):
     rowb, rt = (4 if wl.W <= 32 else 8), wl.R + 4
     if ((wl.C + 1) * (wl.H + 16) + rt * 80 + 2 * (wl.C + 1) * 64) * rowb + 4 * (rt + 2 + 192) <= 65536:
         out.append("wave")
-    return out + (["rows"] if rows_ok(wl) else [])
+    return out + (["rows"] if rows_ok(wl) else []) + (["group"] if group_ok(wl) else [])
 
 
 def check(wl, maps, rules, actions, engine):
@@ -96,7 +96,7 @@ def test_tall_maps_in_long_launches(name, variant):
     np.testing.assert_array_equal(final, want_m[-1])
 
 
-@pytest.mark.parametrize("engine", ["generic", "lane16", "wave", "rows"])
+@pytest.mark.parametrize("engine", ["generic", "lane16", "wave", "rows", "group"])
 def test_rules_with_no_specified_input(engine):
     """An all-don't-care input matches at every anchor (the paper's empty "no-op" rules,
     Sec. 2.2.1); with outputs it writes everywhere, with heavily overlapping votes."""
@@ -110,7 +110,7 @@ def test_rules_with_no_specified_input(engine):
     assert (r != 0).all()
 
 
-@pytest.mark.parametrize("engine", ["generic", "lane16", "wave", "rows"])
+@pytest.mark.parametrize("engine", ["generic", "lane16", "wave", "rows", "group"])
 def test_no_loaded_rules(engine):
     require_gpu()
     wl = W_("moves", 52, B=41, H=13, W=16, C=4, R=0, shapes=((1, 1),), T=30, L=0)
@@ -121,7 +121,7 @@ def test_no_loaded_rules(engine):
     check(wl, maps, empty, actions, engine)
 
 
-@pytest.mark.parametrize("engine", ["generic", "lane16", "wave", "rows"])
+@pytest.mark.parametrize("engine", ["generic", "lane16", "wave", "rows", "group"])
 def test_out_of_range_actions_are_no_ops(engine):
     require_gpu()
     wl = W_("acts", 53, B=24, H=8, W=8, C=4, R=2, shapes=((1, 2),), T=10)
@@ -149,4 +149,22 @@ def test_vote_counts_beyond_4096(engine):
     actions[:] = 0
     want_m, want_r, want_d = oracle.run(wl, maps, (shape, ip, op, rw), actions, nthreads=8)
     assert want_m[0][:, 3, 15:49, 15:49].all()      # the interior became (or stayed) goal
+    check(wl, maps, (shape, ip, op, rw), actions, engine)
+
+
+@pytest.mark.parametrize("rules_per_sign", [1, 2])
+@pytest.mark.parametrize("engine", ["group", "wave", "generic"])
+def test_overlapping_votes_of_both_signs(engine, rules_per_sign):
+    """All-don't-care 3 x 3 rules, half voting +1 and half -1 on the goal plane: a cell away
+    from the edges gets 9 votes of each sign per rule, so every cell needs an exact count;
+    with two rules per sign the counts reach 18, beyond 4-bit counters."""
+    require_gpu()
+    R = 2 * rules_per_sign
+    wl = W_("both", 58, B=7, H=12, W=15, C=5, R=R, shapes=((3, 3),), T=4, L=0)
+    maps, (shape, ip, op, rw), actions = inputs.make_all(wl, 0, "literal")
+    ip[:] = -1
+    op[:] = -1
+    op[:, :rules_per_sign, 3] = 1
+    op[:, rules_per_sign:, 3] = 0
+    rw[:] = 0
     check(wl, maps, (shape, ip, op, rw), actions, engine)

@@ -7,8 +7,8 @@ of lane words, random others) over every step.  Rewards and done flags are compa
 step; the sampled maps are compared after every launch.  The first launch is 37 steps long, so
 launch ends fall on steps 1000 k + 37: never on a multiple of the episode length (100), where
 an environment whose episode did not end early would just have been reset to its initial map.
-Every config x variant runs (15 pairs), on the engine AUTO picks for it (c3 at B = 4096 runs
-the wave engine with the group count of that size)."""
+Every config x variant runs (15 pairs), on the engine AUTO picks for it (the per-environment
+rule sets of c2 and c3 on the group engine, at the occupancy their full batch sizes set)."""
 import numpy as np
 import pytest
 
@@ -136,7 +136,7 @@ def test_full_size_bench_launches(name, variant):
     # properties of every environment, not just the sample
     r, d = got[0], got[1]
     assert d.max() <= 1 and np.array_equal(r, np.round(r))
-    expect = {"c1": "lane16", "c2": "wave", "c3": "wave", "c4": "lane16", "c5": "rows"}
+    expect = {"c1": "lane16", "c2": "group", "c3": "group", "c4": "lane16", "c5": "rows"}
     assert got[3] == expect[name]
 
 

@@ -20,7 +20,8 @@ pytestmark = pytest.mark.gpu
 
 # (workload, B, engine, control): control None, or the site order of a random cap/inhibition
 CASES = [("c4", 333, "lane16", None), ("c2", 70, "rows", None), ("c3", 9, "wave", None),
-         ("c5", 3, "rows", None), ("c2", 21, "generic", None),
+         ("c5", 3, "rows", None), ("c2", 21, "generic", None), ("c2", 70, "group", None),
+         ("c3", 9, "group", None),
          ("c4", 333, "lane16", "random"), ("c4", 77, "lane16", "rowmajor"),
          ("c2", 37, "wave", "random"), ("c3", 9, "generic", "random"),
          ("c5", 2, "generic", "random")]

@@ -7,7 +7,7 @@ import numpy as np
 import pytest
 
 import oracle
-from gpu_util import first_mismatch, gpu_run, require_gpu, say
+from gpu_util import first_mismatch, gpu_run, group_ok, require_gpu, say
 from paper_2407_04221_amd import inputs
 
 pytestmark = pytest.mark.gpu
@@ -22,12 +22,14 @@ def _case_ids():
 
 @pytest.mark.parametrize("variant", inputs.VARIANTS)
 @pytest.mark.parametrize("seed", [0, 1])
-@pytest.mark.parametrize("engine", ["generic", "wave", "rows", "auto"])
+@pytest.mark.parametrize("engine", ["generic", "wave", "rows", "group", "auto"])
 @pytest.mark.parametrize("case", CASES, ids=_case_ids())
 def test_step_matches_oracle(case, engine, seed, variant):
     require_gpu()
     name, B, T = case
     wl = inputs.WORKLOADS[name].with_(B=B, T=T, L=25)
+    if engine == "group" and not group_ok(wl):
+        pytest.skip("not eligible for the group engine")
     say(f"[parity] {name} B={B} T={T} engine={engine} seed={seed} variant={variant}")
     maps, rules, actions = inputs.make_all(wl, seed, variant)
     want_m, want_r, want_d = oracle.run(wl, maps, rules, actions, nthreads=8)
@@ -48,12 +50,14 @@ STEP_N_CASES = [("c1", 1, 150), ("c2", 203, 150), ("c3", 37, 80), ("c4", 333, 16
 
 @pytest.mark.parametrize("chunk", [7, 70])
 @pytest.mark.parametrize("variant", ["literal", "dense"])
-@pytest.mark.parametrize("engine", ["generic", "wave", "rows", "auto"])
+@pytest.mark.parametrize("engine", ["generic", "wave", "rows", "group", "auto"])
 @pytest.mark.parametrize("case", STEP_N_CASES, ids=[f"{n}-B{b}-T{t}" for n, b, t in STEP_N_CASES])
 def test_step_n_matches_oracle(case, engine, variant, chunk):
     require_gpu()
     name, B, T = case
     wl = inputs.WORKLOADS[name].with_(B=B, T=T, L=25)
+    if engine == "group" and not group_ok(wl):
+        pytest.skip("not eligible for the group engine")
     say(f"[parity step_n] {name} B={B} T={T} engine={engine} variant={variant} chunk={chunk}")
     maps, rules, actions = inputs.make_all(wl, 2, variant)
     want_m, want_r, want_d = oracle.run(wl, maps, rules, actions, nthreads=8)
@@ -84,11 +88,13 @@ EDGE = {
 
 
 @pytest.mark.parametrize("variant", inputs.VARIANTS)
-@pytest.mark.parametrize("engine", ["generic", "lane16", "wave", "rows"])
+@pytest.mark.parametrize("engine", ["generic", "lane16", "wave", "rows", "group"])
 @pytest.mark.parametrize("name", sorted(EDGE))
 def test_edge_shapes_match_oracle(name, engine, variant):
     require_gpu()
     wl = EDGE[name]
+    if engine == "group" and not group_ok(wl):
+        pytest.skip("not eligible for the group engine")
     say(f"[parity edge] {name} engine={engine} variant={variant}")
     maps, rules, actions = inputs.make_all(wl, 0, variant)
     want_m, want_r, want_d = oracle.run(wl, maps, rules, actions, nthreads=8)
