@@ -387,6 +387,9 @@ def main():
         launches[0] = run(T)
     rep_ms = timed_repeats(torch, stream, region, repeats, hold)
     ms = float(np.median(rep_ms))
+    # the same events around an empty region after the same hold: what the window costs with
+    # no launch in it
+    floor_us = float(np.median(timed_repeats(torch, stream, lambda: None, repeats, hold))) * 1e3
 
     env_steps = wl.B * T
     value = env_steps / (ms / 1e3)
@@ -475,6 +478,7 @@ def main():
                 "site_order": args.site_order},
         },
         "repeats_ms": rep_ms,
+        "event_floor_us": floor_us,
         "timing": "median of the repeats; each repeat times exactly `steps` steps between HIP "
                   "events on the launch stream, synchronised on both sides, with a device-side "
                   "hold queued before the start event so the launches are queued when it fires"
