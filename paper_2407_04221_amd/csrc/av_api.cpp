@@ -91,6 +91,7 @@ void free_device_program(av_batch_t b) {
     dev_free(b->dprog.match);
     dev_free(b->dprog.vote);
     dev_free(b->dprog.rvote);
+    dev_free(b->dprog.gtab);
     b->dprog = DeviceProgram{};
     dev_free(b->d_rows);
     b->d_rows = nullptr;
@@ -479,6 +480,11 @@ av_status av_load_rules(av_batch_t b, int32_t R, const int32_t *shape, const int
     b->dprog.vote_stride = b->prog.vote_stride;
     b->dprog.rvote_stride = b->prog.rvote_stride;
     b->dprog.any_reward = b->prog.any_reward;
+    if (b->plain_engine == AV_ENGINE_GROUP) {
+        std::vector<uint32_t> tab;
+        compile_group_tables(b->prog, c.height, c.width, c.channels, tab, b->dprog.gtab_stride);
+        if (av_status st = upload(&b->dprog.gtab, tab)) return st;
+    }
     if (b->plain_engine == AV_ENGINE_ROWS) {
         compile_rows(b->prog, c.channels, b->rprog);
         if (av_status st = upload(&b->d_rows, b->rprog.words)) return st;

@@ -225,41 +225,17 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
         vote = pc;
     }
     {
-        const int words = (C1 + 1) * PR + Rt * MS + 3 * C * Hq + (Rt + 1) * kProbeWords + C * Rt;
+        const int words = (C1 + 1) * PR + Rt * MS + 3 * C * Hq;   // (PT and RS are copied)
         for (int w = lane; w < words; w += 64) lds[w] = 0u;
     }
 
-    // rule ranges of the channel vote lists (each list is ordered by rule): RS[c][r] = first |
-    // end << 16 of rule r's votes on channel c, 0 when it has none
-    for (int c = 0; c < C; ++c) {
-        const uint32_t *vc = vote + int(vlw[2 * c]);
-        const int n = int(vlw[2 * c + 1]);
-        for (int k = lane; k < n; k += 64) {
-            const uint32_t r = vc[k] & 255u;
-            uint32_t w = 0u;
-            if (k == 0 || (vc[k - 1] & 255u) != r) w |= uint32_t(k);
-            if (k == n - 1 || (vc[k + 1] & 255u) != r) w |= uint32_t(k + 1) << 16;
-            atomicOr(RS + c * Rt + int(r), w);
-        }
+    // the probe table and the rule ranges (built with the program: compile_group_tables)
+    {
+        const uint32_t *gt = a.prog.gtab + size_t(s) * a.prog.gtab_stride;
+        for (int w = lane; w < a.prog.gtab_stride; w += 64) PT[w] = gt[w];
     }
-    // probe table: per loaded rule, its first four input entries (a missing entry is one that
-    // always passes: must-be-0 on the zero plane) and its anchor rows and columns
     const int nl = Rt - kMoveRules;               // loaded rules
     const int nr = (nl - g + G - 1) / G;          // this group's loaded rule count
-    for (int r = kMoveRules + lane; r < Rt; r += 64) {
-        const uint32_t *hw = ghdr + r * kHdrWords;
-        const int n = int(hw[0]), m = int(hw[1]);
-        const int moff = int(hw[3]), mcnt = int(hw[4]);
-        const uint32_t pass = uint32_t(C1);       // plane C + 1 is all zeros
-        uint32_t *pt = PT + r * kProbeWords;
-#pragma unroll
-        for (int e = 0; e < kProbeEntries; ++e) pt[e] = e < mcnt ? gment[moff + e] : pass;
-        // anchors: columns 0 .. W - m (the low W - m + 1 bits: ~0 >> (32 - (W - m + 1))) of
-        // rows 0 .. H - n
-        const int cols = W - m + 1, rows = H - n + 1;
-        pt[4] = (cols >= 1 && rows >= 1) ? uint32_t(32 - cols) | (uint32_t(rows) << 8) : 0u;
-        pt[5] = pt[6] = pt[7] = 0u;
-    }
 #pragma unroll
     for (int q = 0; q < kMaxChanPerGroup; ++q) {
         const int c = g + G * q;
@@ -521,6 +497,39 @@ bool group_eligible(int H, int W, int C, int rules_per_set, int max_pat_h, int m
            group_lds_bytes(H, C, rules_per_set, max_pat_h) <= size_t(kLdsBudget);
 }
 
+void compile_group_tables(const GenericProgram &p, int H, int W, int C,
+                          std::vector<uint32_t> &tab, int &stride) {
+    const int Rt = p.rules_per_set, C1 = C + 1;
+    stride = (Rt + 1) * kProbeWords + C * Rt;
+    tab.assign(size_t(p.sets) * stride, 0u);
+    for (int s = 0; s < p.sets; ++s) {
+        uint32_t *pt = tab.data() + size_t(s) * stride, *rs = pt + (Rt + 1) * kProbeWords;
+        // probe rows of the loaded rules: the first four input entries (rarest first; a
+        // missing one always passes: must-be-0 on the zero plane C + 1) and the anchors,
+        // columns 0 .. W - m (~0 >> (32 - (W - m + 1))) of rows 0 .. H - n
+        for (int r = kMoveRules; r < Rt; ++r) {
+            const RuleHdr &h = p.hdr[size_t(s) * Rt + r];
+            const uint32_t *ent = p.match.data() + size_t(s) * p.match_stride + h.match_off;
+            uint32_t *row = pt + r * kProbeWords;
+            for (int e = 0; e < kProbeEntries; ++e)
+                row[e] = e < h.match_cnt ? ent[e] : uint32_t(C1);
+            const int cols = W - h.m + 1, rows = H - h.n + 1;
+            row[4] = (cols >= 1 && rows >= 1) ? uint32_t(32 - cols) | (uint32_t(rows) << 8) : 0u;
+        }
+        // rule ranges of the channel vote lists (each ordered by rule): first | end << 16
+        for (int c = 0; c < C; ++c) {
+            const VoteList &vl = p.votes[size_t(s) * C1 + c];
+            const uint32_t *v = p.vote.data() + size_t(s) * p.vote_stride + vl.off;
+            for (int k = 0; k < vl.cnt; ++k) {
+                const int r = int(v[k] & 255u);
+                uint32_t &w = rs[c * Rt + r];
+                if (k == 0 || int(v[k - 1] & 255u) != r) w |= uint32_t(k);
+                if (k == vl.cnt - 1 || int(v[k + 1] & 255u) != r) w |= uint32_t(k + 1) << 16;
+            }
+        }
+    }
+}
+
 namespace {
 template <int Hq>
 void launch_hq(const StepArgs &a, size_t lds, int prog_lds, hipStream_t s) {
@@ -539,10 +548,10 @@ hipError_t launch_group_step(const StepArgs &a, hipStream_t s) {
     const size_t prog = sizeof(uint32_t) * (size_t(a.prog.rules_per_set) * kHdrWords +
                                             a.prog.match_stride + a.prog.rvote_stride +
                                             2 * (a.C + 1) + a.prog.vote_stride);
-    // the program goes to LDS when it fits and leaves room for as many waves per CU (160 KiB
-    // of LDS) as the batch can use, up to 16 (4 per SIMD)
+    // the program goes to LDS for launches of 16 steps or more, when it fits and leaves room
+    // for as many waves per CU (160 KiB of LDS) as the batch can use, up to 16 (4 per SIMD)
     const size_t need = size_t(std::min(16, (a.B + 255) / 256));
-    const int prog_lds = base + prog <= size_t(kLdsBudget) &&
+    const int prog_lds = a.k >= 16 && base + prog <= size_t(kLdsBudget) &&
                          (base + prog) * need <= size_t(160) * 1024 ? 1 : 0;
     const size_t lds = base + (prog_lds ? prog : 0);
     if (group_lanes(a.H) == 16) launch_hq<16>(a, lds, prog_lds, s);
