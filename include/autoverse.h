@@ -129,7 +129,9 @@ typedef struct {
     size_t blob_bytes;          /* size av_get_state needs */
 } av_info;
 
-/* Create a batch on cfg->device.  Maps start empty; av_load_rules and av_reset must both
+/* Create a batch of B independent environments on cfg->device (paper Sec. 2.1: a game is a
+ * board of C binary tile channels over H x W cells; Sec. 2.3: many environments are stepped
+ * in parallel on the accelerator).  Maps start empty; av_load_rules and av_reset must both
  * be called before the first step.  Fails with AV_EINVAL for sizes outside the limits in
  * av_config, when one environment's working set (its C + 1 planes and one match plane per
  * rule, 64-bit rows for W > 32) exceeds 64 KiB of LDS, or when an explicitly requested
@@ -174,26 +176,40 @@ typedef enum {
  *   seed     key of the random index channel
  * Engines: on a lane16 batch the control is compiled into the lane16 program (a new
  * program per call); the wave engine runs it when its scratch (about 1.3 KiB, plus 4 bytes
- * per cell for the random channel) still fits its 64 KiB of LDS; otherwise it runs on the
- * generic engine, to which a batch created with AV_ENGINE_AUTO switches while some limit or
- * inhibition is set (an explicit wave engine then gives AV_EINVAL).
+ * per cell for the random channel) still fits its 64 KiB of LDS.  A batch created with
+ * AV_ENGINE_AUTO whose engine is group or rows switches to the wave engine on those terms,
+ * and otherwise to the generic engine, while some limit or inhibition is set; explicit group
+ * and rows batches refuse the control, and so does an explicit wave batch whose scratch does
+ * not fit (AV_EINVAL).
  * AV_ESTATE before av_load_rules (which clears the control); AV_EINVAL for a negative
  * limit, an inhibition with q >= r or an unknown order.  Synchronises the stream. */
 av_status av_set_rule_control(av_batch_t b, const int32_t *limit, const uint8_t *inhibit,
                               int32_t order, uint64_t seed);
 
 /* Set every environment's initial map and current map to init_maps (device, uint8
- * [B][C][H][W], nonzero = tile present), its step counter and the batch step number to 0.
- * Environments that end an episode return to these maps.  May synchronise. */
+ * [B][C][H][W], nonzero = tile present), its step counter and the batch step number to 0
+ * (paper Sec. 2.2.1: an environment is its initial layout and its rules; Sec. 2.3: an episode
+ * that ends restarts from the initial layout).  Environments that end an episode return to
+ * these maps.  Rules (av_load_rules) and maps may be given in either order.  May
+ * synchronise. */
 av_status av_reset(av_batch_t b, const uint8_t *init_maps);
 
-/* One step of all B environments.  actions: device uint8 [B]; rewards: device float
- * [B] (exact small integers); done: device uint8 [B] (0/1).  Asynchronous. */
+/* One step of all B environments (paper Sec. 2.1: the action places force tiles next to the
+ * player, every rule is matched by a thresholded convolution with its input pattern and its
+ * output written by a transposed convolution; Sec. 2.1.1: the rules apply in parallel, or
+ * per av_config.rule_mode; Sec. 2.2.1: rules pay rewards, and a step that leaves no player
+ * ends the episode).  actions: device uint8 [B] (0 none, 1 up, 2 right, 3 down, 4 left,
+ * other values as 0); rewards: device float [B] (exact small integers); done: device uint8
+ * [B] (0/1).  AV_ESTATE before av_load_rules and av_reset.  Asynchronous; a launch made on a
+ * capturing stream (av_set_stream) can be replayed from a HIP graph: the batch step number
+ * is kept on the device and advances on every replay. */
 av_status av_step(av_batch_t b, const uint8_t *actions, float *rewards, uint8_t *done);
 
-/* k consecutive steps in one launch, identical in result to k calls of av_step.
- * actions uint8 [k][B], rewards float [k][B], done uint8 [k][B], all device; k >= 1.
- * Maps stay on chip between the k steps.  Asynchronous. */
+/* k consecutive steps in one launch, identical in result to k calls of av_step (the same
+ * step, paper Sec. 2.1, Sec. 2.1.1, Sec. 2.2.1, repeated as the learning loop of Sec. 2.3
+ * steps its environments).  actions uint8 [k][B], rewards float [k][B], done uint8 [k][B],
+ * all device; k >= 1.  Maps stay on chip between the k steps.  AV_ESTATE before
+ * av_load_rules and av_reset.  Asynchronous (capturable as av_step). */
 av_status av_step_n(av_batch_t b, int32_t k, const uint8_t *actions, float *rewards,
                     uint8_t *done);
 
