@@ -395,8 +395,12 @@ def main():
     # between two events, so the events' own cost (event_floor_us for an empty window) is
     # spread over them; this is what a kernel trace reports per launch
     nb = max(3, min(50, 20000 // chunk))
-    launch_ms = float(np.median(timed_repeats(torch, stream, lambda: run(nb * chunk), 3,
-                                              hold))) / nb
+    nl = [0]
+
+    def back_to_back():
+        nl[0] = run(nb * chunk)
+    b2b_ms = float(np.median(timed_repeats(torch, stream, back_to_back, 3, hold)))
+    launch_ms = b2b_ms / nl[0]
 
     env_steps = wl.B * T
     value = env_steps / (ms / 1e3)
@@ -485,17 +489,20 @@ def main():
         },
         "repeats_ms": rep_ms,
         "event_floor_us": floor_us,
+        # per step inside the kernel: the back-to-back launch duration (roofline.launch_ms) over
+        # its steps, what a kernel trace of this launch shape shows; ms_per_step also holds the
+        # event window's own cost, which is large against one short launch
+        "kernel_ms_per_step": b2b_ms / (nb * chunk),
         "timing": "median of the repeats; each repeat times exactly `steps` steps between HIP "
                   "events on the launch stream, synchronised on both sides, with a device-side "
                   "hold queued before the start event so the launches are queued when it fires"
                   + ("" if hold else " (no hold available: host submission is inside the window)"),
         "cell_rule_updates_per_sec": value * wl.H * wl.W * wl.R,
-        "pct_hbm_roofline": 100.0 * value / roof_env_steps,
         "roofline": {
             "bound": "alu", "achieved": achieved, "peak": VALU_PEAK_TOPS, "unit": "Tlane-op/s",
             "frac": None if achieved is None else achieved / VALU_PEAK_TOPS,
             "traffic": rec["bytes_per_launch"] if rec else None,
-            "kernel": kernel, "launch_ms": launch_ms, "launches_back_to_back": nb,
+            "kernel": kernel, "launch_ms": launch_ms, "launches_back_to_back": nl[0],
             "valu_lane_ops_per_launch": valu_ops,
             "counters": rec["source"] if rec else None,
             "hbm_normaliser": {"algorithmic_bytes_per_env_step": A,
