@@ -59,7 +59,8 @@ constexpr int kCountBits = 8;           // votes of one sign a cell-channel can 
                                         // (eligibility: rules x pattern cells <= 255)
 constexpr int kHdrWords = int(sizeof(RuleHdr) / 4);
 constexpr int kProbeEntries = 4;        // input entries of every rule tested in one round
-constexpr int kProbeWords = 8;          // probe table row: 4 entries, anchor word, pad
+constexpr int kProbeWords = 8;          // probe table row: 4 entries, anchor word, match
+                                        // offset | count << 16, pad
 
 __device__ inline uint32_t low_mask(int bits) { return bits >= 32 ? ~0u : ((1u << bits) - 1u); }
 
@@ -324,41 +325,85 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
             cand |= __builtin_amdgcn_ballot_w64(mk[kr] != 0u) ? 1u << kr : 0u;
         }
 
-        // loaded rules whose probe passed somewhere in their group: the remaining entries,
-        // then the rule's reward and votes
+        // candidates: the rest of their input entries four at a time.  With up to four rules per
+        // group, in rounds in which every candidate of every group takes its next four (a lane
+        // only while it still holds an anchor of the rule; otherwise it reads the zero plane,
+        // which changes nothing); with more, one rule after another, the next four entries
+        // read while the current ones' plane rows are (rounds would issue every rule's reads
+        // while most rules are done, and four waves share each CU's LDS there).  A rule is done
+        // when its entries run out or its lanes have no anchor left.
         int rsum = 0;
         uint32_t voted = 0u;                      // bit c: a loaded rule voted on channel c
-        for (uint32_t cl = cand; cl; cl &= cl - 1u) {
-            const int kr = __builtin_ctz(cl);
-            const int r = kMoveRules + g + G * kr;
-            uint32_t m = 0u;                      // mk[kr] (kr is wave-uniform)
+        if (cand) {
+            uint32_t meta[NR];                    // match offset | entry count << 16
 #pragma unroll
-            for (int kk = 0; kk < NR; ++kk) m = kk == kr ? mk[kk] : m;
-            if (kr < nr && group_any<Hq>(m != 0u, lane)) {
-                const uint32_t *hw = hdrw + r * kHdrWords;
-                const uint32_t *en = ment + int(hw[3]);
-                const int cnt = int(hw[4]);
-                // the rest of the entries kChunk at a time, the next chunk read while the
-                // current one's plane rows are; indices past the last entry repeat it (AND is
-                // idempotent), which keeps every read inside the rule's list
-                int e = kProbeEntries;
-                const int last = cnt - 1;
-                uint32_t x[kChunk];
+            for (int kr = 0; kr < NR; ++kr) {
+                const int r = kr < nr ? kMoveRules + g + G * kr : kMoveRules;
+                meta[kr] = kr < nr ? PT[r * kProbeWords + 5] : 0u;
+            }
+            if constexpr (NR <= 4) {
+                for (int e = kProbeEntries;; e += 4) {
+                    bool any = false;
 #pragma unroll
-                for (int u = 0; u < kChunk; ++u) x[u] = en[min(e + u, last)];
-                while (e < cnt && group_any<Hq>(m != 0u, lane)) {
-                    uint32_t cur[kChunk];
+                    for (int kr = 0; kr < NR; ++kr) any |= mk[kr] != 0u && e < int(meta[kr] >> 16);
+                    if (!__builtin_amdgcn_ballot_w64(any)) break;
+                    uint32_t x[NR][4];
 #pragma unroll
-                    for (int u = 0; u < kChunk; ++u) cur[u] = x[u];
-                    e += kChunk;
-                    if (e < cnt) {
+                    for (int kr = 0; kr < NR; ++kr) {
+                        const int off = int(meta[kr] & 0xFFFFu), cnt = int(meta[kr] >> 16);
+                        const bool live = mk[kr] != 0u && e < cnt;
 #pragma unroll
-                        for (int u = 0; u < kChunk; ++u) x[u] = en[min(e + u, last)];
+                        for (int u = 0; u < 4; ++u) {
+                            // past the last entry the last one again (AND is idempotent)
+                            const uint32_t w = ment[live ? off + min(e + u, cnt - 1) : 0];
+                            x[kr][u] = live ? w : uint32_t(C1);
+                        }
                     }
 #pragma unroll
-                    for (int u = 0; u < kChunk; ++u) m &= entry(cur[u]);
+                    for (int kr = 0; kr < NR; ++kr)
+                        mk[kr] &= entry(x[kr][0]) & entry(x[kr][1]) & entry(x[kr][2]) & entry(x[kr][3]);
                 }
-                if (group_any<Hq>(m != 0u, lane)) {
+            } else {
+#pragma unroll
+                for (int kr = 0; kr < NR; ++kr) {
+                    if (!((cand >> kr) & 1u)) continue;
+                    uint32_t m = mk[kr];
+                    if (!(kr < nr && group_any<Hq>(m != 0u, lane))) continue;
+                    const uint32_t *en = ment + int(meta[kr] & 0xFFFFu);
+                    const int cnt = int(meta[kr] >> 16), last = cnt - 1;
+                    int e = kProbeEntries;
+                    uint32_t x[4] = {uint32_t(C1), uint32_t(C1), uint32_t(C1), uint32_t(C1)};
+                    if (e < cnt) {                // (reads stay inside the rule's entries)
+#pragma unroll
+                        for (int u = 0; u < 4; ++u) x[u] = en[min(e + u, last)];
+                    }
+                    while (e < cnt && group_any<Hq>(m != 0u, lane)) {
+                        uint32_t cur[4];
+#pragma unroll
+                        for (int u = 0; u < 4; ++u) cur[u] = x[u];
+                        e += 4;
+                        if (e < cnt) {
+#pragma unroll
+                            for (int u = 0; u < 4; ++u) x[u] = en[min(e + u, last)];
+                        }
+                        m &= entry(cur[0]) & entry(cur[1]) & entry(cur[2]) & entry(cur[3]);
+                    }
+                    mk[kr] = m;
+                }
+            }
+            // the rules that fired in some group: match row, reward and votes
+            uint32_t fl = 0u;
+#pragma unroll
+            for (int kr = 0; kr < NR; ++kr)
+                fl |= __builtin_amdgcn_ballot_w64(mk[kr] != 0u) ? 1u << kr : 0u;
+            for (; fl; fl &= fl - 1u) {
+                const int kr = __builtin_ctz(fl);
+                const int r = kMoveRules + g + G * kr;
+                uint32_t m = 0u;                  // mk[kr] (kr is wave-uniform)
+#pragma unroll
+                for (int kk = 0; kk < NR; ++kk) m = kk == kr ? mk[kk] : m;
+                if (kr < nr && group_any<Hq>(m != 0u, lane)) {
+                    const uint32_t *hw = hdrw + r * kHdrWords;
                     M[r * MS + PAD + y] = m;
                     fired |= 1ull << r;
                     voted |= hw[7];
@@ -515,6 +560,7 @@ void compile_group_tables(const GenericProgram &p, int H, int W, int C,
                 row[e] = e < h.match_cnt ? ent[e] : uint32_t(C1);
             const int cols = W - h.m + 1, rows = H - h.n + 1;
             row[4] = (cols >= 1 && rows >= 1) ? uint32_t(32 - cols) | (uint32_t(rows) << 8) : 0u;
+            row[5] = uint32_t(h.match_off) | (uint32_t(h.match_cnt) << 16);
         }
         // rule ranges of the channel vote lists (each ordered by rule): first | end << 16
         for (int c = 0; c < C; ++c) {
