@@ -112,6 +112,21 @@ __device__ inline bool same_map(const void *kids, int n, int i, int j, const voi
                                 int H) {
     const RowT *a = static_cast<const RowT *>(kids);
     const RowT *b = j >= 0 ? a : static_cast<const RowT *>(other);
+    if ((H * sizeof(RowT)) % 16 == 0) {
+        // a channel's rows are whole 16-byte words at 16-byte aligned offsets (buffers from
+        // hipMalloc, blocks of H rows): compared 16 bytes at a time
+        const int q = int(H * sizeof(RowT) / 16);
+        for (int c = 0; c < C; ++c) {
+            const uint4 *ra = reinterpret_cast<const uint4 *>(a + (size_t(c) * n + i) * H);
+            const uint4 *rb = reinterpret_cast<const uint4 *>(
+                j >= 0 ? b + (size_t(c) * n + j) * H : b + size_t(c) * H);
+            for (int k = 0; k < q; ++k) {
+                const uint4 x = ra[k], z = rb[k];
+                if ((x.x ^ z.x) | (x.y ^ z.y) | (x.z ^ z.z) | (x.w ^ z.w)) return false;
+            }
+        }
+        return true;
+    }
     for (int c = 0; c < C; ++c) {
         const RowT *ra = a + (size_t(c) * n + i) * H;
         const RowT *rb = j >= 0 ? b + (size_t(c) * n + j) * H : b + size_t(c) * H;
@@ -218,8 +233,17 @@ __global__ void __launch_bounds__(256) claim_kernel(SearchArgs a, const void *ki
         RowT *dst = reinterpret_cast<RowT *>(static_cast<char *>(a.store) +
                                              size_t(s) * a.C * a.H * sizeof(RowT));
         const RowT *src = static_cast<const RowT *>(kids);
-        for (int c = 0; c < a.C; ++c)
-            for (int y = 0; y < a.H; ++y) dst[c * a.H + y] = src[(size_t(c) * a.n + i) * a.H + y];
+        if ((a.H * sizeof(RowT)) % 16 == 0) {          // 16 bytes at a time (see same_map)
+            const int q = int(a.H * sizeof(RowT) / 16);
+            for (int c = 0; c < a.C; ++c) {
+                const uint4 *from = reinterpret_cast<const uint4 *>(src + (size_t(c) * a.n + i) * a.H);
+                uint4 *to = reinterpret_cast<uint4 *>(dst + size_t(c) * a.H);
+                for (int k = 0; k < q; ++k) to[k] = from[k];
+            }
+        } else {
+            for (int c = 0; c < a.C; ++c)
+                for (int y = 0; y < a.H; ++y) dst[c * a.H + y] = src[(size_t(c) * a.n + i) * a.H + y];
+        }
         a.keys[s] = (key & 0xFFFFFFFF00000000ull) | kPublished;
     }
     if (a.vals[s] == a.kid_val[i] && a.epoch[s] == a.cur_epoch)
