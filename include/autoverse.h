@@ -370,7 +370,9 @@ av_status av_search_begin(av_search_t s, const uint8_t *root);
 /* Expand one level (above) with at most max_children >= 0 children; fills *info (host).
  * An empty frontier or max_children = 0 expands nothing and keeps the frontier.  A search
  * visits at most 2^32 - 2 states (AV_EINVAL beyond).
- * Synchronises (the next level's size is needed on the host).  AV_ENOMEM when an insertion
+ * Synchronises once, after the children are posted (the next level's size is needed on the
+ * host); the level's last copies may still run on the search's stream when it returns (later
+ * calls on the search are ordered after them).  AV_ENOMEM when an insertion
  * finds 4096 consecutive slots taken by other keys (the table is too full) or, best-first,
  * when the node pool is full: the search must then be restarted with av_search_begin. */
 av_status av_search_expand(av_search_t s, int64_t max_children, av_search_info *info);

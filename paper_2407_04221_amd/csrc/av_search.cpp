@@ -98,13 +98,18 @@ SearchArgs level_args(av_search_t s, int n) {
     return a;
 }
 
+// best node word: (reward with its sign bit flipped) << 32 | ~visit
+av_status decode_best(uint64_t best, av_search_info *info) {
+    info->best_reward = int32_t(uint32_t(best >> 32) ^ 0x80000000u);
+    info->best_visit = int64_t(0xFFFFFFFFull - (best & 0xFFFFFFFFull));
+    return AV_OK;
+}
+
 av_status read_best(av_search_t s, av_search_info *info) {
     uint64_t best = 0;
     SEARCH_HIP(hipMemcpyAsync(&best, s->best, sizeof best, hipMemcpyDeviceToHost, s->stream));
     SEARCH_HIP(hipStreamSynchronize(s->stream));
-    info->best_reward = int32_t(uint32_t(best >> 32) ^ 0x80000000u);
-    info->best_visit = int64_t(0xFFFFFFFFull - (best & 0xFFFFFFFFull));
-    return AV_OK;
+    return decode_best(best, info);
 }
 
 }  // namespace
@@ -282,6 +287,7 @@ av_status expand_best_first(av_search_t s, int64_t max_children, av_search_info 
         return set_error(AV_EINVAL, "a search may visit at most 2^32 - 2 states");
     int64_t nn = 0;
     uint32_t counts[3] = {0, 0, 0};
+    uint64_t best = 0;                 // read with the counts: final once the children are posted
     if (n > 0) {
         s->cur = 0;
         SEARCH_HIP(launch_copy_rows(s->row_bytes, s->pool, int(s->pcap), s->parents, s->front[0],
@@ -307,6 +313,7 @@ av_status expand_best_first(av_search_t s, int64_t max_children, av_search_info 
                                        s->stream, 1, 0));
         SEARCH_HIP(hipMemcpyAsync(counts, s->counts, sizeof counts, hipMemcpyDeviceToHost,
                                   s->stream));
+        SEARCH_HIP(hipMemcpyAsync(&best, s->best, sizeof best, hipMemcpyDeviceToHost, s->stream));
         SEARCH_HIP(hipStreamSynchronize(s->stream));
         if (counts[1] || int64_t(counts[2]) > s->pcap - s->pool_n) {
             s->begun = false;
@@ -340,7 +347,7 @@ av_status expand_best_first(av_search_t s, int64_t max_children, av_search_info 
     info->level = s->level;
     info->frontier = s->open_n;
     info->visited = s->visited;
-    return read_best(s, info);
+    return n > 0 ? decode_best(best, info) : read_best(s, info);
 }
 
 }  // namespace
@@ -355,6 +362,7 @@ av_status av_search_expand(av_search_t s, int64_t max_children, av_search_info *
     if (s->K > 0) return expand_best_first(s, max_children, info);
     info->parents = s->n_front;
     const int64_t n = std::min<int64_t>(int64_t(s->A) * s->n_front, max_children);
+    uint64_t best = 0;                 // read with the counts: final once the children are posted
     if (s->visited + n > int64_t(0xFFFFFFFEll))
         return set_error(AV_EINVAL, "a search may visit at most 2^32 - 2 states");
     if (n > 0) {
@@ -378,6 +386,7 @@ av_status av_search_expand(av_search_t s, int64_t max_children, av_search_info *
         uint32_t counts[3];
         SEARCH_HIP(hipMemcpyAsync(counts, s->counts, sizeof counts, hipMemcpyDeviceToHost,
                                   s->stream));
+        SEARCH_HIP(hipMemcpyAsync(&best, s->best, sizeof best, hipMemcpyDeviceToHost, s->stream));
         SEARCH_HIP(hipStreamSynchronize(s->stream));
         if (counts[1]) {
             s->begun = false;
@@ -401,7 +410,7 @@ av_status av_search_expand(av_search_t s, int64_t max_children, av_search_info *
     info->level = s->level;
     info->frontier = s->n_front;
     info->visited = s->visited;
-    return read_best(s, info);
+    return n > 0 ? decode_best(best, info) : read_best(s, info);
 }
 
 av_status av_search_frontier(av_search_t s, uint8_t *maps, int32_t *reward, int32_t *depth) {
