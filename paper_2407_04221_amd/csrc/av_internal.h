@@ -209,7 +209,7 @@ hipError_t launch_copy_rows(int row_bytes, const void *src, int nsrc, const int3
                             void *dst, int ndst, int off, int n, int C, int H, hipStream_t s);
 hipError_t launch_bf_pop(const uint32_t *open_ids, int kp, const int64_t *pool_slot,
                          const uint64_t *pool_val, const uint64_t *vals, int32_t *parents,
-                         uint32_t *n_par, hipStream_t s);
+                         uint32_t *n_par, uint32_t *counts, hipStream_t s);
 hipError_t launch_bf_gather_meta(const int32_t *parents, int np, const int32_t *pool_reward,
                                  const int32_t *pool_depth, int32_t *front_reward,
                                  int32_t *front_depth, hipStream_t s);

@@ -279,7 +279,7 @@ av_status expand_best_first(av_search_t s, int64_t max_children, av_search_info 
     }
     uint32_t npar = 0;
     SEARCH_HIP(launch_bf_pop(s->oids[s->ocur], kp, s->pool_slot, s->pool_val, s->vals, s->parents,
-                             s->n_par, s->stream));
+                             s->n_par, s->counts, s->stream));
     SEARCH_HIP(hipMemcpyAsync(&npar, s->n_par, sizeof npar, hipMemcpyDeviceToHost, s->stream));
     SEARCH_HIP(hipStreamSynchronize(s->stream));
     const int64_t n = std::min<int64_t>(int64_t(s->A) * npar, max_children);
@@ -298,8 +298,7 @@ av_status expand_best_first(av_search_t s, int64_t max_children, av_search_info 
         a.cap = int(s->pcap - s->pool_n);
         a.next_reward = s->pool_reward + s->pool_n;
         a.next_depth = s->pool_depth + s->pool_n;
-        void *kst = batch_state(s->kids);
-        SEARCH_HIP(hipMemsetAsync(s->counts, 0, 3 * sizeof(uint32_t), s->stream));
+        void *kst = batch_state(s->kids);           // (bf_pop cleared the counts)
         if (batch_engine(s->kids) == AV_ENGINE_LANE16) {
             if (av_status st = step_prefix(s->kids, int(n), s->actions, s->rew, s->done,
                                            s->front[0], int(npar), s->A, s->depth[0]))

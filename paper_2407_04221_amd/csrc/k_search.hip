@@ -385,16 +385,20 @@ __global__ void __launch_bounds__(512) bf_pop_kernel(const uint32_t *open_ids, i
                                                      const int64_t *pool_slot,
                                                      const uint64_t *pool_val,
                                                      const uint64_t *vals, int32_t *parents,
-                                                     uint32_t *n_par) {
+                                                     uint32_t *n_par, uint32_t *counts) {
     __shared__ uint32_t ids[512];
+    if (threadIdx.x < 3) counts[threadIdx.x] = 0u;   // the level's counters, for what follows
     __shared__ int sums[8];
     const int t = threadIdx.x;
     ids[t] = t < kp ? open_ids[t] : 0xFFFFFFFFu;
     __syncthreads();
-    for (int k = 2; k <= 512; k <<= 1)
+    // a bitonic network over the first P = next power of two >= kp entries (the rest hold the
+    // largest id and stay in place)
+    const int P = kp <= 1 ? 1 : 1 << (32 - __builtin_clz(uint32_t(kp - 1)));
+    for (int k = 2; k <= P; k <<= 1)
         for (int j = k >> 1; j > 0; j >>= 1) {
             const int o = t ^ j;
-            if (o > t) {
+            if (t < P && o > t) {
                 const uint32_t a = ids[t], b = ids[o];
                 const bool up = (t & k) == 0;
                 if ((a > b) == up) {
@@ -601,9 +605,9 @@ hipError_t launch_copy_rows(int row_bytes, const void *src, int nsrc, const int3
 
 hipError_t launch_bf_pop(const uint32_t *open_ids, int kp, const int64_t *pool_slot,
                          const uint64_t *pool_val, const uint64_t *vals, int32_t *parents,
-                         uint32_t *n_par, hipStream_t s) {
+                         uint32_t *n_par, uint32_t *counts, hipStream_t s) {
     hipLaunchKernelGGL(bf_pop_kernel, dim3(1), dim3(512), 0, s, open_ids, kp, pool_slot, pool_val,
-                       vals, parents, n_par);
+                       vals, parents, n_par, counts);
     return hipGetLastError();
 }
 
