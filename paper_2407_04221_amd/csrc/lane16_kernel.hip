@@ -13,9 +13,9 @@
 //
 // Environments of a wave that do not exist (B not a multiple of 8) compute on zero rows and
 // are never stored.  The launch issues all of its first loads (current and initial rows, step
-// counters, three blocks of actions) before using any, so it waits for memory once; the
-// initial rows then stay in registers for resets (a one-step launch reads them only in waves
-// where an episode ends).  Actions are read 16 steps at a time and
+// counters, three blocks of actions) before using any, so it waits for memory once.  The
+// initial rows are read by a wave when one of its environments first ends an episode, and
+// then stay in registers for later resets.  Actions are read 16 steps at a time and
 // turned into per-direction force masks, which each step fetches across its row with
 // ds_bpermute one step ahead; rewards and done flags are kept in registers for 16 steps and
 // stored together.
@@ -139,24 +139,15 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
         rb = u32(row[iB]);
     };
     // Every global load the launch starts with is issued before any of them is used, so the
-    // prologue waits for memory once: the current rows, the initial rows (a launch of several
-    // steps keeps them in registers for resets; a one-step launch reads them only in waves
-    // where an episode ends, and a search expansion, which never resets, not at all), the
-    // step counters and three blocks of actions.
-    const bool lazy_init = K == 1 || gsrc;
-    u32 slo[AV_C], shi[AV_C], ilo[AV_C], ihi[AV_C];
+    // prologue waits for memory once: the current rows, the step counters and three blocks
+    // of actions.  The initial rows are read at the wave's first reset (a search expansion,
+    // which never resets, keeps its current rows instead).
+    bool have_init = false;
+    u32 slo[AV_C], shi[AV_C];
 #pragma unroll
     for (int c = 0; c < AV_C; ++c) {
         slo[c] = u32(src[(size_t(c) * sstride + sA) * AV_H + yy]);
         shi[c] = u32(src[(size_t(c) * sstride + sB) * AV_H + yy]);
-        ilo[c] = ihi[c] = 0u;
-    }
-    if (!lazy_init) {
-#pragma unroll
-        for (int c = 0; c < AV_C; ++c) {
-            ilo[c] = u32(init[(size_t(c) * B + iA) * AV_H + yy]);
-            ihi[c] = u32(init[(size_t(c) * B + iB) * AV_H + yy]);
-        }
     }
     const int *const tsrc = gsrc ? gdepth : tctr;
     int tA = tsrc[sA], tB = tsrc[sB];
@@ -168,7 +159,7 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
 #pragma unroll
     for (int c = 0; c < AV_C; ++c) {
         p[c] = (slo[c] | (shi[c] << 16)) & keep;
-        q[c] = gsrc ? p[c] : (ilo[c] | (ihi[c] << 16)) & keep;
+        q[c] = p[c];                            // (replaced at the first reset)
     }
     const u32 COLS = BOTH(COLMASK(AV_W));
     auto dir_masks = [&](u32 aA, u32 aB, u32 *m) {
@@ -264,7 +255,8 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
             if (dA) tA = 0;
             if (dB) tB = 0;
             if (y == s) dbuf = u32(dA) | (u32(dB) << 1);
-            if (lazy_init && !gsrc) {           // a one-step launch: the initial rows now
+            if (!gsrc && !have_init) {          // the initial rows, once
+                have_init = true;
 #pragma unroll
                 for (int c = 0; c < AV_C; ++c) {
                     const u32 lo = u32(init[(size_t(c) * B + iA) * AV_H + yy]);
