@@ -7,11 +7,13 @@
 //
 // The four built-in moves are computed in registers from the lanes' own rows of the player,
 // wall and force planes and the rows next to them (DPP row shifts within 16-lane groups,
-// ds_bpermute within 32-lane groups).  Each loaded rule's first four entries of its
-// rarest-first input list sit in a probe table that a step reads together with the player and
-// wall rows, so the probe of every loaded rule is one more round of LDS reads with no branch
-// between the rules; only rules that pass it somewhere read the rest of their entries, and only
-// channels that received votes are rewritten.
+// ds_bpermute within 32-lane groups); the player and wall rows stay in registers from step to
+// step unless a loaded rule wrote those planes.  Each loaded rule's first four entries of its
+// rarest-first input list sit in a probe table (held in registers for the launch when a group
+// has at most two rules, else read at the start of each step), so the probe of every loaded
+// rule is one round of LDS reads with no branch between the rules; only rules that pass it
+// somewhere read the rest of their entries, and only channels that received votes are
+// rewritten.
 //
 // LDS (32-bit rows):
 //   P    [C+2][PR]     the map, the force plane (channel C) and a zero plane (an entry that
@@ -268,20 +270,36 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
     const uint32_t cm1 = low_mask(W - 1);         // anchors of a 1 x 2 pattern
     const uint32_t vrow2 = (y + 2 <= H) ? wmask : 0u;   // rows of a 2 x 1 pattern's anchors
     const int pown = kChPlayer % G;               // the group that writes the player plane
-    for (int k = 0; k < a.k; ++k) {
-        const int kb = k & 63;
-        if (kb == 0) ablk = (k + lane < a.k) ? uint32_t(a.actions[size_t(k + lane) * a.B + b]) : 0u;
-        const int act = __builtin_amdgcn_readlane(int(ablk), kb);
-        // the lane's rows of the player and wall planes (0 past the map), and the probe table
-        // rows of the group's rules (they do not depend on the map: read with the rows)
-        const uint32_t Py = row ? P2[y] : 0u, Wy = row ? P[kChWall * PR + y] : 0u;
-        uint4 pe[NR];
-        uint32_t pv[NR];
+    // the player and wall rows of the lane (every group holds them): the next step's follow
+    // from the moves' votes in registers unless a loaded rule voted on either plane, a player
+    // cell got votes of both signs or the episode ended; then they are read again
+    uint32_t Pyr = row ? P2[y] : 0u, Wyr = row ? P[kChWall * PR + y] : 0u;
+    // the probe rows of the group's rules: read once when the group has at most two rules,
+    // else every step (registers would spill)
+    uint4 pe[NR];
+    uint32_t pv[NR];
+    if constexpr (NR <= 2) {
 #pragma unroll
         for (int kr = 0; kr < NR; ++kr) {
             const int r = kr < nr ? kMoveRules + g + G * kr : kMoveRules;
             pe[kr] = *reinterpret_cast<const uint4 *>(PT + r * kProbeWords);
             pv[kr] = PT[r * kProbeWords + 4];
+        }
+    }
+    for (int k = 0; k < a.k; ++k) {
+        const int kb = k & 63;
+        if (kb == 0) ablk = (k + lane < a.k) ? uint32_t(a.actions[size_t(k + lane) * a.B + b]) : 0u;
+        const int act = __builtin_amdgcn_readlane(int(ablk), kb);
+        // the lane's rows of the player and wall planes (0 past the map; kept in registers
+        // from step to step), and the probe table rows of the group's rules
+        const uint32_t Py = Pyr, Wy = Wyr;
+        if constexpr (NR > 2) {                   // (up to two rules: held for the launch)
+#pragma unroll
+            for (int kr = 0; kr < NR; ++kr) {
+                const int r = kr < nr ? kMoveRules + g + G * kr : kMoveRules;
+                pe[kr] = *reinterpret_cast<const uint4 *>(PT + r * kProbeWords);
+                pv[kr] = PT[r * kProbeWords + 4];
+            }
         }
         // the rows next to them and the force row
         const uint32_t Pn = next_row<Hq>(Py, lane, y), Wn = next_row<Hq>(Wy, lane, y);
@@ -491,6 +509,13 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
 #pragma unroll 1
                 for (int c = g; c < C; c += G) P[c * PR + y] = I0[c * Hq + y];
             }
+        }
+        if (d || ((lvoted >> kChPlayer) & 1u) || ((lvoted >> kChWall) & 1u) ||
+            __builtin_amdgcn_ballot_w64((mplus & mminus) != 0u)) {
+            Pyr = row ? P2[y] : 0u;
+            Wyr = row ? P[kChWall * PR + y] : 0u;
+        } else {
+            Pyr = (Py | mplus) & ~mminus;
         }
         if (lane == kb) {
             rbuf = float(rsum);
