@@ -265,7 +265,8 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
     float rbuf = 0.f;       // lane l: reward of step k0 + l
     uint32_t dbuf = 0u;     // lane l: done flag of step k0 + l
     uint32_t *const F = P + C * PR;
-    const uint32_t *const P2 = P + kChPlayer * PR;
+    uint32_t *const P2w = P + kChPlayer * PR;
+    const uint32_t *const P2 = P2w;
 
     const uint32_t cm1 = low_mask(W - 1);         // anchors of a 1 x 2 pattern
     const uint32_t vrow2 = (y + 2 <= H) ? wmask : 0u;   // rows of a 2 x 1 pattern's anchors
@@ -456,21 +457,33 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
         }
         // every rule that fired anywhere in the wave and every channel a loaded rule voted on
         // (the groups' masks OR-ed)
-        uint64_t fired_all = 0;
+        uint64_t fired_all = fired & 15ull;       // (the moves' bits are the same in every lane)
         uint32_t lvoted = 0u;                     // channels the loaded rules voted on
+        if (__builtin_amdgcn_ballot_w64((fired >> kMoveRules) != 0ull)) {
 #pragma unroll
-        for (int gg = 0; gg < G; ++gg) {
-            const uint32_t lo = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(fired)), gg * Hq));
-            const uint32_t hi = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(fired >> 32)), gg * Hq));
-            fired_all |= uint64_t(lo) | (uint64_t(hi) << 32);
-            lvoted |= uint32_t(__builtin_amdgcn_readlane(int(voted), gg * Hq));
+            for (int gg = 0; gg < G; ++gg) {
+                const uint32_t lo = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(fired)), gg * Hq));
+                const uint32_t hi = uint32_t(__builtin_amdgcn_readlane(int(uint32_t(fired >> 32)), gg * Hq));
+                fired_all |= uint64_t(lo) | (uint64_t(hi) << 32);
+                lvoted |= uint32_t(__builtin_amdgcn_readlane(int(voted), gg * Hq));
+            }
         }
         const uint32_t voted_all = lvoted | ((fired_all & 15ull) ? 1u << kChPlayer : 0u);
 
         // new rows of the channels that received votes: group g rewrites channels g, g + G, ...
         // (the moves' votes on the player plane are in registers, the loaded rules' in LDS)
         bool pl_any = g == pown && row && Py != 0u;   // a player bit after the write
-        if (voted_all) {
+        if (voted_all == (1u << kChPlayer) && lvoted == 0u) {
+            // only the moves voted (most steps): the player plane, from registers
+            uint32_t nw = (Py | mplus) & ~mminus;
+            if (__builtin_amdgcn_ballot_w64((mplus & mminus) != 0u))
+                nw = exact_channel<Hq>(Py, fired_all, vote + int(vlw[2 * kChPlayer]),
+                                       RS + kChPlayer * Rt, M, MS, PAD, y, row, lane);
+            if (g == pown) {
+                if (row) P2w[y] = nw;
+                pl_any = row && nw != 0u;
+            }
+        } else if (voted_all) {
 #pragma unroll 1
             for (int c = g; c < C; c += G) {
                 if (!((voted_all >> c) & 1u)) continue;
