@@ -24,9 +24,9 @@
 //                      above let a vote read match row y - i without a test
 //   PL, MI [C][Hq]     per stored channel, the OR of the +1 and of the -1 votes
 //   I0   [C][Hq]       the initial rows, for resets
-//   PT   [R+5][8]      probe table: per loaded rule its first four input entries and its
-//                      anchor rows and columns (row R + 4: zeros, read by
-//                      groups with fewer rules than others)
+//   PT   [R+5][12]     probe table: per loaded rule its first eight input entries, its
+//                      anchor rows and columns and where its entries are (row R + 4: zeros,
+//                      read by groups with fewer rules than others)
 //   RS   [C][R+4]      per channel and rule, the range of the rule's votes in the channel's
 //                      vote list (for exact recounts)
 //   program            (when it fits, see the launcher) the environment's rule headers, input
@@ -61,8 +61,8 @@ constexpr int kCountBits = 8;           // votes of one sign a cell-channel can 
                                         // (eligibility: rules x pattern cells <= 255)
 constexpr int kHdrWords = int(sizeof(RuleHdr) / 4);
 constexpr int kProbeEntries = 4;        // input entries of every rule tested in one round
-constexpr int kProbeWords = 8;          // probe table row: 4 entries, anchor word, match
-                                        // offset | count << 16, pad
+constexpr int kProbeWords = 12;         // probe table row: entries 0-3, anchor word, match
+                                        // offset | count << 16, pad, pad, entries 4-7
 
 __device__ inline uint32_t low_mask(int bits) { return bits >= 32 ? ~0u : ((1u << bits) - 1u); }
 
@@ -279,12 +279,16 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
     // else every step (registers would spill)
     uint4 pe[NR];
     uint32_t pv[NR];
+    uint4 pe2[NR];                                // entries 4 .. 7 (NR <= 2)
+    uint32_t pm[NR];                              // match offset | count << 16 (NR <= 2)
     if constexpr (NR <= 2) {
 #pragma unroll
         for (int kr = 0; kr < NR; ++kr) {
             const int r = kr < nr ? kMoveRules + g + G * kr : kMoveRules;
             pe[kr] = *reinterpret_cast<const uint4 *>(PT + r * kProbeWords);
             pv[kr] = PT[r * kProbeWords + 4];
+            pe2[kr] = *reinterpret_cast<const uint4 *>(PT + r * kProbeWords + 8);
+            pm[kr] = kr < nr ? PT[r * kProbeWords + 5] : 0u;
         }
     }
     for (int k = 0; k < a.k; ++k) {
@@ -358,7 +362,8 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
 #pragma unroll
             for (int kr = 0; kr < NR; ++kr) {
                 const int r = kr < nr ? kMoveRules + g + G * kr : kMoveRules;
-                meta[kr] = kr < nr ? PT[r * kProbeWords + 5] : 0u;
+                if constexpr (NR <= 2) meta[kr] = pm[kr];
+                else meta[kr] = kr < nr ? PT[r * kProbeWords + 5] : 0u;
             }
             if constexpr (NR <= 4) {
                 for (int e = kProbeEntries;; e += 4) {
@@ -371,6 +376,14 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
                     for (int kr = 0; kr < NR; ++kr) {
                         const int off = int(meta[kr] & 0xFFFFu), cnt = int(meta[kr] >> 16);
                         const bool live = mk[kr] != 0u && e < cnt;
+                        if (NR <= 2 && e == kProbeEntries) {   // entries 4 .. 7: in registers
+                            const uint4 q = pe2[kr];
+                            x[kr][0] = live ? q.x : uint32_t(C1);
+                            x[kr][1] = live ? q.y : uint32_t(C1);
+                            x[kr][2] = live ? q.z : uint32_t(C1);
+                            x[kr][3] = live ? q.w : uint32_t(C1);
+                            continue;
+                        }
 #pragma unroll
                         for (int u = 0; u < 4; ++u) {
                             // past the last entry the last one again (AND is idempotent)
@@ -599,6 +612,11 @@ void compile_group_tables(const GenericProgram &p, int H, int W, int C,
             const int cols = W - h.m + 1, rows = H - h.n + 1;
             row[4] = (cols >= 1 && rows >= 1) ? uint32_t(32 - cols) | (uint32_t(rows) << 8) : 0u;
             row[5] = uint32_t(h.match_off) | (uint32_t(h.match_cnt) << 16);
+            // entries 4 .. 7 (past the last, the last again; none: the zero plane)
+            for (int e = 0; e < 4; ++e)
+                row[8 + e] = h.match_cnt > kProbeEntries
+                                 ? ent[std::min(kProbeEntries + e, h.match_cnt - 1)]
+                                 : uint32_t(C1);
         }
         // rule ranges of the channel vote lists (each ordered by rule): first | end << 16
         for (int c = 0; c < C; ++c) {
