@@ -55,7 +55,7 @@
 namespace av {
 namespace {
 
-constexpr int kMaxRulesPerGroup = 16;   // rules a group holds in registers, at most
+constexpr int kMaxRulesPerGroup = 16;   // loaded and built-in rules per group, at most
 constexpr int kMaxChanPerGroup = 8;     // stored channels a group writes, at most
 constexpr int kCountBits = 8;           // votes of one sign a cell-channel can get: <= 255
                                         // (eligibility: rules x pattern cells <= 255)
