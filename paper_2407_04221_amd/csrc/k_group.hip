@@ -272,8 +272,8 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
     const uint32_t vrow2 = (y + 2 <= H) ? wmask : 0u;   // rows of a 2 x 1 pattern's anchors
     const int pown = kChPlayer % G;               // the group that writes the player plane
     // the player and wall rows of the lane (every group holds them): the next step's follow
-    // from the moves' votes in registers unless a loaded rule voted on either plane, a player
-    // cell got votes of both signs or the episode ended; then they are read again
+    // from the moves' votes in registers unless a loaded rule voted on either plane or the
+    // episode ended; then they are read again
     uint32_t Pyr = row ? P2[y] : 0u, Wyr = row ? P[kChWall * PR + y] : 0u;
     // the probe rows of the group's rules: read once when the group has at most two rules,
     // else every step (registers would spill)
@@ -319,8 +319,25 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
         const uint32_t m1 = Fy & ~Wy & (Py >> 1) & cm1;
         const uint32_t m2 = Py & Fn & ~Wn & vrow2;
         const uint32_t m3 = Fy & ~Wy & Pn & vrow2;
-        const uint32_t mplus = (m0 << 1) | m1 | prev_row<Hq>(m2, lane, y) | m3;
-        const uint32_t mminus = m0 | (m1 << 1) | m2 | prev_row<Hq>(m3, lane, y);
+        const uint32_t m2p = prev_row<Hq>(m2, lane, y), m3p = prev_row<Hq>(m3, lane, y);
+        const uint32_t mplus = (m0 << 1) | m1 | m2p | m3;
+        const uint32_t mminus = m0 | (m1 << 1) | m2 | m3p;
+        // the player rows after the moves' votes alone: one sign OR-ed, or, where some cell got
+        // votes of both signs (players moving into cells other players leave), counted exactly
+        // in registers: old + #plus > #minus over the four plus and four minus terms
+        uint32_t pnew = (Py | mplus) & ~mminus;
+        if (__builtin_amdgcn_ballot_w64((mplus & mminus) != 0u)) {
+            const uint32_t a1 = m0 << 1, b2 = m1 << 1;
+            // plus: old, a1, m1, m2p, m3 -> p2 p1 p0 (at most 5)
+            const uint32_t s1 = Py ^ a1 ^ m1, c1 = (Py & a1) | (m1 & (Py ^ a1));
+            const uint32_t p0 = s1 ^ m2p ^ m3, c2 = (s1 & m2p) | (m3 & (s1 ^ m2p));
+            const uint32_t p1 = c1 ^ c2, p2 = c1 & c2;
+            // minus: m0, b2, m2, m3p -> n2 n1 n0 (at most 4)
+            const uint32_t s3 = m0 ^ b2 ^ m2, c3 = (m0 & b2) | (m2 & (m0 ^ b2));
+            const uint32_t n0 = s3 ^ m3p, c4 = s3 & m3p;
+            const uint32_t n1 = c3 ^ c4, n2 = c3 & c4;
+            pnew = (p2 & ~n2) | (~(p2 ^ n2) & ((p1 & ~n1) | (~(p1 ^ n1) & p0 & ~n0)));
+        }
         if (g == 0) {
             M[0 * MS + PAD + y] = m0;
             M[1 * MS + PAD + y] = m1;
@@ -488,10 +505,7 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
         bool pl_any = g == pown && row && Py != 0u;   // a player bit after the write
         if (voted_all == (1u << kChPlayer) && lvoted == 0u) {
             // only the moves voted (most steps): the player plane, from registers
-            uint32_t nw = (Py | mplus) & ~mminus;
-            if (__builtin_amdgcn_ballot_w64((mplus & mminus) != 0u))
-                nw = exact_channel<Hq>(Py, fired_all, vote + int(vlw[2 * kChPlayer]),
-                                       RS + kChPlayer * Rt, M, MS, PAD, y, row, lane);
+            const uint32_t nw = pnew;
             if (g == pown) {
                 if (row) P2w[y] = nw;
                 pl_any = row && nw != 0u;
@@ -508,7 +522,9 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
                     mi |= mminus;
                 }
                 uint32_t nw = (old | pl) & ~mi;
-                if (group_any<Hq>((pl & mi) != 0u, lane))
+                if (c == kChPlayer && !lv)
+                    nw = pnew;                    // only the moves voted on it
+                else if (group_any<Hq>((pl & mi) != 0u, lane))
                     nw = exact_channel<Hq>(old, fired_all, vote + int(vlw[2 * c]),
                                            RS + c * Rt, M, MS, PAD, y, row, lane);
                 if (row) P[c * PR + y] = nw;
@@ -536,12 +552,11 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
                 for (int c = g; c < C; c += G) P[c * PR + y] = I0[c * Hq + y];
             }
         }
-        if (d || ((lvoted >> kChPlayer) & 1u) || ((lvoted >> kChWall) & 1u) ||
-            __builtin_amdgcn_ballot_w64((mplus & mminus) != 0u)) {
+        if (d || ((lvoted >> kChPlayer) & 1u) || ((lvoted >> kChWall) & 1u)) {
             Pyr = row ? P2[y] : 0u;
             Wyr = row ? P[kChWall * PR + y] : 0u;
         } else {
-            Pyr = (Py | mplus) & ~mminus;
+            Pyr = pnew;
         }
         if (lane == kb) {
             rbuf = float(rsum);
