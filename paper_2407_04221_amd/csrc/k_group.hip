@@ -6,8 +6,8 @@
 // barrier: the wave's LDS operations take effect in the order it issues them.
 //
 // The four built-in moves are computed in registers from the lanes' own rows of the player,
-// wall and force planes and the rows next to them (DPP row shifts within 16-lane groups,
-// ds_bpermute within 32-lane groups); the player and wall rows stay in registers from step to
+// wall and force planes and the rows next to them (DPP row shifts within 16-lane groups, DPP
+// shifts of the whole wave for 32-lane groups); the player and wall rows stay in registers from step to
 // step unless a loaded rule wrote those planes.  Each loaded rule's first four entries of its
 // rarest-first input list sit in a probe table (held in registers for the launch when a group
 // has at most two rules, else read at the start of each step), so the probe of every loaded
@@ -76,17 +76,20 @@ __device__ inline bool group_any(bool p, int lane) {
 }
 
 // Row y + 1 (next) and y - 1 (prev) of the lane's group, 0 past the group's ends: a DPP row
-// shift within 16-lane groups, ds_bpermute within 32-lane groups.
+// shift within 16-lane groups; for 32-lane groups a DPP shift of the whole wave by one lane,
+// the lane at the group's end taking 0.
 template <int Hq>
 __device__ inline uint32_t next_row(uint32_t v, int lane, int y) {
+    (void)lane;
     if (Hq == 16) return uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x101, 0xF, 0xF, true));
-    const uint32_t u = uint32_t(__builtin_amdgcn_ds_bpermute((lane + 1) << 2, int(v)));
+    const uint32_t u = uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x130, 0xF, 0xF, true));
     return y + 1 < Hq ? u : 0u;
 }
 template <int Hq>
 __device__ inline uint32_t prev_row(uint32_t v, int lane, int y) {
+    (void)lane;
     if (Hq == 16) return uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x111, 0xF, 0xF, true));
-    const uint32_t u = uint32_t(__builtin_amdgcn_ds_bpermute((lane > 0 ? lane - 1 : 0) << 2, int(v)));
+    const uint32_t u = uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x138, 0xF, 0xF, true));
     return y > 0 ? u : 0u;
 }
 
