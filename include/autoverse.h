@@ -84,11 +84,12 @@ typedef enum {
     AV_ENGINE_GROUP = 5     /* one environment per 64-lane wave, no barriers: 4 groups of 16
                                lanes (maps of up to 16 rows) or 2 of 32 (up to 32 rows),
                                lane y of each owning map row y, group g matching rules g,
-                               g + 4 (or g + 2), ...; every rule's first four input entries
-                               are tested in one round of LDS reads, and only rules that pass
-                               somewhere read the rest.  Needs parallel rule order, H, W <= 32,
+                               g + 4 (or g + 2), ...; input entries are merged per pattern
+                               row, every rule's first four merged entries are tested in one
+                               round of LDS reads, and only rules that pass somewhere read the
+                               rest.  Needs parallel rule order, H, W <= 32,
                                (max_rules + 4) x max_pat_h x max_pat_w <= 254, at most 8
-                               channels per lane group and, within 64 KiB of LDS, C + 2 planes
+                               channels per lane group and, within 64 KiB of LDS, C + 1 planes
                                and R + 4 match planes of Hq + max_pat_h - 1 rows (rounded up to
                                4), 3 C rows of Hq, 12 words per rule plus 12, and C (R + 4)
                                words, 4 bytes each (Hq = 16 or 32); no rule application

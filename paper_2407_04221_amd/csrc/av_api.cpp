@@ -92,6 +92,7 @@ void free_device_program(av_batch_t b) {
     dev_free(b->dprog.vote);
     dev_free(b->dprog.rvote);
     dev_free(b->dprog.gtab);
+    dev_free(b->dprog.gmatch);
     b->dprog = DeviceProgram{};
     dev_free(b->d_rows);
     b->d_rows = nullptr;
@@ -320,6 +321,7 @@ av_status step_prefix(av_batch_t b, int n, const uint8_t *actions, float *reward
     a.L = c.max_episode_steps; a.per_env = 0; a.k = 1;
     a.sequential = c.rule_mode == AV_RULES_SEQUENTIAL;
     a.row_bytes = b->row_bytes; a.max_pat_h = c.max_pat_h;
+    a.max_pat_w = c.max_pat_w;
     a.state = b->d_state; a.init = b->d_init; a.t = b->d_t; a.nctr = b->d_n;
     a.actions = actions; a.rewards = rewards; a.done = done;
     a.prog = b->dprog;
@@ -482,8 +484,11 @@ av_status av_load_rules(av_batch_t b, int32_t R, const int32_t *shape, const int
     b->dprog.any_reward = b->prog.any_reward;
     if (b->plain_engine == AV_ENGINE_GROUP) {
         std::vector<uint32_t> tab;
-        compile_group_tables(b->prog, c.height, c.width, c.channels, tab, b->dprog.gtab_stride);
+        std::vector<uint32_t> gm;
+        compile_group_tables(b->prog, c.height, c.width, c.channels, c.max_pat_h, tab,
+                             b->dprog.gtab_stride, gm, b->dprog.gmatch_stride);
         if (av_status st = upload(&b->dprog.gtab, tab)) return st;
+        if (av_status st = upload(&b->dprog.gmatch, gm)) return st;
     }
     if (b->plain_engine == AV_ENGINE_ROWS) {
         compile_rows(b->prog, c.channels, b->rprog);
@@ -650,6 +655,7 @@ static av_status step_k(av_batch_t b, int32_t k, const uint8_t *actions, float *
     a.L = c.max_episode_steps; a.per_env = c.per_env_rules; a.k = k;
     a.sequential = c.rule_mode == AV_RULES_SEQUENTIAL;
     a.row_bytes = b->row_bytes; a.max_pat_h = c.max_pat_h;
+    a.max_pat_w = c.max_pat_w;
     a.state = b->d_state; a.init = b->d_init; a.t = b->d_t; a.nctr = b->d_n;
     a.actions = actions; a.rewards = rewards; a.done = done;
     a.prog = b->dprog;

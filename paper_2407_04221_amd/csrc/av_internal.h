@@ -97,9 +97,12 @@ struct DeviceProgram {
     int32_t rules_per_set = 0, match_stride = 0, vote_stride = 0, rvote_stride = 0;
     int32_t any_reward = 0;           // some rule of some set pays a nonzero reward
     // group engine only (k_group.hip): per set, the probe table and the channel vote lists'
-    // rule ranges, gtab_stride words each
+    // rule ranges, gtab_stride words each, and the input entries merged per plane row,
+    // gmatch_stride words each
     uint32_t *gtab = nullptr;
     int32_t gtab_stride = 0;
+    uint32_t *gmatch = nullptr;
+    int32_t gmatch_stride = 0;
 };
 
 // Rule application control (paper Sec. 2.1.1): per loaded rule a cap on the matches applied
@@ -122,6 +125,7 @@ struct StepArgs {
     int32_t k;                       // steps in this launch
     int32_t row_bytes;
     int32_t max_pat_h = 1;           // largest pattern rows a loaded rule may have
+    int32_t max_pat_w = 1;           // largest pattern columns
     void *state;                     // [C][B][H] rows
     const void *init;                // [C][B][H] rows
     int32_t *t;                      // [B] step counters
@@ -257,9 +261,12 @@ hipError_t launch_rows_step(const StepArgs &a, const uint32_t *words, int set_wo
 // of lanes; parallel rule order, no rule application control.
 bool group_eligible(int H, int W, int C, int rules_per_set, int max_pat_h, int max_pat_w);
 // The group engine's per-set tables (probe rows of the loaded rules, rule ranges of the
-// channel vote lists) for maps of H x W, laid out as the kernel keeps them in LDS.
-void compile_group_tables(const GenericProgram &p, int H, int W, int C,
-                          std::vector<uint32_t> &tab, int &stride);
+// channel vote lists) for maps of H x W with patterns of up to max_pat_h rows, laid out as
+// the kernel keeps them in LDS, and its input entries merged per plane row (gm, gm_stride
+// words per set).
+void compile_group_tables(const GenericProgram &p, int H, int W, int C, int max_pat_h,
+                          std::vector<uint32_t> &tab, int &stride, std::vector<uint32_t> &gm,
+                          int &gm_stride);
 hipError_t launch_group_step(const StepArgs &a, hipStream_t s);
 
 // Wave slots of the current device (8 waves per SIMD, 4 SIMDs per CU; 0 if it cannot be

@@ -140,6 +140,7 @@ extern "C" av_status av_step_n_static(const av_config *cfg, int32_t num_rules,
     a.L = c.max_episode_steps; a.per_env = c.per_env_rules; a.k = k;
     a.sequential = c.rule_mode == AV_RULES_SEQUENTIAL;
     a.row_bytes = c.width <= 16 ? 2 : (c.width <= 32 ? 4 : 8); a.max_pat_h = c.max_pat_h;
+    a.max_pat_w = c.max_pat_w;
     a.state = state; a.init = init; a.t = counters;
     a.nctr = reinterpret_cast<uint64_t *>(p + o_n);
     a.actions = actions; a.rewards = rewards; a.done = done;

@@ -8,29 +8,29 @@
 // The four built-in moves are computed in registers from the lanes' own rows of the player,
 // wall and force planes and the rows next to them (DPP row shifts within 16-lane groups, DPP
 // shifts of the whole wave for 32-lane groups); the player and wall rows stay in registers from step to
-// step unless a loaded rule wrote those planes.  Each loaded rule's first four entries of its
-// rarest-first input list sit in a probe table (held in registers for the launch when a group
-// has at most two rules, else read at the start of each step), so the probe of every loaded
-// rule is one round of LDS reads with no branch between the rules; only rules that pass it
-// somewhere read the rest of their entries, and only channels that received votes are
+// step unless a loaded rule wrote those planes.  A rule's input entries are merged per plane
+// row (one LDS read tests every specified column of a pattern row, up to 8); each loaded
+// rule's first four merged entries sit in a probe table (held in registers for the launch when
+// a group has at most two rules, else read at the start of each step), so the probe of every
+// loaded rule is one round of LDS reads with no branch between the rules; only rules that
+// pass it somewhere read the rest of their entries, and only channels that received votes are
 // rewritten.
 //
 // LDS (32-bit rows):
-//   P    [C+2][PR]     the map, the force plane (channel C) and a zero plane (an entry that
-//                      always passes reads it); PR = Hq + ph - 1 rounded up to 4 rows (ph: the
-//                      largest pattern's rows), so a lane reads row y + i of any pattern entry
-//                      without a bounds test (rows H .. PR - 1 stay zero)
+//   P    [C+1][PR]     the map and the force plane (channel C); PR = Hq + ph - 1 rounded up to
+//                      4 rows (ph: the largest pattern's rows), so a lane reads row y + i of
+//                      any pattern entry without a bounds test (rows H .. PR - 1 stay zero)
 //   M    [R+4][PR]     match planes of the rules that fired, row y at ph - 1 + y: the zero rows
 //                      above let a vote read match row y - i without a test
 //   PL, MI [C][Hq]     per stored channel, the OR of the +1 and of the -1 votes
 //   I0   [C][Hq]       the initial rows, for resets
-//   PT   [R+5][12]     probe table: per loaded rule its first eight input entries, its
+//   PT   [R+5][12]     probe table: per loaded rule its first eight merged entries, its
 //                      anchor rows and columns and where its entries are (row R + 4: zeros,
 //                      read by groups with fewer rules than others)
 //   RS   [C][R+4]      per channel and rule, the range of the rule's votes in the channel's
 //                      vote list (for exact recounts)
 //   program            (when it fits, see the launcher) the environment's rule headers, input
-//                      entries, rule-major votes and channel-major vote lists
+//                      merged entries, rule-major votes and channel-major vote lists
 //
 // Per step (paper Sec. 2.1, Sec. 2.1.1, Sec. 2.2.1):
 //   force  F[y] = the player row moved one cell toward the action (group 0 writes it);
@@ -38,17 +38,19 @@
 //          F & ~W & P' (primes: the next row); their votes on the player plane are OR-ed in
 //          registers (-1 on the source cell, +1 on the target);
 //   match  per loaded rule, AND over its specified entries of plane row y + i shifted right by j,
-//          complemented for must-be-0, within the valid-anchor mask; a group leaves a rule as
-//          soon as no lane of the group has an anchor left;
+//          complemented for must-be-0, within the valid-anchor mask (the entries of one plane
+//          row i share its LDS read); a group leaves a rule as soon as no lane of the group has
+//          an anchor left;
 //   votes  a rule that fired stores its match plane and ORs match row y - i, shifted left by
 //          j, into the plus or minus row of each nonzero K_O = O - I entry's channel;
 //   write  group g rewrites channels g, g + G, ...: new = (old | plus) & ~minus where no cell
-//          got votes of both signs; a channel with such cells is recounted exactly with
-//          bit-sliced counters over every fired rule's votes: new = (old + #plus > #minus);
+//          got votes of both signs; a channel with such cells is recounted exactly with one
+//          bit-sliced counter over every fired rule's votes: new = (old + #plus > #minus);
 //   end    done when no player bit is left or the counter reaches L; reward = sum over fired
 //          rules of reward * popcount; done environments return to their initial rows.
 // Parallel rule order only, without rule application control.
 #include <algorithm>
+#include <type_traits>
 
 #include "av_internal.h"
 
@@ -57,12 +59,24 @@ namespace {
 
 constexpr int kMaxRulesPerGroup = 16;   // loaded and built-in rules per group, at most
 constexpr int kMaxChanPerGroup = 8;     // stored channels a group writes, at most
-constexpr int kCountBits = 8;           // votes of one sign a cell-channel can get: <= 255
-                                        // (eligibility: rules x pattern cells <= 255)
+constexpr int kCountBits = 8;           // exact write counters: a channel list holds <= 254
+                                        // entries (eligibility: rules x pattern cells <= 254)
 constexpr int kHdrWords = int(sizeof(RuleHdr) / 4);
 constexpr int kProbeEntries = 4;        // input entries of every rule tested in one round
 constexpr int kProbeWords = 12;         // probe table row: entries 0-3, anchor word, match
                                         // offset | count << 16, pad, pad, entries 4-7
+// Input entries merged per plane row: o | jb << 12 | care << 16 | want << 24 tests row
+// o + y of the planes (o = c * PR + i: pattern row i of plane c) at the pattern columns
+// 8 jb + j, j < 8, whose bit j of care is set: there the cell must equal bit j of want.
+// kPassEntry tests no column (it passes everywhere).
+constexpr uint32_t kPassEntry = 0u;
+constexpr int kMaxEntryOffset = 4095;
+
+// Words per plane row block: Hq rows plus the pattern rows hanging below the last one,
+// rounded up to 4 (16-byte aligned probe table after the planes).
+__host__ __device__ constexpr int group_plane_words(int Hq, int max_pat_h) {
+    return (Hq + max_pat_h - 1 + 3) & ~3;
+}
 
 __device__ inline uint32_t low_mask(int bits) { return bits >= 32 ? ~0u : ((1u << bits) - 1u); }
 
@@ -93,98 +107,102 @@ __device__ inline uint32_t prev_row(uint32_t v, int lane, int y) {
     return y > 0 ? u : 0u;
 }
 
-// Add the one-bit plane t to the bit-sliced counter cnt; the carry ripples only as far as some
-// lane of the group still carries.
-template <int Hq>
-__device__ inline void count_add(uint32_t (&cnt)[kCountBits], uint32_t t, int lane) {
+// Count the votes of rule r's channel-list entries lo .. hi - 1 (packed r | i << 8 | j << 16 |
+// plus << 24) into the KB-bit bit-sliced counter cnt: a plus vote adds its cells, a minus
+// vote adds the complement of its cells; nm counts the minus entries.  Four entries at a
+// time: carry-save adders make the four one-bit planes a 3-bit number, then one ripple add.
+template <int KB>
+__device__ inline void count_votes(uint32_t (&cnt)[KB], int &nm, const uint32_t *vl, int lo,
+                                   int hi, const uint32_t *Mr, int y, bool row) {
+    for (int ev = lo; ev < hi; ev += 4) {
+        uint32_t v[4], x[4];
 #pragma unroll
-    for (int k = 0; k < kCountBits; ++k) {
-        if (!group_any<Hq>(t != 0u, lane)) break;
-        const uint32_t carry = cnt[k] & t;
-        cnt[k] ^= t;
-        t = carry;
+        for (int u = 0; u < 4; ++u) v[u] = vl[min(ev + u, hi - 1)];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const uint32_t t = row ? Mr[y - int((v[u] >> 8) & 255u)] << ((v[u] >> 16) & 255u) : 0u;
+            const bool live = ev + u < hi, minus = live && !((v[u] >> 24) & 1u);
+            x[u] = !live ? 0u : minus ? ~t : t;
+            nm += minus ? 1 : 0;
+        }
+        const uint32_t a = x[0] ^ x[1], s1 = a ^ x[2];
+        const uint32_t c1 = (x[0] & x[1]) | (x[2] & a);            // weight 2
+        const uint32_t s0 = s1 ^ x[3], c2 = s1 & x[3];             // weight 1, 2
+        const uint32_t w2 = c1 ^ c2, w4 = c1 & c2;                 // weight 2, 4
+        uint32_t k = cnt[0] & s0;
+        cnt[0] ^= s0;
+        const uint32_t a1 = cnt[1] ^ w2;
+        const uint32_t k1 = (cnt[1] & w2) | (k & a1);
+        cnt[1] = a1 ^ k;
+        const uint32_t a2 = cnt[2] ^ w4;
+        k = (cnt[2] & w4) | (k1 & a2);
+        cnt[2] = a2 ^ k1;
+#pragma unroll
+        for (int q = 3; q < KB; ++q) {
+            const uint32_t kq = cnt[q] & k;
+            cnt[q] ^= k;
+            k = kq;
+        }
     }
 }
 
 // The exact write of channel c for this lane's row (needed only where some cell of the group
-// got votes of both signs): counts the votes on c of every rule in `fired` (the channel's vote
-// list `vl`, packed r | i << 8 | j << 16 | plus << 24 and ordered by rule; rule r's votes are
-// vl[rsc[r] & 0xFFFF .. rsc[r] >> 16)) with the old value as a plus vote, and
-// returns the cells where old + #plus > #minus, i.e. old + sum of votes >= 1.  Counts are
-// 4-bit planes per sign; only if some cell of the group reaches 16 votes of one sign are they
-// recounted with kCountBits-bit counters.
-template <int Hq>
+// got votes of both signs): the votes on c of every rule in `fired` (the channel's vote list
+// `vl`, ordered by rule; rule r's entries are vl[rsc[r] & 0xFFFF .. rsc[r] >> 16)) with the old
+// value as a plus vote.  One counter takes old + #plus + (#minus entries - #minus votes), so a
+// cell is set, old + #plus - #minus >= 1, where it reaches 1 + #minus entries.  A list holds
+// at most 254 entries (eligibility: every entry is a distinct rule and pattern cell), so
+// 8-bit counters never overflow; 4 bits do when the fired rules' entries are at most 14.
 __device__ inline uint32_t exact_channel(uint32_t old, uint64_t fired, const uint32_t *vl,
                                          const uint32_t *rsc, const uint32_t *M, int MS, int pad,
-                                         int y, bool row, int lane) {
-    uint32_t pc[4] = {row ? old : 0u, 0u, 0u, 0u}, nc[4] = {0u, 0u, 0u, 0u};
-    uint32_t ovf = 0u;
+                                         int y, bool row) {
+    int total = 0;
     for (uint64_t fr = fired; fr; fr &= fr - 1) {
-        const int r = __builtin_ctzll(fr);
-        const uint32_t rs = rsc[r];
-        const int lo = int(rs & 0xFFFFu), hi = int(rs >> 16);
-        for (int ev = lo; ev < hi; ev += 4) {
-            uint32_t v[4], t[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) v[u] = vl[min(ev + u, hi - 1)];
-#pragma unroll
-            for (int u = 0; u < 4; ++u)
-                t[u] = (row && ev + u < hi)
-                           ? M[r * MS + pad + y - int((v[u] >> 8) & 255u)] << ((v[u] >> 16) & 255u)
-                           : 0u;
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                const bool plus = (v[u] >> 24) & 1u;
-                uint32_t xp = plus ? t[u] : 0u, xn = plus ? 0u : t[u];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const uint32_t cp = pc[q] & xp, cn = nc[q] & xn;
-                    pc[q] ^= xp;
-                    nc[q] ^= xn;
-                    xp = cp;
-                    xn = cn;
-                }
-                ovf |= xp | xn;
-            }
-        }
+        const uint32_t rs = rsc[__builtin_ctzll(fr)];
+        total += int(rs >> 16) - int(rs & 0xFFFFu);
     }
-    if (!group_any<Hq>(ovf != 0u, lane)) {
-        uint32_t gt = 0u, eq = ~0u;
-#pragma unroll
-        for (int q = 3; q >= 0; --q) {
-            gt |= eq & pc[q] & ~nc[q];
-            eq &= ~(pc[q] ^ nc[q]);
-        }
-        return gt;
-    }
-    uint32_t pw[kCountBits], nw[kCountBits];
-#pragma unroll
-    for (int u = 0; u < kCountBits; ++u) pw[u] = nw[u] = 0u;
-    count_add<Hq>(pw, row ? old : 0u, lane);
-    for (uint64_t fr = fired; fr; fr &= fr - 1) {
-        const int r = __builtin_ctzll(fr);
-        const uint32_t rs = rsc[r];
-        for (int ev = int(rs & 0xFFFFu); ev < int(rs >> 16); ++ev) {
-            const uint32_t v = vl[ev];
-            const uint32_t t = row ? M[r * MS + pad + y - int((v >> 8) & 255u)] << ((v >> 16) & 255u)
-                                   : 0u;
-            const bool plus = (v >> 24) & 1u;
-            count_add<Hq>(pw, plus ? t : 0u, lane);
-            count_add<Hq>(nw, plus ? 0u : t, lane);
-        }
-    }
+    const uint32_t o = row ? old : 0u;
+    int nm = 0;
     uint32_t gt = 0u, eq = ~0u;
+    auto ge = [&](auto &cnt, auto kb) {           // cnt >= 1 + nm, bit-sliced
+        constexpr int KB = decltype(kb)::value;
+        const uint32_t T = uint32_t(1 + nm);
 #pragma unroll
-    for (int u = kCountBits - 1; u >= 0; --u) {
-        gt |= eq & pw[u] & ~nw[u];
-        eq &= ~(pw[u] ^ nw[u]);
+        for (int q = KB - 1; q >= 0; --q) {
+            const uint32_t tb = ((T >> q) & 1u) ? ~0u : 0u;
+            gt |= eq & cnt[q] & ~tb;
+            eq &= ~(cnt[q] ^ tb);
+        }
+    };
+    if (total <= 14) {
+        uint32_t cnt[4] = {o, 0u, 0u, 0u};
+        for (uint64_t fr = fired; fr; fr &= fr - 1) {
+            const int r = __builtin_ctzll(fr);
+            const uint32_t rs = rsc[r];
+            count_votes<4>(cnt, nm, vl, int(rs & 0xFFFFu), int(rs >> 16), M + r * MS + pad, y,
+                           row);
+        }
+        ge(cnt, std::integral_constant<int, 4>{});
+    } else {
+        uint32_t cnt[kCountBits] = {o, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+        for (uint64_t fr = fired; fr; fr &= fr - 1) {
+            const int r = __builtin_ctzll(fr);
+            const uint32_t rs = rsc[r];
+            count_votes<kCountBits>(cnt, nm, vl, int(rs & 0xFFFFu), int(rs >> 16),
+                                    M + r * MS + pad, y, row);
+        }
+        ge(cnt, std::integral_constant<int, kCountBits>{});
     }
-    return gt;
+    return gt | eq;
 }
 
 // NR: rules a group holds (a bound on this launch's ceil(R / G)).
-template <int Hq, int NR>
-__global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, int prog_lds) {
+// NJ: columns a merged entry tests (3 when no pattern is wider, else 8).
+// PROG_LDS: the rule program is copied to LDS.  A compile-time choice, so that the program's
+// reads are LDS reads or global loads: a pointer that may be either makes every read a flat
+// load, which the LDS reads' waits then wait for as well.
+template <int Hq, int NR, int NJ, bool PROG_LDS>
+__global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
     constexpr int G = 64 / Hq;
     constexpr int kChunk = 4;                 // entries or votes of a rule read in one round
     extern __shared__ __align__(16) uint32_t lds[];
@@ -194,33 +212,33 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
     // pattern rows beyond a lane's row: plane rows y + i and match rows y - i, i <= PAD, are
     // read without a bounds test; rows of 4 words keep the probe table 16-byte aligned
     const int PAD = a.max_pat_h - 1;
-    const int PR = (Hq + PAD + 3) & ~3, MS = PR;
+    const int PR = group_plane_words(Hq, a.max_pat_h), MS = PR;
     const int s = a.per_env ? b : 0;
     const bool row = y < H;
     const int ry = row ? y : 0;
     const uint32_t wmask = low_mask(W);
 
-    uint32_t *P = lds;                             // [C1 + 1][PR]
-    uint32_t *M = P + (C1 + 1) * PR;               // [Rt][MS]
+    uint32_t *P = lds;                             // [C1][PR]
+    uint32_t *M = P + C1 * PR;                     // [Rt][MS]
     uint32_t *PL = M + Rt * MS;                    // [C][Hq]
     uint32_t *MI = PL + C * Hq;                    // [C][Hq]
     uint32_t *I0 = MI + C * Hq;                    // [C][Hq] initial rows
     uint32_t *PT = I0 + C * Hq;                    // [Rt + 1][kProbeWords] probe table
     uint32_t *RS = PT + (Rt + 1) * kProbeWords;    // [C][Rt] rule ranges of channel lists
-    uint32_t *lprog = RS + C * Rt;                 // program copy (prog_lds)
+    uint32_t *lprog = RS + C * Rt;                 // program copy (PROG_LDS)
 
     const uint32_t *ghdr = reinterpret_cast<const uint32_t *>(a.prog.hdr + size_t(s) * Rt);
-    const uint32_t *gment = a.prog.match + size_t(s) * a.prog.match_stride;
+    const uint32_t *gment = a.prog.gmatch + size_t(s) * a.prog.gmatch_stride;
     const uint32_t *gvent = a.prog.rvote + size_t(s) * a.prog.rvote_stride;
     const uint32_t *gvl = reinterpret_cast<const uint32_t *>(a.prog.votes + size_t(s) * C1);
     const uint32_t *gvote = a.prog.vote + size_t(s) * a.prog.vote_stride;
     const int hdr_words = Rt * kHdrWords;
     const uint32_t *hdrw = ghdr, *ment = gment, *vent = gvent, *vlw = gvl, *vote = gvote;
-    if (prog_lds) {
-        uint32_t *ph = lprog, *pm = ph + hdr_words, *pv = pm + a.prog.match_stride;
+    if constexpr (PROG_LDS) {
+        uint32_t *ph = lprog, *pm = ph + hdr_words, *pv = pm + a.prog.gmatch_stride;
         uint32_t *pl = pv + a.prog.rvote_stride, *pc = pl + 2 * C1;
         for (int w = lane; w < hdr_words; w += 64) ph[w] = ghdr[w];
-        for (int w = lane; w < a.prog.match_stride; w += 64) pm[w] = gment[w];
+        for (int w = lane; w < a.prog.gmatch_stride; w += 64) pm[w] = gment[w];
         for (int w = lane; w < a.prog.rvote_stride; w += 64) pv[w] = gvent[w];
         for (int w = lane; w < 2 * C1; w += 64) pl[w] = gvl[w];
         for (int w = lane; w < a.prog.vote_stride; w += 64) pc[w] = gvote[w];
@@ -231,7 +249,7 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
         vote = pc;
     }
     {
-        const int words = (C1 + 1) * PR + Rt * MS + 3 * C * Hq;   // (PT and RS are copied)
+        const int words = C1 * PR + Rt * MS + 3 * C * Hq;   // (PT and RS are copied)
         for (int w = lane; w < words; w += 64) lds[w] = 0u;
     }
 
@@ -257,11 +275,26 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
     int t_env = a.t[b];
     const uint64_t nbase = a.nctr[b];
 
-    // entry e (packed c | i << 8 | j << 16 | want << 24) at this lane's row: 1 where the plane
-    // row y + i, moved right by j, holds the wanted value
-    auto entry = [&](uint32_t e) {
-        const uint32_t v = P[int(e & 255u) * PR + ry + int((e >> 8) & 255u)] >> ((e >> 16) & 255u);
-        return ((e >> 24) & 1u) ? v : ~v;
+    // entry e (merged per plane row) at this lane's row: OR-s into bad the anchors where a
+    // tested column does not hold the wanted value (the row moved right by the column's
+    // offset); a column's care and want bits sign-extended are all-ones masks
+    auto miss = [&](uint32_t e, uint32_t &bad) {
+        uint32_t v = P[int(e & uint32_t(kMaxEntryOffset)) + ry];
+        if constexpr (NJ > 3) v >>= (e >> 9) & 24u;
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            const uint32_t want = uint32_t(int32_t(e << (7 - j)) >> 31);
+            const uint32_t care = uint32_t(int32_t(e << (15 - j)) >> 31);
+            bad |= ((v >> j) ^ want) & care;
+        }
+    };
+    auto entries4 = [&](uint32_t e0, uint32_t e1, uint32_t e2, uint32_t e3) {
+        uint32_t bad = 0u;
+        miss(e0, bad);
+        miss(e1, bad);
+        miss(e2, bad);
+        miss(e3, bad);
+        return ~bad;
     };
 
     uint32_t ablk = 0u;     // lane l: action of step k0 + l of the current block of 64
@@ -359,7 +392,7 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
 #pragma unroll
         for (int kr = 0; kr < NR; ++kr) {
             const uint32_t vm = (kr < nr && y < int(pv[kr] >> 8)) ? ~0u >> (pv[kr] & 255u) : 0u;
-            mk[kr] = vm & entry(pe[kr].x) & entry(pe[kr].y) & entry(pe[kr].z) & entry(pe[kr].w);
+            mk[kr] = vm & entries4(pe[kr].x, pe[kr].y, pe[kr].z, pe[kr].w);
         }
         uint32_t cand = 0u;
 #pragma unroll
@@ -370,8 +403,8 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
 
         // candidates: the rest of their input entries four at a time.  With up to four rules per
         // group, in rounds in which every candidate of every group takes its next four (a lane
-        // only while it still holds an anchor of the rule; otherwise it reads the zero plane,
-        // which changes nothing); with more, one rule after another, the next four entries
+        // only while it still holds an anchor of the rule; otherwise the pass entry, which
+        // tests nothing); with more, one rule after another, the next four entries
         // read while the current ones' plane rows are (rounds would issue every rule's reads
         // while most rules are done, and four waves share each CU's LDS there).  A rule is done
         // when its entries run out or its lanes have no anchor left.
@@ -398,22 +431,22 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
                         const bool live = mk[kr] != 0u && e < cnt;
                         if (NR <= 2 && e == kProbeEntries) {   // entries 4 .. 7: in registers
                             const uint4 q = pe2[kr];
-                            x[kr][0] = live ? q.x : uint32_t(C1);
-                            x[kr][1] = live ? q.y : uint32_t(C1);
-                            x[kr][2] = live ? q.z : uint32_t(C1);
-                            x[kr][3] = live ? q.w : uint32_t(C1);
+                            x[kr][0] = live ? q.x : kPassEntry;
+                            x[kr][1] = live ? q.y : kPassEntry;
+                            x[kr][2] = live ? q.z : kPassEntry;
+                            x[kr][3] = live ? q.w : kPassEntry;
                             continue;
                         }
 #pragma unroll
                         for (int u = 0; u < 4; ++u) {
                             // past the last entry the last one again (AND is idempotent)
                             const uint32_t w = ment[live ? off + min(e + u, cnt - 1) : 0];
-                            x[kr][u] = live ? w : uint32_t(C1);
+                            x[kr][u] = live ? w : kPassEntry;
                         }
                     }
 #pragma unroll
                     for (int kr = 0; kr < NR; ++kr)
-                        mk[kr] &= entry(x[kr][0]) & entry(x[kr][1]) & entry(x[kr][2]) & entry(x[kr][3]);
+                        mk[kr] &= entries4(x[kr][0], x[kr][1], x[kr][2], x[kr][3]);
                 }
             } else {
 #pragma unroll
@@ -424,7 +457,7 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
                     const uint32_t *en = ment + int(meta[kr] & 0xFFFFu);
                     const int cnt = int(meta[kr] >> 16), last = cnt - 1;
                     int e = kProbeEntries;
-                    uint32_t x[4] = {uint32_t(C1), uint32_t(C1), uint32_t(C1), uint32_t(C1)};
+                    uint32_t x[4] = {kPassEntry, kPassEntry, kPassEntry, kPassEntry};
                     if (e < cnt) {                // (reads stay inside the rule's entries)
 #pragma unroll
                         for (int u = 0; u < 4; ++u) x[u] = en[min(e + u, last)];
@@ -438,7 +471,7 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
 #pragma unroll
                             for (int u = 0; u < 4; ++u) x[u] = en[min(e + u, last)];
                         }
-                        m &= entry(cur[0]) & entry(cur[1]) & entry(cur[2]) & entry(cur[3]);
+                        m &= entries4(cur[0], cur[1], cur[2], cur[3]);
                     }
                     mk[kr] = m;
                 }
@@ -528,8 +561,8 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
                 if (c == kChPlayer && !lv)
                     nw = pnew;                    // only the moves voted on it
                 else if (group_any<Hq>((pl & mi) != 0u, lane))
-                    nw = exact_channel<Hq>(old, fired_all, vote + int(vlw[2 * c]),
-                                           RS + c * Rt, M, MS, PAD, y, row, lane);
+                    nw = exact_channel(old, fired_all, vote + int(vlw[2 * c]), RS + c * Rt, M,
+                                       MS, PAD, y, row);
                 if (row) P[c * PR + y] = nw;
                 if (c == kChPlayer) pl_any = row && nw != 0u;
                 if (lv) {
@@ -594,8 +627,8 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a, in
 int group_lanes(int H) { return H <= 16 ? 16 : 32; }
 
 size_t group_lds_bytes(int H, int C, int rules_per_set, int max_pat_h) {
-    const int Hq = group_lanes(H), PR = (Hq + max_pat_h - 1 + 3) & ~3;
-    return sizeof(uint32_t) * (size_t(C + 2) * PR + size_t(rules_per_set) * PR +
+    const int Hq = group_lanes(H), PR = group_plane_words(Hq, max_pat_h);
+    return sizeof(uint32_t) * (size_t(C + 1) * PR + size_t(rules_per_set) * PR +
                                size_t(3) * C * Hq + size_t(rules_per_set + 1) * kProbeWords +
                                size_t(C) * rules_per_set);
 }
@@ -606,36 +639,63 @@ bool group_eligible(int H, int W, int C, int rules_per_set, int max_pat_h, int m
     // counts of the exact write hold them (plus the old value) when there are at most 255
     if (long(rules_per_set) * max_pat_h * max_pat_w > 254) return false;
     const int G = 64 / group_lanes(H);
+    // (merged entries address rows of the stored and force planes in 12 bits)
     return rules_per_set <= kMaxRulesPerGroup * G && rules_per_set <= 64 &&
            C <= kMaxChanPerGroup * G &&
+           (C + 1) * group_plane_words(group_lanes(H), max_pat_h) <= kMaxEntryOffset + 1 &&
            group_lds_bytes(H, C, rules_per_set, max_pat_h) <= size_t(kLdsBudget);
 }
 
-void compile_group_tables(const GenericProgram &p, int H, int W, int C,
-                          std::vector<uint32_t> &tab, int &stride) {
+// A rule's input entries (c | i << 8 | j << 16 | want << 24, rarest first) merged per plane
+// row and block of 8 columns, in the order of each row's first entry.
+static std::vector<uint32_t> merge_entries(const uint32_t *ent, int cnt, int PR) {
+    std::vector<uint32_t> key, out;               // key: c | i << 8 | jb << 16
+    for (int e = 0; e < cnt; ++e) {
+        const uint32_t c = ent[e] & 255u, i = (ent[e] >> 8) & 255u, j = (ent[e] >> 16) & 255u;
+        const uint32_t k = c | (i << 8) | ((j >> 3) << 16), bit = 1u << (j & 7u);
+        size_t q = 0;
+        while (q < key.size() && key[q] != k) ++q;
+        if (q == key.size()) {                    // no column tested yet
+            key.push_back(k);
+            out.push_back((c * uint32_t(PR) + i) | ((j >> 3) << 12));
+        }
+        out[q] |= bit << 16;                      // column tested
+        if ((ent[e] >> 24) & 1u) out[q] |= bit << 24;   // must be 1
+    }
+    return out;
+}
+
+void compile_group_tables(const GenericProgram &p, int H, int W, int C, int max_pat_h,
+                          std::vector<uint32_t> &tab, int &stride, std::vector<uint32_t> &gm,
+                          int &gm_stride) {
     const int Rt = p.rules_per_set, C1 = C + 1;
+    const int PR = group_plane_words(group_lanes(H), max_pat_h);
     stride = (Rt + 1) * kProbeWords + C * Rt;
     tab.assign(size_t(p.sets) * stride, 0u);
+    std::vector<std::vector<uint32_t>> merged(p.sets);
+    gm_stride = 1;
     for (int s = 0; s < p.sets; ++s) {
         uint32_t *pt = tab.data() + size_t(s) * stride, *rs = pt + (Rt + 1) * kProbeWords;
-        // probe rows of the loaded rules: the first four input entries (rarest first; a
-        // missing one always passes: must-be-0 on the zero plane C + 1) and the anchors,
-        // columns 0 .. W - m (~0 >> (32 - (W - m + 1))) of rows 0 .. H - n
+        // probe rows of the loaded rules: the first four merged entries (a missing one always
+        // passes) and the anchors, columns 0 .. W - m (~0 >> (32 - (W - m + 1))) of rows
+        // 0 .. H - n
         for (int r = kMoveRules; r < Rt; ++r) {
             const RuleHdr &h = p.hdr[size_t(s) * Rt + r];
-            const uint32_t *ent = p.match.data() + size_t(s) * p.match_stride + h.match_off;
+            const std::vector<uint32_t> ent = merge_entries(
+                p.match.data() + size_t(s) * p.match_stride + h.match_off, h.match_cnt, PR);
+            const int off = int(merged[s].size()), cnt = int(ent.size());
+            merged[s].insert(merged[s].end(), ent.begin(), ent.end());
             uint32_t *row = pt + r * kProbeWords;
-            for (int e = 0; e < kProbeEntries; ++e)
-                row[e] = e < h.match_cnt ? ent[e] : uint32_t(C1);
+            for (int e = 0; e < kProbeEntries; ++e) row[e] = e < cnt ? ent[e] : kPassEntry;
             const int cols = W - h.m + 1, rows = H - h.n + 1;
             row[4] = (cols >= 1 && rows >= 1) ? uint32_t(32 - cols) | (uint32_t(rows) << 8) : 0u;
-            row[5] = uint32_t(h.match_off) | (uint32_t(h.match_cnt) << 16);
-            // entries 4 .. 7 (past the last, the last again; none: the zero plane)
+            row[5] = uint32_t(off) | (uint32_t(cnt) << 16);
+            // entries 4 .. 7 (past the last, the last again; none: the pass entry)
             for (int e = 0; e < 4; ++e)
-                row[8 + e] = h.match_cnt > kProbeEntries
-                                 ? ent[std::min(kProbeEntries + e, h.match_cnt - 1)]
-                                 : uint32_t(C1);
+                row[8 + e] = cnt > kProbeEntries ? ent[std::min(kProbeEntries + e, cnt - 1)]
+                                                 : kPassEntry;
         }
+        gm_stride = std::max(gm_stride, int(merged[s].size()));
         // rule ranges of the channel vote lists (each ordered by rule): first | end << 16
         for (int c = 0; c < C; ++c) {
             const VoteList &vl = p.votes[size_t(s) * C1 + c];
@@ -648,34 +708,49 @@ void compile_group_tables(const GenericProgram &p, int H, int W, int C,
             }
         }
     }
+    gm.assign(size_t(p.sets) * gm_stride, kPassEntry);
+    for (int s = 0; s < p.sets; ++s)
+        std::copy(merged[s].begin(), merged[s].end(), gm.begin() + size_t(s) * gm_stride);
 }
 
 namespace {
-template <int Hq>
-void launch_hq(const StepArgs &a, size_t lds, int prog_lds, hipStream_t s) {
+template <int Hq, int NJ, bool PROG_LDS>
+void launch_nr(const StepArgs &a, size_t lds, hipStream_t s) {
     constexpr int G = 64 / Hq;
     const int nrmax = (a.prog.rules_per_set - kMoveRules + G - 1) / G;
-    if (nrmax <= 2) hipLaunchKernelGGL((group_step<Hq, 2>), dim3(a.B), dim3(64), lds, s, a, prog_lds);
-    else if (nrmax <= 4) hipLaunchKernelGGL((group_step<Hq, 4>), dim3(a.B), dim3(64), lds, s, a, prog_lds);
-    else if (nrmax <= 8) hipLaunchKernelGGL((group_step<Hq, 8>), dim3(a.B), dim3(64), lds, s, a, prog_lds);
-    else if (nrmax <= 12) hipLaunchKernelGGL((group_step<Hq, 12>), dim3(a.B), dim3(64), lds, s, a, prog_lds);
-    else hipLaunchKernelGGL((group_step<Hq, 16>), dim3(a.B), dim3(64), lds, s, a, prog_lds);
+    const dim3 grid(a.B), block(64);
+    if (nrmax <= 2) hipLaunchKernelGGL((group_step<Hq, 2, NJ, PROG_LDS>), grid, block, lds, s, a);
+    else if (nrmax <= 4) hipLaunchKernelGGL((group_step<Hq, 4, NJ, PROG_LDS>), grid, block, lds, s, a);
+    else if (nrmax <= 8) hipLaunchKernelGGL((group_step<Hq, 8, NJ, PROG_LDS>), grid, block, lds, s, a);
+    else if (nrmax <= 12) hipLaunchKernelGGL((group_step<Hq, 12, NJ, PROG_LDS>), grid, block, lds, s, a);
+    else hipLaunchKernelGGL((group_step<Hq, 16, NJ, PROG_LDS>), grid, block, lds, s, a);
+}
+template <int Hq, int NJ>
+void launch_hq(const StepArgs &a, size_t lds, bool prog_lds, hipStream_t s) {
+    if (prog_lds) launch_nr<Hq, NJ, true>(a, lds, s);
+    else launch_nr<Hq, NJ, false>(a, lds, s);
 }
 }  // namespace
 
 hipError_t launch_group_step(const StepArgs &a, hipStream_t s) {
     const size_t base = group_lds_bytes(a.H, a.C, a.prog.rules_per_set, a.max_pat_h);
     const size_t prog = sizeof(uint32_t) * (size_t(a.prog.rules_per_set) * kHdrWords +
-                                            a.prog.match_stride + a.prog.rvote_stride +
+                                            a.prog.gmatch_stride + a.prog.rvote_stride +
                                             2 * (a.C + 1) + a.prog.vote_stride);
     // the program goes to LDS for launches of 16 steps or more, when it fits and leaves room
     // for as many waves per CU (160 KiB of LDS) as the batch can use, up to 16 (4 per SIMD)
     const size_t need = size_t(std::min(16, (a.B + 255) / 256));
-    const int prog_lds = a.k >= 16 && base + prog <= size_t(kLdsBudget) &&
-                         (base + prog) * need <= size_t(160) * 1024 ? 1 : 0;
+    const size_t budget = std::min(size_t(kLdsBudget), size_t(160) * 1024 / need);
+    const bool prog_lds = a.k >= 16 && base + prog <= budget;
     const size_t lds = base + (prog_lds ? prog : 0);
-    if (group_lanes(a.H) == 16) launch_hq<16>(a, lds, prog_lds, s);
-    else launch_hq<32>(a, lds, prog_lds, s);
+    const bool narrow = a.max_pat_w <= 3;
+    if (group_lanes(a.H) == 16) {
+        if (narrow) launch_hq<16, 3>(a, lds, prog_lds, s);
+        else launch_hq<16, 8>(a, lds, prog_lds, s);
+    } else {
+        if (narrow) launch_hq<32, 3>(a, lds, prog_lds, s);
+        else launch_hq<32, 8>(a, lds, prog_lds, s);
+    }
     return hipGetLastError();
 }
 

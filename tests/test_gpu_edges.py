@@ -41,6 +41,9 @@ CASES = {
     # 4 x 4 (three pad rows under the planes), per-environment rules
     "mid24x20": W_("mid24x20", 59, B=11, H=24, W=20, C=7, R=9,
                    shapes=((4, 4), (1, 3), (2, 1)), per_env=True, T=14),
+    # patterns wider than 8 columns (the group engine tests a plane row in blocks of 8)
+    "wide_pat": W_("wide_pat", 60, B=9, H=12, W=24, C=5, R=3, shapes=((1, 13), (2, 9)),
+                   per_env=True, T=14),
 }
 LANE16 = {n for n, w in CASES.items() if w.H <= 16 and w.W <= 16 and not w.per_env}
 
@@ -156,15 +159,17 @@ def test_vote_counts_beyond_4096(engine):
     check(wl, maps, (shape, ip, op, rw), actions, engine)
 
 
+@pytest.mark.parametrize("shape", [(3, 3), (1, 3), (1, 7)])
 @pytest.mark.parametrize("rules_per_sign", [1, 2])
 @pytest.mark.parametrize("engine", ["group", "wave", "generic"])
-def test_overlapping_votes_of_both_signs(engine, rules_per_sign):
-    """All-don't-care 3 x 3 rules, half voting +1 and half -1 on the goal plane: a cell away
-    from the edges gets 9 votes of each sign per rule, so every cell needs an exact count;
-    with two rules per sign the counts reach 18, beyond 4-bit counters."""
+def test_overlapping_votes_of_both_signs(engine, rules_per_sign, shape):
+    """All-don't-care n x m rules, half voting +1 and half -1 on the goal plane: a cell away
+    from the edges gets n m votes of each sign per rule, so every cell needs an exact count.
+    The rules' vote entries on the plane number 6 (1 x 3, one rule per sign), 12, 14 (1 x 7:
+    counts up to 15, the most 4-bit counters hold), 18, 28 and 36 (beyond 4 bits)."""
     require_gpu()
     R = 2 * rules_per_sign
-    wl = W_("both", 58, B=7, H=12, W=15, C=5, R=R, shapes=((3, 3),), T=4, L=0)
+    wl = W_("both", 58, B=7, H=12, W=15, C=5, R=R, shapes=(shape,), T=4, L=0)
     maps, (shape, ip, op, rw), actions = inputs.make_all(wl, 0, "literal")
     ip[:] = -1
     op[:] = -1
