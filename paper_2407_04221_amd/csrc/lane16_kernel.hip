@@ -86,7 +86,12 @@ av_lane16_step(unsigned short *__restrict__ state, const unsigned short *__restr
                const unsigned short *__restrict__ gsrc, int gnf, int gA,
                const int *__restrict__ gdepth) {
     const int lane = threadIdx.x & 63;
-    const int wave = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
+    // Workgroups are dealt to the GPU's 8 XCDs (each with its own L2) in turn: number them so
+    // that each XCD takes one contiguous run of environments, whose result rows share cache
+    // lines (a bijection for any grid size).
+    const unsigned xg = blockIdx.x, xcd = xg % 8u, xq = gridDim.x / 8u, xr = gridDim.x % 8u;
+    const unsigned block = xcd * xq + (xcd < xr ? xcd : xr) + xg / 8u;
+    const int wave = int((block * blockDim.x + threadIdx.x) >> 6);
     const int y = lane & 15;
     const int eA = 2 * (wave * 4 + (lane >> 4));
     const int eB = eA + 1;
