@@ -87,7 +87,11 @@ typedef enum {
                                g + 4 (or g + 2), ...; input entries are merged per pattern
                                row, every rule's first four merged entries are tested in one
                                round of LDS reads, and only rules that pass somewhere read the
-                               rest.  Needs parallel rule order, H, W <= 32,
+                               rest.  After launches of 64 steps or more it measures each
+                               environment's cycles and deals environments to workgroups so that
+                               the slowest ones do not share a SIMD (results never depend on
+                               the order; not while the stream is captured).  Needs parallel
+                               rule order, H, W <= 32,
                                (max_rules + 4) x max_pat_h x max_pat_w <= 254, at most 8
                                channels per lane group and, within 64 KiB of LDS, C + 1 planes
                                and R + 4 match planes of Hq + max_pat_h - 1 rows (rounded up to

@@ -8,6 +8,8 @@
 
 #include <algorithm>
 #include <cstdarg>
+#include <numeric>
+#include <queue>
 #include <cstdio>
 #include <cstring>
 #include <new>
@@ -77,6 +79,15 @@ struct av_batch_s {
     Lane16Program lprog_ctl;       // lane16 program with rule application control compiled in
     Lane16Device dlprog_ctl;
     bool lane16_ctl = false;       // steps use dlprog_ctl
+    // group engine: which environment each workgroup steps, and the cycles each environment
+    // took in a launch (device arrays; host copies in pinned memory, filled after launches)
+    int32_t *d_order = nullptr;
+    uint32_t *d_cost = nullptr;
+    int32_t *h_order = nullptr;
+    uint32_t *h_cost = nullptr;
+    hipEvent_t cost_ev = nullptr;  // recorded after the copy of d_cost to h_cost
+    bool cost_pending = false;     // that copy is queued and its costs not used yet
+    int simds = 0;                 // SIMDs of the device
 };
 
 namespace {
@@ -286,6 +297,29 @@ av_status upload(T **dst, const std::vector<T> &src) {
     return AV_OK;
 }
 
+// The group engine's order and cost arrays, once per batch: workgroup i starts on
+// environment i; a step reorders them (group_order_update).
+av_status group_order_init(av_batch_t b) {
+    const int B = b->cfg.num_envs;
+    if (b->d_order) {
+        b->cost_pending = false;                  // costs of another rule set
+        std::iota(b->h_order, b->h_order + B, 0);
+        AV_HIP(hipMemcpy(b->d_order, b->h_order, sizeof(int32_t) * size_t(B), hipMemcpyHostToDevice));
+        return AV_OK;
+    }
+    int cus = 0;
+    AV_HIP(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, b->cfg.device));
+    b->simds = 4 * cus;                           // 4 SIMDs per CU
+    AV_HIP(hipHostMalloc(reinterpret_cast<void **>(&b->h_order), sizeof(int32_t) * size_t(B)));
+    AV_HIP(hipHostMalloc(reinterpret_cast<void **>(&b->h_cost), sizeof(uint32_t) * size_t(B)));
+    AV_HIP(hipEventCreateWithFlags(&b->cost_ev, hipEventDisableTiming));
+    std::vector<int32_t> ident(static_cast<size_t>(B));
+    std::iota(ident.begin(), ident.end(), 0);
+    std::copy(ident.begin(), ident.end(), b->h_order);
+    if (av_status st = upload(&b->d_order, ident)) return st;
+    return upload(&b->d_cost, std::vector<uint32_t>(size_t(B), 0u));
+}
+
 // Copies of the batch step number: one per launch unit (at most one per environment, and
 // the lane16 engine's last workgroup may hold up to three waves past the batch), plus slack.
 int step_copies(int B) { return B + 8; }
@@ -489,6 +523,7 @@ av_status av_load_rules(av_batch_t b, int32_t R, const int32_t *shape, const int
                              b->dprog.gtab_stride, gm, b->dprog.gmatch_stride);
         if (av_status st = upload(&b->dprog.gtab, tab)) return st;
         if (av_status st = upload(&b->dprog.gmatch, gm)) return st;
+        if (av_status st = group_order_init(b)) return st;
     }
     if (b->plain_engine == AV_ENGINE_ROWS) {
         compile_rows(b->prog, c.channels, b->rprog);
@@ -641,6 +676,60 @@ av_status av_set_rule_control(av_batch_t b, const int32_t *limit, const uint8_t 
     return AV_OK;
 }
 
+// Group engine: the order in which workgroups take environments.  With several waves per SIMD,
+// workgroups i, i + P, i + 2P, ... (P: the device's SIMDs) share a SIMD, and a launch lasts as
+// long as its slowest SIMD.  An environment's steps cost about the same from launch to launch
+// (its rule set does not change), so, from the cycles each took in an earlier launch of 64
+// steps or more, environments are dealt slowest first, each to the SIMD with the least work so
+// far among those with a workgroup left (longest processing time first): the P slowest get a
+// SIMD each, and the slowest one's SIMD gets the lightest of the rest.  Results do not depend
+// on the order.  The
+// costs come back through an asynchronous copy; a launch uses them once that copy is done,
+// and never while the stream is being captured.
+constexpr int kGroupOrderMinSteps = 64;
+
+static bool capturing(hipStream_t s) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    return hipStreamIsCapturing(s, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone;
+}
+
+static hipError_t group_order_update(av_batch_t b, int k) {
+    if (!b->d_order || k < kGroupOrderMinSteps || !b->cost_pending || capturing(b->stream))
+        return hipSuccess;
+    if (hipEventQuery(b->cost_ev) != hipSuccess) return hipSuccess;   // not back yet
+    b->cost_pending = false;
+    const int B = b->cfg.num_envs, P = b->simds;
+    if (B <= P) return hipSuccess;
+    std::vector<int> idx(static_cast<size_t>(B));
+    std::iota(idx.begin(), idx.end(), 0);
+    std::stable_sort(idx.begin(), idx.end(),
+                     [&](int x, int y) { return b->h_cost[x] > b->h_cost[y]; });
+    // SIMD j holds workgroups j, j + P, ...: (work so far, j) of the SIMDs with one left
+    std::vector<int> used(static_cast<size_t>(P), 0);
+    std::priority_queue<std::pair<uint64_t, int>, std::vector<std::pair<uint64_t, int>>,
+                        std::greater<std::pair<uint64_t, int>>> open;
+    for (int j = 0; j < P; ++j) open.push({0ull, j});
+    for (int e : idx) {
+        const auto [work, j] = open.top();
+        open.pop();
+        const int i = used[size_t(j)]++ * P + j;
+        b->h_order[i] = e;
+        if (i + P < B) open.push({work + b->h_cost[e], j});
+    }
+    return hipMemcpyAsync(b->d_order, b->h_order, sizeof(int32_t) * size_t(B),
+                          hipMemcpyHostToDevice, b->stream);
+}
+
+static hipError_t group_cost_collect(av_batch_t b, int k) {
+    if (!b->d_order || k < kGroupOrderMinSteps || b->cost_pending || capturing(b->stream))
+        return hipSuccess;
+    hipError_t e = hipMemcpyAsync(b->h_cost, b->d_cost, sizeof(uint32_t) * size_t(b->cfg.num_envs),
+                                  hipMemcpyDeviceToHost, b->stream);
+    if (e == hipSuccess) e = hipEventRecord(b->cost_ev, b->stream);
+    if (e == hipSuccess) b->cost_pending = true;
+    return e;
+}
+
 static av_status step_k(av_batch_t b, int32_t k, const uint8_t *actions, float *rewards,
                         uint8_t *done, uint8_t *obs = nullptr, int32_t w = 0) {
     if (av_status st = check_batch(b)) return st;
@@ -677,7 +766,11 @@ static av_status step_k(av_batch_t b, int32_t k, const uint8_t *actions, float *
     } else if (b->engine == AV_ENGINE_ROWS) {
         AV_HIP(launch_rows_step(a, b->d_rows, b->rprog.set_words, b->rprog.rules, b->stream));
     } else if (b->engine == AV_ENGINE_GROUP) {
+        AV_HIP(group_order_update(b, k));
+        a.order = b->d_order;
+        a.cost = b->d_cost;
         AV_HIP(launch_group_step(a, b->stream));
+        AV_HIP(group_cost_collect(b, k));
     } else if (b->engine == AV_ENGINE_WAVE) {
         AV_HIP(launch_wave_step(a, b->stream));
     } else {
@@ -894,6 +987,11 @@ av_status av_destroy_batch(av_batch_t b) {
         dev_free(b->d_init);
         dev_free(b->d_t);
         dev_free(b->d_n);
+        dev_free(b->d_order);
+        dev_free(b->d_cost);
+        if (b->h_order) (void)hipHostFree(b->h_order);
+        if (b->h_cost) (void)hipHostFree(b->h_cost);
+        if (b->cost_ev) (void)hipEventDestroy(b->cost_ev);
     }
     delete b;
     return st;

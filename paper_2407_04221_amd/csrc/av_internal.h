@@ -126,6 +126,10 @@ struct StepArgs {
     int32_t row_bytes;
     int32_t max_pat_h = 1;           // largest pattern rows a loaded rule may have
     int32_t max_pat_w = 1;           // largest pattern columns
+    // group engine: workgroup i steps environment order[i] (null: environment i) and, when cost
+    // is set, records the cycles its wave took in cost[environment] / 256
+    const int32_t *order = nullptr;
+    uint32_t *cost = nullptr;
     void *state;                     // [C][B][H] rows
     const void *init;                // [C][B][H] rows
     int32_t *t;                      // [B] step counters

@@ -207,7 +207,8 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
     constexpr int kChunk = 4;                 // entries or votes of a rule read in one round
     extern __shared__ __align__(16) uint32_t lds[];
     const int lane = int(threadIdx.x), g = lane / Hq, y = lane % Hq;
-    const int b = int(blockIdx.x);
+    const uint64_t t_start = __builtin_amdgcn_s_memtime();
+    const int b = a.order ? a.order[blockIdx.x] : int(blockIdx.x);
     const int H = a.H, W = a.W, C = a.C, C1 = C + 1, Rt = a.prog.rules_per_set;
     // pattern rows beyond a lane's row: plane rows y + i and match rows y - i, i <= PAD, are
     // read without a bounds test; rows of 4 words keep the probe table 16-byte aligned
@@ -619,6 +620,10 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
     if (lane == 0) {
         a.t[b] = t_env;
         a.nctr[b] = nbase + uint64_t(a.k);
+        if (a.cost) {
+            const uint64_t c = (__builtin_amdgcn_s_memtime() - t_start) >> 8;
+            a.cost[b] = uint32_t(c < 0xFFFFFFFFull ? c : 0xFFFFFFFFull);
+        }
     }
 }
 
