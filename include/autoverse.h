@@ -95,7 +95,7 @@ typedef enum {
                                (max_rules + 4) x max_pat_h x max_pat_w <= 254, at most 8
                                channels per lane group and, within 64 KiB of LDS, C + 1 planes
                                and R + 4 match planes of Hq + max_pat_h - 1 rows (rounded up to
-                               4), 3 C rows of Hq, 12 words per rule plus 12, and C (R + 4)
+                               4), 3 C rows of Hq, 12 words per rule plus 12, and C (R + 6)
                                words, 4 bytes each (Hq = 16 or 32); no rule application
                                control */
 } av_engine;

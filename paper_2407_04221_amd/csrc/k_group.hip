@@ -29,6 +29,7 @@
 //                      read by groups with fewer rules than others)
 //   RS   [C][R+4]      per channel and rule, the range of the rule's votes in the channel's
 //                      vote list (for exact recounts)
+//   RM   [C][2]        per channel, the 64-bit mask of the rules with votes in that list
 //   program            (when it fits, see the launcher) the environment's rule headers, input
 //                      merged entries, rule-major votes and channel-major vote lists
 //
@@ -226,7 +227,8 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
     uint32_t *I0 = MI + C * Hq;                    // [C][Hq] initial rows
     uint32_t *PT = I0 + C * Hq;                    // [Rt + 1][kProbeWords] probe table
     uint32_t *RS = PT + (Rt + 1) * kProbeWords;    // [C][Rt] rule ranges of channel lists
-    uint32_t *lprog = RS + C * Rt;                 // program copy (PROG_LDS)
+    uint32_t *RM = RS + C * Rt;                    // [C][2] rules with votes on each channel
+    uint32_t *lprog = RM + 2 * C;                  // program copy (PROG_LDS)
 
     const uint32_t *ghdr = reinterpret_cast<const uint32_t *>(a.prog.hdr + size_t(s) * Rt);
     const uint32_t *gment = a.prog.gmatch + size_t(s) * a.prog.gmatch_stride;
@@ -562,7 +564,8 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
                 if (c == kChPlayer && !lv)
                     nw = pnew;                    // only the moves voted on it
                 else if (group_any<Hq>((pl & mi) != 0u, lane))
-                    nw = exact_channel(old, fired_all, vote + int(vlw[2 * c]), RS + c * Rt, M,
+                    nw = exact_channel(old, fired_all & (uint64_t(RM[2 * c]) | uint64_t(RM[2 * c + 1]) << 32),
+                                       vote + int(vlw[2 * c]), RS + c * Rt, M,
                                        MS, PAD, y, row);
                 if (row) P[c * PR + y] = nw;
                 if (c == kChPlayer) pl_any = row && nw != 0u;
@@ -635,7 +638,7 @@ size_t group_lds_bytes(int H, int C, int rules_per_set, int max_pat_h) {
     const int Hq = group_lanes(H), PR = group_plane_words(Hq, max_pat_h);
     return sizeof(uint32_t) * (size_t(C + 1) * PR + size_t(rules_per_set) * PR +
                                size_t(3) * C * Hq + size_t(rules_per_set + 1) * kProbeWords +
-                               size_t(C) * rules_per_set);
+                               size_t(C) * (rules_per_set + 2));
 }
 
 bool group_eligible(int H, int W, int C, int rules_per_set, int max_pat_h, int max_pat_w) {
@@ -675,7 +678,7 @@ void compile_group_tables(const GenericProgram &p, int H, int W, int C, int max_
                           int &gm_stride) {
     const int Rt = p.rules_per_set, C1 = C + 1;
     const int PR = group_plane_words(group_lanes(H), max_pat_h);
-    stride = (Rt + 1) * kProbeWords + C * Rt;
+    stride = (Rt + 1) * kProbeWords + C * Rt + 2 * C;
     tab.assign(size_t(p.sets) * stride, 0u);
     std::vector<std::vector<uint32_t>> merged(p.sets);
     gm_stride = 1;
@@ -710,6 +713,9 @@ void compile_group_tables(const GenericProgram &p, int H, int W, int C, int max_
                 uint32_t &w = rs[c * Rt + r];
                 if (k == 0 || int(v[k - 1] & 255u) != r) w |= uint32_t(k);
                 if (k == vl.cnt - 1 || int(v[k + 1] & 255u) != r) w |= uint32_t(k + 1) << 16;
+                // the rules with votes on the channel, a 64-bit mask (an exact write visits
+                // only the fired ones among them)
+                rs[C * Rt + 2 * c + (r >> 5)] |= 1u << (r & 31);
             }
         }
     }
