@@ -699,7 +699,6 @@ static hipError_t group_order_update(av_batch_t b, int k) {
     if (hipEventQuery(b->cost_ev) != hipSuccess) return hipSuccess;   // not back yet
     b->cost_pending = false;
     const int B = b->cfg.num_envs, P = b->simds;
-    if (B <= P) return hipSuccess;
     std::vector<int> idx(static_cast<size_t>(B));
     std::iota(idx.begin(), idx.end(), 0);
     std::stable_sort(idx.begin(), idx.end(),
@@ -721,7 +720,9 @@ static hipError_t group_order_update(av_batch_t b, int k) {
 }
 
 static hipError_t group_cost_collect(av_batch_t b, int k) {
-    if (!b->d_order || k < kGroupOrderMinSteps || b->cost_pending || capturing(b->stream))
+    // (a batch of at most P environments has one wave per SIMD: nothing to deal)
+    if (!b->d_order || k < kGroupOrderMinSteps || b->cost_pending || b->cfg.num_envs <= b->simds ||
+        capturing(b->stream))
         return hipSuccess;
     hipError_t e = hipMemcpyAsync(b->h_cost, b->d_cost, sizeof(uint32_t) * size_t(b->cfg.num_envs),
                                   hipMemcpyDeviceToHost, b->stream);
