@@ -318,7 +318,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU: this build has no multi-GPU path (asked for "
+        print(f"bench.py runs on one GPU: the library has no multi-GPU path (asked for "
               f"--gpus {args.gpus}); environments are independent, so N GPUs would each run "
               f"this same kernel on B/N environments.", file=sys.stderr)
         sys.exit(2)
