@@ -82,22 +82,21 @@ typedef enum {
                                per row for W <= 32, else 8), 36 bytes per rule and 96 more;
                                no rule application control */
     AV_ENGINE_GROUP = 5     /* one environment per 64-lane wave, no barriers: 4 groups of 16
-                               lanes (maps of up to 16 rows) or 2 of 32 (up to 32 rows),
-                               lane y of each owning map row y, group g matching rules g,
-                               g + 4 (or g + 2), ...; input entries are merged per pattern
-                               row, every rule's first four merged entries are tested in one
-                               round of LDS reads, and only rules that pass somewhere read the
-                               rest.  After launches of 64 steps or more it measures each
+                               lanes, lane y of each owning map row y (and row y + 16 on maps
+                               of 17 to 32 rows), group g matching rules g, g + 4, ...; input
+                               entries are merged per pattern row, every rule's first four
+                               merged entries are tested in one round of LDS reads, and only
+                               rules that pass somewhere read the rest.  After launches of 64 steps or more it measures each
                                environment's cycles and deals environments to workgroups so that
                                the slowest ones do not share a SIMD (results never depend on
                                the order; not while the stream is captured).  Needs parallel
                                rule order, H, W <= 32,
                                (max_rules + 4) x max_pat_h x max_pat_w <= 254, at most 8
                                channels per lane group and, within 64 KiB of LDS, C + 1 planes
-                               and R + 4 match planes of Hq + max_pat_h - 1 rows (rounded up to
-                               4), 3 C rows of Hq, 12 words per rule plus 12, and C (R + 6)
-                               words, 4 bytes each (Hq = 16 or 32); no rule application
-                               control */
+                               and R + 4 match planes of HR + max_pat_h - 1 rows (rounded up to
+                               4), 3 C rows of HR, 12 words per rule plus 12, and C (R + 6)
+                               words, 4 bytes each (HR = 16, or 32 on maps of 17 to 32 rows);
+                               no rule application control */
 } av_engine;
 
 /* Order in which the rules of one step are applied. */

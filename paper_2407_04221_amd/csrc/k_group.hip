@@ -1,14 +1,15 @@
 // group engine: one environment per wave, its rules dealt to groups of lanes.
 //
-// The wave's 64 lanes form G = 64 / Hq groups of Hq lanes (Hq = 16 for maps of up to 16 rows,
-// 32 for up to 32); lane y of every group owns map row y (a 32-bit word, bit x = column x), and
-// group g matches rules g, g + G, g + 2G, ...  One workgroup is one wave, so a step needs no
-// barrier: the wave's LDS operations take effect in the order it issues them.
+// The wave's 64 lanes form G = 4 groups of 16 lanes; lane y of every group owns map row y (a
+// 32-bit word, bit x = column x) and, on maps of 17 to 32 rows, row y + 16 too (HR = 16 or 32
+// rows a group covers), and group g matches rules g, g + G, g + 2G, ...  One workgroup is one
+// wave, so a step needs no barrier: the wave's LDS operations take effect in the order it issues
+// them.
 //
 // The four built-in moves are computed in registers from the lanes' own rows of the player,
-// wall and force planes and the rows next to them (DPP row shifts within 16-lane groups, DPP
-// shifts of the whole wave for 32-lane groups); the player and wall rows stay in registers from step to
-// step unless a loaded rule wrote those planes.  A rule's input entries are merged per plane
+// wall and force planes and the rows next to them (DPP row shifts within the 16-lane groups;
+// with two rows a lane, the rows 15 and 16 meet across the lanes' two words); the player and
+// wall rows stay in registers from step to step unless a loaded rule wrote those planes.  A rule's input entries are merged per plane
 // row (one LDS read tests every specified column of a pattern row, up to 8); each loaded
 // rule's first four merged entries sit in a probe table (held in registers for the launch when
 // a group has at most two rules, else read at the start of each step), so the probe of every
@@ -17,13 +18,13 @@
 // rewritten.
 //
 // LDS (32-bit rows):
-//   P    [C+1][PR]     the map and the force plane (channel C); PR = Hq + ph - 1 rounded up to
+//   P    [C+1][PR]     the map and the force plane (channel C); PR = HR + ph - 1 rounded up to
 //                      4 rows (ph: the largest pattern's rows), so a lane reads row y + i of
 //                      any pattern entry without a bounds test (rows H .. PR - 1 stay zero)
 //   M    [R+4][PR]     match planes of the rules that fired, row y at ph - 1 + y: the zero rows
 //                      above let a vote read match row y - i without a test
-//   PL, MI [C][Hq]     per stored channel, the OR of the +1 and of the -1 votes
-//   I0   [C][Hq]       the initial rows, for resets
+//   PL, MI [C][HR]     per stored channel, the OR of the +1 and of the -1 votes
+//   I0   [C][HR]       the initial rows, for resets
 //   PT   [R+5][12]     probe table: per loaded rule its first eight merged entries, its
 //                      anchor rows and columns and where its entries are (row R + 4: zeros,
 //                      read by groups with fewer rules than others)
@@ -73,7 +74,7 @@ constexpr int kProbeWords = 12;         // probe table row: entries 0-3, anchor 
 constexpr uint32_t kPassEntry = 0u;
 constexpr int kMaxEntryOffset = 4095;
 
-// Words per plane row block: Hq rows plus the pattern rows hanging below the last one,
+// Words per plane row block: HR rows plus the pattern rows hanging below the last one,
 // rounded up to 4 (16-byte aligned probe table after the planes).
 __host__ __device__ constexpr int group_plane_words(int Hq, int max_pat_h) {
     return (Hq + max_pat_h - 1 + 3) & ~3;
@@ -108,103 +109,189 @@ __device__ inline uint32_t prev_row(uint32_t v, int lane, int y) {
     return y > 0 ? u : 0u;
 }
 
+// The same for the rows a lane holds, RPL of them (2: on maps of 17 to 32 rows a lane of a
+// 16-lane group holds rows y and y + 16): within each 16-row half a DPP row shift, across the
+// halves a DPP row rotate (lane 15's next row is lane 0's second row, lane 0's second row's
+// previous row is lane 15's first).
+template <int Hq, int RPL>
+__device__ inline void next_rows(const uint32_t (&v)[RPL], uint32_t (&n)[RPL], int lane, int y) {
+    if constexpr (RPL == 1) {
+        n[0] = next_row<Hq>(v[0], lane, y);
+    } else {
+        const uint32_t s0 = uint32_t(__builtin_amdgcn_update_dpp(0, int(v[0]), 0x101, 0xF, 0xF, true));
+        const uint32_t w1 = uint32_t(__builtin_amdgcn_update_dpp(0, int(v[1]), 0x12F, 0xF, 0xF, true));
+        n[0] = y == Hq - 1 ? w1 : s0;
+        n[1] = uint32_t(__builtin_amdgcn_update_dpp(0, int(v[1]), 0x101, 0xF, 0xF, true));
+    }
+}
+template <int Hq, int RPL>
+__device__ inline void prev_rows(const uint32_t (&v)[RPL], uint32_t (&p)[RPL], int lane, int y) {
+    if constexpr (RPL == 1) {
+        p[0] = prev_row<Hq>(v[0], lane, y);
+    } else {
+        p[0] = uint32_t(__builtin_amdgcn_update_dpp(0, int(v[0]), 0x111, 0xF, 0xF, true));
+        const uint32_t t1 = uint32_t(__builtin_amdgcn_update_dpp(0, int(v[1]), 0x111, 0xF, 0xF, true));
+        const uint32_t w0 = uint32_t(__builtin_amdgcn_update_dpp(0, int(v[0]), 0x121, 0xF, 0xF, true));
+        p[1] = y == 0 ? w0 : t1;
+    }
+}
+
+template <int RPL>
+__device__ inline bool any_row(const uint32_t (&v)[RPL]) {
+    uint32_t o = 0u;
+#pragma unroll
+    for (int h = 0; h < RPL; ++h) o |= v[h];
+    return o != 0u;
+}
+
 // Count the votes of rule r's channel-list entries lo .. hi - 1 (packed r | i << 8 | j << 16 |
-// plus << 24) into the KB-bit bit-sliced counter cnt: a plus vote adds its cells, a minus
-// vote adds the complement of its cells; nm counts the minus entries.  Four entries at a
-// time: carry-save adders make the four one-bit planes a 3-bit number, then one ripple add.
-template <int KB>
-__device__ inline void count_votes(uint32_t (&cnt)[KB], int &nm, const uint32_t *vl, int lo,
-                                   int hi, const uint32_t *Mr, int y, bool row) {
+// plus << 24) into the KB-bit bit-sliced counters cnt of the lane's rows yr: a plus vote adds
+// its cells, a minus vote adds the complement of its cells; nm counts the minus entries.  Four
+// entries at a time: carry-save adders make the four one-bit planes a 3-bit number, then one
+// ripple add.
+template <int KB, int RPL>
+__device__ inline void count_votes(uint32_t (&cnt)[RPL][KB], int &nm, const uint32_t *vl, int lo,
+                                   int hi, const uint32_t *Mr, const int (&yr)[RPL],
+                                   const bool (&rw)[RPL]) {
     for (int ev = lo; ev < hi; ev += 4) {
-        uint32_t v[4], x[4];
+        uint32_t v[4];
+        bool live[4], minus[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) v[u] = vl[min(ev + u, hi - 1)];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-            const uint32_t t = row ? Mr[y - int((v[u] >> 8) & 255u)] << ((v[u] >> 16) & 255u) : 0u;
-            const bool live = ev + u < hi, minus = live && !((v[u] >> 24) & 1u);
-            x[u] = !live ? 0u : minus ? ~t : t;
-            nm += minus ? 1 : 0;
+            live[u] = ev + u < hi;
+            minus[u] = live[u] && !((v[u] >> 24) & 1u);
+            nm += minus[u] ? 1 : 0;
         }
-        const uint32_t a = x[0] ^ x[1], s1 = a ^ x[2];
-        const uint32_t c1 = (x[0] & x[1]) | (x[2] & a);            // weight 2
-        const uint32_t s0 = s1 ^ x[3], c2 = s1 & x[3];             // weight 1, 2
-        const uint32_t w2 = c1 ^ c2, w4 = c1 & c2;                 // weight 2, 4
-        uint32_t k = cnt[0] & s0;
-        cnt[0] ^= s0;
-        const uint32_t a1 = cnt[1] ^ w2;
-        const uint32_t k1 = (cnt[1] & w2) | (k & a1);
-        cnt[1] = a1 ^ k;
-        const uint32_t a2 = cnt[2] ^ w4;
-        k = (cnt[2] & w4) | (k1 & a2);
-        cnt[2] = a2 ^ k1;
 #pragma unroll
-        for (int q = 3; q < KB; ++q) {
-            const uint32_t kq = cnt[q] & k;
-            cnt[q] ^= k;
-            k = kq;
+        for (int h = 0; h < RPL; ++h) {
+            uint32_t x[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const uint32_t t =
+                    rw[h] ? Mr[yr[h] - int((v[u] >> 8) & 255u)] << ((v[u] >> 16) & 255u) : 0u;
+                x[u] = !live[u] ? 0u : minus[u] ? ~t : t;
+            }
+            const uint32_t a = x[0] ^ x[1], s1 = a ^ x[2];
+            const uint32_t c1 = (x[0] & x[1]) | (x[2] & a);            // weight 2
+            const uint32_t s0 = s1 ^ x[3], c2 = s1 & x[3];             // weight 1, 2
+            const uint32_t w2 = c1 ^ c2, w4 = c1 & c2;                 // weight 2, 4
+            uint32_t *const q = cnt[h];
+            uint32_t k = q[0] & s0;
+            q[0] ^= s0;
+            const uint32_t a1 = q[1] ^ w2;
+            const uint32_t k1 = (q[1] & w2) | (k & a1);
+            q[1] = a1 ^ k;
+            const uint32_t a2 = q[2] ^ w4;
+            k = (q[2] & w4) | (k1 & a2);
+            q[2] = a2 ^ k1;
+#pragma unroll
+            for (int b = 3; b < KB; ++b) {
+                const uint32_t kq = q[b] & k;
+                q[b] ^= k;
+                k = kq;
+            }
         }
     }
 }
 
-// The exact write of channel c for this lane's row (needed only where some cell of the group
+// The exact write of channel c for the lane's rows (needed only where some cell of the group
 // got votes of both signs): the votes on c of every rule in `fired` (the channel's vote list
 // `vl`, ordered by rule; rule r's entries are vl[rsc[r] & 0xFFFF .. rsc[r] >> 16)) with the old
 // value as a plus vote.  One counter takes old + #plus + (#minus entries - #minus votes), so a
 // cell is set, old + #plus - #minus >= 1, where it reaches 1 + #minus entries.  A list holds
 // at most 254 entries (eligibility: every entry is a distinct rule and pattern cell), so
 // 8-bit counters never overflow; 4 bits do when the fired rules' entries are at most 14.
-__device__ inline uint32_t exact_channel(uint32_t old, uint64_t fired, const uint32_t *vl,
-                                         const uint32_t *rsc, const uint32_t *M, int MS, int pad,
-                                         int y, bool row) {
-    int total = 0;
-    for (uint64_t fr = fired; fr; fr &= fr - 1) {
+// With `moves` (the player plane) the four moves' votes, two entries each (-1 on the player's
+// cell, +1 on the cell it moves to), are read from their match rows at once: the counter starts
+// at old + their four plus votes + (4 - their four minus votes) and only the loaded rules'
+// lists are walked.  (Groups of up to two rules, whose probe rows stay in registers, walk the
+// moves too: the start's registers would spill the step's own.)
+template <int RPL>
+__device__ inline void exact_channel(const uint32_t (&old)[RPL], uint64_t fired, bool moves,
+                                     const uint32_t *vl, const uint32_t *rsc, const uint32_t *M,
+                                     int MS, int pad, const int (&yr)[RPL], const bool (&rw)[RPL],
+                                     uint32_t (&out)[RPL]) {
+    const uint64_t walk = moves ? fired & ~((1ull << kMoveRules) - 1ull) : fired;
+    int total = moves ? 2 * kMoveRules : 0;
+    for (uint64_t fr = walk; fr; fr &= fr - 1) {
         const uint32_t rs = rsc[__builtin_ctzll(fr)];
         total += int(rs >> 16) - int(rs & 0xFFFFu);
     }
-    const uint32_t o = row ? old : 0u;
-    int nm = 0;
-    uint32_t gt = 0u, eq = ~0u;
+    int nm = moves ? kMoveRules : 0;
     auto ge = [&](auto &cnt, auto kb) {           // cnt >= 1 + nm, bit-sliced
         constexpr int KB = decltype(kb)::value;
         const uint32_t T = uint32_t(1 + nm);
 #pragma unroll
-        for (int q = KB - 1; q >= 0; --q) {
-            const uint32_t tb = ((T >> q) & 1u) ? ~0u : 0u;
-            gt |= eq & cnt[q] & ~tb;
-            eq &= ~(cnt[q] ^ tb);
+        for (int h = 0; h < RPL; ++h) {
+            uint32_t gt = 0u, eq = ~0u;
+#pragma unroll
+            for (int q = KB - 1; q >= 0; --q) {
+                const uint32_t tb = ((T >> q) & 1u) ? ~0u : 0u;
+                gt |= eq & cnt[h][q] & ~tb;
+                eq &= ~(cnt[h][q] ^ tb);
+            }
+            out[h] = gt | eq;
         }
     };
-    if (total <= 14) {
-        uint32_t cnt[4] = {o, 0u, 0u, 0u};
-        for (uint64_t fr = fired; fr; fr &= fr - 1) {
+    auto run = [&](auto kb) {
+        constexpr int KB = decltype(kb)::value;
+        uint32_t cnt[RPL][KB];
+#pragma unroll
+        for (int h = 0; h < RPL; ++h) {
+#pragma unroll
+            for (int q = 0; q < KB; ++q) cnt[h][q] = 0u;
+            const uint32_t o = rw[h] ? old[h] : 0u;
+            if (moves) {
+                // match rows of right, left, down, up (rules 0..3) at this row and the one above
+                const uint32_t *m = M + pad + yr[h];
+                const uint32_t m0 = m[0], m1 = m[MS], m2 = m[2 * MS], m3 = m[3 * MS];
+                const uint32_t m2p = m[2 * MS - 1], m3p = m[3 * MS - 1];
+                const uint32_t a1 = m0 << 1, b2 = m1 << 1;
+                // plus: old, a1, m1, m2p, m3 -> p2 p1 p0
+                const uint32_t s1 = o ^ a1 ^ m1, c1 = (o & a1) | (m1 & (o ^ a1));
+                const uint32_t p0 = s1 ^ m2p ^ m3, c2 = (s1 & m2p) | (m3 & (s1 ^ m2p));
+                const uint32_t p1 = c1 ^ c2, p2 = c1 & c2;
+                // complements of the minus votes m0, b2, m2, m3p -> q2 q1 q0 (4 - their sum)
+                const uint32_t s3 = m0 ^ b2 ^ m2, c3 = (m0 & b2) | (m2 & (m0 ^ b2));
+                const uint32_t q0 = s3 ^ m3p, q1 = c3 ^ (s3 | m3p), q2 = ~(c3 | s3 | m3p);
+                // p + q (at most 9)
+                const uint32_t k0 = p0 & q0;
+                const uint32_t k1 = (p1 & q1) | (k0 & (p1 ^ q1));
+                const uint32_t k2 = (p2 & q2) | (k1 & (p2 ^ q2));
+                cnt[h][0] = p0 ^ q0;
+                cnt[h][1] = p1 ^ q1 ^ k0;
+                cnt[h][2] = p2 ^ q2 ^ k1;
+                cnt[h][3] = k2;
+            } else {
+                cnt[h][0] = o;
+            }
+        }
+        for (uint64_t fr = walk; fr; fr &= fr - 1) {
             const int r = __builtin_ctzll(fr);
             const uint32_t rs = rsc[r];
-            count_votes<4>(cnt, nm, vl, int(rs & 0xFFFFu), int(rs >> 16), M + r * MS + pad, y,
-                           row);
+            count_votes<KB, RPL>(cnt, nm, vl, int(rs & 0xFFFFu), int(rs >> 16),
+                                 M + r * MS + pad, yr, rw);
         }
-        ge(cnt, std::integral_constant<int, 4>{});
-    } else {
-        uint32_t cnt[kCountBits] = {o, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
-        for (uint64_t fr = fired; fr; fr &= fr - 1) {
-            const int r = __builtin_ctzll(fr);
-            const uint32_t rs = rsc[r];
-            count_votes<kCountBits>(cnt, nm, vl, int(rs & 0xFFFFu), int(rs >> 16),
-                                    M + r * MS + pad, y, row);
-        }
-        ge(cnt, std::integral_constant<int, kCountBits>{});
-    }
-    return gt | eq;
+        ge(cnt, kb);
+    };
+    if (total <= 14) run(std::integral_constant<int, 4>{});
+    else run(std::integral_constant<int, kCountBits>{});
 }
 
 // NR: rules a group holds (a bound on this launch's ceil(R / G)).
+// RPL: map rows a lane holds: 2 on maps of 17 to 32 rows (lane y of a 16-lane group holds rows
+// y and y + 16), else 1.
 // NJ: columns a merged entry tests (3 when no pattern is wider, else 8).
 // PROG_LDS: the rule program is copied to LDS.  A compile-time choice, so that the program's
 // reads are LDS reads or global loads: a pointer that may be either makes every read a flat
 // load, which the LDS reads' waits then wait for as well.
-template <int Hq, int NR, int NJ, bool PROG_LDS>
+template <int Hq, int RPL, int NR, int NJ, bool PROG_LDS>
 __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
+    static_assert(RPL == 1 || Hq == 16, "two rows a lane in 16-lane groups");
     constexpr int G = 64 / Hq;
+    constexpr int HR = Hq * RPL;              // map rows a group covers
     constexpr int kChunk = 4;                 // entries or votes of a rule read in one round
     extern __shared__ __align__(16) uint32_t lds[];
     const int lane = int(threadIdx.x), g = lane / Hq, y = lane % Hq;
@@ -214,18 +301,25 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
     // pattern rows beyond a lane's row: plane rows y + i and match rows y - i, i <= PAD, are
     // read without a bounds test; rows of 4 words keep the probe table 16-byte aligned
     const int PAD = a.max_pat_h - 1;
-    const int PR = group_plane_words(Hq, a.max_pat_h), MS = PR;
+    const int PR = group_plane_words(HR, a.max_pat_h), MS = PR;
     const int s = a.per_env ? b : 0;
-    const bool row = y < H;
-    const int ry = row ? y : 0;
+    // the lane's rows; past the map (rw false) their plane rows stay zero and are read freely
+    // (row yr + i < PR), their anchors are masked off and they are never written
+    int yr[RPL];
+    bool rw[RPL];
+#pragma unroll
+    for (int h = 0; h < RPL; ++h) {
+        yr[h] = y + Hq * h;
+        rw[h] = yr[h] < H;
+    }
     const uint32_t wmask = low_mask(W);
 
     uint32_t *P = lds;                             // [C1][PR]
     uint32_t *M = P + C1 * PR;                     // [Rt][MS]
-    uint32_t *PL = M + Rt * MS;                    // [C][Hq]
-    uint32_t *MI = PL + C * Hq;                    // [C][Hq]
-    uint32_t *I0 = MI + C * Hq;                    // [C][Hq] initial rows
-    uint32_t *PT = I0 + C * Hq;                    // [Rt + 1][kProbeWords] probe table
+    uint32_t *PL = M + Rt * MS;                    // [C][HR]
+    uint32_t *MI = PL + C * HR;                    // [C][HR]
+    uint32_t *I0 = MI + C * HR;                    // [C][HR] initial rows
+    uint32_t *PT = I0 + C * HR;                    // [Rt + 1][kProbeWords] probe table
     uint32_t *RS = PT + (Rt + 1) * kProbeWords;    // [C][Rt] rule ranges of channel lists
     uint32_t *RM = RS + C * Rt;                    // [C][2] rules with votes on each channel
     uint32_t *lprog = RM + 2 * C;                  // program copy (PROG_LDS)
@@ -252,7 +346,7 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
         vote = pc;
     }
     {
-        const int words = C1 * PR + Rt * MS + 3 * C * Hq;   // (PT and RS are copied)
+        const int words = C1 * PR + Rt * MS + 3 * C * HR;   // (PT and RS are copied)
         for (int w = lane; w < words; w += 64) lds[w] = 0u;
     }
 
@@ -266,12 +360,17 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
 #pragma unroll
     for (int q = 0; q < kMaxChanPerGroup; ++q) {
         const int c = g + G * q;
-        if (c < C && row) {
-            const size_t at = (size_t(c) * a.B + b) * H + y;
-            P[c * PR + y] = a.row_bytes == 2 ? uint32_t(static_cast<const uint16_t *>(a.state)[at])
-                                             : static_cast<const uint32_t *>(a.state)[at];
-            I0[c * Hq + y] = a.row_bytes == 2 ? uint32_t(static_cast<const uint16_t *>(a.init)[at])
-                                              : static_cast<const uint32_t *>(a.init)[at];
+#pragma unroll
+        for (int h = 0; h < RPL; ++h) {
+            if (c < C && rw[h]) {
+                const size_t at = (size_t(c) * a.B + b) * H + yr[h];
+                P[c * PR + yr[h]] = a.row_bytes == 2
+                                        ? uint32_t(static_cast<const uint16_t *>(a.state)[at])
+                                        : static_cast<const uint32_t *>(a.state)[at];
+                I0[c * HR + yr[h]] = a.row_bytes == 2
+                                         ? uint32_t(static_cast<const uint16_t *>(a.init)[at])
+                                         : static_cast<const uint32_t *>(a.init)[at];
+            }
         }
     }
     __syncthreads();   // (one wave: orders the set-up's LDS writes before the step's reads)
@@ -281,23 +380,32 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
     // entry e (merged per plane row) at this lane's row: OR-s into bad the anchors where a
     // tested column does not hold the wanted value (the row moved right by the column's
     // offset); a column's care and want bits sign-extended are all-ones masks
-    auto miss = [&](uint32_t e, uint32_t &bad) {
-        uint32_t v = P[int(e & uint32_t(kMaxEntryOffset)) + ry];
-        if constexpr (NJ > 3) v >>= (e >> 9) & 24u;
+    auto miss = [&](uint32_t e, uint32_t (&bad)[RPL]) {
+        uint32_t v[RPL];
+#pragma unroll
+        for (int h = 0; h < RPL; ++h) {
+            v[h] = P[int(e & uint32_t(kMaxEntryOffset)) + yr[h]];
+            if constexpr (NJ > 3) v[h] >>= (e >> 9) & 24u;
+        }
 #pragma unroll
         for (int j = 0; j < NJ; ++j) {
             const uint32_t want = uint32_t(int32_t(e << (7 - j)) >> 31);
             const uint32_t care = uint32_t(int32_t(e << (15 - j)) >> 31);
-            bad |= ((v >> j) ^ want) & care;
+#pragma unroll
+            for (int h = 0; h < RPL; ++h) bad[h] |= ((v[h] >> j) ^ want) & care;
         }
     };
-    auto entries4 = [&](uint32_t e0, uint32_t e1, uint32_t e2, uint32_t e3) {
-        uint32_t bad = 0u;
+    // the anchors m of the lane's rows that pass four entries more
+    auto entries4 = [&](uint32_t e0, uint32_t e1, uint32_t e2, uint32_t e3, uint32_t (&m)[RPL]) {
+        uint32_t bad[RPL];
+#pragma unroll
+        for (int h = 0; h < RPL; ++h) bad[h] = 0u;
         miss(e0, bad);
         miss(e1, bad);
         miss(e2, bad);
         miss(e3, bad);
-        return ~bad;
+#pragma unroll
+        for (int h = 0; h < RPL; ++h) m[h] &= ~bad[h];
     };
 
     uint32_t ablk = 0u;     // lane l: action of step k0 + l of the current block of 64
@@ -308,12 +416,19 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
     const uint32_t *const P2 = P2w;
 
     const uint32_t cm1 = low_mask(W - 1);         // anchors of a 1 x 2 pattern
-    const uint32_t vrow2 = (y + 2 <= H) ? wmask : 0u;   // rows of a 2 x 1 pattern's anchors
+    uint32_t vrow2[RPL];                          // rows of a 2 x 1 pattern's anchors
+#pragma unroll
+    for (int h = 0; h < RPL; ++h) vrow2[h] = (yr[h] + 2 <= H) ? wmask : 0u;
     const int pown = kChPlayer % G;               // the group that writes the player plane
     // the player and wall rows of the lane (every group holds them): the next step's follow
     // from the moves' votes in registers unless a loaded rule voted on either plane or the
     // episode ended; then they are read again
-    uint32_t Pyr = row ? P2[y] : 0u, Wyr = row ? P[kChWall * PR + y] : 0u;
+    uint32_t Pyr[RPL], Wyr[RPL];
+#pragma unroll
+    for (int h = 0; h < RPL; ++h) {
+        Pyr[h] = rw[h] ? P2[yr[h]] : 0u;
+        Wyr[h] = rw[h] ? P[kChWall * PR + yr[h]] : 0u;
+    }
     // the probe rows of the group's rules: read once when the group has at most two rules,
     // else every step (registers would spill)
     uint4 pe[NR];
@@ -336,7 +451,12 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
         const int act = __builtin_amdgcn_readlane(int(ablk), kb);
         // the lane's rows of the player and wall planes (0 past the map; kept in registers
         // from step to step), and the probe table rows of the group's rules
-        const uint32_t Py = Pyr, Wy = Wyr;
+        uint32_t Py[RPL], Wy[RPL];
+#pragma unroll
+        for (int h = 0; h < RPL; ++h) {
+            Py[h] = Pyr[h];
+            Wy[h] = Wyr[h];
+        }
         if constexpr (NR > 2) {                   // (up to two rules: held for the launch)
 #pragma unroll
             for (int kr = 0; kr < NR; ++kr) {
@@ -346,68 +466,96 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
             }
         }
         // the rows next to them and the force row
-        const uint32_t Pn = next_row<Hq>(Py, lane, y), Wn = next_row<Hq>(Wy, lane, y);
-        const uint32_t Pp = prev_row<Hq>(Py, lane, y);
-        const uint32_t Fy = act == 1 ? Pn : act == 3 ? Pp : act == 2 ? ((Py << 1) & wmask)
-                          : act == 4 ? (Py >> 1) : 0u;
-        if (g == 0 && row) F[y] = Fy;
-        const uint32_t Fn = next_row<Hq>(Fy, lane, y);
+        uint32_t Pn[RPL], Wn[RPL], Pp[RPL], Fy[RPL], Fn[RPL];
+        next_rows<Hq, RPL>(Py, Pn, lane, y);
+        next_rows<Hq, RPL>(Wy, Wn, lane, y);
+        prev_rows<Hq, RPL>(Py, Pp, lane, y);
+#pragma unroll
+        for (int h = 0; h < RPL; ++h) {
+            Fy[h] = act == 1 ? Pn[h] : act == 3 ? Pp[h] : act == 2 ? ((Py[h] << 1) & wmask)
+                  : act == 4 ? (Py[h] >> 1) : 0u;
+            if (g == 0 && rw[h]) F[yr[h]] = Fy[h];
+        }
+        next_rows<Hq, RPL>(Fy, Fn, lane, y);
         // the four moves (rules 0..3: right, left, down, up) and their votes on the player
         // plane; group 0 stores their match rows for an exact recount
-        const uint32_t m0 = Py & (Fy >> 1) & ~(Wy >> 1) & cm1;
-        const uint32_t m1 = Fy & ~Wy & (Py >> 1) & cm1;
-        const uint32_t m2 = Py & Fn & ~Wn & vrow2;
-        const uint32_t m3 = Fy & ~Wy & Pn & vrow2;
-        const uint32_t m2p = prev_row<Hq>(m2, lane, y), m3p = prev_row<Hq>(m3, lane, y);
-        const uint32_t mplus = (m0 << 1) | m1 | m2p | m3;
-        const uint32_t mminus = m0 | (m1 << 1) | m2 | m3p;
-        // the player rows after the moves' votes alone: one sign OR-ed, or, where some cell got
-        // votes of both signs (players moving into cells other players leave), counted exactly
-        // in registers: old + #plus > #minus over the four plus and four minus terms
-        uint32_t pnew = (Py | mplus) & ~mminus;
-        if (__builtin_amdgcn_ballot_w64((mplus & mminus) != 0u)) {
-            const uint32_t a1 = m0 << 1, b2 = m1 << 1;
-            // plus: old, a1, m1, m2p, m3 -> p2 p1 p0 (at most 5)
-            const uint32_t s1 = Py ^ a1 ^ m1, c1 = (Py & a1) | (m1 & (Py ^ a1));
-            const uint32_t p0 = s1 ^ m2p ^ m3, c2 = (s1 & m2p) | (m3 & (s1 ^ m2p));
-            const uint32_t p1 = c1 ^ c2, p2 = c1 & c2;
-            // minus: m0, b2, m2, m3p -> n2 n1 n0 (at most 4)
-            const uint32_t s3 = m0 ^ b2 ^ m2, c3 = (m0 & b2) | (m2 & (m0 ^ b2));
-            const uint32_t n0 = s3 ^ m3p, c4 = s3 & m3p;
-            const uint32_t n1 = c3 ^ c4, n2 = c3 & c4;
-            pnew = (p2 & ~n2) | (~(p2 ^ n2) & ((p1 & ~n1) | (~(p1 ^ n1) & p0 & ~n0)));
+        uint32_t m0[RPL], m1[RPL], m2[RPL], m3[RPL], m2p[RPL], m3p[RPL];
+        uint32_t mplus[RPL], mminus[RPL], pnew[RPL];
+#pragma unroll
+        for (int h = 0; h < RPL; ++h) {
+            m0[h] = Py[h] & (Fy[h] >> 1) & ~(Wy[h] >> 1) & cm1;
+            m1[h] = Fy[h] & ~Wy[h] & (Py[h] >> 1) & cm1;
+            m2[h] = Py[h] & Fn[h] & ~Wn[h] & vrow2[h];
+            m3[h] = Fy[h] & ~Wy[h] & Pn[h] & vrow2[h];
+        }
+        prev_rows<Hq, RPL>(m2, m2p, lane, y);
+        prev_rows<Hq, RPL>(m3, m3p, lane, y);
+        uint32_t both = 0u;
+#pragma unroll
+        for (int h = 0; h < RPL; ++h) {
+            mplus[h] = (m0[h] << 1) | m1[h] | m2p[h] | m3[h];
+            mminus[h] = m0[h] | (m1[h] << 1) | m2[h] | m3p[h];
+            // the player rows after the moves' votes alone: one sign OR-ed, or, where some cell
+            // got votes of both signs (players moving into cells other players leave), counted
+            // exactly in registers: old + #plus > #minus over the four plus and four minus terms
+            pnew[h] = (Py[h] | mplus[h]) & ~mminus[h];
+            both |= mplus[h] & mminus[h];
+        }
+        if (__builtin_amdgcn_ballot_w64(both != 0u)) {
+#pragma unroll
+            for (int h = 0; h < RPL; ++h) {
+                const uint32_t a1 = m0[h] << 1, b2 = m1[h] << 1, o = Py[h];
+                // plus: old, a1, m1, m2p, m3 -> p2 p1 p0 (at most 5)
+                const uint32_t s1 = o ^ a1 ^ m1[h], c1 = (o & a1) | (m1[h] & (o ^ a1));
+                const uint32_t p0 = s1 ^ m2p[h] ^ m3[h], c2 = (s1 & m2p[h]) | (m3[h] & (s1 ^ m2p[h]));
+                const uint32_t p1 = c1 ^ c2, p2 = c1 & c2;
+                // minus: m0, b2, m2, m3p -> n2 n1 n0 (at most 4)
+                const uint32_t s3 = m0[h] ^ b2 ^ m2[h], c3 = (m0[h] & b2) | (m2[h] & (m0[h] ^ b2));
+                const uint32_t n0 = s3 ^ m3p[h], c4 = s3 & m3p[h];
+                const uint32_t n1 = c3 ^ c4, n2 = c3 & c4;
+                pnew[h] = (p2 & ~n2) | (~(p2 ^ n2) & ((p1 & ~n1) | (~(p1 ^ n1) & p0 & ~n0)));
+            }
         }
         if (g == 0) {
-            M[0 * MS + PAD + y] = m0;
-            M[1 * MS + PAD + y] = m1;
-            M[2 * MS + PAD + y] = m2;
-            M[3 * MS + PAD + y] = m3;
+#pragma unroll
+            for (int h = 0; h < RPL; ++h) {
+                M[0 * MS + PAD + yr[h]] = m0[h];
+                M[1 * MS + PAD + yr[h]] = m1[h];
+                M[2 * MS + PAD + yr[h]] = m2[h];
+                M[3 * MS + PAD + yr[h]] = m3[h];
+            }
         }
-        uint64_t fired = (__builtin_amdgcn_ballot_w64(m0 != 0u) ? 1ull : 0ull) |
-                         (__builtin_amdgcn_ballot_w64(m1 != 0u) ? 2ull : 0ull) |
-                         (__builtin_amdgcn_ballot_w64(m2 != 0u) ? 4ull : 0ull) |
-                         (__builtin_amdgcn_ballot_w64(m3 != 0u) ? 8ull : 0ull);
+        uint64_t fired = (__builtin_amdgcn_ballot_w64(any_row<RPL>(m0)) ? 1ull : 0ull) |
+                         (__builtin_amdgcn_ballot_w64(any_row<RPL>(m1)) ? 2ull : 0ull) |
+                         (__builtin_amdgcn_ballot_w64(any_row<RPL>(m2)) ? 4ull : 0ull) |
+                         (__builtin_amdgcn_ballot_w64(any_row<RPL>(m3)) ? 8ull : 0ull);
 
         // probe: every loaded rule of the group with its first four entries, all reads at once
         // (no branch between the rules); the results go to the rules' match rows, and a
         // wave-uniform mask of the rule indices kr whose probe passed in some group
-        uint32_t mk[NR];
+        uint32_t mk[NR][RPL];
 #pragma unroll
         for (int kr = 0; kr < NR; ++kr) {
-            const uint32_t vm = (kr < nr && y < int(pv[kr] >> 8)) ? ~0u >> (pv[kr] & 255u) : 0u;
-            mk[kr] = vm & entries4(pe[kr].x, pe[kr].y, pe[kr].z, pe[kr].w);
+#pragma unroll
+            for (int h = 0; h < RPL; ++h)
+                mk[kr][h] = (kr < nr && yr[h] < int(pv[kr] >> 8)) ? ~0u >> (pv[kr] & 255u) : 0u;
+            entries4(pe[kr].x, pe[kr].y, pe[kr].z, pe[kr].w, mk[kr]);
         }
         uint32_t cand = 0u;
 #pragma unroll
         for (int kr = 0; kr < NR; ++kr) {
-            if (kr < nr) M[(kMoveRules + g + G * kr) * MS + PAD + y] = mk[kr];
-            cand |= __builtin_amdgcn_ballot_w64(mk[kr] != 0u) ? 1u << kr : 0u;
+            if (kr < nr) {
+#pragma unroll
+                for (int h = 0; h < RPL; ++h)
+                    M[(kMoveRules + g + G * kr) * MS + PAD + yr[h]] = mk[kr][h];
+            }
+            cand |= __builtin_amdgcn_ballot_w64(any_row<RPL>(mk[kr])) ? 1u << kr : 0u;
         }
 
         // candidates: the rest of their input entries four at a time.  With up to four rules per
         // group, in rounds in which every candidate of every group takes its next four (a lane
         // only while it still holds an anchor of the rule; otherwise the pass entry, which
-        // tests nothing); with more, one rule after another, the next four entries
+        // tests nothing; a rule slot no group still needs is skipped); with more, one rule after another, the next four entries
         // read while the current ones' plane rows are (rounds would issue every rule's reads
         // while most rules are done, and four waves share each CU's LDS there).  A rule is done
         // when its entries run out or its lanes have no anchor left.
@@ -423,15 +571,19 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
             }
             if constexpr (NR <= 4) {
                 for (int e = kProbeEntries;; e += 4) {
-                    bool any = false;
+                    // the rule slots still live in some group (the others are skipped)
+                    uint32_t lk = 0u;
 #pragma unroll
-                    for (int kr = 0; kr < NR; ++kr) any |= mk[kr] != 0u && e < int(meta[kr] >> 16);
-                    if (!__builtin_amdgcn_ballot_w64(any)) break;
+                    for (int kr = 0; kr < NR; ++kr)
+                        lk |= __builtin_amdgcn_ballot_w64(any_row<RPL>(mk[kr]) && e < int(meta[kr] >> 16))
+                                  ? 1u << kr : 0u;
+                    if (!lk) break;
                     uint32_t x[NR][4];
 #pragma unroll
                     for (int kr = 0; kr < NR; ++kr) {
+                        if (!((lk >> kr) & 1u)) continue;
                         const int off = int(meta[kr] & 0xFFFFu), cnt = int(meta[kr] >> 16);
-                        const bool live = mk[kr] != 0u && e < cnt;
+                        const bool live = any_row<RPL>(mk[kr]) && e < cnt;
                         if (NR <= 2 && e == kProbeEntries) {   // entries 4 .. 7: in registers
                             const uint4 q = pe2[kr];
                             x[kr][0] = live ? q.x : kPassEntry;
@@ -449,14 +601,16 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
                     }
 #pragma unroll
                     for (int kr = 0; kr < NR; ++kr)
-                        mk[kr] &= entries4(x[kr][0], x[kr][1], x[kr][2], x[kr][3]);
+                        if ((lk >> kr) & 1u) entries4(x[kr][0], x[kr][1], x[kr][2], x[kr][3], mk[kr]);
                 }
             } else {
 #pragma unroll
                 for (int kr = 0; kr < NR; ++kr) {
                     if (!((cand >> kr) & 1u)) continue;
-                    uint32_t m = mk[kr];
-                    if (!(kr < nr && group_any<Hq>(m != 0u, lane))) continue;
+                    uint32_t m[RPL];
+#pragma unroll
+                    for (int h = 0; h < RPL; ++h) m[h] = mk[kr][h];
+                    if (!(kr < nr && group_any<Hq>(any_row<RPL>(m), lane))) continue;
                     const uint32_t *en = ment + int(meta[kr] & 0xFFFFu);
                     const int cnt = int(meta[kr] >> 16), last = cnt - 1;
                     int e = kProbeEntries;
@@ -465,7 +619,7 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
 #pragma unroll
                         for (int u = 0; u < 4; ++u) x[u] = en[min(e + u, last)];
                     }
-                    while (e < cnt && group_any<Hq>(m != 0u, lane)) {
+                    while (e < cnt && group_any<Hq>(any_row<RPL>(m), lane)) {
                         uint32_t cur[4];
 #pragma unroll
                         for (int u = 0; u < 4; ++u) cur[u] = x[u];
@@ -474,28 +628,39 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
 #pragma unroll
                             for (int u = 0; u < 4; ++u) x[u] = en[min(e + u, last)];
                         }
-                        m &= entries4(cur[0], cur[1], cur[2], cur[3]);
+                        entries4(cur[0], cur[1], cur[2], cur[3], m);
                     }
-                    mk[kr] = m;
+#pragma unroll
+                    for (int h = 0; h < RPL; ++h) mk[kr][h] = m[h];
                 }
             }
             // the rules that fired in some group: match row, reward and votes
             uint32_t fl = 0u;
 #pragma unroll
             for (int kr = 0; kr < NR; ++kr)
-                fl |= __builtin_amdgcn_ballot_w64(mk[kr] != 0u) ? 1u << kr : 0u;
+                fl |= __builtin_amdgcn_ballot_w64(any_row<RPL>(mk[kr])) ? 1u << kr : 0u;
             for (; fl; fl &= fl - 1u) {
                 const int kr = __builtin_ctz(fl);
                 const int r = kMoveRules + g + G * kr;
-                uint32_t m = 0u;                  // mk[kr] (kr is wave-uniform)
+                uint32_t m[RPL];                  // mk[kr] (kr is wave-uniform)
 #pragma unroll
-                for (int kk = 0; kk < NR; ++kk) m = kk == kr ? mk[kk] : m;
-                if (kr < nr && group_any<Hq>(m != 0u, lane)) {
+                for (int h = 0; h < RPL; ++h) m[h] = 0u;
+#pragma unroll
+                for (int kk = 0; kk < NR; ++kk) {
+#pragma unroll
+                    for (int h = 0; h < RPL; ++h) m[h] = kk == kr ? mk[kk][h] : m[h];
+                }
+                if (kr < nr && group_any<Hq>(any_row<RPL>(m), lane)) {
                     const uint32_t *hw = hdrw + r * kHdrWords;
-                    M[r * MS + PAD + y] = m;
+                    int cells = 0;
+#pragma unroll
+                    for (int h = 0; h < RPL; ++h) {
+                        M[r * MS + PAD + yr[h]] = m[h];
+                        cells += __popc(m[h]);
+                    }
                     fired |= 1ull << r;
                     voted |= hw[7];
-                    rsum += int(hw[2]) * __popc(m);
+                    rsum += int(hw[2]) * cells;
                     // votes kChunk at a time, the next chunk read with the current one's match
                     // rows (a repeated last vote ORs the same bits again)
                     const uint32_t *ve = vent + int(hw[5]);
@@ -506,7 +671,7 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
                         for (int u = 0; u < kChunk; ++u) v[u] = ve[min(u, vlast)];
                     }
                     for (int ev = 0; ev < vcnt; ev += kChunk) {
-                        uint32_t cv[kChunk], tv[kChunk];
+                        uint32_t cv[kChunk], tv[kChunk][RPL];
 #pragma unroll
                         for (int u = 0; u < kChunk; ++u) cv[u] = v[u];
                         if (ev + kChunk < vcnt) {
@@ -514,12 +679,20 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
                             for (int u = 0; u < kChunk; ++u) v[u] = ve[min(ev + kChunk + u, vlast)];
                         }
 #pragma unroll
-                        for (int u = 0; u < kChunk; ++u)
-                            tv[u] = M[r * MS + PAD + y - int((cv[u] >> 8) & 255u)] << ((cv[u] >> 16) & 255u);
+                        for (int u = 0; u < kChunk; ++u) {
 #pragma unroll
-                        for (int u = 0; u < kChunk; ++u)
-                            if (row && tv[u])
-                                atomicOr(((cv[u] >> 24) & 1u ? PL : MI) + int(cv[u] & 255u) * Hq + y, tv[u]);
+                            for (int h = 0; h < RPL; ++h)
+                                tv[u][h] = M[r * MS + PAD + yr[h] - int((cv[u] >> 8) & 255u)]
+                                           << ((cv[u] >> 16) & 255u);
+                        }
+#pragma unroll
+                        for (int u = 0; u < kChunk; ++u) {
+#pragma unroll
+                            for (int h = 0; h < RPL; ++h)
+                                if (rw[h] && tv[u][h])
+                                    atomicOr(((cv[u] >> 24) & 1u ? PL : MI) + int(cv[u] & 255u) * HR + yr[h],
+                                             tv[u][h]);
+                        }
                     }
                 }
             }
@@ -541,37 +714,54 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
 
         // new rows of the channels that received votes: group g rewrites channels g, g + G, ...
         // (the moves' votes on the player plane are in registers, the loaded rules' in LDS)
-        bool pl_any = g == pown && row && Py != 0u;   // a player bit after the write
+        bool pl_any = false;                      // a player bit after the write
+#pragma unroll
+        for (int h = 0; h < RPL; ++h) pl_any |= g == pown && rw[h] && Py[h] != 0u;
         if (voted_all == (1u << kChPlayer) && lvoted == 0u) {
             // only the moves voted (most steps): the player plane, from registers
-            const uint32_t nw = pnew;
             if (g == pown) {
-                if (row) P2w[y] = nw;
-                pl_any = row && nw != 0u;
+                pl_any = false;
+#pragma unroll
+                for (int h = 0; h < RPL; ++h) {
+                    if (rw[h]) P2w[yr[h]] = pnew[h];
+                    pl_any |= rw[h] && pnew[h] != 0u;
+                }
             }
         } else if (voted_all) {
 #pragma unroll 1
             for (int c = g; c < C; c += G) {
                 if (!((voted_all >> c) & 1u)) continue;
-                const uint32_t old = c == kChPlayer ? Py : P[c * PR + ry];
                 const bool lv = (lvoted >> c) & 1u;
-                uint32_t pl = lv ? PL[c * Hq + y] : 0u, mi = lv ? MI[c * Hq + y] : 0u;
-                if (c == kChPlayer) {
-                    pl |= mplus;
-                    mi |= mminus;
+                uint32_t old[RPL], pl[RPL], mi[RPL], nw[RPL], mixed = 0u;
+#pragma unroll
+                for (int h = 0; h < RPL; ++h) {
+                    old[h] = c == kChPlayer ? Py[h] : P[c * PR + yr[h]];
+                    pl[h] = lv ? PL[c * HR + yr[h]] : 0u;
+                    mi[h] = lv ? MI[c * HR + yr[h]] : 0u;
+                    if (c == kChPlayer) {
+                        pl[h] |= mplus[h];
+                        mi[h] |= mminus[h];
+                    }
+                    nw[h] = (old[h] | pl[h]) & ~mi[h];
+                    mixed |= pl[h] & mi[h];
                 }
-                uint32_t nw = (old | pl) & ~mi;
-                if (c == kChPlayer && !lv)
-                    nw = pnew;                    // only the moves voted on it
-                else if (group_any<Hq>((pl & mi) != 0u, lane))
-                    nw = exact_channel(old, fired_all & (uint64_t(RM[2 * c]) | uint64_t(RM[2 * c + 1]) << 32),
-                                       vote + int(vlw[2 * c]), RS + c * Rt, M,
-                                       MS, PAD, y, row);
-                if (row) P[c * PR + y] = nw;
-                if (c == kChPlayer) pl_any = row && nw != 0u;
-                if (lv) {
-                    PL[c * Hq + y] = 0u;
-                    MI[c * Hq + y] = 0u;
+                if (c == kChPlayer && !lv) {
+#pragma unroll
+                    for (int h = 0; h < RPL; ++h) nw[h] = pnew[h];   // only the moves voted on it
+                } else if (group_any<Hq>(mixed != 0u, lane)) {
+                    exact_channel<RPL>(old, fired_all & (uint64_t(RM[2 * c]) | uint64_t(RM[2 * c + 1]) << 32),
+                                       NR > 2 && c == kChPlayer, vote + int(vlw[2 * c]), RS + c * Rt,
+                                       M, MS, PAD, yr, rw, nw);
+                }
+                if (c == kChPlayer) pl_any = false;
+#pragma unroll
+                for (int h = 0; h < RPL; ++h) {
+                    if (rw[h]) P[c * PR + yr[h]] = nw[h];
+                    if (c == kChPlayer) pl_any |= rw[h] && nw[h] != 0u;
+                    if (lv) {
+                        PL[c * HR + yr[h]] = 0u;
+                        MI[c * HR + yr[h]] = 0u;
+                    }
                 }
             }
         }
@@ -587,16 +777,23 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
         const bool d = !anyp || (a.L > 0 && t_env == a.L);
         if (d) {                                  // back to the initial rows
             t_env = 0;
-            if (row) {
+#pragma unroll
+            for (int h = 0; h < RPL; ++h) {
+                if (rw[h]) {
 #pragma unroll 1
-                for (int c = g; c < C; c += G) P[c * PR + y] = I0[c * Hq + y];
+                    for (int c = g; c < C; c += G) P[c * PR + yr[h]] = I0[c * HR + yr[h]];
+                }
             }
         }
         if (d || ((lvoted >> kChPlayer) & 1u) || ((lvoted >> kChWall) & 1u)) {
-            Pyr = row ? P2[y] : 0u;
-            Wyr = row ? P[kChWall * PR + y] : 0u;
+#pragma unroll
+            for (int h = 0; h < RPL; ++h) {
+                Pyr[h] = rw[h] ? P2[yr[h]] : 0u;
+                Wyr[h] = rw[h] ? P[kChWall * PR + yr[h]] : 0u;
+            }
         } else {
-            Pyr = pnew;
+#pragma unroll
+            for (int h = 0; h < RPL; ++h) Pyr[h] = pnew[h];
         }
         if (lane == kb) {
             rbuf = float(rsum);
@@ -614,10 +811,13 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
 #pragma unroll
     for (int q = 0; q < kMaxChanPerGroup; ++q) {
         const int c = g + G * q;
-        if (c < C && row) {
-            const size_t at = (size_t(c) * a.B + b) * H + y;
-            if (a.row_bytes == 2) static_cast<uint16_t *>(a.state)[at] = uint16_t(P[c * PR + y]);
-            else static_cast<uint32_t *>(a.state)[at] = P[c * PR + y];
+#pragma unroll
+        for (int h = 0; h < RPL; ++h) {
+            if (c < C && rw[h]) {
+                const size_t at = (size_t(c) * a.B + b) * H + yr[h];
+                if (a.row_bytes == 2) static_cast<uint16_t *>(a.state)[at] = uint16_t(P[c * PR + yr[h]]);
+                else static_cast<uint32_t *>(a.state)[at] = P[c * PR + yr[h]];
+            }
         }
     }
     if (lane == 0) {
@@ -632,12 +832,13 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
 
 }  // namespace
 
-int group_lanes(int H) { return H <= 16 ? 16 : 32; }
+// Map rows a lane group covers: its 16 lanes hold one row each, or two on maps of 17 to 32 rows.
+static int group_rows(int H) { return H <= 16 ? 16 : 32; }
 
 size_t group_lds_bytes(int H, int C, int rules_per_set, int max_pat_h) {
-    const int Hq = group_lanes(H), PR = group_plane_words(Hq, max_pat_h);
+    const int HR = group_rows(H), PR = group_plane_words(HR, max_pat_h);
     return sizeof(uint32_t) * (size_t(C + 1) * PR + size_t(rules_per_set) * PR +
-                               size_t(3) * C * Hq + size_t(rules_per_set + 1) * kProbeWords +
+                               size_t(3) * C * HR + size_t(rules_per_set + 1) * kProbeWords +
                                size_t(C) * (rules_per_set + 2));
 }
 
@@ -646,11 +847,11 @@ bool group_eligible(int H, int W, int C, int rules_per_set, int max_pat_h, int m
     // every vote a cell-channel gets comes from a distinct (rule, pattern cell): the 8-bit
     // counts of the exact write hold them (plus the old value) when there are at most 255
     if (long(rules_per_set) * max_pat_h * max_pat_w > 254) return false;
-    const int G = 64 / group_lanes(H);
+    constexpr int G = 4;                          // lane groups a wave holds
     // (merged entries address rows of the stored and force planes in 12 bits)
     return rules_per_set <= kMaxRulesPerGroup * G && rules_per_set <= 64 &&
            C <= kMaxChanPerGroup * G &&
-           (C + 1) * group_plane_words(group_lanes(H), max_pat_h) <= kMaxEntryOffset + 1 &&
+           (C + 1) * group_plane_words(group_rows(H), max_pat_h) <= kMaxEntryOffset + 1 &&
            group_lds_bytes(H, C, rules_per_set, max_pat_h) <= size_t(kLdsBudget);
 }
 
@@ -677,7 +878,7 @@ void compile_group_tables(const GenericProgram &p, int H, int W, int C, int max_
                           std::vector<uint32_t> &tab, int &stride, std::vector<uint32_t> &gm,
                           int &gm_stride) {
     const int Rt = p.rules_per_set, C1 = C + 1;
-    const int PR = group_plane_words(group_lanes(H), max_pat_h);
+    const int PR = group_plane_words(group_rows(H), max_pat_h);
     stride = (Rt + 1) * kProbeWords + C * Rt + 2 * C;
     tab.assign(size_t(p.sets) * stride, 0u);
     std::vector<std::vector<uint32_t>> merged(p.sets);
@@ -725,21 +926,21 @@ void compile_group_tables(const GenericProgram &p, int H, int W, int C, int max_
 }
 
 namespace {
-template <int Hq, int NJ, bool PROG_LDS>
+template <int RPL, int NJ, bool PROG_LDS>
 void launch_nr(const StepArgs &a, size_t lds, hipStream_t s) {
-    constexpr int G = 64 / Hq;
+    constexpr int G = 4;
     const int nrmax = (a.prog.rules_per_set - kMoveRules + G - 1) / G;
     const dim3 grid(a.B), block(64);
-    if (nrmax <= 2) hipLaunchKernelGGL((group_step<Hq, 2, NJ, PROG_LDS>), grid, block, lds, s, a);
-    else if (nrmax <= 4) hipLaunchKernelGGL((group_step<Hq, 4, NJ, PROG_LDS>), grid, block, lds, s, a);
-    else if (nrmax <= 8) hipLaunchKernelGGL((group_step<Hq, 8, NJ, PROG_LDS>), grid, block, lds, s, a);
-    else if (nrmax <= 12) hipLaunchKernelGGL((group_step<Hq, 12, NJ, PROG_LDS>), grid, block, lds, s, a);
-    else hipLaunchKernelGGL((group_step<Hq, 16, NJ, PROG_LDS>), grid, block, lds, s, a);
+    if (nrmax <= 2) hipLaunchKernelGGL((group_step<16, RPL, 2, NJ, PROG_LDS>), grid, block, lds, s, a);
+    else if (nrmax <= 4) hipLaunchKernelGGL((group_step<16, RPL, 4, NJ, PROG_LDS>), grid, block, lds, s, a);
+    else if (nrmax <= 8) hipLaunchKernelGGL((group_step<16, RPL, 8, NJ, PROG_LDS>), grid, block, lds, s, a);
+    else if (nrmax <= 12) hipLaunchKernelGGL((group_step<16, RPL, 12, NJ, PROG_LDS>), grid, block, lds, s, a);
+    else hipLaunchKernelGGL((group_step<16, RPL, 16, NJ, PROG_LDS>), grid, block, lds, s, a);
 }
-template <int Hq, int NJ>
-void launch_hq(const StepArgs &a, size_t lds, bool prog_lds, hipStream_t s) {
-    if (prog_lds) launch_nr<Hq, NJ, true>(a, lds, s);
-    else launch_nr<Hq, NJ, false>(a, lds, s);
+template <int RPL, int NJ>
+void launch_rpl(const StepArgs &a, size_t lds, bool prog_lds, hipStream_t s) {
+    if (prog_lds) launch_nr<RPL, NJ, true>(a, lds, s);
+    else launch_nr<RPL, NJ, false>(a, lds, s);
 }
 }  // namespace
 
@@ -755,12 +956,12 @@ hipError_t launch_group_step(const StepArgs &a, hipStream_t s) {
     const bool prog_lds = a.k >= 16 && base + prog <= budget;
     const size_t lds = base + (prog_lds ? prog : 0);
     const bool narrow = a.max_pat_w <= 3;
-    if (group_lanes(a.H) == 16) {
-        if (narrow) launch_hq<16, 3>(a, lds, prog_lds, s);
-        else launch_hq<16, 8>(a, lds, prog_lds, s);
+    if (group_rows(a.H) == 16) {
+        if (narrow) launch_rpl<1, 3>(a, lds, prog_lds, s);
+        else launch_rpl<1, 8>(a, lds, prog_lds, s);
     } else {
-        if (narrow) launch_hq<32, 3>(a, lds, prog_lds, s);
-        else launch_hq<32, 8>(a, lds, prog_lds, s);
+        if (narrow) launch_rpl<2, 3>(a, lds, prog_lds, s);
+        else launch_rpl<2, 8>(a, lds, prog_lds, s);
     }
     return hipGetLastError();
 }

@@ -23,17 +23,17 @@ def rows_ok(wl):
 def group_ok(wl, rule_mode="parallel"):
     """The group engine takes maps of at most 32 x 32 in parallel rule order with (R + 4) x
     pattern cells <= 254, at most 8 channels per lane group and 16 rules per group (4 groups of
-    16 lanes up to 16 rows, 2 of 32 up to 32), and within 64 KiB of LDS: C + 1 planes and R + 4
-    match planes of PR = Hq + ph - 1 rows (rounded up to 4), 3 C rows of Hq (votes, initial
-    rows), a 12-word probe row per rule plus one, and a word per channel and rule plus two; the stored
-    and force planes' rows addressed in 12 bits."""
+    16 lanes, covering 16 rows, or 32 with two rows a lane), and within 64 KiB of LDS: C + 1
+    planes and R + 4 match planes of PR = HR + ph - 1 rows (rounded up to 4), 3 C rows of HR
+    (votes, initial rows), a 12-word probe row per rule plus one, and a word per channel and rule
+    plus two; the stored and force planes' rows addressed in 12 bits."""
     if rule_mode != "parallel" or wl.H > 32 or wl.W > 32:
         return False
     rt = wl.R + 4
-    hq = 16 if wl.H <= 16 else 32
-    G = 64 // hq
-    pr = (hq + wl.max_h - 1 + 3) & ~3
-    lds = 4 * ((wl.C + 1) * pr + rt * pr + 3 * wl.C * hq + (rt + 1) * 12 + wl.C * (rt + 2))
+    hr = 16 if wl.H <= 16 else 32
+    G = 4
+    pr = (hr + wl.max_h - 1 + 3) & ~3
+    lds = 4 * ((wl.C + 1) * pr + rt * pr + 3 * wl.C * hr + (rt + 1) * 12 + wl.C * (rt + 2))
     return (rt * wl.max_h * wl.max_w <= 254 and rt <= 16 * G and rt <= 64 and wl.C <= 8 * G
             and (wl.C + 1) * pr <= 4096 and lds <= 65536)
 
