@@ -73,6 +73,8 @@ constexpr int kProbeWords = 12;         // probe table row: entries 0-3, anchor 
 // kPassEntry tests no column (it passes everywhere).
 constexpr uint32_t kPassEntry = 0u;
 constexpr int kMaxEntryOffset = 4095;
+constexpr int kShortLaunch = 16;        // launches of fewer steps: SHORT kernels, program in
+                                        // global memory
 
 // Words per plane row block: HR rows plus the pattern rows hanging below the last one,
 // rounded up to 4 (16-byte aligned probe table after the planes).
@@ -81,6 +83,23 @@ __host__ __device__ constexpr int group_plane_words(int Hq, int max_pat_h) {
 }
 
 __device__ inline uint32_t low_mask(int bits) { return bits >= 32 ? ~0u : ((1u << bits) - 1u); }
+
+// Copy n words from global memory to LDS, eight loads of a lane in flight before its writes.
+__device__ inline void copy_to_lds(uint32_t *dst, const uint32_t *src, int n, int lane) {
+    for (int w0 = lane; w0 < n; w0 += 8 * 64) {
+        uint32_t v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int w = w0 + 64 * u;
+            v[u] = w < n ? src[w] : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int w = w0 + 64 * u;
+            if (w < n) dst[w] = v[u];
+        }
+    }
+}
 
 // Does any lane of this lane's group hold a nonzero?
 template <int Hq>
@@ -287,9 +306,17 @@ __device__ inline void exact_channel(const uint32_t (&old)[RPL], uint64_t fired,
 // PROG_LDS: the rule program is copied to LDS.  A compile-time choice, so that the program's
 // reads are LDS reads or global loads: a pointer that may be either makes every read a flat
 // load, which the LDS reads' waits then wait for as well.
-template <int Hq, int RPL, int NR, int NJ, bool PROG_LDS>
-__global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
+// SHORT: a launch of fewer than 16 steps (one step per observation), whose time is its set-up,
+// a step or a few and the final store, each a chain of memory round trips: every load of the
+// set-up is issued before its LDS writes (copy loops that wait for each load are one round
+// trip per 64 words), the final store forms its addresses anew, and the kernel may take 256
+// VGPRs, so nothing spills to scratch (at 128 a cold scratch reload on the path costs a round
+// trip).  Longer launches keep four waves per SIMD and the per-row set-up, whose step loop
+// measured faster (the set-up's code changes the loop's register assignment).
+template <int Hq, int RPL, int NR, int NJ, bool PROG_LDS, bool SHORT>
+__global__ void __launch_bounds__(64, NR <= 8 ? (SHORT ? 2 : 4) : 1) group_step(StepArgs a) {
     static_assert(RPL == 1 || Hq == 16, "two rows a lane in 16-lane groups");
+    static_assert(!(SHORT && PROG_LDS), "short launches read the program from global memory");
     constexpr int G = 64 / Hq;
     constexpr int HR = Hq * RPL;              // map rows a group covers
     constexpr int kChunk = 4;                 // entries or votes of a rule read in one round
@@ -353,10 +380,42 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
     // the probe table and the rule ranges (built with the program: compile_group_tables)
     {
         const uint32_t *gt = a.prog.gtab + size_t(s) * a.prog.gtab_stride;
-        for (int w = lane; w < a.prog.gtab_stride; w += 64) PT[w] = gt[w];
+        if constexpr (SHORT) copy_to_lds(PT, gt, a.prog.gtab_stride, lane);
+        else for (int w = lane; w < a.prog.gtab_stride; w += 64) PT[w] = gt[w];
     }
     const int nl = Rt - kMoveRules;               // loaded rules
     const int nr = (nl - g + G - 1) / G;          // this group's loaded rule count
+    // (SHORT) lane l takes row l % H of channels l / H, l / H + 64 / H, ...
+    const int rcs = 64 / H;
+    if constexpr (SHORT) {
+        const int rcl = lane / H, rrow = lane - rcl * H;
+        auto load_rows = [&](const auto *st, const auto *in) {
+            for (int c0 = rcl; c0 < C; c0 += 4 * rcs) {
+                uint32_t sv[4], iv[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int c = c0 + u * rcs;
+                    const size_t at = (size_t(c) * a.B + b) * H + rrow;
+                    sv[u] = c < C ? uint32_t(st[at]) : 0u;
+                    iv[u] = c < C ? uint32_t(in[at]) : 0u;
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int c = c0 + u * rcs;
+                    if (c < C) {
+                        P[c * PR + rrow] = sv[u];
+                        I0[c * HR + rrow] = iv[u];
+                    }
+                }
+            }
+        };
+        if (rcl < rcs) {
+            if (a.row_bytes == 2)
+                load_rows(static_cast<const uint16_t *>(a.state), static_cast<const uint16_t *>(a.init));
+            else
+                load_rows(static_cast<const uint32_t *>(a.state), static_cast<const uint32_t *>(a.init));
+        }
+    } else {
 #pragma unroll
     for (int q = 0; q < kMaxChanPerGroup; ++q) {
         const int c = g + G * q;
@@ -372,6 +431,7 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
                                          : static_cast<const uint32_t *>(a.init)[at];
             }
         }
+    }
     }
     __syncthreads();   // (one wave: orders the set-up's LDS writes before the step's reads)
     int t_env = a.t[b];
@@ -808,6 +868,21 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
         }
     }
 
+    if constexpr (SHORT) {
+        // the rows back as they were read, the lane's channel and row formed again from an
+        // opaque copy of its index (kept from the set-up they were spilled through the launch)
+        int le = lane;
+        asm volatile("" : "+v"(le));
+        const int wcl = le / H, wrow = le - wcl * H;
+        if (wcl < rcs) {
+#pragma unroll 4
+            for (int c = wcl; c < C; c += rcs) {
+                const size_t at = (size_t(c) * a.B + b) * H + wrow;
+                if (a.row_bytes == 2) static_cast<uint16_t *>(a.state)[at] = uint16_t(P[c * PR + wrow]);
+                else static_cast<uint32_t *>(a.state)[at] = P[c * PR + wrow];
+            }
+        }
+    } else {
 #pragma unroll
     for (int q = 0; q < kMaxChanPerGroup; ++q) {
         const int c = g + G * q;
@@ -819,6 +894,7 @@ __global__ void __launch_bounds__(64, NR <= 8 ? 4 : 1) group_step(StepArgs a) {
                 else static_cast<uint32_t *>(a.state)[at] = P[c * PR + yr[h]];
             }
         }
+    }
     }
     if (lane == 0) {
         a.t[b] = t_env;
@@ -926,21 +1002,22 @@ void compile_group_tables(const GenericProgram &p, int H, int W, int C, int max_
 }
 
 namespace {
-template <int RPL, int NJ, bool PROG_LDS>
+template <int RPL, int NJ, bool PROG_LDS, bool SHORT>
 void launch_nr(const StepArgs &a, size_t lds, hipStream_t s) {
     constexpr int G = 4;
     const int nrmax = (a.prog.rules_per_set - kMoveRules + G - 1) / G;
     const dim3 grid(a.B), block(64);
-    if (nrmax <= 2) hipLaunchKernelGGL((group_step<16, RPL, 2, NJ, PROG_LDS>), grid, block, lds, s, a);
-    else if (nrmax <= 4) hipLaunchKernelGGL((group_step<16, RPL, 4, NJ, PROG_LDS>), grid, block, lds, s, a);
-    else if (nrmax <= 8) hipLaunchKernelGGL((group_step<16, RPL, 8, NJ, PROG_LDS>), grid, block, lds, s, a);
-    else if (nrmax <= 12) hipLaunchKernelGGL((group_step<16, RPL, 12, NJ, PROG_LDS>), grid, block, lds, s, a);
-    else hipLaunchKernelGGL((group_step<16, RPL, 16, NJ, PROG_LDS>), grid, block, lds, s, a);
+    if (nrmax <= 2) hipLaunchKernelGGL((group_step<16, RPL, 2, NJ, PROG_LDS, SHORT>), grid, block, lds, s, a);
+    else if (nrmax <= 4) hipLaunchKernelGGL((group_step<16, RPL, 4, NJ, PROG_LDS, SHORT>), grid, block, lds, s, a);
+    else if (nrmax <= 8) hipLaunchKernelGGL((group_step<16, RPL, 8, NJ, PROG_LDS, SHORT>), grid, block, lds, s, a);
+    else if (nrmax <= 12) hipLaunchKernelGGL((group_step<16, RPL, 12, NJ, PROG_LDS, SHORT>), grid, block, lds, s, a);
+    else hipLaunchKernelGGL((group_step<16, RPL, 16, NJ, PROG_LDS, SHORT>), grid, block, lds, s, a);
 }
 template <int RPL, int NJ>
 void launch_rpl(const StepArgs &a, size_t lds, bool prog_lds, hipStream_t s) {
-    if (prog_lds) launch_nr<RPL, NJ, true>(a, lds, s);
-    else launch_nr<RPL, NJ, false>(a, lds, s);
+    if (prog_lds) launch_nr<RPL, NJ, true, false>(a, lds, s);
+    else if (a.k < kShortLaunch) launch_nr<RPL, NJ, false, true>(a, lds, s);
+    else launch_nr<RPL, NJ, false, false>(a, lds, s);
 }
 }  // namespace
 
@@ -953,7 +1030,7 @@ hipError_t launch_group_step(const StepArgs &a, hipStream_t s) {
     // for as many waves per CU (160 KiB of LDS) as the batch can use, up to 16 (4 per SIMD)
     const size_t need = size_t(std::min(16, (a.B + 255) / 256));
     const size_t budget = std::min(size_t(kLdsBudget), size_t(160) * 1024 / need);
-    const bool prog_lds = a.k >= 16 && base + prog <= budget;
+    const bool prog_lds = a.k >= kShortLaunch && base + prog <= budget;
     const size_t lds = base + (prog_lds ? prog : 0);
     const bool narrow = a.max_pat_w <= 3;
     if (group_rows(a.H) == 16) {
