@@ -6,8 +6,10 @@
 #include <algorithm>
 #include <cstdlib>
 #include <deque>
+#include <map>
 #include <sstream>
 #include <string>
+#include <tuple>
 #include <vector>
 
 #include "av_internal.h"
@@ -142,21 +144,119 @@ class Gen {
         return t;
     }
 
+    // A bit-sliced sum in progress: level k holds terms of weight 2^k.
+    using Levels = std::vector<std::deque<Bit>>;
+
+    static int sum3(int a, int b, int c) { return a ^ b ^ c; }
+    static int maj3(int a, int b, int c) { return (a & b) | (a & c) | (b & c); }
+    Bit op3(const Bit &a, const Bit &b, const Bit &c, int table) {
+        const std::string r = fresh();
+        o << "const " << type << " " << r << " = __builtin_amdgcn_bitop3_b32(" << a.name << ", "
+          << b.name << ", " << c.name << ", 0x" << std::hex << table << std::dec << ");\n";
+        return Bit{r, false};
+    }
+
+    // Carry-save sums of several term lists started together: a full adder over three terms
+    // that several lists hold serves them all.  Its inputs may be complemented in one list and
+    // not in another as long as all three are (the sum and carry of complements are the
+    // complements of the sum and carry), so a list takes the adder's outputs complemented
+    // then.  Greedy, level by level: the signed pairs held by the most lists, each widened to
+    // the third term most of their holders share, until no three terms are held by two lists;
+    // a shared sum stays on its level (it may be shared again), a shared carry moves up one.
+    // Only terms that several lists hold are added here; the rest is left to at_least.
+    std::vector<Levels> share(const std::vector<std::vector<Bit>> &lists) {
+        std::vector<Levels> lv(lists.size());
+        for (size_t l = 0; l < lists.size(); ++l)
+            lv[l].emplace_back(lists[l].begin(), lists[l].end());
+        auto find = [](const std::deque<Bit> &q, const std::string &n) {
+            for (size_t x = 0; x < q.size(); ++x)
+                if (q[x].name == n) return int(x);
+            return -1;
+        };
+        for (size_t k = 0;; ++k) {
+            bool any_level = false;
+            for (auto &L : lv) any_level |= L.size() > k;
+            if (!any_level) break;
+            for (;;) {
+                // signed pairs (names in order, relative complement) and the lists holding them
+                std::map<std::tuple<std::string, std::string, bool>, std::vector<int>> pairs;
+                for (size_t l = 0; l < lv.size(); ++l) {
+                    if (lv[l].size() <= k) continue;
+                    const std::deque<Bit> &q = lv[l][k];
+                    for (size_t x = 0; x < q.size(); ++x)
+                        for (size_t y = x + 1; y < q.size(); ++y) {
+                            const Bit &a = q[x].name < q[y].name ? q[x] : q[y];
+                            const Bit &b = q[x].name < q[y].name ? q[y] : q[x];
+                            pairs[{a.name, b.name, a.inv != b.inv}].push_back(int(l));
+                        }
+                }
+                std::vector<std::pair<size_t, std::tuple<std::string, std::string, bool>>> order;
+                for (auto &pr : pairs)
+                    if (pr.second.size() >= 2) order.push_back({pr.second.size(), pr.first});
+                if (order.empty()) break;
+                std::stable_sort(order.begin(), order.end(),
+                                 [](const auto &u, const auto &v) { return u.first > v.first; });
+                // the best triple among the most held pairs: (holders, a, b, c, c relative to a)
+                size_t best_n = 0;
+                std::string ba, bb, bc;
+                bool bab = false, bac = false;
+                for (size_t t = 0; t < order.size() && t < 8; ++t) {
+                    const auto &[na, nb, ab] = order[t].second;
+                    std::map<std::pair<std::string, bool>, size_t> third;
+                    for (int l : pairs[order[t].second]) {
+                        const std::deque<Bit> &q = lv[l][k];
+                        const bool ia = q[find(q, na)].inv;
+                        for (const Bit &c : q)
+                            if (c.name != na && c.name != nb) ++third[{c.name, c.inv != ia}];
+                    }
+                    for (auto &tc : third)
+                        if (tc.second > best_n) {
+                            best_n = tc.second;
+                            ba = na; bb = nb; bab = ab;
+                            bc = tc.first.first; bac = tc.first.second;
+                        }
+                }
+                if (best_n < 2) break;
+                // one adder, inputs as the first holder has them
+                Bit s{}, cy{};
+                bool first = true, first_ia = false;
+                for (size_t l = 0; l < lv.size(); ++l) {
+                    if (lv[l].size() <= k) continue;
+                    std::deque<Bit> &q = lv[l][k];
+                    const int xa = find(q, ba), xb = find(q, bb), xc = find(q, bc);
+                    if (xa < 0 || xb < 0 || xc < 0) continue;
+                    const Bit a = q[xa], b = q[xb], c = q[xc];
+                    if ((a.inv != b.inv) != bab || (a.inv != c.inv) != bac) continue;
+                    if (first) {
+                        s = op3(a, b, c, table3(sum3, a.inv, b.inv, c.inv));
+                        cy = op3(a, b, c, table3(maj3, a.inv, b.inv, c.inv));
+                        first_ia = a.inv;
+                        first = false;
+                    }
+                    const bool flip = a.inv != first_ia;
+                    std::deque<Bit> rest;
+                    for (size_t x = 0; x < q.size(); ++x)
+                        if (int(x) != xa && int(x) != xb && int(x) != xc) rest.push_back(q[x]);
+                    rest.push_back(Bit{s.name, flip});
+                    q = rest;
+                    if (lv[l].size() == k + 1) lv[l].emplace_back();
+                    lv[l][k + 1].push_back(Bit{cy.name, flip});
+                }
+            }
+        }
+        return lv;
+    }
+
     // The cells where the number of set terms is at least K (K >= 1): the terms are added
     // with a carry-save tree of full adders (sum and carry are one v_bitop3 each, with the
     // terms' complements folded into the truth tables) and the count's bits are compared with
     // the constant K; emitted as GT.
     void at_least(const std::vector<Bit> &terms, long K) {
-        std::vector<std::deque<Bit>> lv(1, std::deque<Bit>(terms.begin(), terms.end()));
+        at_least(Levels(1, std::deque<Bit>(terms.begin(), terms.end())), K);
+    }
+    // The same for a sum already started (share): terms of weight 2^k on level k.
+    void at_least(Levels lv, long K) {
         std::vector<Bit> bits;
-        auto op3 = [&](const Bit &a, const Bit &b, const Bit &c, int table) {
-            const std::string r = fresh();
-            o << "const " << type << " " << r << " = __builtin_amdgcn_bitop3_b32(" << a.name << ", "
-              << b.name << ", " << c.name << ", 0x" << std::hex << table << std::dec << ");\n";
-            return Bit{r, false};
-        };
-        auto sum3 = [](int a, int b, int c) { return a ^ b ^ c; };
-        auto maj3 = [](int a, int b, int c) { return (a & b) | (a & c) | (b & c); };
         auto xor2 = [](int a, int b, int) { return a ^ b; };
         auto and2 = [](int a, int b, int) { return a & b; };
         for (size_t k = 0; k < lv.size(); ++k) {

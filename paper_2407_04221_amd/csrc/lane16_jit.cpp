@@ -16,7 +16,8 @@
 //          of the wave has votes of both signs, the channel's votes are counted exactly with
 //          carry-save adders and the cell becomes 1 iff old + sum >= 1 (Sec. 2.1
 //          transposed-convolution write, clamped to {0, 1}), counted as old + #plus +
-//          #(minus terms that are 0) >= #minus + 1.
+//          #(minus terms that are 0) >= #minus + 1; full adders over terms that several
+//          channels count are formed once for all of them.
 //   The force plane's own votes are not evaluated: the plane is dropped after the step.
 #include <hip/hip_runtime.h>
 
@@ -344,13 +345,22 @@ std::string lane16_rules_body(int C, int H, int W, const std::vector<Lane16Rule>
                 o << "const u32 " << tname(r, i, j) << " = "
                   << (i ? "DPP_SHR(" + src + ", " + std::to_string(i) + ")" : src) << ";\n";
             }
+            // the channels' counts start together: full adders over terms that several
+            // channels share (a shifted match word votes on about five channels of a dense
+            // rule set) are formed once; each mixed channel finishes its own count
+            std::vector<std::vector<Gen::Bit>> lists;
             for (int c : both) {
-                o << "if (ANY(PL" << c << " & MI" << c << ")) { // channel " << c << ": "
-                  << pl[c].size() << " + votes, " << mi[c].size() << " - votes\n";
                 std::vector<Gen::Bit> cnt{{"p[" + std::to_string(c) + "]", false}};
                 for (const Vote &v : pl[c]) cnt.push_back({tname(v.r, v.i, v.j), false});
                 for (const Vote &v : mi[c]) cnt.push_back({tname(v.r, v.i, v.j), true});
-                g.at_least(cnt, long(mi[c].size()) + 1);
+                lists.push_back(std::move(cnt));
+            }
+            std::vector<Gen::Levels> started = g.share(lists);
+            for (size_t k = 0; k < both.size(); ++k) {
+                const int c = both[k];
+                o << "if (ANY(PL" << c << " & MI" << c << ")) { // channel " << c << ": "
+                  << pl[c].size() << " + votes, " << mi[c].size() << " - votes\n";
+                g.at_least(started[k], long(mi[c].size()) + 1);
                 o << "N" << c << " = GT;\n}\n";
             }
             o << "}\n";
