@@ -225,8 +225,8 @@ __device__ inline void count_votes(uint32_t (&cnt)[RPL][KB], int &nm, const uint
 // With `moves` (the player plane) the four moves' votes, two entries each (-1 on the player's
 // cell, +1 on the cell it moves to), are read from their match rows at once: the counter starts
 // at old + their four plus votes + (4 - their four minus votes) and only the loaded rules'
-// lists are walked.  (Groups of up to two rules, whose probe rows stay in registers, walk the
-// moves too: the start's registers would spill the step's own.)
+// lists are walked.  (The four-wave kernels of groups of up to two rules, whose probe rows stay
+// in registers, walk the moves too: the start's registers would spill the step's own.)
 template <int RPL>
 __device__ inline void exact_channel(const uint32_t (&old)[RPL], uint64_t fired, bool moves,
                                      const uint32_t *vl, const uint32_t *rsc, const uint32_t *M,
@@ -313,10 +313,13 @@ __device__ inline void exact_channel(const uint32_t (&old)[RPL], uint64_t fired,
 // VGPRs, so nothing spills to scratch (at 128 a cold scratch reload on the path costs a round
 // trip).  Longer launches keep four waves per SIMD and the per-row set-up, whose step loop
 // measured faster (the set-up's code changes the loop's register assignment).
-template <int Hq, int RPL, int NR, int NJ, bool PROG_LDS, bool SHORT>
-__global__ void __launch_bounds__(64, NR <= 8 ? (SHORT ? 2 : 4) : 1) group_step(StepArgs a) {
+// WIDE: a batch of at most two waves per SIMD (program in LDS), which four-wave occupancy
+// would not serve: the kernel may take 256 VGPRs, so nothing spills.
+template <int Hq, int RPL, int NR, int NJ, bool PROG_LDS, bool SHORT, bool WIDE>
+__global__ void __launch_bounds__(64, NR <= 8 ? ((SHORT || WIDE) ? 2 : 4) : 1) group_step(StepArgs a) {
     static_assert(RPL == 1 || Hq == 16, "two rows a lane in 16-lane groups");
     static_assert(!(SHORT && PROG_LDS), "short launches read the program from global memory");
+    static_assert(!(WIDE && (SHORT || !PROG_LDS)), "wide kernels are long launches with the program in LDS");
     constexpr int G = 64 / Hq;
     constexpr int HR = Hq * RPL;              // map rows a group covers
     constexpr int kChunk = 4;                 // entries or votes of a rule read in one round
@@ -810,8 +813,8 @@ __global__ void __launch_bounds__(64, NR <= 8 ? (SHORT ? 2 : 4) : 1) group_step(
                     for (int h = 0; h < RPL; ++h) nw[h] = pnew[h];   // only the moves voted on it
                 } else if (group_any<Hq>(mixed != 0u, lane)) {
                     exact_channel<RPL>(old, fired_all & (uint64_t(RM[2 * c]) | uint64_t(RM[2 * c + 1]) << 32),
-                                       NR > 2 && c == kChPlayer, vote + int(vlw[2 * c]), RS + c * Rt,
-                                       M, MS, PAD, yr, rw, nw);
+                                       (NR > 2 || SHORT || WIDE) && c == kChPlayer, vote + int(vlw[2 * c]),
+                                       RS + c * Rt, M, MS, PAD, yr, rw, nw);
                 }
                 if (c == kChPlayer) pl_any = false;
 #pragma unroll
@@ -1002,22 +1005,37 @@ void compile_group_tables(const GenericProgram &p, int H, int W, int C, int max_
 }
 
 namespace {
-template <int RPL, int NJ, bool PROG_LDS, bool SHORT>
+template <int RPL, int NJ, bool PROG_LDS, bool SHORT, bool WIDE>
 void launch_nr(const StepArgs &a, size_t lds, hipStream_t s) {
     constexpr int G = 4;
     const int nrmax = (a.prog.rules_per_set - kMoveRules + G - 1) / G;
     const dim3 grid(a.B), block(64);
-    if (nrmax <= 2) hipLaunchKernelGGL((group_step<16, RPL, 2, NJ, PROG_LDS, SHORT>), grid, block, lds, s, a);
-    else if (nrmax <= 4) hipLaunchKernelGGL((group_step<16, RPL, 4, NJ, PROG_LDS, SHORT>), grid, block, lds, s, a);
-    else if (nrmax <= 8) hipLaunchKernelGGL((group_step<16, RPL, 8, NJ, PROG_LDS, SHORT>), grid, block, lds, s, a);
-    else if (nrmax <= 12) hipLaunchKernelGGL((group_step<16, RPL, 12, NJ, PROG_LDS, SHORT>), grid, block, lds, s, a);
-    else hipLaunchKernelGGL((group_step<16, RPL, 16, NJ, PROG_LDS, SHORT>), grid, block, lds, s, a);
+    if (nrmax <= 2) hipLaunchKernelGGL((group_step<16, RPL, 2, NJ, PROG_LDS, SHORT, WIDE>), grid, block, lds, s, a);
+    else if (nrmax <= 4) hipLaunchKernelGGL((group_step<16, RPL, 4, NJ, PROG_LDS, SHORT, WIDE>), grid, block, lds, s, a);
+    else if (nrmax <= 8) hipLaunchKernelGGL((group_step<16, RPL, 8, NJ, PROG_LDS, SHORT, WIDE>), grid, block, lds, s, a);
+    else if (nrmax <= 12) hipLaunchKernelGGL((group_step<16, RPL, 12, NJ, PROG_LDS, SHORT, WIDE>), grid, block, lds, s, a);
+    else hipLaunchKernelGGL((group_step<16, RPL, 16, NJ, PROG_LDS, SHORT, WIDE>), grid, block, lds, s, a);
 }
 template <int RPL, int NJ>
-void launch_rpl(const StepArgs &a, size_t lds, bool prog_lds, hipStream_t s) {
-    if (prog_lds) launch_nr<RPL, NJ, true, false>(a, lds, s);
-    else if (a.k < kShortLaunch) launch_nr<RPL, NJ, false, true>(a, lds, s);
-    else launch_nr<RPL, NJ, false, false>(a, lds, s);
+void launch_rpl(const StepArgs &a, size_t lds, bool prog_lds, bool wide, hipStream_t s) {
+    if (prog_lds && wide) launch_nr<RPL, NJ, true, false, true>(a, lds, s);
+    else if (prog_lds) launch_nr<RPL, NJ, true, false, false>(a, lds, s);
+    else if (a.k < kShortLaunch) launch_nr<RPL, NJ, false, true, false>(a, lds, s);
+    else launch_nr<RPL, NJ, false, false, false>(a, lds, s);
+}
+
+// SIMDs of the current device (4 per compute unit), looked up once per device.
+int device_simds() {
+    static int simds[64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 1024;
+    if (!simds[dev]) {
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+            return 1024;
+        simds[dev] = 4 * cus;
+    }
+    return simds[dev];
 }
 }  // namespace
 
@@ -1033,12 +1051,14 @@ hipError_t launch_group_step(const StepArgs &a, hipStream_t s) {
     const bool prog_lds = a.k >= kShortLaunch && base + prog <= budget;
     const size_t lds = base + (prog_lds ? prog : 0);
     const bool narrow = a.max_pat_w <= 3;
+    // at most two waves per SIMD: the 256-VGPR kernels
+    const bool wide = a.B <= 2 * device_simds();
     if (group_rows(a.H) == 16) {
-        if (narrow) launch_rpl<1, 3>(a, lds, prog_lds, s);
-        else launch_rpl<1, 8>(a, lds, prog_lds, s);
+        if (narrow) launch_rpl<1, 3>(a, lds, prog_lds, wide, s);
+        else launch_rpl<1, 8>(a, lds, prog_lds, wide, s);
     } else {
-        if (narrow) launch_rpl<2, 3>(a, lds, prog_lds, s);
-        else launch_rpl<2, 8>(a, lds, prog_lds, s);
+        if (narrow) launch_rpl<2, 3>(a, lds, prog_lds, wide, s);
+        else launch_rpl<2, 8>(a, lds, prog_lds, wide, s);
     }
     return hipGetLastError();
 }
