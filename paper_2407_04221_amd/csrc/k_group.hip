@@ -655,6 +655,13 @@ __global__ void __launch_bounds__(64, NR <= 8 ? ((SHORT || WIDE) ? 2 : 4) : 1) g
                             x[kr][3] = live ? q.w : kPassEntry;
                             continue;
                         }
+                        if (NR > 2 && e == kProbeEntries) {    // entries 4 .. 7: the probe row's
+                            const int r = kr < nr ? kMoveRules + g + G * kr : kMoveRules;
+#pragma unroll
+                            for (int u = 0; u < 4; ++u)
+                                x[kr][u] = live ? PT[r * kProbeWords + 8 + u] : kPassEntry;
+                            continue;
+                        }
 #pragma unroll
                         for (int u = 0; u < 4; ++u) {
                             // past the last entry the last one again (AND is idempotent)
