@@ -110,32 +110,16 @@ __device__ inline bool group_any(bool p, int lane) {
     return ((bal >> base) & ((1ull << Hq) - 1ull)) != 0ull;
 }
 
-// Row y + 1 (next) and y - 1 (prev) of the lane's group, 0 past the group's ends: a DPP row
-// shift within 16-lane groups; for 32-lane groups a DPP shift of the whole wave by one lane,
-// the lane at the group's end taking 0.
-template <int Hq>
-__device__ inline uint32_t next_row(uint32_t v, int lane, int y) {
-    (void)lane;
-    if (Hq == 16) return uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x101, 0xF, 0xF, true));
-    const uint32_t u = uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x130, 0xF, 0xF, true));
-    return y + 1 < Hq ? u : 0u;
-}
-template <int Hq>
-__device__ inline uint32_t prev_row(uint32_t v, int lane, int y) {
-    (void)lane;
-    if (Hq == 16) return uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x111, 0xF, 0xF, true));
-    const uint32_t u = uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x138, 0xF, 0xF, true));
-    return y > 0 ? u : 0u;
-}
-
-// The same for the rows a lane holds, RPL of them (2: on maps of 17 to 32 rows a lane of a
-// 16-lane group holds rows y and y + 16): within each 16-row half a DPP row shift, across the
-// halves a DPP row rotate (lane 15's next row is lane 0's second row, lane 0's second row's
-// previous row is lane 15's first).
+// Rows y + 1 (next) and y - 1 (prev) of the rows a lane holds, 0 past the group's ends, RPL
+// of them (2: on maps of 17 to 32 rows a lane of a 16-lane group holds rows y and y + 16):
+// within each 16-row half a DPP row shift, across the halves a DPP row rotate (lane 15's next
+// row is lane 0's second row, lane 0's second row's previous row is lane 15's first).
 template <int Hq, int RPL>
 __device__ inline void next_rows(const uint32_t (&v)[RPL], uint32_t (&n)[RPL], int lane, int y) {
+    static_assert(Hq == 16, "16-lane groups");
+    (void)lane;
     if constexpr (RPL == 1) {
-        n[0] = next_row<Hq>(v[0], lane, y);
+        n[0] = uint32_t(__builtin_amdgcn_update_dpp(0, int(v[0]), 0x101, 0xF, 0xF, true));
     } else {
         const uint32_t s0 = uint32_t(__builtin_amdgcn_update_dpp(0, int(v[0]), 0x101, 0xF, 0xF, true));
         const uint32_t w1 = uint32_t(__builtin_amdgcn_update_dpp(0, int(v[1]), 0x12F, 0xF, 0xF, true));
@@ -145,8 +129,11 @@ __device__ inline void next_rows(const uint32_t (&v)[RPL], uint32_t (&n)[RPL], i
 }
 template <int Hq, int RPL>
 __device__ inline void prev_rows(const uint32_t (&v)[RPL], uint32_t (&p)[RPL], int lane, int y) {
+    static_assert(Hq == 16, "16-lane groups");
+    (void)lane;
     if constexpr (RPL == 1) {
-        p[0] = prev_row<Hq>(v[0], lane, y);
+        (void)y;
+        p[0] = uint32_t(__builtin_amdgcn_update_dpp(0, int(v[0]), 0x111, 0xF, 0xF, true));
     } else {
         p[0] = uint32_t(__builtin_amdgcn_update_dpp(0, int(v[0]), 0x111, 0xF, 0xF, true));
         const uint32_t t1 = uint32_t(__builtin_amdgcn_update_dpp(0, int(v[1]), 0x111, 0xF, 0xF, true));

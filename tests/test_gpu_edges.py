@@ -37,8 +37,8 @@ CASES = {
     "tall40x20": W_("tall40x20", 56, B=7, H=40, W=20, C=6, R=12, shapes=((3, 3), (2, 1)), T=10),
     "tall_per_env": W_("tall_per_env", 57, B=5, H=48, W=40, C=5, R=8,
                        shapes=((3, 3), (1, 2)), per_env=True, T=10),
-    # 32-lane groups on a map of 24 rows (rows 24..31 of each group empty), patterns up to
-    # 4 x 4 (three pad rows under the planes), per-environment rules
+    # two rows a lane on a map of 24 rows (second rows 24..31 of each group empty), patterns
+    # up to 4 x 4 (three pad rows under the planes), per-environment rules
     "mid24x20": W_("mid24x20", 59, B=11, H=24, W=20, C=7, R=9,
                    shapes=((4, 4), (1, 3), (2, 1)), per_env=True, T=14),
     # patterns wider than 8 columns (the group engine tests a plane row in blocks of 8)
