@@ -26,7 +26,8 @@
 //   PL, MI [C][HR]     per stored channel, the OR of the +1 and of the -1 votes
 //   I0   [C][HR]       the initial rows, for resets
 //   PT   [R+5][12]     probe table: per loaded rule its first eight merged entries, its
-//                      anchor rows and columns and where its entries are (row R + 4: zeros,
+//                      anchor rows and columns, where its entries and its votes are and the
+//                      channels it votes on (row R + 4: zeros,
 //                      read by groups with fewer rules than others)
 //   RS   [C][R+4]      per channel and rule, the range of the rule's votes in the channel's
 //                      vote list (for exact recounts)
@@ -66,7 +67,8 @@ constexpr int kCountBits = 8;           // exact write counters: a channel list 
 constexpr int kHdrWords = int(sizeof(RuleHdr) / 4);
 constexpr int kProbeEntries = 4;        // input entries of every rule tested in one round
 constexpr int kProbeWords = 12;         // probe table row: entries 0-3, anchor word, match
-                                        // offset | count << 16, pad, pad, entries 4-7
+                                        // offset | count << 16, vote offset | count << 16,
+                                        // voted channels, entries 4-7
 // Input entries merged per plane row: o | jb << 12 | care << 16 | want << 24 tests row
 // o + y of the planes (o = c * PR + i: pattern row i of plane c) at the pattern columns
 // 8 jb + j, j < 8, whose bit j of care is set: there the cell must equal bit j of want.
@@ -716,12 +718,25 @@ __global__ void __launch_bounds__(64, NR <= 8 ? ((SHORT || WIDE) ? 2 : 4) : 1) g
                         cells += __popc(m[h]);
                     }
                     fired |= 1ull << r;
-                    voted |= hw[7];
-                    rsum += int(hw[2]) * cells;
+                    // the vote list's place and the voted channels: with the program in global
+                    // memory from the probe row (LDS), a memory round trip less before the votes
+                    int voff, vcnt;
+                    if constexpr (PROG_LDS) {
+                        voted |= hw[7];
+                        rsum += int(hw[2]) * cells;
+                        voff = int(hw[5]);
+                        vcnt = int(hw[6]);
+                    } else {
+                        const uint32_t pvw = PT[r * kProbeWords + 6];
+                        voted |= PT[r * kProbeWords + 7];
+                        rsum += int(hw[2]) * cells;
+                        voff = int(pvw & 0xFFFFu);
+                        vcnt = int(pvw >> 16);
+                    }
                     // votes kChunk at a time, the next chunk read with the current one's match
                     // rows (a repeated last vote ORs the same bits again)
-                    const uint32_t *ve = vent + int(hw[5]);
-                    const int vcnt = int(hw[6]), vlast = vcnt - 1;
+                    const uint32_t *ve = vent + voff;
+                    const int vlast = vcnt - 1;
                     uint32_t v[kChunk];
                     if (vcnt > 0) {
 #pragma unroll
@@ -972,6 +987,10 @@ void compile_group_tables(const GenericProgram &p, int H, int W, int C, int max_
             const int cols = W - h.m + 1, rows = H - h.n + 1;
             row[4] = (cols >= 1 && rows >= 1) ? uint32_t(32 - cols) | (uint32_t(rows) << 8) : 0u;
             row[5] = uint32_t(off) | (uint32_t(cnt) << 16);
+            // the rule-major votes (a set holds at most 64 rules of at most 254 votes, so the
+            // offset and count fit 16 bits each) and the channels they are on
+            row[6] = uint32_t(h.vote_off) | (uint32_t(h.vote_cnt) << 16);
+            row[7] = uint32_t(h.pad);
             // entries 4 .. 7 (past the last, the last again; none: the pass entry)
             for (int e = 0; e < 4; ++e)
                 row[8 + e] = cnt > kProbeEntries ? ent[std::min(kProbeEntries + e, cnt - 1)]
